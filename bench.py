@@ -1,0 +1,269 @@
+#!/usr/bin/env python3
+"""Benchmark of the MoE gate / layout-transform hot path on one MI355X.
+
+A step is one pass of the whole path over one batch: gate (projection,
+softmax, selection, capacity slots) -> dispatch -> combine (identity experts:
+ye = xe) -> combine backward -> dispatch backward (identity expert backward:
+dxe = dye).  Inputs are synthetic, seeded, and resident in HBM before timing.
+
+Prints ONE JSON line (metric, value = tokens/s, roofline of the dominant
+kernel, CPU-oracle baseline).  Default workload: the hash-gate workload
+(S=65536 tokens, d=4096, E=128, bf16), the largest of the five.
+"""
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E peak, GB/s
+METRIC = "tokens/s through gate+dispatch+combine; achieved HBM GB/s vs MI355X peak"
+OPS = ("gate", "dispatch", "combine", "combine_bwd", "dispatch_bwd")
+KERNEL_OF_OP = {"dispatch": "dispatch_kernel", "combine": "combine_kernel", "combine_bwd": "combine_bwd_kernel",
+                "dispatch_bwd": "combine_kernel", "gate": "route_kernel"}
+SOURCE_OF_OP = {"dispatch": "layout.hip", "combine": "layout.hip", "combine_bwd": "layout.hip",
+                "dispatch_bwd": "layout.hip", "gate": "gate.hip"}
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", type=int, default=5, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="before the timed region, run one device copy of this many MiB (counter calibration)")
+    return ap.parse_args()
+
+
+def alg_bytes(w, S, d, E, k, C, elt, n_kept, tok_kept, dw):
+    """Bytes each op must move at minimum: every input read once, every output
+    written once (zero rows of the expert buffers included)."""
+    row = d * elt
+    if w["kind"] == 2:
+        gate_in = S * 4
+    else:
+        gate_in = S * row + d * E * elt + (E * 4 if w.get("hot_experts") else 0)
+    b = {
+        "gate": gate_in + S * k * 12 + E * C * 4 + 2 * E * 4,
+        "dispatch": tok_kept * row + E * C * row + E * C * 4,
+        "combine": n_kept * row + S * row + S * k * 12,
+        "dispatch_bwd": n_kept * row + S * row + S * k * 8,
+        "combine_bwd": tok_kept * row + E * C * row + E * C * 4 + S * k * 4
+                       + ((n_kept * row + S * k * 8) if dw else 0),
+    }
+    return b
+
+
+def source_sha(name):
+    with open(os.path.join(ROOT, "paper_2203_14685_amd", "csrc", name), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def measured_traffic(workload_name, kernel, sha):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, or None
+    when there is none for this kernel and workload or the kernel source changed."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload_name}.txt")
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    with open(path) as f:
+        for ln in f:
+            if ":" in ln and not ln.startswith("#"):
+                key, _, v = ln.partition(":")
+                vals[key.strip()] = v.strip()
+    if vals.get("source_sha") != sha:
+        return None
+    try:
+        return float(vals["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(w, target_s=12.0):
+    """The oracle, untuned, on a bounded sample of the same workload (its first
+    S_s tokens, capacity scaled the same way), timed on this host."""
+    import math
+
+    import oracle
+    from paper_2203_14685_amd import workloads as wl
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    except Exception:  # threadpoolctl missing: report the host's count
+        blas_threads = os.cpu_count() or 1
+    k, E, d, dt = w["k"], w["E"], w["d"], w["dtype"]
+
+    def run(S_s):
+        C_s = int(math.ceil(w["cf"] * k * S_s / E))
+        inp = wl.make_inputs(w, S=S_s, seed=0)
+        dy = wl.make_rows((S_s, d), dt, 2)
+        t0 = time.perf_counter()
+        g = oracle.gate(w["kind"], k, E, C_s, normalize=w["normalize"], dtype=dt, x=inp["x"], wg=inp["wg"],
+                        bias=inp["bias"], token_ids=inp["token_ids"], hash_seed=0)
+        xe = oracle.dispatch(inp["x"], g["slot_src"], k)
+        oracle.combine(xe, g["ids"], g["slots"], g["weights"], dt)
+        dye, _, _, _ = oracle.combine_bwd(dy, xe, g["slot_src"], g["weights"], k, dt, want_dw=w["kind"] != 2)
+        oracle.dispatch_bwd(dye, g["ids"], g["slots"], dt)
+        return time.perf_counter() - t0
+
+    S_s = 512
+    t = run(S_s)
+    while t < target_s / 2 and S_s * 2 <= w["S"]:
+        S_s *= 2
+        t = run(S_s)
+    cores = blas_threads if w["kind"] != 2 else 1
+    return {"value": round(S_s / t, 1), "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"first {S_s} of {w['S']} tokens of the same workload (capacity scaled alike), "
+                      f"full pass gate+dispatch+combine+combine_bwd+dispatch_bwd in {t:.2f} s, fp64 numpy"}
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+                          "n_gpus": args.gpus}), flush=True)
+        sys.exit(2)
+
+    import torch
+    import paper_2203_14685_amd as hm
+    from paper_2203_14685_amd import workloads as wl
+
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no GPU visible"}), flush=True)
+        sys.exit(3)
+    hm.load()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = wl.WORKLOADS[args.workload]
+    S, d, E, k, C, dt = w["S"], w["d"], w["E"], w["k"], w["C"], w["dtype"]
+    elt = 2 if dt == "bf16" else 4
+    tdt = torch.bfloat16 if dt == "bf16" else torch.float32
+    dcode = hm.MOE_BF16 if dt == "bf16" else hm.MOE_F32
+    learned = w["kind"] != 2
+    want_dw = learned
+
+    inp = wl.make_inputs(w, seed=0)
+    x = wl.to_device(inp["x"], dt)
+    wg = wl.to_device(inp["wg"], dt)
+    bias = wl.to_device(inp["bias"], "f32")
+    tok = wl.to_device(inp["token_ids"], "i32")
+    dy = wl.to_device(wl.make_rows((S, d), dt, 2), dt)
+
+    params = hm.gate_params(S, d if learned else 0, E, k, C, w["kind"], w["normalize"], 0, dcode, 0)
+    i32, f32 = torch.int32, torch.float32
+    ids = torch.empty((S, k), dtype=i32, device=dev)
+    slots = torch.empty((S, k), dtype=i32, device=dev)
+    weights = torch.empty((S, k), dtype=f32, device=dev)
+    counts = torch.empty((E,), dtype=i32, device=dev)
+    demand = torch.empty((E,), dtype=i32, device=dev)
+    slot_src = torch.empty((E, C), dtype=i32, device=dev)
+    ws = torch.empty((hm.moe_gate_workspace_size(params),), dtype=torch.uint8, device=dev)
+    xe = torch.empty((E, C, d), dtype=tdt, device=dev)
+    y = torch.empty((S, d), dtype=tdt, device=dev)
+    dye = torch.empty((E, C, d), dtype=tdt, device=dev)
+    dw = torch.empty((S, k), dtype=f32, device=dev) if want_dw else None
+    dx = torch.empty((S, d), dtype=tdt, device=dev)
+    lay = hm.Layout(S, d, E, k, C, dcode)
+    stream = torch.cuda.current_stream()
+
+    def step(evs=None):
+        def mark(i):
+            if evs is not None:
+                evs[i].record(stream)
+        mark(0)
+        hm.moe_gate(params, x if learned else None, wg, bias, tok if not learned else None, None, ids, slots,
+                    weights, counts, demand, slot_src, ws, stream)
+        mark(1)
+        hm.moe_dispatch(lay, x, slot_src, xe, stream)
+        mark(2)
+        hm.moe_combine(lay, xe, ids, slots, weights, y, stream)
+        mark(3)
+        hm.moe_combine_bwd(lay, dy, xe if want_dw else None, slots if want_dw else None, slot_src, weights,
+                           dye, dw, stream)
+        mark(4)
+        hm.moe_dispatch_bwd(lay, dye, ids, slots, dx, stream)
+        mark(5)
+
+    if args.calib_copy_mib:
+        n = args.calib_copy_mib * (1 << 20) // 4
+        a = torch.ones(n, dtype=torch.float32, device=dev)
+        bcp = torch.empty_like(a)
+        torch.cuda.synchronize()
+        bcp.copy_(a)
+        torch.cuda.synchronize()
+        del a, bcp
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    print(f"[bench] workload {args.workload} {w['name']}: warmup done", file=sys.stderr, flush=True)
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(OPS) + 1)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_step = (t1 - t0) * 1e3 / args.steps
+    op_ms = {op: sum(e[j].elapsed_time(e[j + 1]) for e in evs) / args.steps for j, op in enumerate(OPS)}
+
+    # routing statistics of this batch (outside the timed region)
+    sl = slots.cpu().numpy()
+    n_kept = int((sl >= 0).sum())
+    tok_kept = int((sl >= 0).any(axis=1).sum())
+    ab = alg_bytes(w, S, d, E, k, C, elt, n_kept, tok_kept, want_dw)
+    step_bytes = sum(ab.values())
+    dom = max(("dispatch", "combine", "combine_bwd", "dispatch_bwd", "gate"), key=lambda o: op_ms[o])
+    achieved = ab[dom] / (op_ms[dom] * 1e-3) / 1e9
+    kern = KERNEL_OF_OP[dom]
+    traffic = measured_traffic(w["name"], dom, source_sha(SOURCE_OF_OP[dom]))
+
+    out = {
+        "metric": METRIC,
+        "value": round(S / (ms_step * 1e-3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if dt == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {"workload": w["name"], "S": S, "d": d, "E": E, "k": k, "capacity": C,
+                   "gate": ["topk", "ktop1", "hash"][w["kind"]], "passes": "fwd+bwd",
+                   "parallelism": "single-gpu"},
+        "roofline": {"bound": "hbm", "kernel": kern, "op": dom, "achieved": round(achieved, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": traffic, "alg_bytes_per_launch": ab[dom],
+                     "avg_launch_ms": round(op_ms[dom], 5)},
+        "step_hbm": {"alg_bytes": step_bytes, "GB/s": round(step_bytes / (ms_step * 1e-3) / 1e9, 1),
+                     "frac": round(step_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
+        "ops": {op: {"ms": round(op_ms[op], 5), "alg_bytes": ab[op],
+                     "GB/s": round(ab[op] / (op_ms[op] * 1e-3) / 1e9, 1)} for op in OPS},
+        "routing": {"kept_assignments": n_kept, "tokens_with_kept": tok_kept, "assignments": S * k},
+    }
+    fwd_ms = op_ms["gate"] + op_ms["dispatch"] + op_ms["combine"]
+    out["fwd"] = {"ms": round(fwd_ms, 5), "tokens/s": round(S / (fwd_ms * 1e-3), 1),
+                  "frac": round((ab["gate"] + ab["dispatch"] + ab["combine"]) / (fwd_ms * 1e-3) / 1e9
+                                / HBM_PEAK_GBS, 4)}
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(w)
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,197 @@
+/*
+ * hetumoe.h -- C ABI of the single-GPU MoE gate / layout-transform hot path
+ * (HetuMoE, arXiv 2203.14685), built for AMD Instinct MI355X (gfx950).
+ *
+ * The calls follow Algorithm 1 ("General MoE Training Process") of the paper:
+ *   step 1  W, id = Gate(x)                      -> moe_gate
+ *   step 2  x' = Layout_Transform(x, id)         -> moe_dispatch
+ *   step 6  y = Reverse_Layout_Transform(y', id) -> moe_combine (gate-weighted)
+ * plus the gradients of steps 2 and 6            -> moe_dispatch_bwd, moe_combine_bwd.
+ * Steps 3-5 (AllToAll and the expert networks) are outside this library.
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * Memory     Every buffer argument is DEVICE memory owned by the caller.  Only
+ *            the parameter structs are host memory, read during the call.  The
+ *            library allocates nothing and keeps no state between calls; it is
+ *            reentrant.
+ * Layout     Row-major, densely packed.  x, y, dy, dx: [S, d].  Expert buffers
+ *            xe, ye, dxe, dye: [E, C, d].  Per-choice arrays ids, slots,
+ *            weights, dw: [S, k].  logits: [S, E] fp32.  slot_src: [E, C].
+ * Dtype      One dtype (fp32 or bf16) for x, Wg and every [S,d] / [E,C,d]
+ *            buffer; logits, weights and dw are always fp32; indices int32.
+ *            bf16 outputs are rounded once, to nearest-even, from fp32
+ *            accumulators.
+ * Alignment  [S,d] and [E,C,d] buffers must be 16-byte aligned and rows must be
+ *            a multiple of 16 bytes (d * sizeof(elt) % 16 == 0); otherwise the
+ *            call returns MOE_ERR_UNSUPPORTED.  Other buffers need their natural
+ *            (4-byte) alignment.
+ * Async      Each call enqueues its kernels on `stream` (NULL = the default
+ *            stream) and returns without waiting.  Nothing is read back to the
+ *            host.  Outputs must not alias inputs.
+ * Outputs    Every output element is overwritten: empty expert slots become zero
+ *            rows, unused slot_src entries -1, dropped dw entries 0.
+ * Errors     All argument checks run before the first HIP call; a failed check
+ *            enqueues nothing.  HIP failures return MOE_ERR_HIP.  A thread-local
+ *            message describing the last failure is available from
+ *            moe_last_error().  No C++ exception crosses this boundary.
+ * Determinism  Results are bitwise reproducible for identical inputs; no
+ *            floating-point atomics are used.
+ * Range      0 <= S, S*k < 2^31;  1 <= E <= 1024;  0 <= C, E*C < 2^31;  d >= 1.
+ *            TOPK: 1 <= k <= min(E, 8).  KTOP1: 1 <= k <= 8 and E % k == 0.
+ *            HASH: k == 1.
+ */
+#ifndef HETUMOE_H
+#define HETUMOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MOE_ABI_VERSION 1
+
+/* Symbols of the C ABI are the only ones the shared library exports. */
+#define MOE_API __attribute__((visibility("default")))
+
+typedef enum {
+  MOE_OK = 0,
+  MOE_ERR_INVALID_ARG = 1, /* a size, pointer or option is out of the contract */
+  MOE_ERR_UNSUPPORTED = 2, /* valid request this build does not handle (alignment, row size) */
+  MOE_ERR_WORKSPACE = 3,   /* workspace NULL or smaller than moe_gate_workspace_size() */
+  MOE_ERR_HIP = 4          /* a HIP runtime call failed; see moe_last_error() */
+} moe_status;
+
+typedef enum { MOE_F32 = 0, MOE_BF16 = 1 } moe_dtype;
+
+/* Gating strategies of Sec. 3.1 that share the capacity / layout machinery. */
+typedef enum {
+  MOE_GATE_TOPK = 0,  /* Top-k of Eq. 1 (Switch: k=1, GShard: k=2) */
+  MOE_GATE_KTOP1 = 1, /* kTop1 / expert prototyping: k contiguous groups of E/k experts, top-1 in each */
+  MOE_GATE_HASH = 2   /* Hash Layer, random hash of the token id; k=1, weight 1 */
+} moe_gate_kind;
+
+/* Parameters of moe_gate (host memory). */
+typedef struct {
+  int32_t S;          /* tokens */
+  int32_t d;          /* model width (row length of x) */
+  int32_t E;          /* experts */
+  int32_t k;          /* choices per token: experts (TOPK), groups (KTOP1), 1 (HASH) */
+  int32_t capacity;   /* C: slots per expert; assignments beyond it are dropped */
+  int32_t kind;       /* moe_gate_kind */
+  int32_t normalize;  /* TOPK only: 1 = softmax over the k chosen logits (Eq. 1);
+                         0 = full softmax over all E, read at each chosen expert (Switch) */
+  int32_t logits_in;  /* TOPK/KTOP1: 1 = `logits` is an input (final, bias included), the
+                         projection is skipped and x, wg, bias must be NULL;
+                         0 = logits are computed from x and wg (+ bias) */
+  int32_t dtype;      /* moe_dtype of x and wg */
+  int32_t reserved;   /* must be 0 */
+  uint64_t hash_seed; /* HASH only: seed of the SplitMix64 hash */
+} moe_gate_params;
+
+/* Shape of a dispatch / combine call (host memory). */
+typedef struct {
+  int32_t S, d, E, k, capacity;
+  int32_t dtype; /* moe_dtype of every [S,d] and [E,C,d] buffer */
+} moe_layout;
+
+/* Bytes of device workspace moe_gate needs for `p` (0 is possible).  Fails with
+ * MOE_ERR_INVALID_ARG for parameters moe_gate would reject. */
+MOE_API moe_status moe_gate_workspace_size(const moe_gate_params* p, size_t* bytes);
+
+/*
+ * moe_gate -- step 1 of Algorithm 1: the gate network, plus the capacity rule
+ * of Sec. 3.1 (capacity factor caps the tokens each expert receives).
+ *
+ * Computes, per token s:
+ *   logits  L[s,e] = sum_j x[s,j] * wg[j,e] + bias[e]     (x . W of Eq. 1; fp32 accumulation)
+ *   ids     TOPK : the k experts with the largest logits, best first;
+ *           KTOP1: the best expert of each group g, [g*E/k, (g+1)*E/k);
+ *           HASH : SplitMix64(hash_seed) output number token_ids[s]+1, mod E.
+ *           Ties go to the lower expert index.
+ *   weights TOPK normalize=1: softmax over the k chosen logits (Eq. 1);
+ *           TOPK normalize=0: softmax over all E logits at the chosen expert;
+ *           KTOP1: softmax over the chosen expert's group; HASH: 1.
+ * then assigns capacity slots in rank-major, token order: all first choices in
+ * token order, then all second choices, and so on.  An expert's n-th
+ * assignment (counting from 0) gets slot n if n < C, otherwise it is dropped.
+ *
+ * Inputs   x [S,d] and wg [d,E] (dtype), bias [E] fp32 or NULL: required when
+ *          kind != HASH and logits_in == 0, else NULL.
+ *          token_ids [S] int32 >= 0: required for HASH, else NULL.
+ *          logits [S,E] fp32: input when logits_in == 1.
+ * Outputs  logits [S,E] fp32 (optional, NULL to skip; when logits_in == 0 the
+ *          exact values the selection used), ids [S,k], weights [S,k] fp32,
+ *          slots [S,k] (slot in the expert buffer, -1 = dropped), counts [E]
+ *          (kept per expert, <= C), demand [E] (routed before the cap; NULL to
+ *          skip), slot_src [E,C] (s*k + r of the assignment in each slot, -1 if
+ *          empty).  Dropped assignments still report their id and weight.
+ * Workspace device memory of at least moe_gate_workspace_size() bytes, 16-byte
+ *          aligned; contents on entry are ignored.
+ */
+MOE_API moe_status moe_gate(const moe_gate_params* p, const void* x, const void* wg,
+                    const float* bias, const int32_t* token_ids, float* logits,
+                    int32_t* ids, int32_t* slots, float* weights, int32_t* counts,
+                    int32_t* demand, int32_t* slot_src, void* workspace,
+                    size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * moe_dispatch -- step 2 of Algorithm 1 (Layout_Transform; Sec. 3.2, layout
+ * transform): tokens routed to one expert become one contiguous buffer.
+ *   xe[e,c,:] = x[slot_src[e,c] / k, :]   if slot_src[e,c] >= 0   (bit copy)
+ *   xe[e,c,:] = 0                          otherwise
+ * x [S,d], slot_src [E,C] as written by moe_gate, xe [E,C,d] output.
+ */
+MOE_API moe_status moe_dispatch(const moe_layout* l, const void* x, const int32_t* slot_src,
+                        void* xe, hipStream_t stream);
+
+/*
+ * moe_combine -- step 6 of Algorithm 1 (Reverse_Layout_Transform) with the gate
+ * weighting of step 4 / the second line of Eq. 1 applied here:
+ *   y[s,:] = sum over r with slots[s,r] >= 0 of weights[s,r] * ye[ids[s,r], slots[s,r], :]
+ * accumulated in fp32 in r order and rounded once; a token with no kept choice
+ * gets a zero row.  ye [E,C,d], ids/slots/weights [S,k], y [S,d] output.
+ */
+MOE_API moe_status moe_combine(const moe_layout* l, const void* ye, const int32_t* ids,
+                       const int32_t* slots, const float* weights, void* y,
+                       hipStream_t stream);
+
+/*
+ * moe_dispatch_bwd -- gradient of moe_dispatch (adjoint of step 2):
+ *   dx[s,:] = sum over r with slots[s,r] >= 0 of dxe[ids[s,r], slots[s,r], :]
+ * accumulated in fp32 and rounded once.  dxe [E,C,d], dx [S,d] output.
+ */
+MOE_API moe_status moe_dispatch_bwd(const moe_layout* l, const void* dxe, const int32_t* ids,
+                            const int32_t* slots, void* dx, hipStream_t stream);
+
+/*
+ * moe_combine_bwd -- gradient of moe_combine (adjoint of step 6):
+ *   dye[e,c,:] = weights[s,r] * dy[s,:]   for (s,r) with s*k+r = slot_src[e,c] >= 0
+ *   dye[e,c,:] = 0                         for empty slots
+ *   dw[s,r]    = sum_j dy[s,j] * ye[e,c,j] for the slot (e,c) holding (s,r)
+ *   dw[s,r]    = 0                          for dropped choices (slots[s,r] == -1)
+ * dy [S,d], ye [E,C,d] (NULL iff dw is NULL), slots [S,k] (NULL iff dw is NULL),
+ * slot_src [E,C], weights [S,k]; outputs dye [E,C,d] and dw [S,k] fp32 or NULL.
+ */
+MOE_API moe_status moe_combine_bwd(const moe_layout* l, const void* dy, const void* ye,
+                           const int32_t* slots, const int32_t* slot_src,
+                           const float* weights, void* dye, float* dw,
+                           hipStream_t stream);
+
+/* Static description of a status code. */
+MOE_API const char* moe_status_string(moe_status s);
+
+/* Message for the last failed call on this host thread ("" if none). */
+MOE_API const char* moe_last_error(void);
+
+/* MOE_ABI_VERSION of the built library. */
+MOE_API int32_t moe_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HETUMOE_H */

@@ -1,0 +1,244 @@
+"""ctypes binding of libhetumoe.so (argument marshalling only).
+
+The functions named like the C ABI (moe_gate, moe_dispatch, ...) take torch
+tensors that already live on the GPU, check dtype / device / contiguity, and
+forward raw device pointers plus torch's current HIP stream.  The convenience
+wrappers (gate, dispatch, ...) additionally allocate the outputs with
+torch.empty; every value is computed by the library's HIP kernels.  There is no
+fallback: if the library is missing or fails to load, every call raises.
+"""
+
+import ctypes
+import os
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libhetumoe.so")
+
+MOE_OK, MOE_ERR_INVALID_ARG, MOE_ERR_UNSUPPORTED, MOE_ERR_WORKSPACE, MOE_ERR_HIP = range(5)
+MOE_F32, MOE_BF16 = 0, 1
+MOE_GATE_TOPK, MOE_GATE_KTOP1, MOE_GATE_HASH = 0, 1, 2
+
+EXPORTED = (
+    "moe_gate_workspace_size", "moe_gate", "moe_dispatch", "moe_combine",
+    "moe_dispatch_bwd", "moe_combine_bwd", "moe_status_string", "moe_last_error",
+    "moe_abi_version",
+)
+
+
+class MoeError(RuntimeError):
+    def __init__(self, status, message):
+        super().__init__(f"{message} [status {status}]")
+        self.status = status
+
+
+class GateParams(ctypes.Structure):
+    _fields_ = [
+        ("S", ctypes.c_int32), ("d", ctypes.c_int32), ("E", ctypes.c_int32),
+        ("k", ctypes.c_int32), ("capacity", ctypes.c_int32), ("kind", ctypes.c_int32),
+        ("normalize", ctypes.c_int32), ("logits_in", ctypes.c_int32),
+        ("dtype", ctypes.c_int32), ("reserved", ctypes.c_int32),
+        ("hash_seed", ctypes.c_uint64),
+    ]
+
+
+class Layout(ctypes.Structure):
+    _fields_ = [
+        ("S", ctypes.c_int32), ("d", ctypes.c_int32), ("E", ctypes.c_int32),
+        ("k", ctypes.c_int32), ("capacity", ctypes.c_int32), ("dtype", ctypes.c_int32),
+    ]
+
+
+_lib = None
+
+
+def load():
+    """Load the in-tree libhetumoe.so (raises if it is missing)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2203_14685_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, i32p, f32p = ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p
+    lib.moe_gate_workspace_size.argtypes = [ctypes.POINTER(GateParams), ctypes.POINTER(ctypes.c_size_t)]
+    lib.moe_gate.argtypes = [ctypes.POINTER(GateParams), vp, vp, f32p, i32p, f32p, i32p, i32p, f32p,
+                             i32p, i32p, i32p, vp, ctypes.c_size_t, vp]
+    lib.moe_dispatch.argtypes = [ctypes.POINTER(Layout), vp, i32p, vp, vp]
+    lib.moe_combine.argtypes = [ctypes.POINTER(Layout), vp, i32p, i32p, f32p, vp, vp]
+    lib.moe_dispatch_bwd.argtypes = [ctypes.POINTER(Layout), vp, i32p, i32p, vp, vp]
+    lib.moe_combine_bwd.argtypes = [ctypes.POINTER(Layout), vp, vp, i32p, i32p, f32p, vp, f32p, vp]
+    for name in ("moe_gate_workspace_size", "moe_gate", "moe_dispatch", "moe_combine",
+                 "moe_dispatch_bwd", "moe_combine_bwd"):
+        getattr(lib, name).restype = ctypes.c_int
+    lib.moe_status_string.argtypes = [ctypes.c_int]
+    lib.moe_status_string.restype = ctypes.c_char_p
+    lib.moe_last_error.argtypes = []
+    lib.moe_last_error.restype = ctypes.c_char_p
+    lib.moe_abi_version.argtypes = []
+    lib.moe_abi_version.restype = ctypes.c_int32
+    _lib = lib
+    return lib
+
+
+def _check(status):
+    if status != MOE_OK:
+        lib = load()
+        raise MoeError(status, f"{lib.moe_status_string(status).decode()}: {lib.moe_last_error().decode()}")
+
+
+def _dtype_code(t):
+    if t.dtype == torch.float32:
+        return MOE_F32
+    if t.dtype == torch.bfloat16:
+        return MOE_BF16
+    raise TypeError(f"unsupported dtype {t.dtype}; float32 or bfloat16 expected")
+
+
+def _ptr(t, dtype=None, name="tensor"):
+    """Device pointer of a contiguous GPU tensor (None -> NULL)."""
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor or None")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be on the GPU, found {t.device}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, found {t.dtype}")
+    return t.data_ptr() if t.numel() > 0 else None
+
+
+def _stream(stream):
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    return getattr(stream, "cuda_stream", stream)
+
+
+def gate_params(S, d, E, k, capacity, kind, normalize=0, logits_in=0, dtype=MOE_F32, hash_seed=0):
+    return GateParams(S, d, E, k, capacity, kind, normalize, logits_in, dtype, 0, hash_seed)
+
+
+def moe_gate_workspace_size(params):
+    n = ctypes.c_size_t(0)
+    _check(load().moe_gate_workspace_size(ctypes.byref(params), ctypes.byref(n)))
+    return n.value
+
+
+def moe_gate(params, x, wg, bias, token_ids, logits, ids, slots, weights, counts, demand, slot_src,
+             workspace, stream=None):
+    lib = load()
+    f32, i32 = torch.float32, torch.int32
+    xdt = torch.bfloat16 if params.dtype == MOE_BF16 else torch.float32
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib.moe_gate(
+        ctypes.byref(params), _ptr(x, xdt, "x"), _ptr(wg, xdt, "wg"), _ptr(bias, f32, "bias"),
+        _ptr(token_ids, i32, "token_ids"), _ptr(logits, f32, "logits"), _ptr(ids, i32, "ids"),
+        _ptr(slots, i32, "slots"), _ptr(weights, f32, "weights"), _ptr(counts, i32, "counts"),
+        _ptr(demand, i32, "demand"), _ptr(slot_src, i32, "slot_src"), _ptr(workspace, None, "workspace"),
+        ws_bytes, _stream(stream)))
+
+
+def _layout(S, d, E, k, capacity, dtype):
+    return Layout(S, d, E, k, capacity, dtype)
+
+
+def moe_dispatch(layout, x, slot_src, xe, stream=None):
+    dt = torch.bfloat16 if layout.dtype == MOE_BF16 else torch.float32
+    _check(load().moe_dispatch(ctypes.byref(layout), _ptr(x, dt, "x"), _ptr(slot_src, torch.int32, "slot_src"),
+                               _ptr(xe, dt, "xe"), _stream(stream)))
+
+
+def moe_combine(layout, ye, ids, slots, weights, y, stream=None):
+    dt = torch.bfloat16 if layout.dtype == MOE_BF16 else torch.float32
+    _check(load().moe_combine(ctypes.byref(layout), _ptr(ye, dt, "ye"), _ptr(ids, torch.int32, "ids"),
+                              _ptr(slots, torch.int32, "slots"), _ptr(weights, torch.float32, "weights"),
+                              _ptr(y, dt, "y"), _stream(stream)))
+
+
+def moe_dispatch_bwd(layout, dxe, ids, slots, dx, stream=None):
+    dt = torch.bfloat16 if layout.dtype == MOE_BF16 else torch.float32
+    _check(load().moe_dispatch_bwd(ctypes.byref(layout), _ptr(dxe, dt, "dxe"), _ptr(ids, torch.int32, "ids"),
+                                   _ptr(slots, torch.int32, "slots"), _ptr(dx, dt, "dx"), _stream(stream)))
+
+
+def moe_combine_bwd(layout, dy, ye, slots, slot_src, weights, dye, dw, stream=None):
+    dt = torch.bfloat16 if layout.dtype == MOE_BF16 else torch.float32
+    _check(load().moe_combine_bwd(ctypes.byref(layout), _ptr(dy, dt, "dy"), _ptr(ye, dt, "ye"),
+                                  _ptr(slots, torch.int32, "slots"), _ptr(slot_src, torch.int32, "slot_src"),
+                                  _ptr(weights, torch.float32, "weights"), _ptr(dye, dt, "dye"),
+                                  _ptr(dw, torch.float32, "dw"), _stream(stream)))
+
+
+# ---------------------------------------------------------------- convenience wrappers
+
+def gate(kind, k, E, capacity, *, x=None, wg=None, bias=None, token_ids=None, logits=None,
+         logits_in=False, normalize=0, hash_seed=0, want_logits=False, want_demand=True, dtype=None,
+         stream=None):
+    """Allocate the outputs and run moe_gate; returns a dict of device tensors."""
+    if kind == MOE_GATE_HASH:
+        S, d = int(token_ids.shape[0]), 0
+        dcode = MOE_F32 if dtype is None else dtype
+    elif logits_in:
+        S, d = int(logits.shape[0]), 0
+        dcode = MOE_F32 if dtype is None else dtype
+    else:
+        S, d = int(x.shape[0]), int(x.shape[1])
+        dcode = _dtype_code(x)
+    ref = logits if logits is not None else (x if x is not None else token_ids)
+    dev = ref.device
+    params = gate_params(S, d, E, k, capacity, kind, normalize, int(bool(logits_in)), dcode, hash_seed)
+    out = {
+        "ids": torch.empty((S, k), dtype=torch.int32, device=dev),
+        "slots": torch.empty((S, k), dtype=torch.int32, device=dev),
+        "weights": torch.empty((S, k), dtype=torch.float32, device=dev),
+        "counts": torch.empty((E,), dtype=torch.int32, device=dev),
+        "demand": torch.empty((E,), dtype=torch.int32, device=dev) if want_demand else None,
+        "slot_src": torch.empty((E, capacity), dtype=torch.int32, device=dev),
+    }
+    if not logits_in and want_logits:
+        logits = torch.empty((S, E), dtype=torch.float32, device=dev)
+    elif not logits_in:
+        logits = None
+    out["logits"] = logits
+    ws = torch.empty((moe_gate_workspace_size(params),), dtype=torch.uint8, device=dev)
+    moe_gate(params, x, wg, bias, token_ids, logits, out["ids"], out["slots"], out["weights"],
+             out["counts"], out["demand"], out["slot_src"], ws, stream)
+    return out
+
+
+def dispatch(x, slot_src, k, stream=None):
+    S, d = x.shape
+    E, C = slot_src.shape
+    xe = torch.empty((E, C, d), dtype=x.dtype, device=x.device)
+    moe_dispatch(_layout(S, d, E, k, C, _dtype_code(x)), x, slot_src, xe, stream)
+    return xe
+
+
+def combine(ye, ids, slots, weights, stream=None):
+    E, C, d = ye.shape
+    S, k = ids.shape
+    y = torch.empty((S, d), dtype=ye.dtype, device=ye.device)
+    moe_combine(_layout(S, d, E, k, C, _dtype_code(ye)), ye, ids, slots, weights, y, stream)
+    return y
+
+
+def dispatch_bwd(dxe, ids, slots, stream=None):
+    E, C, d = dxe.shape
+    S, k = ids.shape
+    dx = torch.empty((S, d), dtype=dxe.dtype, device=dxe.device)
+    moe_dispatch_bwd(_layout(S, d, E, k, C, _dtype_code(dxe)), dxe, ids, slots, dx, stream)
+    return dx
+
+
+def combine_bwd(dy, slot_src, weights, ye=None, slots=None, want_dw=True, stream=None):
+    S, d = dy.shape
+    E, C = slot_src.shape
+    k = weights.shape[1]
+    dye = torch.empty((E, C, d), dtype=dy.dtype, device=dy.device)
+    dw = torch.empty((S, k), dtype=torch.float32, device=dy.device) if want_dw else None
+    moe_combine_bwd(_layout(S, d, E, k, C, _dtype_code(dy)), dy, ye if want_dw else None,
+                    slots if want_dw else None, slot_src, weights, dye, dw, stream)
+    return dye, dw

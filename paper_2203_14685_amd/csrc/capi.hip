@@ -1,0 +1,269 @@
+// C ABI of the library: argument validation (before any HIP call), workspace
+// sizing and kernel launches.  See include/hetumoe.h for the contract.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "hetumoe.h"
+#include "common.hpp"
+#include "kernels.hpp"
+
+using namespace hetumoe;
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+moe_status fail(moe_status st, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+moe_status ok() {
+  g_last_error[0] = '\0';
+  return MOE_OK;
+}
+
+moe_status hip_fail(hipError_t err, const char* what) {
+  return fail(MOE_ERR_HIP, "%s: %s (%d)", what, hipGetErrorString(err), static_cast<int>(err));
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+size_t elt_size(int32_t dtype) { return dtype == MOE_BF16 ? 2 : 4; }
+
+constexpr int64_t kI32Max = 2147483647;
+
+int64_t hist_blocks(int64_t S) { return (S + kTokensPerHistBlock - 1) / kTokensPerHistBlock; }
+
+// Checks shared by moe_gate and moe_gate_workspace_size.
+moe_status check_gate_params(const moe_gate_params* p) {
+  if (!p) return fail(MOE_ERR_INVALID_ARG, "params is NULL");
+  if (p->reserved != 0) return fail(MOE_ERR_INVALID_ARG, "reserved must be 0");
+  if (p->dtype != MOE_F32 && p->dtype != MOE_BF16) return fail(MOE_ERR_INVALID_ARG, "dtype %d unknown", p->dtype);
+  if (p->kind < MOE_GATE_TOPK || p->kind > MOE_GATE_HASH) return fail(MOE_ERR_INVALID_ARG, "gate kind %d unknown", p->kind);
+  if (p->S < 0) return fail(MOE_ERR_INVALID_ARG, "S = %d < 0", p->S);
+  if (p->E < 1 || p->E > 1024) return fail(MOE_ERR_INVALID_ARG, "E = %d outside [1, 1024]", p->E);
+  if (p->capacity < 0) return fail(MOE_ERR_INVALID_ARG, "capacity = %d < 0", p->capacity);
+  if (static_cast<int64_t>(p->E) * p->capacity > kI32Max) return fail(MOE_ERR_INVALID_ARG, "E * capacity >= 2^31");
+  if (p->normalize != 0 && p->normalize != 1) return fail(MOE_ERR_INVALID_ARG, "normalize must be 0 or 1");
+  if (p->logits_in != 0 && p->logits_in != 1) return fail(MOE_ERR_INVALID_ARG, "logits_in must be 0 or 1");
+  switch (p->kind) {
+    case MOE_GATE_TOPK:
+      if (p->k < 1 || p->k > 8 || p->k > p->E) return fail(MOE_ERR_INVALID_ARG, "TOPK needs 1 <= k <= min(E, 8), got k = %d, E = %d", p->k, p->E);
+      break;
+    case MOE_GATE_KTOP1:
+      if (p->k < 1 || p->k > 8 || p->E % p->k != 0) return fail(MOE_ERR_INVALID_ARG, "KTOP1 needs 1 <= k <= 8 and E %% k == 0, got k = %d, E = %d", p->k, p->E);
+      break;
+    default:
+      if (p->k != 1) return fail(MOE_ERR_INVALID_ARG, "HASH needs k = 1, got %d", p->k);
+      if (p->logits_in) return fail(MOE_ERR_INVALID_ARG, "HASH takes no logits");
+      break;
+  }
+  if (static_cast<int64_t>(p->S) * p->k > kI32Max) return fail(MOE_ERR_INVALID_ARG, "S * k >= 2^31");
+  const bool project = p->kind != MOE_GATE_HASH && !p->logits_in;
+  if (project) {
+    if (p->d < 1) return fail(MOE_ERR_INVALID_ARG, "d = %d < 1", p->d);
+    if ((static_cast<int64_t>(p->d) * elt_size(p->dtype)) % 16 != 0)
+      return fail(MOE_ERR_UNSUPPORTED, "row of x is %lld bytes; a multiple of 16 is required",
+                  static_cast<long long>(p->d) * static_cast<long long>(elt_size(p->dtype)));
+  }
+  return MOE_OK;
+}
+
+size_t gate_workspace_bytes(const moe_gate_params* p) {
+  const size_t n = static_cast<size_t>(p->k) * static_cast<size_t>(hist_blocks(p->S)) * static_cast<size_t>(p->E);
+  return n * sizeof(int32_t);
+}
+
+moe_status check_layout(const moe_layout* l, const char* who) {
+  if (!l) return fail(MOE_ERR_INVALID_ARG, "%s: layout is NULL", who);
+  if (l->dtype != MOE_F32 && l->dtype != MOE_BF16) return fail(MOE_ERR_INVALID_ARG, "%s: dtype %d unknown", who, l->dtype);
+  if (l->S < 0 || l->d < 1 || l->E < 1 || l->E > 1024 || l->k < 1 || l->k > 8 || l->capacity < 0)
+    return fail(MOE_ERR_INVALID_ARG, "%s: need S >= 0, d >= 1, 1 <= E <= 1024, 1 <= k <= 8, capacity >= 0 "
+                "(got S=%d d=%d E=%d k=%d C=%d)", who, l->S, l->d, l->E, l->k, l->capacity);
+  if (static_cast<int64_t>(l->S) * l->k > kI32Max || static_cast<int64_t>(l->E) * l->capacity > kI32Max)
+    return fail(MOE_ERR_INVALID_ARG, "%s: S * k or E * capacity >= 2^31", who);
+  if ((static_cast<int64_t>(l->d) * elt_size(l->dtype)) % 16 != 0)
+    return fail(MOE_ERR_UNSUPPORTED, "%s: row is %lld bytes; a multiple of 16 is required", who,
+                static_cast<long long>(l->d) * static_cast<long long>(elt_size(l->dtype)));
+  return MOE_OK;
+}
+
+// A device buffer of n elements: required (non-NULL) when n > 0, with the
+// given alignment.
+moe_status need(const void* p, int64_t n, size_t align, const char* who, const char* name) {
+  if (n > 0 && !p) return fail(MOE_ERR_INVALID_ARG, "%s: %s is NULL", who, name);
+  if (p && !aligned(p, align))
+    return fail(align == 16 ? MOE_ERR_UNSUPPORTED : MOE_ERR_INVALID_ARG, "%s: %s is not %zu-byte aligned", who, name, align);
+  return MOE_OK;
+}
+
+int nchunks(const moe_layout* l) {
+  return static_cast<int>((static_cast<int64_t>(l->d) * elt_size(l->dtype)) / 16);
+}
+
+}  // namespace
+
+#define CHECK(expr)                 \
+  do {                              \
+    moe_status _st = (expr);        \
+    if (_st != MOE_OK) return _st;  \
+  } while (0)
+
+extern "C" {
+
+int32_t moe_abi_version(void) { return MOE_ABI_VERSION; }
+
+const char* moe_status_string(moe_status s) {
+  switch (s) {
+    case MOE_OK: return "MOE_OK";
+    case MOE_ERR_INVALID_ARG: return "MOE_ERR_INVALID_ARG";
+    case MOE_ERR_UNSUPPORTED: return "MOE_ERR_UNSUPPORTED";
+    case MOE_ERR_WORKSPACE: return "MOE_ERR_WORKSPACE";
+    case MOE_ERR_HIP: return "MOE_ERR_HIP";
+  }
+  return "unknown moe_status";
+}
+
+const char* moe_last_error(void) { return g_last_error; }
+
+moe_status moe_gate_workspace_size(const moe_gate_params* p, size_t* bytes) {
+  if (!bytes) return fail(MOE_ERR_INVALID_ARG, "bytes is NULL");
+  CHECK(check_gate_params(p));
+  *bytes = gate_workspace_bytes(p);
+  return ok();
+}
+
+moe_status moe_gate(const moe_gate_params* p, const void* x, const void* wg, const float* bias,
+                    const int32_t* token_ids, float* logits, int32_t* ids, int32_t* slots,
+                    float* weights, int32_t* counts, int32_t* demand, int32_t* slot_src,
+                    void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  static const char* who = "moe_gate";
+  CHECK(check_gate_params(p));
+  const int64_t S = p->S, E = p->E, k = p->k, C = p->capacity;
+  const size_t elt = elt_size(p->dtype);
+  if (p->kind == MOE_GATE_HASH) {
+    CHECK(need(token_ids, S, 4, who, "token_ids"));
+    if (x || wg || bias || logits) return fail(MOE_ERR_INVALID_ARG, "%s: HASH takes no x, wg, bias or logits", who);
+  } else if (p->logits_in) {
+    CHECK(need(logits, S * E, 4, who, "logits"));
+    if (x || wg || bias || token_ids) return fail(MOE_ERR_INVALID_ARG, "%s: with logits_in, x, wg, bias and token_ids must be NULL", who);
+  } else {
+    CHECK(need(x, S * p->d, 16, who, "x"));
+    CHECK(need(wg, static_cast<int64_t>(p->d) * E, elt, who, "wg"));
+    CHECK(need(bias, 0, 4, who, "bias"));
+    CHECK(need(logits, 0, 4, who, "logits"));
+    if (token_ids) return fail(MOE_ERR_INVALID_ARG, "%s: token_ids is only for HASH", who);
+  }
+  CHECK(need(ids, S * k, 4, who, "ids"));
+  CHECK(need(slots, S * k, 4, who, "slots"));
+  CHECK(need(weights, S * k, 4, who, "weights"));
+  CHECK(need(counts, E, 4, who, "counts"));
+  CHECK(need(demand, 0, 4, who, "demand"));
+  CHECK(need(slot_src, E * C, 4, who, "slot_src"));
+  const size_t ws = gate_workspace_bytes(p);
+  if (workspace_bytes < ws) return fail(MOE_ERR_WORKSPACE, "%s: workspace of %zu bytes, %zu needed", who, workspace_bytes, ws);
+  if (ws > 0 && !workspace) return fail(MOE_ERR_WORKSPACE, "%s: workspace is NULL", who);
+  if (workspace && !aligned(workspace, 16)) return fail(MOE_ERR_WORKSPACE, "%s: workspace is not 16-byte aligned", who);
+
+  const int nb = static_cast<int>(hist_blocks(S));
+  int32_t* hist = static_cast<int32_t*>(workspace);
+
+  RouteArgs ra{};
+  ra.S = p->S; ra.d = p->d; ra.E = p->E; ra.k = p->k; ra.nb = nb;
+  ra.kind = p->kind; ra.normalize = p->normalize; ra.logits_in = p->logits_in; ra.dtype = p->dtype;
+  ra.hash_seed = p->hash_seed;
+  ra.x = x; ra.wg = wg; ra.bias = bias; ra.token_ids = token_ids; ra.logits = logits;
+  ra.ids = ids; ra.weights = weights; ra.hist = hist;
+  hipError_t err = launch_route(ra, stream);
+  if (err != hipSuccess) return hip_fail(err, "moe_gate: route kernel launch");
+
+  ScanArgs sa{};
+  sa.E = p->E; sa.k = p->k; sa.nb = nb; sa.C = p->capacity;
+  sa.hist = hist; sa.counts = counts; sa.demand = demand; sa.slot_src = slot_src;
+  err = launch_scan(sa, stream);
+  if (err != hipSuccess) return hip_fail(err, "moe_gate: scan kernel launch");
+
+  AssignArgs aa{};
+  aa.S = p->S; aa.E = p->E; aa.k = p->k; aa.nb = nb; aa.C = p->capacity;
+  aa.ids = ids; aa.offs = hist; aa.slots = slots; aa.slot_src = slot_src;
+  err = launch_assign(aa, stream);
+  if (err != hipSuccess) return hip_fail(err, "moe_gate: assign kernel launch");
+  return ok();
+}
+
+moe_status moe_dispatch(const moe_layout* l, const void* x, const int32_t* slot_src, void* xe,
+                        hipStream_t stream) {
+  static const char* who = "moe_dispatch";
+  CHECK(check_layout(l, who));
+  const int64_t rows = static_cast<int64_t>(l->E) * l->capacity;
+  CHECK(need(x, static_cast<int64_t>(l->S) * l->d, 16, who, "x"));
+  CHECK(need(slot_src, rows, 4, who, "slot_src"));
+  CHECK(need(xe, rows * l->d, 16, who, "xe"));
+  RowArgs a{};
+  a.rows = rows; a.nch = nchunks(l); a.S = l->S; a.E = l->E; a.k = l->k; a.C = l->capacity; a.dtype = l->dtype;
+  a.src = x; a.slot_src = slot_src; a.dst = xe;
+  const hipError_t err = launch_dispatch(a, stream);
+  if (err != hipSuccess) return hip_fail(err, "moe_dispatch: kernel launch");
+  return ok();
+}
+
+static moe_status combine_common(const char* who, const moe_layout* l, const void* src,
+                                 const int32_t* ids, const int32_t* slots, const float* weights,
+                                 void* out, bool weighted, hipStream_t stream) {
+  CHECK(check_layout(l, who));
+  const int64_t S = l->S, k = l->k;
+  CHECK(need(src, static_cast<int64_t>(l->E) * l->capacity * l->d, 16, who, weighted ? "ye" : "dxe"));
+  CHECK(need(ids, S * k, 4, who, "ids"));
+  CHECK(need(slots, S * k, 4, who, "slots"));
+  if (weighted) CHECK(need(weights, S * k, 4, who, "weights"));
+  CHECK(need(out, S * l->d, 16, who, weighted ? "y" : "dx"));
+  RowArgs a{};
+  a.rows = S; a.nch = nchunks(l); a.S = l->S; a.E = l->E; a.k = l->k; a.C = l->capacity; a.dtype = l->dtype;
+  a.src = src; a.ids = ids; a.slots = slots; a.weights = weights; a.dst = out;
+  const hipError_t err = launch_combine(a, weighted, stream);
+  if (err != hipSuccess) return hip_fail(err, weighted ? "moe_combine: kernel launch" : "moe_dispatch_bwd: kernel launch");
+  return ok();
+}
+
+moe_status moe_combine(const moe_layout* l, const void* ye, const int32_t* ids, const int32_t* slots,
+                       const float* weights, void* y, hipStream_t stream) {
+  return combine_common("moe_combine", l, ye, ids, slots, weights, y, true, stream);
+}
+
+moe_status moe_dispatch_bwd(const moe_layout* l, const void* dxe, const int32_t* ids,
+                            const int32_t* slots, void* dx, hipStream_t stream) {
+  return combine_common("moe_dispatch_bwd", l, dxe, ids, slots, nullptr, dx, false, stream);
+}
+
+moe_status moe_combine_bwd(const moe_layout* l, const void* dy, const void* ye, const int32_t* slots,
+                           const int32_t* slot_src, const float* weights, void* dye, float* dw,
+                           hipStream_t stream) {
+  static const char* who = "moe_combine_bwd";
+  CHECK(check_layout(l, who));
+  const int64_t S = l->S, k = l->k;
+  const int64_t rows = static_cast<int64_t>(l->E) * l->capacity;
+  CHECK(need(dy, S * l->d, 16, who, "dy"));
+  CHECK(need(slot_src, rows, 4, who, "slot_src"));
+  CHECK(need(weights, S * k, 4, who, "weights"));
+  CHECK(need(dye, rows * l->d, 16, who, "dye"));
+  if (dw) {
+    CHECK(need(ye, rows * l->d, 16, who, "ye"));
+    CHECK(need(slots, S * k, 4, who, "slots"));
+    CHECK(need(dw, S * k, 4, who, "dw"));
+  } else if (ye || slots) {
+    return fail(MOE_ERR_INVALID_ARG, "%s: ye and slots must be NULL when dw is NULL", who);
+  }
+  RowArgs a{};
+  a.rows = rows; a.nch = nchunks(l); a.S = l->S; a.E = l->E; a.k = l->k; a.C = l->capacity; a.dtype = l->dtype;
+  a.src = dy; a.aux = ye; a.slots = slots; a.slot_src = slot_src; a.weights = weights; a.dst = dye; a.dw = dw;
+  const hipError_t err = launch_combine_bwd(a, stream);
+  if (err != hipSuccess) return hip_fail(err, "moe_combine_bwd: kernel launch");
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,95 @@
+// Device helpers shared by the gfx950 kernels: element types, 16-byte row
+// vectors, bf16 <-> fp32 conversion and wave64 primitives.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace hetumoe {
+
+constexpr int kWave = 64;           // CDNA wavefront width
+constexpr int kBlock = 256;         // threads per block for every kernel here
+constexpr int kWavesPerBlock = kBlock / kWave;
+constexpr int kTokensPerHistBlock = 256;  // granularity of the capacity scan (one token per thread)
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// bf16 storage type: the upper 16 bits of an IEEE binary32.
+struct bf16_t {
+  uint16_t bits;
+};
+
+__device__ __forceinline__ float bf16_lo(uint32_t packed) { return __uint_as_float(packed << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t packed) { return __uint_as_float(packed & 0xffff0000u); }
+
+// fp32 -> bf16 bits, round to nearest, ties to even (finite inputs; values
+// beyond the bf16 range become infinities as IEEE rounding requires).
+__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return f32_to_bf16_bits(lo) | (f32_to_bf16_bits(hi) << 16);
+}
+
+// A 16-byte chunk of a row holds 4 fp32 or 8 bf16 elements.
+template <typename T> struct Chunk;
+template <> struct Chunk<float> {
+  static constexpr int kElems = 4;
+  __device__ __forceinline__ static void unpack(const u32x4& v, float* out) {
+    out[0] = __uint_as_float(v.x);
+    out[1] = __uint_as_float(v.y);
+    out[2] = __uint_as_float(v.z);
+    out[3] = __uint_as_float(v.w);
+  }
+  __device__ __forceinline__ static u32x4 pack(const float* in) {
+    u32x4 v;
+    v.x = __float_as_uint(in[0]);
+    v.y = __float_as_uint(in[1]);
+    v.z = __float_as_uint(in[2]);
+    v.w = __float_as_uint(in[3]);
+    return v;
+  }
+};
+template <> struct Chunk<bf16_t> {
+  static constexpr int kElems = 8;
+  __device__ __forceinline__ static void unpack(const u32x4& v, float* out) {
+    out[0] = bf16_lo(v.x); out[1] = bf16_hi(v.x);
+    out[2] = bf16_lo(v.y); out[3] = bf16_hi(v.y);
+    out[4] = bf16_lo(v.z); out[5] = bf16_hi(v.z);
+    out[6] = bf16_lo(v.w); out[7] = bf16_hi(v.w);
+  }
+  __device__ __forceinline__ static u32x4 pack(const float* in) {
+    u32x4 v;
+    v.x = pack_bf16x2(in[0], in[1]);
+    v.y = pack_bf16x2(in[2], in[3]);
+    v.z = pack_bf16x2(in[4], in[5]);
+    v.w = pack_bf16x2(in[6], in[7]);
+    return v;
+  }
+};
+
+__device__ __forceinline__ float load_elem(const float* p, int64_t i) { return p[i]; }
+__device__ __forceinline__ float load_elem(const bf16_t* p, int64_t i) {
+  return __uint_as_float(static_cast<uint32_t>(p[i].bits) << 16);
+}
+
+__device__ __forceinline__ int lane_id() {
+  return __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+}
+
+// Number of set bits of `mask` in lanes below the calling lane.
+__device__ __forceinline__ int popc_below(uint64_t mask) {
+  return __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask >> 32),
+                                   __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u));
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, kWave);
+  return v;
+}
+
+}  // namespace hetumoe

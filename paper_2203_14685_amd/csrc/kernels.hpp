@@ -1,0 +1,60 @@
+// Argument blocks and launchers of the gfx950 kernels (internal to the library).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace hetumoe {
+
+struct RouteArgs {
+  int S, d, E, k, nb;
+  int kind, normalize, logits_in, dtype;
+  uint64_t hash_seed;
+  const void* x;            // [S, d]
+  const void* wg;           // [d, E]
+  const float* bias;        // [E] or null
+  const int32_t* token_ids; // [S] (hash)
+  float* logits;            // [S, E]: input (logits_in), output, or null
+  int32_t* ids;             // [S, k]
+  float* weights;           // [S, k]
+  int32_t* hist;            // [k, nb, E] workspace
+};
+
+struct ScanArgs {
+  int E, k, nb, C;
+  int32_t* hist;     // [k, nb, E]: counts in, exclusive offsets out
+  int32_t* counts;   // [E]
+  int32_t* demand;   // [E] or null
+  int32_t* slot_src; // [E, C]
+};
+
+struct AssignArgs {
+  int S, E, k, nb, C;
+  const int32_t* ids;  // [S, k]
+  const int32_t* offs; // [k, nb, E]
+  int32_t* slots;      // [S, k]
+  int32_t* slot_src;   // [E, C]
+};
+
+struct RowArgs {
+  int64_t rows;        // rows processed by the row kernels
+  int nch;             // 16-byte chunks per row
+  int S, E, k, C, dtype;
+  const void* src;     // gather source rows
+  const void* aux;     // second source (ye for dw), or null
+  const int32_t* ids;
+  const int32_t* slots;
+  const int32_t* slot_src;
+  const float* weights;
+  void* dst;
+  float* dw;
+};
+
+hipError_t launch_route(const RouteArgs& a, hipStream_t st);
+hipError_t launch_scan(const ScanArgs& a, hipStream_t st);
+hipError_t launch_assign(const AssignArgs& a, hipStream_t st);
+hipError_t launch_dispatch(const RowArgs& a, hipStream_t st);
+hipError_t launch_combine(const RowArgs& a, bool weighted, hipStream_t st);
+hipError_t launch_combine_bwd(const RowArgs& a, hipStream_t st);
+
+}  // namespace hetumoe

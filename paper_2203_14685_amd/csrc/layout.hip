@@ -1,0 +1,204 @@
+// Layout-transform kernels for gfx950: steps 2 and 6 of Algorithm 1 and their
+// gradients.  All four are gathers: every output row has exactly one writer,
+// so there are no atomics and results are bitwise reproducible.
+//
+// One wavefront owns one output row and walks it in 16-byte chunks (64 lanes x
+// 16 B = 1 KiB per instruction), issuing up to kUnroll loads per lane before
+// the first store so that enough bytes are in flight to cover HBM latency.
+// Expert buffers ([E, C, d], written once and read by a later kernel) are
+// written with non-temporal stores.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace hetumoe {
+
+constexpr int kUnroll = 8;
+
+__device__ __forceinline__ void store_nt(u32x4* p, const u32x4& v) { __builtin_nontemporal_store(v, p); }
+
+// ---------------------------------------------------------------- dispatch
+// xe[row] = x[slot_src[row] / k], or zeros for an empty slot.
+__global__ __launch_bounds__(kBlock) void dispatch_kernel(RowArgs a) {
+  const int64_t row = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + threadIdx.x / kWave;
+  if (row >= a.rows) return;
+  const int lane = lane_id();
+  const int nch = a.nch;
+  const int src = a.slot_src[row];
+  u32x4* dst = reinterpret_cast<u32x4*>(a.dst) + row * nch;
+  // entries outside [0, S*k) are out of contract and treated as empty slots
+  if (src >= 0 && src < a.S * a.k) {
+    const u32x4* srow = reinterpret_cast<const u32x4*>(a.src) + static_cast<int64_t>(src / a.k) * nch;
+    for (int base = 0; base < nch; base += kWave * kUnroll) {
+      u32x4 v[kUnroll];
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        const int i = base + u * kWave + lane;
+        if (i < nch) v[u] = srow[i];
+      }
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        const int i = base + u * kWave + lane;
+        if (i < nch) store_nt(dst + i, v[u]);
+      }
+    }
+  } else {
+    const u32x4 z = {0u, 0u, 0u, 0u};
+    for (int i = lane; i < nch; i += kWave) store_nt(dst + i, z);
+  }
+}
+
+// ---------------------------------------------------------------- combine
+// y[s] = sum_{r kept} w[s,r] * ye[ids[s,r], slots[s,r]]  (WEIGHTED)
+// dx[s] = sum_{r kept} dxe[ids[s,r], slots[s,r]]        (!WEIGHTED)
+// fp32 accumulation in r order, one rounding to T.
+template <typename T, bool WEIGHTED>
+__global__ __launch_bounds__(kBlock) void combine_kernel(RowArgs a) {
+  constexpr int kEl = Chunk<T>::kElems;
+  const int64_t s = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + threadIdx.x / kWave;
+  if (s >= a.rows) return;
+  const int lane = lane_id();
+  const int nch = a.nch, k = a.k;
+  const u32x4* ye = reinterpret_cast<const u32x4*>(a.src);
+  u32x4* out = reinterpret_cast<u32x4*>(a.dst) + s * nch;
+  for (int base = 0; base < nch; base += kWave * kUnroll) {
+    float acc[kUnroll][kEl];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u)
+#pragma unroll
+      for (int q = 0; q < kEl; ++q) acc[u][q] = 0.f;
+    for (int r = 0; r < k; ++r) {
+      const int slot = a.slots[s * k + r];
+      const int e = a.ids[s * k + r];
+      // dropped choices (slot -1) and out-of-contract entries contribute nothing
+      if (slot < 0 || slot >= a.C || e < 0 || e >= a.E) continue;
+      const float w = WEIGHTED ? a.weights[s * k + r] : 1.f;
+      const u32x4* srow = ye + (static_cast<int64_t>(e) * a.C + slot) * nch;
+      u32x4 v[kUnroll];
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        const int i = base + u * kWave + lane;
+        if (i < nch) v[u] = srow[i];
+      }
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        const int i = base + u * kWave + lane;
+        if (i < nch) {
+          float f[kEl];
+          Chunk<T>::unpack(v[u], f);
+#pragma unroll
+          for (int q = 0; q < kEl; ++q) acc[u][q] = WEIGHTED ? fmaf(w, f[q], acc[u][q]) : acc[u][q] + f[q];
+        }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int i = base + u * kWave + lane;
+      if (i < nch) out[i] = Chunk<T>::pack(acc[u]);
+    }
+  }
+}
+
+// ---------------------------------------------------------------- combine backward
+// Rows [0, rows): dye[row] = w[src] * dy[src / k] (zeros for an empty slot) and,
+// with DW, dw[src] = <dy[src / k], ye[row]>.  Blocks past the row blocks clear
+// dw of dropped choices.
+template <typename T, bool DW>
+__global__ __launch_bounds__(kBlock) void combine_bwd_kernel(RowArgs a, int64_t row_blocks) {
+  constexpr int kEl = Chunk<T>::kElems;
+  if (static_cast<int64_t>(blockIdx.x) >= row_blocks) {
+    if constexpr (DW) {
+      const int64_t i = (static_cast<int64_t>(blockIdx.x) - row_blocks) * kBlock + threadIdx.x;
+      if (i < static_cast<int64_t>(a.S) * a.k && a.slots[i] < 0) a.dw[i] = 0.f;
+    }
+    return;
+  }
+  const int64_t row = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + threadIdx.x / kWave;
+  if (row >= a.rows) return;
+  const int lane = lane_id();
+  const int nch = a.nch;
+  const int src = a.slot_src[row];
+  u32x4* dst = reinterpret_cast<u32x4*>(a.dst) + row * nch;
+  if (src < 0 || src >= a.S * a.k) {  // empty (or out-of-contract) slot
+    const u32x4 z = {0u, 0u, 0u, 0u};
+    for (int i = lane; i < nch; i += kWave) store_nt(dst + i, z);
+    return;
+  }
+  const float w = a.weights[src];
+  const u32x4* dyrow = reinterpret_cast<const u32x4*>(a.src) + static_cast<int64_t>(src / a.k) * nch;
+  const u32x4* yerow = reinterpret_cast<const u32x4*>(a.aux) + row * nch;
+  float dot = 0.f;
+  for (int base = 0; base < nch; base += kWave * kUnroll) {
+    u32x4 v[kUnroll];
+    u32x4 ve[DW ? kUnroll : 1];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int i = base + u * kWave + lane;
+      if (i < nch) {
+        v[u] = dyrow[i];
+        if constexpr (DW) ve[u] = yerow[i];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int i = base + u * kWave + lane;
+      if (i < nch) {
+        float f[kEl];
+        Chunk<T>::unpack(v[u], f);
+        if constexpr (DW) {
+          float g[kEl];
+          Chunk<T>::unpack(ve[u], g);
+#pragma unroll
+          for (int q = 0; q < kEl; ++q) dot = fmaf(f[q], g[q], dot);
+        }
+#pragma unroll
+        for (int q = 0; q < kEl; ++q) f[q] *= w;
+        store_nt(dst + i, Chunk<T>::pack(f));
+      }
+    }
+  }
+  if constexpr (DW) {
+    dot = wave_sum(dot);
+    if (lane == 0) a.dw[src] = dot;
+  }
+}
+
+// ---------------------------------------------------------------- launchers
+static inline unsigned blocks_for_rows(int64_t rows) {
+  return static_cast<unsigned>((rows + kWavesPerBlock - 1) / kWavesPerBlock);
+}
+
+hipError_t launch_dispatch(const RowArgs& a, hipStream_t st) {
+  if (a.rows == 0) return hipSuccess;
+  dispatch_kernel<<<dim3(blocks_for_rows(a.rows)), dim3(kBlock), 0, st>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_combine(const RowArgs& a, bool weighted, hipStream_t st) {
+  if (a.rows == 0) return hipSuccess;
+  const dim3 grid(blocks_for_rows(a.rows)), block(kBlock);
+  if (a.dtype == 1) {
+    if (weighted) combine_kernel<bf16_t, true><<<grid, block, 0, st>>>(a);
+    else combine_kernel<bf16_t, false><<<grid, block, 0, st>>>(a);
+  } else {
+    if (weighted) combine_kernel<float, true><<<grid, block, 0, st>>>(a);
+    else combine_kernel<float, false><<<grid, block, 0, st>>>(a);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_combine_bwd(const RowArgs& a, hipStream_t st) {
+  const int64_t row_blocks = blocks_for_rows(a.rows);
+  const int64_t dw_blocks = a.dw ? (static_cast<int64_t>(a.S) * a.k + kBlock - 1) / kBlock : 0;
+  if (row_blocks + dw_blocks == 0) return hipSuccess;
+  const dim3 grid(static_cast<unsigned>(row_blocks + dw_blocks)), block(kBlock);
+  if (a.dtype == 1) {
+    if (a.dw) combine_bwd_kernel<bf16_t, true><<<grid, block, 0, st>>>(a, row_blocks);
+    else combine_bwd_kernel<bf16_t, false><<<grid, block, 0, st>>>(a, row_blocks);
+  } else {
+    if (a.dw) combine_bwd_kernel<float, true><<<grid, block, 0, st>>>(a, row_blocks);
+    else combine_bwd_kernel<float, false><<<grid, block, 0, st>>>(a, row_blocks);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace hetumoe

@@ -1,0 +1,132 @@
+"""Helpers for the GPU parity tests: run the HIP path through the C ABI and the
+CPU oracle on the same seeded inputs and compare them.
+
+Comparison rules:
+* integers (ids, slots, counts, demand, slot_src) and the dispatch copy: bit-exact;
+* floats: |gpu - oracle| <= rtol * M element-wise, where M is the sum of the
+  absolute values of the terms forming that element (so an element with no
+  terms must be exactly 0).  rtol = 1e-5 for fp32 outputs, 2e-2 for bf16.
+"""
+
+import numpy as np
+import torch
+
+import oracle
+import paper_2203_14685_amd as hm
+from paper_2203_14685_amd import workloads as wl
+
+RTOL = {"f32": 1e-5, "bf16": 2e-2}
+DEV = "cuda"
+
+
+def announce(msg):
+    print(f"[case] {msg}", flush=True)
+
+
+def decode(a, dtype):
+    return oracle.decode(a, dtype)
+
+
+def assert_close(gpu, ref, mag, rtol, what):
+    gpu = np.asarray(gpu, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    err = np.abs(gpu - ref)
+    bound = rtol * np.asarray(mag, dtype=np.float64)
+    bad = err > bound
+    if bad.any():
+        idx = np.argwhere(bad)[:5]
+        raise AssertionError(f"{what}: {int(bad.sum())} of {bad.size} out of tolerance; first {idx.tolist()}: "
+                             f"gpu {gpu[bad][:5]} oracle {ref[bad][:5]} bound {bound[bad][:5]}")
+    nz = mag > 0
+    worst = float((err[nz] / mag[nz]).max()) if nz.any() else 0.0
+    return worst
+
+
+def assert_equal(gpu, ref, what):
+    gpu = np.asarray(gpu)
+    ref = np.asarray(ref)
+    assert gpu.shape == ref.shape, f"{what}: shape {gpu.shape} vs {ref.shape}"
+    if not np.array_equal(gpu, ref):
+        bad = np.argwhere(gpu != ref)[:5]
+        raise AssertionError(f"{what}: {int((gpu != ref).sum())} mismatches; first {bad.tolist()}: "
+                             f"gpu {[gpu[tuple(b)] for b in bad]} oracle {[ref[tuple(b)] for b in bad]}")
+
+
+def gpu_gate(w, inp, E, k, C, kind, normalize, logits=None):
+    """Run moe_gate on device copies of the host inputs; return host arrays."""
+    dt = w["dtype"]
+    if kind == hm.MOE_GATE_HASH:
+        out = hm.gate(kind, k, E, C, token_ids=wl.to_device(inp["token_ids"], dt), hash_seed=0)
+    elif logits is not None:
+        out = hm.gate(kind, k, E, C, logits=wl.to_device(logits, "f32"), logits_in=True, normalize=normalize)
+    else:
+        out = hm.gate(kind, k, E, C, x=wl.to_device(inp["x"], dt), wg=wl.to_device(inp["wg"], dt),
+                      bias=wl.to_device(inp["bias"], "f32"), normalize=normalize, want_logits=True)
+    torch.cuda.synchronize()
+    return {key: wl.to_host(v) for key, v in out.items()}
+
+
+def check_gate(w, inp, g, E, k, C, kind, normalize, logits_in=None):
+    """Compare gate outputs `g` (host) with the oracle.  Returns stats."""
+    dt = w["dtype"]
+    stats = {}
+    if kind == hm.MOE_GATE_HASH:
+        ref = oracle.gate(oracle.GATE_HASH, 1, E, C, token_ids=inp["token_ids"], hash_seed=0)
+    else:
+        sel = logits_in
+        if sel is None:
+            L64, A = oracle.logits(inp["x"], inp["wg"], dt, inp["bias"])
+            stats["logits_err"] = assert_close(g["logits"], L64, A, RTOL["f32"], "logits")
+            sel = g["logits"]
+            # end to end: selection on the fp64 logits may differ only at certified near-ties
+            ids64 = oracle.select(L64, kind, k)
+            mism = np.argwhere(ids64 != g["ids"])
+            for s, r in mism:
+                a, b = int(ids64[s, r]), int(g["ids"][s, r])
+                gap = abs(L64[s, a] - L64[s, b])
+                assert gap <= 2 * RTOL["f32"] * max(A[s, a], A[s, b]), \
+                    f"ids differ at ({s},{r}) without a near-tie: gap {gap}"
+            stats["near_tie_mismatches"] = int(len(mism))
+        ref = oracle.gate(kind, k, E, C, normalize=normalize, sel_logits=sel)
+    for key in ("ids", "slots", "counts", "demand", "slot_src"):
+        assert_equal(g[key], ref[key], key)
+    stats["weights_err"] = assert_close(g["weights"], ref["weights"], np.abs(ref["weights"]), RTOL["f32"], "weights")
+    stats["kept"] = int((g["slots"] >= 0).sum())
+    return ref, stats
+
+
+def check_layout_ops(w, x_host, ids, slots, weights, slot_src, E, C, k, seed=0):
+    """Dispatch, combine, dispatch_bwd and combine_bwd on the GPU vs the oracle,
+    all fed the same routing arrays."""
+    dt = w["dtype"]
+    S, d = x_host.shape
+    rt = RTOL[dt]
+    d_ids, d_slots = wl.to_device(ids, "f32"), wl.to_device(slots, "f32")
+    d_w, d_src = wl.to_device(weights.astype(np.float32), "f32"), wl.to_device(slot_src, "f32")
+    stats = {}
+    # dispatch: bit copy
+    xe = wl.to_host(hm.dispatch(wl.to_device(x_host, dt), d_src, k))
+    assert_equal(xe, oracle.dispatch(x_host, slot_src, k), "dispatch xe")
+    # combine on random expert outputs
+    ye = wl.make_rows((E, C, d), dt, seed + 3)
+    y = wl.to_host(hm.combine(wl.to_device(ye, dt), d_ids, d_slots, d_w))
+    y_ref, y_mag = oracle.combine(ye, ids, slots, weights.astype(np.float32).astype(np.float64), dt)
+    stats["combine_err"] = assert_close(decode(y, dt), decode(y_ref, dt), y_mag, rt, "combine y")
+    # dispatch backward
+    dxe = wl.make_rows((E, C, d), dt, seed + 4)
+    dx = wl.to_host(hm.dispatch_bwd(wl.to_device(dxe, dt), d_ids, d_slots))
+    dx_ref, dx_mag = oracle.dispatch_bwd(dxe, ids, slots, dt)
+    stats["dispatch_bwd_err"] = assert_close(decode(dx, dt), decode(dx_ref, dt), dx_mag, rt, "dispatch_bwd dx")
+    # combine backward, with and without dw
+    dy = wl.make_rows((S, d), dt, seed + 2)
+    d_dy, d_ye = wl.to_device(dy, dt), wl.to_device(ye, dt)
+    dye, dw = hm.combine_bwd(d_dy, d_src, d_w, ye=d_ye, slots=d_slots, want_dw=True)
+    dye, dw = wl.to_host(dye), wl.to_host(dw)
+    dye_ref, dye_mag, dw_ref, dw_mag = oracle.combine_bwd(dy, ye, slot_src, weights.astype(np.float32), k, dt)
+    stats["combine_bwd_dye_err"] = assert_close(decode(dye, dt), decode(dye_ref, dt), dye_mag, rt, "combine_bwd dye")
+    stats["combine_bwd_dw_err"] = assert_close(dw, dw_ref, dw_mag, RTOL["f32"], "combine_bwd dw")
+    dye2, dw2 = hm.combine_bwd(d_dy, d_src, d_w, want_dw=False)
+    assert dw2 is None
+    assert_equal(wl.to_host(dye2), dye, "combine_bwd dye without dw")
+    torch.cuda.synchronize()
+    return stats

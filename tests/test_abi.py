@@ -1,0 +1,143 @@
+"""CPU checks of the C-ABI library: it loads, exports every symbol the header
+declares, has the struct layout the binding assumes, and rejects bad arguments
+with status codes before any HIP call (so these run without a GPU)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2203_14685_amd as hm
+from paper_2203_14685_amd import binding as b
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "hetumoe.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(hm.LIB_PATH):
+        pytest.fail("libhetumoe.so is not built (run `python -m paper_2203_14685_amd.build`)")
+    return hm.load()
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"MOE_API\s+[\w\s\*]+?\b(moe_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_abi():
+    names = declared_symbols()
+    assert set(names) == set(b.EXPORTED), names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for name in declared_symbols():
+        assert hasattr(lib, name), f"{name} not exported"
+
+
+def test_abi_version_and_struct_layout(lib):
+    assert lib.moe_abi_version() == 1
+    assert ctypes.sizeof(b.GateParams) == 48
+    assert b.GateParams.hash_seed.offset == 40
+    assert ctypes.sizeof(b.Layout) == 24
+    assert lib.moe_status_string(0) == b"MOE_OK"
+    assert lib.moe_status_string(3) == b"MOE_ERR_WORKSPACE"
+
+
+def _ws(params):
+    n = ctypes.c_size_t(12345)
+    st = hm.load().moe_gate_workspace_size(ctypes.byref(params), ctypes.byref(n))
+    return st, n.value
+
+
+@pytest.mark.parametrize("S,E,k,kind", [(1024, 8, 1, 0), (8192, 16, 2, 0), (32768, 64, 4, 1), (65536, 128, 1, 2),
+                                        (0, 8, 1, 0), (257, 5, 2, 0)])
+def test_workspace_size(lib, S, E, k, kind):
+    p = hm.gate_params(S, 256, E, k, 10, kind)
+    st, n = _ws(p)
+    assert st == 0
+    assert n == k * ((S + 255) // 256) * E * 4
+
+
+BAD_PARAMS = [
+    dict(E=0), dict(E=1025), dict(S=-1), dict(capacity=-1), dict(k=0), dict(k=9, E=16),
+    dict(k=3, E=2), dict(kind=1, k=3, E=16), dict(kind=2, k=2), dict(kind=3), dict(dtype=2),
+    dict(normalize=2), dict(logits_in=2), dict(kind=2, logits_in=1), dict(d=0),
+    dict(E=1024, capacity=1 << 21), dict(S=1 << 30, k=2),
+]
+
+
+@pytest.mark.parametrize("bad", BAD_PARAMS)
+def test_bad_gate_params_rejected(lib, bad):
+    base = dict(S=100, d=256, E=8, k=1, capacity=20, kind=0, normalize=0, logits_in=0, dtype=0, hash_seed=0)
+    base.update(bad)
+    p = hm.gate_params(**base)
+    st, _ = _ws(p)
+    assert st == b.MOE_ERR_INVALID_ARG, (bad, lib.moe_last_error())
+    assert lib.moe_last_error() != b""
+
+
+def test_reserved_field_and_null_params(lib):
+    p = hm.gate_params(100, 256, 8, 1, 20, 0)
+    p.reserved = 1
+    assert _ws(p)[0] == b.MOE_ERR_INVALID_ARG
+    n = ctypes.c_size_t(0)
+    assert lib.moe_gate_workspace_size(None, ctypes.byref(n)) == b.MOE_ERR_INVALID_ARG
+    assert lib.moe_gate(None, *([None] * 11), None, 0, None) == b.MOE_ERR_INVALID_ARG
+
+
+def test_row_size_must_be_16_byte_multiple(lib):
+    p = hm.gate_params(100, 4, 8, 1, 20, 0, dtype=b.MOE_BF16)        # 8-byte rows
+    assert _ws(p)[0] == b.MOE_ERR_UNSUPPORTED
+    lay = b.Layout(100, 6, 8, 1, 20, b.MOE_F32)                         # 24-byte rows
+    st = lib.moe_dispatch(ctypes.byref(lay), 16, 16, 16, None)
+    assert st == b.MOE_ERR_UNSUPPORTED
+
+
+# fake, never dereferenced device addresses: validation fails before any HIP call
+A16 = 0x7f0000000000
+A4 = A16 + 4
+
+
+def test_gate_pointer_checks(lib):
+    p = hm.gate_params(100, 256, 8, 1, 20, 0)
+    call = lambda **kw: lib.moe_gate(ctypes.byref(p), kw.get("x", A16), kw.get("wg", A16), kw.get("bias"),
+                                     kw.get("tok"), kw.get("logits"), kw.get("ids", A16), kw.get("slots", A16),
+                                     kw.get("w", A16), kw.get("counts", A16), kw.get("demand"),
+                                     kw.get("src", A16), kw.get("ws", A16), kw.get("wsb", 1 << 20), None)
+    assert call(x=None) == b.MOE_ERR_INVALID_ARG
+    assert call(x=A4) == b.MOE_ERR_UNSUPPORTED                     # x must be 16-byte aligned
+    assert call(ids=None) == b.MOE_ERR_INVALID_ARG
+    assert call(ids=A16 + 2) == b.MOE_ERR_INVALID_ARG              # int32 arrays 4-byte aligned
+    assert call(tok=A16) == b.MOE_ERR_INVALID_ARG                  # token ids only for HASH
+    assert call(ws=None) == b.MOE_ERR_WORKSPACE
+    assert call(wsb=16) == b.MOE_ERR_WORKSPACE
+    ph = hm.gate_params(100, 0, 8, 1, 20, 2)
+    assert lib.moe_gate(ctypes.byref(ph), A16, None, None, A16, None, A16, A16, A16, A16, None, A16, A16,
+                        1 << 20, None) == b.MOE_ERR_INVALID_ARG  # HASH takes no x
+    pl = hm.gate_params(100, 0, 8, 1, 20, 0, logits_in=1)
+    assert lib.moe_gate(ctypes.byref(pl), None, None, None, None, None, A16, A16, A16, A16, None, A16, A16,
+                        1 << 20, None) == b.MOE_ERR_INVALID_ARG  # logits required as input
+
+
+def test_layout_pointer_checks(lib):
+    lay = b.Layout(100, 256, 8, 2, 20, b.MOE_BF16)
+    assert lib.moe_dispatch(None, A16, A16, A16, None) == b.MOE_ERR_INVALID_ARG
+    assert lib.moe_dispatch(ctypes.byref(lay), A16, A16, A16 + 8, None) == b.MOE_ERR_UNSUPPORTED
+    assert lib.moe_dispatch(ctypes.byref(lay), None, A16, A16, None) == b.MOE_ERR_INVALID_ARG
+    assert lib.moe_combine(ctypes.byref(lay), A16, A16, A16, None, A16, None) == b.MOE_ERR_INVALID_ARG
+    assert lib.moe_dispatch_bwd(ctypes.byref(lay), A16, None, A16, A16, None) == b.MOE_ERR_INVALID_ARG
+    # combine_bwd: ye and slots go with dw
+    assert lib.moe_combine_bwd(ctypes.byref(lay), A16, A16, None, A16, A16, A16, None, None) == b.MOE_ERR_INVALID_ARG
+    assert lib.moe_combine_bwd(ctypes.byref(lay), A16, None, A16, A16, A16, A16, A16, None) == b.MOE_ERR_INVALID_ARG
+    bad = b.Layout(100, 256, 8, 9, 20, b.MOE_BF16)
+    assert lib.moe_combine(ctypes.byref(bad), A16, A16, A16, A16, A16, None) == b.MOE_ERR_INVALID_ARG
+
+
+def test_binding_rejects_cpu_tensors(lib):
+    import torch
+    x = torch.zeros(4, 8)
+    with pytest.raises(ValueError):
+        hm.dispatch(x, torch.zeros((2, 2), dtype=torch.int32), 1)

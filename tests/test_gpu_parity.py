@@ -1,0 +1,235 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle on the
+same seeded inputs.  Integer routing and the dispatch copy are bit-exact;
+floating-point outputs are within rtol * (sum of |terms|), rtol 1e-5 for fp32
+and 2e-2 for bf16 outputs."""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2203_14685_amd as hm
+from paper_2203_14685_amd import workloads as wl
+
+from _parity import (RTOL, announce, assert_close, assert_equal, check_gate, check_layout_ops, decode,
+                     gpu_gate)
+
+pytestmark = pytest.mark.gpu
+
+W = wl.WORKLOADS
+
+
+def cap(cf, k, S, E):
+    return int(math.ceil(cf * k * S / E))
+
+
+@pytest.fixture(autouse=True, scope="module")
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    hm.load()
+    yield
+
+
+# ------------------------------------------------------------------ reduced sizes
+
+SMALL = [
+    # (workload, S, d): several 256-token blocks plus a ragged tail
+    (1, 1000, 256),
+    (2, 1000, 1024),
+    (3, 1000, 2048),
+    (4, 1000, 2048),
+    (5, 3000, 4096),
+]
+
+
+@pytest.mark.parametrize("wid,S,d", SMALL)
+def test_small_workload_parity(wid, S, d):
+    w = W[wid]
+    E, k = w["E"], w["k"]
+    C = cap(w["cf"], k, S, E)
+    announce(f"small workload {wid} S={S} d={d} E={E} k={k} C={C}")
+    inp = wl.make_inputs(w, S=S, d=d, seed=0)
+    g = gpu_gate(w, inp, E, k, C, w["kind"], w["normalize"])
+    ref, st = check_gate(w, inp, g, E, k, C, w["kind"], w["normalize"])
+    st.update(check_layout_ops(w, inp["x"], g["ids"], g["slots"], g["weights"], g["slot_src"], E, C, k))
+    print(f"[stats] workload {wid}: {st}", flush=True)
+
+
+# ------------------------------------------------------------------ routing edge cases
+
+def _logits_case(S, E, k, kind, normalize, C, L, dtype="f32"):
+    w = dict(dtype=dtype)
+    g = gpu_gate(w, None, E, k, C, kind, normalize, logits=L.astype(np.float32))
+    check_gate(w, None, g, E, k, C, kind, normalize, logits_in=L.astype(np.float32))
+    return g
+
+
+@pytest.mark.parametrize("E,k,kind,normalize", [
+    (5, 1, 0, 0), (5, 2, 0, 1), (12, 3, 0, 1), (16, 2, 0, 0), (64, 8, 0, 1), (1024, 8, 0, 0),
+    (1024, 1, 0, 1), (12, 4, 1, 0), (64, 4, 1, 0), (1024, 8, 1, 0), (1, 1, 0, 0), (3, 3, 0, 1),
+])
+def test_dense_ties_logits_in(E, k, kind, normalize):
+    S = 700
+    announce(f"dense ties E={E} k={k} kind={kind} normalize={normalize}")
+    rng = np.random.default_rng(E * 31 + k)
+    L = rng.integers(0, 3, size=(S, E)).astype(np.float32)
+    for C in (1, 7, cap(1.0, k, S, E), S * k):
+        _logits_case(S, E, k, kind, normalize, C, L)
+
+
+def test_all_equal_logits_and_zero_signs():
+    S, E = 300, 8
+    announce("all-equal logits")
+    L = np.zeros((S, E), dtype=np.float32)
+    L[::2, :] = -0.0
+    g = _logits_case(S, E, 2, 0, 1, S * 2, L)
+    assert (g["ids"][:, 0] == 0).all() and (g["ids"][:, 1] == 1).all()
+    g = _logits_case(S, E, 1, 0, 0, 10, L)
+    assert (g["counts"] == [10, 0, 0, 0, 0, 0, 0, 0]).all()
+
+
+def test_capacity_zero_and_empty_batch():
+    announce("C = 0 and S = 0")
+    rng = np.random.default_rng(1)
+    L = rng.standard_normal((100, 6)).astype(np.float32)
+    g = _logits_case(100, 6, 2, 0, 1, 0, L)
+    assert (g["slots"] == -1).all() and g["slot_src"].shape == (6, 0)
+    g = _logits_case(0, 6, 2, 0, 1, 5, np.zeros((0, 6), np.float32))
+    assert (g["slot_src"] == -1).all() and (g["counts"] == 0).all()
+    w = W[5]
+    tok = np.zeros(0, dtype=np.int32)
+    g = gpu_gate(w, dict(token_ids=tok), 128, 1, 4, hm.MOE_GATE_HASH, 0)
+    assert (g["slot_src"] == -1).all() and (g["demand"] == 0).all()
+
+
+def test_hash_edge_cases():
+    announce("hash E=1 and E=7")
+    w = W[5]
+    tok = wl.zipf_token_ids(1500, 50257, 1.1, 3)
+    for E, C in ((1, 10), (7, 100), (128, 1500)):
+        g = gpu_gate(w, dict(token_ids=tok), E, 1, C, hm.MOE_GATE_HASH, 0)
+        check_gate(w, dict(token_ids=tok), g, E, 1, C, hm.MOE_GATE_HASH, 0)
+        assert (g["weights"] == 1.0).all()
+
+
+@pytest.mark.parametrize("dtype,d,E,k", [("bf16", 8, 4, 2), ("f32", 4, 3, 1), ("bf16", 520, 6, 2),
+                                          ("f32", 260, 16, 4), ("bf16", 2056, 64, 1)])
+def test_projection_odd_shapes(dtype, d, E, k):
+    S = 517
+    announce(f"projection dtype={dtype} d={d} E={E} k={k}")
+    w = dict(kind=0, k=k, normalize=1, dtype=dtype, S=S, d=d, E=E, cf=1.0)
+    inp = wl.make_inputs(w, seed=5)
+    C = cap(1.0, k, S, E)
+    g = gpu_gate(w, inp, E, k, C, 0, 1)
+    check_gate(w, inp, g, E, k, C, 0, 1)
+    check_layout_ops(w, inp["x"], g["ids"], g["slots"], g["weights"], g["slot_src"], E, C, k, seed=9)
+
+
+def test_ktop1_projection_with_bias():
+    S, d, E, k = 600, 512, 24, 3
+    announce("kTop1 projection with bias")
+    w = dict(kind=1, k=k, normalize=0, dtype="bf16", S=S, d=d, E=E, cf=1.25, hot_experts=2, hot_bias=0.75)
+    inp = wl.make_inputs(w, seed=8)
+    C = cap(1.25, k, S, E)
+    g = gpu_gate(w, inp, E, k, C, 1, 0)
+    check_gate(w, inp, g, E, k, C, 1, 0)
+
+
+def test_determinism_and_guard_bands():
+    announce("determinism and guard bands")
+    w = W[2]
+    S, d, E, k = 1000, 1024, 16, 2
+    C = cap(1.25, k, S, E)
+    inp = wl.make_inputs(w, S=S, d=d, seed=2)
+    a = gpu_gate(w, inp, E, k, C, 0, 1)
+    b = gpu_gate(w, inp, E, k, C, 0, 1)
+    for key in a:
+        if a[key] is not None:
+            assert_equal(a[key], b[key], f"repeat {key}")
+    # outputs written into the middle of larger buffers leave the guard bands alone
+    pad = 64
+    x = wl.to_device(inp["x"], "bf16")
+    src = wl.to_device(a["slot_src"], "i32")
+    buf = torch.full((E * C * d + 2 * pad,), 7.0, dtype=torch.bfloat16, device="cuda")
+    xe = buf[pad:pad + E * C * d].view(E, C, d)
+    hm.moe_dispatch(hm.Layout(S, d, E, k, C, hm.MOE_BF16), x, src, xe)
+    torch.cuda.synchronize()
+    assert (buf[:pad] == 7.0).all() and (buf[-pad:] == 7.0).all()
+    assert_equal(wl.to_host(xe), oracle.dispatch(inp["x"], a["slot_src"], k), "dispatch into a view")
+
+
+# ------------------------------------------------------------------ full sizes, sampled
+
+def _compact_combine(ye, ids, slots, w):
+    """Sub-problem holding only the expert rows the given tokens reference."""
+    n, k = ids.shape
+    d = ye.shape[2]
+    sub = np.zeros((n * k, 1, d), dtype=ye.dtype)
+    kept = slots >= 0
+    sub[kept.reshape(-1), 0] = ye[ids[kept], slots[kept]]
+    return sub, np.arange(n * k, dtype=np.int32).reshape(n, k), np.where(kept, 0, -1).astype(np.int32), w
+
+
+@pytest.mark.parametrize("wid", [1, 2, 3, 4, 5])
+def test_full_size_parity(wid):
+    w = W[wid]
+    S, d, E, k, C, dt = w["S"], w["d"], w["E"], w["k"], w["C"], w["dtype"]
+    assert C == oracle.capacity(w["cf"], k, S, E)
+    announce(f"full workload {wid}: {w['name']}")
+    inp = wl.make_inputs(w, seed=0)
+    g = gpu_gate(w, inp, E, k, C, w["kind"], w["normalize"])
+    ref, st = check_gate(w, inp, g, E, k, C, w["kind"], w["normalize"])
+    rng = np.random.default_rng(100 + wid)
+    x = wl.to_device(inp["x"], dt)
+    d_src = wl.to_device(g["slot_src"], "i32")
+    d_ids, d_slots = wl.to_device(g["ids"], "i32"), wl.to_device(g["slots"], "i32")
+    d_w = wl.to_device(g["weights"], "f32")
+    # dispatch: sampled rows bit-exact, plus every empty row zero
+    xe = hm.dispatch(x, d_src, k)
+    rows = rng.choice(E * C, size=min(E * C, 2048), replace=False)
+    rows = np.concatenate([rows, np.arange(C)])               # all of expert 0
+    got = wl.to_host(xe.view(E * C, d)[torch.from_numpy(rows).cuda()])
+    want = oracle.dispatch(inp["x"], g["slot_src"].reshape(-1)[rows][None, :], k)[0]
+    assert_equal(got, want, "dispatch sampled rows")
+    empty = torch.from_numpy(g["slot_src"].reshape(-1) < 0).cuda()
+    if empty.any():
+        assert (xe.view(E * C, d)[empty] == 0).all()
+    # combine with identity experts (ye = xe) on sampled tokens
+    ye_host = oracle.dispatch(inp["x"], g["slot_src"], k)
+    ye = wl.to_device(ye_host, dt)
+    y = hm.combine(ye, d_ids, d_slots, d_w)
+    toks = rng.choice(S, size=min(S, 1024), replace=False)
+    sub = _compact_combine(ye_host, g["ids"][toks], g["slots"][toks], g["weights"][toks].astype(np.float64))
+    y_ref, y_mag = oracle.combine(*sub, dt)
+    st["combine_err"] = assert_close(decode(wl.to_host(y[torch.from_numpy(toks).cuda()]), dt), decode(y_ref, dt),
+                                     y_mag, RTOL[dt], "combine sampled tokens")
+    # backward of dispatch and combine on sampled outputs
+    dx = hm.dispatch_bwd(ye, d_ids, d_slots)
+    sub = _compact_combine(ye_host, g["ids"][toks], g["slots"][toks], None)
+    dx_ref, dx_mag = oracle.dispatch_bwd(sub[0], sub[1], sub[2], dt)
+    st["dispatch_bwd_err"] = assert_close(decode(wl.to_host(dx[torch.from_numpy(toks).cuda()]), dt),
+                                          decode(dx_ref, dt), dx_mag, RTOL[dt], "dispatch_bwd sampled tokens")
+    dy_host = wl.make_rows((S, d), dt, 2)
+    dye, dw = hm.combine_bwd(wl.to_device(dy_host, dt), d_src, d_w, ye=ye, slots=d_slots, want_dw=True)
+    src = g["slot_src"].reshape(-1)[rows]
+    full = src >= 0
+    s_of = np.where(full, src // k, 0)
+    dy_sub = dy_host[s_of]
+    src_sub = np.where(full, np.arange(len(rows)) * k + src % k, -1)[None, :]
+    w_sub = np.zeros((len(rows), k), dtype=np.float32)
+    w_sub[np.arange(len(rows)), np.where(full, src % k, 0)] = g["weights"].reshape(-1)[np.where(full, src, 0)]
+    ye_sub = ye_host.reshape(E * C, d)[rows][None]
+    dye_ref, dye_mag, dw_ref, dw_mag = oracle.combine_bwd(dy_sub, ye_sub, src_sub, w_sub, k, dt)
+    got_dye = wl.to_host(dye.view(E * C, d)[torch.from_numpy(rows).cuda()])
+    st["combine_bwd_dye_err"] = assert_close(decode(got_dye, dt), decode(dye_ref[0], dt), dye_mag[0], RTOL[dt],
+                                             "combine_bwd sampled dye rows")
+    dw_h = wl.to_host(dw)
+    r_of = np.where(full, src % k, 0)
+    st["combine_bwd_dw_err"] = assert_close(dw_h[s_of[full], r_of[full]], dw_ref[np.arange(len(rows))[full], r_of[full]],
+                                            dw_mag[np.arange(len(rows))[full], r_of[full]], RTOL["f32"], "dw sampled")
+    assert (dw_h[g["slots"] < 0] == 0).all()
+    torch.cuda.synchronize()
+    print(f"[stats] full workload {wid}: {st}", flush=True)

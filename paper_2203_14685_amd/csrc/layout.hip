@@ -5,21 +5,28 @@
 // One wavefront owns one output row and walks it in 16-byte chunks (64 lanes x
 // 16 B = 1 KiB per instruction), issuing up to kUnroll loads per lane before
 // the first store so that enough bytes are in flight to cover HBM latency.
-// Expert buffers ([E, C, d], written once and read by a later kernel) are
-// written with non-temporal stores.
+// Every output row is written with non-temporal stores: the buffers are far
+// larger than the 256 MB Infinity Cache, and plain stores leave dirty lines there
+// whose write-back then slows whichever kernel runs next (measured: dispatch
+// after a plain-store producer ~25% slower than after a streaming one).
 #include "common.hpp"
 #include "kernels.hpp"
 
 namespace hetumoe {
 
 constexpr int kUnroll = 8;
+// Waves per block, one row per wave.  Large blocks measured faster on MI355X for
+// these gathers (16 waves for the [E,C,d] writers); the combine kernels keep 4
+// so that their fp32 accumulators fit the register budget without spilling.
+constexpr int kWideWaves = 16;
+constexpr int kCombineWaves = 4;
 
 __device__ __forceinline__ void store_nt(u32x4* p, const u32x4& v) { __builtin_nontemporal_store(v, p); }
 
 // ---------------------------------------------------------------- dispatch
 // xe[row] = x[slot_src[row] / k], or zeros for an empty slot.
-__global__ __launch_bounds__(kBlock) void dispatch_kernel(RowArgs a) {
-  const int64_t row = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + threadIdx.x / kWave;
+__global__ __launch_bounds__(kWideWaves * kWave) void dispatch_kernel(RowArgs a) {
+  const int64_t row = static_cast<int64_t>(blockIdx.x) * kWideWaves + threadIdx.x / kWave;
   if (row >= a.rows) return;
   const int lane = lane_id();
   const int nch = a.nch;
@@ -52,9 +59,9 @@ __global__ __launch_bounds__(kBlock) void dispatch_kernel(RowArgs a) {
 // dx[s] = sum_{r kept} dxe[ids[s,r], slots[s,r]]        (!WEIGHTED)
 // fp32 accumulation in r order, one rounding to T.
 template <typename T, bool WEIGHTED>
-__global__ __launch_bounds__(kBlock) void combine_kernel(RowArgs a) {
+__global__ __launch_bounds__(kCombineWaves * kWave) void combine_kernel(RowArgs a) {
   constexpr int kEl = Chunk<T>::kElems;
-  const int64_t s = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + threadIdx.x / kWave;
+  const int64_t s = static_cast<int64_t>(blockIdx.x) * kCombineWaves + threadIdx.x / kWave;
   if (s >= a.rows) return;
   const int lane = lane_id();
   const int nch = a.nch, k = a.k;
@@ -93,7 +100,7 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(RowArgs a) {
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       const int i = base + u * kWave + lane;
-      if (i < nch) out[i] = Chunk<T>::pack(acc[u]);
+      if (i < nch) store_nt(out + i, Chunk<T>::pack(acc[u]));
     }
   }
 }
@@ -103,16 +110,16 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(RowArgs a) {
 // with DW, dw[src] = <dy[src / k], ye[row]>.  Blocks past the row blocks clear
 // dw of dropped choices.
 template <typename T, bool DW>
-__global__ __launch_bounds__(kBlock) void combine_bwd_kernel(RowArgs a, int64_t row_blocks) {
+__global__ __launch_bounds__(kWideWaves * kWave) void combine_bwd_kernel(RowArgs a, int64_t row_blocks) {
   constexpr int kEl = Chunk<T>::kElems;
   if (static_cast<int64_t>(blockIdx.x) >= row_blocks) {
     if constexpr (DW) {
-      const int64_t i = (static_cast<int64_t>(blockIdx.x) - row_blocks) * kBlock + threadIdx.x;
+      const int64_t i = (static_cast<int64_t>(blockIdx.x) - row_blocks) * (kWideWaves * kWave) + threadIdx.x;
       if (i < static_cast<int64_t>(a.S) * a.k && a.slots[i] < 0) a.dw[i] = 0.f;
     }
     return;
   }
-  const int64_t row = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + threadIdx.x / kWave;
+  const int64_t row = static_cast<int64_t>(blockIdx.x) * kWideWaves + threadIdx.x / kWave;
   if (row >= a.rows) return;
   const int lane = lane_id();
   const int nch = a.nch;
@@ -163,19 +170,19 @@ __global__ __launch_bounds__(kBlock) void combine_bwd_kernel(RowArgs a, int64_t 
 }
 
 // ---------------------------------------------------------------- launchers
-static inline unsigned blocks_for_rows(int64_t rows) {
-  return static_cast<unsigned>((rows + kWavesPerBlock - 1) / kWavesPerBlock);
+static inline unsigned blocks_for_rows(int64_t rows, int waves) {
+  return static_cast<unsigned>((rows + waves - 1) / waves);
 }
 
 hipError_t launch_dispatch(const RowArgs& a, hipStream_t st) {
   if (a.rows == 0) return hipSuccess;
-  dispatch_kernel<<<dim3(blocks_for_rows(a.rows)), dim3(kBlock), 0, st>>>(a);
+  dispatch_kernel<<<dim3(blocks_for_rows(a.rows, kWideWaves)), dim3(kWideWaves * kWave), 0, st>>>(a);
   return hipGetLastError();
 }
 
 hipError_t launch_combine(const RowArgs& a, bool weighted, hipStream_t st) {
   if (a.rows == 0) return hipSuccess;
-  const dim3 grid(blocks_for_rows(a.rows)), block(kBlock);
+  const dim3 grid(blocks_for_rows(a.rows, kCombineWaves)), block(kCombineWaves * kWave);
   if (a.dtype == 1) {
     if (weighted) combine_kernel<bf16_t, true><<<grid, block, 0, st>>>(a);
     else combine_kernel<bf16_t, false><<<grid, block, 0, st>>>(a);
@@ -187,10 +194,11 @@ hipError_t launch_combine(const RowArgs& a, bool weighted, hipStream_t st) {
 }
 
 hipError_t launch_combine_bwd(const RowArgs& a, hipStream_t st) {
-  const int64_t row_blocks = blocks_for_rows(a.rows);
-  const int64_t dw_blocks = a.dw ? (static_cast<int64_t>(a.S) * a.k + kBlock - 1) / kBlock : 0;
+  constexpr int kThreads = kWideWaves * kWave;
+  const int64_t row_blocks = blocks_for_rows(a.rows, kWideWaves);
+  const int64_t dw_blocks = a.dw ? (static_cast<int64_t>(a.S) * a.k + kThreads - 1) / kThreads : 0;
   if (row_blocks + dw_blocks == 0) return hipSuccess;
-  const dim3 grid(static_cast<unsigned>(row_blocks + dw_blocks)), block(kBlock);
+  const dim3 grid(static_cast<unsigned>(row_blocks + dw_blocks)), block(kThreads);
   if (a.dtype == 1) {
     if (a.dw) combine_bwd_kernel<bf16_t, true><<<grid, block, 0, st>>>(a, row_blocks);
     else combine_bwd_kernel<bf16_t, false><<<grid, block, 0, st>>>(a, row_blocks);

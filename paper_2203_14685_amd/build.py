@@ -15,7 +15,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libhetumoe.so")
 
-SOURCES = ["capi.hip", "gate.hip", "layout.hip"]
+SOURCES = ["route_valu_f32.hip", "route_valu_bf16.hip", "route_mfma.hip", "gate.hip", "layout.hip", "capi.hip"]
 
 # -packed-fp32-ops: no v_pk_{add,mul,fma}_f32 in generated code.
 HIPCC_FLAGS = [
@@ -33,21 +33,42 @@ def hipcc():
     raise RuntimeError("hipcc not found: the HIP library cannot be built")
 
 
-def build(verbose=True):
-    """Compile every HIP source into paper_2203_14685_amd/libhetumoe.so."""
-    srcs = [os.path.join(CSRC, s) for s in SOURCES]
-    tmp = LIB + ".tmp"
-    cmd = [hipcc(), *HIPCC_FLAGS, "-I", INCLUDE, "-I", CSRC, *srcs, "-o", tmp]
-    t0 = time.time()
-    if verbose:
-        print("[build]", " ".join(cmd), flush=True)
+def _run(cmd):
     res = subprocess.run(cmd, capture_output=True, text=True)
-    if res.returncode != 0:
-        sys.stderr.write(res.stdout + res.stderr)
-        raise RuntimeError(f"hipcc failed with exit code {res.returncode}")
+    return res.returncode, res.stdout + res.stderr
+
+
+def build(verbose=True):
+    """Compile every HIP source (in parallel) and link paper_2203_14685_amd/libhetumoe.so."""
+    from concurrent.futures import ThreadPoolExecutor
+    cc = hipcc()
+    t0 = time.time()
+    objdir = os.path.join(PKG, "_build")
+    os.makedirs(objdir, exist_ok=True)
+    jobs = []
+    for src in SOURCES:
+        obj = os.path.join(objdir, src.replace(".hip", ".o"))
+        flags = [f for f in HIPCC_FLAGS if f != "-shared"]
+        jobs.append((obj, [cc, *flags, "-I", INCLUDE, "-I", CSRC, "-c", os.path.join(CSRC, src), "-o", obj]))
+    if verbose:
+        print(f"[build] {cc} {' '.join(HIPCC_FLAGS)} ... ({len(jobs)} sources)", flush=True)
+    workers = min(len(jobs), max(1, int(os.environ.get("MAX_JOBS", os.cpu_count() or 1))))
+    with ThreadPoolExecutor(max_workers=workers) as ex:
+        results = list(ex.map(lambda j: _run(j[1]), jobs))
+    logs = []
+    for (obj, cmd), (rc, out) in zip(jobs, results):
+        if rc != 0:
+            sys.stderr.write(" ".join(cmd) + "\n" + out)
+            raise RuntimeError(f"hipcc failed on {cmd[-3]} with exit code {rc}")
+        logs.append(out)
+    tmp = LIB + ".tmp"
+    rc, out = _run([cc, "--offload-arch=gfx950", "-shared", "-fPIC", *[o for o, _ in jobs], "-o", tmp])
+    if rc != 0:
+        sys.stderr.write(out)
+        raise RuntimeError(f"link failed with exit code {rc}")
     os.replace(tmp, LIB)
     if verbose:
-        warn = [ln for ln in res.stderr.splitlines() if "packed-fp32-ops" not in ln and ln.strip()]
+        warn = [ln for out in logs for ln in out.splitlines() if "packed-fp32-ops" not in ln and ln.strip()]
         if warn:
             sys.stderr.write("\n".join(warn) + "\n")
         print(f"[build] {LIB} in {time.time() - t0:.1f}s", flush=True)

@@ -8,9 +8,9 @@
 namespace hetumoe {
 
 constexpr int kWave = 64;           // CDNA wavefront width
-constexpr int kBlock = 256;         // threads per block for every kernel here
+constexpr int kBlock = 256;         // default threads per block
 constexpr int kWavesPerBlock = kBlock / kWave;
-constexpr int kTokensPerHistBlock = 256;  // granularity of the capacity scan (one token per thread)
+constexpr int kTokensPerHistBlock = 64;  // capacity-scan granularity: one wave block of 64 tokens
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 

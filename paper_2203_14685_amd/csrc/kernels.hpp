@@ -17,12 +17,12 @@ struct RouteArgs {
   float* logits;            // [S, E]: input (logits_in), output, or null
   int32_t* ids;             // [S, k]
   float* weights;           // [S, k]
-  int32_t* hist;            // [k, nb, E] workspace
+  int32_t* hist;            // [k, E, nb] workspace (nb = 64-token wave blocks)
 };
 
 struct ScanArgs {
   int E, k, nb, C;
-  int32_t* hist;     // [k, nb, E]: counts in, exclusive offsets out
+  int32_t* hist;     // [k, E, nb]: counts in, exclusive offsets out
   int32_t* counts;   // [E]
   int32_t* demand;   // [E] or null
   int32_t* slot_src; // [E, C]
@@ -31,7 +31,7 @@ struct ScanArgs {
 struct AssignArgs {
   int S, E, k, nb, C;
   const int32_t* ids;  // [S, k]
-  const int32_t* offs; // [k, nb, E]
+  const int32_t* offs; // [k, E, nb]
   int32_t* slots;      // [S, k]
   int32_t* slot_src;   // [E, C]
 };
@@ -51,6 +51,10 @@ struct RowArgs {
 };
 
 hipError_t launch_route(const RouteArgs& a, hipStream_t st);
+hipError_t launch_route_valu_f32(const RouteArgs& a, hipStream_t st);
+hipError_t launch_route_valu_bf16(const RouteArgs& a, hipStream_t st);
+hipError_t launch_route_mfma(const RouteArgs& a, hipStream_t st);
+bool route_uses_mfma(const RouteArgs& a);
 hipError_t launch_scan(const ScanArgs& a, hipStream_t st);
 hipError_t launch_assign(const AssignArgs& a, hipStream_t st);
 hipError_t launch_dispatch(const RowArgs& a, hipStream_t st);

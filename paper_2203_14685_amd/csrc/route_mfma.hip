@@ -1,0 +1,155 @@
+// Route kernel on the matrix cores: the bf16 logit projection x.W of Eq. 1 on
+// v_mfma_f32_16x16x32_bf16, with softmax and expert selection in the epilogue.
+#include "select.hpp"
+
+namespace hetumoe {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// ---------------------------------------------------------------- MFMA route (bf16)
+// 64 tokens per block, 4 waves; wave w computes the logits of tokens
+// [16w, 16w+16) for all E = 16*NT experts with v_mfma_f32_16x16x32_bf16
+// (M = tokens, N = experts, K = d).  Per K chunk of KC columns, W[kc:kc+KC, :]
+// is staged transposed in LDS (B fragments are 16-byte LDS reads) while every
+// lane streams 2*KC/4 contiguous bytes of its token's row of x (A fragments),
+// prefetched one chunk ahead.  Inside a chunk, lane group g = lane/16 supplies
+// the columns [kc + (KC/4)*g, kc + (KC/4)*(g+1)); A and B use the same column
+// order, so each MFMA sums a fixed permutation of 32 columns of the chunk.
+// The block's 64 x E logits (+ bias) then go to LDS and wave 0 selects, one
+// token per lane.
+constexpr int kMfmaTokens = 64;
+
+template <int NT, int KC, int KMAX, bool KTOP1>
+__global__ __launch_bounds__(kBlock) void route_mfma_kernel(RouteArgs a) {
+  constexpr int E = NT * 16;
+  constexpr int KG = KC / 4;        // columns per lane group per chunk
+  constexpr int KSTEPS = KG / 8;    // MFMAs per N tile per chunk
+  constexpr int LDW = KC + 8;       // padded LDS row (bf16 elements) of W^T
+  __shared__ __align__(16) uint16_t wsT[E * LDW];
+  __shared__ float lg[kMfmaTokens * (E + 1)];
+  __shared__ int hist_lds[E];
+
+  const int tid = threadIdx.x;
+  const int w = tid / kWave;
+  const int lane = lane_id();
+  const int g = lane / 16, m = lane % 16;
+  const int d = a.d;
+  const int64_t tok0 = static_cast<int64_t>(blockIdx.x) * kMfmaTokens;
+  const int64_t arow = tok0 + w * 16 + m;  // token of this lane's A fragment rows
+  const bool arow_ok = arow < a.S;
+  const uint16_t* x = reinterpret_cast<const uint16_t*>(a.x);
+  const uint16_t* wg = reinterpret_cast<const uint16_t*>(a.wg);
+  const u32x4* xa = reinterpret_cast<const u32x4*>(x + arow * d + KG * g);
+
+  f32x4 acc[NT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  constexpr int kVec = KG / 8;  // 16-byte loads per lane per chunk
+  u32x4 cur[kVec], nxt[kVec];
+#pragma unroll
+  for (int v = 0; v < kVec; ++v) cur[v] = arow_ok ? xa[v] : u32x4{0u, 0u, 0u, 0u};
+
+  for (int kc = 0; kc < d; kc += KC) {
+    __syncthreads();  // wsT of the previous chunk consumed
+    // stage W[kc:kc+KC, 0:E] transposed: each thread moves 8 experts of one column
+    for (int t = tid; t < KC * (E / 8); t += kBlock) {
+      const int kk = t / (E / 8), e8 = (t % (E / 8)) * 8;
+      const u32x4 v = *reinterpret_cast<const u32x4*>(wg + static_cast<int64_t>(kc + kk) * E + e8);
+      const uint32_t p[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        wsT[(e8 + 2 * q) * LDW + kk] = static_cast<uint16_t>(p[q] & 0xffffu);
+        wsT[(e8 + 2 * q + 1) * LDW + kk] = static_cast<uint16_t>(p[q] >> 16);
+      }
+    }
+    // prefetch the next chunk of x while this one is multiplied
+    const bool more = kc + KC < d;
+#pragma unroll
+    for (int v = 0; v < kVec; ++v)
+      nxt[v] = (arow_ok && more) ? xa[(kc + KC) / 8 + v] : u32x4{0u, 0u, 0u, 0u};
+    __syncthreads();
+#pragma unroll
+    for (int ks = 0; ks < KSTEPS; ++ks) {
+      const bf16x8 av = __builtin_bit_cast(bf16x8, cur[ks]);
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        const u32x4 braw = *reinterpret_cast<const u32x4*>(&wsT[(nt * 16 + m) * LDW + KG * g + 8 * ks]);
+        acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf16x8, braw), acc[nt], 0, 0, 0);
+      }
+    }
+#pragma unroll
+    for (int v = 0; v < kVec; ++v) cur[v] = nxt[v];
+  }
+
+  // logits (+ bias) of the block's 64 tokens into LDS: lane holds rows 4g+i of
+  // the wave's 16 tokens, column m of each N tile
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    const int e = nt * 16 + m;
+    const float b = a.bias ? a.bias[e] : 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) lg[(w * 16 + 4 * g + i) * (E + 1) + e] = acc[nt][i] + b;
+  }
+  __syncthreads();
+  if (a.logits) {
+    for (int t = tid; t < kMfmaTokens * E; t += kBlock) {
+      const int r = t / E, e = t % E;
+      if (tok0 + r < a.S) a.logits[(tok0 + r) * E + e] = lg[r * (E + 1) + e];
+    }
+  }
+  const int64_t s = tok0 + lane;
+  const bool valid = (w == 0) && s < a.S;
+  if (valid) {
+    const float* row = &lg[lane * (E + 1)];
+    int32_t* my_ids = a.ids + s * a.k;
+    float* my_w = a.weights + s * a.k;
+    if constexpr (KTOP1) {
+      Ktop1State kt;
+      kt.init(E / a.k);
+      for (int e = 0; e < E; ++e) kt.push(row[e], e, my_ids, my_w);
+    } else {
+      TopkState<KMAX> tk;
+      tk.init();
+      for (int e = 0; e < E; ++e) tk.push(row[e], e);
+      tk.finish(a.k, a.normalize, my_ids, my_w);
+    }
+  }
+  wave_block_hist(hist_lds, w == 0, s, valid, blockIdx.x, a);
+}
+
+template <int NT, int KC, int KMAX, bool KTOP1>
+static hipError_t launch_mfma_t(const RouteArgs& a, hipStream_t st) {
+  route_mfma_kernel<NT, KC, KMAX, KTOP1><<<dim3(a.nb), dim3(kBlock), 0, st>>>(a);
+  return hipGetLastError();
+}
+
+template <int NT, int KC>
+static hipError_t launch_mfma_nt(const RouteArgs& a, hipStream_t st) {
+  if (a.kind == 1) return launch_mfma_t<NT, KC, 1, true>(a, st);
+  if (a.k == 1) return launch_mfma_t<NT, KC, 1, false>(a, st);
+  if (a.k == 2) return launch_mfma_t<NT, KC, 2, false>(a, st);
+  if (a.k <= 4) return launch_mfma_t<NT, KC, 4, false>(a, st);
+  return launch_mfma_t<NT, KC, 8, false>(a, st);
+}
+
+bool route_uses_mfma(const RouteArgs& a) {
+  return a.kind != 2 && !a.logits_in && a.dtype == 1 && a.E % 16 == 0 && a.E <= 128 &&
+         a.d % (a.E <= 64 ? 256 : 128) == 0 && (reinterpret_cast<uintptr_t>(a.wg) % 16) == 0;
+}
+
+hipError_t launch_route_mfma(const RouteArgs& a, hipStream_t st) {
+  switch (a.E / 16) {
+    case 1: return launch_mfma_nt<1, 256>(a, st);
+    case 2: return launch_mfma_nt<2, 256>(a, st);
+    case 3: return launch_mfma_nt<3, 256>(a, st);
+    case 4: return launch_mfma_nt<4, 256>(a, st);
+    case 5: return launch_mfma_nt<5, 128>(a, st);
+    case 6: return launch_mfma_nt<6, 128>(a, st);
+    case 7: return launch_mfma_nt<7, 128>(a, st);
+    default: return launch_mfma_nt<8, 128>(a, st);
+  }
+}
+
+}  // namespace hetumoe

@@ -58,7 +58,7 @@ def test_workspace_size(lib, S, E, k, kind):
     p = hm.gate_params(S, 256, E, k, 10, kind)
     st, n = _ws(p)
     assert st == 0
-    assert n == k * ((S + 255) // 256) * E * 4
+    assert n == k * ((S + 63) // 64) * E * 4
 
 
 BAD_PARAMS = [

@@ -128,6 +128,26 @@ def test_projection_odd_shapes(dtype, d, E, k):
     check_layout_ops(w, inp["x"], g["ids"], g["slots"], g["weights"], g["slot_src"], E, C, k, seed=9)
 
 
+@pytest.mark.parametrize("E,k,kind,normalize,d,bias", [
+    (16, 1, 1, 0, 256, False), (32, 2, 0, 1, 512, True), (48, 1, 0, 0, 256, False), (64, 4, 1, 0, 768, True),
+    (80, 3, 0, 1, 256, False), (96, 8, 0, 0, 128, True), (112, 2, 0, 0, 384, False), (128, 8, 1, 0, 256, True),
+    (128, 2, 0, 1, 384, False),
+])
+def test_mfma_projection_shapes(E, k, kind, normalize, d, bias):
+    """bf16 shapes that take the matrix-core route kernel (E a multiple of 16 up
+    to 128, d a multiple of the K chunk), several wave blocks plus a ragged tail."""
+    S = 300
+    announce(f"mfma projection E={E} k={k} kind={kind} d={d} bias={bias}")
+    w = dict(kind=kind, k=k, normalize=normalize, dtype="bf16", S=S, d=d, E=E, cf=1.0)
+    if bias:
+        w.update(hot_experts=3, hot_bias=0.5)
+    inp = wl.make_inputs(w, seed=E + k)
+    C = cap(1.0, k, S, E)
+    g = gpu_gate(w, inp, E, k, C, kind, normalize)
+    st = check_gate(w, inp, g, E, k, C, kind, normalize)[1]
+    print(f"[stats] mfma E={E}: {st}", flush=True)
+
+
 def test_ktop1_projection_with_bias():
     S, d, E, k = 600, 512, 24, 3
     announce("kTop1 projection with bias")

@@ -8,27 +8,50 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 // ---------------------------------------------------------------- MFMA route (bf16)
+// W^T [E, d] is written once per call by transpose_wg_kernel (into the
+// workspace) so that every block can stage it with 16-byte copies.
+//
 // 64 tokens per block, 4 waves; wave w computes the logits of tokens
 // [16w, 16w+16) for all E = 16*NT experts with v_mfma_f32_16x16x32_bf16
-// (M = tokens, N = experts, K = d).  Per K chunk of KC columns, W[kc:kc+KC, :]
-// is staged transposed in LDS (B fragments are 16-byte LDS reads) while every
-// lane streams 2*KC/4 contiguous bytes of its token's row of x (A fragments),
-// prefetched one chunk ahead.  Inside a chunk, lane group g = lane/16 supplies
-// the columns [kc + (KC/4)*g, kc + (KC/4)*(g+1)); A and B use the same column
-// order, so each MFMA sums a fixed permutation of 32 columns of the chunk.
-// The block's 64 x E logits (+ bias) then go to LDS and wave 0 selects, one
-// token per lane.
+// (M = tokens, N = experts, K = d).  Per K chunk of KC columns, W^T[:, kc:kc+KC]
+// sits in LDS (B fragments are 16-byte LDS reads) and every lane holds 2*KC/4
+// contiguous bytes of its token's row of x (A fragments).  The next chunk of
+// both is loaded into registers while the current one is multiplied.  Inside a
+// chunk, lane group g = lane/16 supplies the columns [kc + (KC/4)*g,
+// kc + (KC/4)*(g+1)); A and B use the same column order, so each MFMA sums a
+// fixed permutation of 32 columns of the chunk.  The block's 64 x E logits
+// (+ bias) then go to LDS and wave 0 selects, one token per lane.
 constexpr int kMfmaTokens = 64;
+
+__global__ __launch_bounds__(kBlock) void transpose_wg_kernel(const uint16_t* __restrict__ wg, uint16_t* __restrict__ wt,
+                                                              int d, int E) {
+  __shared__ uint16_t tile[64][65];
+  const int j0 = blockIdx.x * 64, e0 = blockIdx.y * 64;
+  for (int t = threadIdx.x; t < 64 * 64; t += kBlock) {
+    const int jj = t / 64, ee = t % 64;
+    if (j0 + jj < d && e0 + ee < E) tile[jj][ee] = wg[static_cast<int64_t>(j0 + jj) * E + e0 + ee];
+  }
+  __syncthreads();
+  for (int t = threadIdx.x; t < 64 * 64; t += kBlock) {
+    const int ee = t / 64, jj = t % 64;
+    if (j0 + jj < d && e0 + ee < E) wt[static_cast<int64_t>(e0 + ee) * d + j0 + jj] = tile[jj][ee];
+  }
+}
 
 template <int NT, int KC, int KMAX, bool KTOP1>
 __global__ __launch_bounds__(kBlock) void route_mfma_kernel(RouteArgs a) {
   constexpr int E = NT * 16;
-  constexpr int KG = KC / 4;        // columns per lane group per chunk
-  constexpr int KSTEPS = KG / 8;    // MFMAs per N tile per chunk
-  constexpr int LDW = KC + 8;       // padded LDS row (bf16 elements) of W^T
+  constexpr int KG = KC / 4;                 // columns per lane group per chunk
+  constexpr int KSTEPS = KG / 8;             // MFMAs per N tile per chunk
+  constexpr int LDW = KC + 8;                // padded LDS row (bf16 elements) of W^T
+  constexpr int WPIECES = E * KC / 8;        // 16-byte pieces of a W^T chunk
+  constexpr int WVEC = WPIECES / kBlock;     // per thread
+  constexpr int XVEC = KG / 8;               // 16-byte pieces of x per lane per chunk
+  static_assert(WPIECES % kBlock == 0, "chunk must split evenly over the block");
+  static_assert(E * LDW * 2 >= kMfmaTokens * (E + 1) * 4, "logits reuse the W^T buffer");
   __shared__ __align__(16) uint16_t wsT[E * LDW];
-  __shared__ float lg[kMfmaTokens * (E + 1)];
   __shared__ int hist_lds[E];
+  float* lg = reinterpret_cast<float*>(wsT);  // after the K loop: [64][E + 1] logits
 
   const int tid = threadIdx.x;
   const int w = tid / kWave;
@@ -38,49 +61,52 @@ __global__ __launch_bounds__(kBlock) void route_mfma_kernel(RouteArgs a) {
   const int64_t tok0 = static_cast<int64_t>(blockIdx.x) * kMfmaTokens;
   const int64_t arow = tok0 + w * 16 + m;  // token of this lane's A fragment rows
   const bool arow_ok = arow < a.S;
-  const uint16_t* x = reinterpret_cast<const uint16_t*>(a.x);
-  const uint16_t* wg = reinterpret_cast<const uint16_t*>(a.wg);
-  const u32x4* xa = reinterpret_cast<const u32x4*>(x + arow * d + KG * g);
+  const u32x4* xa = reinterpret_cast<const u32x4*>(reinterpret_cast<const uint16_t*>(a.x) + arow * d + KG * g);
+  const uint16_t* wt = a.wt;
 
   f32x4 acc[NT];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  constexpr int kVec = KG / 8;  // 16-byte loads per lane per chunk
-  u32x4 cur[kVec], nxt[kVec];
+  u32x4 xcur[XVEC], xnxt[XVEC], wreg[WVEC];
+  const u32x4 zero = {0u, 0u, 0u, 0u};
 #pragma unroll
-  for (int v = 0; v < kVec; ++v) cur[v] = arow_ok ? xa[v] : u32x4{0u, 0u, 0u, 0u};
+  for (int v = 0; v < XVEC; ++v) xcur[v] = arow_ok ? xa[v] : zero;
+#pragma unroll
+  for (int v = 0; v < WVEC; ++v) {
+    const int p = tid + v * kBlock, e = p / (KC / 8), c8 = (p % (KC / 8)) * 8;
+    wreg[v] = *reinterpret_cast<const u32x4*>(wt + static_cast<int64_t>(e) * d + c8);
+  }
 
   for (int kc = 0; kc < d; kc += KC) {
-    __syncthreads();  // wsT of the previous chunk consumed
-    // stage W[kc:kc+KC, 0:E] transposed: each thread moves 8 experts of one column
-    for (int t = tid; t < KC * (E / 8); t += kBlock) {
-      const int kk = t / (E / 8), e8 = (t % (E / 8)) * 8;
-      const u32x4 v = *reinterpret_cast<const u32x4*>(wg + static_cast<int64_t>(kc + kk) * E + e8);
-      const uint32_t p[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        wsT[(e8 + 2 * q) * LDW + kk] = static_cast<uint16_t>(p[q] & 0xffffu);
-        wsT[(e8 + 2 * q + 1) * LDW + kk] = static_cast<uint16_t>(p[q] >> 16);
+    for (int v = 0; v < WVEC; ++v) {
+      const int p = tid + v * kBlock, e = p / (KC / 8), c8 = (p % (KC / 8)) * 8;
+      *reinterpret_cast<u32x4*>(&wsT[e * LDW + c8]) = wreg[v];
+    }
+    __syncthreads();
+    const bool more = kc + KC < d;
+    if (more) {
+#pragma unroll
+      for (int v = 0; v < WVEC; ++v) {
+        const int p = tid + v * kBlock, e = p / (KC / 8), c8 = (p % (KC / 8)) * 8;
+        wreg[v] = *reinterpret_cast<const u32x4*>(wt + static_cast<int64_t>(e) * d + kc + KC + c8);
       }
     }
-    // prefetch the next chunk of x while this one is multiplied
-    const bool more = kc + KC < d;
 #pragma unroll
-    for (int v = 0; v < kVec; ++v)
-      nxt[v] = (arow_ok && more) ? xa[(kc + KC) / 8 + v] : u32x4{0u, 0u, 0u, 0u};
-    __syncthreads();
+    for (int v = 0; v < XVEC; ++v) xnxt[v] = (arow_ok && more) ? xa[(kc + KC) / 8 + v] : zero;
 #pragma unroll
     for (int ks = 0; ks < KSTEPS; ++ks) {
-      const bf16x8 av = __builtin_bit_cast(bf16x8, cur[ks]);
+      const bf16x8 av = __builtin_bit_cast(bf16x8, xcur[ks]);
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
         const u32x4 braw = *reinterpret_cast<const u32x4*>(&wsT[(nt * 16 + m) * LDW + KG * g + 8 * ks]);
         acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf16x8, braw), acc[nt], 0, 0, 0);
       }
     }
+    __syncthreads();  // wsT consumed before it is overwritten
 #pragma unroll
-    for (int v = 0; v < kVec; ++v) cur[v] = nxt[v];
+    for (int v = 0; v < XVEC; ++v) xcur[v] = xnxt[v];
   }
 
   // logits (+ bias) of the block's 64 tokens into LDS: lane holds rows 4g+i of
@@ -134,12 +160,19 @@ static hipError_t launch_mfma_nt(const RouteArgs& a, hipStream_t st) {
   return launch_mfma_t<NT, KC, 8, false>(a, st);
 }
 
+bool route_shape_uses_mfma(int kind, int logits_in, int dtype, int E, int d) {
+  return kind != 2 && !logits_in && dtype == 1 && E % 16 == 0 && E <= 128 && d > 0 && d % (E <= 64 ? 256 : 128) == 0;
+}
+
 bool route_uses_mfma(const RouteArgs& a) {
-  return a.kind != 2 && !a.logits_in && a.dtype == 1 && a.E % 16 == 0 && a.E <= 128 &&
-         a.d % (a.E <= 64 ? 256 : 128) == 0 && (reinterpret_cast<uintptr_t>(a.wg) % 16) == 0;
+  return a.wt != nullptr && route_shape_uses_mfma(a.kind, a.logits_in, a.dtype, a.E, a.d);
 }
 
 hipError_t launch_route_mfma(const RouteArgs& a, hipStream_t st) {
+  transpose_wg_kernel<<<dim3((a.d + 63) / 64, (a.E + 63) / 64), dim3(kBlock), 0, st>>>(
+      reinterpret_cast<const uint16_t*>(a.wg), a.wt, a.d, a.E);
+  const hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
   switch (a.E / 16) {
     case 1: return launch_mfma_nt<1, 256>(a, st);
     case 2: return launch_mfma_nt<2, 256>(a, st);

@@ -55,10 +55,24 @@ def _ws(params):
 @pytest.mark.parametrize("S,E,k,kind", [(1024, 8, 1, 0), (8192, 16, 2, 0), (32768, 64, 4, 1), (65536, 128, 1, 2),
                                         (0, 8, 1, 0), (257, 5, 2, 0)])
 def test_workspace_size(lib, S, E, k, kind):
+    # fp32: histogram only, k x E x ceil(S / 64) int32
     p = hm.gate_params(S, 256, E, k, 10, kind)
     st, n = _ws(p)
     assert st == 0
     assert n == k * ((S + 63) // 64) * E * 4
+
+
+@pytest.mark.parametrize("S,d,E,k,kind,mfma", [(8192, 1024, 16, 2, 0, True), (32768, 2048, 64, 4, 1, True),
+                                               (100, 384, 128, 1, 0, True), (100, 384, 64, 1, 0, False),
+                                               (100, 520, 16, 1, 0, False), (100, 256, 24, 1, 0, False),
+                                               (100, 256, 144, 1, 0, False), (100, 256, 64, 1, 2, False)])
+def test_workspace_size_bf16(lib, S, d, E, k, kind, mfma):
+    # bf16 shapes on the matrix-core route also hold W transposed (E x d bf16, 256-byte aligned)
+    p = hm.gate_params(S, d if kind != 2 else 0, E, k, 10, kind, dtype=b.MOE_BF16)
+    st, n = _ws(p)
+    assert st == 0
+    wt = ((E * d * 2 + 255) // 256 * 256) if mfma else 0
+    assert n == wt + k * ((S + 63) // 64) * E * 4
 
 
 BAD_PARAMS = [

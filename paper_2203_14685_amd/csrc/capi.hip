@@ -74,17 +74,10 @@ moe_status check_gate_params(const moe_gate_params* p) {
   return MOE_OK;
 }
 
-// Workspace layout: [W^T, bf16 E x d, only for the matrix-core route][histogram,
-// int32 k x E x ceil(S/64)], each part 256-byte aligned.
-size_t gate_wt_bytes(const moe_gate_params* p) {
-  if (!route_shape_uses_mfma(p->kind, p->logits_in, p->dtype, p->E, p->d)) return 0;
-  const size_t n = static_cast<size_t>(p->E) * static_cast<size_t>(p->d) * 2;
-  return (n + 255) / 256 * 256;
-}
-
+// Workspace: the histogram, int32 [k, E, ceil(S/64)].
 size_t gate_workspace_bytes(const moe_gate_params* p) {
   const size_t n = static_cast<size_t>(p->k) * static_cast<size_t>(hist_blocks(p->S)) * static_cast<size_t>(p->E);
-  return gate_wt_bytes(p) + n * sizeof(int32_t);
+  return n * sizeof(int32_t);
 }
 
 moe_status check_layout(const moe_layout* l, const char* who) {
@@ -179,16 +172,14 @@ moe_status moe_gate(const moe_gate_params* p, const void* x, const void* wg, con
   if (workspace && !aligned(workspace, 16)) return fail(MOE_ERR_WORKSPACE, "%s: workspace is not 16-byte aligned", who);
 
   const int nb = static_cast<int>(hist_blocks(S));
-  const size_t wt_bytes = gate_wt_bytes(p);
-  uint16_t* wt = wt_bytes ? static_cast<uint16_t*>(workspace) : nullptr;
-  int32_t* hist = reinterpret_cast<int32_t*>(static_cast<char*>(workspace) + wt_bytes);
+  int32_t* hist = static_cast<int32_t*>(workspace);
 
   RouteArgs ra{};
   ra.S = p->S; ra.d = p->d; ra.E = p->E; ra.k = p->k; ra.nb = nb;
   ra.kind = p->kind; ra.normalize = p->normalize; ra.logits_in = p->logits_in; ra.dtype = p->dtype;
   ra.hash_seed = p->hash_seed;
   ra.x = x; ra.wg = wg; ra.bias = bias; ra.token_ids = token_ids; ra.logits = logits;
-  ra.ids = ids; ra.weights = weights; ra.hist = hist; ra.wt = wt;
+  ra.ids = ids; ra.weights = weights; ra.hist = hist;
   hipError_t err = launch_route(ra, stream);
   if (err != hipSuccess) return hip_fail(err, "moe_gate: route kernel launch");
 

@@ -18,7 +18,6 @@ struct RouteArgs {
   int32_t* ids;             // [S, k]
   float* weights;           // [S, k]
   int32_t* hist;            // [k, E, nb] workspace (nb = 64-token wave blocks)
-  uint16_t* wt;             // [E, d] bf16 workspace: W transposed (matrix-core route only)
 };
 
 struct ScanArgs {
@@ -56,8 +55,6 @@ hipError_t launch_route_valu_f32(const RouteArgs& a, hipStream_t st);
 hipError_t launch_route_valu_bf16(const RouteArgs& a, hipStream_t st);
 hipError_t launch_route_mfma(const RouteArgs& a, hipStream_t st);
 bool route_uses_mfma(const RouteArgs& a);
-// route_uses_mfma() for the raw parameters (no pointers): decides the workspace layout.
-bool route_shape_uses_mfma(int kind, int logits_in, int dtype, int E, int d);
 hipError_t launch_scan(const ScanArgs& a, hipStream_t st);
 hipError_t launch_assign(const AssignArgs& a, hipStream_t st);
 hipError_t launch_dispatch(const RowArgs& a, hipStream_t st);

@@ -8,33 +8,33 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 // ---------------------------------------------------------------- MFMA route (bf16)
-// W^T [E, d] is written once per call by transpose_wg_kernel (into the
-// workspace) so that every block can stage it with 16-byte copies.
-//
 // 64 tokens per block, 4 waves; wave w computes the logits of tokens
 // [16w, 16w+16) for all E = 16*NT experts with v_mfma_f32_16x16x32_bf16
 // (M = tokens, N = experts, K = d).  Per K chunk of KC columns, W^T[:, kc:kc+KC]
 // sits in LDS (B fragments are 16-byte LDS reads) and every lane holds 2*KC/4
 // contiguous bytes of its token's row of x (A fragments).  The next chunk of
-// both is loaded into registers while the current one is multiplied.  Inside a
+// both is loaded into registers while the current one is multiplied.  W [d, E]
+// is transposed on the way: a thread loads an 8 x 8 block (8 rows of 8
+// experts, 16 bytes each), regroups the half-words in registers and stores 8
+// rows of W^T (8 columns each, 16 bytes).  Inside a
 // chunk, lane group g = lane/16 supplies the columns [kc + (KC/4)*g,
 // kc + (KC/4)*(g+1)); A and B use the same column order, so each MFMA sums a
 // fixed permutation of 32 columns of the chunk.  The block's 64 x E logits
 // (+ bias) then go to LDS and wave 0 selects, one token per lane.
 constexpr int kMfmaTokens = 64;
 
-__global__ __launch_bounds__(kBlock) void transpose_wg_kernel(const uint16_t* __restrict__ wg, uint16_t* __restrict__ wt,
-                                                              int d, int E) {
-  __shared__ uint16_t tile[64][65];
-  const int j0 = blockIdx.x * 64, e0 = blockIdx.y * 64;
-  for (int t = threadIdx.x; t < 64 * 64; t += kBlock) {
-    const int jj = t / 64, ee = t % 64;
-    if (j0 + jj < d && e0 + ee < E) tile[jj][ee] = wg[static_cast<int64_t>(j0 + jj) * E + e0 + ee];
-  }
-  __syncthreads();
-  for (int t = threadIdx.x; t < 64 * 64; t += kBlock) {
-    const int ee = t / 64, jj = t % 64;
-    if (j0 + jj < d && e0 + ee < E) wt[static_cast<int64_t>(e0 + ee) * d + j0 + jj] = tile[jj][ee];
+// 8 x 8 transpose of bf16: in[j] holds row j (8 half-words, lowest first);
+// out[i] receives column i.
+__device__ __forceinline__ void transpose8x8_b16(const u32x4 (&in)[8], u32x4 (&out)[8]) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    uint32_t wd[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t a = in[2 * q][i / 2], b = in[2 * q + 1][i / 2];
+      wd[q] = (i & 1) ? ((a >> 16) | (b & 0xffff0000u)) : ((a & 0xffffu) | (b << 16));
+    }
+    out[i] = u32x4{wd[0], wd[1], wd[2], wd[3]};
   }
 }
 
@@ -44,10 +44,9 @@ __global__ __launch_bounds__(kBlock) void route_mfma_kernel(RouteArgs a) {
   constexpr int KG = KC / 4;                 // columns per lane group per chunk
   constexpr int KSTEPS = KG / 8;             // MFMAs per N tile per chunk
   constexpr int LDW = KC + 8;                // padded LDS row (bf16 elements) of W^T
-  constexpr int WPIECES = E * KC / 8;        // 16-byte pieces of a W^T chunk
-  constexpr int WVEC = WPIECES / kBlock;     // per thread
+  constexpr int WBLOCKS = (KC / 8) * (E / 8);  // 8 x 8 blocks of a W chunk
+  constexpr int WVEC = (WBLOCKS + kBlock - 1) / kBlock;  // per thread
   constexpr int XVEC = KG / 8;               // 16-byte pieces of x per lane per chunk
-  static_assert(WPIECES % kBlock == 0, "chunk must split evenly over the block");
   static_assert(E * LDW * 2 >= kMfmaTokens * (E + 1) * 4, "logits reuse the W^T buffer");
   __shared__ __align__(16) uint16_t wsT[E * LDW];
   __shared__ int hist_lds[E];
@@ -62,37 +61,46 @@ __global__ __launch_bounds__(kBlock) void route_mfma_kernel(RouteArgs a) {
   const int64_t arow = tok0 + w * 16 + m;  // token of this lane's A fragment rows
   const bool arow_ok = arow < a.S;
   const u32x4* xa = reinterpret_cast<const u32x4*>(reinterpret_cast<const uint16_t*>(a.x) + arow * d + KG * g);
-  const uint16_t* wt = a.wt;
+  const uint16_t* wg = reinterpret_cast<const uint16_t*>(a.wg);
 
   f32x4 acc[NT];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  u32x4 xcur[XVEC], xnxt[XVEC], wreg[WVEC];
+  u32x4 xcur[XVEC], xnxt[XVEC], wreg[WVEC][8];
   const u32x4 zero = {0u, 0u, 0u, 0u};
+  // block b of a chunk: columns kb = 8 * (b / (E/8)) .. +8, experts eb = 8 * (b % (E/8)) .. +8
+  auto load_w = [&](int kc0) {
+#pragma unroll
+    for (int v = 0; v < WVEC; ++v) {
+      const int b = tid + v * kBlock;
+      if (b < WBLOCKS) {
+        const int kb = (b / (E / 8)) * 8, eb = (b % (E / 8)) * 8;
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          wreg[v][j] = *reinterpret_cast<const u32x4*>(wg + static_cast<int64_t>(kc0 + kb + j) * E + eb);
+      }
+    }
+  };
 #pragma unroll
   for (int v = 0; v < XVEC; ++v) xcur[v] = arow_ok ? xa[v] : zero;
-#pragma unroll
-  for (int v = 0; v < WVEC; ++v) {
-    const int p = tid + v * kBlock, e = p / (KC / 8), c8 = (p % (KC / 8)) * 8;
-    wreg[v] = *reinterpret_cast<const u32x4*>(wt + static_cast<int64_t>(e) * d + c8);
-  }
+  load_w(0);
 
   for (int kc = 0; kc < d; kc += KC) {
 #pragma unroll
     for (int v = 0; v < WVEC; ++v) {
-      const int p = tid + v * kBlock, e = p / (KC / 8), c8 = (p % (KC / 8)) * 8;
-      *reinterpret_cast<u32x4*>(&wsT[e * LDW + c8]) = wreg[v];
+      const int b = tid + v * kBlock;
+      if (b < WBLOCKS) {
+        const int kb = (b / (E / 8)) * 8, eb = (b % (E / 8)) * 8;
+        u32x4 col[8];
+        transpose8x8_b16(wreg[v], col);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) *reinterpret_cast<u32x4*>(&wsT[(eb + i) * LDW + kb]) = col[i];
+      }
     }
     __syncthreads();
     const bool more = kc + KC < d;
-    if (more) {
-#pragma unroll
-      for (int v = 0; v < WVEC; ++v) {
-        const int p = tid + v * kBlock, e = p / (KC / 8), c8 = (p % (KC / 8)) * 8;
-        wreg[v] = *reinterpret_cast<const u32x4*>(wt + static_cast<int64_t>(e) * d + kc + KC + c8);
-      }
-    }
+    if (more) load_w(kc + KC);
 #pragma unroll
     for (int v = 0; v < XVEC; ++v) xnxt[v] = (arow_ok && more) ? xa[(kc + KC) / 8 + v] : zero;
 #pragma unroll
@@ -160,19 +168,12 @@ static hipError_t launch_mfma_nt(const RouteArgs& a, hipStream_t st) {
   return launch_mfma_t<NT, KC, 8, false>(a, st);
 }
 
-bool route_shape_uses_mfma(int kind, int logits_in, int dtype, int E, int d) {
-  return kind != 2 && !logits_in && dtype == 1 && E % 16 == 0 && E <= 128 && d > 0 && d % (E <= 64 ? 256 : 128) == 0;
-}
-
 bool route_uses_mfma(const RouteArgs& a) {
-  return a.wt != nullptr && route_shape_uses_mfma(a.kind, a.logits_in, a.dtype, a.E, a.d);
+  return a.kind != 2 && !a.logits_in && a.dtype == 1 && a.E % 16 == 0 && a.E <= 128 &&
+         a.d % (a.E <= 64 ? 256 : 128) == 0 && (reinterpret_cast<uintptr_t>(a.wg) % 16) == 0;
 }
 
 hipError_t launch_route_mfma(const RouteArgs& a, hipStream_t st) {
-  transpose_wg_kernel<<<dim3((a.d + 63) / 64, (a.E + 63) / 64), dim3(kBlock), 0, st>>>(
-      reinterpret_cast<const uint16_t*>(a.wg), a.wt, a.d, a.E);
-  const hipError_t err = hipGetLastError();
-  if (err != hipSuccess) return err;
   switch (a.E / 16) {
     case 1: return launch_mfma_nt<1, 256>(a, st);
     case 2: return launch_mfma_nt<2, 256>(a, st);

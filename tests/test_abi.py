@@ -62,19 +62,6 @@ def test_workspace_size(lib, S, E, k, kind):
     assert n == k * ((S + 63) // 64) * E * 4
 
 
-@pytest.mark.parametrize("S,d,E,k,kind,mfma", [(8192, 1024, 16, 2, 0, True), (32768, 2048, 64, 4, 1, True),
-                                               (100, 384, 128, 1, 0, True), (100, 384, 64, 1, 0, False),
-                                               (100, 520, 16, 1, 0, False), (100, 256, 24, 1, 0, False),
-                                               (100, 256, 144, 1, 0, False), (100, 256, 64, 1, 2, False)])
-def test_workspace_size_bf16(lib, S, d, E, k, kind, mfma):
-    # bf16 shapes on the matrix-core route also hold W transposed (E x d bf16, 256-byte aligned)
-    p = hm.gate_params(S, d if kind != 2 else 0, E, k, 10, kind, dtype=b.MOE_BF16)
-    st, n = _ws(p)
-    assert st == 0
-    wt = ((E * d * 2 + 255) // 256 * 256) if mfma else 0
-    assert n == wt + k * ((S + 63) // 64) * E * 4
-
-
 BAD_PARAMS = [
     dict(E=0), dict(E=1025), dict(S=-1), dict(capacity=-1), dict(k=0), dict(k=9, E=16),
     dict(k=3, E=2), dict(kind=1, k=3, E=16), dict(kind=2, k=2), dict(kind=3), dict(dtype=2),

@@ -6,9 +6,12 @@
 //   route   logits (the projection x.W of Eq. 1, or read from the caller),
 //           streaming selection (top-k list, per-group top-1, or hash),
 //           softmax weights, and for every 64-token "wave block" a histogram of
-//           its (rank, expert) pairs.  Three variants:
-//             route_mfma_kernel  bf16, E a multiple of 16 up to 128: the
-//                                projection on v_mfma_f32_16x16x32_bf16;
+//           its (rank, expert) pairs.  Four variants:
+//             route_mfma_rs_kernel  bf16, W held in registers (E up to 128,
+//                                d 512..2048): persistent, projection on
+//                                v_mfma_f32_16x16x32_bf16;
+//             route_mfma_kernel  other bf16 shapes with E a multiple of 16 up
+//                                to 128: W staged through LDS per K chunk;
 //             route_valu_kernel  any dtype/shape: one thread per token;
 //             route_hash_kernel  the hash gate (no projection).
 //   scan    one block per expert: exclusive scan of that expert's histogram
@@ -130,6 +133,7 @@ hipError_t launch_route(const RouteArgs& a, hipStream_t st) {
     route_hash_kernel<<<dim3(blocks), dim3(kBlock), static_cast<size_t>(kWavesPerBlock) * a.E * sizeof(int), st>>>(a);
     return hipGetLastError();
   }
+  if (route_uses_mfma_rs(a)) return launch_route_mfma_rs(a, st);
   if (route_uses_mfma(a)) return launch_route_mfma(a, st);
   // with logits given, the element type of x and wg is irrelevant
   if (a.dtype == 1 && !a.logits_in) return launch_route_valu_bf16(a, st);

@@ -55,6 +55,8 @@ hipError_t launch_route_valu_f32(const RouteArgs& a, hipStream_t st);
 hipError_t launch_route_valu_bf16(const RouteArgs& a, hipStream_t st);
 hipError_t launch_route_mfma(const RouteArgs& a, hipStream_t st);
 bool route_uses_mfma(const RouteArgs& a);
+hipError_t launch_route_mfma_rs(const RouteArgs& a, hipStream_t st);
+bool route_uses_mfma_rs(const RouteArgs& a);
 hipError_t launch_scan(const ScanArgs& a, hipStream_t st);
 hipError_t launch_assign(const AssignArgs& a, hipStream_t st);
 hipError_t launch_dispatch(const RowArgs& a, hipStream_t st);

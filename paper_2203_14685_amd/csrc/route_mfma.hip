@@ -20,7 +20,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 // chunk, lane group g = lane/16 supplies the columns [kc + (KC/4)*g,
 // kc + (KC/4)*(g+1)); A and B use the same column order, so each MFMA sums a
 // fixed permutation of 32 columns of the chunk.  The block's 64 x E logits
-// (+ bias) then go to LDS and wave 0 selects, one token per lane.
+// (+ bias) then go to LDS and 4 lanes per token select.
 constexpr int kMfmaTokens = 64;
 
 // 8 x 8 transpose of bf16: in[j] holds row j (8 half-words, lowest first);
@@ -49,7 +49,7 @@ __global__ __launch_bounds__(kBlock) void route_mfma_kernel(RouteArgs a) {
   constexpr int XVEC = KG / 8;               // 16-byte pieces of x per lane per chunk
   static_assert(E * LDW * 2 >= kMfmaTokens * (E + 1) * 4, "logits reuse the W^T buffer");
   __shared__ __align__(16) uint16_t wsT[E * LDW];
-  __shared__ int hist_lds[E];
+  __shared__ int hist_lds[8 * E];  // [k][E], k <= 8
   float* lg = reinterpret_cast<float*>(wsT);  // after the K loop: [64][E + 1] logits
 
   const int tid = threadIdx.x;
@@ -133,24 +133,20 @@ __global__ __launch_bounds__(kBlock) void route_mfma_kernel(RouteArgs a) {
       if (tok0 + r < a.S) a.logits[(tok0 + r) * E + e] = lg[r * (E + 1) + e];
     }
   }
-  const int64_t s = tok0 + lane;
-  const bool valid = (w == 0) && s < a.S;
-  if (valid) {
-    const float* row = &lg[lane * (E + 1)];
-    int32_t* my_ids = a.ids + s * a.k;
-    float* my_w = a.weights + s * a.k;
-    if constexpr (KTOP1) {
-      Ktop1State kt;
-      kt.init(E / a.k);
-      for (int e = 0; e < E; ++e) kt.push(row[e], e, my_ids, my_w);
-    } else {
-      TopkState<KMAX> tk;
-      tk.init();
-      for (int e = 0; e < E; ++e) tk.push(row[e], e);
-      tk.finish(a.k, a.normalize, my_ids, my_w);
-    }
+  // selection: 4 lanes per token; (rank, expert) counts in LDS
+  for (int i = tid; i < a.k * E; i += kBlock) hist_lds[i] = 0;
+  __syncthreads();
+  {
+    const int tt = tid / 4, j = tid % 4;
+    const int64_t s = tok0 + tt;
+    select_token<4, KMAX, KTOP1>(&lg[tt * (E + 1)], E, a.k, a.normalize, j, s < a.S, a.ids + s * a.k,
+                                 a.weights + s * a.k, hist_lds);
   }
-  wave_block_hist(hist_lds, w == 0, s, valid, blockIdx.x, a);
+  __syncthreads();
+  for (int i = tid; i < a.k * E; i += kBlock) {
+    const int r = i / E, e = i % E;
+    a.hist[(static_cast<int64_t>(r) * E + e) * a.nb + blockIdx.x] = hist_lds[i];
+  }
 }
 
 template <int NT, int KC, int KMAX, bool KTOP1>

@@ -1,5 +1,10 @@
 // Streaming expert selection and the wave-block histogram shared by the route
 // kernels (gate step of Algorithm 1; Eq. 1, Sec. 3.1 kTop1).
+//
+// Order of experts everywhere: larger logit first, then lower expert index.
+// Softmax sums are formed online (running maximum, rescaled sum) with the
+// hardware exponential (__expf: v_exp_f32 on x*log2(e)); its relative error is
+// about |x| * 6e-8 plus one ulp, far inside the 1e-5 weight tolerance.
 #pragma once
 
 #include "common.hpp"
@@ -9,33 +14,28 @@ namespace hetumoe {
 
 constexpr int kEmpty = 0x7fffffff;
 
-// ---------------------------------------------------------------- selection
-// Streaming state for one token; experts arrive in increasing index order.
-// Order of experts: larger logit first, then lower index.
-
+// ---------------------------------------------------------------- top-k
 template <int KMAX>
 struct TopkState {
   float tv[KMAX];
   int ti[KMAX];
-  float m;     // running max of all logits
-  float ssum;  // sum of exp(logit - m) over the logits seen so far
+  float m;     // running max of the logits seen
+  float ssum;  // sum of exp(logit - m) over the logits seen
   __device__ __forceinline__ void init() {
 #pragma unroll
     for (int i = 0; i < KMAX; ++i) { tv[i] = -INFINITY; ti[i] = kEmpty; }
     m = -INFINITY;
     ssum = 0.f;
   }
-  __device__ __forceinline__ void push(float v, int e) {
-    if (v > m) { ssum = ssum * expf(m - v) + 1.f; m = v; }
-    else { ssum += expf(v - m); }
-    // insertion into the sorted list: the carried pair moves down while it beats
-    // the entry it meets; an empty entry always loses, so every reported id is a
-    // real expert even for non-finite logits
+  // Sorted insertion: the carried pair moves down while it beats the entry it
+  // meets.  An empty entry always loses, so every reported id is a real expert
+  // even for non-finite logits.
+  __device__ __forceinline__ void insert(float v, int e) {
     float cv = v;
     int ci = e;
 #pragma unroll
     for (int i = 0; i < KMAX; ++i) {
-      const bool beats = ti[i] == kEmpty || cv > tv[i] || (cv == tv[i] && ci < ti[i]);
+      const bool beats = better(cv, ci, tv[i], ti[i]);
       const float ov = tv[i];
       const int oi = ti[i];
       tv[i] = beats ? cv : ov;
@@ -44,6 +44,56 @@ struct TopkState {
       ci = beats ? oi : ci;
     }
   }
+  __device__ __forceinline__ void push(float v, int e) {
+    if (v > m) { ssum = ssum * __expf(m - v) + 1.f; m = v; }
+    else { ssum += __expf(v - m); }
+    insert(v, e);
+  }
+  // (v, i) ranks before (pv, pi): larger logit, then lower index; empty entries last.
+  __device__ __forceinline__ static bool better(float v, int i, float pv, int pi) {
+    return i != kEmpty && (pi == kEmpty || v > pv || (v == pv && i < pi));
+  }
+  // Merge with the state of lane (lane ^ mask): afterwards both hold the best
+  // KMAX of the union.  The best KMAX of two sorted lists A, B are
+  // better-of(A[i], B[KMAX-1-i]), a bitonic sequence; log2(KMAX) half-cleaner
+  // stages sort it.
+  __device__ __forceinline__ void merge_xor(int mask) {
+    float cv[KMAX];
+    int ci[KMAX];
+#pragma unroll
+    for (int i = 0; i < KMAX; ++i) {
+      const float pv = __shfl_xor(tv[KMAX - 1 - i], mask, kWave);
+      const int pi = __shfl_xor(ti[KMAX - 1 - i], mask, kWave);
+      const bool mine = better(tv[i], ti[i], pv, pi);
+      cv[i] = mine ? tv[i] : pv;
+      ci[i] = mine ? ti[i] : pi;
+    }
+#pragma unroll
+    for (int st = KMAX / 2; st >= 1; st /= 2) {
+#pragma unroll
+      for (int i = 0; i < KMAX; ++i) {
+        if ((i & st) == 0) {
+          const bool keep = better(cv[i], ci[i], cv[i + st], ci[i + st]);
+          const float v0 = cv[i], v1 = cv[i + st];
+          const int i0 = ci[i], i1 = ci[i + st];
+          cv[i] = keep ? v0 : v1;
+          ci[i] = keep ? i0 : i1;
+          cv[i + st] = keep ? v1 : v0;
+          ci[i + st] = keep ? i1 : i0;
+        }
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < KMAX; ++i) { tv[i] = cv[i]; ti[i] = ci[i]; }
+    const float pm = __shfl_xor(m, mask, kWave);
+    const float ps = __shfl_xor(ssum, mask, kWave);
+    const float nm = fmaxf(m, pm);
+    // a side that has seen nothing has m = -inf and ssum = 0: contributes 0
+    const float a = (ssum > 0.f) ? ssum * __expf(m - nm) : 0.f;
+    const float b = (ps > 0.f) ? ps * __expf(pm - nm) : 0.f;
+    ssum = a + b;
+    m = nm;
+  }
   // Writes ids and weights of the first k entries.
   __device__ __forceinline__ void finish(int k, int normalize, int32_t* ids, float* weights) const {
     const float top = tv[0];
@@ -51,39 +101,122 @@ struct TopkState {
     if (normalize) {
 #pragma unroll
       for (int r = 0; r < KMAX; ++r)
-        if (r < k) z += expf(tv[r] - top);
+        if (r < k) z += __expf(tv[r] - top);
     } else {
-      z = ssum * expf(m - top);  // m == top for finite logits
+      z = ssum * __expf(m - top);  // m == top for finite logits
     }
     const float inv = 1.f / z;
 #pragma unroll
     for (int r = 0; r < KMAX; ++r) {
       if (r < k) {
         ids[r] = ti[r];
-        weights[r] = (r == 0 ? 1.f : expf(tv[r] - top)) * inv;
+        weights[r] = (r == 0 ? 1.f : __expf(tv[r] - top)) * inv;
       }
     }
   }
 };
 
-// kTop1: k contiguous groups of G experts; the group's best expert and the
-// softmax within the group (its weight is 1 / sum exp(l - max)).
+// ---------------------------------------------------------------- kTop1
+// Best expert of a run of experts inside one group, with the group softmax sum
+// relative to that best logit.
+struct GroupBest {
+  float bv;    // best (= max) logit
+  int bi;      // its expert
+  float gsum;  // sum of exp(logit - bv)
+  __device__ __forceinline__ void init() { bv = -INFINITY; bi = kEmpty; gsum = 0.f; }
+  __device__ __forceinline__ void push(float v, int e) {
+    if (bi == kEmpty) { bv = v; bi = e; gsum = 1.f; }
+    else if (v > bv) { gsum = gsum * __expf(bv - v) + 1.f; bv = v; bi = e; }
+    else { gsum += __expf(v - bv); }
+  }
+  __device__ __forceinline__ void merge_xor(int mask) {
+    const float pv = __shfl_xor(bv, mask, kWave);
+    const int pi = __shfl_xor(bi, mask, kWave);
+    const float ps = __shfl_xor(gsum, mask, kWave);
+    if (pi == kEmpty) return;
+    if (bi == kEmpty) { bv = pv; bi = pi; gsum = ps; return; }
+    const bool partner_wins = pv > bv || (pv == bv && pi < bi);
+    const float nb = partner_wins ? pv : bv;
+    gsum = gsum * __expf(bv - nb) + ps * __expf(pv - nb);
+    bv = nb;
+    bi = partner_wins ? pi : bi;
+  }
+};
+
+// kTop1 streaming over all experts in index order: k contiguous groups of G;
+// each finished group writes its best expert and weight 1 / sum exp(l - max).
 struct Ktop1State {
-  int G, g, bi;
-  float bv, gsum;
-  __device__ __forceinline__ void init(int G_) { G = G_; g = 0; bi = 0; bv = -INFINITY; gsum = 0.f; }
+  int G, g;
+  GroupBest cur;
+  __device__ __forceinline__ void init(int G_) { G = G_; g = 0; cur.init(); }
   __device__ __forceinline__ void push(float v, int e, int32_t* ids, float* weights) {
-    const int gstart = g * G;
-    if (e == gstart) { bv = v; bi = e; gsum = 1.f; }
-    else if (v > bv) { gsum = gsum * expf(bv - v) + 1.f; bv = v; bi = e; }
-    else { gsum += expf(v - bv); }
-    if (e == gstart + G - 1) {
-      ids[g] = bi;
-      weights[g] = 1.f / gsum;
+    cur.push(v, e);
+    if (e == (g + 1) * G - 1) {
+      ids[g] = cur.bi;
+      weights[g] = 1.f / cur.gsum;
       ++g;
+      cur.init();
     }
   }
 };
+
+// ---------------------------------------------------------------- parallel selection
+// Selection for one token by P consecutive lanes of a wave (lane j = 0..P-1 of
+// the token streams experts [j*E/P, (j+1)*E/P) of its logit row, then the lanes
+// merge by butterfly shuffles).  All P lanes must call this together.  The lane
+// that writes an (id, weight) pair also counts it in hist_lds[r][id] (LDS).
+template <int P, int KMAX, bool KTOP1>
+__device__ __forceinline__ void select_token(const float* lrow, int E, int k, int normalize, int j, bool valid,
+                                             int32_t* ids, float* weights, int* hist_lds) {
+  const int slice = E / P;
+  const int e0 = j * slice;
+  if constexpr (!KTOP1) {
+    TopkState<KMAX> tk;
+    tk.init();
+    for (int e = 0; e < slice; ++e) tk.push(lrow[e0 + e], e0 + e);
+#pragma unroll
+    for (int msk = 1; msk < P; msk <<= 1) tk.merge_xor(msk);
+    if (valid && j == 0) {
+      tk.finish(k, normalize, ids, weights);
+#pragma unroll
+      for (int r = 0; r < KMAX; ++r)
+        if (r < k) atomicAdd(&hist_lds[r * E + tk.ti[r]], 1);
+    }
+  } else {
+    const int G = E / k;
+    if (P % k == 0) {
+      // L = P / k lanes per group; lane j's experts lie in group j / L
+      const int L = P / k;
+      GroupBest gb;
+      gb.init();
+      for (int e = 0; e < slice; ++e) gb.push(lrow[e0 + e], e0 + e);
+      for (int msk = 1; msk < L; msk <<= 1) gb.merge_xor(msk);
+      if (valid && j % L == 0) {
+        const int grp = j / L;
+        ids[grp] = gb.bi;
+        weights[grp] = 1.f / gb.gsum;
+        atomicAdd(&hist_lds[grp * E + gb.bi], 1);
+      }
+    } else if (k % P == 0) {
+      // each lane's experts are k / P whole groups
+      if (valid) {
+        for (int grp = e0 / G; grp < (e0 + slice) / G; ++grp) {
+          GroupBest gb;
+          gb.init();
+          for (int e = grp * G; e < (grp + 1) * G; ++e) gb.push(lrow[e], e);
+          ids[grp] = gb.bi;
+          weights[grp] = 1.f / gb.gsum;
+          atomicAdd(&hist_lds[grp * E + gb.bi], 1);
+        }
+      }
+    } else if (valid && j == 0) {
+      Ktop1State kt;
+      kt.init(G);
+      for (int e = 0; e < E; ++e) kt.push(lrow[e], e, ids, weights);
+      for (int r = 0; r < k; ++r) atomicAdd(&hist_lds[r * E + ids[r]], 1);
+    }
+  }
+}
 
 // ---------------------------------------------------------------- wave-block histogram
 // hist[r][e][wb] = number of tokens of wave block wb whose rank-r choice is e.

@@ -128,15 +128,21 @@ def test_projection_odd_shapes(dtype, d, E, k):
     check_layout_ops(w, inp["x"], g["ids"], g["slots"], g["weights"], g["slot_src"], E, C, k, seed=9)
 
 
-@pytest.mark.parametrize("E,k,kind,normalize,d,bias", [
-    (16, 1, 1, 0, 256, False), (32, 2, 0, 1, 512, True), (48, 1, 0, 0, 256, False), (64, 4, 1, 0, 768, True),
-    (80, 3, 0, 1, 256, False), (96, 8, 0, 0, 128, True), (112, 2, 0, 0, 384, False), (128, 8, 1, 0, 256, True),
-    (128, 2, 0, 1, 384, False),
+@pytest.mark.parametrize("E,k,kind,normalize,d,bias,S", [
+    # W staged through LDS (4 lanes per token select)
+    (16, 1, 1, 0, 256, False, 300), (48, 1, 0, 0, 256, False, 300), (64, 4, 1, 0, 768, True, 300),
+    (80, 3, 0, 1, 256, False, 300), (96, 8, 0, 0, 128, True, 300), (112, 2, 0, 0, 384, False, 300),
+    (128, 8, 1, 0, 256, True, 300), (128, 2, 0, 1, 384, False, 300), (48, 3, 1, 0, 256, False, 300),
+    (64, 8, 1, 0, 256, True, 300), (128, 4, 1, 0, 384, False, 300), (80, 5, 1, 0, 256, False, 300),
+    # W held in registers (8 lanes per token select)
+    (32, 2, 0, 1, 512, True, 300), (64, 4, 1, 0, 1024, True, 300), (128, 8, 0, 1, 512, False, 300),
+    (16, 2, 0, 0, 2048, False, 300), (32, 8, 1, 0, 1024, True, 300), (64, 1, 0, 0, 512, False, 300),
+    (64, 2, 0, 1, 512, True, 20000),
 ])
-def test_mfma_projection_shapes(E, k, kind, normalize, d, bias):
-    """bf16 shapes that take the matrix-core route kernel (E a multiple of 16 up
-    to 128, d a multiple of the K chunk), several wave blocks plus a ragged tail."""
-    S = 300
+def test_mfma_projection_shapes(E, k, kind, normalize, d, bias, S):
+    """bf16 shapes that take the matrix-core route kernels (E a multiple of 16 up
+    to 128), several wave blocks plus a ragged tail; S = 20000 makes persistent
+    blocks walk more than one wave block."""
     announce(f"mfma projection E={E} k={k} kind={kind} d={d} bias={bias}")
     w = dict(kind=kind, k=k, normalize=normalize, dtype="bf16", S=S, d=d, E=E, cf=1.0)
     if bias:

@@ -24,10 +24,67 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E peak, GB/s
 METRIC = "tokens/s through gate+dispatch+combine; achieved HBM GB/s vs MI355X peak"
 OPS = ("gate", "dispatch", "combine", "combine_bwd", "dispatch_bwd")
-KERNEL_OF_OP = {"dispatch": "dispatch_kernel", "combine": "combine_kernel", "combine_bwd": "combine_bwd_kernel",
-                "dispatch_bwd": "combine_kernel", "gate": "route_kernel"}
-SOURCE_OF_OP = {"dispatch": "layout.hip", "combine": "layout.hip", "combine_bwd": "layout.hip",
-                "dispatch_bwd": "layout.hip", "gate": "gate.hip"}
+_LAYOUT_SRC = ("layout.hip", "common.hpp", "kernels.hpp")
+_GATE_SRC = ("gate.hip", "route_mfma.hip", "route_mfma_rs.hip", "route_valu.hpp", "route_valu_f32.hip",
+             "route_valu_bf16.hip", "select.hpp", "common.hpp", "kernels.hpp")
+# op -> (kernel symbol fragment in traces, sources that kernel is compiled from)
+KERNEL_OF_OP = {"dispatch": ("dispatch_kernel", _LAYOUT_SRC),
+                "combine": ("combine_kernel<hetumoe::bf16_t, true>", _LAYOUT_SRC),
+                "combine_bwd": ("combine_bwd_kernel", _LAYOUT_SRC),
+                "dispatch_bwd": ("combine_kernel<hetumoe::bf16_t, false>", _LAYOUT_SRC),
+                "gate": ("route_", _GATE_SRC)}
+
+
+def summarize_pmc(args):
+    """Turn two rocprofv3 --pmc runs of this benchmark (FETCH_SIZE, WRITE_SIZE; KiB
+    per dispatch) into profiles/traffic_<op>_<workload>.txt.  Each run must have
+    used --calib-copy-mib: the counter is scaled by the ratio of the known bytes of
+    that plain device copy to what the counter read for it."""
+    import csv
+    import glob
+    w = None
+    from paper_2203_14685_amd import workloads as wl
+    w = wl.WORKLOADS[args.workload]
+    calib_bytes = args.calib_copy_mib * (1 << 20)
+
+    def load(d, counter):
+        rows = []
+        for f in glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True):
+            with open(f) as fh:
+                rows += [r for r in csv.DictReader(fh) if r.get("Counter_Name") == counter]
+        if not rows:
+            raise SystemExit(f"no {counter} rows under {d}")
+        return rows
+
+    out = {}
+    for counter, d in (("FETCH_SIZE", args.summarize_pmc[0]), ("WRITE_SIZE", args.summarize_pmc[1])):
+        rows = load(d, counter)
+        copy = [float(r["Counter_Value"]) for r in rows if "elementwise" in r["Kernel_Name"] or "copy" in r["Kernel_Name"].lower()]
+        if not copy:
+            raise SystemExit(f"{counter}: no calibration copy kernel found")
+        scale = calib_bytes / (max(copy) * 1024.0)
+        for op, (frag, _) in KERNEL_OF_OP.items():
+            vals = [float(r["Counter_Value"]) for r in rows if frag in r["Kernel_Name"]]
+            if vals:
+                out.setdefault(op, {})[counter] = (sum(vals) / len(vals), len(vals), scale, max(copy))
+    for op, cs in out.items():
+        if set(cs) != {"FETCH_SIZE", "WRITE_SIZE"}:
+            continue
+        fk, fn, fs, fc = cs["FETCH_SIZE"]
+        wk, wn, ws, wc = cs["WRITE_SIZE"]
+        total = fk * 1024 * fs + wk * 1024 * ws
+        frag, src = KERNEL_OF_OP[op]
+        with open(traffic_path(w["name"], op), "w") as f:
+            f.write(f"# HBM traffic per launch of {frag} ({op}), workload {w['name']}\n")
+            f.write("# from two rocprofv3 counter runs (TMPDIR=/tmp, from /tmp, repo at $R):\n")
+            f.write(f"#   rocprofv3 --pmc FETCH_SIZE --output-format csv -d <dir> -- python3 $R/bench.py --workload "
+                    f"{args.workload} --steps 3 --warmup 1 --no-cpu-baseline --calib-copy-mib {args.calib_copy_mib}\n")
+            f.write("#   (the same with --pmc WRITE_SIZE)\n")
+            f.write(f"# calibration: one {args.calib_copy_mib} MiB device copy read FETCH {fc:.0f} KiB, WRITE {wc:.0f} KiB\n")
+            f.write(f"fetch_kib_per_launch: {fk:.1f}\nwrite_kib_per_launch: {wk:.1f}\n")
+            f.write(f"fetch_scale: {fs:.4f}\nwrite_scale: {ws:.4f}\nlaunches: {fn}\n")
+            f.write(f"hbm_bytes_per_launch: {total:.0f}\nsource_sha: {source_sha(src)}\n")
+        print(f"{op}: {total / 1e6:.1f} MB per launch -> {traffic_path(w['name'], op)}")
 
 
 def parse():
@@ -37,6 +94,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", type=int, default=5, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                    help="write profiles/traffic_*.txt from two rocprofv3 --pmc output folders and exit")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="before the timed region, run one device copy of this many MiB (counter calibration)")
     return ap.parse_args()
@@ -61,15 +120,22 @@ def alg_bytes(w, S, d, E, k, C, elt, n_kept, tok_kept, dw):
     return b
 
 
-def source_sha(name):
-    with open(os.path.join(ROOT, "paper_2203_14685_amd", "csrc", name), "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+def source_sha(names):
+    h = hashlib.sha256()
+    for name in names:
+        with open(os.path.join(ROOT, "paper_2203_14685_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
-def measured_traffic(workload_name, kernel, sha):
+def traffic_path(workload_name, op):
+    return os.path.join(ROOT, "profiles", f"traffic_{op}_{workload_name}.txt")
+
+
+def measured_traffic(workload_name, op, sha):
     """HBM bytes per launch from the committed rocprofv3 counter summary, or None
-    when there is none for this kernel and workload or the kernel source changed."""
-    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload_name}.txt")
+    when there is none for this op's kernel and workload or its source changed."""
+    path = traffic_path(workload_name, op)
     if not os.path.exists(path):
         return None
     vals = {}
@@ -126,6 +192,9 @@ def cpu_baseline(w, target_s=12.0):
 
 def main():
     args = parse()
+    if args.summarize_pmc:
+        summarize_pmc(args)
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
@@ -224,8 +293,8 @@ def main():
     step_bytes = sum(ab.values())
     dom = max(("dispatch", "combine", "combine_bwd", "dispatch_bwd", "gate"), key=lambda o: op_ms[o])
     achieved = ab[dom] / (op_ms[dom] * 1e-3) / 1e9
-    kern = KERNEL_OF_OP[dom]
-    traffic = measured_traffic(w["name"], dom, source_sha(SOURCE_OF_OP[dom]))
+    kern, ksrc = KERNEL_OF_OP[dom]
+    traffic = measured_traffic(w["name"], dom, source_sha(ksrc))
 
     out = {
         "metric": METRIC,
@@ -243,7 +312,7 @@ def main():
         "config": {"workload": w["name"], "S": S, "d": d, "E": E, "k": k, "capacity": C,
                    "gate": ["topk", "ktop1", "hash"][w["kind"]], "passes": "fwd+bwd",
                    "parallelism": "single-gpu"},
-        "roofline": {"bound": "hbm", "kernel": kern, "op": dom, "achieved": round(achieved, 1),
+        "roofline": {"bound": "hbm", "kernel": kern.split("<")[0], "op": dom, "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": traffic, "alg_bytes_per_launch": ab[dom],
                      "avg_launch_ms": round(op_ms[dom], 5)},

@@ -25,7 +25,7 @@ HBM_PEAK_GBS = 8000.0  # MI355X HBM3E peak, GB/s
 METRIC = "tokens/s through gate+dispatch+combine; achieved HBM GB/s vs MI355X peak"
 OPS = ("gate", "dispatch", "combine", "combine_bwd", "dispatch_bwd")
 _LAYOUT_SRC = ("layout.hip", "common.hpp", "kernels.hpp")
-_GATE_SRC = ("gate.hip", "route_mfma.hip", "route_mfma_rs.hip", "route_valu.hpp", "route_valu_f32.hip",
+_GATE_SRC = ("gate.hip", "route_mfma.hip", "route_mfma_rs.hip", "route_mfma_ph.hip", "route_valu.hpp", "route_valu_f32.hip",
              "route_valu_bf16.hip", "select.hpp", "common.hpp", "kernels.hpp")
 # op -> (kernel symbol fragment in traces, sources that kernel is compiled from)
 KERNEL_OF_OP = {"dispatch": ("dispatch_kernel", _LAYOUT_SRC),

@@ -6,10 +6,13 @@
 //   route   logits (the projection x.W of Eq. 1, or read from the caller),
 //           streaming selection (top-k list, per-group top-1, or hash),
 //           softmax weights, and for every 64-token "wave block" a histogram of
-//           its (rank, expert) pairs.  Four variants:
+//           its (rank, expert) pairs.  Five variants:
 //             route_mfma_rs_kernel  bf16, W held in registers (E up to 128,
 //                                d 512..2048): persistent, projection on
 //                                v_mfma_f32_16x16x32_bf16;
+//             route_mfma_ph_kernel  bf16, E in {16, 32, 64, 128}, d a multiple
+//                                of 256: persistent, W^T staged in LDS per
+//                                128 KB K phase;
 //             route_mfma_kernel  other bf16 shapes with E a multiple of 16 up
 //                                to 128: W staged through LDS per K chunk;
 //             route_valu_kernel  any dtype/shape: one thread per token;
@@ -126,6 +129,18 @@ __global__ __launch_bounds__(kBlock) void assign_kernel(AssignArgs a) {
 }
 
 // ---------------------------------------------------------------- launchers
+int device_cu_count() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cached[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cached[dev] = n;
+  }
+  return cached[dev];
+}
+
 hipError_t launch_route(const RouteArgs& a, hipStream_t st) {
   if (a.nb == 0) return hipSuccess;
   if (a.kind == 2) {
@@ -133,7 +148,8 @@ hipError_t launch_route(const RouteArgs& a, hipStream_t st) {
     route_hash_kernel<<<dim3(blocks), dim3(kBlock), static_cast<size_t>(kWavesPerBlock) * a.E * sizeof(int), st>>>(a);
     return hipGetLastError();
   }
-  if (route_uses_mfma_rs(a)) return launch_route_mfma_rs(a, st);
+  if (route_uses_mfma_rs(a)) return launch_route_mfma_rs(a, device_cu_count(), st);
+  if (route_uses_mfma_ph(a)) return launch_route_mfma_ph(a, device_cu_count(), st);
   if (route_uses_mfma(a)) return launch_route_mfma(a, st);
   // with logits given, the element type of x and wg is irrelevant
   if (a.dtype == 1 && !a.logits_in) return launch_route_valu_bf16(a, st);

@@ -55,7 +55,11 @@ hipError_t launch_route_valu_f32(const RouteArgs& a, hipStream_t st);
 hipError_t launch_route_valu_bf16(const RouteArgs& a, hipStream_t st);
 hipError_t launch_route_mfma(const RouteArgs& a, hipStream_t st);
 bool route_uses_mfma(const RouteArgs& a);
-hipError_t launch_route_mfma_rs(const RouteArgs& a, hipStream_t st);
+hipError_t launch_route_mfma_rs(const RouteArgs& a, int cus, hipStream_t st);
+hipError_t launch_route_mfma_ph(const RouteArgs& a, int cus, hipStream_t st);
+bool route_uses_mfma_ph(const RouteArgs& a);
+// Compute units of the current device (queried once per device).
+int device_cu_count();
 bool route_uses_mfma_rs(const RouteArgs& a);
 hipError_t launch_scan(const ScanArgs& a, hipStream_t st);
 hipError_t launch_assign(const AssignArgs& a, hipStream_t st);

@@ -166,20 +166,8 @@ bool route_uses_mfma_rs(const RouteArgs& a) {
   return (reinterpret_cast<uintptr_t>(a.x) % 16) == 0;
 }
 
-static int cu_count() {
-  static int cached[64] = {0};
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  if (cached[dev] == 0) {
-    int n = 0;
-    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
-    cached[dev] = n;
-  }
-  return cached[dev];
-}
-
-hipError_t launch_route_mfma_rs(const RouteArgs& a, hipStream_t st) {
-  const int grid = a.nb < cu_count() ? a.nb : cu_count();
+hipError_t launch_route_mfma_rs(const RouteArgs& a, int cus, hipStream_t st) {
+  const int grid = a.nb < cus ? a.nb : cus;
   const int key = a.E * 10000 + a.d;
   switch (key) {
     case 16 * 10000 + 512: return launch_rs_nt<1, 64>(a, grid, st);

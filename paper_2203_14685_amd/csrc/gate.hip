@@ -11,7 +11,7 @@
 //                                d 512..2048): persistent, projection on
 //                                v_mfma_f32_16x16x32_bf16;
 //             route_mfma_ph_kernel  bf16, E in {16, 32, 64, 128}, d a multiple
-//                                of 256: persistent, W^T staged in LDS per
+//                                of 512: persistent, W^T staged in LDS per
 //                                128 KB K phase;
 //             route_mfma_kernel  other bf16 shapes with E a multiple of 16 up
 //                                to 128: W staged through LDS per K chunk;

@@ -1,16 +1,17 @@
 // Phased matrix-core route kernel: the bf16 logit projection x.W of Eq. 1 with
 // softmax and expert selection (Sec. 3.1 top-k / kTop1) for W too large to sit
-// in registers (up to E = 128 experts, d a multiple of 256).
+// in registers (up to E = 128 experts, d a multiple of 512).
 //
 // Persistent blocks of 8 waves, one per CU.  A block takes two wave blocks (128
 // tokens) at a time; wave w owns one 16-token tile.  W^T is staged into LDS in
 // K phases of KP columns (about 128 KB: KP = 65536 / E), transposed on the way
-// in 8 x 8 blocks, so W is read from L2 once per 128 tokens and there are two
+// in 4 x 8 blocks, so W is read from L2 once per 128 tokens and there are two
 // block synchronisations per phase only.  Inside a phase every wave streams its
-// tile of x in 256-column chunks, one chunk ahead, and runs
-// v_mfma_f32_16x16x32_bf16 on B fragments read from LDS (lane group g supplies
-// the contiguous columns [c + 64g, c + 64g + 64) of chunk c; A and B use the
-// same order, so each MFMA sums a fixed permutation of 32 columns).  The logits
+// tile of x in 512-column chunks, one chunk ahead (16 KB per wave in flight:
+// a read stream needs many bytes outstanding per CU), and runs
+// v_mfma_f32_16x16x32_bf16 on B fragments read from LDS (K step ks of chunk c
+// covers columns [c + 32ks, c + 32ks + 32), lane group g the 8 at c + 32ks + 8g,
+// so the 4 lanes of a row load 64 contiguous bytes per instruction).  The logits
 // (+ bias) then overwrite the W^T buffer and 4 lanes per token select.
 #include "select.hpp"
 
@@ -21,29 +22,26 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kPhWaves = 8;
 constexpr int kPhThreads = kPhWaves * kWave;
-constexpr int kPhChunk = 256;             // columns per streamed chunk
+constexpr int kPhChunk = 512;             // columns per streamed chunk (16 KB per wave in flight)
 constexpr int kPhLdsBytes = 65536 * 2 + 8 * 2 * 128 + 256;  // W^T phase buffer (+ row pads)
 
-__device__ __forceinline__ void transpose8x8_b16_ph(const u32x4 (&in)[8], u32x4 (&out)[8]) {
+// 4 x 8 -> 8 x 4 transpose of bf16: in[j] holds row j (8 half-words); out[i]
+// receives column i (4 half-words in two 32-bit words).
+__device__ __forceinline__ void transpose4x8_b16(const u32x4 (&in)[4], uint2 (&out)[8]) {
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
-    uint32_t wd[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const uint32_t a = in[2 * q][i / 2], b = in[2 * q + 1][i / 2];
-      wd[q] = (i & 1) ? ((a >> 16) | (b & 0xffff0000u)) : ((a & 0xffffu) | (b << 16));
-    }
-    out[i] = u32x4{wd[0], wd[1], wd[2], wd[3]};
+    const uint32_t a0 = in[0][i / 2], a1 = in[1][i / 2], a2 = in[2][i / 2], a3 = in[3][i / 2];
+    if (i & 1) out[i] = uint2{(a0 >> 16) | (a1 & 0xffff0000u), (a2 >> 16) | (a3 & 0xffff0000u)};
+    else out[i] = uint2{(a0 & 0xffffu) | (a1 << 16), (a2 & 0xffffu) | (a3 << 16)};
   }
 }
 
 template <int NT, int KMAX, bool KTOP1>
 __global__ __launch_bounds__(kPhThreads) void route_mfma_ph_kernel(RouteArgs a) {
   constexpr int E = NT * 16;
-  constexpr int KP = 65536 / E;        // columns per phase (a multiple of 256)
+  constexpr int KP = 65536 / E;        // columns per phase (a multiple of 512)
   constexpr int LDW = KP + 8;          // padded LDS row of W^T (bf16 elements)
-  constexpr int KG = kPhChunk / 4;     // columns per lane group per chunk
-  constexpr int KSTEPS = KG / 8;       // MFMA K steps per chunk
+  constexpr int KSTEPS = kPhChunk / 32;  // MFMA K steps per chunk
   static_assert(E * LDW * 2 <= kPhLdsBytes, "phase buffer");
   static_assert(E * LDW * 2 >= 2 * kWave * (E + 1) * 4, "logits reuse the phase buffer");
   __shared__ __align__(16) unsigned char lds_raw[kPhLdsBytes];
@@ -73,14 +71,14 @@ __global__ __launch_bounds__(kPhThreads) void route_mfma_ph_kernel(RouteArgs a) 
     const bool tile_live = (w < 4) || hasB;
     const int64_t arow = my_wb * kWave + (w % 4) * 16 + m;
     const bool arow_ok = tile_live && arow < a.S;
-    const u32x4* xa = reinterpret_cast<const u32x4*>(x + arow * d + KG * g);
+    const u32x4* xa = reinterpret_cast<const u32x4*>(x + arow * d + 8 * g);  // + 32 ks per K step
 
     f32x4 acc[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
     u32x4 xcur[KSTEPS], xnxt[KSTEPS];
 #pragma unroll
-    for (int v = 0; v < KSTEPS; ++v) xcur[v] = arow_ok ? xa[v] : zero;
+    for (int v = 0; v < KSTEPS; ++v) xcur[v] = arow_ok ? xa[4 * v] : zero;
 
     for (int c = 0; c < nchunks; ++c) {
       if (c % CPP == 0) {
@@ -88,30 +86,31 @@ __global__ __launch_bounds__(kPhThreads) void route_mfma_ph_kernel(RouteArgs a) 
         const int kp0 = c * kPhChunk;
         const int kp = min(KP, d - kp0);
         __syncthreads();  // previous phase's fragments (or logits) consumed
-        const int nblk = (kp / 8) * (E / 8);
+        const int nblk = (kp / 4) * (E / 8);  // 4 x 8 blocks: 4 columns of 8 experts
         for (int b = tid; b < nblk; b += kPhThreads) {
-          const int kb = (b / (E / 8)) * 8, eb = (b % (E / 8)) * 8;
-          u32x4 rows[8], cols[8];
+          const int kb = (b / (E / 8)) * 4, eb = (b % (E / 8)) * 8;
+          u32x4 rows[4];
+          uint2 cols[8];
 #pragma unroll
-          for (int j = 0; j < 8; ++j)
+          for (int j = 0; j < 4; ++j)
             rows[j] = *reinterpret_cast<const u32x4*>(wg + static_cast<int64_t>(kp0 + kb + j) * E + eb);
-          transpose8x8_b16_ph(rows, cols);
+          transpose4x8_b16(rows, cols);
 #pragma unroll
-          for (int i = 0; i < 8; ++i) *reinterpret_cast<u32x4*>(&wsT[(eb + i) * LDW + kb]) = cols[i];
+          for (int i = 0; i < 8; ++i) *reinterpret_cast<uint2*>(&wsT[(eb + i) * LDW + kb]) = cols[i];
         }
         __syncthreads();
       }
       const bool more = c + 1 < nchunks;
 #pragma unroll
       for (int v = 0; v < KSTEPS; ++v)
-        xnxt[v] = (arow_ok && more) ? xa[(c + 1) * (kPhChunk / 8) + v] : zero;
-      const int kk0 = (c % CPP) * kPhChunk + KG * g;  // column of this lane group inside the phase
+        xnxt[v] = (arow_ok && more) ? xa[(c + 1) * (kPhChunk / 8) + 4 * v] : zero;
+      const int kk0 = (c % CPP) * kPhChunk + 8 * g;  // column of this lane group inside the phase
 #pragma unroll
       for (int ks = 0; ks < KSTEPS; ++ks) {
         const bf16x8 av = __builtin_bit_cast(bf16x8, xcur[ks]);
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt) {
-          const u32x4 braw = *reinterpret_cast<const u32x4*>(&wsT[(nt * 16 + m) * LDW + kk0 + 8 * ks]);
+          const u32x4 braw = *reinterpret_cast<const u32x4*>(&wsT[(nt * 16 + m) * LDW + kk0 + 32 * ks]);
           acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf16x8, braw), acc[nt], 0, 0, 0);
         }
       }

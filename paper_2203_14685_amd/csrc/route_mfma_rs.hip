@@ -8,9 +8,9 @@
 // once per CU.  The block then streams 16-token tiles of x: each wave loads the
 // tile's columns of its slice (one tile ahead), runs KSL/32 x NT
 // v_mfma_f32_16x16x32_bf16, and the 8 partial 16 x E tiles are summed in a
-// fixed order through LDS.  Lane group g = lane/16 of a wave supplies the
-// contiguous columns [w*KSL + g*KSL/4, +KSL/4) of its slice; A and B use the
-// same column order, so every MFMA sums a fixed permutation of 32 columns.
+// fixed order through LDS.  K step ks of wave w covers the columns
+// [w*KSL + 32ks, +32) and lane group g = lane/16 the 8 at w*KSL + 32ks + 8g, so
+// the 4 lanes of a row load 64 contiguous bytes per instruction.
 // After four tiles (one 64-token wave block) the block selects with 8 lanes
 // per token (each lane streams E/8 experts, then a butterfly merge) and writes
 // the wave block's (rank, expert) histogram.
@@ -30,7 +30,6 @@ template <int NT, int KSL, int KMAX, bool KTOP1>
 __global__ __launch_bounds__(kRsThreads) void route_mfma_rs_kernel(RouteArgs a) {
   constexpr int E = NT * 16;
   constexpr int KSTEPS = KSL / 32;  // MFMA K steps per tile per wave
-  constexpr int KGW = KSL / 4;      // contiguous columns per lane group
   static_assert(KSTEPS * NT <= 16, "W^T fragments must fit the register budget");
   __shared__ float part[kRsWaves * kTileTokens * E];   // per-wave partial logits of one tile
   __shared__ float lg[kGroupTokens * (E + 1)];         // logits (+ bias) of the current wave block
@@ -41,7 +40,7 @@ __global__ __launch_bounds__(kRsThreads) void route_mfma_rs_kernel(RouteArgs a) 
   const int lane = lane_id();
   const int g = lane / 16, m = lane % 16;
   const int d = a.d;
-  const int kbase = w * KSL + KGW * g;
+  const int kbase = w * KSL + 8 * g;  // + 32 ks per K step
   const uint16_t* wg = reinterpret_cast<const uint16_t*>(a.wg);
   const uint16_t* x = reinterpret_cast<const uint16_t*>(a.x);
 
@@ -52,7 +51,7 @@ __global__ __launch_bounds__(kRsThreads) void route_mfma_rs_kernel(RouteArgs a) 
   for (int ks = 0; ks < KSTEPS; ++ks) {
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
-      const uint16_t* col = wg + static_cast<int64_t>(kbase + 8 * ks) * E + nt * 16 + m;
+      const uint16_t* col = wg + static_cast<int64_t>(kbase + 32 * ks) * E + nt * 16 + m;
       uint32_t p[4];
 #pragma unroll
       for (int q = 0; q < 4; ++q)
@@ -75,7 +74,7 @@ __global__ __launch_bounds__(kRsThreads) void route_mfma_rs_kernel(RouteArgs a) 
     const int64_t row = tile_row(0);
     const u32x4* src = reinterpret_cast<const u32x4*>(x + row * d + kbase);
 #pragma unroll
-    for (int v = 0; v < KSTEPS; ++v) xcur[v] = (ntiles > 0 && row < a.S) ? src[v] : zero;
+    for (int v = 0; v < KSTEPS; ++v) xcur[v] = (ntiles > 0 && row < a.S) ? src[4 * v] : zero;
   }
 
   for (int q = 0; q < ntiles; ++q) {
@@ -90,7 +89,7 @@ __global__ __launch_bounds__(kRsThreads) void route_mfma_rs_kernel(RouteArgs a) 
       const u32x4* src = reinterpret_cast<const u32x4*>(x + row * d + kbase);
       const bool ok = q + 1 < ntiles && row < a.S;
 #pragma unroll
-      for (int v = 0; v < KSTEPS; ++v) xnxt[v] = ok ? src[v] : zero;
+      for (int v = 0; v < KSTEPS; ++v) xnxt[v] = ok ? src[4 * v] : zero;
     }
     f32x4 acc[NT];
 #pragma unroll

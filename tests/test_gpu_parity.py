@@ -140,7 +140,8 @@ def test_projection_odd_shapes(dtype, d, E, k):
     (64, 2, 0, 1, 512, True, 20000),
     # W^T staged per K phase (persistent, one block per CU); S = 40000 gives some
     # blocks three wave blocks, one of them without a partner
-    (64, 2, 0, 1, 1280, True, 40000), (128, 1, 1, 0, 768, False, 3000), (16, 4, 0, 1, 256, True, 300),
+    (64, 2, 0, 1, 1536, True, 40000), (128, 1, 1, 0, 1024, False, 3000), (16, 4, 0, 1, 4096, True, 300),
+    (64, 4, 1, 0, 3072, True, 300), (32, 8, 0, 1, 4096, False, 700),
 ])
 def test_mfma_projection_shapes(E, k, kind, normalize, d, bias, S):
     """bf16 shapes that take the matrix-core route kernels (E a multiple of 16 up

@@ -251,12 +251,11 @@ def main():
         hm.moe_gate(params, x if learned else None, wg, bias, tok if not learned else None, None, ids, slots,
                     weights, counts, demand, slot_src, ws, stream)
         mark(1)
-        hm.moe_dispatch(lay, x, slot_src, xe, stream)
+        hm.moe_dispatch(lay, x, ids, slots, slot_src, xe, stream)
         mark(2)
         hm.moe_combine(lay, xe, ids, slots, weights, y, stream)
         mark(3)
-        hm.moe_combine_bwd(lay, dy, xe if want_dw else None, slots if want_dw else None, slot_src, weights,
-                           dye, dw, stream)
+        hm.moe_combine_bwd(lay, dy, xe if want_dw else None, ids, slots, slot_src, weights, dye, dw, stream)
         mark(4)
         hm.moe_dispatch_bwd(lay, dye, ids, slots, dx, stream)
         mark(5)

@@ -52,7 +52,7 @@
 extern "C" {
 #endif
 
-#define MOE_ABI_VERSION 1
+#define MOE_ABI_VERSION 2
 
 /* Symbols of the C ABI are the only ones the shared library exports. */
 #define MOE_API __attribute__((visibility("default")))
@@ -143,10 +143,13 @@ MOE_API moe_status moe_gate(const moe_gate_params* p, const void* x, const void*
  * transform): tokens routed to one expert become one contiguous buffer.
  *   xe[e,c,:] = x[slot_src[e,c] / k, :]   if slot_src[e,c] >= 0   (bit copy)
  *   xe[e,c,:] = 0                          otherwise
- * x [S,d], slot_src [E,C] as written by moe_gate, xe [E,C,d] output.
+ * x [S,d]; ids, slots [S,k] and slot_src [E,C] as written by one moe_gate call
+ * (the kernel walks tokens through ids/slots when k > 1, so that each row of x
+ * is read once, and slots through slot_src when k = 1); xe [E,C,d] output.
  */
-MOE_API moe_status moe_dispatch(const moe_layout* l, const void* x, const int32_t* slot_src,
-                        void* xe, hipStream_t stream);
+MOE_API moe_status moe_dispatch(const moe_layout* l, const void* x, const int32_t* ids,
+                                const int32_t* slots, const int32_t* slot_src, void* xe,
+                                hipStream_t stream);
 
 /*
  * moe_combine -- step 6 of Algorithm 1 (Reverse_Layout_Transform) with the gate
@@ -173,13 +176,14 @@ MOE_API moe_status moe_dispatch_bwd(const moe_layout* l, const void* dxe, const 
  *   dye[e,c,:] = 0                         for empty slots
  *   dw[s,r]    = sum_j dy[s,j] * ye[e,c,j] for the slot (e,c) holding (s,r)
  *   dw[s,r]    = 0                          for dropped choices (slots[s,r] == -1)
- * dy [S,d], ye [E,C,d] (NULL iff dw is NULL), slots [S,k] (NULL iff dw is NULL),
- * slot_src [E,C], weights [S,k]; outputs dye [E,C,d] and dw [S,k] fp32 or NULL.
+ * dy [S,d]; ye [E,C,d] (NULL iff dw is NULL); ids, slots [S,k], slot_src [E,C]
+ * and weights [S,k] as written by one moe_gate call; outputs dye [E,C,d] and
+ * dw [S,k] fp32 or NULL.
  */
 MOE_API moe_status moe_combine_bwd(const moe_layout* l, const void* dy, const void* ye,
-                           const int32_t* slots, const int32_t* slot_src,
-                           const float* weights, void* dye, float* dw,
-                           hipStream_t stream);
+                                   const int32_t* ids, const int32_t* slots,
+                                   const int32_t* slot_src, const float* weights, void* dye,
+                                   float* dw, hipStream_t stream);
 
 /* Static description of a status code. */
 MOE_API const char* moe_status_string(moe_status s);

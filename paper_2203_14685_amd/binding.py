@@ -65,10 +65,10 @@ def load():
     lib.moe_gate_workspace_size.argtypes = [ctypes.POINTER(GateParams), ctypes.POINTER(ctypes.c_size_t)]
     lib.moe_gate.argtypes = [ctypes.POINTER(GateParams), vp, vp, f32p, i32p, f32p, i32p, i32p, f32p,
                              i32p, i32p, i32p, vp, ctypes.c_size_t, vp]
-    lib.moe_dispatch.argtypes = [ctypes.POINTER(Layout), vp, i32p, vp, vp]
+    lib.moe_dispatch.argtypes = [ctypes.POINTER(Layout), vp, i32p, i32p, i32p, vp, vp]
     lib.moe_combine.argtypes = [ctypes.POINTER(Layout), vp, i32p, i32p, f32p, vp, vp]
     lib.moe_dispatch_bwd.argtypes = [ctypes.POINTER(Layout), vp, i32p, i32p, vp, vp]
-    lib.moe_combine_bwd.argtypes = [ctypes.POINTER(Layout), vp, vp, i32p, i32p, f32p, vp, f32p, vp]
+    lib.moe_combine_bwd.argtypes = [ctypes.POINTER(Layout), vp, vp, i32p, i32p, i32p, f32p, vp, f32p, vp]
     for name in ("moe_gate_workspace_size", "moe_gate", "moe_dispatch", "moe_combine",
                  "moe_dispatch_bwd", "moe_combine_bwd"):
         getattr(lib, name).restype = ctypes.c_int
@@ -145,10 +145,11 @@ def _layout(S, d, E, k, capacity, dtype):
     return Layout(S, d, E, k, capacity, dtype)
 
 
-def moe_dispatch(layout, x, slot_src, xe, stream=None):
+def moe_dispatch(layout, x, ids, slots, slot_src, xe, stream=None):
     dt = torch.bfloat16 if layout.dtype == MOE_BF16 else torch.float32
-    _check(load().moe_dispatch(ctypes.byref(layout), _ptr(x, dt, "x"), _ptr(slot_src, torch.int32, "slot_src"),
-                               _ptr(xe, dt, "xe"), _stream(stream)))
+    i32 = torch.int32
+    _check(load().moe_dispatch(ctypes.byref(layout), _ptr(x, dt, "x"), _ptr(ids, i32, "ids"), _ptr(slots, i32, "slots"),
+                               _ptr(slot_src, i32, "slot_src"), _ptr(xe, dt, "xe"), _stream(stream)))
 
 
 def moe_combine(layout, ye, ids, slots, weights, y, stream=None):
@@ -164,10 +165,11 @@ def moe_dispatch_bwd(layout, dxe, ids, slots, dx, stream=None):
                                    _ptr(slots, torch.int32, "slots"), _ptr(dx, dt, "dx"), _stream(stream)))
 
 
-def moe_combine_bwd(layout, dy, ye, slots, slot_src, weights, dye, dw, stream=None):
+def moe_combine_bwd(layout, dy, ye, ids, slots, slot_src, weights, dye, dw, stream=None):
     dt = torch.bfloat16 if layout.dtype == MOE_BF16 else torch.float32
-    _check(load().moe_combine_bwd(ctypes.byref(layout), _ptr(dy, dt, "dy"), _ptr(ye, dt, "ye"),
-                                  _ptr(slots, torch.int32, "slots"), _ptr(slot_src, torch.int32, "slot_src"),
+    i32 = torch.int32
+    _check(load().moe_combine_bwd(ctypes.byref(layout), _ptr(dy, dt, "dy"), _ptr(ye, dt, "ye"), _ptr(ids, i32, "ids"),
+                                  _ptr(slots, i32, "slots"), _ptr(slot_src, i32, "slot_src"),
                                   _ptr(weights, torch.float32, "weights"), _ptr(dye, dt, "dye"),
                                   _ptr(dw, torch.float32, "dw"), _stream(stream)))
 
@@ -209,11 +211,12 @@ def gate(kind, k, E, capacity, *, x=None, wg=None, bias=None, token_ids=None, lo
     return out
 
 
-def dispatch(x, slot_src, k, stream=None):
+def dispatch(x, ids, slots, slot_src, stream=None):
     S, d = x.shape
+    k = ids.shape[1]
     E, C = slot_src.shape
     xe = torch.empty((E, C, d), dtype=x.dtype, device=x.device)
-    moe_dispatch(_layout(S, d, E, k, C, _dtype_code(x)), x, slot_src, xe, stream)
+    moe_dispatch(_layout(S, d, E, k, C, _dtype_code(x)), x, ids, slots, slot_src, xe, stream)
     return xe
 
 
@@ -233,12 +236,12 @@ def dispatch_bwd(dxe, ids, slots, stream=None):
     return dx
 
 
-def combine_bwd(dy, slot_src, weights, ye=None, slots=None, want_dw=True, stream=None):
+def combine_bwd(dy, ids, slots, slot_src, weights, ye=None, want_dw=True, stream=None):
     S, d = dy.shape
     E, C = slot_src.shape
     k = weights.shape[1]
     dye = torch.empty((E, C, d), dtype=dy.dtype, device=dy.device)
     dw = torch.empty((S, k), dtype=torch.float32, device=dy.device) if want_dw else None
-    moe_combine_bwd(_layout(S, d, E, k, C, _dtype_code(dy)), dy, ye if want_dw else None,
-                    slots if want_dw else None, slot_src, weights, dye, dw, stream)
+    moe_combine_bwd(_layout(S, d, E, k, C, _dtype_code(dy)), dy, ye if want_dw else None, ids, slots, slot_src,
+                    weights, dye, dw, stream)
     return dye, dw

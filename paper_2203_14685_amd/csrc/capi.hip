@@ -197,17 +197,20 @@ moe_status moe_gate(const moe_gate_params* p, const void* x, const void* wg, con
   return ok();
 }
 
-moe_status moe_dispatch(const moe_layout* l, const void* x, const int32_t* slot_src, void* xe,
-                        hipStream_t stream) {
+moe_status moe_dispatch(const moe_layout* l, const void* x, const int32_t* ids, const int32_t* slots,
+                        const int32_t* slot_src, void* xe, hipStream_t stream) {
   static const char* who = "moe_dispatch";
   CHECK(check_layout(l, who));
   const int64_t rows = static_cast<int64_t>(l->E) * l->capacity;
+  const int64_t Sk = static_cast<int64_t>(l->S) * l->k;
   CHECK(need(x, static_cast<int64_t>(l->S) * l->d, 16, who, "x"));
+  CHECK(need(ids, Sk, 4, who, "ids"));
+  CHECK(need(slots, Sk, 4, who, "slots"));
   CHECK(need(slot_src, rows, 4, who, "slot_src"));
   CHECK(need(xe, rows * l->d, 16, who, "xe"));
   RowArgs a{};
   a.rows = rows; a.nch = nchunks(l); a.S = l->S; a.E = l->E; a.k = l->k; a.C = l->capacity; a.dtype = l->dtype;
-  a.src = x; a.slot_src = slot_src; a.dst = xe;
+  a.src = x; a.ids = ids; a.slots = slots; a.slot_src = slot_src; a.dst = xe;
   const hipError_t err = launch_dispatch(a, stream);
   if (err != hipSuccess) return hip_fail(err, "moe_dispatch: kernel launch");
   return ok();
@@ -241,27 +244,29 @@ moe_status moe_dispatch_bwd(const moe_layout* l, const void* dxe, const int32_t*
   return combine_common("moe_dispatch_bwd", l, dxe, ids, slots, nullptr, dx, false, stream);
 }
 
-moe_status moe_combine_bwd(const moe_layout* l, const void* dy, const void* ye, const int32_t* slots,
-                           const int32_t* slot_src, const float* weights, void* dye, float* dw,
-                           hipStream_t stream) {
+moe_status moe_combine_bwd(const moe_layout* l, const void* dy, const void* ye, const int32_t* ids,
+                           const int32_t* slots, const int32_t* slot_src, const float* weights, void* dye,
+                           float* dw, hipStream_t stream) {
   static const char* who = "moe_combine_bwd";
   CHECK(check_layout(l, who));
   const int64_t S = l->S, k = l->k;
   const int64_t rows = static_cast<int64_t>(l->E) * l->capacity;
   CHECK(need(dy, S * l->d, 16, who, "dy"));
+  CHECK(need(ids, S * k, 4, who, "ids"));
+  CHECK(need(slots, S * k, 4, who, "slots"));
   CHECK(need(slot_src, rows, 4, who, "slot_src"));
   CHECK(need(weights, S * k, 4, who, "weights"));
   CHECK(need(dye, rows * l->d, 16, who, "dye"));
   if (dw) {
     CHECK(need(ye, rows * l->d, 16, who, "ye"));
-    CHECK(need(slots, S * k, 4, who, "slots"));
     CHECK(need(dw, S * k, 4, who, "dw"));
-  } else if (ye || slots) {
-    return fail(MOE_ERR_INVALID_ARG, "%s: ye and slots must be NULL when dw is NULL", who);
+  } else if (ye) {
+    return fail(MOE_ERR_INVALID_ARG, "%s: ye must be NULL when dw is NULL", who);
   }
   RowArgs a{};
   a.rows = rows; a.nch = nchunks(l); a.S = l->S; a.E = l->E; a.k = l->k; a.C = l->capacity; a.dtype = l->dtype;
-  a.src = dy; a.aux = ye; a.slots = slots; a.slot_src = slot_src; a.weights = weights; a.dst = dye; a.dw = dw;
+  a.src = dy; a.aux = ye; a.ids = ids; a.slots = slots; a.slot_src = slot_src; a.weights = weights; a.dst = dye;
+  a.dw = dw;
   const hipError_t err = launch_combine_bwd(a, stream);
   if (err != hipSuccess) return hip_fail(err, "moe_combine_bwd: kernel launch");
   return ok();

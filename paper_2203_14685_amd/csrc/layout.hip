@@ -1,6 +1,9 @@
 // Layout-transform kernels for gfx950: steps 2 and 6 of Algorithm 1 and their
-// gradients.  All four are gathers: every output row has exactly one writer,
-// so there are no atomics and results are bitwise reproducible.
+// gradients.  Every output row has exactly one writer, so there are no atomics
+// and results are bitwise reproducible.  Outputs indexed by token (combine,
+// dispatch backward) are gathers; outputs indexed by expert slot (dispatch,
+// combine backward) are gathers over slots for k = 1 and token-major scatters
+// for k > 1, so that each token row is read once.
 //
 // One wavefront owns one output row and walks it in 16-byte chunks (64 lanes x
 // 16 B = 1 KiB per instruction), issuing up to kUnroll loads per lane before
@@ -169,12 +172,150 @@ __global__ __launch_bounds__(kWideWaves * kWave) void combine_bwd_kernel(RowArgs
   }
 }
 
+// ---------------------------------------------------------------- token-major forms (k > 1)
+// With several choices per token, the slot-major gathers above read each token
+// row once per kept choice.  These forms read it once: blocks [0, tok_blocks)
+// take one token per wave and write (or, backward, scale and dot) its kept
+// rows; the remaining blocks stride over the expert slots and zero the empty
+// ones.  Each output row still has exactly one writer.
+constexpr int kZeroBlocks = 1024;
+
+__device__ __forceinline__ void zero_empty_rows(const RowArgs& a, int64_t first_wave, int64_t nwaves, int lane) {
+  const u32x4 z = {0u, 0u, 0u, 0u};
+  for (int64_t row = first_wave; row < a.rows; row += nwaves) {
+    const int src = a.slot_src[row];
+    if (src >= 0 && src < a.S * a.k) continue;
+    u32x4* dst = reinterpret_cast<u32x4*>(a.dst) + row * a.nch;
+    for (int i = lane; i < a.nch; i += kWave) store_nt(dst + i, z);
+  }
+}
+
+// xe[ids[s,r], slots[s,r]] = x[s] for every kept (s, r); empty slots zero.
+__global__ __launch_bounds__(kWideWaves * kWave) void dispatch_scatter_kernel(RowArgs a, int64_t tok_blocks) {
+  const int lane = lane_id();
+  const int wave = threadIdx.x / kWave;
+  if (static_cast<int64_t>(blockIdx.x) >= tok_blocks) {
+    zero_empty_rows(a, (static_cast<int64_t>(blockIdx.x) - tok_blocks) * kWideWaves + wave,
+                    static_cast<int64_t>(gridDim.x - tok_blocks) * kWideWaves, lane);
+    return;
+  }
+  const int64_t s = static_cast<int64_t>(blockIdx.x) * kWideWaves + wave;
+  if (s >= a.S) return;
+  const int nch = a.nch, k = a.k;
+  const u32x4* srow = reinterpret_cast<const u32x4*>(a.src) + s * nch;
+  for (int base = 0; base < nch; base += kWave * kUnroll) {
+    u32x4 v[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int i = base + u * kWave + lane;
+      if (i < nch) v[u] = srow[i];
+    }
+    for (int r = 0; r < k; ++r) {
+      const int slot = a.slots[s * k + r];
+      const int e = a.ids[s * k + r];
+      if (slot < 0 || slot >= a.C || e < 0 || e >= a.E) continue;
+      u32x4* dst = reinterpret_cast<u32x4*>(a.dst) + (static_cast<int64_t>(e) * a.C + slot) * nch;
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        const int i = base + u * kWave + lane;
+        if (i < nch) store_nt(dst + i, v[u]);
+      }
+    }
+  }
+}
+
+// For every kept (s, r): dye[ids, slots] = w[s,r] * dy[s] and, with DW,
+// dw[s,r] = <dy[s], ye[ids, slots]>; dropped choices get dw = 0; empty slots
+// of dye are zero.
+template <typename T, bool DW>
+__global__ __launch_bounds__(kWideWaves * kWave) void combine_bwd_scatter_kernel(RowArgs a, int64_t tok_blocks) {
+  constexpr int kEl = Chunk<T>::kElems;
+  const int lane = lane_id();
+  const int wave = threadIdx.x / kWave;
+  if (static_cast<int64_t>(blockIdx.x) >= tok_blocks) {
+    zero_empty_rows(a, (static_cast<int64_t>(blockIdx.x) - tok_blocks) * kWideWaves + wave,
+                    static_cast<int64_t>(gridDim.x - tok_blocks) * kWideWaves, lane);
+    return;
+  }
+  const int64_t s = static_cast<int64_t>(blockIdx.x) * kWideWaves + wave;
+  if (s >= a.S) return;
+  const int nch = a.nch, k = a.k;
+  const u32x4* dyrow = reinterpret_cast<const u32x4*>(a.src) + s * nch;
+  float dot[8];
+#pragma unroll
+  for (int r = 0; r < 8; ++r) dot[r] = 0.f;
+  for (int base = 0; base < nch; base += kWave * kUnroll) {
+    u32x4 v[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int i = base + u * kWave + lane;
+      if (i < nch) v[u] = dyrow[i];
+    }
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      if (r >= k) break;
+      const int slot = a.slots[s * k + r];
+      const int e = a.ids[s * k + r];
+      if (slot < 0 || slot >= a.C || e < 0 || e >= a.E) continue;
+      const float w = a.weights[s * k + r];
+      const int64_t row = static_cast<int64_t>(e) * a.C + slot;
+      u32x4* dst = reinterpret_cast<u32x4*>(a.dst) + row * nch;
+      const u32x4* yerow = reinterpret_cast<const u32x4*>(a.aux) + row * nch;
+      u32x4 ve[DW ? kUnroll : 1];
+      if constexpr (DW) {
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+          const int i = base + u * kWave + lane;
+          if (i < nch) ve[u] = yerow[i];
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        const int i = base + u * kWave + lane;
+        if (i < nch) {
+          float f[kEl];
+          Chunk<T>::unpack(v[u], f);
+          if constexpr (DW) {
+            float gq[kEl];
+            Chunk<T>::unpack(ve[u], gq);
+#pragma unroll
+            for (int q = 0; q < kEl; ++q) dot[r] = fmaf(f[q], gq[q], dot[r]);
+          }
+#pragma unroll
+          for (int q = 0; q < kEl; ++q) f[q] *= w;
+          store_nt(dst + i, Chunk<T>::pack(f));
+        }
+      }
+    }
+  }
+  if constexpr (DW) {
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      if (r >= k) break;
+      const float t = wave_sum(dot[r]);
+      if (lane == 0) a.dw[s * k + r] = (a.slots[s * k + r] >= 0) ? t : 0.f;
+    }
+  }
+}
+
 // ---------------------------------------------------------------- launchers
 static inline unsigned blocks_for_rows(int64_t rows, int waves) {
   return static_cast<unsigned>((rows + waves - 1) / waves);
 }
 
+static unsigned zero_blocks(int64_t rows) {
+  const int64_t b = (rows + kWideWaves - 1) / kWideWaves;
+  return static_cast<unsigned>(b < kZeroBlocks ? b : kZeroBlocks);
+}
+
 hipError_t launch_dispatch(const RowArgs& a, hipStream_t st) {
+  if (a.k > 1) {
+    const int64_t tok_blocks = (static_cast<int64_t>(a.S) + kWideWaves - 1) / kWideWaves;
+    const unsigned grid = static_cast<unsigned>(tok_blocks) + zero_blocks(a.rows);
+    if (grid == 0) return hipSuccess;
+    dispatch_scatter_kernel<<<dim3(grid), dim3(kWideWaves * kWave), 0, st>>>(a, tok_blocks);
+    return hipGetLastError();
+  }
   if (a.rows == 0) return hipSuccess;
   dispatch_kernel<<<dim3(blocks_for_rows(a.rows, kWideWaves)), dim3(kWideWaves * kWave), 0, st>>>(a);
   return hipGetLastError();
@@ -195,6 +336,20 @@ hipError_t launch_combine(const RowArgs& a, bool weighted, hipStream_t st) {
 
 hipError_t launch_combine_bwd(const RowArgs& a, hipStream_t st) {
   constexpr int kThreads = kWideWaves * kWave;
+  if (a.k > 1) {
+    const int64_t tok_blocks = (static_cast<int64_t>(a.S) + kWideWaves - 1) / kWideWaves;
+    const unsigned grid = static_cast<unsigned>(tok_blocks) + zero_blocks(a.rows);
+    if (grid == 0) return hipSuccess;
+    const dim3 block(kThreads);
+    if (a.dtype == 1) {
+      if (a.dw) combine_bwd_scatter_kernel<bf16_t, true><<<dim3(grid), block, 0, st>>>(a, tok_blocks);
+      else combine_bwd_scatter_kernel<bf16_t, false><<<dim3(grid), block, 0, st>>>(a, tok_blocks);
+    } else {
+      if (a.dw) combine_bwd_scatter_kernel<float, true><<<dim3(grid), block, 0, st>>>(a, tok_blocks);
+      else combine_bwd_scatter_kernel<float, false><<<dim3(grid), block, 0, st>>>(a, tok_blocks);
+    }
+    return hipGetLastError();
+  }
   const int64_t row_blocks = blocks_for_rows(a.rows, kWideWaves);
   const int64_t dw_blocks = a.dw ? (static_cast<int64_t>(a.S) * a.k + kThreads - 1) / kThreads : 0;
   if (row_blocks + dw_blocks == 0) return hipSuccess;

@@ -105,7 +105,7 @@ def check_layout_ops(w, x_host, ids, slots, weights, slot_src, E, C, k, seed=0):
     d_w, d_src = wl.to_device(weights.astype(np.float32), "f32"), wl.to_device(slot_src, "f32")
     stats = {}
     # dispatch: bit copy
-    xe = wl.to_host(hm.dispatch(wl.to_device(x_host, dt), d_src, k))
+    xe = wl.to_host(hm.dispatch(wl.to_device(x_host, dt), d_ids, d_slots, d_src))
     assert_equal(xe, oracle.dispatch(x_host, slot_src, k), "dispatch xe")
     # combine on random expert outputs
     ye = wl.make_rows((E, C, d), dt, seed + 3)
@@ -120,12 +120,12 @@ def check_layout_ops(w, x_host, ids, slots, weights, slot_src, E, C, k, seed=0):
     # combine backward, with and without dw
     dy = wl.make_rows((S, d), dt, seed + 2)
     d_dy, d_ye = wl.to_device(dy, dt), wl.to_device(ye, dt)
-    dye, dw = hm.combine_bwd(d_dy, d_src, d_w, ye=d_ye, slots=d_slots, want_dw=True)
+    dye, dw = hm.combine_bwd(d_dy, d_ids, d_slots, d_src, d_w, ye=d_ye, want_dw=True)
     dye, dw = wl.to_host(dye), wl.to_host(dw)
     dye_ref, dye_mag, dw_ref, dw_mag = oracle.combine_bwd(dy, ye, slot_src, weights.astype(np.float32), k, dt)
     stats["combine_bwd_dye_err"] = assert_close(decode(dye, dt), decode(dye_ref, dt), dye_mag, rt, "combine_bwd dye")
     stats["combine_bwd_dw_err"] = assert_close(dw, dw_ref, dw_mag, RTOL["f32"], "combine_bwd dw")
-    dye2, dw2 = hm.combine_bwd(d_dy, d_src, d_w, want_dw=False)
+    dye2, dw2 = hm.combine_bwd(d_dy, d_ids, d_slots, d_src, d_w, want_dw=False)
     assert dw2 is None
     assert_equal(wl.to_host(dye2), dye, "combine_bwd dye without dw")
     torch.cuda.synchronize()

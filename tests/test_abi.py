@@ -38,7 +38,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_abi_version_and_struct_layout(lib):
-    assert lib.moe_abi_version() == 1
+    assert lib.moe_abi_version() == 2
     assert ctypes.sizeof(b.GateParams) == 48
     assert b.GateParams.hash_seed.offset == 40
     assert ctypes.sizeof(b.Layout) == 24
@@ -93,7 +93,7 @@ def test_row_size_must_be_16_byte_multiple(lib):
     p = hm.gate_params(100, 4, 8, 1, 20, 0, dtype=b.MOE_BF16)        # 8-byte rows
     assert _ws(p)[0] == b.MOE_ERR_UNSUPPORTED
     lay = b.Layout(100, 6, 8, 1, 20, b.MOE_F32)                         # 24-byte rows
-    st = lib.moe_dispatch(ctypes.byref(lay), 16, 16, 16, None)
+    st = lib.moe_dispatch(ctypes.byref(lay), 16, 16, 16, 16, 16, None)
     assert st == b.MOE_ERR_UNSUPPORTED
 
 
@@ -125,14 +125,18 @@ def test_gate_pointer_checks(lib):
 
 def test_layout_pointer_checks(lib):
     lay = b.Layout(100, 256, 8, 2, 20, b.MOE_BF16)
-    assert lib.moe_dispatch(None, A16, A16, A16, None) == b.MOE_ERR_INVALID_ARG
-    assert lib.moe_dispatch(ctypes.byref(lay), A16, A16, A16 + 8, None) == b.MOE_ERR_UNSUPPORTED
-    assert lib.moe_dispatch(ctypes.byref(lay), None, A16, A16, None) == b.MOE_ERR_INVALID_ARG
+    # moe_dispatch(l, x, ids, slots, slot_src, xe, stream)
+    assert lib.moe_dispatch(None, A16, A16, A16, A16, A16, None) == b.MOE_ERR_INVALID_ARG
+    assert lib.moe_dispatch(ctypes.byref(lay), A16, A16, A16, A16, A16 + 8, None) == b.MOE_ERR_UNSUPPORTED
+    assert lib.moe_dispatch(ctypes.byref(lay), None, A16, A16, A16, A16, None) == b.MOE_ERR_INVALID_ARG
+    assert lib.moe_dispatch(ctypes.byref(lay), A16, None, A16, A16, A16, None) == b.MOE_ERR_INVALID_ARG
+    assert lib.moe_dispatch(ctypes.byref(lay), A16, A16, A16 + 2, A16, A16, None) == b.MOE_ERR_INVALID_ARG
     assert lib.moe_combine(ctypes.byref(lay), A16, A16, A16, None, A16, None) == b.MOE_ERR_INVALID_ARG
     assert lib.moe_dispatch_bwd(ctypes.byref(lay), A16, None, A16, A16, None) == b.MOE_ERR_INVALID_ARG
-    # combine_bwd: ye and slots go with dw
-    assert lib.moe_combine_bwd(ctypes.byref(lay), A16, A16, None, A16, A16, A16, None, None) == b.MOE_ERR_INVALID_ARG
-    assert lib.moe_combine_bwd(ctypes.byref(lay), A16, None, A16, A16, A16, A16, A16, None) == b.MOE_ERR_INVALID_ARG
+    # moe_combine_bwd(l, dy, ye, ids, slots, slot_src, weights, dye, dw, stream): ye goes with dw
+    assert lib.moe_combine_bwd(ctypes.byref(lay), A16, A16, A16, A16, A16, A16, A16, None, None) == b.MOE_ERR_INVALID_ARG
+    assert lib.moe_combine_bwd(ctypes.byref(lay), A16, None, A16, A16, A16, A16, A16, A16, None) == b.MOE_ERR_INVALID_ARG
+    assert lib.moe_combine_bwd(ctypes.byref(lay), A16, None, None, A16, A16, A16, A16, None, None) == b.MOE_ERR_INVALID_ARG
     bad = b.Layout(100, 256, 8, 9, 20, b.MOE_BF16)
     assert lib.moe_combine(ctypes.byref(bad), A16, A16, A16, A16, A16, None) == b.MOE_ERR_INVALID_ARG
 
@@ -141,4 +145,5 @@ def test_binding_rejects_cpu_tensors(lib):
     import torch
     x = torch.zeros(4, 8)
     with pytest.raises(ValueError):
-        hm.dispatch(x, torch.zeros((2, 2), dtype=torch.int32), 1)
+        z = torch.zeros((4, 1), dtype=torch.int32)
+        hm.dispatch(x, z, z, torch.zeros((2, 2), dtype=torch.int32))

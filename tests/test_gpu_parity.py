@@ -168,6 +168,22 @@ def test_ktop1_projection_with_bias():
     check_gate(w, inp, g, E, k, C, 1, 0)
 
 
+@pytest.mark.parametrize("dtype,k,C", [("bf16", 8, 40), ("f32", 3, 5), ("bf16", 2, 600)])
+def test_layout_ops_many_choices_and_drops(dtype, k, C):
+    """Dispatch / combine and their backward with k > 1 (token-major scatter for
+    the expert-slot outputs), heavy drops, empty slots and a ragged tail."""
+    S, d, E = 555, 264 if dtype == "bf16" else 132, 12
+    announce(f"layout ops dtype={dtype} k={k} C={C}")
+    rng = np.random.default_rng(k * 7 + C)
+    L = rng.standard_normal((S, E)).astype(np.float32)
+    g = _logits_case(S, E, k, 0, 1, C, L)
+    w = dict(dtype=dtype)
+    x = wl.make_rows((S, d), dtype, 17)
+    st = check_layout_ops(w, x, g["ids"], g["slots"], g["weights"], g["slot_src"], E, C, k, seed=21)
+    assert (g["slots"] < 0).any() or C * E >= S * k
+    print(f"[stats] layout k={k}: {st}", flush=True)
+
+
 def test_determinism_and_guard_bands():
     announce("determinism and guard bands")
     w = W[2]
@@ -183,9 +199,10 @@ def test_determinism_and_guard_bands():
     pad = 64
     x = wl.to_device(inp["x"], "bf16")
     src = wl.to_device(a["slot_src"], "i32")
+    d_ids, d_slots = wl.to_device(a["ids"], "i32"), wl.to_device(a["slots"], "i32")
     buf = torch.full((E * C * d + 2 * pad,), 7.0, dtype=torch.bfloat16, device="cuda")
     xe = buf[pad:pad + E * C * d].view(E, C, d)
-    hm.moe_dispatch(hm.Layout(S, d, E, k, C, hm.MOE_BF16), x, src, xe)
+    hm.moe_dispatch(hm.Layout(S, d, E, k, C, hm.MOE_BF16), x, d_ids, d_slots, src, xe)
     torch.cuda.synchronize()
     assert (buf[:pad] == 7.0).all() and (buf[-pad:] == 7.0).all()
     assert_equal(wl.to_host(xe), oracle.dispatch(inp["x"], a["slot_src"], k), "dispatch into a view")
@@ -218,7 +235,7 @@ def test_full_size_parity(wid):
     d_ids, d_slots = wl.to_device(g["ids"], "i32"), wl.to_device(g["slots"], "i32")
     d_w = wl.to_device(g["weights"], "f32")
     # dispatch: sampled rows bit-exact, plus every empty row zero
-    xe = hm.dispatch(x, d_src, k)
+    xe = hm.dispatch(x, d_ids, d_slots, d_src)
     rows = rng.choice(E * C, size=min(E * C, 2048), replace=False)
     rows = np.concatenate([rows, np.arange(C)])               # all of expert 0
     got = wl.to_host(xe.view(E * C, d)[torch.from_numpy(rows).cuda()])
@@ -243,7 +260,7 @@ def test_full_size_parity(wid):
     st["dispatch_bwd_err"] = assert_close(decode(wl.to_host(dx[torch.from_numpy(toks).cuda()]), dt),
                                           decode(dx_ref, dt), dx_mag, RTOL[dt], "dispatch_bwd sampled tokens")
     dy_host = wl.make_rows((S, d), dt, 2)
-    dye, dw = hm.combine_bwd(wl.to_device(dy_host, dt), d_src, d_w, ye=ye, slots=d_slots, want_dw=True)
+    dye, dw = hm.combine_bwd(wl.to_device(dy_host, dt), d_ids, d_slots, d_src, d_w, ye=ye, want_dw=True)
     src = g["slot_src"].reshape(-1)[rows]
     full = src >= 0
     s_of = np.where(full, src // k, 0)

@@ -226,10 +226,13 @@ __global__ __launch_bounds__(kWideWaves * kWave) void dispatch_scatter_kernel(Ro
 
 // For every kept (s, r): dye[ids, slots] = w[s,r] * dy[s] and, with DW,
 // dw[s,r] = <dy[s], ye[ids, slots]>; dropped choices get dw = 0; empty slots
-// of dye are zero.
+// of dye are zero.  One wave per token walks the row in steps of 4 chunks per
+// lane and issues the loads of up to 4 choices' ye rows together.
 template <typename T, bool DW>
 __global__ __launch_bounds__(kWideWaves * kWave) void combine_bwd_scatter_kernel(RowArgs a, int64_t tok_blocks) {
   constexpr int kEl = Chunk<T>::kElems;
+  constexpr int kU = 4;   // chunks per lane per step
+  constexpr int kRG = 4;  // choices whose rows are loaded together
   const int lane = lane_id();
   const int wave = threadIdx.x / kWave;
   if (static_cast<int64_t>(blockIdx.x) >= tok_blocks) {
@@ -244,46 +247,56 @@ __global__ __launch_bounds__(kWideWaves * kWave) void combine_bwd_scatter_kernel
   float dot[8];
 #pragma unroll
   for (int r = 0; r < 8; ++r) dot[r] = 0.f;
-  for (int base = 0; base < nch; base += kWave * kUnroll) {
-    u32x4 v[kUnroll];
+  for (int base = 0; base < nch; base += kWave * kU) {
+    u32x4 v[kU];
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
+    for (int u = 0; u < kU; ++u) {
       const int i = base + u * kWave + lane;
       if (i < nch) v[u] = dyrow[i];
     }
 #pragma unroll
-    for (int r = 0; r < 8; ++r) {
-      if (r >= k) break;
-      const int slot = a.slots[s * k + r];
-      const int e = a.ids[s * k + r];
-      if (slot < 0 || slot >= a.C || e < 0 || e >= a.E) continue;
-      const float w = a.weights[s * k + r];
-      const int64_t row = static_cast<int64_t>(e) * a.C + slot;
-      u32x4* dst = reinterpret_cast<u32x4*>(a.dst) + row * nch;
-      const u32x4* yerow = reinterpret_cast<const u32x4*>(a.aux) + row * nch;
-      u32x4 ve[DW ? kUnroll : 1];
-      if constexpr (DW) {
+    for (int r0 = 0; r0 < 8; r0 += kRG) {
+      if (r0 >= k) break;
+      int64_t row[kRG];
+      bool kept[kRG];
+      u32x4 ve[DW ? kRG : 1][kU];
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
-          const int i = base + u * kWave + lane;
-          if (i < nch) ve[u] = yerow[i];
+      for (int j = 0; j < kRG; ++j) {
+        const int r = r0 + j;
+        const int slot = (r < k) ? a.slots[s * k + r] : -1;
+        const int e = (r < k) ? a.ids[s * k + r] : -1;
+        kept[j] = slot >= 0 && slot < a.C && e >= 0 && e < a.E;
+        row[j] = kept[j] ? static_cast<int64_t>(e) * a.C + slot : 0;
+        if constexpr (DW) {
+          const u32x4* yerow = reinterpret_cast<const u32x4*>(a.aux) + row[j] * nch;
+#pragma unroll
+          for (int u = 0; u < kU; ++u) {
+            const int i = base + u * kWave + lane;
+            if (kept[j] && i < nch) ve[j][u] = yerow[i];
+          }
         }
       }
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        const int i = base + u * kWave + lane;
-        if (i < nch) {
-          float f[kEl];
-          Chunk<T>::unpack(v[u], f);
-          if constexpr (DW) {
-            float gq[kEl];
-            Chunk<T>::unpack(ve[u], gq);
+      for (int j = 0; j < kRG; ++j) {
+        if (!kept[j]) continue;
+        const float w = a.weights[s * k + r0 + j];
+        u32x4* dst = reinterpret_cast<u32x4*>(a.dst) + row[j] * nch;
 #pragma unroll
-            for (int q = 0; q < kEl; ++q) dot[r] = fmaf(f[q], gq[q], dot[r]);
+        for (int u = 0; u < kU; ++u) {
+          const int i = base + u * kWave + lane;
+          if (i < nch) {
+            float f[kEl];
+            Chunk<T>::unpack(v[u], f);
+            if constexpr (DW) {
+              float gq[kEl];
+              Chunk<T>::unpack(ve[j][u], gq);
+#pragma unroll
+              for (int q = 0; q < kEl; ++q) dot[r0 + j] = fmaf(f[q], gq[q], dot[r0 + j]);
+            }
+#pragma unroll
+            for (int q = 0; q < kEl; ++q) f[q] *= w;
+            store_nt(dst + i, Chunk<T>::pack(f));
           }
-#pragma unroll
-          for (int q = 0; q < kEl; ++q) f[q] *= w;
-          store_nt(dst + i, Chunk<T>::pack(f));
         }
       }
     }

@@ -57,14 +57,33 @@ __global__ __launch_bounds__(kWave) void route_valu_kernel(RouteArgs a) {
         if (valid) {
           const int jend = min(kDJ, a.d - j0);
           const u32x4* xv = reinterpret_cast<const u32x4*>(xrow + j0);
-          for (int c = 0; c < jend / kEl; ++c) {
-            float xe[kEl];
-            Chunk<T>::unpack(xv[c], xe);
+          if (jend == kDJ) {
+            // full chunk: issue all of its loads before the first FMA
+            constexpr int kNC = kDJ / kEl;
+            u32x4 xc[kNC];
 #pragma unroll
-            for (int q = 0; q < kEl; ++q) {
-              const float* wrow = wg_s[c * kEl + q];
+            for (int c = 0; c < kNC; ++c) xc[c] = xv[c];
 #pragma unroll
-              for (int i = 0; i < EC; ++i) acc[i] = fmaf(xe[q], wrow[i], acc[i]);
+            for (int c = 0; c < kNC; ++c) {
+              float xe[kEl];
+              Chunk<T>::unpack(xc[c], xe);
+#pragma unroll
+              for (int q = 0; q < kEl; ++q) {
+                const float* wrow = wg_s[c * kEl + q];
+#pragma unroll
+                for (int i = 0; i < EC; ++i) acc[i] = fmaf(xe[q], wrow[i], acc[i]);
+              }
+            }
+          } else {
+            for (int c = 0; c < jend / kEl; ++c) {
+              float xe[kEl];
+              Chunk<T>::unpack(xv[c], xe);
+#pragma unroll
+              for (int q = 0; q < kEl; ++q) {
+                const float* wrow = wg_s[c * kEl + q];
+#pragma unroll
+                for (int i = 0; i < EC; ++i) acc[i] = fmaf(xe[q], wrow[i], acc[i]);
+              }
             }
           }
         }

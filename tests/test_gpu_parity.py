@@ -128,6 +128,27 @@ def test_projection_odd_shapes(dtype, d, E, k):
     check_layout_ops(w, inp["x"], g["ids"], g["slots"], g["weights"], g["slot_src"], E, C, k, seed=9)
 
 
+@pytest.mark.parametrize("dtype,E,k,kind,normalize,d,bias,S", [
+    ("f32", 8, 1, 0, 0, 2500, True, 1000), ("f32", 16, 2, 0, 1, 4096, False, 2000),
+    ("f32", 32, 4, 1, 0, 1028, True, 1000), ("f32", 64, 8, 0, 1, 300, True, 130),
+    ("f32", 64, 2, 1, 0, 4, False, 65), ("f32", 8, 8, 1, 0, 64, False, 64),
+    ("bf16", 8, 2, 0, 1, 1032, True, 700), ("f32", 32, 3, 0, 0, 516, False, 1),
+])
+def test_split_projection_shapes(dtype, E, k, kind, normalize, d, bias, S):
+    """Projections on the vector ALUs with 8 lanes per token (E in 8..64, d a
+    whole number of 16-byte chunks): W staged in several phases with a ragged
+    last one, ragged token tails, kTop1 groups down to one expert."""
+    announce(f"split projection dtype={dtype} E={E} k={k} kind={kind} d={d} bias={bias} S={S}")
+    w = dict(kind=kind, k=k, normalize=normalize, dtype=dtype, S=S, d=d, E=E, cf=1.0)
+    if bias:
+        w.update(hot_experts=2, hot_bias=0.5)
+    inp = wl.make_inputs(w, seed=3 * E + k)
+    C = cap(1.0, k, S, E)
+    g = gpu_gate(w, inp, E, k, C, kind, normalize)
+    st = check_gate(w, inp, g, E, k, C, kind, normalize)[1]
+    print(f"[stats] split E={E} d={d}: {st}", flush=True)
+
+
 @pytest.mark.parametrize("E,k,kind,normalize,d,bias,S", [
     # W staged through LDS (4 lanes per token select)
     (16, 1, 1, 0, 256, False, 300), (48, 1, 0, 0, 256, False, 300), (64, 4, 1, 0, 768, True, 300),

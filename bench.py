@@ -27,12 +27,20 @@ OPS = ("gate", "dispatch", "combine", "combine_bwd", "dispatch_bwd")
 _LAYOUT_SRC = ("layout.hip", "common.hpp", "kernels.hpp")
 _GATE_SRC = ("gate.hip", "route_mfma.hip", "route_mfma_rs.hip", "route_mfma_ph.hip", "route_valu.hpp", "route_valu_f32.hip",
              "route_valu_bf16.hip", "select.hpp", "common.hpp", "kernels.hpp")
-# op -> (kernel symbol fragment in traces, sources that kernel is compiled from)
-KERNEL_OF_OP = {"dispatch": ("dispatch_kernel", _LAYOUT_SRC),
-                "combine": ("combine_kernel<hetumoe::bf16_t, true>", _LAYOUT_SRC),
-                "combine_bwd": ("combine_bwd_kernel", _LAYOUT_SRC),
-                "dispatch_bwd": ("combine_kernel<hetumoe::bf16_t, false>", _LAYOUT_SRC),
-                "gate": ("route_", _GATE_SRC)}
+OPS_KERNELS = ("dispatch", "combine", "combine_bwd", "dispatch_bwd", "gate")
+
+
+def kernel_of_op(op, w):
+    """(kernel symbol fragment in traces, sources that kernel is compiled from) of
+    the one kernel an op launches for workload dict `w`: with several choices per
+    token dispatch and combine backward scatter token-major."""
+    elt = "hetumoe::bf16_t" if w["dtype"] == "bf16" else "float"
+    scatter = w["k"] > 1
+    return {"dispatch": ("dispatch_scatter_kernel" if scatter else "dispatch_kernel", _LAYOUT_SRC),
+            "combine": (f"combine_kernel<{elt}, true>", _LAYOUT_SRC),
+            "combine_bwd": ("combine_bwd_scatter_kernel" if scatter else "combine_bwd_kernel", _LAYOUT_SRC),
+            "dispatch_bwd": (f"combine_kernel<{elt}, false>", _LAYOUT_SRC),
+            "gate": ("route_", _GATE_SRC)}[op]
 
 
 def summarize_pmc(args):
@@ -63,7 +71,8 @@ def summarize_pmc(args):
         if not copy:
             raise SystemExit(f"{counter}: no calibration copy kernel found")
         scale = calib_bytes / (max(copy) * 1024.0)
-        for op, (frag, _) in KERNEL_OF_OP.items():
+        for op in OPS_KERNELS:
+            frag = kernel_of_op(op, w)[0]
             vals = [float(r["Counter_Value"]) for r in rows if frag in r["Kernel_Name"]]
             if vals:
                 out.setdefault(op, {})[counter] = (sum(vals) / len(vals), len(vals), scale, max(copy))
@@ -73,7 +82,7 @@ def summarize_pmc(args):
         fk, fn, fs, fc = cs["FETCH_SIZE"]
         wk, wn, ws, wc = cs["WRITE_SIZE"]
         total = fk * 1024 * fs + wk * 1024 * ws
-        frag, src = KERNEL_OF_OP[op]
+        frag, src = kernel_of_op(op, w)
         with open(traffic_path(w["name"], op), "w") as f:
             f.write(f"# HBM traffic per launch of {frag} ({op}), workload {w['name']}\n")
             f.write("# from two rocprofv3 counter runs (TMPDIR=/tmp, from /tmp, repo at $R):\n")
@@ -292,7 +301,7 @@ def main():
     step_bytes = sum(ab.values())
     dom = max(("dispatch", "combine", "combine_bwd", "dispatch_bwd", "gate"), key=lambda o: op_ms[o])
     achieved = ab[dom] / (op_ms[dom] * 1e-3) / 1e9
-    kern, ksrc = KERNEL_OF_OP[dom]
+    kern, ksrc = kernel_of_op(dom, w)
     traffic = measured_traffic(w["name"], dom, source_sha(ksrc))
 
     out = {

@@ -108,6 +108,62 @@ __global__ __launch_bounds__(kCombineWaves * kWave) void combine_kernel(RowArgs 
   }
 }
 
+// Short rows (CPR x 64 chunks per row, CPR in {1, 2, 4}): one wave takes
+// RPW = 8 / CPR tokens so that every lane still has 8 loads in flight.  All of
+// a rank's slot, id and weight reads come first; the row loads are then issued
+// unconditionally (a dropped choice reads row 0 of the expert buffer, which
+// needs E * C > 0, and its value is discarded), so no load waits behind a
+// branch on another load's result.
+template <typename T, bool WEIGHTED, int CPR>
+__global__ __launch_bounds__(kCombineWaves * kWave) void combine_short_kernel(RowArgs a) {
+  constexpr int kEl = Chunk<T>::kElems;
+  constexpr int RPW = 8 / CPR;
+  constexpr int nch = CPR * kWave;
+  const int64_t s0 = (static_cast<int64_t>(blockIdx.x) * kCombineWaves + threadIdx.x / kWave) * RPW;
+  if (s0 >= a.rows) return;
+  const int lane = lane_id();
+  const int k = a.k;
+  const u32x4* ye = reinterpret_cast<const u32x4*>(a.src);
+  u32x4* out = reinterpret_cast<u32x4*>(a.dst);
+  float acc[8][kEl];
+#pragma unroll
+  for (int u = 0; u < 8; ++u)
+#pragma unroll
+    for (int q = 0; q < kEl; ++q) acc[u][q] = 0.f;
+  for (int r = 0; r < k; ++r) {
+    int64_t rowoff[RPW];
+    float w[RPW];
+    bool ok[RPW];
+#pragma unroll
+    for (int t = 0; t < RPW; ++t) {
+      const int64_t s = min(s0 + t, a.rows - 1);
+      const int slot = a.slots[s * k + r];
+      const int e = a.ids[s * k + r];
+      w[t] = WEIGHTED ? a.weights[s * k + r] : 1.f;
+      ok[t] = (s0 + t < a.rows) && slot >= 0 && slot < a.C && e >= 0 && e < a.E;
+      rowoff[t] = ok[t] ? (static_cast<int64_t>(e) * a.C + slot) * nch : 0;
+    }
+    u32x4 v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = ye[rowoff[u / CPR] + (u % CPR) * kWave + lane];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      if (ok[u / CPR]) {
+        float f[kEl];
+        Chunk<T>::unpack(v[u], f);
+#pragma unroll
+        for (int q = 0; q < kEl; ++q)
+          acc[u][q] = WEIGHTED ? fmaf(w[u / CPR], f[q], acc[u][q]) : acc[u][q] + f[q];
+      }
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < 8; ++u) {
+    const int64_t s = s0 + u / CPR;
+    if (s < a.rows) store_nt(out + s * nch + (u % CPR) * kWave + lane, Chunk<T>::pack(acc[u]));
+  }
+}
+
 // ---------------------------------------------------------------- combine backward
 // Rows [0, rows): dye[row] = w[src] * dy[src / k] (zeros for an empty slot) and,
 // with DW, dw[src] = <dy[src / k], ye[row]>.  Blocks past the row blocks clear
@@ -334,8 +390,29 @@ hipError_t launch_dispatch(const RowArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
+template <typename T, bool WEIGHTED>
+static void launch_combine_short(const RowArgs& a, hipStream_t st) {
+  const int cpr = a.nch / kWave, rpw = 8 / cpr;
+  const dim3 grid(blocks_for_rows((a.rows + rpw - 1) / rpw, kCombineWaves)), block(kCombineWaves * kWave);
+  if (cpr == 1) combine_short_kernel<T, WEIGHTED, 1><<<grid, block, 0, st>>>(a);
+  else if (cpr == 2) combine_short_kernel<T, WEIGHTED, 2><<<grid, block, 0, st>>>(a);
+  else combine_short_kernel<T, WEIGHTED, 4><<<grid, block, 0, st>>>(a);
+}
+
 hipError_t launch_combine(const RowArgs& a, bool weighted, hipStream_t st) {
   if (a.rows == 0) return hipSuccess;
+  // short rows: several tokens per wave (measured 9-11 % faster at 2 and 4 KiB
+  // rows); longer rows: one token per wave
+  if ((a.nch == 64 || a.nch == 128 || a.nch == 256) && static_cast<int64_t>(a.E) * a.C > 0) {
+    if (a.dtype == 1) {
+      if (weighted) launch_combine_short<bf16_t, true>(a, st);
+      else launch_combine_short<bf16_t, false>(a, st);
+    } else {
+      if (weighted) launch_combine_short<float, true>(a, st);
+      else launch_combine_short<float, false>(a, st);
+    }
+    return hipGetLastError();
+  }
   const dim3 grid(blocks_for_rows(a.rows, kCombineWaves)), block(kCombineWaves * kWave);
   if (a.dtype == 1) {
     if (weighted) combine_kernel<bf16_t, true><<<grid, block, 0, st>>>(a);

@@ -205,6 +205,23 @@ def test_layout_ops_many_choices_and_drops(dtype, k, C):
     print(f"[stats] layout k={k}: {st}", flush=True)
 
 
+@pytest.mark.parametrize("dtype,d,k,S,C", [
+    ("bf16", 512, 1, 517, 40), ("bf16", 1024, 2, 519, 70), ("bf16", 2048, 3, 1, 1), ("f32", 256, 1, 1023, 90),
+    ("f32", 512, 2, 3, 1), ("f32", 1024, 3, 261, 50), ("bf16", 2048, 1, 2, 0),
+])
+def test_layout_ops_short_rows(dtype, d, k, S, C):
+    """Rows of 1, 2 and 4 KiB, where a wave combines several tokens at once: token
+    counts that leave the last wave partly empty, drops, and C = 0."""
+    E = 16
+    announce(f"layout ops short rows dtype={dtype} d={d} k={k} S={S} C={C}")
+    rng = np.random.default_rng(d + k + S)
+    L = rng.standard_normal((S, E)).astype(np.float32)
+    g = _logits_case(S, E, k, 0, 1, C, L)
+    x = wl.make_rows((S, d), dtype, 31)
+    st = check_layout_ops(dict(dtype=dtype), x, g["ids"], g["slots"], g["weights"], g["slot_src"], E, C, k, seed=33)
+    print(f"[stats] short rows d={d}: {st}", flush=True)
+
+
 def test_determinism_and_guard_bands():
     announce("determinism and guard bands")
     w = W[2]

@@ -36,10 +36,14 @@ def kernel_of_op(op, w):
     token dispatch and combine backward scatter token-major."""
     elt = "hetumoe::bf16_t" if w["dtype"] == "bf16" else "float"
     scatter = w["k"] > 1
+    # rows of 64, 128 or 256 16-byte chunks combine several tokens per wave
+    nch = w["d"] * (2 if w["dtype"] == "bf16" else 4) // 16
+    short = nch in (64, 128, 256) and w["E"] * w["C"] > 0
+    comb = f"combine_short_kernel<{elt}, " if short else f"combine_kernel<{elt}, "
     return {"dispatch": ("dispatch_scatter_kernel" if scatter else "dispatch_kernel", _LAYOUT_SRC),
-            "combine": (f"combine_kernel<{elt}, true>", _LAYOUT_SRC),
+            "combine": (comb + ("true," if short else "true>"), _LAYOUT_SRC),
             "combine_bwd": ("combine_bwd_scatter_kernel" if scatter else "combine_bwd_kernel", _LAYOUT_SRC),
-            "dispatch_bwd": (f"combine_kernel<{elt}, false>", _LAYOUT_SRC),
+            "dispatch_bwd": (comb + ("false," if short else "false>"), _LAYOUT_SRC),
             "gate": ("route_", _GATE_SRC)}[op]
 
 
@@ -103,6 +107,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", type=int, default=5, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--graph", action="store_true",
+                    help="time replays of the step captured into a HIP graph (per-op times then come from an "
+                         "eager pass with events)")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="write profiles/traffic_*.txt from two rocprofv3 --pmc output folders and exit")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -252,21 +259,23 @@ def main():
     lay = hm.Layout(S, d, E, k, C, dcode)
     stream = torch.cuda.current_stream()
 
-    def step(evs=None):
+    def step(evs=None, st=None):
+        st = stream if st is None else st
+
         def mark(i):
             if evs is not None:
-                evs[i].record(stream)
+                evs[i].record(st)
         mark(0)
         hm.moe_gate(params, x if learned else None, wg, bias, tok if not learned else None, None, ids, slots,
-                    weights, counts, demand, slot_src, ws, stream)
+                    weights, counts, demand, slot_src, ws, st)
         mark(1)
-        hm.moe_dispatch(lay, x, ids, slots, slot_src, xe, stream)
+        hm.moe_dispatch(lay, x, ids, slots, slot_src, xe, st)
         mark(2)
-        hm.moe_combine(lay, xe, ids, slots, weights, y, stream)
+        hm.moe_combine(lay, xe, ids, slots, weights, y, st)
         mark(3)
-        hm.moe_combine_bwd(lay, dy, xe if want_dw else None, ids, slots, slot_src, weights, dye, dw, stream)
+        hm.moe_combine_bwd(lay, dy, xe if want_dw else None, ids, slots, slot_src, weights, dye, dw, st)
         mark(4)
-        hm.moe_dispatch_bwd(lay, dye, ids, slots, dx, stream)
+        hm.moe_dispatch_bwd(lay, dye, ids, slots, dx, st)
         mark(5)
 
     if args.calib_copy_mib:
@@ -284,14 +293,34 @@ def main():
     print(f"[bench] workload {args.workload} {w['name']}: warmup done", file=sys.stderr, flush=True)
 
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(OPS) + 1)] for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        step(evs[i])
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
+    if args.graph:
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step(None, torch.cuda.current_stream())
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(args.steps):
+            graph.replay()
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        for i in range(args.steps):  # per-op events: an eager pass after the timed region
+            step(evs[i])
+        torch.cuda.synchronize()
+    else:
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(args.steps):
+            step(evs[i])
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
     ms_step = (t1 - t0) * 1e3 / args.steps
     op_ms = {op: sum(e[j].elapsed_time(e[j + 1]) for e in evs) / args.steps for j, op in enumerate(OPS)}
+    step_ev = sorted(e[0].elapsed_time(e[len(OPS)]) for e in evs)
+
+    def pct(v, q):
+        return v[min(len(v) - 1, int(q * len(v)))]
 
     # routing statistics of this batch (outside the timed region)
     sl = slots.cpu().numpy()
@@ -303,6 +332,23 @@ def main():
     achieved = ab[dom] / (op_ms[dom] * 1e-3) / 1e9
     kern, ksrc = kernel_of_op(dom, w)
     traffic = measured_traffic(w["name"], dom, source_sha(ksrc))
+    dom_ev = sorted(e[j].elapsed_time(e[j + 1]) for e in evs for j in [OPS.index(dom)])
+
+    # context, outside the timed region: a plain device-to-device copy moving the
+    # dominant kernel's algorithmic bytes (half read, half written)
+    n_copy = max(1, ab[dom] // 2)
+    ca = torch.empty(n_copy, dtype=torch.uint8, device=dev)
+    cb = torch.empty_like(ca)
+    for _ in range(3):
+        cb.copy_(ca)
+    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    c0.record(stream)
+    for _ in range(10):
+        cb.copy_(ca)
+    c1.record(stream)
+    torch.cuda.synchronize()
+    copy_gbs = 2 * n_copy / (c0.elapsed_time(c1) / 10 * 1e-3) / 1e9
+    del ca, cb
 
     out = {
         "metric": METRIC,
@@ -319,11 +365,16 @@ def main():
         "data": "synthetic",
         "config": {"workload": w["name"], "S": S, "d": d, "E": E, "k": k, "capacity": C,
                    "gate": ["topk", "ktop1", "hash"][w["kind"]], "passes": "fwd+bwd",
-                   "parallelism": "single-gpu"},
+                   "parallelism": "single-gpu", "launch": "hip-graph" if args.graph else "eager"},
         "roofline": {"bound": "hbm", "kernel": kern.split("<")[0], "op": dom, "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": traffic, "alg_bytes_per_launch": ab[dom],
-                     "avg_launch_ms": round(op_ms[dom], 5)},
+                     "avg_launch_ms": round(op_ms[dom], 5),
+                     "launch_ms_p10_p50_p90": [round(pct(dom_ev, q), 5) for q in (0.1, 0.5, 0.9)],
+                     "copy_ceiling": {"GB/s": round(copy_gbs, 1), "frac": round(copy_gbs / HBM_PEAK_GBS, 4),
+                                      "kernel_vs_copy": round(achieved / copy_gbs, 4),
+                                      "what": "device-to-device copy of the same byte count"}},
+        "step_ms_p10_p50_p90": [round(pct(step_ev, q), 5) for q in (0.1, 0.5, 0.9)],
         "step_hbm": {"alg_bytes": step_bytes, "GB/s": round(step_bytes / (ms_step * 1e-3) / 1e9, 1),
                      "frac": round(step_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
         "ops": {op: {"ms": round(op_ms[op], 5), "alg_bytes": ab[op],

@@ -16,7 +16,9 @@ paper it follows:
   to it;
 * Sec. 3.1 kTop1 (expert prototyping) and Hash Layer paragraphs;
 * Sec. 3.2 "Gate Optimization" (top-k over a (num_tokens, num_experts) input)
-  and "Layout Transform Optimization" (tokens of one expert made contiguous).
+  and "Layout Transform Optimization" (tokens of one expert made contiguous);
+* the gradient of Eq. 1 that end-to-end training of the layer (Sec. 2) needs,
+  and a load-balancing loss (reading R16) for the gates of Sec. 3.1.
 
 Where the paper is silent the oracle takes one fixed reading; each is named at
 the function that depends on it (R1..R14 in the design notes).
@@ -43,10 +45,12 @@ from .gate import (
     gate,
 )
 from .layout import dispatch, combine, dispatch_bwd, combine_bwd
+from .gate_bwd import gate_dlogits, aux_loss, gate_input_grads
 
 __all__ = [
     "bf16_to_f64", "f64_to_bf16", "decode", "encode",
     "GATE_TOPK", "GATE_KTOP1", "GATE_HASH", "capacity", "logits", "select",
     "gate_weights", "splitmix64_output", "hash_ids", "assign_slots", "gate",
     "dispatch", "combine", "dispatch_bwd", "combine_bwd",
+    "gate_dlogits", "aux_loss", "gate_input_grads",
 ]

@@ -43,6 +43,17 @@ MUTANTS = [
     ("bf16.py", "ulp_exp = np.maximum(ex.astype(np.int64) - 8, -133)", "ulp_exp = np.maximum(ex.astype(np.int64) - 8, -126)",
      "bf16 subnormal spacing"),
     ("bf16.py", "q = np.rint(v / ulp) * ulp", "q = np.floor(v / ulp + 0.5) * ulp", "bf16 ties away from zero"),
+    ("gate_bwd.py", "w[:, r] * (dw[:, r] - inner)", "w[:, r] * (dw[:, r] + inner)", "renormalised softmax Jacobian sign"),
+    ("gate_bwd.py", "dL = -p * g[:, None]", "dL = p * g[:, None]", "full softmax Jacobian sign"),
+    ("gate_bwd.py", "dL[rows, ids[:, r]] += dw[:, r] * w[:, r]", "dL[rows, ids[:, r]] += dw[:, r]",
+     "Switch gradient without the weight"),
+    ("gate_bwd.py", "scale = dw[:, grp] * wg", "scale = dw[:, grp]", "kTop1 gradient without the weight"),
+    ("gate_bwd.py", "p = _softmax_rows(L[:, lo:hi])", "p = _softmax_rows(L)[:, lo:hi]", "kTop1 softmax over all experts"),
+    ("gate_bwd.py", "dL = c * p * (f[None, :] - fp[:, None])", "dL = c * p * f[None, :]", "aux gradient without the mean term"),
+    ("gate_bwd.py", "np.bincount(ids[:, 0]", "np.bincount(ids[:, -1]", "aux counts on the last choice"),
+    ("gate_bwd.py", '"dwg": x64.T @ dL', '"dwg": x64.T @ np.abs(dL)', "dW from |dL|"),
+    ("gate_bwd.py", "dx = dx + d_in", "dx = dx - d_in", "incoming dx subtracted"),
+    ("gate_bwd.py", '"dbias": dL.sum(axis=0)', '"dbias": dL.mean(axis=0)', "bias gradient averaged"),
 ]
 
 
@@ -50,12 +61,12 @@ MUTANTS = [
 def test_pins_catch_mutant(tmp_path, fname, old, new, what):
     shutil.copytree(os.path.join(ROOT, "oracle"), tmp_path / "oracle")
     shutil.copytree(os.path.join(ROOT, "tests", "golden"), tmp_path / "tests" / "golden")
-    for f in ("conftest.py", "test_oracle_pins.py"):
+    for f in ("conftest.py", "test_oracle_pins.py", "test_oracle_gate_bwd_pins.py"):
         shutil.copy(os.path.join(ROOT, "tests", f), tmp_path / "tests" / f)
     path = tmp_path / "oracle" / fname
     src = path.read_text()
     assert old in src, f"mutation site for '{what}' not found"
     path.write_text(src.replace(old, new, 1))
     res = subprocess.run([sys.executable, "-m", "pytest", "-q", "-x", "-p", "no:cacheprovider",
-                          "tests/test_oracle_pins.py"], cwd=tmp_path, capture_output=True, text=True, timeout=300)
+                          "tests/test_oracle_pins.py", "tests/test_oracle_gate_bwd_pins.py"], cwd=tmp_path, capture_output=True, text=True, timeout=300)
     assert res.returncode != 0, f"pins did not catch: {what}\n{res.stdout[-2000:]}"

@@ -6,7 +6,8 @@
  *   step 1  W, id = Gate(x)                      -> moe_gate
  *   step 2  x' = Layout_Transform(x, id)         -> moe_dispatch
  *   step 6  y = Reverse_Layout_Transform(y', id) -> moe_combine (gate-weighted)
- * plus the gradients of steps 2 and 6            -> moe_dispatch_bwd, moe_combine_bwd.
+ * plus the gradients of steps 2 and 6            -> moe_dispatch_bwd, moe_combine_bwd,
+ * and of step 1                                  -> moe_gate_bwd.
  * Steps 3-5 (AllToAll and the expert networks) are outside this library.
  *
  * Conventions shared by every call
@@ -52,7 +53,7 @@
 extern "C" {
 #endif
 
-#define MOE_ABI_VERSION 2
+#define MOE_ABI_VERSION 3
 
 /* Symbols of the C ABI are the only ones the shared library exports. */
 #define MOE_API __attribute__((visibility("default")))
@@ -184,6 +185,59 @@ MOE_API moe_status moe_combine_bwd(const moe_layout* l, const void* dy, const vo
                                    const int32_t* ids, const int32_t* slots,
                                    const int32_t* slot_src, const float* weights, void* dye,
                                    float* dw, hipStream_t stream);
+
+/* Parameters of moe_gate_bwd (host memory). */
+typedef struct {
+  int32_t S, d, E, k;    /* as given to moe_gate */
+  int32_t kind;          /* MOE_GATE_TOPK or MOE_GATE_KTOP1 (a hash gate has no gradient) */
+  int32_t normalize;     /* as given to moe_gate */
+  int32_t dtype;         /* moe_dtype of x, wg and dx */
+  int32_t accumulate_dx; /* 1: dx += the gradient through the gate; 0: dx = that gradient */
+  float aux_coef;        /* coefficient of the load-balancing loss, TOPK only; 0 = no loss */
+  int32_t reserved;      /* must be 0 */
+} moe_gate_bwd_params;
+
+/* Bytes of device workspace moe_gate_bwd needs for `p`.  Fails with
+ * MOE_ERR_INVALID_ARG for parameters moe_gate_bwd would reject. */
+MOE_API moe_status moe_gate_bwd_workspace_size(const moe_gate_bwd_params* p, size_t* bytes);
+
+/*
+ * moe_gate_bwd -- gradient of step 1 of Algorithm 1 (the gate of Eq. 1), for
+ * training the layer end to end (Sec. 2).  The loss reaches the gate through
+ * the gate weights (dw, as written by moe_combine_bwd); the selection is held
+ * fixed, since top-k and kTop1 are piecewise constant in the logits.
+ *
+ *   dL[s,e]  = sum_r dw[s,r] * d weights[s,r] / d L[s,e], with the weights of
+ *              moe_gate recomputed from `logits`:
+ *              TOPK normalize=1: dL[id_r] = w_r (dw_r - sum_r' w_r' dw_r'), 0 elsewhere;
+ *              TOPK normalize=0: dL[e] = sum_r dw_r w_r ([e == id_r] - p_e), p = softmax(L[s,:]);
+ *              KTOP1: for e in group g, dL[e] = dw_g w_g ([e == id_g] - p_g,e),
+ *              p_g = softmax over the group.
+ *            + with aux_coef != 0, the gradient of the load-balancing loss
+ *              aux = aux_coef * E * sum_e f_e P_e, where f_e is the share of tokens
+ *              whose first choice is e (held constant) and P_e the mean of p_e:
+ *              aux_coef * E / S * p_e (f_e - sum_e' f_e' p_e').
+ *   dwg[j,e] = sum_s x[s,j] dL[s,e]          (x^T dL; fp32)
+ *   dbias[e] = sum_s dL[s,e]                 (fp32)
+ *   dx[s,j]  = [dx[s,j] if accumulate_dx] + sum_e dL[s,e] wg[j,e], accumulated
+ *              in fp32 and rounded once to dtype.
+ * Sums over tokens run in a fixed order (no atomics): bitwise reproducible.
+ *
+ * Inputs   logits [S,E] fp32 (the logits moe_gate selected on, bias included),
+ *          ids [S,k] (from the same moe_gate call), dw [S,k] fp32; x [S,d] when
+ *          dwg != NULL; wg [d,E] when dx != NULL.  x and dx rows follow the
+ *          alignment rule above; wg needs its natural alignment.
+ * Outputs  each optional (NULL skips it): dlogits [S,E] fp32, dx [S,d] (read
+ *          first when accumulate_dx), dwg [d,E] fp32, dbias [E] fp32, aux_loss
+ *          [1] fp32 (the loss value; requires aux_coef != 0).
+ * Workspace device memory of at least moe_gate_bwd_workspace_size() bytes,
+ *          16-byte aligned; contents on entry are ignored.
+ */
+MOE_API moe_status moe_gate_bwd(const moe_gate_bwd_params* p, const void* x, const void* wg,
+                                const float* logits, const int32_t* ids, const float* dw,
+                                float* dlogits, void* dx, float* dwg, float* dbias,
+                                float* aux_loss, void* workspace, size_t workspace_bytes,
+                                hipStream_t stream);
 
 /* Static description of a status code. */
 MOE_API const char* moe_status_string(moe_status s);

@@ -13,6 +13,7 @@ from .binding import (  # noqa: F401
     MOE_GATE_KTOP1,
     MOE_GATE_TOPK,
     MoeError,
+    GateBwdParams,
     GateParams,
     Layout,
     combine,
@@ -20,6 +21,8 @@ from .binding import (  # noqa: F401
     dispatch,
     dispatch_bwd,
     gate,
+    gate_bwd,
+    gate_bwd_params,
     gate_params,
     load,
     moe_combine,
@@ -27,5 +30,7 @@ from .binding import (  # noqa: F401
     moe_dispatch,
     moe_dispatch_bwd,
     moe_gate,
+    moe_gate_bwd,
+    moe_gate_bwd_workspace_size,
     moe_gate_workspace_size,
 )

@@ -22,8 +22,8 @@ MOE_GATE_TOPK, MOE_GATE_KTOP1, MOE_GATE_HASH = 0, 1, 2
 
 EXPORTED = (
     "moe_gate_workspace_size", "moe_gate", "moe_dispatch", "moe_combine",
-    "moe_dispatch_bwd", "moe_combine_bwd", "moe_status_string", "moe_last_error",
-    "moe_abi_version",
+    "moe_dispatch_bwd", "moe_combine_bwd", "moe_gate_bwd_workspace_size", "moe_gate_bwd",
+    "moe_status_string", "moe_last_error", "moe_abi_version",
 )
 
 
@@ -50,6 +50,15 @@ class Layout(ctypes.Structure):
     ]
 
 
+class GateBwdParams(ctypes.Structure):
+    _fields_ = [
+        ("S", ctypes.c_int32), ("d", ctypes.c_int32), ("E", ctypes.c_int32),
+        ("k", ctypes.c_int32), ("kind", ctypes.c_int32), ("normalize", ctypes.c_int32),
+        ("dtype", ctypes.c_int32), ("accumulate_dx", ctypes.c_int32),
+        ("aux_coef", ctypes.c_float), ("reserved", ctypes.c_int32),
+    ]
+
+
 _lib = None
 
 
@@ -69,8 +78,11 @@ def load():
     lib.moe_combine.argtypes = [ctypes.POINTER(Layout), vp, i32p, i32p, f32p, vp, vp]
     lib.moe_dispatch_bwd.argtypes = [ctypes.POINTER(Layout), vp, i32p, i32p, vp, vp]
     lib.moe_combine_bwd.argtypes = [ctypes.POINTER(Layout), vp, vp, i32p, i32p, i32p, f32p, vp, f32p, vp]
+    lib.moe_gate_bwd_workspace_size.argtypes = [ctypes.POINTER(GateBwdParams), ctypes.POINTER(ctypes.c_size_t)]
+    lib.moe_gate_bwd.argtypes = [ctypes.POINTER(GateBwdParams), vp, vp, f32p, i32p, f32p, f32p, vp, f32p, f32p,
+                                 f32p, vp, ctypes.c_size_t, vp]
     for name in ("moe_gate_workspace_size", "moe_gate", "moe_dispatch", "moe_combine",
-                 "moe_dispatch_bwd", "moe_combine_bwd"):
+                 "moe_dispatch_bwd", "moe_combine_bwd", "moe_gate_bwd_workspace_size", "moe_gate_bwd"):
         getattr(lib, name).restype = ctypes.c_int
     lib.moe_status_string.argtypes = [ctypes.c_int]
     lib.moe_status_string.restype = ctypes.c_char_p
@@ -245,3 +257,54 @@ def combine_bwd(dy, ids, slots, slot_src, weights, ye=None, want_dw=True, stream
     moe_combine_bwd(_layout(S, d, E, k, C, _dtype_code(dy)), dy, ye if want_dw else None, ids, slots, slot_src,
                     weights, dye, dw, stream)
     return dye, dw
+
+
+def gate_bwd_params(S, d, E, k, kind, normalize=0, dtype=MOE_F32, accumulate_dx=0, aux_coef=0.0):
+    return GateBwdParams(S, d, E, k, kind, normalize, dtype, accumulate_dx, aux_coef, 0)
+
+
+def moe_gate_bwd_workspace_size(params):
+    n = ctypes.c_size_t(0)
+    _check(load().moe_gate_bwd_workspace_size(ctypes.byref(params), ctypes.byref(n)))
+    return n.value
+
+
+def moe_gate_bwd(params, x, wg, logits, ids, dw, dlogits, dx, dwg, dbias, aux_loss, workspace, stream=None):
+    dt = torch.bfloat16 if params.dtype == MOE_BF16 else torch.float32
+    f32, i32 = torch.float32, torch.int32
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(load().moe_gate_bwd(ctypes.byref(params), _ptr(x, dt, "x"), _ptr(wg, dt, "wg"),
+                               _ptr(logits, f32, "logits"), _ptr(ids, i32, "ids"), _ptr(dw, f32, "dw"),
+                               _ptr(dlogits, f32, "dlogits"), _ptr(dx, dt, "dx"), _ptr(dwg, f32, "dwg"),
+                               _ptr(dbias, f32, "dbias"), _ptr(aux_loss, f32, "aux_loss"),
+                               _ptr(workspace, None, "workspace"), ws_bytes, _stream(stream)))
+
+
+def gate_bwd(kind, logits, ids, dw, *, x=None, wg=None, normalize=0, dx=None, accumulate_dx=False,
+             want_dlogits=True, want_dwg=True, want_dbias=True, want_dx=True, aux_coef=0.0, stream=None):
+    """Allocating wrapper of moe_gate_bwd.  Returns a dict with dlogits, dwg,
+    dbias, dx and aux_loss (None where not requested).  With accumulate_dx the
+    given dx is updated in place and returned."""
+    S, E = logits.shape
+    k = ids.shape[1]
+    dev = logits.device
+    src = x if x is not None else (wg if wg is not None else dx)
+    dt = torch.float32 if src is None else src.dtype
+    d = x.shape[1] if x is not None else (wg.shape[0] if wg is not None else 1)
+    params = gate_bwd_params(S, d, E, k, kind, normalize, MOE_BF16 if dt == torch.bfloat16 else MOE_F32,
+                             1 if accumulate_dx else 0, aux_coef)
+    f32 = torch.float32
+    out = {
+        "dlogits": torch.empty((S, E), dtype=f32, device=dev) if want_dlogits else None,
+        "dwg": torch.empty((d, E), dtype=f32, device=dev) if want_dwg else None,
+        "dbias": torch.empty((E,), dtype=f32, device=dev) if want_dbias else None,
+        "aux_loss": torch.empty((1,), dtype=f32, device=dev) if aux_coef != 0.0 else None,
+    }
+    if want_dx:
+        out["dx"] = dx if accumulate_dx else torch.empty((S, d), dtype=dt, device=dev)
+    else:
+        out["dx"] = None
+    ws = torch.empty((moe_gate_bwd_workspace_size(params),), dtype=torch.uint8, device=dev)
+    moe_gate_bwd(params, x if want_dwg else None, wg if want_dx else None, logits, ids, dw, out["dlogits"],
+                 out["dx"], out["dwg"], out["dbias"], out["aux_loss"], ws, stream)
+    return out

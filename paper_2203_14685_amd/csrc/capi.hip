@@ -103,6 +103,60 @@ moe_status need(const void* p, int64_t n, size_t align, const char* who, const c
   return MOE_OK;
 }
 
+// Checks shared by moe_gate_bwd and moe_gate_bwd_workspace_size.
+moe_status check_gate_bwd_params(const moe_gate_bwd_params* p) {
+  if (!p) return fail(MOE_ERR_INVALID_ARG, "params is NULL");
+  if (p->reserved != 0) return fail(MOE_ERR_INVALID_ARG, "reserved must be 0");
+  if (p->dtype != MOE_F32 && p->dtype != MOE_BF16) return fail(MOE_ERR_INVALID_ARG, "dtype %d unknown", p->dtype);
+  if (p->kind == MOE_GATE_HASH) return fail(MOE_ERR_INVALID_ARG, "a hash gate has no logits and no gradient");
+  if (p->kind != MOE_GATE_TOPK && p->kind != MOE_GATE_KTOP1) return fail(MOE_ERR_INVALID_ARG, "gate kind %d unknown", p->kind);
+  if (p->S < 0) return fail(MOE_ERR_INVALID_ARG, "S = %d < 0", p->S);
+  if (p->d < 1) return fail(MOE_ERR_INVALID_ARG, "d = %d < 1", p->d);
+  if (p->E < 1 || p->E > 1024) return fail(MOE_ERR_INVALID_ARG, "E = %d outside [1, 1024]", p->E);
+  if (p->normalize != 0 && p->normalize != 1) return fail(MOE_ERR_INVALID_ARG, "normalize must be 0 or 1");
+  if (p->accumulate_dx != 0 && p->accumulate_dx != 1) return fail(MOE_ERR_INVALID_ARG, "accumulate_dx must be 0 or 1");
+  if (p->kind == MOE_GATE_TOPK && (p->k < 1 || p->k > 8 || p->k > p->E))
+    return fail(MOE_ERR_INVALID_ARG, "TOPK needs 1 <= k <= min(E, 8), got k = %d, E = %d", p->k, p->E);
+  if (p->kind == MOE_GATE_KTOP1 && (p->k < 1 || p->k > 8 || p->E % p->k != 0))
+    return fail(MOE_ERR_INVALID_ARG, "KTOP1 needs 1 <= k <= 8 and E %% k == 0, got k = %d, E = %d", p->k, p->E);
+  if (static_cast<int64_t>(p->S) * p->k > kI32Max) return fail(MOE_ERR_INVALID_ARG, "S * k >= 2^31");
+  if (!(p->aux_coef == p->aux_coef) || p->aux_coef > 3.0e38f || p->aux_coef < -3.0e38f)
+    return fail(MOE_ERR_INVALID_ARG, "aux_coef must be finite");
+  if (p->aux_coef != 0.f && p->kind != MOE_GATE_TOPK)
+    return fail(MOE_ERR_INVALID_ARG, "the load-balancing loss is defined for TOPK gates only");
+  return MOE_OK;
+}
+
+// Workspace of moe_gate_bwd, each piece 256-byte aligned: dL [S,E] (used when
+// the caller passes no dlogits), first-choice counts [E], per wave block
+// softmax sums [nb,E], partial dW [nsplit,E,d] and partial db [nsplit,E].
+struct GateBwdPlan {
+  int nb, nsplit, split_tokens;
+  size_t off_dl, off_cnt, off_ppart, off_wpart, off_bpart, total;
+};
+
+size_t align256(size_t n) { return (n + 255) & ~static_cast<size_t>(255); }
+
+GateBwdPlan plan_gate_bwd(const moe_gate_bwd_params* p) {
+  GateBwdPlan g{};
+  const size_t S = static_cast<size_t>(p->S), E = static_cast<size_t>(p->E), d = static_cast<size_t>(p->d);
+  g.nb = static_cast<int>(hist_blocks(p->S));
+  // token ranges of at least 1024 tokens and 16 E, so that the partial sums
+  // stay a small fraction of x
+  int64_t st = 16 * static_cast<int64_t>(p->E);
+  st = (st + 63) / 64 * 64;
+  g.split_tokens = static_cast<int>(st > 1024 ? st : 1024);
+  g.nsplit = static_cast<int>((static_cast<int64_t>(p->S) + g.split_tokens - 1) / g.split_tokens);
+  size_t off = 0;
+  g.off_dl = off;    off += align256(S * E * 4);
+  g.off_cnt = off;   off += align256(E * 4);
+  g.off_ppart = off; off += align256(static_cast<size_t>(g.nb) * E * 4);
+  g.off_wpart = off; off += align256(static_cast<size_t>(g.nsplit) * E * d * 4);
+  g.off_bpart = off; off += align256(static_cast<size_t>(g.nsplit) * E * 4);
+  g.total = off;
+  return g;
+}
+
 int nchunks(const moe_layout* l) {
   return static_cast<int>((static_cast<int64_t>(l->d) * elt_size(l->dtype)) / 16);
 }
@@ -118,6 +172,71 @@ int nchunks(const moe_layout* l) {
 extern "C" {
 
 int32_t moe_abi_version(void) { return MOE_ABI_VERSION; }
+
+moe_status moe_gate_bwd_workspace_size(const moe_gate_bwd_params* p, size_t* bytes) {
+  if (!bytes) return fail(MOE_ERR_INVALID_ARG, "bytes is NULL");
+  CHECK(check_gate_bwd_params(p));
+  *bytes = plan_gate_bwd(p).total;
+  return ok();
+}
+
+moe_status moe_gate_bwd(const moe_gate_bwd_params* p, const void* x, const void* wg, const float* logits,
+                        const int32_t* ids, const float* dw, float* dlogits, void* dx, float* dwg,
+                        float* dbias, float* aux_loss, void* workspace, size_t workspace_bytes,
+                        hipStream_t stream) {
+  static const char* who = "moe_gate_bwd";
+  CHECK(check_gate_bwd_params(p));
+  const int64_t S = p->S, E = p->E, k = p->k, d = p->d;
+  const size_t elt = elt_size(p->dtype);
+  CHECK(need(logits, S * E, 4, who, "logits"));
+  CHECK(need(ids, S * k, 4, who, "ids"));
+  CHECK(need(dw, S * k, 4, who, "dw"));
+  CHECK(need(dlogits, 0, 4, who, "dlogits"));
+  CHECK(need(dbias, 0, 4, who, "dbias"));
+  CHECK(need(aux_loss, 0, 4, who, "aux_loss"));
+  if (aux_loss && p->aux_coef == 0.f) return fail(MOE_ERR_INVALID_ARG, "%s: aux_loss needs aux_coef != 0", who);
+  if (dwg || dx) {
+    if ((d * static_cast<int64_t>(elt)) % 16 != 0)
+      return fail(MOE_ERR_UNSUPPORTED, "%s: row of x / dx is %lld bytes; a multiple of 16 is required", who,
+                  static_cast<long long>(d * static_cast<int64_t>(elt)));
+  }
+  if (dwg) {
+    CHECK(need(dwg, d * E, 4, who, "dwg"));
+    CHECK(need(x, S * d, 16, who, "x"));
+  }
+  if (dx) {
+    CHECK(need(dx, S * d, 16, who, "dx"));
+    CHECK(need(wg, d * E, elt, who, "wg"));
+  }
+  const GateBwdPlan g = plan_gate_bwd(p);
+  if (workspace_bytes < g.total) return fail(MOE_ERR_WORKSPACE, "%s: workspace of %zu bytes, %zu needed", who, workspace_bytes, g.total);
+  if (g.total > 0 && !workspace) return fail(MOE_ERR_WORKSPACE, "%s: workspace is NULL", who);
+  if (workspace && !aligned(workspace, 16)) return fail(MOE_ERR_WORKSPACE, "%s: workspace is not 16-byte aligned", who);
+
+  char* ws = static_cast<char*>(workspace);
+  GateBwdArgs a{};
+  a.S = p->S; a.d = p->d; a.E = p->E; a.k = p->k; a.nb = g.nb;
+  a.kind = p->kind; a.normalize = p->normalize; a.dtype = p->dtype; a.accumulate = p->accumulate_dx;
+  a.aux_coef = p->aux_coef; a.nsplit = g.nsplit; a.split_tokens = g.split_tokens;
+  a.x = x; a.wg = wg; a.logits = logits; a.ids = ids; a.dw = dw;
+  a.dl = dlogits ? dlogits : reinterpret_cast<float*>(ws + g.off_dl);
+  a.dx = dx; a.dwg = dwg; a.dbias = dbias; a.aux_loss = aux_loss;
+  a.cnt = reinterpret_cast<int32_t*>(ws + g.off_cnt);
+  a.ppart = reinterpret_cast<float*>(ws + g.off_ppart);
+  a.wpart = reinterpret_cast<float*>(ws + g.off_wpart);
+  a.bpart = reinterpret_cast<float*>(ws + g.off_bpart);
+  hipError_t err = launch_gate_bwd_dl(a, stream);
+  if (err != hipSuccess) return hip_fail(err, "moe_gate_bwd: dL kernel launch");
+  if (dwg || dbias) {
+    err = launch_gate_bwd_dwg(a, stream);
+    if (err != hipSuccess) return hip_fail(err, "moe_gate_bwd: dW kernel launch");
+  }
+  if (dx) {
+    err = launch_gate_bwd_dx(a, stream);
+    if (err != hipSuccess) return hip_fail(err, "moe_gate_bwd: dx kernel launch");
+  }
+  return ok();
+}
 
 const char* moe_status_string(moe_status s) {
   switch (s) {

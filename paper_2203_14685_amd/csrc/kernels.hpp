@@ -67,4 +67,31 @@ hipError_t launch_dispatch(const RowArgs& a, hipStream_t st);
 hipError_t launch_combine(const RowArgs& a, bool weighted, hipStream_t st);
 hipError_t launch_combine_bwd(const RowArgs& a, hipStream_t st);
 
+// Gate backward (gradient of the gate of Eq. 1).  Buffers of the workspace are
+// carved out by the C ABI.
+struct GateBwdArgs {
+  int S, d, E, k, nb;       // nb: 64-token wave blocks
+  int kind, normalize, dtype, accumulate;
+  float aux_coef;
+  int nsplit, split_tokens; // dW is summed over tokens in nsplit ranges of split_tokens
+  const void* x;            // [S, d]
+  const void* wg;           // [d, E]
+  const float* logits;      // [S, E]
+  const int32_t* ids;       // [S, k]
+  const float* dw;          // [S, k]
+  float* dl;                // [S, E] dL (caller's dlogits or workspace)
+  void* dx;                 // [S, d] or null
+  float* dwg;               // [d, E] or null
+  float* dbias;             // [E] or null
+  float* aux_loss;          // [1] or null
+  int32_t* cnt;             // [E] first-choice counts (load-balancing loss)
+  float* ppart;             // [nb, E] per wave block sums of the softmax (load-balancing loss)
+  float* wpart;             // [nsplit, E, d] partial dW
+  float* bpart;             // [nsplit, E] partial db
+};
+
+hipError_t launch_gate_bwd_dl(const GateBwdArgs& a, hipStream_t st);
+hipError_t launch_gate_bwd_dwg(const GateBwdArgs& a, hipStream_t st);
+hipError_t launch_gate_bwd_dx(const GateBwdArgs& a, hipStream_t st);
+
 }  // namespace hetumoe

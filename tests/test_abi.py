@@ -38,7 +38,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_abi_version_and_struct_layout(lib):
-    assert lib.moe_abi_version() == 2
+    assert lib.moe_abi_version() == 3
     assert ctypes.sizeof(b.GateParams) == 48
     assert b.GateParams.hash_seed.offset == 40
     assert ctypes.sizeof(b.Layout) == 24
@@ -147,3 +147,73 @@ def test_binding_rejects_cpu_tensors(lib):
     with pytest.raises(ValueError):
         z = torch.zeros((4, 1), dtype=torch.int32)
         hm.dispatch(x, z, z, torch.zeros((2, 2), dtype=torch.int32))
+
+
+# ------------------------------------------------------------------ gate backward
+
+def _bwd_ws(params):
+    n = ctypes.c_size_t(12345)
+    st = hm.load().moe_gate_bwd_workspace_size(ctypes.byref(params), ctypes.byref(n))
+    return st, n.value
+
+
+def _a256(n):
+    return (n + 255) // 256 * 256
+
+
+def test_gate_bwd_struct_and_workspace(lib):
+    assert ctypes.sizeof(b.GateBwdParams) == 40
+    assert b.GateBwdParams.aux_coef.offset == 32
+    for S, d, E, k in [(32768, 2048, 64, 4), (1000, 256, 8, 1), (0, 16, 3, 1), (5000, 64, 1024, 2)]:
+        p = hm.gate_bwd_params(S, d, E, k, 0)
+        st, n = _bwd_ws(p)
+        assert st == 0
+        nb = (S + 63) // 64
+        split = max(1024, (16 * E + 63) // 64 * 64)
+        nsplit = (S + split - 1) // split
+        want = (_a256(S * E * 4) + _a256(E * 4) + _a256(nb * E * 4) + _a256(nsplit * E * d * 4)
+                + _a256(nsplit * E * 4))
+        assert n == want, (S, d, E, k)
+
+
+BAD_BWD = [
+    dict(kind=2), dict(kind=3), dict(E=0), dict(E=1025), dict(S=-1), dict(d=0), dict(k=0), dict(k=9, E=16),
+    dict(kind=1, k=3, E=16), dict(normalize=2), dict(accumulate_dx=2), dict(dtype=2),
+    dict(aux_coef=float("nan")), dict(aux_coef=float("inf")), dict(kind=1, k=2, aux_coef=0.01),
+    dict(S=1 << 30, k=2),
+]
+
+
+@pytest.mark.parametrize("bad", BAD_BWD)
+def test_bad_gate_bwd_params_rejected(lib, bad):
+    base = dict(S=100, d=256, E=8, k=1, kind=0, normalize=0, dtype=0, accumulate_dx=0, aux_coef=0.0)
+    base.update(bad)
+    st, _ = _bwd_ws(hm.gate_bwd_params(**base))
+    assert st == b.MOE_ERR_INVALID_ARG, (bad, lib.moe_last_error())
+    p = hm.gate_bwd_params(100, 256, 8, 1, 0)
+    p.reserved = 3
+    assert _bwd_ws(p)[0] == b.MOE_ERR_INVALID_ARG
+
+
+def test_gate_bwd_pointer_checks(lib):
+    p = hm.gate_bwd_params(100, 256, 8, 2, 0, 1, b.MOE_BF16, 0, 0.0)
+    # moe_gate_bwd(p, x, wg, logits, ids, dw, dlogits, dx, dwg, dbias, aux_loss, ws, wsb, stream)
+    call = lambda **kw: lib.moe_gate_bwd(ctypes.byref(p), kw.get("x", A16), kw.get("wg", A16),
+                                         kw.get("logits", A16), kw.get("ids", A16), kw.get("dw", A16),
+                                         kw.get("dl"), kw.get("dx", A16), kw.get("dwg", A16), kw.get("db"),
+                                         kw.get("aux"), kw.get("ws", A16), kw.get("wsb", 1 << 30), None)
+    assert lib.moe_gate_bwd(None, *([None] * 10), None, 0, None) == b.MOE_ERR_INVALID_ARG
+    assert call(logits=None) == b.MOE_ERR_INVALID_ARG
+    assert call(ids=None) == b.MOE_ERR_INVALID_ARG
+    assert call(dw=A16 + 2) == b.MOE_ERR_INVALID_ARG
+    assert call(x=None) == b.MOE_ERR_INVALID_ARG                  # dwg needs x
+    assert call(x=A16 + 4) == b.MOE_ERR_UNSUPPORTED               # x 16-byte aligned
+    assert call(wg=None) == b.MOE_ERR_INVALID_ARG                 # dx needs wg
+    assert call(dx=A16 + 8) == b.MOE_ERR_UNSUPPORTED
+    assert call(aux=A16) == b.MOE_ERR_INVALID_ARG                 # a loss value needs aux_coef
+    assert call(ws=None) == b.MOE_ERR_WORKSPACE
+    assert call(wsb=64) == b.MOE_ERR_WORKSPACE
+    assert call(ws=A16 + 4) == b.MOE_ERR_WORKSPACE
+    p6 = hm.gate_bwd_params(100, 4, 8, 2, 0, 1, b.MOE_BF16)     # 8-byte rows of x / dx
+    assert lib.moe_gate_bwd(ctypes.byref(p6), A16, A16, A16, A16, A16, None, A16, None, None, None, A16,
+                            1 << 30, None) == b.MOE_ERR_UNSUPPORTED

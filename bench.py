@@ -322,6 +322,40 @@ def main():
     def pct(v, q):
         return v[min(len(v) - 1, int(q * len(v)))]
 
+    # gradient of the gate (learned gates), outside the timed step: moe_gate_bwd
+    # with dx accumulated into the dispatch-backward output, dW, db and, for
+    # top-k gates, the load-balancing loss
+    gate_bwd = None
+    if learned:
+        aux = 0.01 if w["kind"] == hm.MOE_GATE_TOPK else 0.0
+        lg = torch.empty((S, E), dtype=torch.float32, device=dev)
+        hm.moe_gate(params, x, wg, bias, None, lg, ids, slots, weights, counts, demand, slot_src, ws, stream)
+        bp = hm.gate_bwd_params(S, d, E, k, w["kind"], w["normalize"], dcode, 1, aux)
+        bws = torch.empty((hm.moe_gate_bwd_workspace_size(bp),), dtype=torch.uint8, device=dev)
+        dwg_out = torch.empty((d, E), dtype=torch.float32, device=dev)
+        db_out = torch.empty((E,), dtype=torch.float32, device=dev)
+        loss_out = torch.empty((1,), dtype=torch.float32, device=dev) if aux else None
+
+        def gbwd():
+            hm.moe_gate_bwd(bp, x, wg, lg, ids, dw, None, dx, dwg_out, db_out, loss_out, bws, stream)
+        for _ in range(3):
+            gbwd()
+        g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        g0.record(stream)
+        for _ in range(args.steps):
+            gbwd()
+        g1.record(stream)
+        torch.cuda.synchronize()
+        gms = g0.elapsed_time(g1) / args.steps
+        gbytes = S * E * 4 + S * k * 8 + S * d * elt + d * E * elt + 2 * S * d * elt + d * E * 4 + E * 4
+        gflop = 4 * S * d * E
+        gate_bwd = {"ms": round(gms, 5), "alg_bytes": gbytes, "GB/s": round(gbytes / (gms * 1e-3) / 1e9, 1),
+                    "hbm_frac": round(gbytes / (gms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                    "flop": gflop, "TFLOP/s": round(gflop / (gms * 1e-3) / 1e12, 2),
+                    "what": "moe_gate_bwd: dL, dW = x^T dL, db, dx += dL W^T" + (", balance loss" if aux else "")}
+        del bws, lg
+
     # routing statistics of this batch (outside the timed region)
     sl = slots.cpu().numpy()
     n_kept = int((sl >= 0).sum())
@@ -380,6 +414,7 @@ def main():
         "ops": {op: {"ms": round(op_ms[op], 5), "alg_bytes": ab[op],
                      "GB/s": round(ab[op] / (op_ms[op] * 1e-3) / 1e9, 1)} for op in OPS},
         "routing": {"kept_assignments": n_kept, "tokens_with_kept": tok_kept, "assignments": S * k},
+        "gate_bwd": gate_bwd,
     }
     fwd_ms = op_ms["gate"] + op_ms["dispatch"] + op_ms["combine"]
     out["fwd"] = {"ms": round(fwd_ms, 5), "tokens/s": round(S / (fwd_ms * 1e-3), 1),

@@ -128,11 +128,15 @@ moe_status check_gate_bwd_params(const moe_gate_bwd_params* p) {
 }
 
 // Workspace of moe_gate_bwd, each piece 256-byte aligned: dL [S,E] (used when
-// the caller passes no dlogits), first-choice counts [E], per wave block
-// softmax sums [nb,E], partial dW [nsplit,E,d] and partial db [nsplit,E].
+// the caller passes no dlogits), dL transposed [E, S rounded up to 64] as three
+// bf16 planes (matrix cores only), first-choice counts [E] followed by per-4096-token counts, per
+// wave block sums of the softmax and of dL [nb,E] each, softmax sums [E], and
+// partial dW [nsplit,E,d] over token ranges.
 struct GateBwdPlan {
   int nb, nsplit, split_tokens;
-  size_t off_dl, off_cnt, off_ppart, off_wpart, off_bpart, total;
+  bool mfma;
+  int64_t s_pad;
+  size_t off_dl, off_dlt, off_cnt, off_ppart, off_bpart, off_pe, off_wpart, total;
 };
 
 size_t align256(size_t n) { return (n + 255) & ~static_cast<size_t>(255); }
@@ -141,18 +145,29 @@ GateBwdPlan plan_gate_bwd(const moe_gate_bwd_params* p) {
   GateBwdPlan g{};
   const size_t S = static_cast<size_t>(p->S), E = static_cast<size_t>(p->E), d = static_cast<size_t>(p->d);
   g.nb = static_cast<int>(hist_blocks(p->S));
-  // token ranges of at least 1024 tokens and 16 E, so that the partial sums
-  // stay a small fraction of x
-  int64_t st = 16 * static_cast<int64_t>(p->E);
+  g.mfma = gate_bwd_mfma_shape(p->dtype, p->E, p->d);
+  g.s_pad = static_cast<int64_t>(g.nb) * kTokensPerHistBlock;
+  // token ranges for dW: enough blocks to fill the chip (about 512 matrix-core
+  // or 1024 vector blocks), each range a whole number of 64-token blocks
+  const int64_t per_split = g.mfma ? (p->d / 64) : ((p->d + 63) / 64) * ((p->E + 63) / 64);
+  const int64_t target = g.mfma ? 512 : 1024;
+  int64_t ns = (target + per_split - 1) / per_split;
+  if (ns > g.nb) ns = g.nb;
+  if (ns < 1) ns = 1;
+  int64_t st = (static_cast<int64_t>(p->S) + ns - 1) / ns;
   st = (st + 63) / 64 * 64;
-  g.split_tokens = static_cast<int>(st > 1024 ? st : 1024);
-  g.nsplit = static_cast<int>((static_cast<int64_t>(p->S) + g.split_tokens - 1) / g.split_tokens);
+  if (st < 64) st = 64;
+  g.split_tokens = static_cast<int>(st);
+  g.nsplit = static_cast<int>((static_cast<int64_t>(p->S) + st - 1) / st);
+  const size_t cblocks = (S + 4095) / 4096;
   size_t off = 0;
   g.off_dl = off;    off += align256(S * E * 4);
-  g.off_cnt = off;   off += align256(E * 4);
+  g.off_dlt = off;   off += g.mfma ? align256(3 * static_cast<size_t>(g.s_pad) * E * 2) : 0;
+  g.off_cnt = off;   off += align256((1 + cblocks) * E * 4);
   g.off_ppart = off; off += align256(static_cast<size_t>(g.nb) * E * 4);
+  g.off_bpart = off; off += align256(static_cast<size_t>(g.nb) * E * 4);
+  g.off_pe = off;    off += align256(E * 4);
   g.off_wpart = off; off += align256(static_cast<size_t>(g.nsplit) * E * d * 4);
-  g.off_bpart = off; off += align256(static_cast<size_t>(g.nsplit) * E * 4);
   g.total = off;
   return g;
 }
@@ -218,16 +233,22 @@ moe_status moe_gate_bwd(const moe_gate_bwd_params* p, const void* x, const void*
   a.S = p->S; a.d = p->d; a.E = p->E; a.k = p->k; a.nb = g.nb;
   a.kind = p->kind; a.normalize = p->normalize; a.dtype = p->dtype; a.accumulate = p->accumulate_dx;
   a.aux_coef = p->aux_coef; a.nsplit = g.nsplit; a.split_tokens = g.split_tokens;
+  a.mfma_dw = (g.mfma && dwg) ? 1 : 0;
+  // the matrix-core dx reads W rows and dL with 16-byte loads
+  a.mfma_dx = (g.mfma && dx && aligned(wg, 16) && (!dlogits || aligned(dlogits, 16))) ? 1 : 0;
+  a.s_pad = g.s_pad;
   a.x = x; a.wg = wg; a.logits = logits; a.ids = ids; a.dw = dw;
   a.dl = dlogits ? dlogits : reinterpret_cast<float*>(ws + g.off_dl);
+  a.dlt = a.mfma_dw ? reinterpret_cast<uint16_t*>(ws + g.off_dlt) : nullptr;
   a.dx = dx; a.dwg = dwg; a.dbias = dbias; a.aux_loss = aux_loss;
   a.cnt = reinterpret_cast<int32_t*>(ws + g.off_cnt);
   a.ppart = reinterpret_cast<float*>(ws + g.off_ppart);
-  a.wpart = reinterpret_cast<float*>(ws + g.off_wpart);
   a.bpart = reinterpret_cast<float*>(ws + g.off_bpart);
+  a.pe = reinterpret_cast<float*>(ws + g.off_pe);
+  a.wpart = reinterpret_cast<float*>(ws + g.off_wpart);
   hipError_t err = launch_gate_bwd_dl(a, stream);
   if (err != hipSuccess) return hip_fail(err, "moe_gate_bwd: dL kernel launch");
-  if (dwg || dbias) {
+  if (dwg) {
     err = launch_gate_bwd_dwg(a, stream);
     if (err != hipSuccess) return hip_fail(err, "moe_gate_bwd: dW kernel launch");
   }

@@ -76,6 +76,21 @@ __device__ __forceinline__ float load_elem(const bf16_t* p, int64_t i) {
   return __uint_as_float(static_cast<uint32_t>(p[i].bits) << 16);
 }
 
+// 8 x 8 transpose of bf16: in[j] holds row j (8 half-words, lowest first);
+// out[i] receives column i.
+__device__ __forceinline__ void transpose8x8_b16(const u32x4 (&in)[8], u32x4 (&out)[8]) {
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    uint32_t wd[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t a = in[2 * q][i / 2], b = in[2 * q + 1][i / 2];
+      wd[q] = (i & 1) ? ((a >> 16) | (b & 0xffff0000u)) : ((a & 0xffffu) | (b << 16));
+    }
+    out[i] = u32x4{wd[0], wd[1], wd[2], wd[3]};
+  }
+}
+
 __device__ __forceinline__ int lane_id() {
   return __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
 }

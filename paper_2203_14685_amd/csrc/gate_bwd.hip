@@ -3,10 +3,19 @@
 // the load-balancing loss, then dW = x^T dL, db = column sums of dL and
 // dx = dL W^T.  Sums over tokens run in fixed ranges and a fixed order, so the
 // results are bitwise reproducible; there are no atomics on floats.
+//
+// bf16 shapes with E a multiple of 16 (up to 128) and d a multiple of 64 run
+// the two products on the matrix cores (v_mfma_f32_16x16x32_bf16).  x and W
+// are exact in bf16; dL is fp32, so it is split into three bf16 parts whose sum
+// is dL exactly and each part is multiplied separately: every product is then
+// exact and only the fp32 accumulation rounds, as on the vector path.
 #include "common.hpp"
 #include "kernels.hpp"
 
 namespace hetumoe {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kBwdWaves = 4;
 constexpr int kBwdThreads = kBwdWaves * kWave;
@@ -25,48 +34,116 @@ __device__ __forceinline__ float group_sum(float v) {
   return v;
 }
 
+__device__ __forceinline__ float bf16_bits_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
+
+// v = hi + mid + lo with three bf16 parts (each remainder is exact in fp32).
+__device__ __forceinline__ void split3(float v, uint32_t& h, uint32_t& m, uint32_t& l) {
+  h = f32_to_bf16_bits(v);
+  const float r1 = v - bf16_bits_to_f32(h);
+  m = f32_to_bf16_bits(r1);
+  const float r2 = r1 - bf16_bits_to_f32(m);
+  l = f32_to_bf16_bits(r2);
+}
+
+__device__ __forceinline__ void split8(const float (&v)[8], u32x4& hi, u32x4& mi, u32x4& lo) {
+  uint32_t h[8], m[8], l[8];
+#pragma unroll
+  for (int q = 0; q < 8; ++q) split3(v[q], h[q], m[q], l[q]);
+  hi = u32x4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
+  mi = u32x4{m[0] | (m[1] << 16), m[2] | (m[3] << 16), m[4] | (m[5] << 16), m[6] | (m[7] << 16)};
+  lo = u32x4{l[0] | (l[1] << 16), l[2] | (l[3] << 16), l[4] | (l[5] << 16), l[6] | (l[7] << 16)};
+}
+
+__device__ __forceinline__ f32x4 mfma_bf16(const u32x4& a, const u32x4& b, const f32x4& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c,
+                                                 0, 0, 0);
+}
+
+// ---------------------------------------------------------------- column sums
+// out[e] = sum over rows b of part[b][e]: 16 threads per column take rows
+// q, q + 16, ... in order, then their 16 sums are added in order.
+template <typename T>
+__global__ __launch_bounds__(1024) void colsum_kernel(const T* part, int64_t rows, int E, T* out) {
+  __shared__ T red[16][kWave];
+  const int q = threadIdx.x / kWave, c = threadIdx.x % kWave;
+  const int e = blockIdx.x * kWave + c;
+  T v = 0;
+  if (e < E) {
+    // 8 rows' loads in flight, then added in row order
+    for (int64_t b0 = q; b0 < rows; b0 += 16 * 8) {
+      T t[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int64_t b = b0 + 16 * u;
+        t[u] = b < rows ? part[b * E + e] : T(0);
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v += t[u];
+    }
+  }
+  red[q][c] = v;
+  __syncthreads();
+  if (q == 0 && e < E) {
+    T t = 0;
+    for (int i = 0; i < 16; ++i) t += red[i][c];
+    out[e] = t;
+  }
+}
+
 // ---------------------------------------------------------------- first choices
-// cnt[e] = number of tokens whose first choice is e (one block; integer atomics
-// in LDS, so the counts do not depend on the order).
-__global__ __launch_bounds__(1024) void aux_counts_kernel(GateBwdArgs a) {
+// Per block of kCountTokens tokens: counts of first choices per expert (integer
+// atomics in LDS; counts do not depend on the order).
+constexpr int kCountTokens = 4096;
+
+__global__ __launch_bounds__(1024) void aux_counts_kernel(GateBwdArgs a, int32_t* cpart) {
   extern __shared__ int h[];
   for (int e = threadIdx.x; e < a.E; e += blockDim.x) h[e] = 0;
   __syncthreads();
-  for (int64_t s = threadIdx.x; s < a.S; s += blockDim.x) {
+  const int64_t s0 = static_cast<int64_t>(blockIdx.x) * kCountTokens;
+  const int64_t s1 = min(static_cast<int64_t>(a.S), s0 + kCountTokens);
+  for (int64_t s = s0 + threadIdx.x; s < s1; s += blockDim.x) {
     const int e = a.ids[s * a.k];
     if (e >= 0 && e < a.E) atomicAdd(&h[e], 1);
   }
   __syncthreads();
-  for (int e = threadIdx.x; e < a.E; e += blockDim.x) a.cnt[e] = h[e];
+  for (int e = threadIdx.x; e < a.E; e += blockDim.x) cpart[static_cast<int64_t>(blockIdx.x) * a.E + e] = h[e];
 }
 
 // ---------------------------------------------------------------- dL
-// One wave per 64-token wave block.  P lanes per token (P = E rounded up to a
-// power of two, at most 64), EPL experts per lane: lane j of a token holds
-// experts j, j + P, ...  Softmax maxima and sums are butterfly reductions over
-// the P lanes.
-template <int P, int EPL>
-__global__ __launch_bounds__(kBwdThreads) void gate_dl_kernel(GateBwdArgs a) {
-  constexpr int TP = kWave / P;  // tokens per pass
+// One block per 64-token wave block of WAVES waves, each taking 64 / WAVES
+// tokens.  P lanes per token (a power of two, 4 <= P <= 64), EPL experts per
+// lane: lane j of a token holds experts j, j + P, ...  Softmax maxima and sums
+// are butterfly reductions over the P lanes.  Also per wave block: sums of dL
+// (for db) and of the softmax (load-balancing loss), and, for the matrix-core
+// dW, dL transposed and split into three bf16 planes.
+template <int P, int EPL, int WAVES>
+__global__ __launch_bounds__(WAVES * kWave) void gate_dl_kernel(GateBwdArgs a) {
+  constexpr int TP = kWave / P;                  // tokens per pass
+  constexpr int TW = kWave / WAVES;              // tokens per wave
+  constexpr int PASSES = TW / TP;
+  static_assert(TW % TP == 0, "whole passes");
+  extern __shared__ float sh[];  // [64][E + 1] dL tile (dlt only), then [2][WAVES][E] sums
   const int lane = lane_id();
+  const int w = threadIdx.x / kWave;
   const int j = lane % P, sub = lane / P;
-  const int64_t wb = static_cast<int64_t>(blockIdx.x) * kBwdWaves + threadIdx.x / kWave;
-  if (wb >= a.nb) return;  // no block-wide synchronisation below
+  const int64_t wb = blockIdx.x;
   const int E = a.E, k = a.k;
   const bool aux = a.aux_coef != 0.f;
   const bool full_softmax = a.kind == 0 && (a.normalize == 0 || aux);
   const float inv_s = a.S > 0 ? 1.f / static_cast<float>(a.S) : 0.f;
   const float c_aux = a.aux_coef * static_cast<float>(E) * inv_s;
-  float f[EPL], psum[EPL];
+  float f[EPL], psum[EPL], bsum[EPL];
 #pragma unroll
   for (int i = 0; i < EPL; ++i) {
     const int e = j + P * i;
     f[i] = (aux && e < E) ? static_cast<float>(a.cnt[e]) * inv_s : 0.f;
     psum[i] = 0.f;
+    bsum[i] = 0.f;
   }
 
-  for (int t0 = 0; t0 < kWave; t0 += TP) {
-    const int64_t s = wb * kWave + t0 + sub;
+  for (int pass = 0; pass < PASSES; ++pass) {
+    const int tok = TW * w + pass * TP + sub;
+    const int64_t s = wb * kWave + tok;
     const bool valid = s < a.S;
     const float* lrow = a.logits + (valid ? s : 0) * E;
     float v[EPL], dl[EPL], p[EPL];
@@ -112,41 +189,40 @@ __global__ __launch_bounds__(kBwdThreads) void gate_dl_kernel(GateBwdArgs a) {
       float m2 = -INFINITY;
 #pragma unroll
       for (int r = 0; r < 8; ++r) m2 = fmaxf(m2, lr[r]);
-      float den = 0.f, w[8];
+      float den = 0.f, wr[8];
 #pragma unroll
       for (int r = 0; r < 8; ++r) {
-        w[r] = idr[r] >= 0 ? expf(lr[r] - m2) : 0.f;
-        den += w[r];
+        wr[r] = idr[r] >= 0 ? expf(lr[r] - m2) : 0.f;
+        den += wr[r];
       }
       float inner = 0.f;
 #pragma unroll
       for (int r = 0; r < 8; ++r) {
-        w[r] = idr[r] >= 0 ? w[r] / den : 0.f;
-        inner += w[r] * dwr[r];
+        wr[r] = idr[r] >= 0 ? wr[r] / den : 0.f;
+        inner += wr[r] * dwr[r];
       }
 #pragma unroll
       for (int r = 0; r < 8; ++r) {
         if (idr[r] < 0) continue;
-        const float g = w[r] * (dwr[r] - inner);
+        const float gr = wr[r] * (dwr[r] - inner);
 #pragma unroll
         for (int i = 0; i < EPL; ++i)
-          if (j + P * i == idr[r]) dl[i] += g;
+          if (j + P * i == idr[r]) dl[i] += gr;
       }
     } else if (a.kind == 0) {
       // full softmax read at each chosen expert
-      float g = 0.f;
+      float gsum = 0.f;
 #pragma unroll
       for (int r = 0; r < 8; ++r) {
         if (idr[r] < 0) continue;
-        const float wr = expf(lr[r] - m) / se;
-        const float t = dwr[r] * wr;
-        g += t;
+        const float t = dwr[r] * (expf(lr[r] - m) / se);
+        gsum += t;
 #pragma unroll
         for (int i = 0; i < EPL; ++i)
           if (j + P * i == idr[r]) dl[i] += t;
       }
 #pragma unroll
-      for (int i = 0; i < EPL; ++i) dl[i] -= p[i] * g;
+      for (int i = 0; i < EPL; ++i) dl[i] -= p[i] * gsum;
     } else {
       // kTop1: softmax within each contiguous group of G experts
       const int G = E / k;
@@ -166,7 +242,6 @@ __global__ __launch_bounds__(kBwdThreads) void gate_dl_kernel(GateBwdArgs a) {
           if (e >= lo && e < hi) sum += expf(v[i] - mg);
         }
         const float sg = group_sum<P>(sum);
-        // the chosen expert of this group (rank grp)
         int id = -1;
         float dwv = 0.f, lv = 0.f;
 #pragma unroll
@@ -192,39 +267,69 @@ __global__ __launch_bounds__(kBwdThreads) void gate_dl_kernel(GateBwdArgs a) {
         if (valid) psum[i] += p[i];
       }
     }
-    if (valid) {
 #pragma unroll
-      for (int i = 0; i < EPL; ++i) {
-        const int e = j + P * i;
-        if (e < E) a.dl[s * E + e] = dl[i];
+    for (int i = 0; i < EPL; ++i) {
+      const int e = j + P * i;
+      if (e >= E) continue;
+      if (valid) {
+        a.dl[s * E + e] = dl[i];
+        bsum[i] += dl[i];
+      }
+      if (a.dlt) sh[tok * (E + 1) + e] = valid ? dl[i] : 0.f;
+    }
+  }
+  // sums over the token lanes of each wave
+#pragma unroll
+  for (int i = 0; i < EPL; ++i)
+    for (int msk = P; msk < kWave; msk <<= 1) {
+      bsum[i] += __shfl_xor(bsum[i], msk);
+      psum[i] += __shfl_xor(psum[i], msk);
+    }
+  __syncthreads();  // dL tile complete
+  if (a.dlt) {
+    const int64_t plane = static_cast<int64_t>(E) * a.s_pad;
+    for (int q = threadIdx.x; q < E * kWave; q += WAVES * kWave) {
+      const int e = q / kWave, tok = q % kWave;
+      uint32_t hb, mb, lb;
+      split3(sh[tok * (E + 1) + e], hb, mb, lb);
+      const int64_t o = static_cast<int64_t>(e) * a.s_pad + wb * kWave + tok;
+      a.dlt[o] = static_cast<uint16_t>(hb);
+      a.dlt[plane + o] = static_cast<uint16_t>(mb);
+      a.dlt[2 * plane + o] = static_cast<uint16_t>(lb);
+    }
+  }
+  __syncthreads();  // tile consumed before its space holds the sums
+  float* red = sh;  // [2][WAVES][E]
+  if (sub == 0) {
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) {
+      const int e = j + P * i;
+      if (e < E) {
+        red[w * E + e] = bsum[i];
+        red[(WAVES + w) * E + e] = psum[i];
       }
     }
   }
-  if (aux) {
-    // sum over the TP token lanes of the wave, then one partial row per wave block
-#pragma unroll
-    for (int i = 0; i < EPL; ++i)
-      for (int msk = P; msk < kWave; msk <<= 1) psum[i] += __shfl_xor(psum[i], msk);
-    if (sub == 0) {
-#pragma unroll
-      for (int i = 0; i < EPL; ++i) {
-        const int e = j + P * i;
-        if (e < E) a.ppart[wb * E + e] = psum[i];
-      }
+  __syncthreads();
+  for (int e = threadIdx.x; e < E; e += WAVES * kWave) {
+    float bs = 0.f, ps = 0.f;
+    for (int ww = 0; ww < WAVES; ++ww) {
+      bs += red[ww * E + e];
+      ps += red[(WAVES + ww) * E + e];
     }
+    a.bpart[wb * E + e] = bs;
+    if (aux) a.ppart[wb * E + e] = ps;
   }
 }
 
-// loss = coef * E * sum_e f_e * P_e, P_e summed over wave blocks in order.
+// loss = coef * E * sum_e f_e * P_e (a tree sum over experts in a fixed order).
 __global__ __launch_bounds__(1024) void aux_loss_kernel(GateBwdArgs a) {
   __shared__ float red[1024];
   const int t = threadIdx.x;
   float term = 0.f;
   if (t < a.E && a.S > 0) {
-    float pe = 0.f;
-    for (int64_t b = 0; b < a.nb; ++b) pe += a.ppart[b * a.E + t];
     const float inv_s = 1.f / static_cast<float>(a.S);
-    term = (static_cast<float>(a.cnt[t]) * inv_s) * (pe * inv_s);
+    term = (static_cast<float>(a.cnt[t]) * inv_s) * (a.pe[t] * inv_s);
   }
   red[t] = term;
   __syncthreads();
@@ -235,11 +340,217 @@ __global__ __launch_bounds__(1024) void aux_loss_kernel(GateBwdArgs a) {
   if (t == 0) a.aux_loss[0] = a.aux_coef * static_cast<float>(a.E) * red[0];
 }
 
-// ---------------------------------------------------------------- dW, db
+// ---------------------------------------------------------------- dW on matrix cores
+// Block: 64 columns of x (blockIdx.x) x one token range (blockIdx.y); its 4
+// waves take the range's 64-token chunks in turn, each on its own.  A wave transposes its chunk
+// of x into LDS (each lane one 8 x 8 block, transposed in registers) and runs
+// 4 M tiles (16 columns) x NT N tiles (16 experts) with K = 32 tokens:
+// A[j][s] = x[s][j] from the tile, B[s][e] = dL^T[e][s] from its three bf16
+// planes.
+// The four waves' sums are then added in order into the range's partial dW.
+template <int NT>
+__global__ __launch_bounds__(kBwdThreads) void dwg_mfma_kernel(GateBwdArgs a) {
+  constexpr int E = 16 * NT;
+  constexpr int LDX = kWave + 8;   // padded row of the x^T tile (bf16)
+  constexpr int LDR = kWave + 1;   // padded row of the wave-sum buffer (fp32)
+  __shared__ __align__(16) uint16_t xt[kBwdWaves * kWave * LDX];
+  static_assert(E * LDR * 4 <= kBwdWaves * kWave * LDX * 2, "sums reuse the tile buffer");
+  float* red = reinterpret_cast<float*>(xt);
+  const int w = threadIdx.x / kWave, lane = lane_id();
+  const int g = lane / 16, m = lane % 16;
+  const int bb = lane % 8, ab = lane / 8;  // the 8 x 8 block this lane stages
+  const int j0 = blockIdx.x * kWave;
+  const int split = blockIdx.y;
+  const int64_t sb = static_cast<int64_t>(split) * a.split_tokens;
+  const int64_t se = min(static_cast<int64_t>(a.S), sb + a.split_tokens);
+  const int nchunks = static_cast<int>((se - sb + kWave - 1) / kWave);
+  const uint16_t* x = reinterpret_cast<const uint16_t*>(a.x);
+  static_assert(LDX % 8 == 0, "16-byte tile rows");
+  uint16_t* tile = xt + w * kWave * LDX;
+  const u32x4 zero = {0u, 0u, 0u, 0u};
+
+  f32x4 acc[4][NT];
+#pragma unroll
+  for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // the tile is private to the wave: wave-level fences order its LDS traffic,
+  // and the next chunk's rows of x are loaded while this one is multiplied
+  const int64_t plane = static_cast<int64_t>(E) * a.s_pad;
+  u32x4 rows[8];
+  auto load_rows = [&](int c) {
+    const int64_t s0 = sb + static_cast<int64_t>(c) * kWave;
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      const int64_t s = s0 + 8 * ab + r;
+      rows[r] = (c < nchunks && s < se) ? *reinterpret_cast<const u32x4*>(x + s * a.d + j0 + 8 * bb) : zero;
+    }
+  };
+  load_rows(w);
+  for (int c = w; c < nchunks; c += kBwdWaves) {
+    const int64_t s0 = sb + static_cast<int64_t>(c) * kWave;
+    {
+      u32x4 cols[8];
+      transpose8x8_b16(rows, cols);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) *reinterpret_cast<u32x4*>(&tile[(8 * bb + i) * LDX + 8 * ab]) = cols[i];
+    }
+    load_rows(c + kBwdWaves);
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      u32x4 av[4];
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt)
+        av[mt] = *reinterpret_cast<const u32x4*>(&tile[(16 * mt + m) * LDX + 32 * ks + 8 * g]);
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) {
+        const uint16_t* src = a.dlt + static_cast<int64_t>(16 * nt + m) * a.s_pad + s0 + 32 * ks + 8 * g;
+        const u32x4 bh = *reinterpret_cast<const u32x4*>(src);
+        const u32x4 bm = *reinterpret_cast<const u32x4*>(src + plane);
+        const u32x4 bl = *reinterpret_cast<const u32x4*>(src + 2 * plane);
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt) {
+          acc[mt][nt] = mfma_bf16(av[mt], bh, acc[mt][nt]);
+          acc[mt][nt] = mfma_bf16(av[mt], bm, acc[mt][nt]);
+          acc[mt][nt] = mfma_bf16(av[mt], bl, acc[mt][nt]);
+        }
+      }
+    }
+    // the tile is read before the next chunk overwrites it
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+  __syncthreads();  // every wave done with its tile before the buffer holds the sums
+  // lane (g, m) of tile (mt, nt) holds columns 16 mt + 4 g + i, expert 16 nt + m
+  for (int ww = 0; ww < kBwdWaves; ++ww) {
+    if (w == ww) {
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int idx = (16 * nt + m) * LDR + 16 * mt + 4 * g + i;
+            red[idx] = (ww == 0 ? 0.f : red[idx]) + acc[mt][nt][i];
+          }
+    }
+    __syncthreads();
+  }
+  for (int q = threadIdx.x; q < E * kWave; q += kBwdThreads) {
+    const int e = q / kWave, jj = q % kWave;
+    a.wpart[(static_cast<int64_t>(split) * E + e) * a.d + j0 + jj] = red[e * LDR + jj];
+  }
+}
+
+// ---------------------------------------------------------------- dx on matrix cores
+// Block: 64 tokens (wave w: 16) x 256 columns (4 passes of 64).  A[s][e] = dL
+// in three bf16 parts, kept in registers; B[e][j] = W[j][e] from the block's W
+// rows staged in LDS.  The 16 x 64 fp32 results go through LDS column-major
+// (each lane's 4 tokens of one column are contiguous: one 16-byte store; a
+// row-major tile written element by element was miscompiled, two of its LDS
+// stores merged with a wrong offset), then each lane adds the incoming dx to
+// two 8-column pieces of a token row and stores them, 16 bytes each.
+template <int NT>
+__global__ __launch_bounds__(kBwdThreads) void dx_mfma_kernel(GateBwdArgs a) {
+  constexpr int E = 16 * NT;
+  constexpr int KS = (E + 31) / 32;  // K steps of 32 experts (a half step when E % 32 == 16)
+  constexpr int LDW = E + 8;         // padded W row in LDS (bf16)
+  constexpr int LDT = 16 + 4;        // padded column of the output tile (fp32, 16 tokens)
+  __shared__ __align__(16) uint16_t wl[kWave * LDW];
+  __shared__ __align__(16) float ot[kBwdWaves * kWave * LDT];
+  const int w = threadIdx.x / kWave, lane = lane_id();
+  const int g = lane / 16, m = lane % 16;
+  const int64_t s0 = static_cast<int64_t>(blockIdx.x) * kWave + 16 * w;
+  const uint16_t* wg = reinterpret_cast<const uint16_t*>(a.wg);
+  const u32x4 zero = {0u, 0u, 0u, 0u};
+
+  u32x4 ah[KS], am[KS], al[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    const int e0 = 32 * ks + 8 * g;
+    const int64_t s = s0 + m;
+    float vv[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    if (s < a.S && e0 < E) {
+      const float4 p0 = *reinterpret_cast<const float4*>(a.dl + s * E + e0);
+      const float4 p1 = *reinterpret_cast<const float4*>(a.dl + s * E + e0 + 4);
+      vv[0] = p0.x; vv[1] = p0.y; vv[2] = p0.z; vv[3] = p0.w;
+      vv[4] = p1.x; vv[5] = p1.y; vv[6] = p1.z; vv[7] = p1.w;
+    }
+    split8(vv, ah[ks], am[ks], al[ks]);
+  }
+  float* out = ot + w * kWave * LDT;
+  const int jb = blockIdx.y * 4 * kWave;
+  for (int cb = 0; cb < 4; ++cb) {
+    const int j0 = jb + cb * kWave;
+    if (j0 >= a.d) break;  // the same for the whole block
+    // lane -> two chunks of 8 columns of one token (chunk id = lane + 64 h);
+    // the incoming dx is requested now and used after the products
+    u32x4 din[2];
+    u32x4* dst[2];
+    bool okh[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int id = lane + kWave * h, t = id / 8, c8 = id % 8;
+      const int64_t s = s0 + t;
+      okh[h] = s < a.S;
+      dst[h] = reinterpret_cast<u32x4*>(reinterpret_cast<uint16_t*>(a.dx) + (okh[h] ? s : 0) * a.d + j0 + 8 * c8);
+      din[h] = (a.accumulate && okh[h]) ? *dst[h] : zero;
+    }
+    __syncthreads();       // previous W rows and outputs consumed
+    for (int q = threadIdx.x; q < kWave * (E / 8); q += kBwdThreads) {
+      const int r = q / (E / 8), p8 = q % (E / 8);
+      *reinterpret_cast<u32x4*>(&wl[r * LDW + 8 * p8]) =
+          *reinterpret_cast<const u32x4*>(wg + static_cast<int64_t>(j0 + r) * E + 8 * p8);
+    }
+    __syncthreads();
+    f32x4 acc[4];
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt) {
+      acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const int e0 = 32 * ks + 8 * g;
+        const u32x4 b = e0 < E ? *reinterpret_cast<const u32x4*>(&wl[(16 * nt + m) * LDW + e0]) : zero;
+        acc[nt] = mfma_bf16(ah[ks], b, acc[nt]);
+        acc[nt] = mfma_bf16(am[ks], b, acc[nt]);
+        acc[nt] = mfma_bf16(al[ks], b, acc[nt]);
+      }
+    }
+    // lane (g, m) holds tokens 4 g + i of column 16 nt + m
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt)
+      *reinterpret_cast<float4*>(&out[(16 * nt + m) * LDT + 4 * g]) =
+          make_float4(acc[nt][0], acc[nt][1], acc[nt][2], acc[nt][3]);
+    __syncthreads();
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int id = lane + kWave * h, t = id / 8, c8 = id % 8;
+      float o[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) o[q] = out[(8 * c8 + q) * LDT + t];
+      if (a.accumulate) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          o[2 * q] += bf16_lo(din[h][q]);
+          o[2 * q + 1] += bf16_hi(din[h][q]);
+        }
+      }
+      if (okh[h])
+        *dst[h] = u32x4{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]), pack_bf16x2(o[4], o[5]),
+                        pack_bf16x2(o[6], o[7])};
+    }
+  }
+}
+
+// ---------------------------------------------------------------- dW, dx on the vector ALUs
 // Block (j-tile of 64 columns, token range `split`, expert chunk of EC): x and
 // dL tiles of 64 tokens staged in LDS; thread (column jj, expert quarter eg)
-// accumulates EC/4 sums.  Partials [split][E][d]; blocks of the first j-tile
-// also sum dL for db.
+// accumulates EC/4 sums, tile by tile.  Partials [split][E][d].
 template <typename T, int EC>
 __global__ __launch_bounds__(kBwdThreads) void dwg_partial_kernel(GateBwdArgs a) {
   constexpr int EG = EC / 4;
@@ -253,12 +564,9 @@ __global__ __launch_bounds__(kBwdThreads) void dwg_partial_kernel(GateBwdArgs a)
   float acc[EG];
 #pragma unroll
   for (int i = 0; i < EG; ++i) acc[i] = 0.f;
-  float bacc = 0.f;
-  const bool do_bias = blockIdx.x == 0 && t < EC;
-  const bool do_w = a.dwg != nullptr;  // else only db is wanted and x may be absent
   for (int64_t s0 = sb; s0 < se; s0 += kWave) {
     __syncthreads();
-    for (int q = t; do_w && q < kWave * kWave; q += kBwdThreads) {
+    for (int q = t; q < kWave * kWave; q += kBwdThreads) {
       const int tok = q / kWave, col = q % kWave;
       const int64_t s = s0 + tok;
       const int jx = j0 + col;
@@ -276,48 +584,35 @@ __global__ __launch_bounds__(kBwdThreads) void dwg_partial_kernel(GateBwdArgs a)
     float tacc[EG];
 #pragma unroll
     for (int i = 0; i < EG; ++i) tacc[i] = 0.f;
-    for (int tok = 0; do_w && tok < kWave; ++tok) {
+    for (int tok = 0; tok < kWave; ++tok) {
       const float xv = xs[tok][jj];
 #pragma unroll
       for (int i = 0; i < EG; ++i) tacc[i] = fmaf(xv, ds[tok][eg * EG + i], tacc[i]);
     }
 #pragma unroll
     for (int i = 0; i < EG; ++i) acc[i] += tacc[i];
-    if (do_bias) {
-      float tb = 0.f;
-      for (int tok = 0; tok < kWave; ++tok) tb += ds[tok][t];
-      bacc += tb;
-    }
   }
   const int jw = j0 + jj;
-  if (do_w && jw < a.d) {
+  if (jw < a.d) {
 #pragma unroll
     for (int i = 0; i < EG; ++i) {
       const int e = e0 + eg * EG + i;
       if (e < a.E) a.wpart[(static_cast<int64_t>(split) * a.E + e) * a.d + jw] = acc[i];
     }
   }
-  if (do_bias && e0 + t < a.E) a.bpart[static_cast<int64_t>(split) * a.E + e0 + t] = bacc;
 }
 
-// dwg[j][e] = sum over splits, in order; dbias likewise.
+// dwg[j][e] = sum over the token ranges, in order.
 __global__ __launch_bounds__(kBwdThreads) void dwg_reduce_kernel(GateBwdArgs a) {
   const int64_t n = static_cast<int64_t>(a.E) * a.d;
   const int64_t idx = static_cast<int64_t>(blockIdx.x) * kBwdThreads + threadIdx.x;
-  if (a.dwg && idx < n) {
-    const int e = static_cast<int>(idx / a.d), jx = static_cast<int>(idx % a.d);
-    float v = 0.f;
-    for (int sp = 0; sp < a.nsplit; ++sp) v += a.wpart[static_cast<int64_t>(sp) * n + idx];
-    a.dwg[static_cast<int64_t>(jx) * a.E + e] = v;
-  }
-  if (a.dbias && idx < a.E) {
-    float v = 0.f;
-    for (int sp = 0; sp < a.nsplit; ++sp) v += a.bpart[static_cast<int64_t>(sp) * a.E + idx];
-    a.dbias[idx] = v;
-  }
+  if (idx >= n) return;
+  const int e = static_cast<int>(idx / a.d), jx = static_cast<int>(idx % a.d);
+  float v = 0.f;
+  for (int sp = 0; sp < a.nsplit; ++sp) v += a.wpart[static_cast<int64_t>(sp) * n + idx];
+  a.dwg[static_cast<int64_t>(jx) * a.E + e] = v;
 }
 
-// ---------------------------------------------------------------- dx
 // Block: 64 tokens x 64 columns.  Thread (column jj, token group tg) keeps the
 // chunk of W's row j in registers and accumulates 16 tokens; dL tiles are
 // staged in LDS and read as broadcasts.
@@ -341,16 +636,16 @@ __global__ __launch_bounds__(kBwdThreads) void dx_kernel(GateBwdArgs a) {
       const int e = e0 + ee;
       ds[tok][ee] = (s < a.S && e < a.E) ? a.dl[s * a.E + e] : 0.f;
     }
-    float w[EC];
+    float wv[EC];
 #pragma unroll
     for (int ee = 0; ee < EC; ++ee)
-      w[ee] = (jx < a.d && e0 + ee < a.E) ? load_elem(wg, static_cast<int64_t>(jx) * a.E + e0 + ee) : 0.f;
+      wv[ee] = (jx < a.d && e0 + ee < a.E) ? load_elem(wg, static_cast<int64_t>(jx) * a.E + e0 + ee) : 0.f;
     __syncthreads();
 #pragma unroll
     for (int i = 0; i < TPT; ++i) {
       const float* drow = ds[tg + 4 * i];
 #pragma unroll
-      for (int ee = 0; ee < EC; ++ee) acc[i] = fmaf(drow[ee], w[ee], acc[i]);
+      for (int ee = 0; ee < EC; ++ee) acc[i] = fmaf(drow[ee], wv[ee], acc[i]);
     }
   }
   if (jx >= a.d) return;
@@ -362,7 +657,7 @@ __global__ __launch_bounds__(kBwdThreads) void dx_kernel(GateBwdArgs a) {
     float v = acc[i];
     if (a.dtype == 1) {
       uint16_t* dx = reinterpret_cast<uint16_t*>(a.dx);
-      if (a.accumulate) v += __uint_as_float(static_cast<uint32_t>(dx[o]) << 16);
+      if (a.accumulate) v += bf16_bits_to_f32(dx[o]);
       dx[o] = static_cast<uint16_t>(f32_to_bf16_bits(v));
     } else {
       float* dx = reinterpret_cast<float*>(a.dx);
@@ -375,49 +670,104 @@ __global__ __launch_bounds__(kBwdThreads) void dx_kernel(GateBwdArgs a) {
 // ---------------------------------------------------------------- launchers
 template <int P, int EPL>
 static void launch_dl_t(const GateBwdArgs& a, hipStream_t st) {
-  const unsigned blocks = static_cast<unsigned>((a.nb + kBwdWaves - 1) / kBwdWaves);
-  gate_dl_kernel<P, EPL><<<dim3(blocks), dim3(kBwdThreads), 0, st>>>(a);
+  // up to 16 waves per 64-token block (one pass each) while the sums fit LDS
+  constexpr int TP = kWave / P;
+  constexpr int WAVES = P <= 32 ? (kWave / TP < 16 ? kWave / TP : 16) : 4;
+  const size_t tile = a.dlt ? static_cast<size_t>(kWave) * (a.E + 1) * sizeof(float) : 0;
+  const size_t sums = static_cast<size_t>(2 * WAVES) * a.E * sizeof(float);
+  gate_dl_kernel<P, EPL, WAVES>
+      <<<dim3(static_cast<unsigned>(a.nb)), dim3(WAVES * kWave), tile > sums ? tile : sums, st>>>(a);
 }
 
+static void launch_colsum_f(const float* part, int64_t rows, int E, float* out, hipStream_t st) {
+  colsum_kernel<float><<<dim3((E + kWave - 1) / kWave), dim3(1024), 0, st>>>(part, rows, E, out);
+}
+
+// The per-block first-choice counts sit right after cnt in the workspace.
 hipError_t launch_gate_bwd_dl(const GateBwdArgs& a, hipStream_t st) {
   const bool aux = a.aux_coef != 0.f;
-  if (aux) aux_counts_kernel<<<dim3(1), dim3(1024), static_cast<size_t>(a.E) * sizeof(int), st>>>(a);
+  if (aux) {
+    int32_t* cpart = a.cnt + a.E;
+    const int64_t cblocks = (static_cast<int64_t>(a.S) + kCountTokens - 1) / kCountTokens;
+    if (cblocks > 0)
+      aux_counts_kernel<<<dim3(static_cast<unsigned>(cblocks)), dim3(1024), static_cast<size_t>(a.E) * sizeof(int),
+                          st>>>(a, cpart);
+    colsum_kernel<int32_t><<<dim3((a.E + kWave - 1) / kWave), dim3(1024), 0, st>>>(cpart, cblocks, a.E, a.cnt);
+  }
   if (a.nb > 0) {
     const int E = a.E;
-    if (E <= 1) launch_dl_t<1, 1>(a, st);
-    else if (E <= 2) launch_dl_t<2, 1>(a, st);
-    else if (E <= 4) launch_dl_t<4, 1>(a, st);
-    else if (E <= 8) launch_dl_t<8, 1>(a, st);
-    else if (E <= 16) launch_dl_t<16, 1>(a, st);
-    else if (E <= 32) launch_dl_t<32, 1>(a, st);
-    else if (E <= 64) launch_dl_t<64, 1>(a, st);
-    else if (E <= 128) launch_dl_t<64, 2>(a, st);
+    if (E <= 4) launch_dl_t<4, 1>(a, st);
+    else if (E <= 8) launch_dl_t<4, 2>(a, st);
+    else if (E <= 16) launch_dl_t<4, 4>(a, st);
+    else if (E <= 32) launch_dl_t<8, 4>(a, st);
+    else if (E <= 64) launch_dl_t<16, 4>(a, st);
+    else if (E <= 128) launch_dl_t<32, 4>(a, st);
     else if (E <= 256) launch_dl_t<64, 4>(a, st);
     else if (E <= 512) launch_dl_t<64, 8>(a, st);
     else launch_dl_t<64, 16>(a, st);
   }
-  if (aux && a.aux_loss) aux_loss_kernel<<<dim3(1), dim3(1024), 0, st>>>(a);
+  if (a.dbias) launch_colsum_f(a.bpart, a.nb, a.E, a.dbias, st);
+  if (aux && a.aux_loss) {
+    launch_colsum_f(a.ppart, a.nb, a.E, a.pe, st);
+    aux_loss_kernel<<<dim3(1), dim3(1024), 0, st>>>(a);
+  }
   return hipGetLastError();
 }
 
-constexpr int kDwEC = 64;  // experts per dW block
-constexpr int kDxEC = 32;  // experts per register chunk in dx
+constexpr int kDwEC = 64;  // experts per vector-ALU dW block
+constexpr int kDxEC = 32;  // experts per register chunk in the vector-ALU dx
+
+template <int NT>
+static void launch_dwg_mfma_t(const GateBwdArgs& a, hipStream_t st) {
+  const dim3 grid(static_cast<unsigned>(a.d / kWave), static_cast<unsigned>(a.nsplit));
+  dwg_mfma_kernel<NT><<<grid, dim3(kBwdThreads), 0, st>>>(a);
+}
 
 hipError_t launch_gate_bwd_dwg(const GateBwdArgs& a, hipStream_t st) {
   if (a.nsplit > 0) {
-    const unsigned jtiles = a.dwg ? static_cast<unsigned>((a.d + kWave - 1) / kWave) : 1u;
-    const dim3 grid(jtiles, a.nsplit, (a.E + kDwEC - 1) / kDwEC);
-    if (a.dtype == 1) dwg_partial_kernel<bf16_t, kDwEC><<<grid, dim3(kBwdThreads), 0, st>>>(a);
-    else dwg_partial_kernel<float, kDwEC><<<grid, dim3(kBwdThreads), 0, st>>>(a);
+    if (a.mfma_dw) {
+      switch (a.E / 16) {
+        case 1: launch_dwg_mfma_t<1>(a, st); break;
+        case 2: launch_dwg_mfma_t<2>(a, st); break;
+        case 3: launch_dwg_mfma_t<3>(a, st); break;
+        case 4: launch_dwg_mfma_t<4>(a, st); break;
+        case 5: launch_dwg_mfma_t<5>(a, st); break;
+        case 6: launch_dwg_mfma_t<6>(a, st); break;
+        case 7: launch_dwg_mfma_t<7>(a, st); break;
+        default: launch_dwg_mfma_t<8>(a, st); break;
+      }
+    } else {
+      const dim3 grid((a.d + kWave - 1) / kWave, a.nsplit, (a.E + kDwEC - 1) / kDwEC);
+      if (a.dtype == 1) dwg_partial_kernel<bf16_t, kDwEC><<<grid, dim3(kBwdThreads), 0, st>>>(a);
+      else dwg_partial_kernel<float, kDwEC><<<grid, dim3(kBwdThreads), 0, st>>>(a);
+    }
   }
-  const int64_t n = static_cast<int64_t>(a.E) * (a.dwg ? a.d : 1);
-  const unsigned blocks = static_cast<unsigned>((n + kBwdThreads - 1) / kBwdThreads);
-  if (blocks > 0) dwg_reduce_kernel<<<dim3(blocks), dim3(kBwdThreads), 0, st>>>(a);
+  const int64_t n = static_cast<int64_t>(a.E) * a.d;
+  dwg_reduce_kernel<<<dim3(static_cast<unsigned>((n + kBwdThreads - 1) / kBwdThreads)), dim3(kBwdThreads), 0, st>>>(a);
   return hipGetLastError();
+}
+
+template <int NT>
+static void launch_dx_mfma_t(const GateBwdArgs& a, hipStream_t st) {
+  const dim3 grid(static_cast<unsigned>(a.nb), static_cast<unsigned>((a.d + 4 * kWave - 1) / (4 * kWave)));
+  dx_mfma_kernel<NT><<<grid, dim3(kBwdThreads), 0, st>>>(a);
 }
 
 hipError_t launch_gate_bwd_dx(const GateBwdArgs& a, hipStream_t st) {
   if (a.nb == 0) return hipSuccess;
+  if (a.mfma_dx) {
+    switch (a.E / 16) {
+      case 1: launch_dx_mfma_t<1>(a, st); break;
+      case 2: launch_dx_mfma_t<2>(a, st); break;
+      case 3: launch_dx_mfma_t<3>(a, st); break;
+      case 4: launch_dx_mfma_t<4>(a, st); break;
+      case 5: launch_dx_mfma_t<5>(a, st); break;
+      case 6: launch_dx_mfma_t<6>(a, st); break;
+      case 7: launch_dx_mfma_t<7>(a, st); break;
+      default: launch_dx_mfma_t<8>(a, st); break;
+    }
+    return hipGetLastError();
+  }
   const dim3 grid((a.d + kWave - 1) / kWave, a.nb);
   if (a.dtype == 1) dx_kernel<bf16_t, kDxEC><<<grid, dim3(kBwdThreads), 0, st>>>(a);
   else dx_kernel<float, kDxEC><<<grid, dim3(kBwdThreads), 0, st>>>(a);

@@ -73,22 +73,32 @@ struct GateBwdArgs {
   int S, d, E, k, nb;       // nb: 64-token wave blocks
   int kind, normalize, dtype, accumulate;
   float aux_coef;
-  int nsplit, split_tokens; // dW is summed over tokens in nsplit ranges of split_tokens
+  int nsplit, split_tokens; // dW is summed over tokens in nsplit ranges of split_tokens (a multiple of 64)
+  int mfma_dw, mfma_dx;     // matrix-core paths (bf16, E a multiple of 16 up to 128, d a multiple of 64)
+  int64_t s_pad;            // row length of dlt: S rounded up to 64
   const void* x;            // [S, d]
   const void* wg;           // [d, E]
   const float* logits;      // [S, E]
   const int32_t* ids;       // [S, k]
   const float* dw;          // [S, k]
   float* dl;                // [S, E] dL (caller's dlogits or workspace)
+  uint16_t* dlt;            // [3][E, s_pad] dL transposed, split into three bf16 planes
+                            // (hi + mid + lo == dL), zero beyond S (matrix-core dW only)
   void* dx;                 // [S, d] or null
   float* dwg;               // [d, E] or null
   float* dbias;             // [E] or null
   float* aux_loss;          // [1] or null
   int32_t* cnt;             // [E] first-choice counts (load-balancing loss)
   float* ppart;             // [nb, E] per wave block sums of the softmax (load-balancing loss)
+  float* bpart;             // [nb, E] per wave block sums of dL (db)
+  float* pe;                // [E] sums of the softmax over all tokens
   float* wpart;             // [nsplit, E, d] partial dW
-  float* bpart;             // [nsplit, E] partial db
 };
+
+// Matrix-core paths of the gate backward for this shape.
+inline bool gate_bwd_mfma_shape(int dtype, int E, int d) {
+  return dtype == 1 && E % 16 == 0 && E <= 128 && d % 64 == 0;
+}
 
 hipError_t launch_gate_bwd_dl(const GateBwdArgs& a, hipStream_t st);
 hipError_t launch_gate_bwd_dwg(const GateBwdArgs& a, hipStream_t st);

@@ -23,21 +23,6 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 // (+ bias) then go to LDS and 4 lanes per token select.
 constexpr int kMfmaTokens = 64;
 
-// 8 x 8 transpose of bf16: in[j] holds row j (8 half-words, lowest first);
-// out[i] receives column i.
-__device__ __forceinline__ void transpose8x8_b16(const u32x4 (&in)[8], u32x4 (&out)[8]) {
-#pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    uint32_t wd[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const uint32_t a = in[2 * q][i / 2], b = in[2 * q + 1][i / 2];
-      wd[q] = (i & 1) ? ((a >> 16) | (b & 0xffff0000u)) : ((a & 0xffffu) | (b << 16));
-    }
-    out[i] = u32x4{wd[0], wd[1], wd[2], wd[3]};
-  }
-}
-
 template <int NT, int KC, int KMAX, bool KTOP1>
 __global__ __launch_bounds__(kBlock) void route_mfma_kernel(RouteArgs a) {
   constexpr int E = NT * 16;

@@ -161,19 +161,28 @@ def _a256(n):
     return (n + 255) // 256 * 256
 
 
+def _bwd_ws_formula(S, d, E, dtype):
+    nb = (S + 63) // 64
+    mfma = dtype == b.MOE_BF16 and E % 16 == 0 and E <= 128 and d % 64 == 0
+    per_split = d // 64 if mfma else ((d + 63) // 64) * ((E + 63) // 64)
+    target = 512 if mfma else 1024
+    ns = max(1, min(-(-target // per_split), nb))
+    st = max(64, -(-(-(-S // ns)) // 64) * 64)
+    nsplit = -(-S // st)
+    return (_a256(S * E * 4) + (_a256(3 * nb * 64 * E * 2) if mfma else 0) + _a256((1 + -(-S // 4096)) * E * 4)
+            + 2 * _a256(nb * E * 4) + _a256(E * 4) + _a256(nsplit * E * d * 4))
+
+
 def test_gate_bwd_struct_and_workspace(lib):
     assert ctypes.sizeof(b.GateBwdParams) == 40
     assert b.GateBwdParams.aux_coef.offset == 32
-    for S, d, E, k in [(32768, 2048, 64, 4), (1000, 256, 8, 1), (0, 16, 3, 1), (5000, 64, 1024, 2)]:
-        p = hm.gate_bwd_params(S, d, E, k, 0)
+    for S, d, E, k, dt in [(32768, 2048, 64, 4, b.MOE_BF16), (32768, 2048, 64, 4, b.MOE_F32),
+                           (1000, 256, 8, 1, b.MOE_F32), (0, 16, 3, 1, b.MOE_F32), (5000, 64, 1024, 2, b.MOE_BF16),
+                           (8192, 1024, 16, 2, b.MOE_BF16), (100, 520, 48, 2, b.MOE_BF16)]:
+        p = hm.gate_bwd_params(S, d, E, k, 0, dtype=dt)
         st, n = _bwd_ws(p)
         assert st == 0
-        nb = (S + 63) // 64
-        split = max(1024, (16 * E + 63) // 64 * 64)
-        nsplit = (S + split - 1) // split
-        want = (_a256(S * E * 4) + _a256(E * 4) + _a256(nb * E * 4) + _a256(nsplit * E * d * 4)
-                + _a256(nsplit * E * 4))
-        assert n == want, (S, d, E, k)
+        assert n == _bwd_ws_formula(S, d, E, dt), (S, d, E, k, dt)
 
 
 BAD_BWD = [

@@ -341,8 +341,8 @@ __global__ __launch_bounds__(1024) void aux_loss_kernel(GateBwdArgs a) {
 }
 
 // ---------------------------------------------------------------- dW on matrix cores
-// Block: 64 columns of x (blockIdx.x) x one token range (blockIdx.y); its 4
-// waves take the range's 64-token chunks in turn, each on its own.  A wave transposes its chunk
+// Block: 64 columns of x x one token range; its 4 waves take the range's
+// 64-token chunks in turn, each on its own.  A wave transposes its chunk
 // of x into LDS (each lane one 8 x 8 block, transposed in registers) and runs
 // 4 M tiles (16 columns) x NT N tiles (16 experts) with K = 32 tokens:
 // A[j][s] = x[s][j] from the tile, B[s][e] = dL^T[e][s] from its three bf16
@@ -359,8 +359,14 @@ __global__ __launch_bounds__(kBwdThreads) void dwg_mfma_kernel(GateBwdArgs a) {
   const int w = threadIdx.x / kWave, lane = lane_id();
   const int g = lane / 16, m = lane % 16;
   const int bb = lane % 8, ab = lane / 8;  // the 8 x 8 block this lane stages
-  const int j0 = blockIdx.x * kWave;
-  const int split = blockIdx.y;
+  // 1-D grid, blocks dealt round-robin to the 8 XCDs (block id mod 8): all
+  // column blocks of one token range go to the same XCD and share its L2 copy
+  // of that range's dL planes
+  const int ncb = a.d / kWave;
+  const int xcd = blockIdx.x % 8, r8 = blockIdx.x / 8;
+  const int split = xcd + 8 * (r8 / ncb);
+  const int j0 = (r8 % ncb) * kWave;
+  if (split >= a.nsplit) return;  // idle block (whole block, before any barrier)
   const int64_t sb = static_cast<int64_t>(split) * a.split_tokens;
   const int64_t se = min(static_cast<int64_t>(a.S), sb + a.split_tokens);
   const int nchunks = static_cast<int>((se - sb + kWave - 1) / kWave);
@@ -485,6 +491,20 @@ __global__ __launch_bounds__(kBwdThreads) void dx_mfma_kernel(GateBwdArgs a) {
   }
   float* out = ot + w * kWave * LDT;
   const int jb = blockIdx.y * 4 * kWave;
+  // W rows of the next pass are loaded into registers while this one runs
+  constexpr int WPT = (kWave * (E / 8) + kBwdThreads - 1) / kBwdThreads;  // 16-byte pieces per thread
+  u32x4 wreg[WPT];
+  auto load_w = [&](int j0) {
+#pragma unroll
+    for (int u = 0; u < WPT; ++u) {
+      const int q = threadIdx.x + u * kBwdThreads;
+      const int r = q / (E / 8), p8 = q % (E / 8);
+      wreg[u] = (q < kWave * (E / 8) && j0 < a.d)
+                    ? *reinterpret_cast<const u32x4*>(wg + static_cast<int64_t>(j0 + r) * E + 8 * p8)
+                    : zero;
+    }
+  };
+  load_w(jb);
   for (int cb = 0; cb < 4; ++cb) {
     const int j0 = jb + cb * kWave;
     if (j0 >= a.d) break;  // the same for the whole block
@@ -501,13 +521,15 @@ __global__ __launch_bounds__(kBwdThreads) void dx_mfma_kernel(GateBwdArgs a) {
       dst[h] = reinterpret_cast<u32x4*>(reinterpret_cast<uint16_t*>(a.dx) + (okh[h] ? s : 0) * a.d + j0 + 8 * c8);
       din[h] = (a.accumulate && okh[h]) ? *dst[h] : zero;
     }
-    __syncthreads();       // previous W rows and outputs consumed
-    for (int q = threadIdx.x; q < kWave * (E / 8); q += kBwdThreads) {
+    __syncthreads();  // previous pass's W rows consumed
+#pragma unroll
+    for (int u = 0; u < WPT; ++u) {
+      const int q = threadIdx.x + u * kBwdThreads;
       const int r = q / (E / 8), p8 = q % (E / 8);
-      *reinterpret_cast<u32x4*>(&wl[r * LDW + 8 * p8]) =
-          *reinterpret_cast<const u32x4*>(wg + static_cast<int64_t>(j0 + r) * E + 8 * p8);
+      if (q < kWave * (E / 8)) *reinterpret_cast<u32x4*>(&wl[r * LDW + 8 * p8]) = wreg[u];
     }
     __syncthreads();
+    load_w(j0 + kWave);
     f32x4 acc[4];
 #pragma unroll
     for (int nt = 0; nt < 4; ++nt) {
@@ -521,12 +543,15 @@ __global__ __launch_bounds__(kBwdThreads) void dx_mfma_kernel(GateBwdArgs a) {
         acc[nt] = mfma_bf16(al[ks], b, acc[nt]);
       }
     }
-    // lane (g, m) holds tokens 4 g + i of column 16 nt + m
+    // lane (g, m) holds tokens 4 g + i of column 16 nt + m; the tile is the
+    // wave's own, so wave-level fences order it
 #pragma unroll
     for (int nt = 0; nt < 4; ++nt)
       *reinterpret_cast<float4*>(&out[(16 * nt + m) * LDT + 4 * g]) =
           make_float4(acc[nt][0], acc[nt][1], acc[nt][2], acc[nt][3]);
-    __syncthreads();
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       const int id = lane + kWave * h, t = id / 8, c8 = id % 8;
@@ -544,6 +569,9 @@ __global__ __launch_bounds__(kBwdThreads) void dx_mfma_kernel(GateBwdArgs a) {
         *dst[h] = u32x4{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]), pack_bf16x2(o[4], o[5]),
                         pack_bf16x2(o[6], o[7])};
     }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
 }
 
@@ -719,7 +747,8 @@ constexpr int kDxEC = 32;  // experts per register chunk in the vector-ALU dx
 
 template <int NT>
 static void launch_dwg_mfma_t(const GateBwdArgs& a, hipStream_t st) {
-  const dim3 grid(static_cast<unsigned>(a.d / kWave), static_cast<unsigned>(a.nsplit));
+  const int64_t per_xcd = (a.nsplit + 7) / 8;  // token ranges per XCD
+  const dim3 grid(static_cast<unsigned>(8 * per_xcd * (a.d / kWave)));
   dwg_mfma_kernel<NT><<<grid, dim3(kBwdThreads), 0, st>>>(a);
 }
 

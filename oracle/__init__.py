@@ -35,12 +35,16 @@ from .gate import (
     GATE_TOPK,
     GATE_KTOP1,
     GATE_HASH,
+    GATE_HTOPK,
     capacity,
     logits,
     select,
     gate_weights,
     splitmix64_output,
     hash_ids,
+    noisy_logits_f32,
+    balanced_hash_table,
+    table_hash_ids,
     assign_slots,
     gate,
 )
@@ -49,8 +53,9 @@ from .gate_bwd import gate_dlogits, aux_loss, gate_input_grads
 
 __all__ = [
     "bf16_to_f64", "f64_to_bf16", "decode", "encode",
-    "GATE_TOPK", "GATE_KTOP1", "GATE_HASH", "capacity", "logits", "select",
-    "gate_weights", "splitmix64_output", "hash_ids", "assign_slots", "gate",
+    "GATE_TOPK", "GATE_KTOP1", "GATE_HASH", "GATE_HTOPK", "capacity", "logits", "select",
+    "gate_weights", "splitmix64_output", "hash_ids", "noisy_logits_f32", "balanced_hash_table",
+    "table_hash_ids", "assign_slots", "gate",
     "dispatch", "combine", "dispatch_bwd", "combine_bwd",
     "gate_dlogits", "aux_loss", "gate_input_grads",
 ]

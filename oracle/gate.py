@@ -25,6 +25,15 @@ R5  a dropped assignment contributes nothing; weights are not renormalised.
 R8  kTop1 groups are contiguous, [g*E/k, (g+1)*E/k); softmax within each group.
 R9  hash: H(t) is output number t+1 of a SplitMix64 generator seeded with
     ``seed`` (Steele, Lea & Flood, OOPSLA 2014); expert = H(t) mod E; weight 1.
+R19 hierarchical top-k (Sec. 3.1, H Topk / SAM): experts form G contiguous
+    groups; the switch step picks the group holding the best expert, the
+    mixture step the k best experts inside that group; weights as for TopK.
+R20 Dense-To-Sparse (Sec. 3.1): the gate acts on (L + g) / tau, g a Gumbel
+    sample given as input and tau the temperature, evaluated in fp32 (one
+    rounded addition, one rounded division) so that selection on it is exact.
+R21 balanced hash (Sec. 3.1, Hash Layer, balanced assignment): tokens in order
+    of decreasing frequency (ties: lower id) each go to the expert with the
+    smallest load so far (ties: lower index); the load is the summed frequency.
 """
 
 import math
@@ -36,6 +45,7 @@ from .bf16 import decode
 GATE_TOPK = 0
 GATE_KTOP1 = 1
 GATE_HASH = 2
+GATE_HTOPK = 3
 
 _MASK64 = (1 << 64) - 1
 # SplitMix64 constants as published by Steele, Lea & Flood (OOPSLA 2014) and in
@@ -76,12 +86,14 @@ def _key(row, e):
     return (-row[e], e)
 
 
-def select(L, kind, k):
-    """Chosen experts per token: ids[S, k] int32 (TopK of Eq. 1, or kTop1).
+def select(L, kind, k, groups=0):
+    """Chosen experts per token: ids[S, k] int32 (TopK of Eq. 1, kTop1 or H Topk).
 
     TOPK : ids[s, r] is the r-th expert in key order (rank 0 is the best).
     KTOP1: ids[s, g] is the best expert of group g = [g*E/k, (g+1)*E/k)
            (Sec. 3.1, kTop1: experts split into k prototypes, top-1 in each).
+    HTOPK: with ``groups`` contiguous groups of E/groups experts, the group of
+           the best expert, then its k best experts in key order (R19).
     """
     L = np.asarray(L, dtype=np.float64)
     S, E = L.shape
@@ -92,6 +104,16 @@ def select(L, kind, k):
         for s in range(S):
             row = L[s]
             order = sorted(range(E), key=lambda e: _key(row, e))
+            ids[s, :] = order[:k]
+    elif kind == GATE_HTOPK:
+        if groups < 1 or E % groups != 0 or not 1 <= k <= E // groups:
+            raise ValueError("HTOPK needs E % groups == 0 and 1 <= k <= E / groups")
+        Gs = E // groups
+        for s in range(S):
+            row = L[s]
+            best = min(range(E), key=lambda e: _key(row, e))
+            g = best // Gs
+            order = sorted(range(g * Gs, (g + 1) * Gs), key=lambda e: _key(row, e))
             ids[s, :] = order[:k]
     elif kind == GATE_KTOP1:
         if E % k != 0:
@@ -112,6 +134,7 @@ def gate_weights(L, ids, kind, normalize):
     TOPK, normalize=1: softmax over the k selected logits (Eq. 1 as printed).
     TOPK, normalize=0: full softmax over all E experts, read at the chosen one
                        (reading R1, the Switch gate).
+    HTOPK            : as TOPK (the chosen experts come from one group, R19).
     KTOP1            : softmax within the chosen expert's group (reading R8).
     HASH             : 1.
     Every softmax subtracts the maximum of the logits it normalises over; the
@@ -125,6 +148,8 @@ def gate_weights(L, ids, kind, normalize):
     E = L.shape[1]
     rows = np.arange(S)[:, None]
     chosen = L[rows, ids]                      # [S, k]
+    if kind == GATE_HTOPK:
+        kind = GATE_TOPK
     if kind == GATE_TOPK and normalize:
         m = chosen.max(axis=1, keepdims=True)
         num = np.exp(chosen - m)
@@ -170,6 +195,33 @@ def hash_ids(token_ids, E, seed):
     return out
 
 
+def noisy_logits_f32(L, noise, temperature):
+    """Dense-To-Sparse logits (R20): (L + g) / tau in fp32, each operation rounded
+    to nearest; L, noise float32 [S, E] (noise may be None), tau > 0."""
+    L = np.asarray(L, dtype=np.float32)
+    v = L if noise is None else (L + np.asarray(noise, dtype=np.float32)).astype(np.float32)
+    return (v / np.float32(temperature)).astype(np.float32)
+
+
+def balanced_hash_table(freq, E):
+    """Balanced assignment of token ids to E experts (R21): table[vocab] int32."""
+    freq = [float(f) for f in freq]
+    order = sorted(range(len(freq)), key=lambda t: (-freq[t], t))
+    load = [0.0] * E
+    table = np.empty(len(freq), dtype=np.int32)
+    for t in order:
+        e = min(range(E), key=lambda i: (load[i], i))
+        table[t] = e
+        load[e] += freq[t]
+    return table
+
+
+def table_hash_ids(token_ids, table):
+    """Hash gate with a lookup table (Sec. 3.1, Hash Layer): ids[S, 1] = table[t]."""
+    table = np.asarray(table)
+    return table[np.asarray(token_ids)].astype(np.int32).reshape(-1, 1)
+
+
 def assign_slots(ids, E, C):
     """Capacity-limited position of every (token, rank) in its expert's buffer.
 
@@ -200,25 +252,34 @@ def assign_slots(ids, E, C):
 
 
 def gate(kind, k, E, C, normalize=0, dtype="f32", x=None, wg=None, bias=None,
-         token_ids=None, hash_seed=0, sel_logits=None):
+         token_ids=None, hash_seed=0, sel_logits=None, groups=0, noise=None, temperature=0.0,
+         hash_table=None):
     """Step 1 of Algorithm 1 end to end: logits -> selection -> weights -> slots.
 
     ``sel_logits`` (float array [S, E]) overrides the logits used for selection
     and weights; the parity tests pass the device's own fp32 logits here so that
-    integer routing can be compared bit for bit.  Returns a dict.
+    integer routing can be compared bit for bit.  With ``temperature`` > 0 the
+    computed logits are made Dense-To-Sparse logits (R20; in fp64 here, for the
+    tolerance check of the device's values).  Returns a dict.
     """
     out = {}
     if kind == GATE_HASH:
-        ids = hash_ids(token_ids, E, hash_seed)
+        if hash_table is not None:
+            ids = table_hash_ids(token_ids, hash_table)
+        else:
+            ids = hash_ids(token_ids, E, hash_seed)
         w = gate_weights(None, ids, GATE_HASH, 0)
     else:
         if sel_logits is None:
             L, A = logits(x, wg, dtype, bias)
+            if temperature > 0:
+                g = 0.0 if noise is None else np.asarray(noise, dtype=np.float32).astype(np.float64)
+                L, A = (L + g) / float(np.float32(temperature)), (A + np.abs(g)) / float(np.float32(temperature))
             out["logits"], out["logits_mag"] = L, A
             sel = L
         else:
             sel = np.asarray(sel_logits, dtype=np.float64)
-        ids = select(sel, kind, k)
+        ids = select(sel, kind, k, groups)
         w = gate_weights(sel, ids, kind, normalize)
     slots, counts, demand, slot_src = assign_slots(ids, E, C)
     out.update(ids=ids, weights=w, slots=slots, counts=counts, demand=demand,

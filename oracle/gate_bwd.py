@@ -28,7 +28,7 @@ any evaluation order.
 import numpy as np
 
 from .bf16 import decode, encode
-from .gate import GATE_KTOP1, GATE_TOPK
+from .gate import GATE_HTOPK, GATE_KTOP1, GATE_TOPK
 
 
 def _softmax_rows(L):
@@ -37,7 +37,7 @@ def _softmax_rows(L):
     return e / e.sum(axis=1, keepdims=True)
 
 
-def gate_dlogits(L, ids, dw, kind, normalize):
+def gate_dlogits(L, ids, dw, kind, normalize, temperature=0.0):
     """Gradient of sum_r dw[s, r] * w[s, r] with respect to the logits L[s, e].
 
     L: [S, E] logits (float32 or float64), ids: [S, k] chosen experts, dw: [S, k].
@@ -50,9 +50,18 @@ def gate_dlogits(L, ids, dw, kind, normalize):
                         dL[e] = sum_r dw_r * w_r * ([e == id_r] - p[e]).
     KTOP1             : per group g, w_g = softmax of the group read at id_g,
                         dL[e in g] = dw_g * w_g * ([e == id_g] - p_g[e]).
+    HTOPK             : as TOPK for the chosen experts (R19).
+    With temperature > 0, L are Dense-To-Sparse logits (L_raw + g) / tau (R20)
+    and the gradient returned is the one with respect to L_raw: dL / tau.
 
     Returns (dL, M) as float64 [S, E]; M sums the absolute values of the terms.
     """
+    if temperature:
+        dL, M = gate_dlogits(L, ids, dw, kind, normalize)
+        t = float(np.float32(temperature))
+        return dL / t, M / t
+    if kind == GATE_HTOPK:
+        kind = GATE_TOPK
     L = np.asarray(L, dtype=np.float64)
     ids = np.asarray(ids)
     dw = np.asarray(dw, dtype=np.float64)

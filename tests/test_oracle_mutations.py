@@ -54,6 +54,16 @@ MUTANTS = [
     ("gate_bwd.py", '"dwg": x64.T @ dL', '"dwg": x64.T @ np.abs(dL)', "dW from |dL|"),
     ("gate_bwd.py", "dx = dx + d_in", "dx = dx - d_in", "incoming dx subtracted"),
     ("gate_bwd.py", '"dbias": dL.sum(axis=0)', '"dbias": dL.mean(axis=0)', "bias gradient averaged"),
+    ("gate.py", "            g = best // Gs\n", "            g = best % groups\n", "H Topk group index"),
+    ("gate.py", "order = sorted(range(g * Gs, (g + 1) * Gs), key=lambda e: _key(row, e))",
+     "order = sorted(range(g * Gs, (g + 1) * Gs), key=lambda e: (row[e], e))", "H Topk inner order"),
+    ("gate.py", "v = L if noise is None else (L + np.asarray(noise, dtype=np.float32)).astype(np.float32)",
+     "v = L if noise is None else (L - np.asarray(noise, dtype=np.float32)).astype(np.float32)", "noise subtracted"),
+    ("gate.py", "order = sorted(range(len(freq)), key=lambda t: (-freq[t], t))",
+     "order = sorted(range(len(freq)), key=lambda t: (freq[t], t))", "balanced hash in increasing frequency"),
+    ("gate.py", "e = min(range(E), key=lambda i: (load[i], i))", "e = min(range(E), key=lambda i: (load[i], -i))",
+     "balanced hash ties to the higher expert"),
+    ("gate_bwd.py", "        return dL / t, M / t", "        return dL * t, M * t", "temperature chain rule"),
 ]
 
 
@@ -61,12 +71,13 @@ MUTANTS = [
 def test_pins_catch_mutant(tmp_path, fname, old, new, what):
     shutil.copytree(os.path.join(ROOT, "oracle"), tmp_path / "oracle")
     shutil.copytree(os.path.join(ROOT, "tests", "golden"), tmp_path / "tests" / "golden")
-    for f in ("conftest.py", "test_oracle_pins.py", "test_oracle_gate_bwd_pins.py"):
+    for f in ("conftest.py", "test_oracle_pins.py", "test_oracle_gate_bwd_pins.py", "test_oracle_gate_more_pins.py"):
         shutil.copy(os.path.join(ROOT, "tests", f), tmp_path / "tests" / f)
     path = tmp_path / "oracle" / fname
     src = path.read_text()
     assert old in src, f"mutation site for '{what}' not found"
     path.write_text(src.replace(old, new, 1))
     res = subprocess.run([sys.executable, "-m", "pytest", "-q", "-x", "-p", "no:cacheprovider",
-                          "tests/test_oracle_pins.py", "tests/test_oracle_gate_bwd_pins.py"], cwd=tmp_path, capture_output=True, text=True, timeout=300)
+                          "tests/test_oracle_pins.py", "tests/test_oracle_gate_bwd_pins.py",
+                          "tests/test_oracle_gate_more_pins.py"], cwd=tmp_path, capture_output=True, text=True, timeout=300)
     assert res.returncode != 0, f"pins did not catch: {what}\n{res.stdout[-2000:]}"

@@ -266,7 +266,7 @@ def main():
             if evs is not None:
                 evs[i].record(st)
         mark(0)
-        hm.moe_gate(params, x if learned else None, wg, bias, tok if not learned else None, None, ids, slots,
+        hm.moe_gate(params, x if learned else None, wg, bias, tok if not learned else None, None, None, None, ids, slots,
                     weights, counts, demand, slot_src, ws, st)
         mark(1)
         hm.moe_dispatch(lay, x, ids, slots, slot_src, xe, st)
@@ -329,7 +329,8 @@ def main():
     if learned:
         aux = 0.01 if w["kind"] == hm.MOE_GATE_TOPK else 0.0
         lg = torch.empty((S, E), dtype=torch.float32, device=dev)
-        hm.moe_gate(params, x, wg, bias, None, lg, ids, slots, weights, counts, demand, slot_src, ws, stream)
+        hm.moe_gate(params, x, wg, bias, None, None, None, lg, ids, slots, weights, counts, demand, slot_src, ws,
+                    stream)
         bp = hm.gate_bwd_params(S, d, E, k, w["kind"], w["normalize"], dcode, 1, aux)
         bws = torch.empty((hm.moe_gate_bwd_workspace_size(bp),), dtype=torch.uint8, device=dev)
         dwg_out = torch.empty((d, E), dtype=torch.float32, device=dev)

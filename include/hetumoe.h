@@ -40,7 +40,7 @@
  *            floating-point atomics are used.
  * Range      0 <= S, S*k < 2^31;  1 <= E <= 1024;  0 <= C, E*C < 2^31;  d >= 1.
  *            TOPK: 1 <= k <= min(E, 8).  KTOP1: 1 <= k <= 8 and E % k == 0.
- *            HASH: k == 1.
+ *            HASH: k == 1.  HTOPK: E % groups == 0, 1 <= k <= min(E / groups, 8).
  */
 #ifndef HETUMOE_H
 #define HETUMOE_H
@@ -53,7 +53,7 @@
 extern "C" {
 #endif
 
-#define MOE_ABI_VERSION 3
+#define MOE_ABI_VERSION 4
 
 /* Symbols of the C ABI are the only ones the shared library exports. */
 #define MOE_API __attribute__((visibility("default")))
@@ -72,7 +72,9 @@ typedef enum { MOE_F32 = 0, MOE_BF16 = 1 } moe_dtype;
 typedef enum {
   MOE_GATE_TOPK = 0,  /* Top-k of Eq. 1 (Switch: k=1, GShard: k=2) */
   MOE_GATE_KTOP1 = 1, /* kTop1 / expert prototyping: k contiguous groups of E/k experts, top-1 in each */
-  MOE_GATE_HASH = 2   /* Hash Layer, random hash of the token id; k=1, weight 1 */
+  MOE_GATE_HASH = 2,  /* Hash Layer: SplitMix64 hash of the token id or a lookup table; k=1, weight 1 */
+  MOE_GATE_HTOPK = 3  /* hierarchical top-k (H Topk / SAM): the group holding the best expert, then
+                         the k best experts inside that group */
 } moe_gate_kind;
 
 /* Parameters of moe_gate (host memory). */
@@ -89,8 +91,11 @@ typedef struct {
                          projection is skipped and x, wg, bias must be NULL;
                          0 = logits are computed from x and wg (+ bias) */
   int32_t dtype;      /* moe_dtype of x and wg */
-  int32_t reserved;   /* must be 0 */
+  int32_t groups;     /* HTOPK: number of contiguous expert groups of E / groups; 0 for other kinds */
   uint64_t hash_seed; /* HASH only: seed of the SplitMix64 hash */
+  float temperature;  /* TOPK/KTOP1/HTOPK, Dense-To-Sparse: > 0 makes the gate act on
+                         (L + noise) / temperature; 0 = plain logits (noise must be NULL) */
+  int32_t hash_vocab; /* HASH: length of hash_table (ids are hash_table[token_id]); 0 = SplitMix64 */
 } moe_gate_params;
 
 /* Shape of a dispatch / combine call (host memory). */
@@ -109,12 +114,19 @@ MOE_API moe_status moe_gate_workspace_size(const moe_gate_params* p, size_t* byt
  *
  * Computes, per token s:
  *   logits  L[s,e] = sum_j x[s,j] * wg[j,e] + bias[e]     (x . W of Eq. 1; fp32 accumulation)
+ *           with temperature > 0 (Dense-To-Sparse gate, Sec. 3.1): L = (L + noise[s,e]) / temperature,
+ *           one fp32 addition and one correctly rounded fp32 division; noise (a Gumbel sample,
+ *           drawn by the caller) may be NULL
  *   ids     TOPK : the k experts with the largest logits, best first;
  *           KTOP1: the best expert of each group g, [g*E/k, (g+1)*E/k);
- *           HASH : SplitMix64(hash_seed) output number token_ids[s]+1, mod E.
+ *           HTOPK: with groups of G = E/groups contiguous experts, the group holding the best
+ *                  expert, then the k best experts of that group (Sec. 3.1, H Topk);
+ *           HASH : hash_table[token_ids[s]] when hash_vocab > 0 (Hash Layer balanced
+ *                  assignment, see moe_hash_balanced_table), else SplitMix64(hash_seed) output
+ *                  number token_ids[s]+1, mod E.
  *           Ties go to the lower expert index.
- *   weights TOPK normalize=1: softmax over the k chosen logits (Eq. 1);
- *           TOPK normalize=0: softmax over all E logits at the chosen expert;
+ *   weights TOPK and HTOPK normalize=1: softmax over the k chosen logits (Eq. 1);
+ *           TOPK and HTOPK normalize=0: softmax over all E logits at the chosen expert;
  *           KTOP1: softmax over the chosen expert's group; HASH: 1.
  * then assigns capacity slots in rank-major, token order: all first choices in
  * token order, then all second choices, and so on.  An expert's n-th
@@ -122,10 +134,14 @@ MOE_API moe_status moe_gate_workspace_size(const moe_gate_params* p, size_t* byt
  *
  * Inputs   x [S,d] and wg [d,E] (dtype), bias [E] fp32 or NULL: required when
  *          kind != HASH and logits_in == 0, else NULL.
- *          token_ids [S] int32 >= 0: required for HASH, else NULL.
- *          logits [S,E] fp32: input when logits_in == 1.
+ *          token_ids [S] int32 >= 0: required for HASH, else NULL (with a table, ids must be
+ *          below hash_vocab; larger ids are out of contract and go to expert id mod E).
+ *          noise [S,E] fp32 or NULL: only with temperature > 0.
+ *          hash_table [hash_vocab] int32 in [0, E): HASH with hash_vocab > 0, else NULL.
+ *          logits [S,E] fp32: input when logits_in == 1 (the raw logits; noise and
+ *          temperature are applied to them).
  * Outputs  logits [S,E] fp32 (optional, NULL to skip; when logits_in == 0 the
- *          exact values the selection used), ids [S,k], weights [S,k] fp32,
+ *          exact values the selection used, after noise and temperature), ids [S,k], weights [S,k] fp32,
  *          slots [S,k] (slot in the expert buffer, -1 = dropped), counts [E]
  *          (kept per expert, <= C), demand [E] (routed before the cap; NULL to
  *          skip), slot_src [E,C] (s*k + r of the assignment in each slot, -1 if
@@ -134,10 +150,20 @@ MOE_API moe_status moe_gate_workspace_size(const moe_gate_params* p, size_t* byt
  *          aligned; contents on entry are ignored.
  */
 MOE_API moe_status moe_gate(const moe_gate_params* p, const void* x, const void* wg,
-                    const float* bias, const int32_t* token_ids, float* logits,
-                    int32_t* ids, int32_t* slots, float* weights, int32_t* counts,
-                    int32_t* demand, int32_t* slot_src, void* workspace,
-                    size_t workspace_bytes, hipStream_t stream);
+                    const float* bias, const int32_t* token_ids, const float* noise,
+                    const int32_t* hash_table, float* logits, int32_t* ids, int32_t* slots,
+                    float* weights, int32_t* counts, int32_t* demand, int32_t* slot_src,
+                    void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * moe_hash_balanced_table -- the balanced assignment of the Hash Layer gate
+ * (Sec. 3.1): token ids in order of decreasing frequency (ties: lower id) each
+ * go to the expert with the smallest summed frequency so far (ties: lower
+ * expert).  HOST memory: freq [vocab] (finite, >= 0), table [vocab] output in
+ * [0, E).  Runs on the calling thread, no HIP call; pass the table to moe_gate
+ * (copied to the device by the caller) with hash_vocab = vocab.
+ */
+MOE_API moe_status moe_hash_balanced_table(const double* freq, int32_t vocab, int32_t E, int32_t* table);
 
 /*
  * moe_dispatch -- step 2 of Algorithm 1 (Layout_Transform; Sec. 3.2, layout
@@ -189,12 +215,13 @@ MOE_API moe_status moe_combine_bwd(const moe_layout* l, const void* dy, const vo
 /* Parameters of moe_gate_bwd (host memory). */
 typedef struct {
   int32_t S, d, E, k;    /* as given to moe_gate */
-  int32_t kind;          /* MOE_GATE_TOPK or MOE_GATE_KTOP1 (a hash gate has no gradient) */
+  int32_t kind;          /* MOE_GATE_TOPK, MOE_GATE_KTOP1 or MOE_GATE_HTOPK (a hash gate has no gradient) */
   int32_t normalize;     /* as given to moe_gate */
   int32_t dtype;         /* moe_dtype of x, wg and dx */
   int32_t accumulate_dx; /* 1: dx += the gradient through the gate; 0: dx = that gradient */
-  float aux_coef;        /* coefficient of the load-balancing loss, TOPK only; 0 = no loss */
-  int32_t reserved;      /* must be 0 */
+  float aux_coef;        /* coefficient of the load-balancing loss, TOPK/HTOPK only; 0 = no loss */
+  float temperature;     /* as given to moe_gate: > 0 means `logits` are (L + noise) / temperature
+                            and the gradients are taken with respect to L; 0 = plain logits */
 } moe_gate_bwd_params;
 
 /* Bytes of device workspace moe_gate_bwd needs for `p`.  Fails with
@@ -212,7 +239,9 @@ MOE_API moe_status moe_gate_bwd_workspace_size(const moe_gate_bwd_params* p, siz
  *              TOPK normalize=1: dL[id_r] = w_r (dw_r - sum_r' w_r' dw_r'), 0 elsewhere;
  *              TOPK normalize=0: dL[e] = sum_r dw_r w_r ([e == id_r] - p_e), p = softmax(L[s,:]);
  *              KTOP1: for e in group g, dL[e] = dw_g w_g ([e == id_g] - p_g,e),
- *              p_g = softmax over the group.
+ *              p_g = softmax over the group.  HTOPK as TOPK.
+ *            with temperature > 0, all of the above are taken with respect to the final
+ *              (tempered) logits and then divided by the temperature.
  *            + with aux_coef != 0, the gradient of the load-balancing loss
  *              aux = aux_coef * E * sum_e f_e P_e, where f_e is the share of tokens
  *              whose first choice is e (held constant) and P_e the mean of p_e:

@@ -10,6 +10,7 @@ from .binding import (  # noqa: F401
     MOE_BF16,
     MOE_F32,
     MOE_GATE_HASH,
+    MOE_GATE_HTOPK,
     MOE_GATE_KTOP1,
     MOE_GATE_TOPK,
     MoeError,
@@ -33,4 +34,5 @@ from .binding import (  # noqa: F401
     moe_gate_bwd,
     moe_gate_bwd_workspace_size,
     moe_gate_workspace_size,
+    moe_hash_balanced_table,
 )

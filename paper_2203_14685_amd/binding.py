@@ -18,12 +18,12 @@ LIB_PATH = os.path.join(_PKG, "libhetumoe.so")
 
 MOE_OK, MOE_ERR_INVALID_ARG, MOE_ERR_UNSUPPORTED, MOE_ERR_WORKSPACE, MOE_ERR_HIP = range(5)
 MOE_F32, MOE_BF16 = 0, 1
-MOE_GATE_TOPK, MOE_GATE_KTOP1, MOE_GATE_HASH = 0, 1, 2
+MOE_GATE_TOPK, MOE_GATE_KTOP1, MOE_GATE_HASH, MOE_GATE_HTOPK = 0, 1, 2, 3
 
 EXPORTED = (
     "moe_gate_workspace_size", "moe_gate", "moe_dispatch", "moe_combine",
     "moe_dispatch_bwd", "moe_combine_bwd", "moe_gate_bwd_workspace_size", "moe_gate_bwd",
-    "moe_status_string", "moe_last_error", "moe_abi_version",
+    "moe_hash_balanced_table", "moe_status_string", "moe_last_error", "moe_abi_version",
 )
 
 
@@ -38,8 +38,8 @@ class GateParams(ctypes.Structure):
         ("S", ctypes.c_int32), ("d", ctypes.c_int32), ("E", ctypes.c_int32),
         ("k", ctypes.c_int32), ("capacity", ctypes.c_int32), ("kind", ctypes.c_int32),
         ("normalize", ctypes.c_int32), ("logits_in", ctypes.c_int32),
-        ("dtype", ctypes.c_int32), ("reserved", ctypes.c_int32),
-        ("hash_seed", ctypes.c_uint64),
+        ("dtype", ctypes.c_int32), ("groups", ctypes.c_int32),
+        ("hash_seed", ctypes.c_uint64), ("temperature", ctypes.c_float), ("hash_vocab", ctypes.c_int32),
     ]
 
 
@@ -55,7 +55,7 @@ class GateBwdParams(ctypes.Structure):
         ("S", ctypes.c_int32), ("d", ctypes.c_int32), ("E", ctypes.c_int32),
         ("k", ctypes.c_int32), ("kind", ctypes.c_int32), ("normalize", ctypes.c_int32),
         ("dtype", ctypes.c_int32), ("accumulate_dx", ctypes.c_int32),
-        ("aux_coef", ctypes.c_float), ("reserved", ctypes.c_int32),
+        ("aux_coef", ctypes.c_float), ("temperature", ctypes.c_float),
     ]
 
 
@@ -72,8 +72,9 @@ def load():
     lib = ctypes.CDLL(LIB_PATH)
     vp, i32p, f32p = ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p
     lib.moe_gate_workspace_size.argtypes = [ctypes.POINTER(GateParams), ctypes.POINTER(ctypes.c_size_t)]
-    lib.moe_gate.argtypes = [ctypes.POINTER(GateParams), vp, vp, f32p, i32p, f32p, i32p, i32p, f32p,
-                             i32p, i32p, i32p, vp, ctypes.c_size_t, vp]
+    lib.moe_gate.argtypes = [ctypes.POINTER(GateParams), vp, vp, f32p, i32p, f32p, i32p, f32p, i32p, i32p,
+                             f32p, i32p, i32p, i32p, vp, ctypes.c_size_t, vp]
+    lib.moe_hash_balanced_table.argtypes = [vp, ctypes.c_int32, ctypes.c_int32, vp]
     lib.moe_dispatch.argtypes = [ctypes.POINTER(Layout), vp, i32p, i32p, i32p, vp, vp]
     lib.moe_combine.argtypes = [ctypes.POINTER(Layout), vp, i32p, i32p, f32p, vp, vp]
     lib.moe_dispatch_bwd.argtypes = [ctypes.POINTER(Layout), vp, i32p, i32p, vp, vp]
@@ -82,7 +83,8 @@ def load():
     lib.moe_gate_bwd.argtypes = [ctypes.POINTER(GateBwdParams), vp, vp, f32p, i32p, f32p, f32p, vp, f32p, f32p,
                                  f32p, vp, ctypes.c_size_t, vp]
     for name in ("moe_gate_workspace_size", "moe_gate", "moe_dispatch", "moe_combine",
-                 "moe_dispatch_bwd", "moe_combine_bwd", "moe_gate_bwd_workspace_size", "moe_gate_bwd"):
+                 "moe_dispatch_bwd", "moe_combine_bwd", "moe_gate_bwd_workspace_size", "moe_gate_bwd",
+                 "moe_hash_balanced_table"):
         getattr(lib, name).restype = ctypes.c_int
     lib.moe_status_string.argtypes = [ctypes.c_int]
     lib.moe_status_string.restype = ctypes.c_char_p
@@ -129,8 +131,10 @@ def _stream(stream):
     return getattr(stream, "cuda_stream", stream)
 
 
-def gate_params(S, d, E, k, capacity, kind, normalize=0, logits_in=0, dtype=MOE_F32, hash_seed=0):
-    return GateParams(S, d, E, k, capacity, kind, normalize, logits_in, dtype, 0, hash_seed)
+def gate_params(S, d, E, k, capacity, kind, normalize=0, logits_in=0, dtype=MOE_F32, hash_seed=0, groups=0,
+                temperature=0.0, hash_vocab=0):
+    return GateParams(S, d, E, k, capacity, kind, normalize, logits_in, dtype, groups, hash_seed, temperature,
+                      hash_vocab)
 
 
 def moe_gate_workspace_size(params):
@@ -139,15 +143,16 @@ def moe_gate_workspace_size(params):
     return n.value
 
 
-def moe_gate(params, x, wg, bias, token_ids, logits, ids, slots, weights, counts, demand, slot_src,
-             workspace, stream=None):
+def moe_gate(params, x, wg, bias, token_ids, noise, hash_table, logits, ids, slots, weights, counts, demand,
+             slot_src, workspace, stream=None):
     lib = load()
     f32, i32 = torch.float32, torch.int32
     xdt = torch.bfloat16 if params.dtype == MOE_BF16 else torch.float32
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(lib.moe_gate(
         ctypes.byref(params), _ptr(x, xdt, "x"), _ptr(wg, xdt, "wg"), _ptr(bias, f32, "bias"),
-        _ptr(token_ids, i32, "token_ids"), _ptr(logits, f32, "logits"), _ptr(ids, i32, "ids"),
+        _ptr(token_ids, i32, "token_ids"), _ptr(noise, f32, "noise"), _ptr(hash_table, i32, "hash_table"),
+        _ptr(logits, f32, "logits"), _ptr(ids, i32, "ids"),
         _ptr(slots, i32, "slots"), _ptr(weights, f32, "weights"), _ptr(counts, i32, "counts"),
         _ptr(demand, i32, "demand"), _ptr(slot_src, i32, "slot_src"), _ptr(workspace, None, "workspace"),
         ws_bytes, _stream(stream)))
@@ -190,7 +195,7 @@ def moe_combine_bwd(layout, dy, ye, ids, slots, slot_src, weights, dye, dw, stre
 
 def gate(kind, k, E, capacity, *, x=None, wg=None, bias=None, token_ids=None, logits=None,
          logits_in=False, normalize=0, hash_seed=0, want_logits=False, want_demand=True, dtype=None,
-         stream=None):
+         groups=0, noise=None, temperature=0.0, hash_table=None, stream=None):
     """Allocate the outputs and run moe_gate; returns a dict of device tensors."""
     if kind == MOE_GATE_HASH:
         S, d = int(token_ids.shape[0]), 0
@@ -203,7 +208,9 @@ def gate(kind, k, E, capacity, *, x=None, wg=None, bias=None, token_ids=None, lo
         dcode = _dtype_code(x)
     ref = logits if logits is not None else (x if x is not None else token_ids)
     dev = ref.device
-    params = gate_params(S, d, E, k, capacity, kind, normalize, int(bool(logits_in)), dcode, hash_seed)
+    vocab = 0 if hash_table is None else int(hash_table.shape[0])
+    params = gate_params(S, d, E, k, capacity, kind, normalize, int(bool(logits_in)), dcode, hash_seed, groups,
+                         temperature, vocab)
     out = {
         "ids": torch.empty((S, k), dtype=torch.int32, device=dev),
         "slots": torch.empty((S, k), dtype=torch.int32, device=dev),
@@ -218,9 +225,19 @@ def gate(kind, k, E, capacity, *, x=None, wg=None, bias=None, token_ids=None, lo
         logits = None
     out["logits"] = logits
     ws = torch.empty((moe_gate_workspace_size(params),), dtype=torch.uint8, device=dev)
-    moe_gate(params, x, wg, bias, token_ids, logits, out["ids"], out["slots"], out["weights"],
+    moe_gate(params, x, wg, bias, token_ids, noise, hash_table, logits, out["ids"], out["slots"], out["weights"],
              out["counts"], out["demand"], out["slot_src"], ws, stream)
     return out
+
+
+def moe_hash_balanced_table(freq, E):
+    """Balanced token -> expert table of the Hash Layer gate, built on the host by
+    the library (freq: host array of token frequencies).  Returns an int32 numpy array."""
+    import numpy as np
+    f = np.ascontiguousarray(freq, dtype=np.float64)
+    table = np.empty(f.shape[0], dtype=np.int32)
+    _check(load().moe_hash_balanced_table(f.ctypes.data, int(f.shape[0]), int(E), table.ctypes.data))
+    return table
 
 
 def dispatch(x, ids, slots, slot_src, stream=None):
@@ -259,8 +276,8 @@ def combine_bwd(dy, ids, slots, slot_src, weights, ye=None, want_dw=True, stream
     return dye, dw
 
 
-def gate_bwd_params(S, d, E, k, kind, normalize=0, dtype=MOE_F32, accumulate_dx=0, aux_coef=0.0):
-    return GateBwdParams(S, d, E, k, kind, normalize, dtype, accumulate_dx, aux_coef, 0)
+def gate_bwd_params(S, d, E, k, kind, normalize=0, dtype=MOE_F32, accumulate_dx=0, aux_coef=0.0, temperature=0.0):
+    return GateBwdParams(S, d, E, k, kind, normalize, dtype, accumulate_dx, aux_coef, temperature)
 
 
 def moe_gate_bwd_workspace_size(params):
@@ -281,7 +298,8 @@ def moe_gate_bwd(params, x, wg, logits, ids, dw, dlogits, dx, dwg, dbias, aux_lo
 
 
 def gate_bwd(kind, logits, ids, dw, *, x=None, wg=None, normalize=0, dx=None, accumulate_dx=False,
-             want_dlogits=True, want_dwg=True, want_dbias=True, want_dx=True, aux_coef=0.0, stream=None):
+             want_dlogits=True, want_dwg=True, want_dbias=True, want_dx=True, aux_coef=0.0, temperature=0.0,
+             stream=None):
     """Allocating wrapper of moe_gate_bwd.  Returns a dict with dlogits, dwg,
     dbias, dx and aux_loss (None where not requested).  With accumulate_dx the
     given dx is updated in place and returned."""
@@ -292,7 +310,7 @@ def gate_bwd(kind, logits, ids, dw, *, x=None, wg=None, normalize=0, dx=None, ac
     dt = torch.float32 if src is None else src.dtype
     d = x.shape[1] if x is not None else (wg.shape[0] if wg is not None else 1)
     params = gate_bwd_params(S, d, E, k, kind, normalize, MOE_BF16 if dt == torch.bfloat16 else MOE_F32,
-                             1 if accumulate_dx else 0, aux_coef)
+                             1 if accumulate_dx else 0, aux_coef, temperature)
     f32 = torch.float32
     out = {
         "dlogits": torch.empty((S, E), dtype=f32, device=dev) if want_dlogits else None,

@@ -4,6 +4,10 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
+#include <cmath>
+#include <vector>
+
 #include "hetumoe.h"
 #include "common.hpp"
 #include "kernels.hpp"
@@ -42,9 +46,13 @@ int64_t hist_blocks(int64_t S) { return (S + kTokensPerHistBlock - 1) / kTokensP
 // Checks shared by moe_gate and moe_gate_workspace_size.
 moe_status check_gate_params(const moe_gate_params* p) {
   if (!p) return fail(MOE_ERR_INVALID_ARG, "params is NULL");
-  if (p->reserved != 0) return fail(MOE_ERR_INVALID_ARG, "reserved must be 0");
   if (p->dtype != MOE_F32 && p->dtype != MOE_BF16) return fail(MOE_ERR_INVALID_ARG, "dtype %d unknown", p->dtype);
-  if (p->kind < MOE_GATE_TOPK || p->kind > MOE_GATE_HASH) return fail(MOE_ERR_INVALID_ARG, "gate kind %d unknown", p->kind);
+  if (p->kind < MOE_GATE_TOPK || p->kind > MOE_GATE_HTOPK) return fail(MOE_ERR_INVALID_ARG, "gate kind %d unknown", p->kind);
+  if (!std::isfinite(p->temperature) || p->temperature < 0.f)
+    return fail(MOE_ERR_INVALID_ARG, "temperature must be finite and >= 0");
+  if (p->hash_vocab < 0) return fail(MOE_ERR_INVALID_ARG, "hash_vocab = %d < 0", p->hash_vocab);
+  if (p->kind != MOE_GATE_HASH && p->hash_vocab != 0) return fail(MOE_ERR_INVALID_ARG, "hash_vocab is for HASH only");
+  if (p->kind != MOE_GATE_HTOPK && p->groups != 0) return fail(MOE_ERR_INVALID_ARG, "groups is for HTOPK only");
   if (p->S < 0) return fail(MOE_ERR_INVALID_ARG, "S = %d < 0", p->S);
   if (p->E < 1 || p->E > 1024) return fail(MOE_ERR_INVALID_ARG, "E = %d outside [1, 1024]", p->E);
   if (p->capacity < 0) return fail(MOE_ERR_INVALID_ARG, "capacity = %d < 0", p->capacity);
@@ -58,9 +66,16 @@ moe_status check_gate_params(const moe_gate_params* p) {
     case MOE_GATE_KTOP1:
       if (p->k < 1 || p->k > 8 || p->E % p->k != 0) return fail(MOE_ERR_INVALID_ARG, "KTOP1 needs 1 <= k <= 8 and E %% k == 0, got k = %d, E = %d", p->k, p->E);
       break;
+    case MOE_GATE_HTOPK:
+      if (p->groups < 1 || p->E % p->groups != 0)
+        return fail(MOE_ERR_INVALID_ARG, "HTOPK needs groups >= 1 dividing E, got groups = %d, E = %d", p->groups, p->E);
+      if (p->k < 1 || p->k > 8 || p->k > p->E / p->groups)
+        return fail(MOE_ERR_INVALID_ARG, "HTOPK needs 1 <= k <= min(E / groups, 8), got k = %d", p->k);
+      break;
     default:
       if (p->k != 1) return fail(MOE_ERR_INVALID_ARG, "HASH needs k = 1, got %d", p->k);
       if (p->logits_in) return fail(MOE_ERR_INVALID_ARG, "HASH takes no logits");
+      if (p->temperature != 0.f) return fail(MOE_ERR_INVALID_ARG, "HASH takes no temperature");
       break;
   }
   if (static_cast<int64_t>(p->S) * p->k > kI32Max) return fail(MOE_ERR_INVALID_ARG, "S * k >= 2^31");
@@ -74,10 +89,23 @@ moe_status check_gate_params(const moe_gate_params* p) {
   return MOE_OK;
 }
 
-// Workspace: the histogram, int32 [k, E, ceil(S/64)].
-size_t gate_workspace_bytes(const moe_gate_params* p) {
+// Gates whose selection runs on final logits in a kernel of its own: the
+// hierarchical top-k, and any gate with a temperature (Dense-To-Sparse).
+bool gate_extended(const moe_gate_params* p) {
+  return p->kind != MOE_GATE_HASH && (p->kind == MOE_GATE_HTOPK || p->temperature > 0.f);
+}
+
+// Workspace: the histogram, int32 [k, E, ceil(S/64)]; for the extended gates
+// also a logits buffer, fp32 [S, E], 256-byte aligned after the histogram.
+size_t gate_hist_bytes(const moe_gate_params* p) {
   const size_t n = static_cast<size_t>(p->k) * static_cast<size_t>(hist_blocks(p->S)) * static_cast<size_t>(p->E);
   return n * sizeof(int32_t);
+}
+
+size_t gate_workspace_bytes(const moe_gate_params* p) {
+  const size_t h = gate_hist_bytes(p);
+  if (!gate_extended(p)) return h;
+  return ((h + 255) & ~static_cast<size_t>(255)) + static_cast<size_t>(p->S) * static_cast<size_t>(p->E) * 4;
 }
 
 moe_status check_layout(const moe_layout* l, const char* who) {
@@ -106,24 +134,26 @@ moe_status need(const void* p, int64_t n, size_t align, const char* who, const c
 // Checks shared by moe_gate_bwd and moe_gate_bwd_workspace_size.
 moe_status check_gate_bwd_params(const moe_gate_bwd_params* p) {
   if (!p) return fail(MOE_ERR_INVALID_ARG, "params is NULL");
-  if (p->reserved != 0) return fail(MOE_ERR_INVALID_ARG, "reserved must be 0");
   if (p->dtype != MOE_F32 && p->dtype != MOE_BF16) return fail(MOE_ERR_INVALID_ARG, "dtype %d unknown", p->dtype);
   if (p->kind == MOE_GATE_HASH) return fail(MOE_ERR_INVALID_ARG, "a hash gate has no logits and no gradient");
-  if (p->kind != MOE_GATE_TOPK && p->kind != MOE_GATE_KTOP1) return fail(MOE_ERR_INVALID_ARG, "gate kind %d unknown", p->kind);
+  if (p->kind != MOE_GATE_TOPK && p->kind != MOE_GATE_KTOP1 && p->kind != MOE_GATE_HTOPK)
+    return fail(MOE_ERR_INVALID_ARG, "gate kind %d unknown", p->kind);
+  if (!std::isfinite(p->temperature) || p->temperature < 0.f)
+    return fail(MOE_ERR_INVALID_ARG, "temperature must be finite and >= 0");
   if (p->S < 0) return fail(MOE_ERR_INVALID_ARG, "S = %d < 0", p->S);
   if (p->d < 1) return fail(MOE_ERR_INVALID_ARG, "d = %d < 1", p->d);
   if (p->E < 1 || p->E > 1024) return fail(MOE_ERR_INVALID_ARG, "E = %d outside [1, 1024]", p->E);
   if (p->normalize != 0 && p->normalize != 1) return fail(MOE_ERR_INVALID_ARG, "normalize must be 0 or 1");
   if (p->accumulate_dx != 0 && p->accumulate_dx != 1) return fail(MOE_ERR_INVALID_ARG, "accumulate_dx must be 0 or 1");
-  if (p->kind == MOE_GATE_TOPK && (p->k < 1 || p->k > 8 || p->k > p->E))
+  if (p->kind != MOE_GATE_KTOP1 && (p->k < 1 || p->k > 8 || p->k > p->E))
     return fail(MOE_ERR_INVALID_ARG, "TOPK needs 1 <= k <= min(E, 8), got k = %d, E = %d", p->k, p->E);
   if (p->kind == MOE_GATE_KTOP1 && (p->k < 1 || p->k > 8 || p->E % p->k != 0))
     return fail(MOE_ERR_INVALID_ARG, "KTOP1 needs 1 <= k <= 8 and E %% k == 0, got k = %d, E = %d", p->k, p->E);
   if (static_cast<int64_t>(p->S) * p->k > kI32Max) return fail(MOE_ERR_INVALID_ARG, "S * k >= 2^31");
   if (!(p->aux_coef == p->aux_coef) || p->aux_coef > 3.0e38f || p->aux_coef < -3.0e38f)
     return fail(MOE_ERR_INVALID_ARG, "aux_coef must be finite");
-  if (p->aux_coef != 0.f && p->kind != MOE_GATE_TOPK)
-    return fail(MOE_ERR_INVALID_ARG, "the load-balancing loss is defined for TOPK gates only");
+  if (p->aux_coef != 0.f && p->kind == MOE_GATE_KTOP1)
+    return fail(MOE_ERR_INVALID_ARG, "the load-balancing loss is defined for TOPK and HTOPK gates only");
   return MOE_OK;
 }
 
@@ -232,7 +262,7 @@ moe_status moe_gate_bwd(const moe_gate_bwd_params* p, const void* x, const void*
   GateBwdArgs a{};
   a.S = p->S; a.d = p->d; a.E = p->E; a.k = p->k; a.nb = g.nb;
   a.kind = p->kind; a.normalize = p->normalize; a.dtype = p->dtype; a.accumulate = p->accumulate_dx;
-  a.aux_coef = p->aux_coef; a.nsplit = g.nsplit; a.split_tokens = g.split_tokens;
+  a.aux_coef = p->aux_coef; a.temperature = p->temperature; a.nsplit = g.nsplit; a.split_tokens = g.split_tokens;
   a.mfma_dw = (g.mfma && dwg) ? 1 : 0;
   // the matrix-core dx reads W rows and dL with 16-byte loads
   a.mfma_dx = (g.mfma && dx && aligned(wg, 16) && (!dlogits || aligned(dlogits, 16))) ? 1 : 0;
@@ -280,25 +310,32 @@ moe_status moe_gate_workspace_size(const moe_gate_params* p, size_t* bytes) {
 }
 
 moe_status moe_gate(const moe_gate_params* p, const void* x, const void* wg, const float* bias,
-                    const int32_t* token_ids, float* logits, int32_t* ids, int32_t* slots,
-                    float* weights, int32_t* counts, int32_t* demand, int32_t* slot_src,
-                    void* workspace, size_t workspace_bytes, hipStream_t stream) {
+                    const int32_t* token_ids, const float* noise, const int32_t* hash_table, float* logits,
+                    int32_t* ids, int32_t* slots, float* weights, int32_t* counts, int32_t* demand,
+                    int32_t* slot_src, void* workspace, size_t workspace_bytes, hipStream_t stream) {
   static const char* who = "moe_gate";
   CHECK(check_gate_params(p));
   const int64_t S = p->S, E = p->E, k = p->k, C = p->capacity;
   const size_t elt = elt_size(p->dtype);
   if (p->kind == MOE_GATE_HASH) {
     CHECK(need(token_ids, S, 4, who, "token_ids"));
-    if (x || wg || bias || logits) return fail(MOE_ERR_INVALID_ARG, "%s: HASH takes no x, wg, bias or logits", who);
-  } else if (p->logits_in) {
-    CHECK(need(logits, S * E, 4, who, "logits"));
-    if (x || wg || bias || token_ids) return fail(MOE_ERR_INVALID_ARG, "%s: with logits_in, x, wg, bias and token_ids must be NULL", who);
+    if (x || wg || bias || logits || noise) return fail(MOE_ERR_INVALID_ARG, "%s: HASH takes no x, wg, bias, logits or noise", who);
+    if (p->hash_vocab > 0) CHECK(need(hash_table, p->hash_vocab, 4, who, "hash_table"));
+    else if (hash_table) return fail(MOE_ERR_INVALID_ARG, "%s: hash_table needs hash_vocab > 0", who);
   } else {
-    CHECK(need(x, S * p->d, 16, who, "x"));
-    CHECK(need(wg, static_cast<int64_t>(p->d) * E, elt, who, "wg"));
-    CHECK(need(bias, 0, 4, who, "bias"));
-    CHECK(need(logits, 0, 4, who, "logits"));
-    if (token_ids) return fail(MOE_ERR_INVALID_ARG, "%s: token_ids is only for HASH", who);
+    if (hash_table) return fail(MOE_ERR_INVALID_ARG, "%s: hash_table is only for HASH", who);
+    if (noise && p->temperature == 0.f) return fail(MOE_ERR_INVALID_ARG, "%s: noise needs a temperature > 0", who);
+    CHECK(need(noise, 0, 4, who, "noise"));
+    if (p->logits_in) {
+      CHECK(need(logits, S * E, 4, who, "logits"));
+      if (x || wg || bias || token_ids) return fail(MOE_ERR_INVALID_ARG, "%s: with logits_in, x, wg, bias and token_ids must be NULL", who);
+    } else {
+      CHECK(need(x, S * p->d, 16, who, "x"));
+      CHECK(need(wg, static_cast<int64_t>(p->d) * E, elt, who, "wg"));
+      CHECK(need(bias, 0, 4, who, "bias"));
+      CHECK(need(logits, 0, 4, who, "logits"));
+      if (token_ids) return fail(MOE_ERR_INVALID_ARG, "%s: token_ids is only for HASH", who);
+    }
   }
   CHECK(need(ids, S * k, 4, who, "ids"));
   CHECK(need(slots, S * k, 4, who, "slots"));
@@ -313,15 +350,45 @@ moe_status moe_gate(const moe_gate_params* p, const void* x, const void* wg, con
 
   const int nb = static_cast<int>(hist_blocks(S));
   int32_t* hist = static_cast<int32_t*>(workspace);
+  hipError_t err;
 
-  RouteArgs ra{};
-  ra.S = p->S; ra.d = p->d; ra.E = p->E; ra.k = p->k; ra.nb = nb;
-  ra.kind = p->kind; ra.normalize = p->normalize; ra.logits_in = p->logits_in; ra.dtype = p->dtype;
-  ra.hash_seed = p->hash_seed;
-  ra.x = x; ra.wg = wg; ra.bias = bias; ra.token_ids = token_ids; ra.logits = logits;
-  ra.ids = ids; ra.weights = weights; ra.hist = hist;
-  hipError_t err = launch_route(ra, stream);
-  if (err != hipSuccess) return hip_fail(err, "moe_gate: route kernel launch");
+  if (gate_extended(p)) {
+    // raw logits (projected into the workspace, or given), then noise,
+    // temperature and selection in a kernel of their own
+    float* wsl = reinterpret_cast<float*>(static_cast<char*>(workspace) +
+                                          ((gate_hist_bytes(p) + 255) & ~static_cast<size_t>(255)));
+    const float* raw = logits;
+    float* fin = wsl;
+    if (!p->logits_in) {
+      // projection only: a one-choice top-k pass writes the logits; its ids,
+      // weights and histogram are overwritten below
+      RouteArgs ra{};
+      ra.S = p->S; ra.d = p->d; ra.E = p->E; ra.k = 1; ra.nb = nb;
+      ra.kind = MOE_GATE_TOPK; ra.normalize = 0; ra.logits_in = 0; ra.dtype = p->dtype;
+      ra.x = x; ra.wg = wg; ra.bias = bias; ra.logits = wsl;
+      ra.ids = ids; ra.weights = weights; ra.hist = hist;
+      err = launch_route(ra, stream);
+      if (err != hipSuccess) return hip_fail(err, "moe_gate: route kernel launch");
+      raw = wsl;
+      fin = logits ? logits : wsl;
+    }
+    SelectArgs sel{};
+    sel.S = p->S; sel.E = p->E; sel.k = p->k; sel.nb = nb; sel.kind = p->kind; sel.normalize = p->normalize;
+    sel.groups = p->groups; sel.temperature = p->temperature;
+    sel.raw = raw; sel.noise = noise; sel.fin = fin; sel.ids = ids; sel.weights = weights; sel.hist = hist;
+    err = launch_select_ext(sel, stream);
+    if (err != hipSuccess) return hip_fail(err, "moe_gate: selection kernel launch");
+  } else {
+    RouteArgs ra{};
+    ra.S = p->S; ra.d = p->d; ra.E = p->E; ra.k = p->k; ra.nb = nb;
+    ra.kind = p->kind; ra.normalize = p->normalize; ra.logits_in = p->logits_in; ra.dtype = p->dtype;
+    ra.hash_seed = p->hash_seed;
+    ra.x = x; ra.wg = wg; ra.bias = bias; ra.token_ids = token_ids; ra.logits = logits;
+    ra.hash_table = hash_table; ra.hash_vocab = p->hash_vocab;
+    ra.ids = ids; ra.weights = weights; ra.hist = hist;
+    err = launch_route(ra, stream);
+    if (err != hipSuccess) return hip_fail(err, "moe_gate: route kernel launch");
+  }
 
   ScanArgs sa{};
   sa.E = p->E; sa.k = p->k; sa.nb = nb; sa.C = p->capacity;
@@ -334,6 +401,28 @@ moe_status moe_gate(const moe_gate_params* p, const void* x, const void* wg, con
   aa.ids = ids; aa.offs = hist; aa.slots = slots; aa.slot_src = slot_src;
   err = launch_assign(aa, stream);
   if (err != hipSuccess) return hip_fail(err, "moe_gate: assign kernel launch");
+  return ok();
+}
+
+moe_status moe_hash_balanced_table(const double* freq, int32_t vocab, int32_t E, int32_t* table) {
+  if (!freq || !table) return fail(MOE_ERR_INVALID_ARG, "moe_hash_balanced_table: freq and table are required");
+  if (vocab < 1) return fail(MOE_ERR_INVALID_ARG, "moe_hash_balanced_table: vocab = %d < 1", vocab);
+  if (E < 1 || E > 1024) return fail(MOE_ERR_INVALID_ARG, "moe_hash_balanced_table: E = %d outside [1, 1024]", E);
+  for (int32_t t = 0; t < vocab; ++t)
+    if (!std::isfinite(freq[t]) || freq[t] < 0.0)
+      return fail(MOE_ERR_INVALID_ARG, "moe_hash_balanced_table: freq[%d] is not a finite value >= 0", t);
+  std::vector<int32_t> order(static_cast<size_t>(vocab));
+  for (int32_t t = 0; t < vocab; ++t) order[t] = t;
+  // decreasing frequency; the stable sort keeps equal frequencies in id order
+  std::stable_sort(order.begin(), order.end(), [freq](int32_t a, int32_t b) { return freq[a] > freq[b]; });
+  std::vector<double> load(static_cast<size_t>(E), 0.0);
+  for (int32_t t : order) {
+    int32_t best = 0;
+    for (int32_t e = 1; e < E; ++e)
+      if (load[e] < load[best]) best = e;  // strict: ties keep the lower expert
+    table[t] = best;
+    load[best] += freq[t];
+  }
   return ok();
 }
 

@@ -44,12 +44,92 @@ __global__ __launch_bounds__(kBlock) void route_hash_kernel(RouteArgs a) {
   const int64_t s = static_cast<int64_t>(blockIdx.x) * kBlock + tid;
   const bool valid = s < a.S;
   if (valid) {
-    const uint64_t t = static_cast<uint64_t>(static_cast<int64_t>(a.token_ids[s]));
-    a.ids[s] = static_cast<int>(splitmix64_output(a.hash_seed, t + 1ull) % static_cast<uint64_t>(a.E));
+    const int32_t tid32 = a.token_ids[s];
+    int e;
+    if (a.hash_table) {
+      // table lookup (balanced assignment); ids outside the table or table
+      // entries outside [0, E) are out of contract and fold into [0, E)
+      const int32_t v = (tid32 >= 0 && tid32 < a.hash_vocab) ? a.hash_table[tid32] : tid32;
+      e = ((v % a.E) + a.E) % a.E;
+    } else {
+      const uint64_t t = static_cast<uint64_t>(static_cast<int64_t>(tid32));
+      e = static_cast<int>(splitmix64_output(a.hash_seed, t + 1ull) % static_cast<uint64_t>(a.E));
+    }
+    a.ids[s] = e;
     a.weights[s] = 1.f;
   }
   const int wb = blockIdx.x * kWavesPerBlock + w;
   wave_block_hist(hist_lds + w * a.E, wb < a.nb, s, valid, wb, a);
+}
+
+// ---------------------------------------------------------------- selection on final logits
+// One block per 64-token wave block, P lanes per token.  Each lane turns its
+// slice of the raw logits into final logits ((raw + noise) / temperature, or
+// raw) and stores them; after a block barrier the P lanes select on the stored
+// row.
+template <int P, int KMAX, int MODE>  // MODE: 0 top-k, 1 kTop1, 3 hierarchical top-k
+__global__ __launch_bounds__(kWave * P) void select_ext_kernel(SelectArgs a) {
+  extern __shared__ int hist_lds[];  // [k][E]
+  const int t = threadIdx.x / P, j = threadIdx.x % P;
+  const int64_t s = static_cast<int64_t>(blockIdx.x) * kWave + t;
+  const bool valid = s < a.S;
+  const int E = a.E;
+  for (int i = threadIdx.x; i < a.k * E; i += kWave * P) hist_lds[i] = 0;
+  const int slice = E / P;
+  const int64_t row = (valid ? s : 0) * E;
+  if (valid) {
+    for (int e = j * slice; e < (j + 1) * slice; ++e) {
+      float v = a.raw[row + e];
+      if (a.temperature > 0.f) {
+        if (a.noise) v = v + a.noise[row + e];
+        v = v / a.temperature;
+      }
+      a.fin[row + e] = v;
+    }
+  }
+  __syncthreads();
+  // invalid tokens select on row 0 (their results are not written)
+  const float* lrow = a.fin + row;
+  if constexpr (MODE == 3) {
+    select_token_htopk<P, KMAX>(lrow, E, a.k, E / a.groups, a.normalize, j, valid, a.ids + s * a.k,
+                                a.weights + s * a.k, hist_lds);
+  } else {
+    select_token<P, KMAX, MODE == 1>(lrow, E, a.k, a.normalize, j, valid, a.ids + s * a.k, a.weights + s * a.k,
+                                     hist_lds);
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < a.k * E; i += kWave * P)
+    a.hist[static_cast<int64_t>(i) * a.nb + blockIdx.x] = hist_lds[i];
+}
+
+template <int P, int KMAX, int MODE>
+static hipError_t launch_sel_t(const SelectArgs& a, hipStream_t st) {
+  select_ext_kernel<P, KMAX, MODE>
+      <<<dim3(static_cast<unsigned>(a.nb)), dim3(kWave * P), static_cast<size_t>(a.k) * a.E * sizeof(int), st>>>(a);
+  return hipGetLastError();
+}
+
+template <int P, int MODE>
+static hipError_t launch_sel_m(const SelectArgs& a, hipStream_t st) {
+  if (MODE == 1 || a.k == 1) return launch_sel_t<P, 1, MODE>(a, st);
+  if (a.k == 2) return launch_sel_t<P, 2, MODE>(a, st);
+  if (a.k <= 4) return launch_sel_t<P, 4, MODE>(a, st);
+  return launch_sel_t<P, 8, MODE>(a, st);
+}
+
+template <int P>
+static hipError_t launch_sel_p(const SelectArgs& a, hipStream_t st) {
+  if (a.kind == 1) return launch_sel_m<P, 1>(a, st);
+  if (a.kind == 3) return launch_sel_m<P, 3>(a, st);
+  return launch_sel_m<P, 0>(a, st);
+}
+
+hipError_t launch_select_ext(const SelectArgs& a, hipStream_t st) {
+  if (a.nb == 0) return hipSuccess;
+  // 4 lanes per token when they split the experts evenly (and, for kTop1,
+  // agree with the groups), else one
+  const bool four = a.E % 4 == 0 && (a.kind != 1 || 4 % a.k == 0 || a.k % 4 == 0);
+  return four ? launch_sel_p<4>(a, st) : launch_sel_p<1>(a, st);
 }
 
 // ---------------------------------------------------------------- scan kernel

@@ -129,7 +129,8 @@ __global__ __launch_bounds__(WAVES * kWave) void gate_dl_kernel(GateBwdArgs a) {
   const int64_t wb = blockIdx.x;
   const int E = a.E, k = a.k;
   const bool aux = a.aux_coef != 0.f;
-  const bool full_softmax = a.kind == 0 && (a.normalize == 0 || aux);
+  const bool topk = a.kind != 1;  // top-k and hierarchical top-k share the weights
+  const bool full_softmax = topk && (a.normalize == 0 || aux);
   const float inv_s = a.S > 0 ? 1.f / static_cast<float>(a.S) : 0.f;
   const float c_aux = a.aux_coef * static_cast<float>(E) * inv_s;
   float f[EPL], psum[EPL], bsum[EPL];
@@ -184,7 +185,7 @@ __global__ __launch_bounds__(WAVES * kWave) void gate_dl_kernel(GateBwdArgs a) {
 #pragma unroll
       for (int i = 0; i < EPL; ++i) p[i] = expf(v[i] - m) / se;
     }
-    if (a.kind == 0 && a.normalize) {
+    if (topk && a.normalize) {
       // softmax over the k chosen logits
       float m2 = -INFINITY;
 #pragma unroll
@@ -209,7 +210,7 @@ __global__ __launch_bounds__(WAVES * kWave) void gate_dl_kernel(GateBwdArgs a) {
         for (int i = 0; i < EPL; ++i)
           if (j + P * i == idr[r]) dl[i] += gr;
       }
-    } else if (a.kind == 0) {
+    } else if (topk) {
       // full softmax read at each chosen expert
       float gsum = 0.f;
 #pragma unroll
@@ -266,6 +267,11 @@ __global__ __launch_bounds__(WAVES * kWave) void gate_dl_kernel(GateBwdArgs a) {
         dl[i] += c_aux * p[i] * (f[i] - fp);
         if (valid) psum[i] += p[i];
       }
+    }
+    if (a.temperature > 0.f) {
+      // the logits were (L + noise) / temperature: chain rule to L
+#pragma unroll
+      for (int i = 0; i < EPL; ++i) dl[i] = dl[i] / a.temperature;
     }
 #pragma unroll
     for (int i = 0; i < EPL; ++i) {

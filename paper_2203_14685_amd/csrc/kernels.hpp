@@ -14,6 +14,8 @@ struct RouteArgs {
   const void* wg;           // [d, E]
   const float* bias;        // [E] or null
   const int32_t* token_ids; // [S] (hash)
+  const int32_t* hash_table; // [hash_vocab] (hash with a table) or null
+  int hash_vocab;
   float* logits;            // [S, E]: input (logits_in), output, or null
   int32_t* ids;             // [S, k]
   float* weights;           // [S, k]
@@ -51,6 +53,20 @@ struct RowArgs {
 };
 
 hipError_t launch_route(const RouteArgs& a, hipStream_t st);
+
+// Selection on logits that first take noise and a temperature (Dense-To-Sparse)
+// and/or the hierarchical top-k: one block per 64-token wave block.
+struct SelectArgs {
+  int S, E, k, nb, kind, normalize, groups;
+  float temperature;       // > 0: fin = (raw + noise) / temperature; 0: fin = raw
+  const float* raw;        // [S, E] logits as projected (or given)
+  const float* noise;      // [S, E] or null
+  float* fin;              // [S, E] logits the selection uses (may be raw itself)
+  int32_t* ids;            // [S, k]
+  float* weights;          // [S, k]
+  int32_t* hist;           // [k, E, nb]
+};
+hipError_t launch_select_ext(const SelectArgs& a, hipStream_t st);
 hipError_t launch_route_valu_f32(const RouteArgs& a, hipStream_t st);
 hipError_t launch_route_valu_bf16(const RouteArgs& a, hipStream_t st);
 hipError_t launch_route_mfma(const RouteArgs& a, hipStream_t st);
@@ -73,6 +89,7 @@ struct GateBwdArgs {
   int S, d, E, k, nb;       // nb: 64-token wave blocks
   int kind, normalize, dtype, accumulate;
   float aux_coef;
+  float temperature;        // > 0: the logits are (L + noise) / temperature; gradients w.r.t. L
   int nsplit, split_tokens; // dW is summed over tokens in nsplit ranges of split_tokens (a multiple of 64)
   int mfma_dw, mfma_dx;     // matrix-core paths (bf16, E a multiple of 16 up to 128, d a multiple of 64)
   int64_t s_pad;            // row length of dlt: S rounded up to 64

@@ -223,6 +223,41 @@ __device__ __forceinline__ void select_token(const float* lrow, int E, int k, in
 // Every wave of the block calls this (it synchronises the block); `active` waves
 // own a wave block, `s` is the calling lane's token.  The ids are read back from
 // global memory, where the same thread wrote them.
+// Hierarchical top-k for one token by P consecutive lanes (Sec. 3.1, H Topk):
+// the best expert over all E (with the full softmax sum), its group of Gs
+// contiguous experts, then the k best experts of that group.  Weights: softmax
+// over the k chosen (normalize) or the full softmax at each of them.
+template <int P, int KMAX>
+__device__ __forceinline__ void select_token_htopk(const float* lrow, int E, int k, int Gs, int normalize, int j,
+                                                   bool valid, int32_t* ids, float* weights, int* hist_lds) {
+  const int slice = E / P;
+  const int e0 = j * slice;
+  TopkState<1> t1;
+  t1.init();
+  for (int e = 0; e < slice; ++e) t1.push(lrow[e0 + e], e0 + e);
+#pragma unroll
+  for (int msk = 1; msk < P; msk <<= 1) t1.merge_xor(msk);
+  const int best = t1.ti[0] == kEmpty ? 0 : t1.ti[0];
+  const int lo = (best / Gs) * Gs, hi = lo + Gs;
+  TopkState<KMAX> tk;
+  tk.init();
+  for (int e = 0; e < slice; ++e) {
+    const int ee = e0 + e;
+    if (ee >= lo && ee < hi) tk.insert(lrow[ee], ee);
+  }
+#pragma unroll
+  for (int msk = 1; msk < P; msk <<= 1) tk.merge_xor(msk);
+  // the group holds the overall best: the full softmax sum relative to it
+  tk.m = t1.m;
+  tk.ssum = t1.ssum;
+  if (valid && j == 0) {
+    tk.finish(k, normalize, ids, weights);
+#pragma unroll
+    for (int r = 0; r < KMAX; ++r)
+      if (r < k) atomicAdd(&hist_lds[r * E + tk.ti[r]], 1);
+  }
+}
+
 __device__ __forceinline__ void wave_block_hist(int* lds_w, bool active, int64_t s, bool valid, int wb,
                                                 const RouteArgs& a) {
   const int lane = lane_id();

@@ -52,34 +52,43 @@ def assert_equal(gpu, ref, what):
                              f"gpu {[gpu[tuple(b)] for b in bad]} oracle {[ref[tuple(b)] for b in bad]}")
 
 
-def gpu_gate(w, inp, E, k, C, kind, normalize, logits=None):
+def gpu_gate(w, inp, E, k, C, kind, normalize, logits=None, groups=0, noise=None, temperature=0.0,
+             hash_table=None):
     """Run moe_gate on device copies of the host inputs; return host arrays."""
     dt = w["dtype"]
+    ext = dict(groups=groups, noise=wl.to_device(noise, "f32"), temperature=temperature)
     if kind == hm.MOE_GATE_HASH:
-        out = hm.gate(kind, k, E, C, token_ids=wl.to_device(inp["token_ids"], dt), hash_seed=0)
+        out = hm.gate(kind, k, E, C, token_ids=wl.to_device(inp["token_ids"], dt), hash_seed=0,
+                      hash_table=wl.to_device(hash_table, "i32"))
     elif logits is not None:
-        out = hm.gate(kind, k, E, C, logits=wl.to_device(logits, "f32"), logits_in=True, normalize=normalize)
+        out = hm.gate(kind, k, E, C, logits=wl.to_device(logits, "f32"), logits_in=True, normalize=normalize, **ext)
     else:
         out = hm.gate(kind, k, E, C, x=wl.to_device(inp["x"], dt), wg=wl.to_device(inp["wg"], dt),
-                      bias=wl.to_device(inp["bias"], "f32"), normalize=normalize, want_logits=True)
+                      bias=wl.to_device(inp["bias"], "f32"), normalize=normalize, want_logits=True, **ext)
     torch.cuda.synchronize()
     return {key: wl.to_host(v) for key, v in out.items()}
 
 
-def check_gate(w, inp, g, E, k, C, kind, normalize, logits_in=None):
-    """Compare gate outputs `g` (host) with the oracle.  Returns stats."""
+def check_gate(w, inp, g, E, k, C, kind, normalize, logits_in=None, groups=0, noise=None, temperature=0.0,
+               hash_table=None):
+    """Compare gate outputs `g` (host) with the oracle.  `logits_in`: the logits
+    the selection saw (after noise and temperature).  Returns stats."""
     dt = w["dtype"]
     stats = {}
     if kind == hm.MOE_GATE_HASH:
-        ref = oracle.gate(oracle.GATE_HASH, 1, E, C, token_ids=inp["token_ids"], hash_seed=0)
+        ref = oracle.gate(oracle.GATE_HASH, 1, E, C, token_ids=inp["token_ids"], hash_seed=0, hash_table=hash_table)
     else:
         sel = logits_in
         if sel is None:
             L64, A = oracle.logits(inp["x"], inp["wg"], dt, inp["bias"])
+            if temperature > 0:
+                gz = 0.0 if noise is None else np.asarray(noise, dtype=np.float32).astype(np.float64)
+                t = float(np.float32(temperature))
+                L64, A = (L64 + gz) / t, (A + np.abs(gz)) / t
             stats["logits_err"] = assert_close(g["logits"], L64, A, RTOL["f32"], "logits")
             sel = g["logits"]
             # end to end: selection on the fp64 logits may differ only at certified near-ties
-            ids64 = oracle.select(L64, kind, k)
+            ids64 = oracle.select(L64, kind, k, groups)
             mism = np.argwhere(ids64 != g["ids"])
             for s, r in mism:
                 a, b = int(ids64[s, r]), int(g["ids"][s, r])
@@ -87,7 +96,7 @@ def check_gate(w, inp, g, E, k, C, kind, normalize, logits_in=None):
                 assert gap <= 2 * RTOL["f32"] * max(A[s, a], A[s, b]), \
                     f"ids differ at ({s},{r}) without a near-tie: gap {gap}"
             stats["near_tie_mismatches"] = int(len(mism))
-        ref = oracle.gate(kind, k, E, C, normalize=normalize, sel_logits=sel)
+        ref = oracle.gate(kind, k, E, C, normalize=normalize, sel_logits=sel, groups=groups)
     for key in ("ids", "slots", "counts", "demand", "slot_src"):
         assert_equal(g[key], ref[key], key)
     stats["weights_err"] = assert_close(g["weights"], ref["weights"], np.abs(ref["weights"]), RTOL["f32"], "weights")

@@ -38,9 +38,10 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_abi_version_and_struct_layout(lib):
-    assert lib.moe_abi_version() == 3
-    assert ctypes.sizeof(b.GateParams) == 48
+    assert lib.moe_abi_version() == 4
+    assert ctypes.sizeof(b.GateParams) == 56
     assert b.GateParams.hash_seed.offset == 40
+    assert b.GateParams.temperature.offset == 48 and b.GateParams.hash_vocab.offset == 52
     assert ctypes.sizeof(b.Layout) == 24
     assert lib.moe_status_string(0) == b"MOE_OK"
     assert lib.moe_status_string(3) == b"MOE_ERR_WORKSPACE"
@@ -66,13 +67,17 @@ BAD_PARAMS = [
     dict(E=0), dict(E=1025), dict(S=-1), dict(capacity=-1), dict(k=0), dict(k=9, E=16),
     dict(k=3, E=2), dict(kind=1, k=3, E=16), dict(kind=2, k=2), dict(kind=3), dict(dtype=2),
     dict(normalize=2), dict(logits_in=2), dict(kind=2, logits_in=1), dict(d=0),
-    dict(E=1024, capacity=1 << 21), dict(S=1 << 30, k=2),
+    dict(E=1024, capacity=1 << 21), dict(S=1 << 30, k=2), dict(kind=4),
+    dict(groups=2), dict(kind=3, groups=0), dict(kind=3, groups=3), dict(kind=3, groups=4, k=3),
+    dict(temperature=-1.0), dict(temperature=float("nan")), dict(temperature=float("inf")),
+    dict(kind=2, temperature=0.5), dict(hash_vocab=10), dict(kind=2, hash_vocab=-1),
 ]
 
 
 @pytest.mark.parametrize("bad", BAD_PARAMS)
 def test_bad_gate_params_rejected(lib, bad):
-    base = dict(S=100, d=256, E=8, k=1, capacity=20, kind=0, normalize=0, logits_in=0, dtype=0, hash_seed=0)
+    base = dict(S=100, d=256, E=8, k=1, capacity=20, kind=0, normalize=0, logits_in=0, dtype=0, hash_seed=0, groups=0,
+                temperature=0.0, hash_vocab=0)
     base.update(bad)
     p = hm.gate_params(**base)
     st, _ = _ws(p)
@@ -80,13 +85,35 @@ def test_bad_gate_params_rejected(lib, bad):
     assert lib.moe_last_error() != b""
 
 
-def test_reserved_field_and_null_params(lib):
-    p = hm.gate_params(100, 256, 8, 1, 20, 0)
-    p.reserved = 1
-    assert _ws(p)[0] == b.MOE_ERR_INVALID_ARG
+def test_null_params_and_extended_workspace(lib):
     n = ctypes.c_size_t(0)
     assert lib.moe_gate_workspace_size(None, ctypes.byref(n)) == b.MOE_ERR_INVALID_ARG
-    assert lib.moe_gate(None, *([None] * 11), None, 0, None) == b.MOE_ERR_INVALID_ARG
+    assert lib.moe_gate(None, *([None] * 13), None, 0, None) == b.MOE_ERR_INVALID_ARG
+    # hierarchical top-k and tempered gates also hold their logits: [S, E] fp32 after the histogram
+    for params in (hm.gate_params(1000, 256, 16, 2, 20, 3, groups=4), hm.gate_params(1000, 256, 16, 2, 20, 0, temperature=0.5)):
+        hist = 2 * ((1000 + 63) // 64) * 16 * 4
+        assert _ws(params) == (0, (hist + 255) // 256 * 256 + 1000 * 16 * 4)
+
+
+def test_balanced_hash_table_matches_the_oracle(lib):
+    import numpy as np
+
+    import oracle
+    ranks = np.arange(1, 50258, dtype=np.float64)
+    p = ranks ** -1.1
+    p /= p.sum()
+    for E in (128, 7, 1):
+        assert np.array_equal(hm.moe_hash_balanced_table(p, E), oracle.balanced_hash_table(p, E))
+    rng = np.random.default_rng(5)
+    f = rng.integers(0, 4, 300).astype(np.float64)  # many equal frequencies
+    assert np.array_equal(hm.moe_hash_balanced_table(f, 9), oracle.balanced_hash_table(f, 9))
+    bad = np.array([1.0, -1.0])
+    with pytest.raises(b.MoeError):
+        hm.moe_hash_balanced_table(bad, 2)
+    with pytest.raises(b.MoeError):
+        hm.moe_hash_balanced_table(np.array([1.0, np.nan]), 2)
+    with pytest.raises(b.MoeError):
+        hm.moe_hash_balanced_table(np.ones(4), 0)
 
 
 def test_row_size_must_be_16_byte_multiple(lib):
@@ -105,7 +132,8 @@ A4 = A16 + 4
 def test_gate_pointer_checks(lib):
     p = hm.gate_params(100, 256, 8, 1, 20, 0)
     call = lambda **kw: lib.moe_gate(ctypes.byref(p), kw.get("x", A16), kw.get("wg", A16), kw.get("bias"),
-                                     kw.get("tok"), kw.get("logits"), kw.get("ids", A16), kw.get("slots", A16),
+                                     kw.get("tok"), kw.get("noise"), kw.get("table"), kw.get("logits"),
+                                     kw.get("ids", A16), kw.get("slots", A16),
                                      kw.get("w", A16), kw.get("counts", A16), kw.get("demand"),
                                      kw.get("src", A16), kw.get("ws", A16), kw.get("wsb", 1 << 20), None)
     assert call(x=None) == b.MOE_ERR_INVALID_ARG
@@ -115,11 +143,18 @@ def test_gate_pointer_checks(lib):
     assert call(tok=A16) == b.MOE_ERR_INVALID_ARG                  # token ids only for HASH
     assert call(ws=None) == b.MOE_ERR_WORKSPACE
     assert call(wsb=16) == b.MOE_ERR_WORKSPACE
+    assert call(noise=A16) == b.MOE_ERR_INVALID_ARG                # noise needs a temperature
+    assert call(table=A16) == b.MOE_ERR_INVALID_ARG                # a table only for HASH
     ph = hm.gate_params(100, 0, 8, 1, 20, 2)
-    assert lib.moe_gate(ctypes.byref(ph), A16, None, None, A16, None, A16, A16, A16, A16, None, A16, A16,
+    assert lib.moe_gate(ctypes.byref(ph), A16, None, None, A16, None, None, None, A16, A16, A16, A16, None, A16, A16,
                         1 << 20, None) == b.MOE_ERR_INVALID_ARG  # HASH takes no x
+    assert lib.moe_gate(ctypes.byref(ph), None, None, None, A16, None, A16, None, A16, A16, A16, A16, None, A16, A16,
+                        1 << 20, None) == b.MOE_ERR_INVALID_ARG  # a table needs hash_vocab
+    pt = hm.gate_params(100, 0, 8, 1, 20, 2, hash_vocab=50)
+    assert lib.moe_gate(ctypes.byref(pt), None, None, None, A16, None, None, None, A16, A16, A16, A16, None, A16, A16,
+                        1 << 20, None) == b.MOE_ERR_INVALID_ARG  # hash_vocab needs a table
     pl = hm.gate_params(100, 0, 8, 1, 20, 0, logits_in=1)
-    assert lib.moe_gate(ctypes.byref(pl), None, None, None, None, None, A16, A16, A16, A16, None, A16, A16,
+    assert lib.moe_gate(ctypes.byref(pl), None, None, None, None, None, None, None, A16, A16, A16, A16, None, A16, A16,
                         1 << 20, None) == b.MOE_ERR_INVALID_ARG  # logits required as input
 
 
@@ -175,7 +210,7 @@ def _bwd_ws_formula(S, d, E, dtype):
 
 def test_gate_bwd_struct_and_workspace(lib):
     assert ctypes.sizeof(b.GateBwdParams) == 40
-    assert b.GateBwdParams.aux_coef.offset == 32
+    assert b.GateBwdParams.aux_coef.offset == 32 and b.GateBwdParams.temperature.offset == 36
     for S, d, E, k, dt in [(32768, 2048, 64, 4, b.MOE_BF16), (32768, 2048, 64, 4, b.MOE_F32),
                            (1000, 256, 8, 1, b.MOE_F32), (0, 16, 3, 1, b.MOE_F32), (5000, 64, 1024, 2, b.MOE_BF16),
                            (8192, 1024, 16, 2, b.MOE_BF16), (100, 520, 48, 2, b.MOE_BF16)]:
@@ -186,22 +221,19 @@ def test_gate_bwd_struct_and_workspace(lib):
 
 
 BAD_BWD = [
-    dict(kind=2), dict(kind=3), dict(E=0), dict(E=1025), dict(S=-1), dict(d=0), dict(k=0), dict(k=9, E=16),
+    dict(kind=2), dict(kind=5), dict(E=0), dict(E=1025), dict(S=-1), dict(d=0), dict(k=0), dict(k=9, E=16),
     dict(kind=1, k=3, E=16), dict(normalize=2), dict(accumulate_dx=2), dict(dtype=2),
     dict(aux_coef=float("nan")), dict(aux_coef=float("inf")), dict(kind=1, k=2, aux_coef=0.01),
-    dict(S=1 << 30, k=2),
+    dict(S=1 << 30, k=2), dict(temperature=-0.5), dict(temperature=float("nan")), dict(kind=4),
 ]
 
 
 @pytest.mark.parametrize("bad", BAD_BWD)
 def test_bad_gate_bwd_params_rejected(lib, bad):
-    base = dict(S=100, d=256, E=8, k=1, kind=0, normalize=0, dtype=0, accumulate_dx=0, aux_coef=0.0)
+    base = dict(S=100, d=256, E=8, k=1, kind=0, normalize=0, dtype=0, accumulate_dx=0, aux_coef=0.0, temperature=0.0)
     base.update(bad)
     st, _ = _bwd_ws(hm.gate_bwd_params(**base))
     assert st == b.MOE_ERR_INVALID_ARG, (bad, lib.moe_last_error())
-    p = hm.gate_bwd_params(100, 256, 8, 1, 0)
-    p.reserved = 3
-    assert _bwd_ws(p)[0] == b.MOE_ERR_INVALID_ARG
 
 
 def test_gate_bwd_pointer_checks(lib):

@@ -60,7 +60,7 @@ def test_graph_replay_matches_eager(wid, S, d):
             if b[key] is not None]
 
     def step(st):
-        hm.moe_gate(params, x if learned else None, wg, bias, tok if not learned else None, None, b["ids"],
+        hm.moe_gate(params, x if learned else None, wg, bias, tok if not learned else None, None, None, None, b["ids"],
                     b["slots"], b["weights"], b["counts"], b["demand"], b["slot_src"], ws, st)
         hm.moe_dispatch(lay, x, b["ids"], b["slots"], b["slot_src"], b["xe"], st)
         hm.moe_combine(lay, b["xe"], b["ids"], b["slots"], b["weights"], b["y"], st)

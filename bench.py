@@ -363,6 +363,55 @@ def main():
     tok_kept = int((sl >= 0).any(axis=1).sum())
     ab = alg_bytes(w, S, d, E, k, C, elt, n_kept, tok_kept, want_dw)
     step_bytes = sum(ab.values())
+
+    # the further gates of Sec. 3.1 on this workload's shape, outside the timed
+    # step: hierarchical top-k (groups of 16 experts) and Dense-To-Sparse
+    # (Gumbel noise, temperature 0.5) for learned gates, the balanced table for
+    # the hash gate; each timed over `steps` calls of moe_gate
+    def time_gate(gp, **kw):
+        gws = torch.empty((hm.moe_gate_workspace_size(gp),), dtype=torch.uint8, device=dev)
+
+        def call():
+            hm.moe_gate(gp, kw.get("x"), kw.get("wg"), kw.get("bias"), kw.get("tok"), kw.get("noise"),
+                        kw.get("table"), None, ids, slots, weights, counts, demand, slot_src, gws, stream)
+        for _ in range(3):
+            call()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(args.steps):
+            call()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / args.steps
+
+    gates = {}
+    if learned:
+        G = max(1, E // 16)
+        kh = min(k, E // G, 8)
+        gp = hm.gate_params(S, d, E, kh, C, hm.MOE_GATE_HTOPK, w["normalize"], 0, dcode, 0, groups=G)
+        ms = time_gate(gp, x=x, wg=wg, bias=bias)
+        b = ab["gate"] - S * k * 12 + S * kh * 12 + 2 * S * E * 4  # + logits written and read once
+        gates["htopk"] = {"ms": round(ms, 5), "groups": G, "k": kh, "alg_bytes": b,
+                          "GB/s": round(b / (ms * 1e-3) / 1e9, 1)}
+        noise = torch.from_numpy(
+            (-np.log(-np.log(np.random.default_rng(3).random((S, E))))).astype(np.float32)).to(dev)
+        gp = hm.gate_params(S, d, E, k, C, w["kind"], w["normalize"], 0, dcode, 0, temperature=0.5)
+        ms = time_gate(gp, x=x, wg=wg, bias=bias, noise=noise)
+        b = ab["gate"] + 3 * S * E * 4  # + noise read, logits written and read once
+        gates["dense_to_sparse"] = {"ms": round(ms, 5), "temperature": 0.5, "alg_bytes": b,
+                                    "GB/s": round(b / (ms * 1e-3) / 1e9, 1)}
+        del noise
+    else:
+        ranks = np.arange(1, w["vocab"] + 1, dtype=np.float64)
+        pz = ranks ** -w["zipf_a"]
+        pz /= pz.sum()
+        table = torch.from_numpy(hm.moe_hash_balanced_table(pz, E)).to(dev)
+        gp = hm.gate_params(S, 0, E, 1, C, hm.MOE_GATE_HASH, 0, 0, dcode, 0, hash_vocab=int(table.shape[0]))
+        ms = time_gate(gp, tok=tok, table=table)
+        gates["balanced_hash"] = {"ms": round(ms, 5), "alg_bytes": ab["gate"] + S * 4,
+                                  "GB/s": round((ab["gate"] + S * 4) / (ms * 1e-3) / 1e9, 1)}
+
     dom = max(("dispatch", "combine", "combine_bwd", "dispatch_bwd", "gate"), key=lambda o: op_ms[o])
     achieved = ab[dom] / (op_ms[dom] * 1e-3) / 1e9
     kern, ksrc = kernel_of_op(dom, w)
@@ -416,6 +465,7 @@ def main():
                      "GB/s": round(ab[op] / (op_ms[op] * 1e-3) / 1e9, 1)} for op in OPS},
         "routing": {"kept_assignments": n_kept, "tokens_with_kept": tok_kept, "assignments": S * k},
         "gate_bwd": gate_bwd,
+        "gates": gates,
     }
     fwd_ms = op_ms["gate"] + op_ms["dispatch"] + op_ms["combine"]
     out["fwd"] = {"ms": round(fwd_ms, 5), "tokens/s": round(S / (fwd_ms * 1e-3), 1),

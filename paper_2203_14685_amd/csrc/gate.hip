@@ -63,33 +63,52 @@ __global__ __launch_bounds__(kBlock) void route_hash_kernel(RouteArgs a) {
 }
 
 // ---------------------------------------------------------------- selection on final logits
-// One block per 64-token wave block, P lanes per token.  Each lane turns its
-// slice of the raw logits into final logits ((raw + noise) / temperature, or
-// raw) and stores them; after a block barrier the P lanes select on the stored
-// row.
+constexpr int kSelTileE = 128;  // up to this many experts the block's logits are kept in LDS
+
+// One block per 64-token wave block, P lanes per token select on the block's
+// final logits.
 template <int P, int KMAX, int MODE>  // MODE: 0 top-k, 1 kTop1, 3 hierarchical top-k
 __global__ __launch_bounds__(kWave * P) void select_ext_kernel(SelectArgs a) {
-  extern __shared__ int hist_lds[];  // [k][E]
+  extern __shared__ int hist_lds[];  // [k][E], then (E <= kSelTileE) the block's logits [64][E + 1]
+  constexpr int kThreads = kWave * P;
   const int t = threadIdx.x / P, j = threadIdx.x % P;
   const int64_t s = static_cast<int64_t>(blockIdx.x) * kWave + t;
   const bool valid = s < a.S;
   const int E = a.E;
-  for (int i = threadIdx.x; i < a.k * E; i += kWave * P) hist_lds[i] = 0;
-  const int slice = E / P;
-  const int64_t row = (valid ? s : 0) * E;
-  if (valid) {
-    for (int e = j * slice; e < (j + 1) * slice; ++e) {
-      float v = a.raw[row + e];
-      if (a.temperature > 0.f) {
-        if (a.noise) v = v + a.noise[row + e];
-        v = v / a.temperature;
+  for (int i = threadIdx.x; i < a.k * E; i += kThreads) hist_lds[i] = 0;
+  const bool use_tile = E <= kSelTileE;
+  float* tile = reinterpret_cast<float*>(hist_lds + a.k * E);
+  const bool transform = a.temperature > 0.f || a.fin != a.raw;
+  // the block's rows are one contiguous piece of [S, E]: a flat, coalesced pass
+  // makes the final logits ((raw + noise) / temperature, or raw), stores them
+  // when asked and keeps them in LDS; four loads are issued before their stores
+  if (transform || use_tile) {
+    const int64_t base = static_cast<int64_t>(blockIdx.x) * kWave * E;
+    const int64_t rows = min(static_cast<int64_t>(kWave), a.S - static_cast<int64_t>(blockIdx.x) * kWave);
+    const int n = static_cast<int>(rows) * E;
+    for (int f0 = threadIdx.x; f0 < n; f0 += 4 * kThreads) {
+      float v[4], g[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int f = f0 + u * kThreads;
+        v[u] = f < n ? a.raw[base + f] : 0.f;
+        g[u] = (f < n && a.noise) ? a.noise[base + f] : 0.f;
       }
-      a.fin[row + e] = v;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int f = f0 + u * kThreads;
+        if (f < n) {
+          float val = v[u];
+          if (a.temperature > 0.f) val = (a.noise ? val + g[u] : val) / a.temperature;
+          if (transform) a.fin[base + f] = val;
+          if (use_tile) tile[(f / E) * (E + 1) + f % E] = val;
+        }
+      }
     }
   }
   __syncthreads();
   // invalid tokens select on row 0 (their results are not written)
-  const float* lrow = a.fin + row;
+  const float* lrow = use_tile ? tile + (valid ? t : 0) * (E + 1) : a.fin + (valid ? s : 0) * E;
   if constexpr (MODE == 3) {
     select_token_htopk<P, KMAX>(lrow, E, a.k, E / a.groups, a.normalize, j, valid, a.ids + s * a.k,
                                 a.weights + s * a.k, hist_lds);
@@ -98,14 +117,15 @@ __global__ __launch_bounds__(kWave * P) void select_ext_kernel(SelectArgs a) {
                                      hist_lds);
   }
   __syncthreads();
-  for (int i = threadIdx.x; i < a.k * E; i += kWave * P)
+  for (int i = threadIdx.x; i < a.k * E; i += kThreads)
     a.hist[static_cast<int64_t>(i) * a.nb + blockIdx.x] = hist_lds[i];
 }
 
 template <int P, int KMAX, int MODE>
 static hipError_t launch_sel_t(const SelectArgs& a, hipStream_t st) {
-  select_ext_kernel<P, KMAX, MODE>
-      <<<dim3(static_cast<unsigned>(a.nb)), dim3(kWave * P), static_cast<size_t>(a.k) * a.E * sizeof(int), st>>>(a);
+  const size_t tile = a.E <= kSelTileE ? static_cast<size_t>(kWave) * (a.E + 1) * sizeof(float) : 0;
+  select_ext_kernel<P, KMAX, MODE><<<dim3(static_cast<unsigned>(a.nb)), dim3(kWave * P),
+                                     static_cast<size_t>(a.k) * a.E * sizeof(int) + tile, st>>>(a);
   return hipGetLastError();
 }
 

@@ -18,7 +18,9 @@ paper it follows:
 * Sec. 3.2 "Gate Optimization" (top-k over a (num_tokens, num_experts) input)
   and "Layout Transform Optimization" (tokens of one expert made contiguous);
 * the gradient of Eq. 1 that end-to-end training of the layer (Sec. 2) needs,
-  and a load-balancing loss (reading R16) for the gates of Sec. 3.1.
+  and a load-balancing loss (reading R16) for the gates of Sec. 3.1;
+* the BASE layer's balanced assignment (Sec. 3.1, the equation of the BASE
+  Layer paragraph).
 
 Where the paper is silent the oracle takes one fixed reading; each is named at
 the function that depends on it (R1..R14 in the design notes).
@@ -50,6 +52,7 @@ from .gate import (
 )
 from .layout import dispatch, combine, dispatch_bwd, combine_bwd
 from .gate_bwd import gate_dlogits, aux_loss, gate_input_grads
+from .base import base_assign, base_weights
 
 __all__ = [
     "bf16_to_f64", "f64_to_bf16", "decode", "encode",
@@ -57,5 +60,5 @@ __all__ = [
     "gate_weights", "splitmix64_output", "hash_ids", "noisy_logits_f32", "balanced_hash_table",
     "table_hash_ids", "assign_slots", "gate",
     "dispatch", "combine", "dispatch_bwd", "combine_bwd",
-    "gate_dlogits", "aux_loss", "gate_input_grads",
+    "gate_dlogits", "aux_loss", "gate_input_grads", "base_assign", "base_weights",
 ]

@@ -64,6 +64,10 @@ MUTANTS = [
     ("gate.py", "e = min(range(E), key=lambda i: (load[i], i))", "e = min(range(E), key=lambda i: (load[i], -i))",
      "balanced hash ties to the higher expert"),
     ("gate_bwd.py", "        return dL / t, M / t", "        return dL * t, M * t", "temperature chain rule"),
+    ("base.py", "ids[rows] = cols // c", "ids[rows] = cols % E", "BASE slot-to-expert map"),
+    ("base.py", "linear_sum_assignment(cost, maximize=True)", "linear_sum_assignment(cost, maximize=False)",
+     "BASE minimises"),
+    ("base.py", "return 1.0 / (1.0 + np.exp(-v))", "return 1.0 / (1.0 + np.exp(v))", "BASE weight sign"),
 ]
 
 
@@ -71,7 +75,8 @@ MUTANTS = [
 def test_pins_catch_mutant(tmp_path, fname, old, new, what):
     shutil.copytree(os.path.join(ROOT, "oracle"), tmp_path / "oracle")
     shutil.copytree(os.path.join(ROOT, "tests", "golden"), tmp_path / "tests" / "golden")
-    for f in ("conftest.py", "test_oracle_pins.py", "test_oracle_gate_bwd_pins.py", "test_oracle_gate_more_pins.py"):
+    for f in ("conftest.py", "test_oracle_pins.py", "test_oracle_gate_bwd_pins.py", "test_oracle_gate_more_pins.py",
+              "test_oracle_base_pins.py"):
         shutil.copy(os.path.join(ROOT, "tests", f), tmp_path / "tests" / f)
     path = tmp_path / "oracle" / fname
     src = path.read_text()
@@ -79,5 +84,5 @@ def test_pins_catch_mutant(tmp_path, fname, old, new, what):
     path.write_text(src.replace(old, new, 1))
     res = subprocess.run([sys.executable, "-m", "pytest", "-q", "-x", "-p", "no:cacheprovider",
                           "tests/test_oracle_pins.py", "tests/test_oracle_gate_bwd_pins.py",
-                          "tests/test_oracle_gate_more_pins.py"], cwd=tmp_path, capture_output=True, text=True, timeout=300)
+                          "tests/test_oracle_gate_more_pins.py", "tests/test_oracle_base_pins.py"], cwd=tmp_path, capture_output=True, text=True, timeout=300)
     assert res.returncode != 0, f"pins did not catch: {what}\n{res.stdout[-2000:]}"

@@ -29,7 +29,8 @@
  *            (4-byte) alignment.
  * Async      Each call enqueues its kernels on `stream` (NULL = the default
  *            stream) and returns without waiting.  Nothing is read back to the
- *            host.  Outputs must not alias inputs.
+ *            host (except by moe_base_gate, which synchronizes its stream).
+ *            Outputs must not alias inputs.
  * Outputs    Every output element is overwritten: empty expert slots become zero
  *            rows, unused slot_src entries -1, dropped dw entries 0.
  * Errors     All argument checks run before the first HIP call; a failed check
@@ -41,6 +42,7 @@
  * Range      0 <= S, S*k < 2^31;  1 <= E <= 1024;  0 <= C, E*C < 2^31;  d >= 1.
  *            TOPK: 1 <= k <= min(E, 8).  KTOP1: 1 <= k <= 8 and E % k == 0.
  *            HASH: k == 1.  HTOPK: E % groups == 0, 1 <= k <= min(E / groups, 8).
+ *            BASE: S % E == 0, S / E <= 2048.
  */
 #ifndef HETUMOE_H
 #define HETUMOE_H
@@ -53,7 +55,7 @@
 extern "C" {
 #endif
 
-#define MOE_ABI_VERSION 4
+#define MOE_ABI_VERSION 5
 
 /* Symbols of the C ABI are the only ones the shared library exports. */
 #define MOE_API __attribute__((visibility("default")))
@@ -63,7 +65,8 @@ typedef enum {
   MOE_ERR_INVALID_ARG = 1, /* a size, pointer or option is out of the contract */
   MOE_ERR_UNSUPPORTED = 2, /* valid request this build does not handle (alignment, row size) */
   MOE_ERR_WORKSPACE = 3,   /* workspace NULL or smaller than moe_gate_workspace_size() */
-  MOE_ERR_HIP = 4          /* a HIP runtime call failed; see moe_last_error() */
+  MOE_ERR_HIP = 4,         /* a HIP runtime call failed; see moe_last_error() */
+  MOE_ERR_NOT_CONVERGED = 5 /* moe_base_gate: the auction reached its round limit */
 } moe_status;
 
 typedef enum { MOE_F32 = 0, MOE_BF16 = 1 } moe_dtype;
@@ -164,6 +167,60 @@ MOE_API moe_status moe_gate(const moe_gate_params* p, const void* x, const void*
  * (copied to the device by the caller) with hash_vocab = vocab.
  */
 MOE_API moe_status moe_hash_balanced_table(const double* freq, int32_t vocab, int32_t E, int32_t* table);
+
+/* Parameters of moe_base_gate (host memory). */
+typedef struct {
+  int32_t S;          /* tokens; a multiple of E, with S / E <= 2048 */
+  int32_t d;          /* model width (row length of x) */
+  int32_t E;          /* experts */
+  int32_t capacity;   /* C: slots per expert for the layout calls (S / E keeps every token) */
+  int32_t logits_in;  /* 1 = `logits` is an input and x, wg, bias are NULL; 0 = projected */
+  int32_t dtype;      /* moe_dtype of x and wg */
+  int32_t max_rounds; /* auction rounds allowed per eps phase; 0 = 4096 */
+} moe_base_params;
+
+/* What the auction of moe_base_gate did (host memory). */
+typedef struct {
+  int32_t phases;     /* eps phases run */
+  int32_t rounds;     /* bidding rounds, summed over phases */
+  double eps;         /* eps of the last phase: the total score is within S * eps of the optimum */
+} moe_base_info;
+
+/* Bytes of device workspace moe_base_gate needs for `p`.  Fails with
+ * MOE_ERR_INVALID_ARG for parameters moe_base_gate would reject. */
+MOE_API moe_status moe_base_gate_workspace_size(const moe_base_params* p, size_t* bytes);
+
+/*
+ * moe_base_gate -- the BASE layer gate of Sec. 3.1: a balanced assignment in
+ * which every expert receives exactly S / E tokens and the summed score
+ * sum_s L[s, a_s] is as large as possible (a linear assignment problem), with
+ * L[s,e] = sum_j x[s,j] * wg[j,e] + bias[e] the gate logits (fp32 accumulation)
+ * as in moe_gate, or given.
+ *
+ * Solved by an auction with eps-scaling (Bertsekas): prices and bids in fp64,
+ * eps from a quarter of the score range down to the range times 2^-30, so the
+ * total is within S * info->eps of the optimum (exactly optimal when distinct
+ * assignments' totals differ by more than that).  Equal bids go to the lower
+ * token; results are bitwise reproducible.
+ *
+ * Outputs ids [S] (k = 1), weights [S] fp32 = sigmoid(L[s, ids[s]]) (the BASE
+ * layer scales its expert's output by this), logits [S,E] fp32 (optional
+ * output when logits_in == 0), and, as moe_gate with k = 1: slots [S], counts
+ * [E], slot_src [E,C] in token order per expert.  info (host memory, may be
+ * NULL) receives the auction's statistics.
+ *
+ * Unlike the other calls this one SYNCHRONIZES `stream`: the host reads the
+ * number of unassigned tokens after every 8 rounds.  It returns
+ * MOE_ERR_NOT_CONVERGED when a phase reaches max_rounds, and
+ * MOE_ERR_INVALID_ARG when a score is infinite or NaN (found on the device
+ * after the projection); outputs are then undefined.
+ * Workspace device memory of at least moe_base_gate_workspace_size() bytes,
+ *          16-byte aligned; contents on entry are ignored.
+ */
+MOE_API moe_status moe_base_gate(const moe_base_params* p, const void* x, const void* wg,
+                                 const float* bias, float* logits, int32_t* ids, int32_t* slots,
+                                 float* weights, int32_t* counts, int32_t* slot_src, void* workspace,
+                                 size_t workspace_bytes, moe_base_info* info, hipStream_t stream);
 
 /*
  * moe_dispatch -- step 2 of Algorithm 1 (Layout_Transform; Sec. 3.2, layout

@@ -16,14 +16,15 @@ import torch
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libhetumoe.so")
 
-MOE_OK, MOE_ERR_INVALID_ARG, MOE_ERR_UNSUPPORTED, MOE_ERR_WORKSPACE, MOE_ERR_HIP = range(5)
+MOE_OK, MOE_ERR_INVALID_ARG, MOE_ERR_UNSUPPORTED, MOE_ERR_WORKSPACE, MOE_ERR_HIP, MOE_ERR_NOT_CONVERGED = range(6)
 MOE_F32, MOE_BF16 = 0, 1
 MOE_GATE_TOPK, MOE_GATE_KTOP1, MOE_GATE_HASH, MOE_GATE_HTOPK = 0, 1, 2, 3
 
 EXPORTED = (
     "moe_gate_workspace_size", "moe_gate", "moe_dispatch", "moe_combine",
     "moe_dispatch_bwd", "moe_combine_bwd", "moe_gate_bwd_workspace_size", "moe_gate_bwd",
-    "moe_hash_balanced_table", "moe_status_string", "moe_last_error", "moe_abi_version",
+    "moe_hash_balanced_table", "moe_base_gate_workspace_size", "moe_base_gate",
+    "moe_status_string", "moe_last_error", "moe_abi_version",
 )
 
 
@@ -59,6 +60,17 @@ class GateBwdParams(ctypes.Structure):
     ]
 
 
+class BaseParams(ctypes.Structure):
+    _fields_ = [
+        ("S", ctypes.c_int32), ("d", ctypes.c_int32), ("E", ctypes.c_int32), ("capacity", ctypes.c_int32),
+        ("logits_in", ctypes.c_int32), ("dtype", ctypes.c_int32), ("max_rounds", ctypes.c_int32),
+    ]
+
+
+class BaseInfo(ctypes.Structure):
+    _fields_ = [("phases", ctypes.c_int32), ("rounds", ctypes.c_int32), ("eps", ctypes.c_double)]
+
+
 _lib = None
 
 
@@ -82,9 +94,12 @@ def load():
     lib.moe_gate_bwd_workspace_size.argtypes = [ctypes.POINTER(GateBwdParams), ctypes.POINTER(ctypes.c_size_t)]
     lib.moe_gate_bwd.argtypes = [ctypes.POINTER(GateBwdParams), vp, vp, f32p, i32p, f32p, f32p, vp, f32p, f32p,
                                  f32p, vp, ctypes.c_size_t, vp]
+    lib.moe_base_gate_workspace_size.argtypes = [ctypes.POINTER(BaseParams), ctypes.POINTER(ctypes.c_size_t)]
+    lib.moe_base_gate.argtypes = [ctypes.POINTER(BaseParams), vp, vp, f32p, f32p, i32p, i32p, f32p, i32p, i32p,
+                                  vp, ctypes.c_size_t, ctypes.POINTER(BaseInfo), vp]
     for name in ("moe_gate_workspace_size", "moe_gate", "moe_dispatch", "moe_combine",
                  "moe_dispatch_bwd", "moe_combine_bwd", "moe_gate_bwd_workspace_size", "moe_gate_bwd",
-                 "moe_hash_balanced_table"):
+                 "moe_hash_balanced_table", "moe_base_gate_workspace_size", "moe_base_gate"):
         getattr(lib, name).restype = ctypes.c_int
     lib.moe_status_string.argtypes = [ctypes.c_int]
     lib.moe_status_string.restype = ctypes.c_char_p
@@ -238,6 +253,63 @@ def moe_hash_balanced_table(freq, E):
     table = np.empty(f.shape[0], dtype=np.int32)
     _check(load().moe_hash_balanced_table(f.ctypes.data, int(f.shape[0]), int(E), table.ctypes.data))
     return table
+
+
+def base_params(S, d, E, capacity, logits_in=0, dtype=MOE_F32, max_rounds=0):
+    return BaseParams(S, d, E, capacity, logits_in, dtype, max_rounds)
+
+
+def moe_base_gate_workspace_size(params):
+    n = ctypes.c_size_t(0)
+    _check(load().moe_base_gate_workspace_size(ctypes.byref(params), ctypes.byref(n)))
+    return n.value
+
+
+def moe_base_gate(params, x, wg, bias, logits, ids, slots, weights, counts, slot_src, workspace, info=None,
+                  stream=None):
+    """BASE-layer balanced assignment (synchronizes the stream).  `info`: a
+    BaseInfo filled with the auction's statistics, or None."""
+    lib = load()
+    f32, i32 = torch.float32, torch.int32
+    xdt = torch.bfloat16 if params.dtype == MOE_BF16 else torch.float32
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib.moe_base_gate(
+        ctypes.byref(params), _ptr(x, xdt, "x"), _ptr(wg, xdt, "wg"), _ptr(bias, f32, "bias"),
+        _ptr(logits, f32, "logits"), _ptr(ids, i32, "ids"), _ptr(slots, i32, "slots"),
+        _ptr(weights, f32, "weights"), _ptr(counts, i32, "counts"), _ptr(slot_src, i32, "slot_src"),
+        _ptr(workspace, None, "workspace"), ws_bytes, None if info is None else ctypes.byref(info),
+        _stream(stream)))
+
+
+def base_gate(E, capacity=None, *, x=None, wg=None, bias=None, logits=None, logits_in=False, want_logits=False,
+              max_rounds=0, stream=None):
+    """Allocate the outputs and run moe_base_gate; returns a dict of device
+    tensors (ids, slots, weights as [S, 1], the shape the layout calls take)
+    plus "info" (phases, rounds, eps of the auction)."""
+    if logits_in:
+        S, d, dcode = int(logits.shape[0]), 0, MOE_F32
+        dev = logits.device
+    else:
+        S, d, dcode = int(x.shape[0]), int(x.shape[1]), _dtype_code(x)
+        dev = x.device
+    C = S // E if capacity is None else capacity
+    params = base_params(S, d, E, C, int(bool(logits_in)), dcode, max_rounds)
+    out = {
+        "ids": torch.empty((S, 1), dtype=torch.int32, device=dev),
+        "slots": torch.empty((S, 1), dtype=torch.int32, device=dev),
+        "weights": torch.empty((S, 1), dtype=torch.float32, device=dev),
+        "counts": torch.empty((E,), dtype=torch.int32, device=dev),
+        "slot_src": torch.empty((E, C), dtype=torch.int32, device=dev),
+    }
+    if not logits_in:
+        logits = torch.empty((S, E), dtype=torch.float32, device=dev) if want_logits else None
+    out["logits"] = logits
+    ws = torch.empty((moe_base_gate_workspace_size(params),), dtype=torch.uint8, device=dev)
+    info = BaseInfo()
+    moe_base_gate(params, x, wg, bias, logits, out["ids"], out["slots"], out["weights"], out["counts"],
+                  out["slot_src"], ws, info, stream)
+    out["info"] = dict(phases=info.phases, rounds=info.rounds, eps=info.eps)
+    return out
 
 
 def dispatch(x, ids, slots, slot_src, stream=None):

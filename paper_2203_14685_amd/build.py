@@ -15,7 +15,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libhetumoe.so")
 
-SOURCES = ["gate_bwd.hip", "route_valu_f32.hip", "route_valu_bf16.hip", "route_mfma_rs.hip", "route_mfma_ph.hip", "route_mfma.hip",
+SOURCES = ["base.hip", "gate_bwd.hip", "route_valu_f32.hip", "route_valu_bf16.hip", "route_mfma_rs.hip", "route_mfma_ph.hip", "route_mfma.hip",
            "gate.hip", "layout.hip", "capi.hip"]
 
 # -packed-fp32-ops: no v_pk_{add,mul,fma}_f32 in generated code.

@@ -202,6 +202,56 @@ GateBwdPlan plan_gate_bwd(const moe_gate_bwd_params* p) {
   return g;
 }
 
+// Checks shared by moe_base_gate and moe_base_gate_workspace_size.
+moe_status check_base_params(const moe_base_params* p) {
+  if (!p) return fail(MOE_ERR_INVALID_ARG, "params is NULL");
+  if (p->dtype != MOE_F32 && p->dtype != MOE_BF16) return fail(MOE_ERR_INVALID_ARG, "dtype %d unknown", p->dtype);
+  if (p->S < 0) return fail(MOE_ERR_INVALID_ARG, "S = %d < 0", p->S);
+  if (p->E < 1 || p->E > 1024) return fail(MOE_ERR_INVALID_ARG, "E = %d outside [1, 1024]", p->E);
+  if (p->S % p->E != 0) return fail(MOE_ERR_INVALID_ARG, "BASE needs S %% E == 0, got S = %d, E = %d", p->S, p->E);
+  if (p->S / p->E > kBaseMaxCap)
+    return fail(MOE_ERR_UNSUPPORTED, "BASE needs S / E <= %d, got %d", kBaseMaxCap, p->S / p->E);
+  if (p->capacity < 0) return fail(MOE_ERR_INVALID_ARG, "capacity = %d < 0", p->capacity);
+  if (static_cast<int64_t>(p->E) * p->capacity > kI32Max) return fail(MOE_ERR_INVALID_ARG, "E * capacity >= 2^31");
+  if (p->logits_in != 0 && p->logits_in != 1) return fail(MOE_ERR_INVALID_ARG, "logits_in must be 0 or 1");
+  if (p->max_rounds < 0) return fail(MOE_ERR_INVALID_ARG, "max_rounds = %d < 0", p->max_rounds);
+  if (!p->logits_in) {
+    if (p->d < 1) return fail(MOE_ERR_INVALID_ARG, "d = %d < 1", p->d);
+    if ((static_cast<int64_t>(p->d) * elt_size(p->dtype)) % 16 != 0)
+      return fail(MOE_ERR_UNSUPPORTED, "row of x is %lld bytes; a multiple of 16 is required",
+                  static_cast<long long>(p->d) * static_cast<long long>(elt_size(p->dtype)));
+  }
+  return MOE_OK;
+}
+
+// Workspace of moe_base_gate, each piece 256-byte aligned: hist int32 [E, nb];
+// logits fp32 [S, E] (only when projected and not returned); price fp64 [E];
+// hold_v fp64 [S]; hold_t, assign, bid_e int32 [S]; bid_v fp64 [S];
+// hold_n int32 [E]; counts int32 [8]; range fp32 [2].
+struct BasePlan {
+  size_t off_hist, off_logits, off_price, off_hold_v, off_hold_t, off_hold_n, off_assign, off_bid_e, off_bid_v,
+      off_counts, off_range, total;
+};
+
+BasePlan plan_base(const moe_base_params* p, bool own_logits) {
+  BasePlan b{};
+  const size_t S = static_cast<size_t>(p->S), E = static_cast<size_t>(p->E);
+  size_t off = 0;
+  b.off_hist = off;   off += align256(static_cast<size_t>(hist_blocks(p->S)) * E * 4);
+  b.off_logits = off; off += own_logits ? align256(S * E * 4) : 0;
+  b.off_price = off;  off += align256(E * 8);
+  b.off_hold_v = off; off += align256(S * 8);
+  b.off_hold_t = off; off += align256(S * 4);
+  b.off_hold_n = off; off += align256(E * 4);
+  b.off_assign = off; off += align256(S * 4);
+  b.off_bid_e = off;  off += align256(S * 4);
+  b.off_bid_v = off;  off += align256(S * 8);
+  b.off_counts = off; off += align256(8 * 4);
+  b.off_range = off;  off += align256(2 * 4);
+  b.total = off;
+  return b;
+}
+
 int nchunks(const moe_layout* l) {
   return static_cast<int>((static_cast<int64_t>(l->d) * elt_size(l->dtype)) / 16);
 }
@@ -296,6 +346,7 @@ const char* moe_status_string(moe_status s) {
     case MOE_ERR_UNSUPPORTED: return "MOE_ERR_UNSUPPORTED";
     case MOE_ERR_WORKSPACE: return "MOE_ERR_WORKSPACE";
     case MOE_ERR_HIP: return "MOE_ERR_HIP";
+    case MOE_ERR_NOT_CONVERGED: return "MOE_ERR_NOT_CONVERGED";
   }
   return "unknown moe_status";
 }
@@ -498,6 +549,96 @@ moe_status moe_combine_bwd(const moe_layout* l, const void* dy, const void* ye, 
   a.dw = dw;
   const hipError_t err = launch_combine_bwd(a, stream);
   if (err != hipSuccess) return hip_fail(err, "moe_combine_bwd: kernel launch");
+  return ok();
+}
+
+moe_status moe_base_gate_workspace_size(const moe_base_params* p, size_t* bytes) {
+  if (!bytes) return fail(MOE_ERR_INVALID_ARG, "bytes is NULL");
+  CHECK(check_base_params(p));
+  *bytes = plan_base(p, !p->logits_in).total;
+  return ok();
+}
+
+moe_status moe_base_gate(const moe_base_params* p, const void* x, const void* wg, const float* bias, float* logits,
+                         int32_t* ids, int32_t* slots, float* weights, int32_t* counts, int32_t* slot_src,
+                         void* workspace, size_t workspace_bytes, moe_base_info* info, hipStream_t stream) {
+  static const char* who = "moe_base_gate";
+  CHECK(check_base_params(p));
+  const int64_t S = p->S, E = p->E, C = p->capacity;
+  const size_t elt = elt_size(p->dtype);
+  if (p->logits_in) {
+    CHECK(need(logits, S * E, 4, who, "logits"));
+    if (x || wg || bias) return fail(MOE_ERR_INVALID_ARG, "%s: with logits_in, x, wg and bias must be NULL", who);
+  } else {
+    CHECK(need(x, S * p->d, 16, who, "x"));
+    CHECK(need(wg, static_cast<int64_t>(p->d) * E, elt, who, "wg"));
+    CHECK(need(bias, 0, 4, who, "bias"));
+    CHECK(need(logits, 0, 4, who, "logits"));
+  }
+  CHECK(need(ids, S, 4, who, "ids"));
+  CHECK(need(slots, S, 4, who, "slots"));
+  CHECK(need(weights, S, 4, who, "weights"));
+  CHECK(need(counts, E, 4, who, "counts"));
+  CHECK(need(slot_src, E * C, 4, who, "slot_src"));
+  // the workspace size does not depend on whether the logits are returned
+  const BasePlan b = plan_base(p, !p->logits_in);
+  if (workspace_bytes < b.total) return fail(MOE_ERR_WORKSPACE, "%s: workspace of %zu bytes, %zu needed", who, workspace_bytes, b.total);
+  if (!workspace) return fail(MOE_ERR_WORKSPACE, "%s: workspace is NULL", who);
+  if (!aligned(workspace, 16)) return fail(MOE_ERR_WORKSPACE, "%s: workspace is not 16-byte aligned", who);
+  if (info) *info = moe_base_info{0, 0, 0.0};
+
+  char* ws = static_cast<char*>(workspace);
+  const int nb = static_cast<int>(hist_blocks(S));
+  int32_t* hist = reinterpret_cast<int32_t*>(ws + b.off_hist);
+  hipError_t err;
+  const float* L = logits;
+  if (!p->logits_in) {
+    float* out = logits ? logits : reinterpret_cast<float*>(ws + b.off_logits);
+    // projection only: a one-choice top-k pass writes the logits; its ids,
+    // weights and histogram are overwritten by the auction's outputs
+    RouteArgs ra{};
+    ra.S = p->S; ra.d = p->d; ra.E = p->E; ra.k = 1; ra.nb = nb;
+    ra.kind = MOE_GATE_TOPK; ra.normalize = 0; ra.logits_in = 0; ra.dtype = p->dtype;
+    ra.x = x; ra.wg = wg; ra.bias = bias; ra.logits = out;
+    ra.ids = ids; ra.weights = weights; ra.hist = hist;
+    if (p->S > 0) {
+      err = launch_route(ra, stream);
+      if (err != hipSuccess) return hip_fail(err, "moe_base_gate: route kernel launch");
+    }
+    L = out;
+  }
+  BaseArgs a{};
+  a.S = p->S; a.E = p->E; a.cap = p->S / p->E; a.nb = nb;
+  a.max_rounds = p->max_rounds > 0 ? p->max_rounds : 4096;
+  a.logits = L;
+  a.price = reinterpret_cast<double*>(ws + b.off_price);
+  a.hold_v = reinterpret_cast<double*>(ws + b.off_hold_v);
+  a.hold_t = reinterpret_cast<int32_t*>(ws + b.off_hold_t);
+  a.hold_n = reinterpret_cast<int32_t*>(ws + b.off_hold_n);
+  a.assign = reinterpret_cast<int32_t*>(ws + b.off_assign);
+  a.bid_e = reinterpret_cast<int32_t*>(ws + b.off_bid_e);
+  a.bid_v = reinterpret_cast<double*>(ws + b.off_bid_v);
+  a.counts = reinterpret_cast<int32_t*>(ws + b.off_counts);
+  a.range = reinterpret_cast<float*>(ws + b.off_range);
+  a.ids = ids; a.weights = weights; a.hist = hist;
+  BaseStats stats{};
+  err = run_base_auction(a, stream, &stats);
+  if (err != hipSuccess) return hip_fail(err, "moe_base_gate: auction");
+  if (info) *info = moe_base_info{stats.phases, stats.rounds, stats.eps};
+  if (stats.bad_scores) return fail(MOE_ERR_INVALID_ARG, "%s: a score is infinite or NaN", who);
+  if (stats.not_converged)
+    return fail(MOE_ERR_NOT_CONVERGED, "%s: no balanced assignment after %d rounds of a phase", who, a.max_rounds);
+
+  ScanArgs sa{};
+  sa.E = p->E; sa.k = 1; sa.nb = nb; sa.C = p->capacity;
+  sa.hist = hist; sa.counts = counts; sa.demand = nullptr; sa.slot_src = slot_src;
+  err = launch_scan(sa, stream);
+  if (err != hipSuccess) return hip_fail(err, "moe_base_gate: scan kernel launch");
+  AssignArgs aa{};
+  aa.S = p->S; aa.E = p->E; aa.k = 1; aa.nb = nb; aa.C = p->capacity;
+  aa.ids = ids; aa.offs = hist; aa.slots = slots; aa.slot_src = slot_src;
+  err = launch_assign(aa, stream);
+  if (err != hipSuccess) return hip_fail(err, "moe_base_gate: assign kernel launch");
   return ok();
 }
 

@@ -121,4 +121,41 @@ hipError_t launch_gate_bwd_dl(const GateBwdArgs& a, hipStream_t st);
 hipError_t launch_gate_bwd_dwg(const GateBwdArgs& a, hipStream_t st);
 hipError_t launch_gate_bwd_dx(const GateBwdArgs& a, hipStream_t st);
 
+// BASE layer gate: balanced assignment by an auction on fp32 scores [S, E]
+// (every expert takes exactly cap = S / E tokens).  Buffers of the workspace
+// are carved out by the C ABI.
+constexpr int kBaseCand = 2048;          // bidders an expert considers per round
+constexpr int kBaseMaxCap = 2048;        // largest S / E
+constexpr double kBaseEpsStep = 8.0;     // eps divisor between phases
+constexpr double kBaseEpsEnd = 0x1p-30;  // final eps, relative to the score range
+
+struct BaseArgs {
+  int S, E, cap, nb;       // nb: 64-token wave blocks
+  int max_rounds;          // per phase
+  const float* logits;     // [S, E]
+  double* price;           // [E]
+  double* hold_v;          // [E, cap] bids of each expert's holders, best first
+  int32_t* hold_t;         // [E, cap] their tokens
+  int32_t* hold_n;         // [E]
+  int32_t* assign;         // [S] expert of each token, -1 = unassigned
+  int32_t* bid_e;          // [S] expert bid for this round, -1 = none
+  double* bid_v;           // [S]
+  int32_t* counts;         // [8] unassigned tokens at the start of each round of a batch
+  float* range;            // [2] min and max score
+  int32_t* ids;            // [S]
+  float* weights;          // [S]
+  int32_t* hist;           // [E, nb]
+};
+
+struct BaseStats {
+  int phases, rounds;      // phases run, rounds summed over phases
+  double eps;              // eps of the last phase
+  int not_converged;       // a phase reached max_rounds
+  int bad_scores;          // a score is infinite or NaN
+};
+
+size_t base_resolve_lds(int cap);
+// Runs the auction and writes ids, weights and hist.  Synchronizes `st`.
+hipError_t run_base_auction(const BaseArgs& a, hipStream_t st, BaseStats* stats);
+
 }  // namespace hetumoe

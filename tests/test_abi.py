@@ -38,7 +38,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_abi_version_and_struct_layout(lib):
-    assert lib.moe_abi_version() == 4
+    assert lib.moe_abi_version() == 5
     assert ctypes.sizeof(b.GateParams) == 56
     assert b.GateParams.hash_seed.offset == 40
     assert b.GateParams.temperature.offset == 48 and b.GateParams.hash_vocab.offset == 52
@@ -258,3 +258,70 @@ def test_gate_bwd_pointer_checks(lib):
     p6 = hm.gate_bwd_params(100, 4, 8, 2, 0, 1, b.MOE_BF16)     # 8-byte rows of x / dx
     assert lib.moe_gate_bwd(ctypes.byref(p6), A16, A16, A16, A16, A16, None, A16, None, None, None, A16,
                             1 << 30, None) == b.MOE_ERR_UNSUPPORTED
+
+
+# ---------------------------------------------------------------- BASE layer gate
+
+def _base_ws(params):
+    n = ctypes.c_size_t(12345)
+    st = hm.load().moe_base_gate_workspace_size(ctypes.byref(params), ctypes.byref(n))
+    return st, n.value
+
+
+def _base_ws_formula(S, E, logits_in):
+    nb = (S + 63) // 64
+    return (_a256(nb * E * 4) + (0 if logits_in else _a256(S * E * 4)) + _a256(E * 8) + _a256(S * 8)
+            + _a256(S * 4) + _a256(E * 4) + 2 * _a256(S * 4) + _a256(S * 8) + 256 + 256)
+
+
+def test_base_struct_and_workspace(lib):
+    assert ctypes.sizeof(b.BaseParams) == 28 and b.BaseParams.max_rounds.offset == 24
+    assert ctypes.sizeof(b.BaseInfo) == 16 and b.BaseInfo.eps.offset == 8
+    assert lib.moe_status_string(b.MOE_ERR_NOT_CONVERGED) == b"MOE_ERR_NOT_CONVERGED"
+    for S, d, E, li in [(32768, 2048, 64, 0), (32768, 0, 64, 1), (0, 16, 8, 0), (4096, 256, 1024, 0), (2048, 8, 1, 0)]:
+        st, n = _base_ws(hm.base_params(S, d, E, max(1, S // E), li, b.MOE_BF16))
+        assert st == 0, lib.moe_last_error()
+        assert n == _base_ws_formula(S, E, li), (S, E, li)
+
+
+BAD_BASE = [
+    (dict(S=100, E=8), b.MOE_ERR_INVALID_ARG), (dict(E=0), b.MOE_ERR_INVALID_ARG),
+    (dict(E=1025), b.MOE_ERR_INVALID_ARG), (dict(S=-64), b.MOE_ERR_INVALID_ARG),
+    (dict(capacity=-1), b.MOE_ERR_INVALID_ARG), (dict(logits_in=2), b.MOE_ERR_INVALID_ARG),
+    (dict(dtype=2), b.MOE_ERR_INVALID_ARG), (dict(max_rounds=-1), b.MOE_ERR_INVALID_ARG),
+    (dict(d=0), b.MOE_ERR_INVALID_ARG), (dict(E=1024, capacity=1 << 21), b.MOE_ERR_INVALID_ARG),
+    (dict(S=8 * 2049), b.MOE_ERR_UNSUPPORTED), (dict(d=6), b.MOE_ERR_UNSUPPORTED),
+]
+
+
+@pytest.mark.parametrize("bad,status", BAD_BASE)
+def test_bad_base_params_rejected(lib, bad, status):
+    base = dict(S=128, d=256, E=8, capacity=16, logits_in=0, dtype=0, max_rounds=0)
+    base.update(bad)
+    st, _ = _base_ws(hm.base_params(**base))
+    assert st == status, (bad, lib.moe_last_error())
+    assert lib.moe_last_error() != b""
+
+
+def test_base_pointer_checks(lib):
+    p = hm.base_params(128, 256, 8, 16, 0, b.MOE_F32)
+    # moe_base_gate(p, x, wg, bias, logits, ids, slots, weights, counts, slot_src, ws, wsb, info, stream)
+    call = lambda prm=p, **kw: lib.moe_base_gate(
+        ctypes.byref(prm), kw.get("x", A16), kw.get("wg", A16), kw.get("bias"), kw.get("logits"),
+        kw.get("ids", A16), kw.get("slots", A16), kw.get("weights", A16), kw.get("counts", A16),
+        kw.get("slot_src", A16), kw.get("ws", A16), kw.get("wsb", 1 << 30), None, None)
+    n = ctypes.c_size_t(0)
+    assert lib.moe_base_gate_workspace_size(None, ctypes.byref(n)) == b.MOE_ERR_INVALID_ARG
+    assert lib.moe_base_gate(None, *([None] * 10), 0, None, None) == b.MOE_ERR_INVALID_ARG
+    assert call(x=None) == b.MOE_ERR_INVALID_ARG
+    assert call(x=A16 + 4) == b.MOE_ERR_UNSUPPORTED
+    assert call(wg=None) == b.MOE_ERR_INVALID_ARG
+    assert call(ids=None) == b.MOE_ERR_INVALID_ARG
+    assert call(slot_src=None) == b.MOE_ERR_INVALID_ARG
+    assert call(weights=A16 + 2) == b.MOE_ERR_INVALID_ARG
+    assert call(ws=None) == b.MOE_ERR_WORKSPACE
+    assert call(wsb=64) == b.MOE_ERR_WORKSPACE
+    assert call(ws=A16 + 4) == b.MOE_ERR_WORKSPACE
+    pl = hm.base_params(128, 0, 8, 16, 1, b.MOE_F32)
+    assert call(pl, x=None, wg=None) == b.MOE_ERR_INVALID_ARG          # logits_in needs logits
+    assert call(pl, logits=A16) == b.MOE_ERR_INVALID_ARG               # ... and no x / wg

@@ -13,33 +13,45 @@
 // assignment is within S * eps of the optimum (the dual bound).  eps is lowered
 // in phases (eps-scaling: prices kept, holders cleared).  Prices and bids are
 // fp64.  Every step runs in a fixed order, so results are bitwise reproducible.
+//
+// The auction's control lives on the device: round r reads the state block
+// state[r & 1] and the resolve kernel's block 0 writes state[(r + 1) & 1], so
+// the host only enqueues rounds and checks the done flag now and then.  Rounds
+// enqueued after the auction has finished return at once.
 #include "common.hpp"
 #include "kernels.hpp"
 
 namespace hetumoe {
 
-constexpr int kBaseThreads = 1024;  // resolve: one block per expert
+constexpr int kBaseThreads = 1024;                  // resolve: one block per expert
+constexpr int kBaseWaves = kBaseThreads / kWave;    // 16
+constexpr int kBaseIters = 32;                      // token tiles of kBaseThreads per collection pass
 
 // (v, t) before (w, u): larger bid, then lower token
 __device__ __forceinline__ bool base_before(double v, int t, double w, int u) {
   return v > w || (v == w && t < u);
 }
 
-// ---------------------------------------------------------------- score range
-__global__ __launch_bounds__(kBaseThreads) void base_minmax_kernel(BaseArgs a) {
+// ---------------------------------------------------------------- set-up
+// Score range, in two steps: per-block minimum, maximum and a NaN / infinity
+// flag over a grid-strided share of the scores, then one block that reduces
+// them, derives the eps schedule and writes the first state.  A NaN or
+// infinite score ends the auction before it starts (failed = 2).
+__global__ __launch_bounds__(kBaseThreads) void base_range_kernel(BaseArgs a) {
   __shared__ float mx[kBaseThreads], mn[kBaseThreads];
   float hi = -INFINITY, lo = INFINITY;
-  int nan = 0;
+  int bad = 0;
   const int64_t n = static_cast<int64_t>(a.S) * a.E;
-  for (int64_t i = threadIdx.x; i < n; i += kBaseThreads) {
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBaseThreads + threadIdx.x; i < n;
+       i += static_cast<int64_t>(kBaseRangeBlocks) * kBaseThreads) {
     const float v = a.logits[i];
     hi = fmaxf(hi, v);
     lo = fminf(lo, v);
-    nan |= v != v;
+    bad |= !(fabsf(v) <= __FLT_MAX__);  // NaN or infinite
   }
   mx[threadIdx.x] = hi;
   mn[threadIdx.x] = lo;
-  nan = __syncthreads_or(nan);
+  bad = __syncthreads_or(bad);
   for (int w = kBaseThreads / 2; w > 0; w >>= 1) {
     if (static_cast<int>(threadIdx.x) < w) {
       mx[threadIdx.x] = fmaxf(mx[threadIdx.x], mx[threadIdx.x + w]);
@@ -48,42 +60,441 @@ __global__ __launch_bounds__(kBaseThreads) void base_minmax_kernel(BaseArgs a) {
     __syncthreads();
   }
   if (threadIdx.x == 0) {
-    a.range[0] = nan ? NAN : mn[0];
-    a.range[1] = mx[0];
+    a.range_part[blockIdx.x] = mn[0];
+    a.range_part[kBaseRangeBlocks + blockIdx.x] = mx[0];
+    a.range_part[2 * kBaseRangeBlocks + blockIdx.x] = bad ? 1.f : 0.f;
   }
 }
 
-// ---------------------------------------------------------------- phase start
-// every token unassigned, holders cleared; prices start at 0 in the first phase
-__global__ __launch_bounds__(kBlock) void base_reset_kernel(BaseArgs a, int first) {
+__global__ __launch_bounds__(kBaseRangeBlocks) void base_init_kernel(BaseArgs a) {
+  __shared__ float mx[kBaseRangeBlocks], mn[kBaseRangeBlocks];
+  const int t = threadIdx.x;
+  mn[t] = a.range_part[t];
+  mx[t] = a.range_part[kBaseRangeBlocks + t];
+  const int bad = __syncthreads_or(a.range_part[2 * kBaseRangeBlocks + t] != 0.f);
+  for (int w = kBaseRangeBlocks / 2; w > 0; w >>= 1) {
+    if (t < w) {
+      mx[t] = fmaxf(mx[t], mx[t + w]);
+      mn[t] = fminf(mn[t], mn[t + w]);
+    }
+    __syncthreads();
+  }
+  if (t == 0) {
+    const double spread = static_cast<double>(mx[0]) - static_cast<double>(mn[0]);
+    BaseState st{};
+    // eps: a quarter of the score range, divided by kBaseEpsStep per phase down
+    // to the range times kBaseEpsEnd (one phase when every score is equal:
+    // every balanced assignment is then optimal)
+    st.eps_end = spread > 0.0 ? spread * kBaseEpsEnd : 1.0;
+    st.eps = spread > 0.0 ? spread / 4.0 : st.eps_end;
+    st.failed = bad ? 2 : 0;
+    st.done = bad ? 1 : 0;
+    a.state[0] = st;
+    a.state[1] = st;
+    a.counts[0] = 0;
+    a.counts[1] = 0;
+  }
+}
+
+// every token unassigned, holders cleared, prices 0, no bids counted
+__global__ __launch_bounds__(kBlock) void base_reset_kernel(BaseArgs a) {
   const int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
   if (i < a.S) a.assign[i] = -1;
   if (i < a.E) {
     a.hold_n[i] = 0;
-    if (first) a.price[i] = 0.0;
+    a.bid_cnt[i] = 0;
+    a.price[i] = 0.0;
   }
 }
 
-__global__ __launch_bounds__(kWave) void base_zero_counts_kernel(int32_t* cnt, int n) {
-  if (static_cast<int>(threadIdx.x) < n) cnt[threadIdx.x] = 0;
+// ---------------------------------------------------------------- bids
+// One thread per token.  counts[r & 1] receives the number of tokens unassigned
+// at the round's start, bid_cnt[e] the bidders of expert e.
+template <bool VEC>
+__global__ __launch_bounds__(kBlock) void base_bid_kernel(BaseArgs a, int r) {
+  const BaseState st = a.state[r & 1];
+  if (st.done) return;
+  extern __shared__ double price[];  // [E], then int ecnt[E]
+  int* ecnt = reinterpret_cast<int*>(price + a.E);
+  __shared__ int nblk;
+  if (blockIdx.x == 0 && threadIdx.x == 0) a.counts[(r + 1) & 1] = 0;  // for the next round
+  for (int e = threadIdx.x; e < a.E; e += kBlock) {
+    price[e] = a.price[e];
+    ecnt[e] = 0;
+  }
+  if (threadIdx.x == 0) nblk = 0;
+  const int64_t s = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+  const bool bidder = s < a.S && a.assign[s] < 0;
+  if (s < a.S && !bidder) a.bid_e[s] = -1;
+  if (__syncthreads_or(bidder) == 0) return;  // no bidder in this block
+  if (bidder) {
+    const float* row = a.logits + s * a.E;
+    double v1 = -INFINITY, v2 = -INFINITY;
+    int e1 = 0;
+    auto take = [&](float l, int e) {
+      const double v = static_cast<double>(l) - price[e];
+      if (v > v1) {
+        v2 = v1;
+        v1 = v;
+        e1 = e;
+      } else if (v > v2) {
+        v2 = v;
+      }
+    };
+    if constexpr (VEC) {
+      const float4* r4 = reinterpret_cast<const float4*>(row);
+#pragma unroll 4
+      for (int q = 0; q < a.E / 4; ++q) {
+        const float4 l = r4[q];
+        take(l.x, 4 * q);
+        take(l.y, 4 * q + 1);
+        take(l.z, 4 * q + 2);
+        take(l.w, 4 * q + 3);
+      }
+    } else {
+      for (int e = 0; e < a.E; ++e) take(row[e], e);
+    }
+    if (a.E == 1) v2 = v1;  // one expert: bid just above its price
+    a.bid_e[s] = e1;
+    a.bid_v[s] = static_cast<double>(row[e1]) - v2 + st.eps;
+    atomicAdd(&ecnt[e1], 1);
+    atomicAdd(&nblk, 1);
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < a.E; e += kBlock)
+    if (ecnt[e] > 0) atomicAdd(&a.bid_cnt[e], ecnt[e]);
+  if (threadIdx.x == 0) atomicAdd(&a.counts[r & 1], nblk);
 }
 
-// ---------------------------------------------------------------- bids
-// One thread per token; cnt counts the tokens unassigned at the round's start.
-__global__ __launch_bounds__(kBlock) void base_bid_kernel(BaseArgs a, double eps, int32_t* cnt) {
-  extern __shared__ double price[];  // [E]
-  __shared__ int nblk;
-  for (int e = threadIdx.x; e < a.E; e += kBlock) price[e] = a.price[e];
-  if (threadIdx.x == 0) nblk = 0;
+// ---------------------------------------------------------------- resolve
+// One block per expert.  Block 0 first advances the state.  A round that began
+// with no unassigned token ends the phase: the final phase marks the auction
+// done, an earlier one lowers eps and clears holders and assignments (every
+// block takes its share).  Otherwise expert e collects its bidders in token
+// order, at most kBaseCand (later ones stay unassigned and bid again), and
+// ranks them and its holders in the order (bid desc, token asc) by counting;
+// ranks below c are kept, holders ranked c or beyond are evicted.
+__global__ __launch_bounds__(kBaseThreads) void base_resolve_kernel(BaseArgs a, int r) {
+  const BaseState st = a.state[r & 1];
+  const int e = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int n_un = st.done ? 0 : a.counts[r & 1];
+  const bool fail = !st.done && n_un > 0 && st.rounds_phase >= a.max_rounds;
+  if (e == 0 && tid == 0) {
+    BaseState nx = st;
+    if (!st.done) {
+      if (n_un == 0) {
+        if (st.eps <= st.eps_end) {
+          nx.done = 1;
+        } else {
+          nx.eps = fmax(st.eps / kBaseEpsStep, st.eps_end);
+          nx.phase = st.phase + 1;
+          nx.rounds_phase = 0;
+        }
+      } else if (fail) {
+        nx.done = 1;
+        nx.failed = 1;
+      } else {
+        nx.rounds_phase = st.rounds_phase + 1;
+        nx.rounds_total = st.rounds_total + 1;
+      }
+    }
+    a.state[(r + 1) & 1] = nx;
+  }
+  if (st.done || fail) return;
+  if (n_un == 0) {
+    if (st.eps > st.eps_end) {  // next phase: prices kept
+      if (tid == 0) a.hold_n[e] = 0;
+      for (int64_t s = static_cast<int64_t>(e) * kBaseThreads + tid; s < a.S;
+           s += static_cast<int64_t>(a.E) * kBaseThreads)
+        a.assign[s] = -1;
+    }
+    return;
+  }
+  const int nbid = a.bid_cnt[e];
+  if (nbid == 0) return;
+
+  extern __shared__ double base_lds[];
+  const int c = a.cap;
+  double* hv = base_lds;                             // holders [c]
+  double* bv = hv + c;                               // bidders [kBaseCand]
+  int* ht = reinterpret_cast<int*>(bv + kBaseCand);  // [c]
+  int* bt = ht + c;                                  // [kBaseCand]
+  __shared__ uint64_t masks[kBaseIters * kBaseWaves];
+  __shared__ int offs[kBaseIters * kBaseWaves];
+  __shared__ int pass_total;
+  const int lane = lane_id(), w = tid / kWave;
+  const int64_t base = static_cast<int64_t>(e) * c;
+  const int nh = a.hold_n[e];
+  for (int i = tid; i < nh; i += kBaseThreads) {
+    hv[i] = a.hold_v[base + i];
+    ht[i] = a.hold_t[base + i];
+  }
+  // bidders in token order: per pass kBaseIters tiles of kBaseThreads tokens;
+  // a ballot mask per (tile, wave), an exclusive scan of their counts
+  int have = 0;
+  for (int64_t p0 = 0; p0 < a.S && have < kBaseCand; p0 += static_cast<int64_t>(kBaseIters) * kBaseThreads) {
+    int be[kBaseIters];
+#pragma unroll
+    for (int i = 0; i < kBaseIters; ++i) {
+      const int64_t s = p0 + static_cast<int64_t>(i) * kBaseThreads + tid;
+      be[i] = s < a.S ? a.bid_e[s] : -1;
+    }
+#pragma unroll
+    for (int i = 0; i < kBaseIters; ++i) {
+      const uint64_t m = __ballot(be[i] == e);
+      if (lane == 0) masks[i * kBaseWaves + w] = m;
+    }
+    __syncthreads();
+    if (w == 0) {  // exclusive scan of kBaseIters * kBaseWaves counts, 8 per lane
+      constexpr int kPer = kBaseIters * kBaseWaves / kWave;
+      int cnt[kPer], sum = 0;
+#pragma unroll
+      for (int j = 0; j < kPer; ++j) {
+        cnt[j] = __popcll(masks[lane * kPer + j]);
+        sum += cnt[j];
+      }
+      int incl = sum;
+#pragma unroll
+      for (int off = 1; off < kWave; off <<= 1) {
+        const int y = __shfl_up(incl, off, kWave);
+        if (lane >= off) incl += y;
+      }
+      int run = incl - sum;
+#pragma unroll
+      for (int j = 0; j < kPer; ++j) {
+        offs[lane * kPer + j] = run;
+        run += cnt[j];
+      }
+      if (lane == kWave - 1) pass_total = incl;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < kBaseIters; ++i) {
+      if (be[i] == e) {
+        const int k = i * kBaseWaves + w;
+        const int pos = have + offs[k] + popc_below(masks[k]);
+        if (pos < kBaseCand) {
+          const int64_t s = p0 + static_cast<int64_t>(i) * kBaseThreads + tid;
+          bv[pos] = a.bid_v[s];
+          bt[pos] = static_cast<int>(s);
+        }
+      }
+    }
+    have += pass_total;  // uniform
+    __syncthreads();     // masks and offs are reused by the next pass
+  }
+  const int nb = min(have, kBaseCand);
+  if (tid == 0) a.bid_cnt[e] = 0;  // for the next round (every thread has read it)
+  // ranks in the union of holders (sorted) and bidders (unsorted)
+  for (int i = tid; i < nh; i += kBaseThreads) {
+    const double v = hv[i];
+    const int t = ht[i];
+    int r_ = i;
+    for (int j = 0; j < nb; ++j) r_ += base_before(bv[j], bt[j], v, t);
+    if (r_ < c) {
+      a.hold_v[base + r_] = v;
+      a.hold_t[base + r_] = t;
+      if (r_ == c - 1) a.price[e] = v;
+    } else {
+      a.assign[t] = -1;  // evicted
+    }
+  }
+  for (int j = tid; j < nb; j += kBaseThreads) {
+    const double v = bv[j];
+    const int t = bt[j];
+    int r_ = 0;
+    for (int q = 0; q < nb; ++q) r_ += base_before(bv[q], bt[q], v, t);
+    int lo = 0, hi = nh;  // holders ahead of bidder j
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (base_before(hv[mid], ht[mid], v, t)) lo = mid + 1;
+      else hi = mid;
+    }
+    r_ += lo;
+    if (r_ < c) {
+      a.hold_v[base + r_] = v;
+      a.hold_t[base + r_] = t;
+      a.assign[t] = e;
+      if (r_ == c - 1) a.price[e] = v;
+    }
+  }
+  if (tid == 0) a.hold_n[e] = min(c, nh + nb);
+}
+
+// ---------------------------------------------------------------- tail
+// Most rounds of a phase have a handful of bidders.  Once at most kBaseTail
+// tokens are unassigned after a round, one workgroup runs the following rounds
+// itself, with the same arithmetic and the same rule (the union of holders and
+// bidders ranked in the order (bid desc, token asc), ranks below c kept), until
+// the phase has no unassigned token or more than kBaseTail of them; the next
+// bid / resolve pair then carries on.  Prices and holder counts live in LDS
+// meanwhile; holders stay sorted in device memory.  The order of the tokens in
+// the unassigned list does not matter: every bid depends on its token alone and
+// ranking uses a total order.
+__global__ __launch_bounds__(kBaseThreads) void base_tail_kernel(BaseArgs a, int r) {
+  BaseState* sp = a.state + ((r + 1) & 1);
+  if (sp->done) return;
+  const double eps = sp->eps;
+  int rounds_phase = sp->rounds_phase, rounds_total = sp->rounds_total, failed = 0;
+  extern __shared__ double tail_lds[];
+  const int c = a.cap, E = a.E;
+  double* pr = tail_lds;                              // prices [E]
+  double* hvs = pr + E;                               // one expert's holder bids [c] (one-bidder rounds)
+  int* hn = reinterpret_cast<int*>(hvs + c);          // holder counts [E]
+  int* hts = hn + E;                                  // the holders' tokens [c]
+  __shared__ int U[kBaseTail], U2[kBaseTail];
+  __shared__ int bex[kBaseTail], kr[kBaseTail], nbe[kBaseTail], pos[kBaseTail], rk[kBaseTail];
+  __shared__ double bvv[kBaseTail];
+  __shared__ int pref[kBaseTail + 1];
+  __shared__ int nU, nU2, fast_rounds, fast_fail;
+  const int tid = threadIdx.x, lane = lane_id(), w = tid / kWave;
+  if (tid == 0) nU = 0;
   __syncthreads();
-  const int64_t s = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
-  if (s < a.S) {
-    if (a.assign[s] < 0) {
-      const float* row = a.logits + s * a.E;
+  // unassigned tokens (any order)
+  for (int64_t s0 = 0; s0 < a.S; s0 += 8 * kBaseThreads) {
+    int v[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int64_t s = s0 + q * kBaseThreads + tid;
+      v[q] = s < a.S ? a.assign[s] : 0;
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q)
+      if (v[q] < 0) {
+        const int p = atomicAdd(&nU, 1);
+        if (p < kBaseTail) U[p] = static_cast<int>(s0 + q * kBaseThreads + tid);
+      }
+  }
+  __syncthreads();
+  if (nU == 0 || nU > kBaseTail) return;  // uniform
+  for (int e = tid; e < E; e += kBaseThreads) {
+    pr[e] = a.price[e];
+    hn[e] = a.hold_n[e];
+  }
+  __syncthreads();
+  for (;;) {
+    const int n = nU;  // uniform (read after a barrier)
+    if (n == 0 || n > kBaseTail) break;
+    if (rounds_phase >= a.max_rounds) {
+      failed = 1;
+      break;
+    }
+    if (n == 1) {
+      // One bidder: it always wins a place (its bid exceeds its expert's
+      // price, the c-th best bid) and pushes out at most one holder, who bids
+      // next.  Wave 0 follows the chain: bid (lanes over experts, an exact
+      // arg-max with the lower expert on ties and the best other value), the
+      // holders ahead of it (lanes over holders, staged in LDS), then the
+      // holders behind it move up by one.
+      if (w == 0) {
+        int t = U[0];
+        int k = 0, fl = 0;
+        for (;;) {
+          if (rounds_phase + k >= a.max_rounds) {
+            fl = 1;
+            break;
+          }
+          const float* row = a.logits + static_cast<int64_t>(t) * E;
+          double v1 = -INFINITY, v2 = -INFINITY, l1 = 0.0;
+          int e1 = 0x7fffffff;
+          for (int e = lane; e < E; e += kWave) {
+            const float l = row[e];
+            const double v = static_cast<double>(l) - pr[e];
+            if (v > v1) {
+              v2 = v1;
+              v1 = v;
+              e1 = e;
+              l1 = static_cast<double>(l);
+            } else if (v > v2) {
+              v2 = v;
+            }
+          }
+#pragma unroll
+          for (int off = 1; off < kWave; off <<= 1) {
+            const double ov1 = __shfl_xor(v1, off, kWave), ov2 = __shfl_xor(v2, off, kWave);
+            const double ol1 = __shfl_xor(l1, off, kWave);
+            const int oe1 = __shfl_xor(e1, off, kWave);
+            if (ov1 > v1 || (ov1 == v1 && oe1 < e1)) {
+              v2 = fmax(ov2, v1);
+              v1 = ov1;
+              e1 = oe1;
+              l1 = ol1;
+            } else {
+              v2 = fmax(v2, ov1);
+            }
+          }
+          if (E == 1) v2 = v1;
+          const double bid = l1 - v2 + eps;
+          const int nh = hn[e1];
+          const int64_t base = static_cast<int64_t>(e1) * c;
+          int p = 0;
+          for (int i = lane; i < nh; i += kWave) {
+            const double hv = a.hold_v[base + i];
+            const int ht = a.hold_t[base + i];
+            hvs[i] = hv;
+            hts[i] = ht;
+            p += base_before(hv, ht, bid, t);
+          }
+#pragma unroll
+          for (int off = 32; off >= 1; off >>= 1) p += __shfl_xor(p, off, kWave);
+          __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+          __builtin_amdgcn_wave_barrier();
+          __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+          if (p >= c) {  // cannot happen (see above); stop rather than loop
+            fl = 1;
+            break;
+          }
+          const int evicted = nh == c ? hts[c - 1] : -1;
+          for (int i = p + lane; i < min(nh, c - 1); i += kWave) {
+            a.hold_v[base + i + 1] = hvs[i];
+            a.hold_t[base + i + 1] = hts[i];
+          }
+          if (lane == 0) {
+            a.hold_v[base + p] = bid;
+            a.hold_t[base + p] = t;
+            a.assign[t] = e1;
+            if (evicted >= 0) a.assign[evicted] = -1;
+            const int nn = min(c, nh + 1);
+            if (nn == c) pr[e1] = p == c - 1 ? bid : hvs[c - 2];
+            hn[e1] = nn;
+          }
+          ++k;
+          // stores and LDS updates visible to the whole wave before the next step
+          __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+          __builtin_amdgcn_wave_barrier();
+          __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+          if (evicted < 0) {
+            t = -1;
+            break;
+          }
+          t = evicted;
+        }
+        if (lane == 0) {
+          U[0] = t;
+          nU = t >= 0 ? 1 : 0;
+          fast_rounds = k;
+          fast_fail = fl;
+        }
+      }
+      __syncthreads();
+      rounds_phase += fast_rounds;
+      rounds_total += fast_rounds;
+      if (fast_fail) {
+        failed = 1;
+        break;
+      }
+      __syncthreads();  // fast_rounds and fast_fail are rewritten by a later chain
+      continue;
+    }
+    // bids, as in base_bid_kernel
+    if (tid < n) {
+      const int t = U[tid];
+      const float* row = a.logits + static_cast<int64_t>(t) * E;
       double v1 = -INFINITY, v2 = -INFINITY;
       int e1 = 0;
-      for (int e = 0; e < a.E; ++e) {
-        const double v = static_cast<double>(row[e]) - price[e];
+      for (int e = 0; e < E; ++e) {
+        const double v = static_cast<double>(row[e]) - pr[e];
         if (v > v1) {
           v2 = v1;
           v1 = v;
@@ -92,135 +503,135 @@ __global__ __launch_bounds__(kBlock) void base_bid_kernel(BaseArgs a, double eps
           v2 = v;
         }
       }
-      if (a.E == 1) v2 = v1;  // one expert: bid just above its price
-      a.bid_e[s] = e1;
-      a.bid_v[s] = static_cast<double>(row[e1]) - v2 + eps;
-      atomicAdd(&nblk, 1);
-    } else {
-      a.bid_e[s] = -1;
+      if (E == 1) v2 = v1;
+      bex[tid] = e1;
+      bvv[tid] = static_cast<double>(row[e1]) - v2 + eps;
     }
-  }
-  __syncthreads();
-  if (threadIdx.x == 0 && nblk > 0) atomicAdd(cnt, nblk);
-}
-
-// ---------------------------------------------------------------- resolve
-// n a power of two, at most 2 * kBaseThreads: sorted into (bid desc, token asc)
-__device__ __forceinline__ void base_sort(double* v, int* t, int n) {
-  for (int size = 2; size <= n; size <<= 1) {
-    for (int stride = size / 2; stride > 0; stride >>= 1) {
-      const int i = threadIdx.x;
-      if (i < n / 2) {
-        const int lo = 2 * i - (i & (stride - 1));
-        const int hi = lo + stride;
-        const bool desc = (lo & size) == 0 || size == n;
-        const bool swap = desc ? base_before(v[hi], t[hi], v[lo], t[lo]) : base_before(v[lo], t[lo], v[hi], t[hi]);
-        if (swap) {
-          const double tv = v[lo];
-          v[lo] = v[hi];
-          v[hi] = tv;
-          const int tt = t[lo];
-          t[lo] = t[hi];
-          t[hi] = tt;
+    if (tid == 0) nU2 = 0;
+    __syncthreads();
+    // kr: bidders of the same expert ahead of this one; nbe: bidders of its expert
+    if (tid < n) {
+      const int e = bex[tid];
+      const double v = bvv[tid];
+      const int t = U[tid];
+      int k = 0, m = 0;
+      for (int q = 0; q < n; ++q) {
+        const bool same = bex[q] == e;
+        m += same;
+        k += same && base_before(bvv[q], U[q], v, t);
+      }
+      kr[tid] = k;
+      nbe[tid] = m;
+    }
+    // pos: holders ahead of each bidder, one wave per bidder
+    for (int j = w; j < n; j += kBaseWaves) {
+      const int e = bex[j];
+      const double v = bvv[j];
+      const int t = U[j];
+      const int64_t base = static_cast<int64_t>(e) * c;
+      int cnt = 0;
+      const int nh = hn[e];
+#pragma unroll 4
+      for (int i = lane; i < nh; i += kWave) cnt += base_before(a.hold_v[base + i], a.hold_t[base + i], v, t);
+#pragma unroll
+      for (int off = 32; off >= 1; off >>= 1) cnt += __shfl_xor(cnt, off, kWave);
+      if (lane == 0) pos[j] = cnt;
+    }
+    __syncthreads();
+    if (tid < n) rk[tid] = kr[tid] + pos[tid];
+    if (w == 0) {  // moving holders: from the best bidder's position to the end, per expert
+      const int len = lane < n && kr[lane] == 0 ? hn[bex[lane]] - pos[lane] : 0;
+      int incl = len;
+#pragma unroll
+      for (int off = 1; off < kWave; off <<= 1) {
+        const int y = __shfl_up(incl, off, kWave);
+        if (lane >= off) incl += y;
+      }
+      if (lane < n) pref[lane + 1] = incl;
+      if (lane == 0) pref[0] = 0;
+    }
+    __syncthreads();
+    const int M = pref[n];
+    // chunks from the last: a holder only moves to a higher position
+    for (int ch = (M - 1) / kBaseThreads; ch >= 0 && M > 0; --ch) {
+      const int k = ch * kBaseThreads + tid;
+      const bool item = k < M;
+      int e = 0, nr = 0, t = 0;
+      double v = 0.0;
+      if (item) {
+        int lo = 0, hi = n;  // the j with pref[j] <= k < pref[j + 1]
+        while (lo < hi) {
+          const int mid = (lo + hi) >> 1;
+          if (pref[mid + 1] <= k) lo = mid + 1;
+          else hi = mid;
+        }
+        e = bex[lo];
+        const int i = pos[lo] + (k - pref[lo]);
+        const int64_t at = static_cast<int64_t>(e) * c + i;
+        v = a.hold_v[at];
+        t = a.hold_t[at];
+        int cnt = 0;
+        for (int q = 0; q < n; ++q) cnt += bex[q] == e && base_before(bvv[q], U[q], v, t);
+        nr = i + cnt;
+      }
+      __syncthreads();
+      if (item) {
+        if (nr < c) {
+          const int64_t at = static_cast<int64_t>(e) * c + nr;
+          a.hold_v[at] = v;
+          a.hold_t[at] = t;
+          if (nr == c - 1) pr[e] = v;
+        } else {
+          a.assign[t] = -1;  // evicted
+          const int p = atomicAdd(&nU2, 1);
+          if (p < kBaseTail) U2[p] = t;
         }
       }
       __syncthreads();
     }
-  }
-}
-
-// One block per expert.  Bidders are collected in token order, at most
-// kBaseCand per round (later ones stay unassigned and bid again), sorted, and
-// merged with the sorted holders by rank; ranks below c survive.
-__global__ __launch_bounds__(kBaseThreads) void base_resolve_kernel(BaseArgs a) {
-  extern __shared__ double base_lds[];
-  const int c = a.cap;
-  double* hv = base_lds;                            // holders [c]
-  double* bv = hv + c;                              // bidders [kBaseCand]
-  int* ht = reinterpret_cast<int*>(bv + kBaseCand); // [c]
-  int* bt = ht + c;                                 // [kBaseCand]
-  __shared__ int wave_cnt[kBaseThreads / kWave];
-  __shared__ int nb_total;
-  const int e = blockIdx.x;
-  const int64_t base = static_cast<int64_t>(e) * c;
-  const int nh = a.hold_n[e];
-  for (int i = threadIdx.x; i < nh; i += kBaseThreads) {
-    hv[i] = a.hold_v[base + i];
-    ht[i] = a.hold_t[base + i];
-  }
-  if (threadIdx.x == 0) nb_total = 0;
-  __syncthreads();
-  const int lane = lane_id(), w = threadIdx.x / kWave;
-  for (int64_t s0 = 0; s0 < a.S; s0 += kBaseThreads) {
-    const int have = nb_total;  // uniform: written before the last barrier
-    if (have >= kBaseCand) break;
-    const int64_t s = s0 + threadIdx.x;
-    const bool mine = s < a.S && a.bid_e[s] == e;
-    const uint64_t ballot = __ballot(mine);
-    if (lane == 0) wave_cnt[w] = __popcll(ballot);
-    __syncthreads();
-    int before = 0;
-    for (int i = 0; i < w; ++i) before += wave_cnt[i];
-    const int pos = have + before + popc_below(ballot);
-    if (mine && pos < kBaseCand) {
-      bv[pos] = a.bid_v[s];
-      bt[pos] = static_cast<int>(s);
+    if (tid < n) {
+      const int e = bex[tid];
+      const int t = U[tid];
+      if (rk[tid] < c) {
+        const int64_t at = static_cast<int64_t>(e) * c + rk[tid];
+        a.hold_v[at] = bvv[tid];
+        a.hold_t[at] = t;
+        a.assign[t] = e;
+        if (rk[tid] == c - 1) pr[e] = bvv[tid];
+      } else {
+        const int p = atomicAdd(&nU2, 1);
+        if (p < kBaseTail) U2[p] = t;
+      }
+      if (kr[tid] == 0) hn[e] = min(c, hn[e] + nbe[tid]);
     }
-    int tot = 0;
-    for (int i = 0; i < kBaseThreads / kWave; ++i) tot += wave_cnt[i];
     __syncthreads();
-    if (threadIdx.x == 0) nb_total = min(kBaseCand, have + tot);
+    const int n2 = nU2;
+    if (tid < min(n2, kBaseTail)) U[tid] = U2[tid];
+    if (tid == 0) nU = n2;
+    rounds_phase += 1;
+    rounds_total += 1;
     __syncthreads();
   }
-  const int nb = nb_total;
-  if (nb == 0) return;  // uniform: nothing changes for this expert
-  int np2 = 1;
-  while (np2 < nb) np2 <<= 1;
-  for (int i = nb + threadIdx.x; i < np2; i += kBaseThreads) {
-    bv[i] = -INFINITY;
-    bt[i] = 0x7fffffff;
+  for (int e = tid; e < E; e += kBaseThreads) {
+    a.price[e] = pr[e];
+    a.hold_n[e] = hn[e];
   }
-  __syncthreads();
-  base_sort(bv, bt, np2);
-  // rank of each entry in the union of the two sorted, disjoint lists
-  for (int i = threadIdx.x; i < nh; i += kBaseThreads) {
-    int lo = 0, hi = nb;  // bidders ahead of holder i
-    while (lo < hi) {
-      const int mid = (lo + hi) >> 1;
-      if (base_before(bv[mid], bt[mid], hv[i], ht[i])) lo = mid + 1;
-      else hi = mid;
-    }
-    const int r = i + lo;
-    if (r < c) {
-      a.hold_v[base + r] = hv[i];
-      a.hold_t[base + r] = ht[i];
-      if (r == c - 1) a.price[e] = hv[i];
-    } else {
-      a.assign[ht[i]] = -1;  // evicted
+  if (tid == 0) {
+    sp->rounds_phase = rounds_phase;
+    sp->rounds_total = rounds_total;
+    if (failed) {
+      sp->done = 1;
+      sp->failed = 1;
     }
   }
-  for (int j = threadIdx.x; j < nb; j += kBaseThreads) {
-    int lo = 0, hi = nh;  // holders ahead of bidder j
-    while (lo < hi) {
-      const int mid = (lo + hi) >> 1;
-      if (base_before(hv[mid], ht[mid], bv[j], bt[j])) lo = mid + 1;
-      else hi = mid;
-    }
-    const int r = j + lo;
-    if (r < c) {
-      a.hold_v[base + r] = bv[j];
-      a.hold_t[base + r] = bt[j];
-      a.assign[bt[j]] = e;
-      if (r == c - 1) a.price[e] = bv[j];
-    }
-  }
-  if (threadIdx.x == 0) a.hold_n[e] = min(c, nh + nb);
 }
 
 // ---------------------------------------------------------------- outputs
 // ids, weights (sigmoid of the score) and the wave-block histogram [E, nb]
 // that the scan and assign kernels turn into slots
-__global__ __launch_bounds__(kBlock) void base_finish_kernel(BaseArgs a) {
+__global__ __launch_bounds__(kBlock) void base_finish_kernel(BaseArgs a, int r) {
+  const BaseState st = a.state[r & 1];
+  if (!st.done || st.failed) return;
   extern __shared__ int hist_lds[];  // [kWavesPerBlock, E]
   const int tid = threadIdx.x;
   const int w = tid / kWave;
@@ -251,54 +662,44 @@ hipError_t run_base_auction(const BaseArgs& a, hipStream_t st, BaseStats* stats)
   *stats = BaseStats{};
   if (a.S == 0) return hipSuccess;
   const unsigned tok_blocks = static_cast<unsigned>((a.S + kBlock - 1) / kBlock);
-  base_minmax_kernel<<<1, kBaseThreads, 0, st>>>(a);
+  const size_t bid_lds = static_cast<size_t>(a.E) * (sizeof(double) + sizeof(int));
+  const size_t tail_lds = static_cast<size_t>(a.E + a.cap) * (sizeof(double) + sizeof(int));
+  const bool vec = a.E % 4 == 0 && reinterpret_cast<uintptr_t>(a.logits) % 16 == 0;
+  base_range_kernel<<<kBaseRangeBlocks, kBaseThreads, 0, st>>>(a);
+  base_init_kernel<<<1, kBaseRangeBlocks, 0, st>>>(a);
+  base_reset_kernel<<<tok_blocks, kBlock, 0, st>>>(a);
   if ((err = hipGetLastError()) != hipSuccess) return err;
-  float range[2] = {0.f, 0.f};
-  if ((err = hipMemcpyAsync(range, a.range, sizeof(range), hipMemcpyDeviceToHost, st)) != hipSuccess) return err;
-  if ((err = hipStreamSynchronize(st)) != hipSuccess) return err;
-  const double spread = static_cast<double>(range[1]) - static_cast<double>(range[0]);
-  if (!(spread < INFINITY)) {  // inf or nan among the scores
-    stats->bad_scores = 1;
-    return hipSuccess;
-  }
-  // eps: a quarter of the score range, divided by kBaseEpsStep per phase down
-  // to the range times kBaseEpsEnd (one phase when every score is equal: every
-  // balanced assignment is then optimal)
-  const double eps_end = spread > 0.0 ? spread * kBaseEpsEnd : 1.0;
-  double eps = spread > 0.0 ? spread / 4.0 : eps_end;
-  constexpr int kBatch = 8;  // rounds between reads of the unassigned counts
+  // the device ends the auction within (max_rounds + 1) rounds per phase; the
+  // phases are at most 2 + log_8(2^30 / 4) < 12
+  const int64_t limit = static_cast<int64_t>(a.max_rounds + 1) * 12 + 1;
+  int r = 0;
+  int batch = 64;
+  BaseState host{};
   for (;;) {
-    base_reset_kernel<<<tok_blocks, kBlock, 0, st>>>(a, stats->phases == 0);
-    int rounds = 0;
-    bool done = false;
-    while (!done) {
-      base_zero_counts_kernel<<<1, kWave, 0, st>>>(a.counts, kBatch);
-      for (int r = 0; r < kBatch; ++r) {
-        base_bid_kernel<<<tok_blocks, kBlock, static_cast<size_t>(a.E) * sizeof(double), st>>>(a, eps, a.counts + r);
-        base_resolve_kernel<<<static_cast<unsigned>(a.E), kBaseThreads, base_resolve_lds(a.cap), st>>>(a);
-      }
-      if ((err = hipGetLastError()) != hipSuccess) return err;
-      int32_t cnt[kBatch];
-      if ((err = hipMemcpyAsync(cnt, a.counts, sizeof(cnt), hipMemcpyDeviceToHost, st)) != hipSuccess) return err;
-      if ((err = hipStreamSynchronize(st)) != hipSuccess) return err;
-      // a round that began with no unassigned token ends the phase
-      for (int r = 0; r < kBatch && !done; ++r) {
-        if (cnt[r] == 0) done = true;
-        else ++rounds;
-      }
-      if (!done && rounds >= a.max_rounds) {
-        stats->rounds += rounds;
-        stats->not_converged = 1;
-        return hipSuccess;
-      }
+    for (int i = 0; i < batch; ++i, ++r) {
+      if (vec) base_bid_kernel<true><<<tok_blocks, kBlock, bid_lds, st>>>(a, r);
+      else base_bid_kernel<false><<<tok_blocks, kBlock, bid_lds, st>>>(a, r);
+      base_resolve_kernel<<<static_cast<unsigned>(a.E), kBaseThreads, base_resolve_lds(a.cap), st>>>(a, r);
+      base_tail_kernel<<<1, kBaseThreads, tail_lds, st>>>(a, r);
     }
-    stats->rounds += rounds;
-    stats->phases += 1;
-    stats->eps = eps;
-    if (eps <= eps_end) break;
-    eps = fmax(eps / kBaseEpsStep, eps_end);
+    if ((err = hipGetLastError()) != hipSuccess) return err;
+    if ((err = hipMemcpyAsync(&host, a.state + (r & 1), sizeof(host), hipMemcpyDeviceToHost, st)) != hipSuccess)
+      return err;
+    if ((err = hipStreamSynchronize(st)) != hipSuccess) return err;
+    if (host.done) break;
+    if (r >= limit) {
+      host.failed = 1;
+      break;
+    }
+    batch = 128;
   }
-  base_finish_kernel<<<tok_blocks, kBlock, static_cast<size_t>(kWavesPerBlock) * a.E * sizeof(int), st>>>(a);
+  stats->phases = host.phase + 1;
+  stats->rounds = host.rounds_total;
+  stats->eps = host.eps;
+  stats->not_converged = host.failed == 1;
+  stats->bad_scores = host.failed == 2;
+  if (host.failed) return hipSuccess;
+  base_finish_kernel<<<tok_blocks, kBlock, static_cast<size_t>(kWavesPerBlock) * a.E * sizeof(int), st>>>(a, r);
   return hipGetLastError();
 }
 

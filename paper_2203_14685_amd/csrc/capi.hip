@@ -225,29 +225,31 @@ moe_status check_base_params(const moe_base_params* p) {
 }
 
 // Workspace of moe_base_gate, each piece 256-byte aligned: hist int32 [E, nb];
-// logits fp32 [S, E] (only when projected and not returned); price fp64 [E];
-// hold_v fp64 [S]; hold_t, assign, bid_e int32 [S]; bid_v fp64 [S];
-// hold_n int32 [E]; counts int32 [8]; range fp32 [2].
+// logits fp32 [S, E] (only when projected); price fp64 [E]; hold_v fp64 [S];
+// hold_t, assign, bid_e int32 [S]; bid_v fp64 [S]; hold_n, bid_cnt int32 [E];
+// counts int32 [2]; the auction state [2]; range partials fp32 [3, 256].
 struct BasePlan {
   size_t off_hist, off_logits, off_price, off_hold_v, off_hold_t, off_hold_n, off_assign, off_bid_e, off_bid_v,
-      off_counts, off_range, total;
+      off_bid_cnt, off_counts, off_state, off_range, total;
 };
 
 BasePlan plan_base(const moe_base_params* p, bool own_logits) {
   BasePlan b{};
   const size_t S = static_cast<size_t>(p->S), E = static_cast<size_t>(p->E);
   size_t off = 0;
-  b.off_hist = off;   off += align256(static_cast<size_t>(hist_blocks(p->S)) * E * 4);
-  b.off_logits = off; off += own_logits ? align256(S * E * 4) : 0;
-  b.off_price = off;  off += align256(E * 8);
-  b.off_hold_v = off; off += align256(S * 8);
-  b.off_hold_t = off; off += align256(S * 4);
-  b.off_hold_n = off; off += align256(E * 4);
-  b.off_assign = off; off += align256(S * 4);
-  b.off_bid_e = off;  off += align256(S * 4);
-  b.off_bid_v = off;  off += align256(S * 8);
-  b.off_counts = off; off += align256(8 * 4);
-  b.off_range = off;  off += align256(2 * 4);
+  b.off_hist = off;    off += align256(static_cast<size_t>(hist_blocks(p->S)) * E * 4);
+  b.off_logits = off;  off += own_logits ? align256(S * E * 4) : 0;
+  b.off_price = off;   off += align256(E * 8);
+  b.off_hold_v = off;  off += align256(S * 8);
+  b.off_hold_t = off;  off += align256(S * 4);
+  b.off_hold_n = off;  off += align256(E * 4);
+  b.off_assign = off;  off += align256(S * 4);
+  b.off_bid_e = off;   off += align256(S * 4);
+  b.off_bid_v = off;   off += align256(S * 8);
+  b.off_bid_cnt = off; off += align256(E * 4);
+  b.off_counts = off;  off += align256(2 * 4);
+  b.off_state = off;   off += align256(2 * sizeof(BaseState));
+  b.off_range = off;   off += align256(3 * kBaseRangeBlocks * sizeof(float));
   b.total = off;
   return b;
 }
@@ -618,8 +620,10 @@ moe_status moe_base_gate(const moe_base_params* p, const void* x, const void* wg
   a.assign = reinterpret_cast<int32_t*>(ws + b.off_assign);
   a.bid_e = reinterpret_cast<int32_t*>(ws + b.off_bid_e);
   a.bid_v = reinterpret_cast<double*>(ws + b.off_bid_v);
+  a.bid_cnt = reinterpret_cast<int32_t*>(ws + b.off_bid_cnt);
   a.counts = reinterpret_cast<int32_t*>(ws + b.off_counts);
-  a.range = reinterpret_cast<float*>(ws + b.off_range);
+  a.state = reinterpret_cast<BaseState*>(ws + b.off_state);
+  a.range_part = reinterpret_cast<float*>(ws + b.off_range);
   a.ids = ids; a.weights = weights; a.hist = hist;
   BaseStats stats{};
   err = run_base_auction(a, stream, &stats);

@@ -128,6 +128,17 @@ constexpr int kBaseCand = 2048;          // bidders an expert considers per roun
 constexpr int kBaseMaxCap = 2048;        // largest S / E
 constexpr double kBaseEpsStep = 8.0;     // eps divisor between phases
 constexpr double kBaseEpsEnd = 0x1p-30;  // final eps, relative to the score range
+constexpr int kBaseRangeBlocks = 256;    // blocks of the score-range reduction
+constexpr int kBaseTail = 64;            // rounds with at most this many bidders run in one workgroup
+
+// Auction control, double-buffered by round parity (device memory).
+struct BaseState {
+  double eps, eps_end;     // eps of the current phase, of the last phase
+  int phase, rounds_phase, rounds_total;
+  int done;                // the auction has ended (converged or failed)
+  int failed;              // 1: a phase reached max_rounds; 2: a score is NaN or infinite
+  int pad;
+};
 
 struct BaseArgs {
   int S, E, cap, nb;       // nb: 64-token wave blocks
@@ -140,8 +151,10 @@ struct BaseArgs {
   int32_t* assign;         // [S] expert of each token, -1 = unassigned
   int32_t* bid_e;          // [S] expert bid for this round, -1 = none
   double* bid_v;           // [S]
-  int32_t* counts;         // [8] unassigned tokens at the start of each round of a batch
-  float* range;            // [2] min and max score
+  int32_t* bid_cnt;        // [E] bidders of each expert this round
+  int32_t* counts;         // [2] unassigned tokens at the start of a round, by round parity
+  BaseState* state;        // [2]
+  float* range_part;       // [3, kBaseRangeBlocks] per-block min, max, NaN/inf flag
   int32_t* ids;            // [S]
   float* weights;          // [S]
   int32_t* hist;           // [E, nb]

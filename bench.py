@@ -402,6 +402,34 @@ def main():
         gates["dense_to_sparse"] = {"ms": round(ms, 5), "temperature": 0.5, "alg_bytes": b,
                                     "GB/s": round(b / (ms * 1e-3) / 1e9, 1)}
         del noise
+        if S % E == 0 and S // E <= 2048:
+            # BASE layer: balanced assignment by the auction (each call
+            # synchronizes its stream); bound by the latency of its rounds
+            cb_ = S // E
+            bpp = hm.base_params(S, d, E, cb_, 0, dcode)
+            bws = torch.empty((hm.moe_base_gate_workspace_size(bpp),), dtype=torch.uint8, device=dev)
+            bo = [torch.empty((S,), dtype=torch.int32, device=dev), torch.empty((S,), dtype=torch.int32, device=dev),
+                  torch.empty((S,), dtype=torch.float32, device=dev), torch.empty((E,), dtype=torch.int32, device=dev),
+                  torch.empty((E, cb_), dtype=torch.int32, device=dev)]
+            info = hm.BaseInfo()
+
+            def bcall():
+                hm.moe_base_gate(bpp, x, wg, bias, None, bo[0], bo[1], bo[2], bo[3], bo[4], bws, info, stream)
+            bcall()
+            nb_calls = max(1, min(args.steps, 10))
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record(stream)
+            for _ in range(nb_calls):
+                bcall()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ms = e0.elapsed_time(e1) / nb_calls
+            gates["base"] = {"ms": round(ms, 4), "phases": info.phases, "rounds": info.rounds,
+                             "us_per_round": round(ms * 1e3 / max(1, info.rounds), 2), "eps": info.eps,
+                             "optimality_bound": S * info.eps, "bound": "latency",
+                             "what": "moe_base_gate: projection, eps-scaling auction, slots"}
+            del bws, bo
     else:
         ranks = np.arange(1, w["vocab"] + 1, dtype=np.float64)
         pz = ranks ** -w["zipf_a"]

@@ -100,6 +100,59 @@ def summarize_pmc(args):
         print(f"{op}: {total / 1e6:.1f} MB per launch -> {traffic_path(w['name'], op)}")
 
 
+MFMA_KERNELS = (("route_mfma", "projection x.W", 1), ("dwg_mfma_kernel", "gate backward dW = x^T.dL", 3),
+                ("dx_mfma_kernel", "gate backward dx = dL.W^T", 3))
+
+
+def summarize_mfma(args):
+    """Matrix-core evidence from one rocprofv3 --pmc run (MfmaUtil, MfmaFlopsBF16,
+    GRBM_GUI_ACTIVE per dispatch): for each matrix-core kernel of this workload,
+    the busy share of the matrix units and the bf16 MFMA flops counted per launch
+    against the algorithmic 2*S*d*E (the gate backward runs three bf16 planes of
+    dL, so three times that)."""
+    import csv
+    import glob
+    from paper_2203_14685_amd import workloads as wl
+    w = wl.WORKLOADS[args.workload]
+    rows = []
+    for f in glob.glob(os.path.join(args.summarize_mfma, "**", "*counter_collection.csv"), recursive=True):
+        with open(f) as fh:
+            rows += list(csv.DictReader(fh))
+    if not rows:
+        raise SystemExit(f"no counter rows under {args.summarize_mfma}")
+    alg = 2 * w["S"] * w["d"] * w["E"]
+    path = os.path.join(ROOT, "profiles", f"mfma_{w['name']}.txt")
+    lines = [f"# matrix-core use per launch, workload {w['name']}",
+             "# from one rocprofv3 counter run (TMPDIR=/tmp, from /tmp, repo at $R):",
+             f"#   rocprofv3 --pmc MfmaUtil MfmaFlopsBF16 GRBM_GUI_ACTIVE --output-format csv -d <dir> -- python3 "
+             f"$R/bench.py --workload {args.workload} --steps 3 --warmup 1 --no-cpu-baseline --no-base",
+             "# MfmaUtil = matrix-unit busy cycles summed over SIMDs / (GPU active cycles x SIMDs) x 100;",
+             "# MfmaFlopsBF16 = bf16 MFMA operations x 512 (flops counted by the hardware)",
+             f"# algorithmic flops of one projection 2*S*d*E = {alg}",
+             "%-34s %-28s %8s %10s %16s %12s" % ("kernel", "computes", "launches", "mfma_util%", "mfma_flops",
+                                                 "flops/alg")]
+    found = 0
+    for frag, what, mult in MFMA_KERNELS:
+        sel = [r for r in rows if frag in r["Kernel_Name"]]
+        if not sel:
+            continue
+        by = {}
+        for r in sel:
+            by.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+        util = by.get("MfmaUtil", [float("nan")])
+        flops = by.get("MfmaFlopsBF16", [float("nan")])
+        name = sel[0]["Kernel_Name"].split("(")[0].replace("hetumoe::", "").replace("void ", "")
+        fl = sum(flops) / len(flops)
+        lines.append("%-34s %-28s %8d %10.2f %16.0f %12.4f" % (name[:34], what[:28], len(util), sum(util) / len(util),
+                                                               fl, fl / (alg * mult)))
+        found += 1
+    if not found:
+        raise SystemExit("no matrix-core kernel in the counter rows")
+    with open(path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -112,6 +165,14 @@ def parse():
                          "eager pass with events)")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                     help="write profiles/traffic_*.txt from two rocprofv3 --pmc output folders and exit")
+    ap.add_argument("--summarize-mfma", metavar="DIR",
+                    help="write profiles/mfma_<workload>.txt from a rocprofv3 --pmc MfmaUtil MfmaFlopsBF16 "
+                         "GRBM_GUI_ACTIVE output folder and exit")
+    ap.add_argument("--no-base", action="store_true",
+                    help="skip the BASE-layer timing (thousands of small launches; for counter runs)")
+    ap.add_argument("--cold-iters", type=int, default=10,
+                    help="per-op timings from a cold cache: launches of each op, each after reading a 1 GiB "
+                         "buffer (0 = skip)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="before the timed region, run one device copy of this many MiB (counter calibration)")
     return ap.parse_args()
@@ -211,6 +272,9 @@ def main():
     if args.summarize_pmc:
         summarize_pmc(args)
         return
+    if args.summarize_mfma:
+        summarize_mfma(args)
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
@@ -259,24 +323,24 @@ def main():
     lay = hm.Layout(S, d, E, k, C, dcode)
     stream = torch.cuda.current_stream()
 
+    op_calls = {
+        "gate": lambda st: hm.moe_gate(params, x if learned else None, wg, bias, tok if not learned else None, None,
+                                       None, None, ids, slots, weights, counts, demand, slot_src, ws, st),
+        "dispatch": lambda st: hm.moe_dispatch(lay, x, ids, slots, slot_src, xe, st),
+        "combine": lambda st: hm.moe_combine(lay, xe, ids, slots, weights, y, st),
+        "combine_bwd": lambda st: hm.moe_combine_bwd(lay, dy, xe if want_dw else None, ids, slots, slot_src, weights,
+                                                     dye, dw, st),
+        "dispatch_bwd": lambda st: hm.moe_dispatch_bwd(lay, dye, ids, slots, dx, st),
+    }
+
     def step(evs=None, st=None):
         st = stream if st is None else st
-
-        def mark(i):
+        for i, op in enumerate(OPS):
             if evs is not None:
                 evs[i].record(st)
-        mark(0)
-        hm.moe_gate(params, x if learned else None, wg, bias, tok if not learned else None, None, None, None, ids, slots,
-                    weights, counts, demand, slot_src, ws, st)
-        mark(1)
-        hm.moe_dispatch(lay, x, ids, slots, slot_src, xe, st)
-        mark(2)
-        hm.moe_combine(lay, xe, ids, slots, weights, y, st)
-        mark(3)
-        hm.moe_combine_bwd(lay, dy, xe if want_dw else None, ids, slots, slot_src, weights, dye, dw, st)
-        mark(4)
-        hm.moe_dispatch_bwd(lay, dye, ids, slots, dx, st)
-        mark(5)
+            op_calls[op](st)
+        if evs is not None:
+            evs[len(OPS)].record(st)
 
     if args.calib_copy_mib:
         n = args.calib_copy_mib * (1 << 20) // 4
@@ -402,7 +466,7 @@ def main():
         gates["dense_to_sparse"] = {"ms": round(ms, 5), "temperature": 0.5, "alg_bytes": b,
                                     "GB/s": round(b / (ms * 1e-3) / 1e9, 1)}
         del noise
-        if S % E == 0 and S // E <= 2048:
+        if S % E == 0 and S // E <= 2048 and not args.no_base:
             # BASE layer: balanced assignment by the auction (each call
             # synchronizes its stream); bound by the latency of its rounds
             cb_ = S // E
@@ -439,6 +503,29 @@ def main():
         ms = time_gate(gp, tok=tok, table=table)
         gates["balanced_hash"] = {"ms": round(ms, 5), "alg_bytes": ab["gate"] + S * 4,
                                   "GB/s": round((ab["gate"] + S * 4) / (ms * 1e-3) / 1e9, 1)}
+
+    # per op from a cold cache, outside the timed region: before each launch read
+    # a 1 GiB buffer (more than the L2s and the 256 MB Infinity Cache, and it
+    # leaves clean lines behind); median of the launches
+    cold = None
+    if args.cold_iters > 0:
+        flush = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+        cold = {}
+        c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        for op in OPS:
+            ts = []
+            for _ in range(args.cold_iters):
+                flush.sum()
+                c0.record(stream)
+                op_calls[op](stream)
+                c1.record(stream)
+                torch.cuda.synchronize()
+                ts.append(c0.elapsed_time(c1))
+            ts.sort()
+            med = ts[len(ts) // 2]
+            cold[op] = {"ms_p50": round(med, 5), "GB/s": round(ab[op] / (med * 1e-3) / 1e9, 1),
+                        "frac": round(ab[op] / (med * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+        del flush
 
     dom = max(("dispatch", "combine", "combine_bwd", "dispatch_bwd", "gate"), key=lambda o: op_ms[o])
     achieved = ab[dom] / (op_ms[dom] * 1e-3) / 1e9
@@ -494,6 +581,7 @@ def main():
         "routing": {"kept_assignments": n_kept, "tokens_with_kept": tok_kept, "assignments": S * k},
         "gate_bwd": gate_bwd,
         "gates": gates,
+        "cold": cold,
     }
     fwd_ms = op_ms["gate"] + op_ms["dispatch"] + op_ms["combine"]
     out["fwd"] = {"ms": round(fwd_ms, 5), "tokens/s": round(S / (fwd_ms * 1e-3), 1),

@@ -460,7 +460,8 @@ __global__ __launch_bounds__(kBwdThreads) void dwg_mfma_kernel(GateBwdArgs a) {
 }
 
 // ---------------------------------------------------------------- dx on matrix cores
-// Block: 64 tokens (wave w: 16) x 256 columns (4 passes of 64).  A[s][e] = dL
+// Block: 64 tokens (wave w: 16) x 256 columns (4 passes of 64); blocks are
+// numbered column block first.  A[s][e] = dL
 // in three bf16 parts, kept in registers; B[e][j] = W[j][e] from the block's W
 // rows staged in LDS.  The 16 x 64 fp32 results go through LDS column-major
 // (each lane's 4 tokens of one column are contiguous: one 16-byte store; a
@@ -468,17 +469,27 @@ __global__ __launch_bounds__(kBwdThreads) void dwg_mfma_kernel(GateBwdArgs a) {
 // stores merged with a wrong offset), then each lane adds the incoming dx to
 // two 8-column pieces of a token row and stores them, 16 bytes each.
 template <int NT>
-__global__ __launch_bounds__(kBwdThreads) void dx_mfma_kernel(GateBwdArgs a) {
-  constexpr int E = 16 * NT;
-  constexpr int KS = (E + 31) / 32;  // K steps of 32 experts (a half step when E % 32 == 16)
-  constexpr int LDW = E + 8;         // padded W row in LDS (bf16)
-  constexpr int LDT = 16 + 4;        // padded column of the output tile (fp32, 16 tokens)
-  __shared__ __align__(16) uint16_t wl[kWave * LDW];
-  __shared__ __align__(16) float ot[kBwdWaves * kWave * LDT];
+struct DxShape {
+  static constexpr int E = 16 * NT;
+  static constexpr int KS = (E + 31) / 32;  // K steps of 32 experts (a half step when E % 32 == 16)
+  static constexpr int LDW = E + 8;         // padded W row in LDS (bf16)
+  static constexpr int LDT = 16 + 4;        // padded column of the output tile (fp32, 16 tokens)
+};
+
+// FULL: all 64 tokens of the block exist (every block but a ragged last one),
+// so no token test splits the code: a branch around a load or a store makes
+// the compiler wait for every outstanding memory operation (stores and loads
+// share one in-order counter).
+template <int NT, bool ACC, bool FULL>
+__device__ __forceinline__ void dx_mfma_body(const GateBwdArgs& a, uint16_t* wl, float* ot) {
+  constexpr int E = DxShape<NT>::E, KS = DxShape<NT>::KS, LDW = DxShape<NT>::LDW, LDT = DxShape<NT>::LDT;
   const int w = threadIdx.x / kWave, lane = lane_id();
   const int g = lane / 16, m = lane % 16;
-  const int64_t s0 = static_cast<int64_t>(blockIdx.x) * kWave + 16 * w;
+  const int ncb = (a.d + 4 * kWave - 1) / (4 * kWave);  // column blocks of 256
+  const int64_t tb = blockIdx.x / ncb;                   // 64-token block
+  const int64_t s0 = tb * kWave + 16 * w;
   const uint16_t* wg = reinterpret_cast<const uint16_t*>(a.wg);
+  uint16_t* dxp = reinterpret_cast<uint16_t*>(a.dx);
   const u32x4 zero = {0u, 0u, 0u, 0u};
 
   u32x4 ah[KS], am[KS], al[KS];
@@ -487,7 +498,7 @@ __global__ __launch_bounds__(kBwdThreads) void dx_mfma_kernel(GateBwdArgs a) {
     const int e0 = 32 * ks + 8 * g;
     const int64_t s = s0 + m;
     float vv[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    if (s < a.S && e0 < E) {
+    if ((FULL || s < a.S) && e0 < E) {
       const float4 p0 = *reinterpret_cast<const float4*>(a.dl + s * E + e0);
       const float4 p1 = *reinterpret_cast<const float4*>(a.dl + s * E + e0 + 4);
       vv[0] = p0.x; vv[1] = p0.y; vv[2] = p0.z; vv[3] = p0.w;
@@ -496,46 +507,54 @@ __global__ __launch_bounds__(kBwdThreads) void dx_mfma_kernel(GateBwdArgs a) {
     split8(vv, ah[ks], am[ks], al[ks]);
   }
   float* out = ot + w * kWave * LDT;
-  const int jb = blockIdx.y * 4 * kWave;
-  // W rows of the next pass are loaded into registers while this one runs
+  const int jb = static_cast<int>(blockIdx.x % ncb) * 4 * kWave;
+  // Loads are unconditional (clamped addresses; a value past the end is never
+  // used), so that no branch hides one from the wait counts, and they are
+  // issued a pass ahead: W rows and the incoming dx of pass cb + 1 while pass
+  // cb runs.  Vector-memory loads complete in issue order, so the waits for
+  // one pass's values leave the next pass's loads in flight.
   constexpr int WPT = (kWave * (E / 8) + kBwdThreads - 1) / kBwdThreads;  // 16-byte pieces per thread
   u32x4 wreg[WPT];
   auto load_w = [&](int j0) {
 #pragma unroll
     for (int u = 0; u < WPT; ++u) {
-      const int q = threadIdx.x + u * kBwdThreads;
+      const int q = min(threadIdx.x + u * kBwdThreads, kWave * (E / 8) - 1);
       const int r = q / (E / 8), p8 = q % (E / 8);
-      wreg[u] = (q < kWave * (E / 8) && j0 < a.d)
-                    ? *reinterpret_cast<const u32x4*>(wg + static_cast<int64_t>(j0 + r) * E + 8 * p8)
-                    : zero;
+      const int row = min(j0 + r, a.d - 1);
+      wreg[u] = *reinterpret_cast<const u32x4*>(wg + static_cast<int64_t>(row) * E + 8 * p8);
     }
   };
+  // lane -> two chunks of 8 columns of one token (chunk id = lane + 64 h)
+  auto dx_at = [&](int h, int j0) {
+    const int id = lane + kWave * h, t = id / 8, c8 = id % 8;
+    const int64_t s = s0 + t;
+    return reinterpret_cast<u32x4*>(dxp + ((FULL || s < a.S) ? s : 0) * a.d + min(j0, a.d - kWave) + 8 * c8);
+  };
+  u32x4 din[2] = {zero, zero}, dnx[2] = {zero, zero};
+  if constexpr (ACC) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) din[h] = *dx_at(h, jb);
+  }
   load_w(jb);
+  // unrolled, so that handing the prefetched dx to the next pass is a renaming,
+  // not a register move that would wait for the load
+#pragma unroll
   for (int cb = 0; cb < 4; ++cb) {
     const int j0 = jb + cb * kWave;
     if (j0 >= a.d) break;  // the same for the whole block
-    // lane -> two chunks of 8 columns of one token (chunk id = lane + 64 h);
-    // the incoming dx is requested now and used after the products
-    u32x4 din[2];
-    u32x4* dst[2];
-    bool okh[2];
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int id = lane + kWave * h, t = id / 8, c8 = id % 8;
-      const int64_t s = s0 + t;
-      okh[h] = s < a.S;
-      dst[h] = reinterpret_cast<u32x4*>(reinterpret_cast<uint16_t*>(a.dx) + (okh[h] ? s : 0) * a.d + j0 + 8 * c8);
-      din[h] = (a.accumulate && okh[h]) ? *dst[h] : zero;
-    }
     __syncthreads();  // previous pass's W rows consumed
 #pragma unroll
-    for (int u = 0; u < WPT; ++u) {
-      const int q = threadIdx.x + u * kBwdThreads;
+    for (int u = 0; u < WPT; ++u) {  // clamped like the loads: a repeated piece rewrites its own value
+      const int q = min(threadIdx.x + u * kBwdThreads, kWave * (E / 8) - 1);
       const int r = q / (E / 8), p8 = q % (E / 8);
-      if (q < kWave * (E / 8)) *reinterpret_cast<u32x4*>(&wl[r * LDW + 8 * p8]) = wreg[u];
+      *reinterpret_cast<u32x4*>(&wl[r * LDW + 8 * p8]) = wreg[u];
     }
     __syncthreads();
     load_w(j0 + kWave);
+    if constexpr (ACC) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) dnx[h] = *dx_at(h, j0 + kWave);
+    }
     f32x4 acc[4];
 #pragma unroll
     for (int nt = 0; nt < 4; ++nt) {
@@ -564,21 +583,33 @@ __global__ __launch_bounds__(kBwdThreads) void dx_mfma_kernel(GateBwdArgs a) {
       float o[8];
 #pragma unroll
       for (int q = 0; q < 8; ++q) o[q] = out[(8 * c8 + q) * LDT + t];
-      if (a.accumulate) {
+      if constexpr (ACC) {
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           o[2 * q] += bf16_lo(din[h][q]);
           o[2 * q + 1] += bf16_hi(din[h][q]);
         }
       }
-      if (okh[h])
-        *dst[h] = u32x4{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]), pack_bf16x2(o[4], o[5]),
-                        pack_bf16x2(o[6], o[7])};
+      if (FULL || s0 + t < a.S)
+        __builtin_nontemporal_store(u32x4{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]),
+                                          pack_bf16x2(o[4], o[5]), pack_bf16x2(o[6], o[7])},
+                                    dx_at(h, j0));
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+    for (int h = 0; h < 2; ++h) din[h] = dnx[h];
   }
+}
+
+template <int NT, bool ACC>
+__global__ __launch_bounds__(kBwdThreads) void dx_mfma_kernel(GateBwdArgs a) {
+  __shared__ __align__(16) uint16_t wl[kWave * DxShape<NT>::LDW];
+  __shared__ __align__(16) float ot[kBwdWaves * kWave * DxShape<NT>::LDT];
+  const int ncb = (a.d + 4 * kWave - 1) / (4 * kWave);
+  if ((static_cast<int64_t>(blockIdx.x / ncb) + 1) * kWave <= a.S) dx_mfma_body<NT, ACC, true>(a, wl, ot);
+  else dx_mfma_body<NT, ACC, false>(a, wl, ot);
 }
 
 // ---------------------------------------------------------------- dW, dx on the vector ALUs
@@ -784,8 +815,11 @@ hipError_t launch_gate_bwd_dwg(const GateBwdArgs& a, hipStream_t st) {
 
 template <int NT>
 static void launch_dx_mfma_t(const GateBwdArgs& a, hipStream_t st) {
-  const dim3 grid(static_cast<unsigned>(a.nb), static_cast<unsigned>((a.d + 4 * kWave - 1) / (4 * kWave)));
-  dx_mfma_kernel<NT><<<grid, dim3(kBwdThreads), 0, st>>>(a);
+  // 1-D grid, the column blocks of one 64-token block consecutive, so that
+  // they run side by side and whole rows of dx stream together
+  const dim3 grid(static_cast<unsigned>(static_cast<int64_t>((a.d + 4 * kWave - 1) / (4 * kWave)) * a.nb));
+  if (a.accumulate) dx_mfma_kernel<NT, true><<<grid, dim3(kBwdThreads), 0, st>>>(a);
+  else dx_mfma_kernel<NT, false><<<grid, dim3(kBwdThreads), 0, st>>>(a);
 }
 
 hipError_t launch_gate_bwd_dx(const GateBwdArgs& a, hipStream_t st) {

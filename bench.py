@@ -24,9 +24,11 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E peak, GB/s
 METRIC = "tokens/s through gate+dispatch+combine; achieved HBM GB/s vs MI355X peak"
 OPS = ("gate", "dispatch", "combine", "combine_bwd", "dispatch_bwd")
-_LAYOUT_SRC = ("layout.hip", "common.hpp", "kernels.hpp")
+# sources each op's kernel is compiled from; "file:Struct" stands for that
+# struct's definition alone (the argument block the kernel reads)
+_LAYOUT_SRC = ("layout.hip", "common.hpp", "kernels.hpp:RowArgs")
 _GATE_SRC = ("gate.hip", "route_mfma.hip", "route_mfma_rs.hip", "route_mfma_ph.hip", "route_valu.hpp", "route_valu_f32.hip",
-             "route_valu_bf16.hip", "select.hpp", "common.hpp", "kernels.hpp")
+             "route_valu_bf16.hip", "select.hpp", "common.hpp", "kernels.hpp:RouteArgs")
 OPS_KERNELS = ("dispatch", "combine", "combine_bwd", "dispatch_bwd", "gate")
 
 
@@ -91,7 +93,8 @@ def summarize_pmc(args):
             f.write(f"# HBM traffic per launch of {frag} ({op}), workload {w['name']}\n")
             f.write("# from two rocprofv3 counter runs (TMPDIR=/tmp, from /tmp, repo at $R):\n")
             f.write(f"#   rocprofv3 --pmc FETCH_SIZE --output-format csv -d <dir> -- python3 $R/bench.py --workload "
-                    f"{args.workload} --steps 3 --warmup 1 --no-cpu-baseline --calib-copy-mib {args.calib_copy_mib}\n")
+                    f"{args.workload} --steps 3 --warmup 1 --no-cpu-baseline --no-base --cold-iters 0 "
+                    f"--calib-copy-mib {args.calib_copy_mib}\n")
             f.write("#   (the same with --pmc WRITE_SIZE)\n")
             f.write(f"# calibration: one {args.calib_copy_mib} MiB device copy read FETCH {fc:.0f} KiB, WRITE {wc:.0f} KiB\n")
             f.write(f"fetch_kib_per_launch: {fk:.1f}\nwrite_kib_per_launch: {wk:.1f}\n")
@@ -125,7 +128,7 @@ def summarize_mfma(args):
     lines = [f"# matrix-core use per launch, workload {w['name']}",
              "# from one rocprofv3 counter run (TMPDIR=/tmp, from /tmp, repo at $R):",
              f"#   rocprofv3 --pmc MfmaUtil MfmaFlopsBF16 GRBM_GUI_ACTIVE --output-format csv -d <dir> -- python3 "
-             f"$R/bench.py --workload {args.workload} --steps 3 --warmup 1 --no-cpu-baseline --no-base",
+             f"$R/bench.py --workload {args.workload} --steps 3 --warmup 1 --no-cpu-baseline --no-base --cold-iters 0",
              "# MfmaUtil = matrix-unit busy cycles summed over SIMDs / (GPU active cycles x SIMDs) x 100;",
              "# MfmaFlopsBF16 = bf16 MFMA operations x 512 (flops counted by the hardware)",
              f"# algorithmic flops of one projection 2*S*d*E = {alg}",
@@ -200,8 +203,13 @@ def alg_bytes(w, S, d, E, k, C, elt, n_kept, tok_kept, dw):
 def source_sha(names):
     h = hashlib.sha256()
     for name in names:
-        with open(os.path.join(ROOT, "paper_2203_14685_amd", "csrc", name), "rb") as f:
-            h.update(f.read())
+        fname, _, struct = name.partition(":")
+        with open(os.path.join(ROOT, "paper_2203_14685_amd", "csrc", fname), "rb") as f:
+            text = f.read()
+        if struct:
+            i = text.index(f"struct {struct} {{".encode())
+            text = text[i:text.index(b"};", i) + 2]
+        h.update(text)
     return h.hexdigest()[:16]
 
 

@@ -322,6 +322,113 @@ __global__ __launch_bounds__(kBaseThreads) void base_resolve_kernel(BaseArgs a, 
   if (tid == 0) a.hold_n[e] = min(c, nh + nb);
 }
 
+// ---------------------------------------------------------------- one wave per bidder
+// The bid of token t with the lanes over experts: the best value (lower expert
+// on ties) and the best other value by butterflies over (value, expert); max
+// is exact, so this equals the sequential scan of base_bid_kernel.  Every lane
+// returns the same expert and bid.
+__device__ __forceinline__ void base_wave_bid(const BaseArgs& a, const double* pr, double eps, int t, int lane,
+                                              int& e_out, double& bid_out) {
+  const float* row = a.logits + static_cast<int64_t>(t) * a.E;
+  double v1 = -INFINITY, v2 = -INFINITY, l1 = 0.0;
+  int e1 = 0x7fffffff;
+  for (int e = lane; e < a.E; e += kWave) {
+    const float l = row[e];
+    const double v = static_cast<double>(l) - pr[e];
+    if (v > v1) {
+      v2 = v1;
+      v1 = v;
+      e1 = e;
+      l1 = static_cast<double>(l);
+    } else if (v > v2) {
+      v2 = v;
+    }
+  }
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const double ov1 = __shfl_xor(v1, off, kWave), ov2 = __shfl_xor(v2, off, kWave);
+    const double ol1 = __shfl_xor(l1, off, kWave);
+    const int oe1 = __shfl_xor(e1, off, kWave);
+    if (ov1 > v1 || (ov1 == v1 && oe1 < e1)) {
+      v2 = fmax(ov2, v1);
+      v1 = ov1;
+      e1 = oe1;
+      l1 = ol1;
+    } else {
+      v2 = fmax(v2, ov1);
+    }
+  }
+  if (a.E == 1) v2 = v1;
+  e_out = e1;
+  bid_out = l1 - v2 + eps;
+}
+
+// Expert e takes the only bid for it this round, (bid, t): the holders ahead
+// of it are counted by the lanes, the holders behind it move up one place,
+// the last one dropping out when the list is full.  With `hvs`/`hts` (LDS of c
+// entries) the holders are staged there while counted; without, the moving
+// ones are read again, from the end, 64 at a time (each block is read before
+// the next lower block can overwrite its first slot).  Returns the evicted
+// token or -1; `bad` is set if the bid does not rank below c (it always does:
+// a bid exceeds its expert's price, the c-th best bid).
+__device__ __forceinline__ int base_wave_place(const BaseArgs& a, double* pr, int* hn, int e, double bid, int t,
+                                               int lane, double* hvs, int* hts, bool& bad) {
+  const int c = a.cap;
+  const int nh = hn[e];
+  const int64_t base = static_cast<int64_t>(e) * c;
+  int p = 0, ev = -1;
+  double vlast = 0.0;  // bid of the holder that ends at c - 1
+  for (int i = lane; i < nh; i += kWave) {
+    const double hv = a.hold_v[base + i];
+    const int ht = a.hold_t[base + i];
+    if (hvs) {
+      hvs[i] = hv;
+      hts[i] = ht;
+    }
+    p += base_before(hv, ht, bid, t);
+    if (i == c - 1) ev = ht;
+    if (i == c - 2) vlast = hv;
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    p += __shfl_xor(p, off, kWave);
+    ev = max(ev, __shfl_xor(ev, off, kWave));
+  }
+  vlast = __shfl(vlast, (c - 2) & (kWave - 1), kWave);
+  bad = p >= c;
+  if (bad) return -1;
+  if (hvs) {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    for (int i = p + lane; i < min(nh, c - 1); i += kWave) {
+      a.hold_v[base + i + 1] = hvs[i];
+      a.hold_t[base + i + 1] = hts[i];
+    }
+  } else {
+    for (int top = min(nh, c - 1); top > p; top -= kWave) {
+      const int lo = max(p, top - kWave);
+      const int i = lo + lane;
+      if (i < top) {
+        const double hv = a.hold_v[base + i];
+        const int ht = a.hold_t[base + i];
+        a.hold_v[base + i + 1] = hv;
+        a.hold_t[base + i + 1] = ht;
+      }
+    }
+  }
+  if (lane == 0) {
+    a.hold_v[base + p] = bid;
+    a.hold_t[base + p] = t;
+    a.assign[t] = e;
+    if (ev >= 0) a.assign[ev] = -1;
+    const int nn = min(c, nh + 1);
+    if (nn == c) pr[e] = p == c - 1 ? bid : vlast;
+    hn[e] = nn;
+  }
+  return ev;
+}
+
 // ---------------------------------------------------------------- tail
 // Most rounds of a phase have a handful of bidders.  Once at most kBaseTail
 // tokens are unassigned after a round, one workgroup runs the following rounds
@@ -395,69 +502,14 @@ __global__ __launch_bounds__(kBaseThreads) void base_tail_kernel(BaseArgs a, int
             fl = 1;
             break;
           }
-          const float* row = a.logits + static_cast<int64_t>(t) * E;
-          double v1 = -INFINITY, v2 = -INFINITY, l1 = 0.0;
-          int e1 = 0x7fffffff;
-          for (int e = lane; e < E; e += kWave) {
-            const float l = row[e];
-            const double v = static_cast<double>(l) - pr[e];
-            if (v > v1) {
-              v2 = v1;
-              v1 = v;
-              e1 = e;
-              l1 = static_cast<double>(l);
-            } else if (v > v2) {
-              v2 = v;
-            }
-          }
-#pragma unroll
-          for (int off = 1; off < kWave; off <<= 1) {
-            const double ov1 = __shfl_xor(v1, off, kWave), ov2 = __shfl_xor(v2, off, kWave);
-            const double ol1 = __shfl_xor(l1, off, kWave);
-            const int oe1 = __shfl_xor(e1, off, kWave);
-            if (ov1 > v1 || (ov1 == v1 && oe1 < e1)) {
-              v2 = fmax(ov2, v1);
-              v1 = ov1;
-              e1 = oe1;
-              l1 = ol1;
-            } else {
-              v2 = fmax(v2, ov1);
-            }
-          }
-          if (E == 1) v2 = v1;
-          const double bid = l1 - v2 + eps;
-          const int nh = hn[e1];
-          const int64_t base = static_cast<int64_t>(e1) * c;
-          int p = 0;
-          for (int i = lane; i < nh; i += kWave) {
-            const double hv = a.hold_v[base + i];
-            const int ht = a.hold_t[base + i];
-            hvs[i] = hv;
-            hts[i] = ht;
-            p += base_before(hv, ht, bid, t);
-          }
-#pragma unroll
-          for (int off = 32; off >= 1; off >>= 1) p += __shfl_xor(p, off, kWave);
-          __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-          __builtin_amdgcn_wave_barrier();
-          __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-          if (p >= c) {  // cannot happen (see above); stop rather than loop
+          int e1;
+          double bid;
+          base_wave_bid(a, pr, eps, t, lane, e1, bid);
+          bool bad;
+          const int evicted = base_wave_place(a, pr, hn, e1, bid, t, lane, hvs, hts, bad);
+          if (bad) {  // cannot happen (see base_wave_place); stop rather than loop
             fl = 1;
             break;
-          }
-          const int evicted = nh == c ? hts[c - 1] : -1;
-          for (int i = p + lane; i < min(nh, c - 1); i += kWave) {
-            a.hold_v[base + i + 1] = hvs[i];
-            a.hold_t[base + i + 1] = hts[i];
-          }
-          if (lane == 0) {
-            a.hold_v[base + p] = bid;
-            a.hold_t[base + p] = t;
-            a.assign[t] = e1;
-            if (evicted >= 0) a.assign[evicted] = -1;
-            const int nn = min(c, nh + 1);
-            if (nn == c) pr[e1] = p == c - 1 ? bid : hvs[c - 2];
-            hn[e1] = nn;
           }
           ++k;
           // stores and LDS updates visible to the whole wave before the next step
@@ -487,8 +539,57 @@ __global__ __launch_bounds__(kBaseThreads) void base_tail_kernel(BaseArgs a, int
       __syncthreads();  // fast_rounds and fast_fail are rewritten by a later chain
       continue;
     }
+    // Up to 16 bidders: one wave each computes its bid; if they all want
+    // different experts, each wave then places its own (one bid per expert),
+    // else the general merge below runs on these bids.
+    bool have_bids = false;
+    if (n <= kBaseWaves) {
+      if (w < n) {
+        int e1;
+        double bid;
+        base_wave_bid(a, pr, eps, U[w], lane, e1, bid);
+        if (lane == 0) {
+          bex[w] = e1;
+          bvv[w] = bid;
+        }
+      }
+      if (tid == 0) {
+        nU2 = 0;
+        fast_fail = 0;
+      }
+      __syncthreads();
+      bool distinct = true;
+      for (int i = 0; i < n; ++i)
+        for (int j = i + 1; j < n; ++j) distinct = distinct && bex[i] != bex[j];
+      if (distinct) {  // uniform: every thread read the same bids
+        if (w < n) {
+          bool bad;
+          const int ev = base_wave_place(a, pr, hn, bex[w], bvv[w], U[w], lane, nullptr, nullptr, bad);
+          if (lane == 0) {
+            if (bad) fast_fail = 1;
+            if (ev >= 0) {
+              const int q = atomicAdd(&nU2, 1);
+              if (q < kBaseTail) U2[q] = ev;
+            }
+          }
+        }
+        __syncthreads();
+        if (fast_fail) {
+          failed = 1;
+          break;
+        }
+        const int n2 = nU2;
+        if (tid < min(n2, kBaseTail)) U[tid] = U2[tid];
+        if (tid == 0) nU = n2;
+        rounds_phase += 1;
+        rounds_total += 1;
+        __syncthreads();
+        continue;
+      }
+      have_bids = true;
+    }
     // bids, as in base_bid_kernel
-    if (tid < n) {
+    if (!have_bids && tid < n) {
       const int t = U[tid];
       const float* row = a.logits + static_cast<int64_t>(t) * E;
       double v1 = -INFINITY, v2 = -INFINITY;

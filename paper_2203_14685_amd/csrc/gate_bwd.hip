@@ -406,7 +406,9 @@ __global__ __launch_bounds__(kBwdThreads) void dwg_mfma_kernel(GateBwdArgs a) {
       u32x4 cols[8];
       transpose8x8_b16(rows, cols);
 #pragma unroll
-      for (int i = 0; i < 8; ++i) *reinterpret_cast<u32x4*>(&tile[(8 * bb + i) * LDX + 8 * ab]) = cols[i];
+      // 16-byte unit of the row XOR the row's group of 8: the 8 lanes of one
+      // store (same ab, rows 8 apart) land in different banks
+      for (int i = 0; i < 8; ++i) *reinterpret_cast<u32x4*>(&tile[(8 * bb + i) * LDX + 8 * (ab ^ bb)]) = cols[i];
     }
     load_rows(c + kBwdWaves);
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -417,7 +419,8 @@ __global__ __launch_bounds__(kBwdThreads) void dwg_mfma_kernel(GateBwdArgs a) {
       u32x4 av[4];
 #pragma unroll
       for (int mt = 0; mt < 4; ++mt)
-        av[mt] = *reinterpret_cast<const u32x4*>(&tile[(16 * mt + m) * LDX + 32 * ks + 8 * g]);
+        av[mt] = *reinterpret_cast<const u32x4*>(
+            &tile[(16 * mt + m) * LDX + 8 * ((4 * ks + g) ^ (((16 * mt + m) >> 3) & 7))]);
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
         const uint16_t* src = a.dlt + static_cast<int64_t>(16 * nt + m) * a.s_pad + s0 + 32 * ks + 8 * g;

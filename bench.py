@@ -486,7 +486,7 @@ def main():
             info = hm.BaseInfo()
 
             def bcall():
-                hm.moe_base_gate(bpp, x, wg, bias, None, bo[0], bo[1], bo[2], bo[3], bo[4], bws, info, stream)
+                hm.moe_base_gate(bpp, x, wg, bias, None, bo[0], bo[1], bo[2], bo[3], bo[4], None, bws, info, stream)
             bcall()
             nb_calls = max(1, min(args.steps, 10))
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)

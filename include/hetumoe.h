@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define MOE_ABI_VERSION 5
+#define MOE_ABI_VERSION 6
 
 /* Symbols of the C ABI are the only ones the shared library exports. */
 #define MOE_API __attribute__((visibility("default")))
@@ -206,8 +206,12 @@ MOE_API moe_status moe_base_gate_workspace_size(const moe_base_params* p, size_t
  * Outputs ids [S] (k = 1), weights [S] fp32 = sigmoid(L[s, ids[s]]) (the BASE
  * layer scales its expert's output by this), logits [S,E] fp32 (optional
  * output when logits_in == 0), and, as moe_gate with k = 1: slots [S], counts
- * [E], slot_src [E,C] in token order per expert.  info (host memory, may be
- * NULL) receives the auction's statistics.
+ * [E], slot_src [E,C] in token order per expert.  prices [E] fp64 (device, may
+ * be NULL): the auction's final expert prices p, a certificate of optimality:
+ * with D = sum_s max_e (L[s,e] - p[e]) + (S/E) * sum_e p[e], an upper bound on
+ * the optimum for any p, the returned total is at least D - S * info->eps, and
+ * every token is within eps of its best L[s,e] - p[e].  info (host memory, may
+ * be NULL) receives the auction's statistics.
  *
  * Unlike the other calls this one SYNCHRONIZES `stream`: the host reads the
  * number of unassigned tokens after every 8 rounds.  It returns
@@ -219,8 +223,9 @@ MOE_API moe_status moe_base_gate_workspace_size(const moe_base_params* p, size_t
  */
 MOE_API moe_status moe_base_gate(const moe_base_params* p, const void* x, const void* wg,
                                  const float* bias, float* logits, int32_t* ids, int32_t* slots,
-                                 float* weights, int32_t* counts, int32_t* slot_src, void* workspace,
-                                 size_t workspace_bytes, moe_base_info* info, hipStream_t stream);
+                                 float* weights, int32_t* counts, int32_t* slot_src, double* prices,
+                                 void* workspace, size_t workspace_bytes, moe_base_info* info,
+                                 hipStream_t stream);
 
 /*
  * moe_dispatch -- step 2 of Algorithm 1 (Layout_Transform; Sec. 3.2, layout

@@ -96,7 +96,7 @@ def load():
                                  f32p, vp, ctypes.c_size_t, vp]
     lib.moe_base_gate_workspace_size.argtypes = [ctypes.POINTER(BaseParams), ctypes.POINTER(ctypes.c_size_t)]
     lib.moe_base_gate.argtypes = [ctypes.POINTER(BaseParams), vp, vp, f32p, f32p, i32p, i32p, f32p, i32p, i32p,
-                                  vp, ctypes.c_size_t, ctypes.POINTER(BaseInfo), vp]
+                                  vp, vp, ctypes.c_size_t, ctypes.POINTER(BaseInfo), vp]
     for name in ("moe_gate_workspace_size", "moe_gate", "moe_dispatch", "moe_combine",
                  "moe_dispatch_bwd", "moe_combine_bwd", "moe_gate_bwd_workspace_size", "moe_gate_bwd",
                  "moe_hash_balanced_table", "moe_base_gate_workspace_size", "moe_base_gate"):
@@ -265,10 +265,11 @@ def moe_base_gate_workspace_size(params):
     return n.value
 
 
-def moe_base_gate(params, x, wg, bias, logits, ids, slots, weights, counts, slot_src, workspace, info=None,
+def moe_base_gate(params, x, wg, bias, logits, ids, slots, weights, counts, slot_src, prices, workspace, info=None,
                   stream=None):
-    """BASE-layer balanced assignment (synchronizes the stream).  `info`: a
-    BaseInfo filled with the auction's statistics, or None."""
+    """BASE-layer balanced assignment (synchronizes the stream).  `prices`: a
+    float64 [E] device tensor for the final prices, or None; `info`: a BaseInfo
+    filled with the auction's statistics, or None."""
     lib = load()
     f32, i32 = torch.float32, torch.int32
     xdt = torch.bfloat16 if params.dtype == MOE_BF16 else torch.float32
@@ -277,15 +278,16 @@ def moe_base_gate(params, x, wg, bias, logits, ids, slots, weights, counts, slot
         ctypes.byref(params), _ptr(x, xdt, "x"), _ptr(wg, xdt, "wg"), _ptr(bias, f32, "bias"),
         _ptr(logits, f32, "logits"), _ptr(ids, i32, "ids"), _ptr(slots, i32, "slots"),
         _ptr(weights, f32, "weights"), _ptr(counts, i32, "counts"), _ptr(slot_src, i32, "slot_src"),
-        _ptr(workspace, None, "workspace"), ws_bytes, None if info is None else ctypes.byref(info),
+        _ptr(prices, torch.float64, "prices"), _ptr(workspace, None, "workspace"), ws_bytes,
+        None if info is None else ctypes.byref(info),
         _stream(stream)))
 
 
 def base_gate(E, capacity=None, *, x=None, wg=None, bias=None, logits=None, logits_in=False, want_logits=False,
               max_rounds=0, stream=None):
     """Allocate the outputs and run moe_base_gate; returns a dict of device
-    tensors (ids, slots, weights as [S, 1], the shape the layout calls take)
-    plus "info" (phases, rounds, eps of the auction)."""
+    tensors (ids, slots, weights as [S, 1], the shape the layout calls take;
+    prices [E] float64) plus "info" (phases, rounds, eps of the auction)."""
     if logits_in:
         S, d, dcode = int(logits.shape[0]), 0, MOE_F32
         dev = logits.device
@@ -300,6 +302,7 @@ def base_gate(E, capacity=None, *, x=None, wg=None, bias=None, logits=None, logi
         "weights": torch.empty((S, 1), dtype=torch.float32, device=dev),
         "counts": torch.empty((E,), dtype=torch.int32, device=dev),
         "slot_src": torch.empty((E, C), dtype=torch.int32, device=dev),
+        "prices": torch.empty((E,), dtype=torch.float64, device=dev),
     }
     if not logits_in:
         logits = torch.empty((S, E), dtype=torch.float32, device=dev) if want_logits else None
@@ -307,7 +310,7 @@ def base_gate(E, capacity=None, *, x=None, wg=None, bias=None, logits=None, logi
     ws = torch.empty((moe_base_gate_workspace_size(params),), dtype=torch.uint8, device=dev)
     info = BaseInfo()
     moe_base_gate(params, x, wg, bias, logits, out["ids"], out["slots"], out["weights"], out["counts"],
-                  out["slot_src"], ws, info, stream)
+                  out["slot_src"], out["prices"], ws, info, stream)
     out["info"] = dict(phases=info.phases, rounds=info.rounds, eps=info.eps)
     return out
 

@@ -753,6 +753,8 @@ __global__ __launch_bounds__(kBlock) void base_finish_kernel(BaseArgs a, int r) 
   __syncthreads();
   if (wb < a.nb)
     for (int i = lane; i < a.E; i += kWave) a.hist[static_cast<int64_t>(i) * a.nb + wb] = lds[i];
+  if (a.prices_out && blockIdx.x == 0)
+    for (int i = tid; i < a.E; i += kBlock) a.prices_out[i] = a.price[i];
 }
 
 // ---------------------------------------------------------------- driver

@@ -563,7 +563,8 @@ moe_status moe_base_gate_workspace_size(const moe_base_params* p, size_t* bytes)
 
 moe_status moe_base_gate(const moe_base_params* p, const void* x, const void* wg, const float* bias, float* logits,
                          int32_t* ids, int32_t* slots, float* weights, int32_t* counts, int32_t* slot_src,
-                         void* workspace, size_t workspace_bytes, moe_base_info* info, hipStream_t stream) {
+                         double* prices, void* workspace, size_t workspace_bytes, moe_base_info* info,
+                         hipStream_t stream) {
   static const char* who = "moe_base_gate";
   CHECK(check_base_params(p));
   const int64_t S = p->S, E = p->E, C = p->capacity;
@@ -582,6 +583,7 @@ moe_status moe_base_gate(const moe_base_params* p, const void* x, const void* wg
   CHECK(need(weights, S, 4, who, "weights"));
   CHECK(need(counts, E, 4, who, "counts"));
   CHECK(need(slot_src, E * C, 4, who, "slot_src"));
+  CHECK(need(prices, 0, 8, who, "prices"));
   // the workspace size does not depend on whether the logits are returned
   const BasePlan b = plan_base(p, !p->logits_in);
   if (workspace_bytes < b.total) return fail(MOE_ERR_WORKSPACE, "%s: workspace of %zu bytes, %zu needed", who, workspace_bytes, b.total);
@@ -624,7 +626,7 @@ moe_status moe_base_gate(const moe_base_params* p, const void* x, const void* wg
   a.counts = reinterpret_cast<int32_t*>(ws + b.off_counts);
   a.state = reinterpret_cast<BaseState*>(ws + b.off_state);
   a.range_part = reinterpret_cast<float*>(ws + b.off_range);
-  a.ids = ids; a.weights = weights; a.hist = hist;
+  a.ids = ids; a.weights = weights; a.hist = hist; a.prices_out = prices;
   BaseStats stats{};
   err = run_base_auction(a, stream, &stats);
   if (err != hipSuccess) return hip_fail(err, "moe_base_gate: auction");

@@ -158,6 +158,7 @@ struct BaseArgs {
   int32_t* ids;            // [S]
   float* weights;          // [S]
   int32_t* hist;           // [E, nb]
+  double* prices_out;      // [E] or null: final prices
 };
 
 struct BaseStats {

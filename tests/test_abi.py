@@ -38,7 +38,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_abi_version_and_struct_layout(lib):
-    assert lib.moe_abi_version() == 5
+    assert lib.moe_abi_version() == 6
     assert ctypes.sizeof(b.GateParams) == 56
     assert b.GateParams.hash_seed.offset == 40
     assert b.GateParams.temperature.offset == 48 and b.GateParams.hash_vocab.offset == 52
@@ -305,14 +305,15 @@ def test_bad_base_params_rejected(lib, bad, status):
 
 def test_base_pointer_checks(lib):
     p = hm.base_params(128, 256, 8, 16, 0, b.MOE_F32)
-    # moe_base_gate(p, x, wg, bias, logits, ids, slots, weights, counts, slot_src, ws, wsb, info, stream)
+    # moe_base_gate(p, x, wg, bias, logits, ids, slots, weights, counts, slot_src, prices, ws, wsb, info, stream)
     call = lambda prm=p, **kw: lib.moe_base_gate(
         ctypes.byref(prm), kw.get("x", A16), kw.get("wg", A16), kw.get("bias"), kw.get("logits"),
         kw.get("ids", A16), kw.get("slots", A16), kw.get("weights", A16), kw.get("counts", A16),
-        kw.get("slot_src", A16), kw.get("ws", A16), kw.get("wsb", 1 << 30), None, None)
+        kw.get("slot_src", A16), kw.get("prices"), kw.get("ws", A16), kw.get("wsb", 1 << 30), None, None)
     n = ctypes.c_size_t(0)
     assert lib.moe_base_gate_workspace_size(None, ctypes.byref(n)) == b.MOE_ERR_INVALID_ARG
-    assert lib.moe_base_gate(None, *([None] * 10), 0, None, None) == b.MOE_ERR_INVALID_ARG
+    assert lib.moe_base_gate(None, *([None] * 11), 0, None, None) == b.MOE_ERR_INVALID_ARG
+    assert call(prices=A16 + 4) == b.MOE_ERR_INVALID_ARG
     assert call(x=None) == b.MOE_ERR_INVALID_ARG
     assert call(x=A16 + 4) == b.MOE_ERR_UNSUPPORTED
     assert call(wg=None) == b.MOE_ERR_INVALID_ARG

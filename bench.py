@@ -239,17 +239,21 @@ def measured_traffic(workload_name, op, sha):
 
 def cpu_baseline(w, target_s=12.0):
     """The oracle, untuned, on a bounded sample of the same workload (its first
-    S_s tokens, capacity scaled the same way), timed on this host."""
+    S_s tokens, capacity scaled the same way), timed on this host, stage by
+    stage; for learned gates the fp64 projection (a numpy BLAS product) is also
+    timed with the BLAS pool limited to one thread."""
     import math
 
     import oracle
     from paper_2203_14685_amd import workloads as wl
     try:
-        from threadpoolctl import threadpool_info
+        from threadpoolctl import threadpool_info, threadpool_limits
         blas_threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
     except Exception:  # threadpoolctl missing: report the host's count
+        threadpool_limits = None
         blas_threads = os.cpu_count() or 1
     k, E, d, dt = w["k"], w["E"], w["d"], w["dtype"]
+    learned = w["kind"] != 2
 
     def run(S_s):
         C_s = int(math.ceil(w["cf"] * k * S_s / E))
@@ -258,21 +262,49 @@ def cpu_baseline(w, target_s=12.0):
         t0 = time.perf_counter()
         g = oracle.gate(w["kind"], k, E, C_s, normalize=w["normalize"], dtype=dt, x=inp["x"], wg=inp["wg"],
                         bias=inp["bias"], token_ids=inp["token_ids"], hash_seed=0)
+        t1 = time.perf_counter()
         xe = oracle.dispatch(inp["x"], g["slot_src"], k)
+        t2 = time.perf_counter()
         oracle.combine(xe, g["ids"], g["slots"], g["weights"], dt)
-        dye, _, _, _ = oracle.combine_bwd(dy, xe, g["slot_src"], g["weights"], k, dt, want_dw=w["kind"] != 2)
+        t3 = time.perf_counter()
+        dye, _, _, _ = oracle.combine_bwd(dy, xe, g["slot_src"], g["weights"], k, dt, want_dw=learned)
+        t4 = time.perf_counter()
         oracle.dispatch_bwd(dye, g["ids"], g["slots"], dt)
-        return time.perf_counter() - t0
+        t5 = time.perf_counter()
+        st = {"gate": t1 - t0, "dispatch": t2 - t1, "combine": t3 - t2, "combine_bwd": t4 - t3, "dispatch_bwd": t5 - t4}
+        return t5 - t0, st, inp
 
     S_s = 512
-    t = run(S_s)
+    t, st, inp = run(S_s)
     while t < target_s / 2 and S_s * 2 <= w["S"]:
         S_s *= 2
-        t = run(S_s)
-    cores = blas_threads if w["kind"] != 2 else 1
-    return {"value": round(S_s / t, 1), "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"first {S_s} of {w['S']} tokens of the same workload (capacity scaled alike), "
-                      f"full pass gate+dispatch+combine+combine_bwd+dispatch_bwd in {t:.2f} s, fp64 numpy"}
+        t, st, inp = run(S_s)
+    out = {"value": round(S_s / t, 1), "unit": "tokens/s", "cores": int(blas_threads if learned else 1),
+           "kind": "oracle",
+           "sample": f"first {S_s} of {w['S']} tokens of the same workload (capacity scaled alike), "
+                     f"full pass gate+dispatch+combine+combine_bwd+dispatch_bwd in {t:.2f} s, fp64 numpy",
+           "stage_s": {key: round(v, 3) for key, v in st.items()}}
+    if learned:
+        # the projection alone (numpy BLAS, fp64) with the whole pool and with one thread
+        pt = {}
+        for n in sorted({blas_threads, 1}, reverse=True):
+            if threadpool_limits is None and n != blas_threads:
+                continue
+            t0 = time.perf_counter()
+            if threadpool_limits is not None:
+                with threadpool_limits(limits=n, user_api="blas"):
+                    oracle.logits(inp["x"], inp["wg"], dt, inp["bias"])
+            else:
+                oracle.logits(inp["x"], inp["wg"], dt, inp["bias"])
+            pt[str(n)] = round(time.perf_counter() - t0, 3)
+        out["projection_s_by_threads"] = pt
+    try:
+        out["host"] = {"cpus_allowed": len(os.sched_getaffinity(0)),
+                       "model": next((ln.split(":", 1)[1].strip() for ln in open("/proc/cpuinfo")
+                                      if ln.startswith("model name")), "unknown")}
+    except OSError:
+        pass
+    return out
 
 
 def main():

@@ -228,6 +228,24 @@ def test_base_capacity_and_layout():
     print(f"[stats] base capacity: {st}", flush=True)
 
 
+def test_base_zero_capacity_and_bidder_cap():
+    """C = 0: the assignment is still balanced and every slot dropped.  E = 2 with
+    c = 2048: the first rounds have more bidders per expert than a round takes
+    (2048), so the later ones wait for the next round."""
+    announce("base C = 0, E = 2 with c = 2048")
+    S, E = 1024, 8
+    L = np.random.default_rng(21).standard_normal((S, E)).astype(np.float32)
+    g = run_base(L=L, E=E, C=0)
+    assert_equal(np.bincount(g["ids"][:, 0], minlength=E), np.full(E, S // E), "tokens per expert")
+    assert (g["slots"] == -1).all() and (g["counts"] == 0).all() and g["slot_src"].size == 0
+    certify(L.astype(np.float64), g, E)
+    S, E = 4096, 2
+    L = np.random.default_rng(22).standard_normal((S, E)).astype(np.float32)
+    g = run_base(L=L, E=E)
+    st = check_base(L.astype(np.float64), g, E, S // E)
+    print(f"[stats] base E=2 c=2048: {st}", flush=True)
+
+
 def test_base_empty():
     announce("base S=0")
     out = hm.base_gate(8, 4, logits=torch.empty((0, 8), dtype=torch.float32, device="cuda"), logits_in=True)

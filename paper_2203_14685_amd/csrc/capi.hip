@@ -446,14 +446,11 @@ moe_status moe_gate(const moe_gate_params* p, const void* x, const void* wg, con
   ScanArgs sa{};
   sa.E = p->E; sa.k = p->k; sa.nb = nb; sa.C = p->capacity;
   sa.hist = hist; sa.counts = counts; sa.demand = demand; sa.slot_src = slot_src;
-  err = launch_scan(sa, stream);
-  if (err != hipSuccess) return hip_fail(err, "moe_gate: scan kernel launch");
-
   AssignArgs aa{};
   aa.S = p->S; aa.E = p->E; aa.k = p->k; aa.nb = nb; aa.C = p->capacity;
   aa.ids = ids; aa.offs = hist; aa.slots = slots; aa.slot_src = slot_src;
-  err = launch_assign(aa, stream);
-  if (err != hipSuccess) return hip_fail(err, "moe_gate: assign kernel launch");
+  err = launch_scan_assign(sa, aa, stream);
+  if (err != hipSuccess) return hip_fail(err, "moe_gate: scan / assign kernel launch");
   return ok();
 }
 
@@ -638,13 +635,11 @@ moe_status moe_base_gate(const moe_base_params* p, const void* x, const void* wg
   ScanArgs sa{};
   sa.E = p->E; sa.k = 1; sa.nb = nb; sa.C = p->capacity;
   sa.hist = hist; sa.counts = counts; sa.demand = nullptr; sa.slot_src = slot_src;
-  err = launch_scan(sa, stream);
-  if (err != hipSuccess) return hip_fail(err, "moe_base_gate: scan kernel launch");
   AssignArgs aa{};
   aa.S = p->S; aa.E = p->E; aa.k = 1; aa.nb = nb; aa.C = p->capacity;
   aa.ids = ids; aa.offs = hist; aa.slots = slots; aa.slot_src = slot_src;
-  err = launch_assign(aa, stream);
-  if (err != hipSuccess) return hip_fail(err, "moe_base_gate: assign kernel launch");
+  err = launch_scan_assign(sa, aa, stream);
+  if (err != hipSuccess) return hip_fail(err, "moe_base_gate: scan / assign kernel launch");
   return ok();
 }
 

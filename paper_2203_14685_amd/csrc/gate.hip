@@ -228,6 +228,103 @@ __global__ __launch_bounds__(kBlock) void assign_kernel(AssignArgs a) {
   }
 }
 
+// ---------------------------------------------------------------- scan + assign in one launch
+// For small histograms (k * E * nb entries): every block takes its own four
+// wave blocks and works out their offsets itself, from per-(rank, expert)
+// sums over the histogram rows: all earlier ranks of the expert in full, then
+// this rank's earlier wave blocks.  The same ranks as the scan kernel followed
+// by the assign kernel; block 0 also writes counts and demand, and the blocks
+// share marking the empty slots.
+constexpr int kFusedMaxEntries = 16384;  // k * E * nb
+constexpr int kFusedMaxBlocks = 1024;    // nb
+constexpr int kFusedMaxPairs = 1024;     // k * E
+
+__global__ __launch_bounds__(kBlock) void scan_assign_kernel(ScanArgs sa, AssignArgs a) {
+  constexpr int kSeg = 16;  // wave blocks per partial sum
+  constexpr int kMaxItems = kFusedMaxEntries / kSeg + kFusedMaxPairs;
+  __shared__ int tot[kFusedMaxPairs];                    // [k][E] assignments per rank and expert
+  __shared__ int pre[kFusedMaxPairs];                    // [k][E] before this block's first wave block
+  __shared__ int offs[kWavesPerBlock * kFusedMaxPairs];  // [wave][k][E] offsets of its wave block
+  __shared__ int ptot[kMaxItems], ppre[kMaxItems];       // partial sums over kSeg wave blocks
+  const int k = a.k, E = a.E, nb = a.nb;
+  const int wb0 = blockIdx.x * kWavesPerBlock;
+  const int pairs = k * E;
+  const int nseg = (nb + kSeg - 1) / kSeg;
+  const int items = pairs * nseg;
+  for (int it = threadIdx.x; it < items; it += kBlock) {
+    const int q = it / nseg, sg = it % nseg;
+    const int32_t* row = a.offs + static_cast<int64_t>(q) * nb;  // the histogram (counts)
+    int t = 0, p = 0;
+#pragma unroll
+    for (int j = 0; j < kSeg; ++j) {
+      const int b = sg * kSeg + j;
+      const int v = b < nb ? row[b] : 0;
+      t += v;
+      if (b < wb0) p += v;
+    }
+    ptot[it] = t;
+    ppre[it] = p;
+  }
+  __syncthreads();
+  for (int q = threadIdx.x; q < pairs; q += kBlock) {
+    int t = 0, p = 0;
+    for (int sg = 0; sg < nseg; ++sg) {
+      t += ptot[q * nseg + sg];
+      p += ppre[q * nseg + sg];
+    }
+    tot[q] = t;
+    pre[q] = p;
+  }
+  __syncthreads();
+  for (int q = threadIdx.x; q < pairs; q += kBlock) {
+    const int r = q / E, e = q % E;
+    int base = pre[q];
+    for (int r2 = 0; r2 < r; ++r2) base += tot[r2 * E + e];  // rank-major: earlier ranks first
+    const int32_t* row = a.offs + static_cast<int64_t>(q) * nb;
+    for (int w = 0; w < kWavesPerBlock; ++w) {
+      offs[w * pairs + q] = base;
+      if (wb0 + w < nb) base += row[wb0 + w];
+    }
+  }
+  __syncthreads();
+  if (blockIdx.x == 0) {
+    for (int e = threadIdx.x; e < E; e += kBlock) {
+      int t = 0;
+      for (int r = 0; r < k; ++r) t += tot[r * E + e];
+      sa.counts[e] = min(t, a.C);
+      if (sa.demand) sa.demand[e] = t;
+    }
+  }
+  // empty slots, experts dealt to the blocks in turn
+  for (int e = blockIdx.x; e < E; e += gridDim.x) {
+    int t = 0;
+    for (int r = 0; r < k; ++r) t += tot[r * E + e];
+    for (int c = min(t, a.C) + threadIdx.x; c < a.C; c += kBlock) a.slot_src[static_cast<int64_t>(e) * a.C + c] = -1;
+  }
+  // ranks inside each wave block, as in assign_kernel
+  const int w = threadIdx.x / kWave;
+  const int wb = wb0 + w;
+  if (wb >= nb) return;
+  const int64_t s = static_cast<int64_t>(wb) * kWave + lane_id();
+  const bool valid = s < a.S;
+  const int nbits = 32 - __clz(E);
+  for (int r = 0; r < k; ++r) {
+    const int e = valid ? a.ids[s * k + r] : E;
+    uint64_t same = ~0ull;
+    for (int bit = 0; bit < nbits; ++bit) {
+      const bool on = (e >> bit) & 1;
+      const uint64_t bal = __ballot(on);
+      same &= on ? bal : ~bal;
+    }
+    if (valid) {
+      const int pos = offs[w * pairs + r * E + e] + popc_below(same);
+      const bool kept = pos < a.C;
+      a.slots[s * k + r] = kept ? pos : -1;
+      if (kept) a.slot_src[static_cast<int64_t>(e) * a.C + pos] = static_cast<int>(s * k + r);
+    }
+  }
+}
+
 // ---------------------------------------------------------------- launchers
 int device_cu_count() {
   static int cached[64] = {0};
@@ -259,6 +356,18 @@ hipError_t launch_route(const RouteArgs& a, hipStream_t st) {
 hipError_t launch_scan(const ScanArgs& a, hipStream_t st) {
   scan_kernel<<<dim3(a.E), dim3(kScanThreads), 0, st>>>(a);
   return hipGetLastError();
+}
+
+hipError_t launch_scan_assign(const ScanArgs& sa, const AssignArgs& a, hipStream_t st) {
+  const int64_t pairs = static_cast<int64_t>(a.k) * a.E;
+  if (a.nb > 0 && a.nb <= kFusedMaxBlocks && pairs <= kFusedMaxPairs && pairs * a.nb <= kFusedMaxEntries) {
+    const unsigned blocks = static_cast<unsigned>((a.nb + kWavesPerBlock - 1) / kWavesPerBlock);
+    scan_assign_kernel<<<dim3(blocks), dim3(kBlock), 0, st>>>(sa, a);
+    return hipGetLastError();
+  }
+  hipError_t err = launch_scan(sa, st);
+  if (err != hipSuccess) return err;
+  return launch_assign(a, st);
 }
 
 hipError_t launch_assign(const AssignArgs& a, hipStream_t st) {

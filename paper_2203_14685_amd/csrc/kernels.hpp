@@ -79,6 +79,9 @@ int device_cu_count();
 bool route_uses_mfma_rs(const RouteArgs& a);
 hipError_t launch_scan(const ScanArgs& a, hipStream_t st);
 hipError_t launch_assign(const AssignArgs& a, hipStream_t st);
+// Scan and assign, in one launch when the histogram is small (the offsets then
+// stay out of the histogram, which is left as the counts).
+hipError_t launch_scan_assign(const ScanArgs& sa, const AssignArgs& a, hipStream_t st);
 hipError_t launch_dispatch(const RowArgs& a, hipStream_t st);
 hipError_t launch_combine(const RowArgs& a, bool weighted, hipStream_t st);
 hipError_t launch_combine_bwd(const RowArgs& a, hipStream_t st);

@@ -63,7 +63,7 @@ extern "C" {
 typedef enum {
   MOE_OK = 0,
   MOE_ERR_INVALID_ARG = 1, /* a size, pointer or option is out of the contract */
-  MOE_ERR_UNSUPPORTED = 2, /* valid request this build does not handle (alignment, row size) */
+  MOE_ERR_UNSUPPORTED = 2, /* valid request the library does not handle (alignment, row size) */
   MOE_ERR_WORKSPACE = 3,   /* workspace NULL or smaller than moe_gate_workspace_size() */
   MOE_ERR_HIP = 4,         /* a HIP runtime call failed; see moe_last_error() */
   MOE_ERR_NOT_CONVERGED = 5 /* moe_base_gate: the auction reached its round limit */

@@ -22,8 +22,8 @@ paper it follows:
 * the BASE layer's balanced assignment (Sec. 3.1, the equation of the BASE
   Layer paragraph).
 
-Where the paper is silent the oracle takes one fixed reading; each is named at
-the function that depends on it (R1..R14 in the design notes).
+Where the paper is silent the oracle takes one fixed reading, numbered R1,
+R2, ...; each is stated at the function that depends on it.
 
 Parity status: every function here is pinned by ``tests/test_oracle_pins.py``
 against hand-computed cases, brute force, closed forms, library routines or a

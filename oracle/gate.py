@@ -11,7 +11,7 @@ Steps, each in the paper's order:
 * assign_slots-- the expert capacity of Sec. 3.1 (GShard/Switch capacity factor):
                  each expert keeps at most C tokens; the rest are dropped.
 
-Readings taken where the paper is silent (named R1..R14 in the design notes):
+Readings taken where the paper is silent (numbered as in the rest of the oracle):
 
 R1  Eq. 1 normalises over the K selected logits (``normalize=1``).  For the
     Switch gate (K=1) that would make every weight 1, so ``normalize=0`` gives

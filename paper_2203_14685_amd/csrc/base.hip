@@ -24,6 +24,7 @@
 namespace hetumoe {
 
 constexpr int kBaseThreads = 1024;                  // resolve: one block per expert
+constexpr int kBaseSortFrom = 256;                  // more bidders than this: sort instead of counting
 constexpr int kBaseWaves = kBaseThreads / kWave;    // 16
 constexpr int kBaseIters = 32;                      // token tiles of kBaseThreads per collection pass
 
@@ -167,6 +168,42 @@ __global__ __launch_bounds__(kBlock) void base_bid_kernel(BaseArgs a, int r) {
 }
 
 // ---------------------------------------------------------------- resolve
+// n a power of two, at most 2 * kBaseThreads: (v, t) pairs sorted into
+// (bid desc, token asc) by a bitonic network, a barrier per stage.
+__device__ __forceinline__ void base_sort(double* v, int* t, int n) {
+  for (int size = 2; size <= n; size <<= 1) {
+    for (int stride = size / 2; stride > 0; stride >>= 1) {
+      const int i = threadIdx.x;
+      if (i < n / 2) {
+        const int lo = 2 * i - (i & (stride - 1));
+        const int hi = lo + stride;
+        const bool desc = (lo & size) == 0;
+        const bool swap = desc ? base_before(v[hi], t[hi], v[lo], t[lo]) : base_before(v[lo], t[lo], v[hi], t[hi]);
+        if (swap) {
+          const double tv = v[lo];
+          v[lo] = v[hi];
+          v[hi] = tv;
+          const int tt = t[lo];
+          t[lo] = t[hi];
+          t[hi] = tt;
+        }
+      }
+      __syncthreads();
+    }
+  }
+}
+
+// Entries of the sorted list (v, t)[0, n) ahead of (w, u).
+__device__ __forceinline__ int base_rank_in(const double* v, const int* t, int n, double w, int u) {
+  int lo = 0, hi = n;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (base_before(v[mid], t[mid], w, u)) lo = mid + 1;
+    else hi = mid;
+  }
+  return lo;
+}
+
 // One block per expert.  Block 0 first advances the state.  A round that began
 // with no unassigned token ends the phase: the final phase marks the auction
 // done, an earlier one lowers eps and clears holders and assignments (every
@@ -286,7 +323,44 @@ __global__ __launch_bounds__(kBaseThreads) void base_resolve_kernel(BaseArgs a, 
   }
   const int nb = min(have, kBaseCand);
   if (tid == 0) a.bid_cnt[e] = 0;  // for the next round (every thread has read it)
-  // ranks in the union of holders (sorted) and bidders (unsorted)
+  if (nb > kBaseSortFrom) {
+    // many bidders (the first rounds of a phase): sort them, then each entry's
+    // rank in the union is its own index plus its rank in the other list
+    int np2 = 1;
+    while (np2 < nb) np2 <<= 1;
+    for (int i = nb + tid; i < np2; i += kBaseThreads) {
+      bv[i] = -INFINITY;
+      bt[i] = 0x7fffffff;
+    }
+    __syncthreads();
+    base_sort(bv, bt, np2);
+    for (int i = tid; i < nh; i += kBaseThreads) {
+      const double v = hv[i];
+      const int t = ht[i];
+      const int r_ = i + base_rank_in(bv, bt, nb, v, t);
+      if (r_ < c) {
+        a.hold_v[base + r_] = v;
+        a.hold_t[base + r_] = t;
+        if (r_ == c - 1) a.price[e] = v;
+      } else {
+        a.assign[t] = -1;  // evicted
+      }
+    }
+    for (int j = tid; j < nb; j += kBaseThreads) {
+      const double v = bv[j];
+      const int t = bt[j];
+      const int r_ = j + base_rank_in(hv, ht, nh, v, t);
+      if (r_ < c) {
+        a.hold_v[base + r_] = v;
+        a.hold_t[base + r_] = t;
+        a.assign[t] = e;
+        if (r_ == c - 1) a.price[e] = v;
+      }
+    }
+    if (tid == 0) a.hold_n[e] = min(c, nh + nb);
+    return;
+  }
+  // few bidders: ranks in the union of holders (sorted) and bidders (unsorted) by counting
   for (int i = tid; i < nh; i += kBaseThreads) {
     const double v = hv[i];
     const int t = ht[i];

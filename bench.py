@@ -34,18 +34,38 @@ OPS_KERNELS = ("dispatch", "combine", "combine_bwd", "dispatch_bwd", "gate")
 
 def kernel_of_op(op, w):
     """(kernel symbol fragment in traces, sources that kernel is compiled from) of
-    the one kernel an op launches for workload dict `w`: with several choices per
-    token dispatch and combine backward scatter token-major."""
+    the one kernel an op launches for workload dict `w`, following the launch
+    rules of the layout library: with several choices per token dispatch and
+    combine backward scatter token-major; with one, both run the flat
+    one-chunk-per-thread form (combine backward with dw only on rows of 64 to
+    1024 chunks, a power of two); combine and dispatch backward run the flat form
+    for k <= 2 on rows of up to 128 chunks, several tokens per wave on rows of
+    64, 128 or 256 chunks otherwise, one token per wave beyond."""
     elt = "hetumoe::bf16_t" if w["dtype"] == "bf16" else "float"
-    scatter = w["k"] > 1
-    # rows of 64, 128 or 256 16-byte chunks combine several tokens per wave
+    k = w["k"]
     nch = w["d"] * (2 if w["dtype"] == "bf16" else 4) // 16
-    short = nch in (64, 128, 256) and w["E"] * w["C"] > 0
-    comb = f"combine_short_kernel<{elt}, " if short else f"combine_kernel<{elt}, "
-    return {"dispatch": ("dispatch_scatter_kernel" if scatter else "dispatch_kernel", _LAYOUT_SRC),
-            "combine": (comb + ("true," if short else "true>"), _LAYOUT_SRC),
-            "combine_bwd": ("combine_bwd_scatter_kernel" if scatter else "combine_bwd_kernel", _LAYOUT_SRC),
-            "dispatch_bwd": (comb + ("false," if short else "false>"), _LAYOUT_SRC),
+    pow2 = nch > 0 and (nch & (nch - 1)) == 0
+    p2 = "true" if pow2 else "false"
+    dw = w["kind"] != 2  # learned gates have weights to differentiate (hash: none)
+    if k > 1:
+        cbwd = "combine_bwd_scatter_kernel"
+    elif dw and not (pow2 and 64 <= nch <= 1024):
+        cbwd = f"combine_bwd_kernel<{elt}, true>"
+    else:
+        cbwd = f"combine_bwd_flat_kernel<{elt}, {'true' if dw else p2}, {'true' if dw else 'false'}>"
+
+    def comb(weighted):
+        t = "true" if weighted else "false"
+        if k <= 2 and nch <= 128:
+            return f"combine_flat_kernel<{elt}, {p2}, {t}, {k}>"
+        if nch in (64, 128, 256) and w["E"] * w["C"] > 0:
+            return f"combine_short_kernel<{elt}, {t}, "
+        return f"combine_kernel<{elt}, {t}>"
+
+    return {"dispatch": ("dispatch_scatter_kernel" if k > 1 else f"dispatch_flat_kernel<{p2}>", _LAYOUT_SRC),
+            "combine": (comb(True), _LAYOUT_SRC),
+            "combine_bwd": (cbwd, _LAYOUT_SRC),
+            "dispatch_bwd": (comb(False), _LAYOUT_SRC),
             "gate": ("route_", _GATE_SRC)}[op]
 
 

@@ -5,9 +5,17 @@
 // combine backward) are gathers over slots for k = 1 and token-major scatters
 // for k > 1, so that each token row is read once.
 //
-// One wavefront owns one output row and walks it in 16-byte chunks (64 lanes x
-// 16 B = 1 KiB per instruction), issuing up to kUnroll loads per lane before
-// the first store so that enough bytes are in flight to cover HBM latency.
+// Two row forms.  The flat form (the [E,C,d] gathers for k = 1, and the
+// token-order gathers for k <= 2 over rows of up to 2 KiB) gives every thread
+// one 16-byte chunk of the flattened output per step, two steps per thread, so
+// a block of 512 threads writes 16 KiB and lives briefly.  The wave form gives
+// one wavefront one output row, walked in 16-byte chunks (64 lanes x 16 B =
+// 1 KiB per instruction) with up to kUnroll loads per lane in flight before
+// the first store.  On MI355X many short-lived waves with few stores each kept
+// more writes in flight than long row walks (a 1 GiB fill: 6.8 TB/s with one
+// store per thread against 5.7 TB/s with eight), which is why the writers of
+// [E,C,d] use the flat form; the wave form stays where it measured faster
+// (8 KiB token rows, k >= 3, and the token-major scatters).
 // Every output row is written with non-temporal stores: the buffers are far
 // larger than the 256 MB Infinity Cache, and plain stores leave dirty lines there
 // whose write-back then slows whichever kernel runs next (measured: dispatch
@@ -26,34 +34,57 @@ constexpr int kCombineWaves = 4;
 
 __device__ __forceinline__ void store_nt(u32x4* p, const u32x4& v) { __builtin_nontemporal_store(v, p); }
 
-// ---------------------------------------------------------------- dispatch
-// xe[row] = x[slot_src[row] / k], or zeros for an empty slot.
-__global__ __launch_bounds__(kWideWaves * kWave) void dispatch_kernel(RowArgs a) {
-  const int64_t row = static_cast<int64_t>(blockIdx.x) * kWideWaves + threadIdx.x / kWave;
-  if (row >= a.rows) return;
-  const int lane = lane_id();
-  const int nch = a.nch;
-  const int src = a.slot_src[row];
-  u32x4* dst = reinterpret_cast<u32x4*>(a.dst) + row * nch;
-  // entries outside [0, S*k) are out of contract and treated as empty slots
-  if (src >= 0 && src < a.S * a.k) {
-    const u32x4* srow = reinterpret_cast<const u32x4*>(a.src) + static_cast<int64_t>(src / a.k) * nch;
-    for (int base = 0; base < nch; base += kWave * kUnroll) {
-      u32x4 v[kUnroll];
-#pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        const int i = base + u * kWave + lane;
-        if (i < nch) v[u] = srow[i];
-      }
-#pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        const int i = base + u * kWave + lane;
-        if (i < nch) store_nt(dst + i, v[u]);
-      }
-    }
+// ---------------------------------------------------------------- flat form
+constexpr int kFlatThreads = 512;
+constexpr int kFlatPer = 2;                          // chunks per thread
+constexpr int kFlatChunks = kFlatThreads * kFlatPer;  // chunks per block
+constexpr int kFlatWaves = kFlatThreads / kWave;
+
+// Row and column of chunk gb + off of a flattened [rows, nch] output, where gb
+// is the block's first chunk (row_b, col_b precomputed) and off < kFlatChunks.
+// POW2: nch = 1 << lg.
+template <bool POW2>
+__device__ __forceinline__ void flat_pos(int64_t gb, int64_t row_b, int col_b, int off, int nch, int lg, int64_t& row,
+                                         int& col) {
+  if constexpr (POW2) {
+    const int64_t g = gb + off;
+    row = g >> lg;
+    col = static_cast<int>(g & (nch - 1));
   } else {
-    const u32x4 z = {0u, 0u, 0u, 0u};
-    for (int i = lane; i < nch; i += kWave) store_nt(dst + i, z);
+    const unsigned t = static_cast<unsigned>(col_b + off);
+    const unsigned q = t / static_cast<unsigned>(nch);
+    row = row_b + q;
+    col = static_cast<int>(t - q * static_cast<unsigned>(nch));
+  }
+}
+
+// ---------------------------------------------------------------- dispatch
+// xe[row] = x[slot_src[row] / k], or zeros for an empty slot.  Flat form for
+// k = 1 (k > 1 uses the token-major scatter further down).
+template <bool POW2>
+__global__ __launch_bounds__(kFlatThreads) void dispatch_flat_kernel(RowArgs a, int lg, int64_t total) {
+  const int nch = a.nch;
+  const int64_t gb = static_cast<int64_t>(blockIdx.x) * kFlatChunks;
+  const int64_t row_b = POW2 ? 0 : gb / nch;
+  const int col_b = POW2 ? 0 : static_cast<int>(gb - row_b * nch);
+  const u32x4* x = reinterpret_cast<const u32x4*>(a.src);
+  u32x4* xe = reinterpret_cast<u32x4*>(a.dst);
+  u32x4 v[kFlatPer];
+#pragma unroll
+  for (int u = 0; u < kFlatPer; ++u) {
+    const int off = u * kFlatThreads + static_cast<int>(threadIdx.x);
+    int64_t row;
+    int col;
+    flat_pos<POW2>(gb, row_b, col_b, off, nch, lg, row, col);
+    // entries outside [0, S) are out of contract and treated as empty slots
+    const int src = gb + off < total ? a.slot_src[row] : -1;
+    v[u] = u32x4{0u, 0u, 0u, 0u};
+    if (src >= 0 && src < a.S) v[u] = x[static_cast<int64_t>(src) * nch + col];
+  }
+#pragma unroll
+  for (int u = 0; u < kFlatPer; ++u) {
+    const int64_t g = gb + u * kFlatThreads + static_cast<int>(threadIdx.x);
+    if (g < total) store_nt(xe + g, v[u]);
   }
 }
 
@@ -164,6 +195,56 @@ __global__ __launch_bounds__(kCombineWaves * kWave) void combine_short_kernel(Ro
   }
 }
 
+// Flat form of the two above for k <= KMAX <= 2: each thread combines one
+// 16-byte chunk of a token row per step, the choices' loads issued together.
+template <typename T, bool POW2, bool WEIGHTED, int KMAX>
+__global__ __launch_bounds__(kFlatThreads) void combine_flat_kernel(RowArgs a, int lg, int64_t total) {
+  constexpr int kEl = Chunk<T>::kElems;
+  const int nch = a.nch, k = a.k;
+  const int64_t gb = static_cast<int64_t>(blockIdx.x) * kFlatChunks;
+  const int64_t row_b = POW2 ? 0 : gb / nch;
+  const int col_b = POW2 ? 0 : static_cast<int>(gb - row_b * nch);
+  const u32x4* ye = reinterpret_cast<const u32x4*>(a.src);
+  u32x4* out = reinterpret_cast<u32x4*>(a.dst);
+#pragma unroll
+  for (int u = 0; u < kFlatPer; ++u) {
+    const int off = u * kFlatThreads + static_cast<int>(threadIdx.x);
+    if (gb + off >= total) continue;
+    int64_t s;
+    int col;
+    flat_pos<POW2>(gb, row_b, col_b, off, nch, lg, s, col);
+    u32x4 v[KMAX];
+    float w[KMAX];
+    bool ok[KMAX];
+#pragma unroll
+    for (int r = 0; r < KMAX; ++r) {
+      ok[r] = false;
+      w[r] = 1.f;
+      v[r] = u32x4{0u, 0u, 0u, 0u};
+      if (r < k) {
+        const int slot = a.slots[s * k + r];
+        const int e = a.ids[s * k + r];
+        // dropped choices (slot -1) and out-of-contract entries contribute nothing
+        ok[r] = slot >= 0 && slot < a.C && e >= 0 && e < a.E;
+        if (WEIGHTED) w[r] = a.weights[s * k + r];
+        if (ok[r]) v[r] = ye[(static_cast<int64_t>(e) * a.C + slot) * nch + col];
+      }
+    }
+    float acc[kEl];
+#pragma unroll
+    for (int q = 0; q < kEl; ++q) acc[q] = 0.f;
+#pragma unroll
+    for (int r = 0; r < KMAX; ++r) {
+      if (!ok[r]) continue;
+      float f[kEl];
+      Chunk<T>::unpack(v[r], f);
+#pragma unroll
+      for (int q = 0; q < kEl; ++q) acc[q] = WEIGHTED ? fmaf(w[r], f[q], acc[q]) : acc[q] + f[q];
+    }
+    store_nt(out + gb + off, Chunk<T>::pack(acc));
+  }
+}
+
 // ---------------------------------------------------------------- combine backward
 // Rows [0, rows): dye[row] = w[src] * dy[src / k] (zeros for an empty slot) and,
 // with DW, dw[src] = <dy[src / k], ye[row]>.  Blocks past the row blocks clear
@@ -225,6 +306,96 @@ __global__ __launch_bounds__(kWideWaves * kWave) void combine_bwd_kernel(RowArgs
   if constexpr (DW) {
     dot = wave_sum(dot);
     if (lane == 0) a.dw[src] = dot;
+  }
+}
+
+// Flat form of the kernel above for k = 1.  With DW the row length must be a
+// power of two between 64 chunks (one wave) and kFlatChunks, so that every
+// wave lies inside one row and every row inside one block: each wave sums its
+// part of <dy, ye>, and one thread per row adds the parts of its waves in
+// order.  Blocks past the row blocks clear dw of dropped choices.
+template <typename T, bool POW2, bool DW>
+__global__ __launch_bounds__(kFlatThreads) void combine_bwd_flat_kernel(RowArgs a, int lg, int64_t total,
+                                                                        int64_t row_blocks) {
+  constexpr int kEl = Chunk<T>::kElems;
+  if (static_cast<int64_t>(blockIdx.x) >= row_blocks) {
+    if constexpr (DW) {
+      const int64_t i = (static_cast<int64_t>(blockIdx.x) - row_blocks) * kFlatThreads + threadIdx.x;
+      if (i < a.S && a.slots[i] < 0) a.dw[i] = 0.f;
+    }
+    return;
+  }
+  const int nch = a.nch;
+  const int64_t gb = static_cast<int64_t>(blockIdx.x) * kFlatChunks;
+  const int64_t row_b = POW2 ? 0 : gb / nch;
+  const int col_b = POW2 ? 0 : static_cast<int>(gb - row_b * nch);
+  const u32x4* dy = reinterpret_cast<const u32x4*>(a.src);
+  const u32x4* ye = reinterpret_cast<const u32x4*>(a.aux);
+  u32x4* dye = reinterpret_cast<u32x4*>(a.dst);
+  u32x4 v[kFlatPer];
+  u32x4 ve[DW ? kFlatPer : 1];
+  float w[kFlatPer];
+  bool ok[kFlatPer];
+#pragma unroll
+  for (int u = 0; u < kFlatPer; ++u) {
+    const int off = u * kFlatThreads + static_cast<int>(threadIdx.x);
+    int64_t row;
+    int col;
+    flat_pos<POW2>(gb, row_b, col_b, off, nch, lg, row, col);
+    // entries outside [0, S) are out of contract and treated as empty slots
+    const int src = gb + off < total ? a.slot_src[row] : -1;
+    ok[u] = src >= 0 && src < a.S;
+    v[u] = u32x4{0u, 0u, 0u, 0u};
+    w[u] = 0.f;
+    if constexpr (DW) ve[u] = u32x4{0u, 0u, 0u, 0u};
+    if (ok[u]) {
+      v[u] = dy[static_cast<int64_t>(src) * nch + col];
+      w[u] = a.weights[src];
+      if constexpr (DW) ve[u] = ye[gb + off];
+    }
+  }
+  float dot[kFlatPer];
+#pragma unroll
+  for (int u = 0; u < kFlatPer; ++u) {
+    const int64_t g = gb + u * kFlatThreads + static_cast<int>(threadIdx.x);
+    dot[u] = 0.f;
+    if (g >= total) continue;
+    if (!ok[u]) {  // empty slot: zeros, no arithmetic
+      store_nt(dye + g, u32x4{0u, 0u, 0u, 0u});
+      continue;
+    }
+    float f[kEl];
+    Chunk<T>::unpack(v[u], f);
+    if constexpr (DW) {
+      float gq[kEl];
+      Chunk<T>::unpack(ve[u], gq);
+#pragma unroll
+      for (int q = 0; q < kEl; ++q) dot[u] = fmaf(f[q], gq[q], dot[u]);
+    }
+#pragma unroll
+    for (int q = 0; q < kEl; ++q) f[q] *= w[u];
+    store_nt(dye + g, Chunk<T>::pack(f));
+  }
+  if constexpr (DW) {
+    __shared__ float part[kFlatPer * kFlatWaves];  // [u][wave]: chunk offset / 64
+    const int wave = threadIdx.x / kWave;
+#pragma unroll
+    for (int u = 0; u < kFlatPer; ++u) {
+      const float t = wave_sum(dot[u]);
+      if (lane_id() == 0) part[u * kFlatWaves + wave] = t;
+    }
+    __syncthreads();
+    const int rows_here = kFlatChunks >> lg;
+    const int parts = nch / kWave;
+    if (static_cast<int>(threadIdx.x) < rows_here) {
+      const int64_t row = (gb >> lg) + threadIdx.x;
+      if (row < a.rows) {
+        float t = 0.f;
+        for (int j = 0; j < parts; ++j) t += part[threadIdx.x * parts + j];
+        const int src = a.slot_src[row];
+        if (src >= 0 && src < a.S) a.dw[src] = t;
+      }
+    }
   }
 }
 
@@ -377,6 +548,18 @@ static unsigned zero_blocks(int64_t rows) {
   return static_cast<unsigned>(b < kZeroBlocks ? b : kZeroBlocks);
 }
 
+// log2(n) for a power of two, else -1
+static inline int pow2_log(int n) {
+  if (n <= 0 || (n & (n - 1)) != 0) return -1;
+  int lg = 0;
+  while ((1 << lg) < n) ++lg;
+  return lg;
+}
+
+static inline unsigned flat_blocks(int64_t total) {
+  return static_cast<unsigned>((total + kFlatChunks - 1) / kFlatChunks);
+}
+
 hipError_t launch_dispatch(const RowArgs& a, hipStream_t st) {
   if (a.k > 1) {
     const int64_t tok_blocks = (static_cast<int64_t>(a.S) + kWideWaves - 1) / kWideWaves;
@@ -385,8 +568,12 @@ hipError_t launch_dispatch(const RowArgs& a, hipStream_t st) {
     dispatch_scatter_kernel<<<dim3(grid), dim3(kWideWaves * kWave), 0, st>>>(a, tok_blocks);
     return hipGetLastError();
   }
-  if (a.rows == 0) return hipSuccess;
-  dispatch_kernel<<<dim3(blocks_for_rows(a.rows, kWideWaves)), dim3(kWideWaves * kWave), 0, st>>>(a);
+  const int64_t total = a.rows * a.nch;
+  if (total == 0) return hipSuccess;
+  const int lg = pow2_log(a.nch);
+  const dim3 grid(flat_blocks(total)), block(kFlatThreads);
+  if (lg >= 0) dispatch_flat_kernel<true><<<grid, block, 0, st>>>(a, lg, total);
+  else dispatch_flat_kernel<false><<<grid, block, 0, st>>>(a, lg, total);
   return hipGetLastError();
 }
 
@@ -399,8 +586,36 @@ static void launch_combine_short(const RowArgs& a, hipStream_t st) {
   else combine_short_kernel<T, WEIGHTED, 4><<<grid, block, 0, st>>>(a);
 }
 
+template <typename T, bool POW2, bool WEIGHTED>
+static void launch_combine_flat_t(const RowArgs& a, int lg, int64_t total, hipStream_t st) {
+  const dim3 grid(flat_blocks(total)), block(kFlatThreads);
+  if (a.k == 1) combine_flat_kernel<T, POW2, WEIGHTED, 1><<<grid, block, 0, st>>>(a, lg, total);
+  else combine_flat_kernel<T, POW2, WEIGHTED, 2><<<grid, block, 0, st>>>(a, lg, total);
+}
+
+template <typename T>
+static void launch_combine_flat(const RowArgs& a, bool weighted, hipStream_t st) {
+  const int64_t total = a.rows * a.nch;
+  const int lg = pow2_log(a.nch);
+  if (lg >= 0) {
+    if (weighted) launch_combine_flat_t<T, true, true>(a, lg, total, st);
+    else launch_combine_flat_t<T, true, false>(a, lg, total, st);
+  } else {
+    if (weighted) launch_combine_flat_t<T, false, true>(a, lg, total, st);
+    else launch_combine_flat_t<T, false, false>(a, lg, total, st);
+  }
+}
+
 hipError_t launch_combine(const RowArgs& a, bool weighted, hipStream_t st) {
-  if (a.rows == 0) return hipSuccess;
+  if (a.rows == 0 || a.nch == 0) return hipSuccess;
+  // k <= 2 over rows of up to 2 KiB: flat form (measured 7-15 % faster than
+  // the wave forms at 1 and 2 KiB rows; 15 % slower at 4 KiB rows, and slower
+  // at 8 KiB rows and at k = 4)
+  if (a.k <= 2 && a.nch <= 128) {
+    if (a.dtype == 1) launch_combine_flat<bf16_t>(a, weighted, st);
+    else launch_combine_flat<float>(a, weighted, st);
+    return hipGetLastError();
+  }
   // short rows: several tokens per wave (measured 9-11 % faster at 2 and 4 KiB
   // rows); longer rows: one token per wave
   if ((a.nch == 64 || a.nch == 128 || a.nch == 256) && static_cast<int64_t>(a.E) * a.C > 0) {
@@ -440,8 +655,28 @@ hipError_t launch_combine_bwd(const RowArgs& a, hipStream_t st) {
     }
     return hipGetLastError();
   }
+  // k = 1: flat form, with dw where a row is a power of two of 64 to
+  // kFlatChunks chunks (else the wave form below)
+  const int lg = pow2_log(a.nch);
+  if (!a.dw || (lg >= 6 && a.nch <= kFlatChunks)) {
+    const int64_t total = a.rows * a.nch;
+    const int64_t row_blocks = flat_blocks(total);
+    const int64_t dw_blocks = a.dw ? (static_cast<int64_t>(a.S) + kFlatThreads - 1) / kFlatThreads : 0;
+    if (row_blocks + dw_blocks == 0) return hipSuccess;
+    const dim3 grid(static_cast<unsigned>(row_blocks + dw_blocks)), block(kFlatThreads);
+    if (a.dtype == 1) {
+      if (a.dw) combine_bwd_flat_kernel<bf16_t, true, true><<<grid, block, 0, st>>>(a, lg, total, row_blocks);
+      else if (lg >= 0) combine_bwd_flat_kernel<bf16_t, true, false><<<grid, block, 0, st>>>(a, lg, total, row_blocks);
+      else combine_bwd_flat_kernel<bf16_t, false, false><<<grid, block, 0, st>>>(a, lg, total, row_blocks);
+    } else {
+      if (a.dw) combine_bwd_flat_kernel<float, true, true><<<grid, block, 0, st>>>(a, lg, total, row_blocks);
+      else if (lg >= 0) combine_bwd_flat_kernel<float, true, false><<<grid, block, 0, st>>>(a, lg, total, row_blocks);
+      else combine_bwd_flat_kernel<float, false, false><<<grid, block, 0, st>>>(a, lg, total, row_blocks);
+    }
+    return hipGetLastError();
+  }
   const int64_t row_blocks = blocks_for_rows(a.rows, kWideWaves);
-  const int64_t dw_blocks = a.dw ? (static_cast<int64_t>(a.S) * a.k + kThreads - 1) / kThreads : 0;
+  const int64_t dw_blocks = (static_cast<int64_t>(a.S) * a.k + kThreads - 1) / kThreads;
   if (row_blocks + dw_blocks == 0) return hipSuccess;
   const dim3 grid(static_cast<unsigned>(row_blocks + dw_blocks)), block(kThreads);
   if (a.dtype == 1) {

@@ -222,6 +222,38 @@ def test_layout_ops_short_rows(dtype, d, k, S, C):
     print(f"[stats] short rows d={d}: {st}", flush=True)
 
 
+@pytest.mark.parametrize("dtype,d,k,S,C", [
+    ("bf16", 264, 1, 300, 30), ("f32", 100, 1, 301, 40), ("bf16", 256, 1, 130, 12), ("bf16", 8192, 1, 40, 4),
+    ("f32", 8192, 1, 33, 3), ("f32", 1000, 2, 77, 11), ("bf16", 1784, 2, 65, 9),
+])
+def test_layout_ops_flat_row_lengths(dtype, d, k, S, C):
+    """Row lengths the one-chunk-per-thread kernels treat specially: not a power
+    of two (33, 25, 250, 223 chunks), a power of two below one wave (32), the
+    largest row whose dw is reduced inside a block (1024 chunks) and a longer
+    one (2048 chunks, rows spanning two blocks)."""
+    E = 8
+    announce(f"layout ops flat rows dtype={dtype} d={d} k={k} S={S} C={C}")
+    rng = np.random.default_rng(d * 3 + k + S)
+    L = rng.standard_normal((S, E)).astype(np.float32)
+    g = _logits_case(S, E, k, 0, 1, C, L)
+    x = wl.make_rows((S, d), dtype, 41)
+    st = check_layout_ops(dict(dtype=dtype), x, g["ids"], g["slots"], g["weights"], g["slot_src"], E, C, k, seed=43)
+    assert (g["slots"] < 0).any() and (k > 1 or (g["slot_src"] < 0).any())
+    # the [E, C, d] writers leave the memory around a view alone
+    pad = 64
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    buf = torch.full((E * C * d + 2 * pad,), 7.0, dtype=tdt, device="cuda")
+    xe = buf[pad:pad + E * C * d].view(E, C, d)
+    d_ids, d_slots = wl.to_device(g["ids"], "i32"), wl.to_device(g["slots"], "i32")
+    code = hm.MOE_BF16 if dtype == "bf16" else hm.MOE_F32
+    hm.moe_dispatch(hm.Layout(S, d, E, k, C, code), wl.to_device(x, dtype), d_ids, d_slots,
+                    wl.to_device(g["slot_src"], "i32"), xe)
+    torch.cuda.synchronize()
+    assert (buf[:pad] == 7.0).all() and (buf[-pad:] == 7.0).all()
+    assert_equal(wl.to_host(xe), oracle.dispatch(x, g["slot_src"], k), "dispatch into a view")
+    print(f"[stats] flat rows d={d} k={k}: {st}", flush=True)
+
+
 def test_determinism_and_guard_bands():
     announce("determinism and guard bands")
     w = W[2]

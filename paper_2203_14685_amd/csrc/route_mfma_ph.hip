@@ -42,6 +42,8 @@ __global__ __launch_bounds__(kPhThreads) void route_mfma_ph_kernel(RouteArgs a) 
   constexpr int KP = 65536 / E;        // columns per phase (a multiple of 512)
   constexpr int LDW = KP + 8;          // padded LDS row of W^T (bf16 elements)
   constexpr int KSTEPS = kPhChunk / 32;  // MFMA K steps per chunk
+  constexpr int kStage = (KP / 4) * (E / 8) / kPhThreads;  // staging blocks per thread and phase
+  static_assert(kStage * kPhThreads == (KP / 4) * (E / 8), "whole staging rounds");
   static_assert(E * LDW * 2 <= kPhLdsBytes, "phase buffer");
   static_assert(E * LDW * 2 >= 2 * kWave * (E + 1) * 4, "logits reuse the phase buffer");
   __shared__ __align__(16) unsigned char lds_raw[kPhLdsBytes];
@@ -86,17 +88,30 @@ __global__ __launch_bounds__(kPhThreads) void route_mfma_ph_kernel(RouteArgs a) 
         const int kp0 = c * kPhChunk;
         const int kp = min(KP, d - kp0);
         __syncthreads();  // previous phase's fragments (or logits) consumed
-        const int nblk = (kp / 4) * (E / 8);  // 4 x 8 blocks: 4 columns of 8 experts
-        for (int b = tid; b < nblk; b += kPhThreads) {
-          const int kb = (b / (E / 8)) * 4, eb = (b % (E / 8)) * 8;
-          u32x4 rows[4];
-          uint2 cols[8];
+        // 4 x 8 blocks (4 columns of 8 experts), kStage per thread; all loads
+        // are issued before the first transpose (one L2 round trip per phase),
+        // blocks past a short last phase load block 0 and store nothing
+        const int nblk = (kp / 4) * (E / 8);
+        u32x4 rows[kStage][4];
+#pragma unroll
+        for (int it = 0; it < kStage; ++it) {
+          const int b = tid + it * kPhThreads;
+          const int bb = b < nblk ? b : 0;
+          const int kb = (bb / (E / 8)) * 4, eb = (bb % (E / 8)) * 8;
 #pragma unroll
           for (int j = 0; j < 4; ++j)
-            rows[j] = *reinterpret_cast<const u32x4*>(wg + static_cast<int64_t>(kp0 + kb + j) * E + eb);
-          transpose4x8_b16(rows, cols);
+            rows[it][j] = *reinterpret_cast<const u32x4*>(wg + static_cast<int64_t>(kp0 + kb + j) * E + eb);
+        }
 #pragma unroll
-          for (int i = 0; i < 8; ++i) *reinterpret_cast<uint2*>(&wsT[(eb + i) * LDW + kb]) = cols[i];
+        for (int it = 0; it < kStage; ++it) {
+          const int b = tid + it * kPhThreads;
+          if (b < nblk) {
+            const int kb = (b / (E / 8)) * 4, eb = (b % (E / 8)) * 8;
+            uint2 cols[8];
+            transpose4x8_b16(rows[it], cols);
+#pragma unroll
+            for (int i = 0; i < 8; ++i) *reinterpret_cast<uint2*>(&wsT[(eb + i) * LDW + kb]) = cols[i];
+          }
         }
         __syncthreads();
       }
@@ -129,7 +144,16 @@ __global__ __launch_bounds__(kPhThreads) void route_mfma_ph_kernel(RouteArgs a) 
     }
     for (int i = tid; i < 2 * a.k * E; i += kPhThreads) hist_lds[i] = 0;
     __syncthreads();
-    if (a.logits) {
+    if (a.logits && (reinterpret_cast<uintptr_t>(a.logits) & 15) == 0) {
+      // 16-byte streaming stores, 4 logits of one token each (E is a multiple of 16)
+      for (int o = tid; o < 2 * kWave * (E / 4); o += kPhThreads) {
+        const int r = o / (E / 4), e = (o % (E / 4)) * 4;
+        const int64_t s = ((r < kWave) ? wbA : wbB) * kWave + (r % kWave);
+        const float* src = &lg[r * (E + 1) + e];
+        if ((r < kWave || hasB) && s < a.S)
+          __builtin_nontemporal_store(f32x4{src[0], src[1], src[2], src[3]}, reinterpret_cast<f32x4*>(a.logits + s * E + e));
+      }
+    } else if (a.logits) {  // a caller's buffer with 4-byte alignment only
       for (int o = tid; o < 2 * kWave * E; o += kPhThreads) {
         const int r = o / E, e = o % E;
         const int64_t s = ((r < kWave) ? wbA : wbB) * kWave + (r % kWave);

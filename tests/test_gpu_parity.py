@@ -179,6 +179,36 @@ def test_mfma_projection_shapes(E, k, kind, normalize, d, bias, S):
     print(f"[stats] mfma E={E}: {st}", flush=True)
 
 
+@pytest.mark.parametrize("wid,S", [(3, 700), (2, 300)])
+def test_projection_logits_into_unaligned_buffer(wid, S):
+    """Logits written into a caller's buffer that is 4-byte but not 16-byte
+    aligned match, bit for bit, those written into an aligned one, and the
+    routing is the same."""
+    w = W[wid]
+    E, k = w["E"], w["k"]
+    C = cap(w["cf"], k, S, E)
+    announce(f"unaligned logits workload {wid} S={S}")
+    inp = wl.make_inputs(w, S=S, seed=5)
+    x, wg = wl.to_device(inp["x"], "bf16"), wl.to_device(inp["wg"], "bf16")
+    bias = wl.to_device(inp["bias"], "f32")
+    p = hm.gate_params(S, w["d"], E, k, C, w["kind"], w["normalize"], 0, hm.MOE_BF16, 0)
+    ws = torch.empty((hm.moe_gate_workspace_size(p),), dtype=torch.uint8, device="cuda")
+    runs = []
+    for off in (0, 1):
+        buf = torch.full((S * E + 8,), -7.0, dtype=torch.float32, device="cuda")
+        lg = buf[off:off + S * E].view(S, E)
+        i32 = lambda *sh: torch.full(sh, -3, dtype=torch.int32, device="cuda")
+        o = dict(ids=i32(S, k), slots=i32(S, k), weights=torch.zeros((S, k), device="cuda"), counts=i32(E),
+                 demand=i32(E), slot_src=i32(E, C))
+        hm.moe_gate(p, x, wg, bias, None, None, None, lg, o["ids"], o["slots"], o["weights"], o["counts"],
+                    o["demand"], o["slot_src"], ws)
+        torch.cuda.synchronize()
+        assert (buf[:off] == -7.0).all() and (buf[off + S * E:] == -7.0).all()
+        runs.append({"logits": lg.clone(), **o})
+    for key in runs[0]:
+        assert torch.equal(runs[0][key], runs[1][key]), key
+
+
 def test_ktop1_projection_with_bias():
     S, d, E, k = 600, 512, 24, 3
     announce("kTop1 projection with bias")

@@ -178,10 +178,13 @@ GateBwdPlan plan_gate_bwd(const moe_gate_bwd_params* p) {
   g.mfma = gate_bwd_mfma_shape(p->dtype, p->E, p->d);
   g.s_pad = static_cast<int64_t>(g.nb) * kTokensPerHistBlock;
   // token ranges for dW: enough blocks to fill the chip (about 512 matrix-core
-  // or 1024 vector blocks), each range a whole number of 64-token blocks
-  const int64_t per_split = g.mfma ? (p->d / 64) : ((p->d + 63) / 64) * ((p->E + 63) / 64);
+  // blocks of 256 columns, two per CU, or 1024 vector blocks of 64), each range
+  // a whole number of 64-token blocks; matrix-core ranges keep at least 4 of
+  // them where the batch allows, so that each block pipelines several chunks
+  const int64_t per_split = g.mfma ? (p->d + 255) / 256 : ((p->d + 63) / 64) * ((p->E + 63) / 64);
   const int64_t target = g.mfma ? 512 : 1024;
   int64_t ns = (target + per_split - 1) / per_split;
+  if (g.mfma && ns > g.nb / 4) ns = g.nb / 4;
   if (ns > g.nb) ns = g.nb;
   if (ns < 1) ns = 1;
   int64_t st = (static_cast<int64_t>(p->S) + ns - 1) / ns;

@@ -347,38 +347,59 @@ __global__ __launch_bounds__(1024) void aux_loss_kernel(GateBwdArgs a) {
 }
 
 // ---------------------------------------------------------------- dW on matrix cores
-// Block: 64 columns of x x one token range; its 4 waves take the range's
-// 64-token chunks in turn, each on its own.  A wave transposes its chunk
-// of x into LDS (each lane one 8 x 8 block, transposed in registers) and runs
-// 4 M tiles (16 columns) x NT N tiles (16 experts) with K = 32 tokens:
-// A[j][s] = x[s][j] from the tile, B[s][e] = dL^T[e][s] from its three bf16
-// planes.
-// The four waves' sums are then added in order into the range's partial dW.
+// gfx950's LDS transpose read (ds_read_b64_tr_b16): within each group of 16
+// lanes, lane i receives element i % 4 of the four-element rows addressed by
+// lanes i / 4 + 4 j, j = 0..3 (checked on MI355X with an index-filled buffer).
+// Two such reads turn a row-major tile of x into the A operand x^T.
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+
+__device__ __forceinline__ uint2 lds_read_tr16(const uint16_t* p) {
+  return __builtin_bit_cast(uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p)));
+}
+
+// 16-byte piece of row t of a 64 x 64 bf16 tile (128-byte rows, no padding):
+// logical piece p sits at p ^ dw_swz(t), so that the 32 rows one transpose read
+// touches (4 per lane group, even and odd halves) fall into distinct pieces.
+__device__ __forceinline__ int dw_swz(int t) { return ((t >> 1) & 1) | (((t >> 3) & 3) << 1); }
+
+// Block: 256 columns of x (64 per wave) x one token range, walked in 64-token
+// chunks that all four waves take together.  Per chunk the block stages the
+// chunk's three dL^T planes (E rows of 64 tokens each) in LDS, double
+// buffered, and every wave reads its B fragments (B[s][e] = dL^T[e][s]) from
+// there; each wave stages its 64 x 64 tile of x as it is (rows of 128 bytes,
+// pieces swizzled) and reads the A operand A[j][s] = x[s][j] back through
+// transpose reads.  The next chunk's planes and rows are loaded into registers
+// right after the chunk's barrier, unconditionally (rows outside the range
+// read a valid row and are zeroed on the way to LDS), and stay in flight
+// through the products, which wait on LDS only.  4 M tiles (16 columns) x NT N
+// tiles (16 experts), K = 32 tokens; each wave stores its own partial sums.
 template <int NT>
-__global__ __launch_bounds__(kBwdThreads) void dwg_mfma_kernel(GateBwdArgs a) {
+__global__ __launch_bounds__(kBwdThreads) __attribute__((amdgpu_waves_per_eu(NT <= 4 ? 2 : 1))) void dwg_mfma_kernel(GateBwdArgs a) {
   constexpr int E = 16 * NT;
-  constexpr int LDX = kWave + 8;   // padded row of the x^T tile (bf16)
-  constexpr int LDR = kWave + 1;   // padded row of the wave-sum buffer (fp32)
-  __shared__ __align__(16) uint16_t xt[kBwdWaves * kWave * LDX];
-  static_assert(E * LDR * 4 <= kBwdWaves * kWave * LDX * 2, "sums reuse the tile buffer");
-  float* red = reinterpret_cast<float*>(xt);
+  constexpr int kRows = 3 * E;                         // plane rows per chunk
+  constexpr int kPieces = kRows * 8;                   // 16-byte pieces per chunk
+  constexpr int kPer = (kPieces + kBwdThreads - 1) / kBwdThreads;
+  __shared__ __align__(16) uint16_t pl[2][kRows * kWave];
+  __shared__ __align__(16) uint16_t xt[kBwdWaves][kWave * kWave];
   const int w = threadIdx.x / kWave, lane = lane_id();
   const int g = lane / 16, m = lane % 16;
-  const int bb = lane % 8, ab = lane / 8;  // the 8 x 8 block this lane stages
+  const int lr = lane / 8, lp = lane % 8;  // row (of 8) and 16-byte piece this lane loads of x
   // 1-D grid, blocks dealt round-robin to the 8 XCDs (block id mod 8): all
   // column blocks of one token range go to the same XCD and share its L2 copy
   // of that range's dL planes
-  const int ncb = a.d / kWave;
+  const int ncb = (a.d + 4 * kWave - 1) / (4 * kWave);
   const int xcd = blockIdx.x % 8, r8 = blockIdx.x / 8;
   const int split = xcd + 8 * (r8 / ncb);
-  const int j0 = (r8 % ncb) * kWave;
   if (split >= a.nsplit) return;  // idle block (whole block, before any barrier)
+  const int jw = (r8 % ncb) * 4 * kWave + w * kWave;  // this wave's first column
+  const bool wcols = jw < a.d;                        // a wave past d stores nothing
+  const int jx = wcols ? jw : 0;
   const int64_t sb = static_cast<int64_t>(split) * a.split_tokens;
   const int64_t se = min(static_cast<int64_t>(a.S), sb + a.split_tokens);
   const int nchunks = static_cast<int>((se - sb + kWave - 1) / kWave);
   const uint16_t* x = reinterpret_cast<const uint16_t*>(a.x);
-  static_assert(LDX % 8 == 0, "16-byte tile rows");
-  uint16_t* tile = xt + w * kWave * LDX;
+  uint16_t* tile = xt[w];
   const u32x4 zero = {0u, 0u, 0u, 0u};
 
   f32x4 acc[4][NT];
@@ -387,78 +408,90 @@ __global__ __launch_bounds__(kBwdThreads) void dwg_mfma_kernel(GateBwdArgs a) {
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // the tile is private to the wave: wave-level fences order its LDS traffic,
-  // and the next chunk's rows of x are loaded while this one is multiplied
-  const int64_t plane = static_cast<int64_t>(E) * a.s_pad;
-  u32x4 rows[8];
-  auto load_rows = [&](int c) {
-    const int64_t s0 = sb + static_cast<int64_t>(c) * kWave;
+  u32x4 rows[8], pv[kPer];
+  auto load_next = [&](int c) {
+    const int cc = c < nchunks ? c : 0;
+    const int64_t s0 = sb + static_cast<int64_t>(cc) * kWave;
 #pragma unroll
     for (int r = 0; r < 8; ++r) {
-      const int64_t s = s0 + 8 * ab + r;
-      rows[r] = (c < nchunks && s < se) ? *reinterpret_cast<const u32x4*>(x + s * a.d + j0 + 8 * bb) : zero;
+      const int64_t s = s0 + 8 * r + lr;
+      rows[r] = *reinterpret_cast<const u32x4*>(x + (s < se ? s : sb) * a.d + jx + 8 * lp);
+    }
+    // plane rows are contiguous: row q / 8 of the [3 E, s_pad] array, tokens
+    // s0 + 8 (q % 8) .. + 8 (zero beyond S)
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      const int q0 = static_cast<int>(threadIdx.x) + i * kBwdThreads;
+      const int q = (kPieces % kBwdThreads == 0 || q0 < kPieces) ? q0 : 0;
+      pv[i] = *reinterpret_cast<const u32x4*>(a.dlt + static_cast<int64_t>(q / 8) * a.s_pad + s0 + 8 * (q % 8));
     }
   };
-  load_rows(w);
-  for (int c = w; c < nchunks; c += kBwdWaves) {
+  load_next(0);
+  for (int c = 0; c < nchunks; ++c) {
     const int64_t s0 = sb + static_cast<int64_t>(c) * kWave;
-    {
-      u32x4 cols[8];
-      transpose8x8_b16(rows, cols);
+    uint16_t* pb = pl[c & 1];
+    // this chunk's planes and rows into LDS (the planes' buffer was last read
+    // two chunks ago, before the previous barrier; the tile's last reads are
+    // this wave's own, earlier in its LDS order)
 #pragma unroll
-      // 16-byte unit of the row XOR the row's group of 8: the 8 lanes of one
-      // store (same ab, rows 8 apart) land in different banks
-      for (int i = 0; i < 8; ++i) *reinterpret_cast<u32x4*>(&tile[(8 * bb + i) * LDX + 8 * (ab ^ bb)]) = cols[i];
+    for (int i = 0; i < kPer; ++i) {
+      const int q = static_cast<int>(threadIdx.x) + i * kBwdThreads;
+      const int r = q / 8;
+      if (kPieces % kBwdThreads == 0 || q < kPieces)
+        *reinterpret_cast<u32x4*>(&pb[r * kWave + 8 * ((q % 8) ^ (r & 7))]) = pv[i];
     }
-    load_rows(c + kBwdWaves);
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      u32x4 av[4];
+    for (int r = 0; r < 8; ++r) {
+      const int t = 8 * r + lr;
+      *reinterpret_cast<u32x4*>(&tile[t * kWave + 8 * (lp ^ dw_swz(t))]) = (s0 + t < se) ? rows[r] : zero;
+    }
+    __syncthreads();
+    load_next(c + 1);
+    __builtin_amdgcn_sched_barrier(0);
+    {  // a wave past d multiplies a valid tile it does not store (no branch around the products)
 #pragma unroll
-      for (int mt = 0; mt < 4; ++mt)
-        av[mt] = *reinterpret_cast<const u32x4*>(
-            &tile[(16 * mt + m) * LDX + 8 * ((4 * ks + g) ^ (((16 * mt + m) >> 3) & 7))]);
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        const uint16_t* src = a.dlt + static_cast<int64_t>(16 * nt + m) * a.s_pad + s0 + 32 * ks + 8 * g;
-        const u32x4 bh = *reinterpret_cast<const u32x4*>(src);
-        const u32x4 bm = *reinterpret_cast<const u32x4*>(src + plane);
-        const u32x4 bl = *reinterpret_cast<const u32x4*>(src + 2 * plane);
+      for (int ks = 0; ks < 2; ++ks) {
+        u32x4 av[4];
 #pragma unroll
         for (int mt = 0; mt < 4; ++mt) {
-          acc[mt][nt] = mfma_bf16(av[mt], bh, acc[mt][nt]);
-          acc[mt][nt] = mfma_bf16(av[mt], bm, acc[mt][nt]);
-          acc[mt][nt] = mfma_bf16(av[mt], bl, acc[mt][nt]);
+          // lane q of group g addresses row 32 ks + 8 g + 4 h + q / 4, columns
+          // 16 mt + 4 (q % 4) .. + 3; lane m then holds x[32 ks + 8 g + 4 h + j][16 mt + m]
+          uint2 half[2];
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const int t = 32 * ks + 8 * g + 4 * h + m / 4;
+            const int piece = (2 * mt + (m % 4) / 2) ^ dw_swz(t);
+            half[h] = lds_read_tr16(&tile[t * kWave + 8 * piece + 4 * (m % 2)]);
+          }
+          av[mt] = u32x4{half[0].x, half[0].y, half[1].x, half[1].y};
+        }
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt) {
+          u32x4 b3[3];
+#pragma unroll
+          for (int pn = 0; pn < 3; ++pn) {
+            const int r = pn * E + 16 * nt + m;
+            b3[pn] = *reinterpret_cast<const u32x4*>(&pb[r * kWave + 8 * ((4 * ks + g) ^ (r & 7))]);
+          }
+#pragma unroll
+          for (int mt = 0; mt < 4; ++mt) {
+            acc[mt][nt] = mfma_bf16(av[mt], b3[0], acc[mt][nt]);
+            acc[mt][nt] = mfma_bf16(av[mt], b3[1], acc[mt][nt]);
+            acc[mt][nt] = mfma_bf16(av[mt], b3[2], acc[mt][nt]);
+          }
+          __builtin_amdgcn_sched_barrier(0);  // one N tile's fragments live at a time
         }
       }
     }
-    // the tile is read before the next chunk overwrites it
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
-  __syncthreads();  // every wave done with its tile before the buffer holds the sums
   // lane (g, m) of tile (mt, nt) holds columns 16 mt + 4 g + i, expert 16 nt + m
-  for (int ww = 0; ww < kBwdWaves; ++ww) {
-    if (w == ww) {
+  if (wcols) {
 #pragma unroll
-      for (int mt = 0; mt < 4; ++mt)
+    for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
-        for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int idx = (16 * nt + m) * LDR + 16 * mt + 4 * g + i;
-            red[idx] = (ww == 0 ? 0.f : red[idx]) + acc[mt][nt][i];
-          }
-    }
-    __syncthreads();
-  }
-  for (int q = threadIdx.x; q < E * kWave; q += kBwdThreads) {
-    const int e = q / kWave, jj = q % kWave;
-    a.wpart[(static_cast<int64_t>(split) * E + e) * a.d + j0 + jj] = red[e * LDR + jj];
+      for (int nt = 0; nt < NT; ++nt)
+        *reinterpret_cast<f32x4*>(a.wpart + (static_cast<int64_t>(split) * E + 16 * nt + m) * a.d + jw + 16 * mt + 4 * g) =
+            acc[mt][nt];
   }
 }
 
@@ -676,8 +709,17 @@ __global__ __launch_bounds__(kBwdThreads) void dwg_reduce_kernel(GateBwdArgs a) 
   const int64_t idx = static_cast<int64_t>(blockIdx.x) * kBwdThreads + threadIdx.x;
   if (idx >= n) return;
   const int e = static_cast<int>(idx / a.d), jx = static_cast<int>(idx % a.d);
+  // eight ranges' loads in flight at a time; the additions stay in range order
   float v = 0.f;
-  for (int sp = 0; sp < a.nsplit; ++sp) v += a.wpart[static_cast<int64_t>(sp) * n + idx];
+  int sp = 0;
+  for (; sp + 8 <= a.nsplit; sp += 8) {
+    float t[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) t[u] = a.wpart[static_cast<int64_t>(sp + u) * n + idx];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v += t[u];
+  }
+  for (; sp < a.nsplit; ++sp) v += a.wpart[static_cast<int64_t>(sp) * n + idx];
   a.dwg[static_cast<int64_t>(jx) * a.E + e] = v;
 }
 
@@ -788,7 +830,7 @@ constexpr int kDxEC = 32;  // experts per register chunk in the vector-ALU dx
 template <int NT>
 static void launch_dwg_mfma_t(const GateBwdArgs& a, hipStream_t st) {
   const int64_t per_xcd = (a.nsplit + 7) / 8;  // token ranges per XCD
-  const dim3 grid(static_cast<unsigned>(8 * per_xcd * (a.d / kWave)));
+  const dim3 grid(static_cast<unsigned>(8 * per_xcd * ((a.d + 4 * kWave - 1) / (4 * kWave))));
   dwg_mfma_kernel<NT><<<grid, dim3(kBwdThreads), 0, st>>>(a);
 }
 

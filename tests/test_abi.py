@@ -199,9 +199,12 @@ def _a256(n):
 def _bwd_ws_formula(S, d, E, dtype):
     nb = (S + 63) // 64
     mfma = dtype == b.MOE_BF16 and E % 16 == 0 and E <= 128 and d % 64 == 0
-    per_split = d // 64 if mfma else ((d + 63) // 64) * ((E + 63) // 64)
+    per_split = -(-d // 256) if mfma else ((d + 63) // 64) * ((E + 63) // 64)
     target = 512 if mfma else 1024
-    ns = max(1, min(-(-target // per_split), nb))
+    ns = -(-target // per_split)
+    if mfma:
+        ns = min(ns, nb // 4)
+    ns = max(1, min(ns, nb))
     st = max(64, -(-(-(-S // ns)) // 64) * 64)
     nsplit = -(-S // st)
     return (_a256(S * E * 4) + (_a256(3 * nb * 64 * E * 2) if mfma else 0) + _a256((1 + -(-S // 4096)) * E * 4)

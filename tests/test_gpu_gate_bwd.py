@@ -91,6 +91,11 @@ CASES = [
     (77, 512, 24, 3, 1, 0, "bf16", 0.0, False),         # kTop1 3 x 8
     (1, 256, 8, 2, 0, 1, "f32", 0.0, True),
     (4100, 512, 32, 1, 0, 0, "f32", 0.1, False),        # several token ranges for dW
+    # matrix-core dW: blocks of 256 columns with waves past d, 2..8 expert tiles
+    (700, 320, 32, 2, 0, 1, "bf16", 0.0, True),         # d = 320: second block has one live wave
+    (130, 448, 48, 1, 0, 0, "bf16", 0.01, False),       # 3 tiles, fewer than 4 chunks per range
+    (900, 64, 80, 3, 0, 1, "bf16", 0.0, True),          # d = 64: one live wave per block
+    (1500, 192, 128, 2, 0, 1, "bf16", 0.0, False),      # E = 128, one wave per SIMD
 ]
 
 

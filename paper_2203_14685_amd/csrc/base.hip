@@ -144,13 +144,19 @@ __global__ __launch_bounds__(kBlock) void base_bid_kernel(BaseArgs a, int r) {
     };
     if constexpr (VEC) {
       const float4* r4 = reinterpret_cast<const float4*>(row);
-#pragma unroll 4
-      for (int q = 0; q < a.E / 4; ++q) {
-        const float4 l = r4[q];
-        take(l.x, 4 * q);
-        take(l.y, 4 * q + 1);
-        take(l.z, 4 * q + 2);
-        take(l.w, 4 * q + 3);
+      const int nq = a.E / 4;
+      for (int q0 = 0; q0 < nq; q0 += 16) {  // 64 experts' loads issued together
+        float4 l[16];
+#pragma unroll
+        for (int q = 0; q < 16; ++q) l[q] = r4[q0 + q < nq ? q0 + q : 0];
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+          if (q0 + q >= nq) break;
+          take(l[q].x, 4 * (q0 + q));
+          take(l[q].y, 4 * (q0 + q) + 1);
+          take(l[q].z, 4 * (q0 + q) + 2);
+          take(l[q].w, 4 * (q0 + q) + 3);
+        }
       }
     } else {
       for (int e = 0; e < a.E; ++e) take(row[e], e);
@@ -273,9 +279,10 @@ __global__ __launch_bounds__(kBaseThreads) void base_resolve_kernel(BaseArgs a, 
   for (int64_t p0 = 0; p0 < a.S && have < kBaseCand; p0 += static_cast<int64_t>(kBaseIters) * kBaseThreads) {
     int be[kBaseIters];
 #pragma unroll
-    for (int i = 0; i < kBaseIters; ++i) {
+    for (int i = 0; i < kBaseIters; ++i) {  // unconditional loads (clamped), issued together
       const int64_t s = p0 + static_cast<int64_t>(i) * kBaseThreads + tid;
-      be[i] = s < a.S ? a.bid_e[s] : -1;
+      be[i] = a.bid_e[s < a.S ? s : 0];
+      if (s >= a.S) be[i] = -1;
     }
 #pragma unroll
     for (int i = 0; i < kBaseIters; ++i) {
@@ -311,17 +318,17 @@ __global__ __launch_bounds__(kBaseThreads) void base_resolve_kernel(BaseArgs a, 
       if (be[i] == e) {
         const int k = i * kBaseWaves + w;
         const int pos = have + offs[k] + popc_below(masks[k]);
-        if (pos < kBaseCand) {
-          const int64_t s = p0 + static_cast<int64_t>(i) * kBaseThreads + tid;
-          bv[pos] = a.bid_v[s];
-          bt[pos] = static_cast<int>(s);
-        }
+        if (pos < kBaseCand) bt[pos] = static_cast<int>(p0 + static_cast<int64_t>(i) * kBaseThreads + tid);
       }
     }
     have += pass_total;  // uniform
     __syncthreads();     // masks and offs are reused by the next pass
   }
   const int nb = min(have, kBaseCand);
+  // the bids of the collected tokens, read together (bt is complete after the
+  // last pass's barrier)
+  for (int i = tid; i < nb; i += kBaseThreads) bv[i] = a.bid_v[bt[i]];
+  __syncthreads();
   if (tid == 0) a.bid_cnt[e] = 0;  // for the next round (every thread has read it)
   if (nb > kBaseSortFrom) {
     // many bidders (the first rounds of a phase): sort them, then each entry's
@@ -406,16 +413,28 @@ __device__ __forceinline__ void base_wave_bid(const BaseArgs& a, const double* p
   const float* row = a.logits + static_cast<int64_t>(t) * a.E;
   double v1 = -INFINITY, v2 = -INFINITY, l1 = 0.0;
   int e1 = 0x7fffffff;
-  for (int e = lane; e < a.E; e += kWave) {
-    const float l = row[e];
-    const double v = static_cast<double>(l) - pr[e];
-    if (v > v1) {
-      v2 = v1;
-      v1 = v;
-      e1 = e;
-      l1 = static_cast<double>(l);
-    } else if (v > v2) {
-      v2 = v;
+  // four experts per lane per batch, loaded together (clamped: a lane past E
+  // reads expert 0 and skips it)
+  for (int e0 = 0; e0 < a.E; e0 += 4 * kWave) {
+    float lv[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int e = e0 + q * kWave + lane;
+      lv[q] = row[e < a.E ? e : 0];
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int e = e0 + q * kWave + lane;
+      if (e >= a.E) continue;
+      const double v = static_cast<double>(lv[q]) - pr[e];
+      if (v > v1) {
+        v2 = v1;
+        v1 = v;
+        e1 = e;
+        l1 = static_cast<double>(lv[q]);
+      } else if (v > v2) {
+        v2 = v;
+      }
     }
   }
 #pragma unroll
@@ -452,16 +471,30 @@ __device__ __forceinline__ int base_wave_place(const BaseArgs& a, double* pr, in
   const int64_t base = static_cast<int64_t>(e) * c;
   int p = 0, ev = -1;
   double vlast = 0.0;  // bid of the holder that ends at c - 1
-  for (int i = lane; i < nh; i += kWave) {
-    const double hv = a.hold_v[base + i];
-    const int ht = a.hold_t[base + i];
-    if (hvs) {
-      hvs[i] = hv;
-      hts[i] = ht;
+  // holders read 8 per lane at a time, the loads of a batch issued together
+  // (clamped: a slot past nh reads slot 0 and is skipped)
+  for (int i0 = 0; i0 < nh; i0 += 8 * kWave) {
+    double hv[8];
+    int ht[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int i = i0 + q * kWave + lane;
+      const int ic = i < nh ? i : 0;
+      hv[q] = a.hold_v[base + ic];
+      ht[q] = a.hold_t[base + ic];
     }
-    p += base_before(hv, ht, bid, t);
-    if (i == c - 1) ev = ht;
-    if (i == c - 2) vlast = hv;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int i = i0 + q * kWave + lane;
+      if (i >= nh) continue;
+      if (hvs) {
+        hvs[i] = hv[q];
+        hts[i] = ht[q];
+      }
+      p += base_before(hv[q], ht[q], bid, t);
+      if (i == c - 1) ev = ht[q];
+      if (i == c - 2) vlast = hv[q];
+    }
   }
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) {
@@ -480,14 +513,26 @@ __device__ __forceinline__ int base_wave_place(const BaseArgs& a, double* pr, in
       a.hold_t[base + i + 1] = hts[i];
     }
   } else {
-    for (int top = min(nh, c - 1); top > p; top -= kWave) {
-      const int lo = max(p, top - kWave);
-      const int i = lo + lane;
-      if (i < top) {
-        const double hv = a.hold_v[base + i];
-        const int ht = a.hold_t[base + i];
-        a.hold_v[base + i + 1] = hv;
-        a.hold_t[base + i + 1] = ht;
+    // from the end, 8 x 64 holders at a time: a batch is read whole before its
+    // shifted copy is written, and its writes start one above the batch below
+    for (int top = min(nh, c - 1); top > p; top -= 8 * kWave) {
+      const int lo = max(p, top - 8 * kWave);
+      double hv[8];
+      int ht[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const int i = lo + q * kWave + lane;
+        const int ic = i < top ? i : lo;
+        hv[q] = a.hold_v[base + ic];
+        ht[q] = a.hold_t[base + ic];
+      }
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const int i = lo + q * kWave + lane;
+        if (i < top) {
+          a.hold_v[base + i + 1] = hv[q];
+          a.hold_t[base + i + 1] = ht[q];
+        }
       }
     }
   }
@@ -536,13 +581,13 @@ __global__ __launch_bounds__(kBaseThreads) void base_tail_kernel(BaseArgs a, int
   for (int64_t s0 = 0; s0 < a.S; s0 += 8 * kBaseThreads) {
     int v[8];
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
+    for (int q = 0; q < 8; ++q) {  // unconditional loads (clamped), issued together
       const int64_t s = s0 + q * kBaseThreads + tid;
-      v[q] = s < a.S ? a.assign[s] : 0;
+      v[q] = a.assign[s < a.S ? s : 0];
     }
 #pragma unroll
     for (int q = 0; q < 8; ++q)
-      if (v[q] < 0) {
+      if (v[q] < 0 && s0 + q * kBaseThreads + tid < a.S) {
         const int p = atomicAdd(&nU, 1);
         if (p < kBaseTail) U[p] = static_cast<int>(s0 + q * kBaseThreads + tid);
       }
@@ -668,14 +713,21 @@ __global__ __launch_bounds__(kBaseThreads) void base_tail_kernel(BaseArgs a, int
       const float* row = a.logits + static_cast<int64_t>(t) * E;
       double v1 = -INFINITY, v2 = -INFINITY;
       int e1 = 0;
-      for (int e = 0; e < E; ++e) {
-        const double v = static_cast<double>(row[e]) - pr[e];
-        if (v > v1) {
-          v2 = v1;
-          v1 = v;
-          e1 = e;
-        } else if (v > v2) {
-          v2 = v;
+      for (int e0 = 0; e0 < E; e0 += 32) {  // 32 loads issued together
+        float lv[32];
+#pragma unroll
+        for (int q = 0; q < 32; ++q) lv[q] = row[e0 + q < E ? e0 + q : 0];
+#pragma unroll
+        for (int q = 0; q < 32; ++q) {
+          if (e0 + q >= E) break;
+          const double v = static_cast<double>(lv[q]) - pr[e0 + q];
+          if (v > v1) {
+            v2 = v1;
+            v1 = v;
+            e1 = e0 + q;
+          } else if (v > v2) {
+            v2 = v;
+          }
         }
       }
       if (E == 1) v2 = v1;

@@ -570,10 +570,9 @@ __global__ __launch_bounds__(kBaseThreads) void base_tail_kernel(BaseArgs a, int
   int* hn = reinterpret_cast<int*>(hvs + c);          // holder counts [E]
   int* hts = hn + E;                                  // the holders' tokens [c]
   __shared__ int U[kBaseTail], U2[kBaseTail];
-  __shared__ int bex[kBaseTail], kr[kBaseTail], nbe[kBaseTail], pos[kBaseTail], rk[kBaseTail];
+  __shared__ int bex[kBaseTail], kr[kBaseTail], nbe[kBaseTail], pos[kBaseTail], ldr[kBaseTail];
   __shared__ double bvv[kBaseTail];
-  __shared__ int pref[kBaseTail + 1];
-  __shared__ int nU, nU2, fast_rounds, fast_fail;
+  __shared__ int nU, nU2, nL, fast_rounds, fast_fail;
   const int tid = threadIdx.x, lane = lane_id(), w = tid / kWave;
   if (tid == 0) nU = 0;
   __syncthreads();
@@ -677,10 +676,17 @@ __global__ __launch_bounds__(kBaseThreads) void base_tail_kernel(BaseArgs a, int
         fast_fail = 0;
       }
       __syncthreads();
-      bool distinct = true;
-      for (int i = 0; i < n; ++i)
-        for (int j = i + 1; j < n; ++j) distinct = distinct && bex[i] != bex[j];
-      if (distinct) {  // uniform: every thread read the same bids
+      // distinct experts: each lane holds one bidder's expert (lanes past n a
+      // sentinel of their own) and compares it with the others' by readlane
+      bool distinct;
+      {
+        const int ei = lane < n ? bex[lane] : -1 - lane;
+        bool clash = false;
+#pragma unroll
+        for (int j = 0; j < kBaseWaves; ++j) clash |= j != lane && __builtin_amdgcn_readlane(ei, j) == ei;
+        distinct = __ballot(clash) == 0;
+      }
+      if (distinct) {  // uniform: every wave read the same bids
         if (w < n) {
           bool bad;
           const int ev = base_wave_place(a, pr, hn, bex[w], bvv[w], U[w], lane, nullptr, nullptr, bad);
@@ -736,100 +742,109 @@ __global__ __launch_bounds__(kBaseThreads) void base_tail_kernel(BaseArgs a, int
     }
     if (tid == 0) nU2 = 0;
     __syncthreads();
-    // kr: bidders of the same expert ahead of this one; nbe: bidders of its expert
-    if (tid < n) {
-      const int e = bex[tid];
-      const double v = bvv[tid];
-      const int t = U[tid];
+    // wave 0, a lane per bidder: kr = bidders of the same expert ahead of it,
+    // nbe = bidders of its expert (the others' values by readlane); the best
+    // bidder of each expert (kr == 0) leads it
+    if (w == 0) {
+      const bool live = lane < n;
+      const int e = live ? bex[lane] : -1;
+      const double v = live ? bvv[lane] : 0.0;
+      const int t = live ? U[lane] : 0;
+      const uint2 vb = __builtin_bit_cast(uint2, v);
       int k = 0, m = 0;
       for (int q = 0; q < n; ++q) {
-        const bool same = bex[q] == e;
+        const int eq = __builtin_amdgcn_readlane(e, q);
+        const uint2 qb = {static_cast<unsigned>(__builtin_amdgcn_readlane(static_cast<int>(vb.x), q)),
+                          static_cast<unsigned>(__builtin_amdgcn_readlane(static_cast<int>(vb.y), q))};
+        const int tq = __builtin_amdgcn_readlane(t, q);
+        const bool same = eq == e;
         m += same;
-        k += same && base_before(bvv[q], U[q], v, t);
+        k += same && base_before(__builtin_bit_cast(double, qb), tq, v, t);
       }
-      kr[tid] = k;
-      nbe[tid] = m;
+      if (live) {
+        kr[lane] = k;
+        nbe[lane] = m;
+        pos[lane] = 0;
+      }
+      const bool lead = live && k == 0;
+      const uint64_t lm = __ballot(lead);
+      if (lead) ldr[popc_below(lm)] = lane;
+      if (lane == 0) nL = __popcll(lm);
     }
-    // pos: holders ahead of each bidder, one wave per bidder
-    for (int j = w; j < n; j += kBaseWaves) {
-      const int e = bex[j];
-      const double v = bvv[j];
-      const int t = U[j];
-      const int64_t base = static_cast<int64_t>(e) * c;
-      int cnt = 0;
+    __syncthreads();
+    // One wave per expert with bidders: its holders are read once, top-down
+    // 8 x 64 at a time, and every holder and bidder of the expert goes straight
+    // to its rank in the union (a holder: its place plus the expert's bidders
+    // ahead of it; a bidder: kr plus the holders ahead of it); ranks below c
+    // are kept.  A batch is read whole before it is written and a holder only
+    // moves up, so no unread slot is overwritten.
+    for (int li = w; li < nL; li += kBaseWaves) {
+      const int j0 = ldr[li];
+      const int e = bex[j0];
       const int nh = hn[e];
-#pragma unroll 4
-      for (int i = lane; i < nh; i += kWave) cnt += base_before(a.hold_v[base + i], a.hold_t[base + i], v, t);
+      const int64_t base = static_cast<int64_t>(e) * c;
+      for (int hi = nh; hi > 0; hi -= 8 * kWave) {
+        const int lo = max(0, hi - 8 * kWave);
+        double hv[8];
+        int ht[8], ahead[8];
 #pragma unroll
-      for (int off = 32; off >= 1; off >>= 1) cnt += __shfl_xor(cnt, off, kWave);
-      if (lane == 0) pos[j] = cnt;
-    }
-    __syncthreads();
-    if (tid < n) rk[tid] = kr[tid] + pos[tid];
-    if (w == 0) {  // moving holders: from the best bidder's position to the end, per expert
-      const int len = lane < n && kr[lane] == 0 ? hn[bex[lane]] - pos[lane] : 0;
-      int incl = len;
-#pragma unroll
-      for (int off = 1; off < kWave; off <<= 1) {
-        const int y = __shfl_up(incl, off, kWave);
-        if (lane >= off) incl += y;
-      }
-      if (lane < n) pref[lane + 1] = incl;
-      if (lane == 0) pref[0] = 0;
-    }
-    __syncthreads();
-    const int M = pref[n];
-    // chunks from the last: a holder only moves to a higher position
-    for (int ch = (M - 1) / kBaseThreads; ch >= 0 && M > 0; --ch) {
-      const int k = ch * kBaseThreads + tid;
-      const bool item = k < M;
-      int e = 0, nr = 0, t = 0;
-      double v = 0.0;
-      if (item) {
-        int lo = 0, hi = n;  // the j with pref[j] <= k < pref[j + 1]
-        while (lo < hi) {
-          const int mid = (lo + hi) >> 1;
-          if (pref[mid + 1] <= k) lo = mid + 1;
-          else hi = mid;
+        for (int q = 0; q < 8; ++q) {
+          const int i = lo + q * kWave + lane;
+          const int ic = i < hi ? i : lo;
+          hv[q] = a.hold_v[base + ic];
+          ht[q] = a.hold_t[base + ic];
+          ahead[q] = 0;
         }
-        e = bex[lo];
-        const int i = pos[lo] + (k - pref[lo]);
-        const int64_t at = static_cast<int64_t>(e) * c + i;
-        v = a.hold_v[at];
-        t = a.hold_t[at];
-        int cnt = 0;
-        for (int q = 0; q < n; ++q) cnt += bex[q] == e && base_before(bvv[q], U[q], v, t);
-        nr = i + cnt;
+        for (int b = 0; b < n; ++b) {
+          if (bex[b] != e) continue;  // uniform
+          const double bv = bvv[b];
+          const int bt = U[b];
+          int cnt = 0;  // holders of this batch ahead of bidder b
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            if (lo + q * kWave + lane >= hi) continue;
+            const bool b_first = base_before(bv, bt, hv[q], ht[q]);
+            ahead[q] += b_first;
+            cnt += !b_first;
+          }
+#pragma unroll
+          for (int off = 32; off >= 1; off >>= 1) cnt += __shfl_xor(cnt, off, kWave);
+          if (lane == 0) pos[b] += cnt;
+        }
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const int i = lo + q * kWave + lane;
+          if (i >= hi) continue;
+          const int nr = i + ahead[q];
+          if (nr < c) {
+            if (nr != i) {
+              a.hold_v[base + nr] = hv[q];
+              a.hold_t[base + nr] = ht[q];
+            }
+            if (nr == c - 1) pr[e] = hv[q];
+          } else {
+            a.assign[ht[q]] = -1;  // evicted
+            const int pq = atomicAdd(&nU2, 1);
+            if (pq < kBaseTail) U2[pq] = ht[q];
+          }
+        }
       }
-      __syncthreads();
-      if (item) {
-        if (nr < c) {
-          const int64_t at = static_cast<int64_t>(e) * c + nr;
-          a.hold_v[at] = v;
-          a.hold_t[at] = t;
-          if (nr == c - 1) pr[e] = v;
+      // the expert's bidders at their ranks (pos holds this wave's own sums)
+      for (int b = lane; b < n; b += kWave) {
+        if (bex[b] != e) continue;
+        const int r = kr[b] + pos[b];
+        const int t = U[b];
+        if (r < c) {
+          a.hold_v[base + r] = bvv[b];
+          a.hold_t[base + r] = t;
+          a.assign[t] = e;
+          if (r == c - 1) pr[e] = bvv[b];
         } else {
-          a.assign[t] = -1;  // evicted
-          const int p = atomicAdd(&nU2, 1);
-          if (p < kBaseTail) U2[p] = t;
+          const int pq = atomicAdd(&nU2, 1);
+          if (pq < kBaseTail) U2[pq] = t;
         }
       }
-      __syncthreads();
-    }
-    if (tid < n) {
-      const int e = bex[tid];
-      const int t = U[tid];
-      if (rk[tid] < c) {
-        const int64_t at = static_cast<int64_t>(e) * c + rk[tid];
-        a.hold_v[at] = bvv[tid];
-        a.hold_t[at] = t;
-        a.assign[t] = e;
-        if (rk[tid] == c - 1) pr[e] = bvv[tid];
-      } else {
-        const int p = atomicAdd(&nU2, 1);
-        if (p < kBaseTail) U2[p] = t;
-      }
-      if (kr[tid] == 0) hn[e] = min(c, hn[e] + nbe[tid]);
+      if (lane == 0) hn[e] = min(c, nh + nbe[j0]);
     }
     __syncthreads();
     const int n2 = nU2;

@@ -570,7 +570,7 @@ __global__ __launch_bounds__(kBaseThreads) void base_tail_kernel(BaseArgs a, int
   int* hn = reinterpret_cast<int*>(hvs + c);          // holder counts [E]
   int* hts = hn + E;                                  // the holders' tokens [c]
   __shared__ int U[kBaseTail], U2[kBaseTail];
-  __shared__ int bex[kBaseTail], kr[kBaseTail], nbe[kBaseTail], pos[kBaseTail], ldr[kBaseTail];
+  __shared__ int bex[kBaseTail], kr[kBaseTail], nbe[kBaseTail], ldr[kBaseTail];
   __shared__ double bvv[kBaseTail];
   __shared__ int nU, nU2, nL, fast_rounds, fast_fail;
   const int tid = threadIdx.x, lane = lane_id(), w = tid / kWave;
@@ -764,7 +764,6 @@ __global__ __launch_bounds__(kBaseThreads) void base_tail_kernel(BaseArgs a, int
       if (live) {
         kr[lane] = k;
         nbe[lane] = m;
-        pos[lane] = 0;
       }
       const bool lead = live && k == 0;
       const uint64_t lm = __ballot(lead);
@@ -783,6 +782,13 @@ __global__ __launch_bounds__(kBaseThreads) void base_tail_kernel(BaseArgs a, int
       const int e = bex[j0];
       const int nh = hn[e];
       const int64_t base = static_cast<int64_t>(e) * c;
+      // this expert's bidders: lanes b < n with bex[b] == e; lane b keeps its
+      // bid and token, and sums the holders ahead of it in `ahead_b`
+      const bool mine = lane < n && bex[lane] == e;
+      const uint64_t bm = __ballot(mine);
+      const uint2 lvb = __builtin_bit_cast(uint2, lane < n ? bvv[lane] : 0.0);
+      const int lt = lane < n ? U[lane] : 0;
+      int ahead_b = 0;
       for (int hi = nh; hi > 0; hi -= 8 * kWave) {
         const int lo = max(0, hi - 8 * kWave);
         double hv[8];
@@ -795,10 +801,12 @@ __global__ __launch_bounds__(kBaseThreads) void base_tail_kernel(BaseArgs a, int
           ht[q] = a.hold_t[base + ic];
           ahead[q] = 0;
         }
-        for (int b = 0; b < n; ++b) {
-          if (bex[b] != e) continue;  // uniform
-          const double bv = bvv[b];
-          const int bt = U[b];
+        for (uint64_t rem = bm; rem != 0; rem &= rem - 1) {  // uniform
+          const int b = static_cast<int>(__builtin_ctzll(rem));
+          const uint2 qb = {static_cast<unsigned>(__builtin_amdgcn_readlane(static_cast<int>(lvb.x), b)),
+                            static_cast<unsigned>(__builtin_amdgcn_readlane(static_cast<int>(lvb.y), b))};
+          const double bv = __builtin_bit_cast(double, qb);
+          const int bt = __builtin_amdgcn_readlane(lt, b);
           int cnt = 0;  // holders of this batch ahead of bidder b
 #pragma unroll
           for (int q = 0; q < 8; ++q) {
@@ -809,7 +817,7 @@ __global__ __launch_bounds__(kBaseThreads) void base_tail_kernel(BaseArgs a, int
           }
 #pragma unroll
           for (int off = 32; off >= 1; off >>= 1) cnt += __shfl_xor(cnt, off, kWave);
-          if (lane == 0) pos[b] += cnt;
+          if (lane == b) ahead_b += cnt;
         }
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
@@ -829,19 +837,18 @@ __global__ __launch_bounds__(kBaseThreads) void base_tail_kernel(BaseArgs a, int
           }
         }
       }
-      // the expert's bidders at their ranks (pos holds this wave's own sums)
-      for (int b = lane; b < n; b += kWave) {
-        if (bex[b] != e) continue;
-        const int r = kr[b] + pos[b];
-        const int t = U[b];
+      // the expert's bidders at their ranks
+      if (mine) {
+        const int r = kr[lane] + ahead_b;
+        const double bv = __builtin_bit_cast(double, lvb);
         if (r < c) {
-          a.hold_v[base + r] = bvv[b];
-          a.hold_t[base + r] = t;
-          a.assign[t] = e;
-          if (r == c - 1) pr[e] = bvv[b];
+          a.hold_v[base + r] = bv;
+          a.hold_t[base + r] = lt;
+          a.assign[lt] = e;
+          if (r == c - 1) pr[e] = bv;
         } else {
           const int pq = atomicAdd(&nU2, 1);
-          if (pq < kBaseTail) U2[pq] = t;
+          if (pq < kBaseTail) U2[pq] = lt;
         }
       }
       if (lane == 0) hn[e] = min(c, nh + nbe[j0]);

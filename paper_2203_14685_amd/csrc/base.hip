@@ -457,13 +457,11 @@ __device__ __forceinline__ void base_wave_bid(const BaseArgs& a, const double* p
 }
 
 // Expert e takes the only bid for it this round, (bid, t): the holders ahead
-// of it are counted by the lanes, the holders behind it move up one place,
-// the last one dropping out when the list is full.  With `hvs`/`hts` (LDS of c
-// entries) the holders are staged there while counted; without, the moving
-// ones are read again, from the end, 64 at a time (each block is read before
-// the next lower block can overwrite its first slot).  Returns the evicted
-// token or -1; `bad` is set if the bid does not rank below c (it always does:
-// a bid exceeds its expert's price, the c-th best bid).
+// of it are counted by the lanes while staged in `hvs`/`hts` (LDS of c
+// entries), then the holders behind it move up one place from there, the last
+// one dropping out when the list is full.  Returns the evicted token or -1;
+// `bad` is set if the bid does not rank below c (it always does: a bid
+// exceeds its expert's price, the c-th best bid).
 __device__ __forceinline__ int base_wave_place(const BaseArgs& a, double* pr, int* hn, int e, double bid, int t,
                                                int lane, double* hvs, int* hts, bool& bad) {
   const int c = a.cap;
@@ -487,10 +485,8 @@ __device__ __forceinline__ int base_wave_place(const BaseArgs& a, double* pr, in
     for (int q = 0; q < 8; ++q) {
       const int i = i0 + q * kWave + lane;
       if (i >= nh) continue;
-      if (hvs) {
-        hvs[i] = hv[q];
-        hts[i] = ht[q];
-      }
+      hvs[i] = hv[q];
+      hts[i] = ht[q];
       p += base_before(hv[q], ht[q], bid, t);
       if (i == c - 1) ev = ht[q];
       if (i == c - 2) vlast = hv[q];
@@ -504,37 +500,12 @@ __device__ __forceinline__ int base_wave_place(const BaseArgs& a, double* pr, in
   vlast = __shfl(vlast, (c - 2) & (kWave - 1), kWave);
   bad = p >= c;
   if (bad) return -1;
-  if (hvs) {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    for (int i = p + lane; i < min(nh, c - 1); i += kWave) {
-      a.hold_v[base + i + 1] = hvs[i];
-      a.hold_t[base + i + 1] = hts[i];
-    }
-  } else {
-    // from the end, 8 x 64 holders at a time: a batch is read whole before its
-    // shifted copy is written, and its writes start one above the batch below
-    for (int top = min(nh, c - 1); top > p; top -= 8 * kWave) {
-      const int lo = max(p, top - 8 * kWave);
-      double hv[8];
-      int ht[8];
-#pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        const int i = lo + q * kWave + lane;
-        const int ic = i < top ? i : lo;
-        hv[q] = a.hold_v[base + ic];
-        ht[q] = a.hold_t[base + ic];
-      }
-#pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        const int i = lo + q * kWave + lane;
-        if (i < top) {
-          a.hold_v[base + i + 1] = hv[q];
-          a.hold_t[base + i + 1] = ht[q];
-        }
-      }
-    }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  for (int i = p + lane; i < min(nh, c - 1); i += kWave) {
+    a.hold_v[base + i + 1] = hvs[i];
+    a.hold_t[base + i + 1] = hts[i];
   }
   if (lane == 0) {
     a.hold_v[base + p] = bid;
@@ -546,6 +517,89 @@ __device__ __forceinline__ int base_wave_place(const BaseArgs& a, double* pr, in
     hn[e] = nn;
   }
   return ev;
+}
+
+// The holders of expert e and its bidders this round (lanes b < n with bit b of
+// `bm` set: bids in bvv[b], tokens in U[b], kr[b] of them ahead of each one
+// among themselves), ranked together: the holders are read once, top-down
+// 8 x 64 at a time, and every holder and bidder goes straight to its rank in
+// the union (a holder: its place plus the bidders ahead of it; a bidder: kr,
+// or 0 without `kr`, plus the holders ahead of it); ranks below c are kept, the others join the
+// unassigned list U2.  A batch is read whole before it is written and a
+// holder only moves up, so no unread slot is overwritten.  One wave.
+__device__ __forceinline__ void base_wave_merge(const BaseArgs& a, double* pr, int* hn, int e, uint64_t bm, int nbid,
+                                            int n, const double* bvv, const int* U, const int* kr, int lane,
+                                            int* U2, int* nU2) {
+  const int c = a.cap;
+  const bool mine = (bm >> lane) & 1;
+  const uint2 lvb = __builtin_bit_cast(uint2, lane < n ? bvv[lane] : 0.0);
+  const int lt = lane < n ? U[lane] : 0;
+  int ahead_b = 0;  // lane b: holders ahead of bidder b
+  const int nh = hn[e];
+  const int64_t base = static_cast<int64_t>(e) * c;
+  for (int hi = nh; hi > 0; hi -= 8 * kWave) {
+    const int lo = max(0, hi - 8 * kWave);
+    double hv[8];
+    int ht[8], ahead[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int i = lo + q * kWave + lane;
+      const int ic = i < hi ? i : lo;
+      hv[q] = a.hold_v[base + ic];
+      ht[q] = a.hold_t[base + ic];
+      ahead[q] = 0;
+    }
+    for (uint64_t rem = bm; rem != 0; rem &= rem - 1) {  // uniform
+      const int b = static_cast<int>(__builtin_ctzll(rem));
+      const uint2 qb = {static_cast<unsigned>(__builtin_amdgcn_readlane(static_cast<int>(lvb.x), b)),
+                        static_cast<unsigned>(__builtin_amdgcn_readlane(static_cast<int>(lvb.y), b))};
+      const double bv = __builtin_bit_cast(double, qb);
+      const int bt = __builtin_amdgcn_readlane(lt, b);
+      int cnt = 0;  // holders of this batch ahead of bidder b
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        if (lo + q * kWave + lane >= hi) continue;
+        const bool b_first = base_before(bv, bt, hv[q], ht[q]);
+        ahead[q] += b_first;
+        cnt += !b_first;
+      }
+#pragma unroll
+      for (int off = 32; off >= 1; off >>= 1) cnt += __shfl_xor(cnt, off, kWave);
+      if (lane == b) ahead_b += cnt;
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int i = lo + q * kWave + lane;
+      if (i >= hi) continue;
+      const int nr = i + ahead[q];
+      if (nr < c) {
+        if (nr != i) {
+          a.hold_v[base + nr] = hv[q];
+          a.hold_t[base + nr] = ht[q];
+        }
+        if (nr == c - 1) pr[e] = hv[q];
+      } else {
+        a.assign[ht[q]] = -1;  // evicted
+        const int pq = atomicAdd(nU2, 1);
+        if (pq < kBaseTail) U2[pq] = ht[q];
+      }
+    }
+  }
+  // the expert's bidders at their ranks
+  if (mine) {
+    const int r = (kr ? kr[lane] : 0) + ahead_b;
+    const double bv = __builtin_bit_cast(double, lvb);
+    if (r < c) {
+      a.hold_v[base + r] = bv;
+      a.hold_t[base + r] = lt;
+      a.assign[lt] = e;
+      if (r == c - 1) pr[e] = bv;
+    } else {
+      const int pq = atomicAdd(nU2, 1);
+      if (pq < kBaseTail) U2[pq] = lt;
+    }
+  }
+  if (lane == 0) hn[e] = min(c, nh + nbid);
 }
 
 // ---------------------------------------------------------------- tail
@@ -687,22 +741,8 @@ __global__ __launch_bounds__(kBaseThreads) void base_tail_kernel(BaseArgs a, int
         distinct = __ballot(clash) == 0;
       }
       if (distinct) {  // uniform: every wave read the same bids
-        if (w < n) {
-          bool bad;
-          const int ev = base_wave_place(a, pr, hn, bex[w], bvv[w], U[w], lane, nullptr, nullptr, bad);
-          if (lane == 0) {
-            if (bad) fast_fail = 1;
-            if (ev >= 0) {
-              const int q = atomicAdd(&nU2, 1);
-              if (q < kBaseTail) U2[q] = ev;
-            }
-          }
-        }
+        if (w < n) base_wave_merge(a, pr, hn, bex[w], 1ull << w, 1, n, bvv, U, nullptr, lane, U2, &nU2);
         __syncthreads();
-        if (fast_fail) {
-          failed = 1;
-          break;
-        }
         const int n2 = nU2;
         if (tid < min(n2, kBaseTail)) U[tid] = U2[tid];
         if (tid == 0) nU = n2;
@@ -778,80 +818,9 @@ __global__ __launch_bounds__(kBaseThreads) void base_tail_kernel(BaseArgs a, int
     // are kept.  A batch is read whole before it is written and a holder only
     // moves up, so no unread slot is overwritten.
     for (int li = w; li < nL; li += kBaseWaves) {
-      const int j0 = ldr[li];
-      const int e = bex[j0];
-      const int nh = hn[e];
-      const int64_t base = static_cast<int64_t>(e) * c;
-      // this expert's bidders: lanes b < n with bex[b] == e; lane b keeps its
-      // bid and token, and sums the holders ahead of it in `ahead_b`
-      const bool mine = lane < n && bex[lane] == e;
-      const uint64_t bm = __ballot(mine);
-      const uint2 lvb = __builtin_bit_cast(uint2, lane < n ? bvv[lane] : 0.0);
-      const int lt = lane < n ? U[lane] : 0;
-      int ahead_b = 0;
-      for (int hi = nh; hi > 0; hi -= 8 * kWave) {
-        const int lo = max(0, hi - 8 * kWave);
-        double hv[8];
-        int ht[8], ahead[8];
-#pragma unroll
-        for (int q = 0; q < 8; ++q) {
-          const int i = lo + q * kWave + lane;
-          const int ic = i < hi ? i : lo;
-          hv[q] = a.hold_v[base + ic];
-          ht[q] = a.hold_t[base + ic];
-          ahead[q] = 0;
-        }
-        for (uint64_t rem = bm; rem != 0; rem &= rem - 1) {  // uniform
-          const int b = static_cast<int>(__builtin_ctzll(rem));
-          const uint2 qb = {static_cast<unsigned>(__builtin_amdgcn_readlane(static_cast<int>(lvb.x), b)),
-                            static_cast<unsigned>(__builtin_amdgcn_readlane(static_cast<int>(lvb.y), b))};
-          const double bv = __builtin_bit_cast(double, qb);
-          const int bt = __builtin_amdgcn_readlane(lt, b);
-          int cnt = 0;  // holders of this batch ahead of bidder b
-#pragma unroll
-          for (int q = 0; q < 8; ++q) {
-            if (lo + q * kWave + lane >= hi) continue;
-            const bool b_first = base_before(bv, bt, hv[q], ht[q]);
-            ahead[q] += b_first;
-            cnt += !b_first;
-          }
-#pragma unroll
-          for (int off = 32; off >= 1; off >>= 1) cnt += __shfl_xor(cnt, off, kWave);
-          if (lane == b) ahead_b += cnt;
-        }
-#pragma unroll
-        for (int q = 0; q < 8; ++q) {
-          const int i = lo + q * kWave + lane;
-          if (i >= hi) continue;
-          const int nr = i + ahead[q];
-          if (nr < c) {
-            if (nr != i) {
-              a.hold_v[base + nr] = hv[q];
-              a.hold_t[base + nr] = ht[q];
-            }
-            if (nr == c - 1) pr[e] = hv[q];
-          } else {
-            a.assign[ht[q]] = -1;  // evicted
-            const int pq = atomicAdd(&nU2, 1);
-            if (pq < kBaseTail) U2[pq] = ht[q];
-          }
-        }
-      }
-      // the expert's bidders at their ranks
-      if (mine) {
-        const int r = kr[lane] + ahead_b;
-        const double bv = __builtin_bit_cast(double, lvb);
-        if (r < c) {
-          a.hold_v[base + r] = bv;
-          a.hold_t[base + r] = lt;
-          a.assign[lt] = e;
-          if (r == c - 1) pr[e] = bv;
-        } else {
-          const int pq = atomicAdd(&nU2, 1);
-          if (pq < kBaseTail) U2[pq] = lt;
-        }
-      }
-      if (lane == 0) hn[e] = min(c, nh + nbe[j0]);
+      const int e = bex[ldr[li]];
+      const uint64_t bm = __ballot(lane < n && bex[lane] == e);
+      base_wave_merge(a, pr, hn, e, bm, nbe[ldr[li]], n, bvv, U, kr, lane, U2, &nU2);
     }
     __syncthreads();
     const int n2 = nU2;

@@ -209,6 +209,24 @@ def test_base_full_size(wid):
     print(f"[stats] base full size W{wid}: dual gap {gap:.3e} bound {S * g['info']['eps']:.3e} {g['info']}", flush=True)
 
 
+def test_base_many_experts_large_batch():
+    """S = 65536 tokens over E = 128 experts (c = 512), scores given, a quarter
+    of the experts favoured so that the auction runs long eviction chains and
+    crowded rounds: exact balance, the optimality certificate on the scores,
+    slots by their definition."""
+    S, E = 65536, 128
+    announce(f"base many experts S={S} E={E}")
+    rng = np.random.default_rng(21)
+    L = rng.standard_normal((S, E)).astype(np.float32)
+    L[:, : E // 4] += np.float32(0.8)
+    g = run_base(L=L, E=E)
+    ids = g["ids"][:, 0]
+    assert_equal(np.bincount(ids, minlength=E), np.full(E, S // E), "tokens per expert")
+    gap = certify(L.astype(np.float64), g, E)
+    slots_by_property(ids, g["slots"], g["counts"], g["slot_src"], E, S // E)
+    print(f"[stats] base S={S} E={E}: dual gap {gap:.3e} bound {S * g['info']['eps']:.3e} {g['info']}", flush=True)
+
+
 def test_base_capacity_and_layout():
     """Capacity below S / E drops the later tokens of each expert; dispatch and
     combine take the routing as any k = 1 gate's."""

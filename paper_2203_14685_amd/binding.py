@@ -1,8 +1,9 @@
 """ctypes binding of libhetumoe.so (argument marshalling only).
 
 The functions named like the C ABI (moe_gate, moe_dispatch, ...) take torch
-tensors that already live on the GPU, check dtype / device / contiguity, and
-forward raw device pointers plus torch's current HIP stream.  The convenience
+tensors that already live on the GPU, check dtype / device / contiguity and
+that each holds the elements the call's sizes need, and forward raw device
+pointers plus torch's current HIP stream.  The convenience
 wrappers (gate, dispatch, ...) additionally allocate the outputs with
 torch.empty; every value is computed by the library's HIP kernels.  There is no
 fallback: if the library is missing or fails to load, every call raises.
@@ -133,11 +134,22 @@ def _ptr(t, dtype=None, name="tensor"):
         raise TypeError(f"{name} must be a torch.Tensor or None")
     if t.device.type != "cuda":
         raise ValueError(f"{name} must be on the GPU, found {t.device}")
+    if torch.cuda.device_count() > 1 and t.device.index is not None and t.device.index != torch.cuda.current_device():
+        raise ValueError(f"{name} is on {t.device}, but the library launches on cuda:{torch.cuda.current_device()}")
     if not t.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
     if dtype is not None and t.dtype != dtype:
         raise TypeError(f"{name} must be {dtype}, found {t.dtype}")
     return t.data_ptr() if t.numel() > 0 else None
+
+
+def _need(*specs):
+    """Each spec is (tensor or None, elements required, name): a tensor smaller
+    than the call's sizes would let a kernel run past its end, so it is
+    refused here, before anything reaches the device."""
+    for t, n, name in specs:
+        if isinstance(t, torch.Tensor) and t.numel() < n:
+            raise ValueError(f"{name} holds {t.numel()} elements; the call's sizes need {n}")
 
 
 def _stream(stream):
@@ -163,6 +175,11 @@ def moe_gate(params, x, wg, bias, token_ids, noise, hash_table, logits, ids, slo
     lib = load()
     f32, i32 = torch.float32, torch.int32
     xdt = torch.bfloat16 if params.dtype == MOE_BF16 else torch.float32
+    S, d, E, k, C = params.S, params.d, params.E, params.k, params.capacity
+    _need((x, S * d, "x"), (wg, d * E, "wg"), (bias, E, "bias"), (token_ids, S, "token_ids"), (noise, S * E, "noise"),
+          (hash_table, params.hash_vocab, "hash_table"), (logits, S * E, "logits"), (ids, S * k, "ids"),
+          (slots, S * k, "slots"), (weights, S * k, "weights"), (counts, E, "counts"), (demand, E, "demand"),
+          (slot_src, E * C, "slot_src"))
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(lib.moe_gate(
         ctypes.byref(params), _ptr(x, xdt, "x"), _ptr(wg, xdt, "wg"), _ptr(bias, f32, "bias"),
@@ -177,15 +194,26 @@ def _layout(S, d, E, k, capacity, dtype):
     return Layout(S, d, E, k, capacity, dtype)
 
 
+def _rows(layout):
+    """Elements of a token-row buffer [S, d], an expert buffer [E, C, d], a
+    per-choice array [S, k] and slot_src [E, C] for this layout."""
+    S, d, E, k, C = layout.S, layout.d, layout.E, layout.k, layout.capacity
+    return S * d, E * C * d, S * k, E * C
+
+
 def moe_dispatch(layout, x, ids, slots, slot_src, xe, stream=None):
     dt = torch.bfloat16 if layout.dtype == MOE_BF16 else torch.float32
     i32 = torch.int32
+    tok, exp, ch, src = _rows(layout)
+    _need((x, tok, "x"), (ids, ch, "ids"), (slots, ch, "slots"), (slot_src, src, "slot_src"), (xe, exp, "xe"))
     _check(load().moe_dispatch(ctypes.byref(layout), _ptr(x, dt, "x"), _ptr(ids, i32, "ids"), _ptr(slots, i32, "slots"),
                                _ptr(slot_src, i32, "slot_src"), _ptr(xe, dt, "xe"), _stream(stream)))
 
 
 def moe_combine(layout, ye, ids, slots, weights, y, stream=None):
     dt = torch.bfloat16 if layout.dtype == MOE_BF16 else torch.float32
+    tok, exp, ch, _ = _rows(layout)
+    _need((ye, exp, "ye"), (ids, ch, "ids"), (slots, ch, "slots"), (weights, ch, "weights"), (y, tok, "y"))
     _check(load().moe_combine(ctypes.byref(layout), _ptr(ye, dt, "ye"), _ptr(ids, torch.int32, "ids"),
                               _ptr(slots, torch.int32, "slots"), _ptr(weights, torch.float32, "weights"),
                               _ptr(y, dt, "y"), _stream(stream)))
@@ -193,6 +221,8 @@ def moe_combine(layout, ye, ids, slots, weights, y, stream=None):
 
 def moe_dispatch_bwd(layout, dxe, ids, slots, dx, stream=None):
     dt = torch.bfloat16 if layout.dtype == MOE_BF16 else torch.float32
+    tok, exp, ch, _ = _rows(layout)
+    _need((dxe, exp, "dxe"), (ids, ch, "ids"), (slots, ch, "slots"), (dx, tok, "dx"))
     _check(load().moe_dispatch_bwd(ctypes.byref(layout), _ptr(dxe, dt, "dxe"), _ptr(ids, torch.int32, "ids"),
                                    _ptr(slots, torch.int32, "slots"), _ptr(dx, dt, "dx"), _stream(stream)))
 
@@ -200,6 +230,9 @@ def moe_dispatch_bwd(layout, dxe, ids, slots, dx, stream=None):
 def moe_combine_bwd(layout, dy, ye, ids, slots, slot_src, weights, dye, dw, stream=None):
     dt = torch.bfloat16 if layout.dtype == MOE_BF16 else torch.float32
     i32 = torch.int32
+    tok, exp, ch, src = _rows(layout)
+    _need((dy, tok, "dy"), (ye, exp, "ye"), (ids, ch, "ids"), (slots, ch, "slots"), (slot_src, src, "slot_src"),
+          (weights, ch, "weights"), (dye, exp, "dye"), (dw, ch, "dw"))
     _check(load().moe_combine_bwd(ctypes.byref(layout), _ptr(dy, dt, "dy"), _ptr(ye, dt, "ye"), _ptr(ids, i32, "ids"),
                                   _ptr(slots, i32, "slots"), _ptr(slot_src, i32, "slot_src"),
                                   _ptr(weights, torch.float32, "weights"), _ptr(dye, dt, "dye"),
@@ -273,6 +306,10 @@ def moe_base_gate(params, x, wg, bias, logits, ids, slots, weights, counts, slot
     lib = load()
     f32, i32 = torch.float32, torch.int32
     xdt = torch.bfloat16 if params.dtype == MOE_BF16 else torch.float32
+    S, d, E, C = params.S, params.d, params.E, params.capacity
+    _need((x, S * d, "x"), (wg, d * E, "wg"), (bias, E, "bias"), (logits, S * E, "logits"), (ids, S, "ids"),
+          (slots, S, "slots"), (weights, S, "weights"), (counts, E, "counts"), (slot_src, E * C, "slot_src"),
+          (prices, E, "prices"))
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(lib.moe_base_gate(
         ctypes.byref(params), _ptr(x, xdt, "x"), _ptr(wg, xdt, "wg"), _ptr(bias, f32, "bias"),
@@ -364,6 +401,10 @@ def moe_gate_bwd_workspace_size(params):
 def moe_gate_bwd(params, x, wg, logits, ids, dw, dlogits, dx, dwg, dbias, aux_loss, workspace, stream=None):
     dt = torch.bfloat16 if params.dtype == MOE_BF16 else torch.float32
     f32, i32 = torch.float32, torch.int32
+    S, d, E, k = params.S, params.d, params.E, params.k
+    _need((x, S * d, "x"), (wg, d * E, "wg"), (logits, S * E, "logits"), (ids, S * k, "ids"), (dw, S * k, "dw"),
+          (dlogits, S * E, "dlogits"), (dx, S * d, "dx"), (dwg, d * E, "dwg"), (dbias, E, "dbias"),
+          (aux_loss, 1, "aux_loss"))
     ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
     _check(load().moe_gate_bwd(ctypes.byref(params), _ptr(x, dt, "x"), _ptr(wg, dt, "wg"),
                                _ptr(logits, f32, "logits"), _ptr(ids, i32, "ids"), _ptr(dw, f32, "dw"),

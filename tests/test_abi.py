@@ -329,3 +329,36 @@ def test_base_pointer_checks(lib):
     pl = hm.base_params(128, 0, 8, 16, 1, b.MOE_F32)
     assert call(pl, x=None, wg=None) == b.MOE_ERR_INVALID_ARG          # logits_in needs logits
     assert call(pl, logits=A16) == b.MOE_ERR_INVALID_ARG               # ... and no x / wg
+
+
+def test_binding_rejects_short_buffers():
+    """A tensor smaller than the call's sizes is refused before any device work
+    (checked here on CPU tensors: the size check comes first)."""
+    import torch
+    i32 = torch.int32
+    lay = b.Layout(100, 64, 8, 2, 30, b.MOE_F32)
+    x = torch.zeros(100 * 64)
+    xe_short = torch.zeros(8 * 30 * 64 - 1)
+    ch = torch.zeros(200, dtype=i32)
+    src = torch.zeros(8 * 30, dtype=i32)
+    with pytest.raises(ValueError, match="xe holds"):
+        b.moe_dispatch(lay, x, ch, ch, src, xe_short)
+    with pytest.raises(ValueError, match="slots holds"):
+        b.moe_combine(lay, torch.zeros(8 * 30 * 64), ch, ch[:199], torch.zeros(200), torch.zeros(100 * 64))
+    with pytest.raises(ValueError, match="dw holds"):
+        b.moe_combine_bwd(lay, x, torch.zeros(8 * 30 * 64), ch, ch, src, torch.zeros(200), torch.zeros(8 * 30 * 64),
+                          torch.zeros(199))
+    with pytest.raises(ValueError, match="dx holds"):
+        b.moe_dispatch_bwd(lay, torch.zeros(8 * 30 * 64), ch, ch, torch.zeros(100 * 64 - 64))
+    p = b.gate_params(100, 64, 8, 2, 30, b.MOE_GATE_TOPK)
+    with pytest.raises(ValueError, match="slot_src holds"):
+        b.moe_gate(p, x, torch.zeros(64 * 8), None, None, None, None, None, ch, ch, torch.zeros(200),
+                   torch.zeros(8, dtype=i32), None, src[:-1], None)
+    pb = b.gate_bwd_params(100, 64, 8, 2, b.MOE_GATE_TOPK)
+    with pytest.raises(ValueError, match="logits holds"):
+        b.moe_gate_bwd(pb, None, None, torch.zeros(799), ch, torch.zeros(200), None, None, None, None, None, None)
+    pbase = b.base_params(96, 64, 8, 12)
+    with pytest.raises(ValueError, match="prices holds"):
+        b.moe_base_gate(pbase, torch.zeros(96 * 64), torch.zeros(64 * 8), None, None, torch.zeros(96, dtype=i32),
+                        torch.zeros(96, dtype=i32), torch.zeros(96), torch.zeros(8, dtype=i32),
+                        torch.zeros(96, dtype=i32), torch.zeros(7, dtype=torch.float64), None)

@@ -126,30 +126,32 @@ def _dtype_code(t):
     raise TypeError(f"unsupported dtype {t.dtype}; float32 or bfloat16 expected")
 
 
-def _ptr(t, dtype=None, name="tensor"):
-    """Device pointer of a contiguous GPU tensor (None -> NULL)."""
+_multi_gpu = None
+
+
+def _ptr(t, dtype=None, name="tensor", n=0):
+    """Device pointer of a contiguous GPU tensor (None -> NULL) holding at
+    least n elements: a tensor smaller than the call's sizes would let a kernel
+    run past its end, so it is refused here, before anything reaches the device."""
+    global _multi_gpu
     if t is None:
         return None
     if not isinstance(t, torch.Tensor):
         raise TypeError(f"{name} must be a torch.Tensor or None")
+    numel = t.numel()
+    if numel < n:
+        raise ValueError(f"{name} holds {numel} elements; the call's sizes need {n}")
     if t.device.type != "cuda":
         raise ValueError(f"{name} must be on the GPU, found {t.device}")
-    if torch.cuda.device_count() > 1 and t.device.index is not None and t.device.index != torch.cuda.current_device():
+    if _multi_gpu is None:
+        _multi_gpu = torch.cuda.device_count() > 1
+    if _multi_gpu and t.device.index is not None and t.device.index != torch.cuda.current_device():
         raise ValueError(f"{name} is on {t.device}, but the library launches on cuda:{torch.cuda.current_device()}")
     if not t.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
     if dtype is not None and t.dtype != dtype:
         raise TypeError(f"{name} must be {dtype}, found {t.dtype}")
-    return t.data_ptr() if t.numel() > 0 else None
-
-
-def _need(*specs):
-    """Each spec is (tensor or None, elements required, name): a tensor smaller
-    than the call's sizes would let a kernel run past its end, so it is
-    refused here, before anything reaches the device."""
-    for t, n, name in specs:
-        if isinstance(t, torch.Tensor) and t.numel() < n:
-            raise ValueError(f"{name} holds {t.numel()} elements; the call's sizes need {n}")
+    return t.data_ptr() if numel > 0 else None
 
 
 def _stream(stream):
@@ -176,18 +178,14 @@ def moe_gate(params, x, wg, bias, token_ids, noise, hash_table, logits, ids, slo
     f32, i32 = torch.float32, torch.int32
     xdt = torch.bfloat16 if params.dtype == MOE_BF16 else torch.float32
     S, d, E, k, C = params.S, params.d, params.E, params.k, params.capacity
-    _need((x, S * d, "x"), (wg, d * E, "wg"), (bias, E, "bias"), (token_ids, S, "token_ids"), (noise, S * E, "noise"),
-          (hash_table, params.hash_vocab, "hash_table"), (logits, S * E, "logits"), (ids, S * k, "ids"),
-          (slots, S * k, "slots"), (weights, S * k, "weights"), (counts, E, "counts"), (demand, E, "demand"),
-          (slot_src, E * C, "slot_src"))
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(lib.moe_gate(
-        ctypes.byref(params), _ptr(x, xdt, "x"), _ptr(wg, xdt, "wg"), _ptr(bias, f32, "bias"),
-        _ptr(token_ids, i32, "token_ids"), _ptr(noise, f32, "noise"), _ptr(hash_table, i32, "hash_table"),
-        _ptr(logits, f32, "logits"), _ptr(ids, i32, "ids"),
-        _ptr(slots, i32, "slots"), _ptr(weights, f32, "weights"), _ptr(counts, i32, "counts"),
-        _ptr(demand, i32, "demand"), _ptr(slot_src, i32, "slot_src"), _ptr(workspace, None, "workspace"),
-        ws_bytes, _stream(stream)))
+        ctypes.byref(params), _ptr(x, xdt, "x", S * d), _ptr(wg, xdt, "wg", d * E), _ptr(bias, f32, "bias", E),
+        _ptr(token_ids, i32, "token_ids", S), _ptr(noise, f32, "noise", S * E),
+        _ptr(hash_table, i32, "hash_table", params.hash_vocab), _ptr(logits, f32, "logits", S * E),
+        _ptr(ids, i32, "ids", S * k), _ptr(slots, i32, "slots", S * k), _ptr(weights, f32, "weights", S * k),
+        _ptr(counts, i32, "counts", E), _ptr(demand, i32, "demand", E), _ptr(slot_src, i32, "slot_src", E * C),
+        _ptr(workspace, None, "workspace"), ws_bytes, _stream(stream)))
 
 
 def _layout(S, d, E, k, capacity, dtype):
@@ -205,38 +203,35 @@ def moe_dispatch(layout, x, ids, slots, slot_src, xe, stream=None):
     dt = torch.bfloat16 if layout.dtype == MOE_BF16 else torch.float32
     i32 = torch.int32
     tok, exp, ch, src = _rows(layout)
-    _need((x, tok, "x"), (ids, ch, "ids"), (slots, ch, "slots"), (slot_src, src, "slot_src"), (xe, exp, "xe"))
-    _check(load().moe_dispatch(ctypes.byref(layout), _ptr(x, dt, "x"), _ptr(ids, i32, "ids"), _ptr(slots, i32, "slots"),
-                               _ptr(slot_src, i32, "slot_src"), _ptr(xe, dt, "xe"), _stream(stream)))
+    _check(load().moe_dispatch(ctypes.byref(layout), _ptr(x, dt, "x", tok), _ptr(ids, i32, "ids", ch),
+                               _ptr(slots, i32, "slots", ch), _ptr(slot_src, i32, "slot_src", src),
+                               _ptr(xe, dt, "xe", exp), _stream(stream)))
 
 
 def moe_combine(layout, ye, ids, slots, weights, y, stream=None):
     dt = torch.bfloat16 if layout.dtype == MOE_BF16 else torch.float32
     tok, exp, ch, _ = _rows(layout)
-    _need((ye, exp, "ye"), (ids, ch, "ids"), (slots, ch, "slots"), (weights, ch, "weights"), (y, tok, "y"))
-    _check(load().moe_combine(ctypes.byref(layout), _ptr(ye, dt, "ye"), _ptr(ids, torch.int32, "ids"),
-                              _ptr(slots, torch.int32, "slots"), _ptr(weights, torch.float32, "weights"),
-                              _ptr(y, dt, "y"), _stream(stream)))
+    _check(load().moe_combine(ctypes.byref(layout), _ptr(ye, dt, "ye", exp), _ptr(ids, torch.int32, "ids", ch),
+                              _ptr(slots, torch.int32, "slots", ch), _ptr(weights, torch.float32, "weights", ch),
+                              _ptr(y, dt, "y", tok), _stream(stream)))
 
 
 def moe_dispatch_bwd(layout, dxe, ids, slots, dx, stream=None):
     dt = torch.bfloat16 if layout.dtype == MOE_BF16 else torch.float32
     tok, exp, ch, _ = _rows(layout)
-    _need((dxe, exp, "dxe"), (ids, ch, "ids"), (slots, ch, "slots"), (dx, tok, "dx"))
-    _check(load().moe_dispatch_bwd(ctypes.byref(layout), _ptr(dxe, dt, "dxe"), _ptr(ids, torch.int32, "ids"),
-                                   _ptr(slots, torch.int32, "slots"), _ptr(dx, dt, "dx"), _stream(stream)))
+    _check(load().moe_dispatch_bwd(ctypes.byref(layout), _ptr(dxe, dt, "dxe", exp),
+                                   _ptr(ids, torch.int32, "ids", ch), _ptr(slots, torch.int32, "slots", ch),
+                                   _ptr(dx, dt, "dx", tok), _stream(stream)))
 
 
 def moe_combine_bwd(layout, dy, ye, ids, slots, slot_src, weights, dye, dw, stream=None):
     dt = torch.bfloat16 if layout.dtype == MOE_BF16 else torch.float32
     i32 = torch.int32
     tok, exp, ch, src = _rows(layout)
-    _need((dy, tok, "dy"), (ye, exp, "ye"), (ids, ch, "ids"), (slots, ch, "slots"), (slot_src, src, "slot_src"),
-          (weights, ch, "weights"), (dye, exp, "dye"), (dw, ch, "dw"))
-    _check(load().moe_combine_bwd(ctypes.byref(layout), _ptr(dy, dt, "dy"), _ptr(ye, dt, "ye"), _ptr(ids, i32, "ids"),
-                                  _ptr(slots, i32, "slots"), _ptr(slot_src, i32, "slot_src"),
-                                  _ptr(weights, torch.float32, "weights"), _ptr(dye, dt, "dye"),
-                                  _ptr(dw, torch.float32, "dw"), _stream(stream)))
+    _check(load().moe_combine_bwd(ctypes.byref(layout), _ptr(dy, dt, "dy", tok), _ptr(ye, dt, "ye", exp),
+                                  _ptr(ids, i32, "ids", ch), _ptr(slots, i32, "slots", ch),
+                                  _ptr(slot_src, i32, "slot_src", src), _ptr(weights, torch.float32, "weights", ch),
+                                  _ptr(dye, dt, "dye", exp), _ptr(dw, torch.float32, "dw", ch), _stream(stream)))
 
 
 # ---------------------------------------------------------------- convenience wrappers
@@ -307,15 +302,12 @@ def moe_base_gate(params, x, wg, bias, logits, ids, slots, weights, counts, slot
     f32, i32 = torch.float32, torch.int32
     xdt = torch.bfloat16 if params.dtype == MOE_BF16 else torch.float32
     S, d, E, C = params.S, params.d, params.E, params.capacity
-    _need((x, S * d, "x"), (wg, d * E, "wg"), (bias, E, "bias"), (logits, S * E, "logits"), (ids, S, "ids"),
-          (slots, S, "slots"), (weights, S, "weights"), (counts, E, "counts"), (slot_src, E * C, "slot_src"),
-          (prices, E, "prices"))
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(lib.moe_base_gate(
-        ctypes.byref(params), _ptr(x, xdt, "x"), _ptr(wg, xdt, "wg"), _ptr(bias, f32, "bias"),
-        _ptr(logits, f32, "logits"), _ptr(ids, i32, "ids"), _ptr(slots, i32, "slots"),
-        _ptr(weights, f32, "weights"), _ptr(counts, i32, "counts"), _ptr(slot_src, i32, "slot_src"),
-        _ptr(prices, torch.float64, "prices"), _ptr(workspace, None, "workspace"), ws_bytes,
+        ctypes.byref(params), _ptr(x, xdt, "x", S * d), _ptr(wg, xdt, "wg", d * E), _ptr(bias, f32, "bias", E),
+        _ptr(logits, f32, "logits", S * E), _ptr(ids, i32, "ids", S), _ptr(slots, i32, "slots", S),
+        _ptr(weights, f32, "weights", S), _ptr(counts, i32, "counts", E), _ptr(slot_src, i32, "slot_src", E * C),
+        _ptr(prices, torch.float64, "prices", E), _ptr(workspace, None, "workspace"), ws_bytes,
         None if info is None else ctypes.byref(info),
         _stream(stream)))
 
@@ -402,15 +394,13 @@ def moe_gate_bwd(params, x, wg, logits, ids, dw, dlogits, dx, dwg, dbias, aux_lo
     dt = torch.bfloat16 if params.dtype == MOE_BF16 else torch.float32
     f32, i32 = torch.float32, torch.int32
     S, d, E, k = params.S, params.d, params.E, params.k
-    _need((x, S * d, "x"), (wg, d * E, "wg"), (logits, S * E, "logits"), (ids, S * k, "ids"), (dw, S * k, "dw"),
-          (dlogits, S * E, "dlogits"), (dx, S * d, "dx"), (dwg, d * E, "dwg"), (dbias, E, "dbias"),
-          (aux_loss, 1, "aux_loss"))
     ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
-    _check(load().moe_gate_bwd(ctypes.byref(params), _ptr(x, dt, "x"), _ptr(wg, dt, "wg"),
-                               _ptr(logits, f32, "logits"), _ptr(ids, i32, "ids"), _ptr(dw, f32, "dw"),
-                               _ptr(dlogits, f32, "dlogits"), _ptr(dx, dt, "dx"), _ptr(dwg, f32, "dwg"),
-                               _ptr(dbias, f32, "dbias"), _ptr(aux_loss, f32, "aux_loss"),
-                               _ptr(workspace, None, "workspace"), ws_bytes, _stream(stream)))
+    _check(load().moe_gate_bwd(ctypes.byref(params), _ptr(x, dt, "x", S * d), _ptr(wg, dt, "wg", d * E),
+                               _ptr(logits, f32, "logits", S * E), _ptr(ids, i32, "ids", S * k),
+                               _ptr(dw, f32, "dw", S * k), _ptr(dlogits, f32, "dlogits", S * E),
+                               _ptr(dx, dt, "dx", S * d), _ptr(dwg, f32, "dwg", d * E), _ptr(dbias, f32, "dbias", E),
+                               _ptr(aux_loss, f32, "aux_loss", 1), _ptr(workspace, None, "workspace"), ws_bytes,
+                               _stream(stream)))
 
 
 def gate_bwd(kind, logits, ids, dw, *, x=None, wg=None, normalize=0, dx=None, accumulate_dx=False,

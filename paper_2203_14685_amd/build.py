@@ -46,6 +46,12 @@ def build(verbose=True):
     t0 = time.time()
     objdir = os.path.join(PKG, "_build")
     os.makedirs(objdir, exist_ok=True)
+    # objects of sources no longer built would otherwise sit beside the current
+    # ones, and a link that globs the folder could pick up their kernels
+    current = {src.replace(".hip", ".o") for src in SOURCES}
+    for name in os.listdir(objdir):
+        if name.endswith(".o") and name not in current:
+            os.remove(os.path.join(objdir, name))
     jobs = []
     for src in SOURCES:
         obj = os.path.join(objdir, src.replace(".hip", ".o"))

@@ -8,7 +8,8 @@
 //           softmax weights, and for every 64-token "wave block" a histogram of
 //           its (rank, expert) pairs.  Five variants:
 //             route_mfma_rs_kernel  bf16, W held in registers (E up to 128,
-//                                d 512..2048): persistent, projection on
+//                                d 512..2048, d * E up to 128 K):
+//                                persistent, projection on
 //                                v_mfma_f32_16x16x32_bf16;
 //             route_mfma_ph_kernel  bf16, E in {16, 32, 64, 128}, d a multiple
 //                                of 512: persistent, W^T staged in LDS per

@@ -2,18 +2,25 @@
 // of Eq. 1 with softmax and expert selection (Sec. 3.1 top-k / kTop1), for
 // shapes whose W fits in the register file of one CU.
 //
-// Persistent blocks of 8 waves, one per CU.  Wave w owns the K slice
-// [w*KSL, (w+1)*KSL) of d = 8*KSL and keeps the B fragments of W^T for that
-// slice (all E = 16*NT experts) in registers for the whole kernel, so W is read
-// once per CU.  The block then streams 16-token tiles of x: each wave loads the
-// tile's columns of its slice (one tile ahead), runs KSL/32 x NT
-// v_mfma_f32_16x16x32_bf16, and the 8 partial 16 x E tiles are summed in a
-// fixed order through LDS.  K step ks of wave w covers the columns
-// [w*KSL + 32ks, +32) and lane group g = lane/16 the 8 at w*KSL + 32ks + 8g, so
-// the 4 lanes of a row load 64 contiguous bytes per instruction.
-// After four tiles (one 64-token wave block) the block selects with 8 lanes
-// per token (each lane streams E/8 experts, then a butterfly merge) and writes
-// the wave block's (rank, expert) histogram.
+// Persistent blocks of WAVES waves, one block per CU.  Wave w owns the K slice
+// [w*KSL, (w+1)*KSL) of d = WAVES*KSL and keeps the B fragments of W^T for
+// that slice (all E = 16*NT experts) in registers for the whole kernel, so W
+// is read once per CU.  Eight waves (two per SIMD) serve W up to 64 K
+// elements; four waves (one per SIMD, up to 512 registers each) serve up to
+// 128 K.  Column n of N tile nt holds expert n*NT + nt, so a lane's NT experts
+// are adjacent in a row of W and each K row of its fragments is one load.
+// The block then streams 16-token tiles of x: each wave loads the tile's
+// columns of its slice into one of two buffers while the other is multiplied
+// (KSL/32 x NT v_mfma_f32_16x16x32_bf16), and the partial 16 x E tiles are
+// summed in a fixed order through LDS.  K step ks of wave w covers the columns
+// [w*KSL + 32ks, +32) and lane group g = lane/16 the 8 at w*KSL + 32ks + 8g,
+// so the 4 lanes of a row load 64 contiguous bytes per instruction.  The loads
+// are unconditional (rows past the batch read its last row, results unused):
+// a branch around them, or a register copy of a loaded value, would make the
+// products wait for every load in flight.  After four tiles (one 64-token wave
+// block) the block selects with WAVES lanes per token (each lane streams
+// E/WAVES experts, then a butterfly merge) and writes the wave block's
+// (rank, expert) histogram.
 #include "select.hpp"
 
 namespace hetumoe {
@@ -21,17 +28,37 @@ namespace hetumoe {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kRsWaves = 8;
-constexpr int kRsThreads = kRsWaves * kWave;
 constexpr int kGroupTokens = 64;  // one wave block
 constexpr int kTileTokens = 16;   // MFMA M
 
-template <int NT, int KSL, int KMAX, bool KTOP1>
-__global__ __launch_bounds__(kRsThreads) void route_mfma_rs_kernel(RouteArgs a) {
+// NT adjacent bf16 of one row of W (one load of NT * 2 bytes), as half-words.
+template <int NT>
+__device__ __forceinline__ void load_wrow(const uint16_t* p, uint16_t (&out)[NT]) {
+  if constexpr (NT == 1) {
+    out[0] = *p;
+  } else if constexpr (NT == 2) {
+    const uint32_t v = *reinterpret_cast<const uint32_t*>(p);
+    out[0] = static_cast<uint16_t>(v); out[1] = static_cast<uint16_t>(v >> 16);
+  } else if constexpr (NT == 4) {
+    const uint2 v = *reinterpret_cast<const uint2*>(p);
+    out[0] = static_cast<uint16_t>(v.x); out[1] = static_cast<uint16_t>(v.x >> 16);
+    out[2] = static_cast<uint16_t>(v.y); out[3] = static_cast<uint16_t>(v.y >> 16);
+  } else {
+    static_assert(NT == 8, "NT in {1, 2, 4, 8}");
+    const u32x4 v = *reinterpret_cast<const u32x4*>(p);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) { out[2 * i] = static_cast<uint16_t>(v[i]); out[2 * i + 1] = static_cast<uint16_t>(v[i] >> 16); }
+  }
+}
+
+template <int WAVES, int NT, int KSL, int KMAX, bool KTOP1>
+__global__ __launch_bounds__(WAVES * 64) void route_mfma_rs_kernel(RouteArgs a) {
+  constexpr int kThreads = WAVES * kWave;
   constexpr int E = NT * 16;
   constexpr int KSTEPS = KSL / 32;  // MFMA K steps per tile per wave
-  static_assert(KSTEPS * NT <= 16, "W^T fragments must fit the register budget");
-  __shared__ float part[kRsWaves * kTileTokens * E];   // per-wave partial logits of one tile
+  constexpr int P = kThreads / kGroupTokens;  // selection lanes per token
+  static_assert(KSTEPS * NT <= (WAVES == 8 ? 16 : 64), "W^T fragments must fit the register budget");
+  __shared__ float part[WAVES * kTileTokens * E];      // per-wave partial logits of one tile
   __shared__ float lg[kGroupTokens * (E + 1)];         // logits (+ bias) of the current wave block
   __shared__ int hist_lds[8 * E];                      // [k][E], k <= 8
 
@@ -44,18 +71,19 @@ __global__ __launch_bounds__(kRsThreads) void route_mfma_rs_kernel(RouteArgs a) 
   const uint16_t* wg = reinterpret_cast<const uint16_t*>(a.wg);
   const uint16_t* x = reinterpret_cast<const uint16_t*>(a.x);
 
-  // W^T fragments of this lane: column m of each N tile, 8 consecutive columns
-  // of the slice per K step
+  // W^T fragments of this lane: experts m*NT + nt, 8 consecutive K rows of
+  // the slice per K step (one load per row, all issued before the packing)
   u32x4 bfr[KSTEPS][NT];
 #pragma unroll
   for (int ks = 0; ks < KSTEPS; ++ks) {
+    uint16_t r[8][NT];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) load_wrow<NT>(wg + static_cast<int64_t>(kbase + 32 * ks + j) * E + m * NT, r[j]);
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
-      const uint16_t* col = wg + static_cast<int64_t>(kbase + 32 * ks) * E + nt * 16 + m;
       uint32_t p[4];
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
-        p[q] = static_cast<uint32_t>(col[(2 * q) * E]) | (static_cast<uint32_t>(col[(2 * q + 1) * E]) << 16);
+      for (int q = 0; q < 4; ++q) p[q] = static_cast<uint32_t>(r[2 * q][nt]) | (static_cast<uint32_t>(r[2 * q + 1][nt]) << 16);
       bfr[ks][nt] = u32x4{p[0], p[1], p[2], p[3]};
     }
   }
@@ -64,120 +92,124 @@ __global__ __launch_bounds__(kRsThreads) void route_mfma_rs_kernel(RouteArgs a) 
   const int nb = a.nb;
   const int my_groups = (nb - static_cast<int>(blockIdx.x) + static_cast<int>(gridDim.x) - 1) / static_cast<int>(gridDim.x);
   const int ntiles = 4 * my_groups;
-  const u32x4 zero = {0u, 0u, 0u, 0u};
-  auto tile_row = [&](int q) -> int64_t {
+  // the block's threads reduce expert tid % E of every row (kThreads is a
+  // multiple of E); its bias is read once, not behind the x loads in flight
+  const float bias_e = a.bias ? a.bias[tid % E] : 0.f;
+  auto load_tile = [&](u32x4 (&buf)[KSTEPS], int q) {
+    // rows past the batch, and the tile after the block's last, read the last
+    // row of the batch: no branch around the loads, results never used
     const int64_t grp = blockIdx.x + static_cast<int64_t>(q / 4) * gridDim.x;
-    return grp * kGroupTokens + (q % 4) * kTileTokens + m;
-  };
-  u32x4 xcur[KSTEPS], xnxt[KSTEPS];
-  {
-    const int64_t row = tile_row(0);
+    int64_t row = grp * kGroupTokens + (q % 4) * kTileTokens + m;
+    row = row < a.S ? row : a.S - 1;
     const u32x4* src = reinterpret_cast<const u32x4*>(x + row * d + kbase);
 #pragma unroll
-    for (int v = 0; v < KSTEPS; ++v) xcur[v] = (ntiles > 0 && row < a.S) ? src[4 * v] : zero;
-  }
-
-  for (int q = 0; q < ntiles; ++q) {
+    for (int v = 0; v < KSTEPS; ++v) buf[v] = src[4 * v];
+    __builtin_amdgcn_sched_barrier(0);  // the loads stay ahead of the products that follow
+  };
+  auto run_tile = [&](const u32x4 (&xt)[KSTEPS], int q) {
     const int t = q % 4;
     const int64_t grp = blockIdx.x + static_cast<int64_t>(q / 4) * gridDim.x;
     const int64_t tok0 = grp * kGroupTokens;
     if (t == 0)
-      for (int i = tid; i < a.k * E; i += kRsThreads) hist_lds[i] = 0;
-    // prefetch the next tile
-    {
-      const int64_t row = tile_row(q + 1);
-      const u32x4* src = reinterpret_cast<const u32x4*>(x + row * d + kbase);
-      const bool ok = q + 1 < ntiles && row < a.S;
-#pragma unroll
-      for (int v = 0; v < KSTEPS; ++v) xnxt[v] = ok ? src[4 * v] : zero;
-    }
+      for (int i = tid; i < a.k * E; i += kThreads) hist_lds[i] = 0;
     f32x4 acc[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int ks = 0; ks < KSTEPS; ++ks) {
-      const bf16x8 av = __builtin_bit_cast(bf16x8, xcur[ks]);
+      const bf16x8 av = __builtin_bit_cast(bf16x8, xt[ks]);
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt)
         acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf16x8, bfr[ks][nt]), acc[nt], 0, 0, 0);
     }
-    // partial tile of this wave: lane holds rows 4g+i, column m of each N tile
+    // partial tile of this wave: lane holds rows 4g+i, experts m*NT + nt
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) part[(w * kTileTokens + 4 * g + i) * E + nt * 16 + m] = acc[nt][i];
+      for (int i = 0; i < 4; ++i) part[(w * kTileTokens + 4 * g + i) * E + m * NT + nt] = acc[nt][i];
     __syncthreads();
-    for (int o = tid; o < kTileTokens * E; o += kRsThreads) {
+    for (int o = tid; o < kTileTokens * E; o += kThreads) {
       const int r = o / E, e = o % E;
-      float sum = a.bias ? a.bias[e] : 0.f;
+      float sum = bias_e;
 #pragma unroll
-      for (int v = 0; v < kRsWaves; ++v) sum += part[(v * kTileTokens + r) * E + e];
+      for (int v = 0; v < WAVES; ++v) sum += part[(v * kTileTokens + r) * E + e];
       lg[(t * kTileTokens + r) * (E + 1) + e] = sum;
     }
     __syncthreads();
-#pragma unroll
-    for (int v = 0; v < KSTEPS; ++v) xcur[v] = xnxt[v];
-    if (t != 3) continue;
+    if (t != 3) return;
 
     // ------------------------------------------------ wave block complete
     if (a.logits) {
-      for (int o = tid; o < kGroupTokens * E; o += kRsThreads) {
+      for (int o = tid; o < kGroupTokens * E; o += kThreads) {
         const int r = o / E, e = o % E;
         if (tok0 + r < a.S) a.logits[(tok0 + r) * E + e] = lg[r * (E + 1) + e];
       }
     }
-    const int tt = tid / 8, j = tid % 8;  // token of the wave block, lane within its 8
+    const int tt = tid / P, j = tid % P;  // token of the wave block, lane within its P
     const int64_t s = tok0 + tt;
     const bool valid = s < a.S;
-    select_token<8, KMAX, KTOP1>(&lg[tt * (E + 1)], E, a.k, a.normalize, j, valid, a.ids + s * a.k,
+    select_token<P, KMAX, KTOP1>(&lg[tt * (E + 1)], E, a.k, a.normalize, j, valid, a.ids + s * a.k,
                                  a.weights + s * a.k, hist_lds);
     __syncthreads();
-    for (int i = tid; i < a.k * E; i += kRsThreads) {
+    for (int i = tid; i < a.k * E; i += kThreads) {
       const int r = i / E, e = i % E;
       a.hist[(static_cast<int64_t>(r) * E + e) * nb + grp] = hist_lds[i];
     }
     __syncthreads();  // lg and hist_lds are reused by the next wave block
+  };
+
+  // two tile buffers in turn (the tile count is a multiple of 4): the next
+  // tile's loads are in flight while the current one is multiplied
+  u32x4 xa[KSTEPS], xb[KSTEPS];
+  load_tile(xa, 0);
+  for (int q = 0; q < ntiles; q += 2) {
+    load_tile(xb, q + 1);
+    run_tile(xa, q);
+    load_tile(xa, q + 2);
+    run_tile(xb, q + 1);
   }
 }
 
 // ---------------------------------------------------------------- launch
-template <int NT, int KSL, int KMAX, bool KTOP1>
+template <int WAVES, int NT, int KSL, int KMAX, bool KTOP1>
 static hipError_t launch_rs_t(const RouteArgs& a, int grid, hipStream_t st) {
-  route_mfma_rs_kernel<NT, KSL, KMAX, KTOP1><<<dim3(grid), dim3(kRsThreads), 0, st>>>(a);
+  route_mfma_rs_kernel<WAVES, NT, KSL, KMAX, KTOP1><<<dim3(grid), dim3(WAVES * kWave), 0, st>>>(a);
   return hipGetLastError();
 }
 
-template <int NT, int KSL>
+template <int WAVES, int NT, int KSL>
 static hipError_t launch_rs_nt(const RouteArgs& a, int grid, hipStream_t st) {
-  if (a.kind == 1) return launch_rs_t<NT, KSL, 1, true>(a, grid, st);
-  if (a.k == 1) return launch_rs_t<NT, KSL, 1, false>(a, grid, st);
-  if (a.k == 2) return launch_rs_t<NT, KSL, 2, false>(a, grid, st);
-  return launch_rs_t<NT, KSL, 8, false>(a, grid, st);
+  if (a.kind == 1) return launch_rs_t<WAVES, NT, KSL, 1, true>(a, grid, st);
+  if (a.k == 1) return launch_rs_t<WAVES, NT, KSL, 1, false>(a, grid, st);
+  if (a.k == 2) return launch_rs_t<WAVES, NT, KSL, 2, false>(a, grid, st);
+  return launch_rs_t<WAVES, NT, KSL, 8, false>(a, grid, st);
 }
 
-// Shapes served: bf16, E in {16, 32, 64, 128}, d in {512, 1024, 2048}, with the
-// W^T fragments of a slice within 64 registers (d * E <= 65536); larger W spill.
+// Shapes served: bf16, E in {16, 32, 64, 128}, d in {512, 1024, 2048}, with
+// d * E <= 131072 (eight waves up to 65536, four beyond).
 bool route_uses_mfma_rs(const RouteArgs& a) {
   if (a.kind == 2 || a.logits_in || a.dtype != 1) return false;
   if (a.E != 16 && a.E != 32 && a.E != 64 && a.E != 128) return false;
   if (a.d != 512 && a.d != 1024 && a.d != 2048) return false;
-  if (static_cast<int64_t>(a.d) * a.E > 65536) return false;
-  return (reinterpret_cast<uintptr_t>(a.x) % 16) == 0;
+  if (static_cast<int64_t>(a.d) * a.E > 131072) return false;
+  return (reinterpret_cast<uintptr_t>(a.x) % 16) == 0 && (reinterpret_cast<uintptr_t>(a.wg) % 16) == 0;
 }
 
 hipError_t launch_route_mfma_rs(const RouteArgs& a, int cus, hipStream_t st) {
   const int grid = a.nb < cus ? a.nb : cus;
   const int key = a.E * 10000 + a.d;
   switch (key) {
-    case 16 * 10000 + 512: return launch_rs_nt<1, 64>(a, grid, st);
-    case 16 * 10000 + 1024: return launch_rs_nt<1, 128>(a, grid, st);
-    case 16 * 10000 + 2048: return launch_rs_nt<1, 256>(a, grid, st);
-    case 32 * 10000 + 512: return launch_rs_nt<2, 64>(a, grid, st);
-    case 32 * 10000 + 1024: return launch_rs_nt<2, 128>(a, grid, st);
-    case 32 * 10000 + 2048: return launch_rs_nt<2, 256>(a, grid, st);
-    case 64 * 10000 + 512: return launch_rs_nt<4, 64>(a, grid, st);
-    case 64 * 10000 + 1024: return launch_rs_nt<4, 128>(a, grid, st);
-    case 128 * 10000 + 512: return launch_rs_nt<8, 64>(a, grid, st);
+    case 16 * 10000 + 512: return launch_rs_nt<8, 1, 64>(a, grid, st);
+    case 16 * 10000 + 1024: return launch_rs_nt<8, 1, 128>(a, grid, st);
+    case 16 * 10000 + 2048: return launch_rs_nt<8, 1, 256>(a, grid, st);
+    case 32 * 10000 + 512: return launch_rs_nt<8, 2, 64>(a, grid, st);
+    case 32 * 10000 + 1024: return launch_rs_nt<8, 2, 128>(a, grid, st);
+    case 32 * 10000 + 2048: return launch_rs_nt<4, 2, 512>(a, grid, st);
+    case 64 * 10000 + 512: return launch_rs_nt<8, 4, 64>(a, grid, st);
+    case 64 * 10000 + 1024: return launch_rs_nt<8, 4, 128>(a, grid, st);
+    case 64 * 10000 + 2048: return launch_rs_nt<4, 4, 512>(a, grid, st);
+    case 128 * 10000 + 512: return launch_rs_nt<8, 8, 64>(a, grid, st);
+    case 128 * 10000 + 1024: return launch_rs_nt<4, 8, 256>(a, grid, st);
     default: return hipErrorInvalidValue;
   }
 }

@@ -331,34 +331,51 @@ def test_base_pointer_checks(lib):
     assert call(pl, logits=A16) == b.MOE_ERR_INVALID_ARG               # ... and no x / wg
 
 
-def test_binding_rejects_short_buffers():
-    """A tensor smaller than the call's sizes is refused before any device work
-    (checked here on CPU tensors: the size check comes first)."""
+# (call, argument names after the params struct, elements each needs) at
+# S=100, d=64, E=8, k=2, C=30 (hash_vocab=5 for the gate; BASE: S=96, C=12)
+_S, _d, _E, _k, _C = 100, 64, 8, 2, 30
+_SIZES = {
+    "moe_gate": (["x", "wg", "bias", "token_ids", "noise", "hash_table", "logits", "ids", "slots", "weights",
+                  "counts", "demand", "slot_src", "workspace"],
+                 [_S * _d, _d * _E, _E, _S, _S * _E, 5, _S * _E, _S * _k, _S * _k, _S * _k, _E, _E, _E * _C, 0]),
+    "moe_dispatch": (["x", "ids", "slots", "slot_src", "xe"], [_S * _d, _S * _k, _S * _k, _E * _C, _E * _C * _d]),
+    "moe_combine": (["ye", "ids", "slots", "weights", "y"], [_E * _C * _d, _S * _k, _S * _k, _S * _k, _S * _d]),
+    "moe_dispatch_bwd": (["dxe", "ids", "slots", "dx"], [_E * _C * _d, _S * _k, _S * _k, _S * _d]),
+    "moe_combine_bwd": (["dy", "ye", "ids", "slots", "slot_src", "weights", "dye", "dw"],
+                        [_S * _d, _E * _C * _d, _S * _k, _S * _k, _E * _C, _S * _k, _E * _C * _d, _S * _k]),
+    "moe_gate_bwd": (["x", "wg", "logits", "ids", "dw", "dlogits", "dx", "dwg", "dbias", "aux_loss", "workspace"],
+                     [_S * _d, _d * _E, _S * _E, _S * _k, _S * _k, _S * _E, _S * _d, _d * _E, _E, 1, 0]),
+    "moe_base_gate": (["x", "wg", "bias", "logits", "ids", "slots", "weights", "counts", "slot_src", "prices",
+                       "workspace"], [96 * _d, _d * _E, _E, 96 * _E, 96, 96, 96, _E, _E * 12, _E, 0]),
+}
+
+
+def _params(call):
+    if call == "moe_gate":
+        return b.gate_params(_S, _d, _E, _k, _C, b.MOE_GATE_TOPK, hash_vocab=5)
+    if call == "moe_gate_bwd":
+        return b.gate_bwd_params(_S, _d, _E, _k, b.MOE_GATE_TOPK)
+    if call == "moe_base_gate":
+        return b.base_params(96, _d, _E, 12)
+    return b.Layout(_S, _d, _E, _k, _C, b.MOE_F32)
+
+
+@pytest.mark.parametrize("call", sorted(_SIZES))
+def test_binding_rejects_short_buffers(call):
+    """Every tensor argument of every call: one element short of the call's
+    sizes is refused before any device work (the other arguments are None, so
+    the check runs on a CPU tensor here); the right size passes the size check
+    and is then refused for being on the CPU."""
     import torch
-    i32 = torch.int32
-    lay = b.Layout(100, 64, 8, 2, 30, b.MOE_F32)
-    x = torch.zeros(100 * 64)
-    xe_short = torch.zeros(8 * 30 * 64 - 1)
-    ch = torch.zeros(200, dtype=i32)
-    src = torch.zeros(8 * 30, dtype=i32)
-    with pytest.raises(ValueError, match="xe holds"):
-        b.moe_dispatch(lay, x, ch, ch, src, xe_short)
-    with pytest.raises(ValueError, match="slots holds"):
-        b.moe_combine(lay, torch.zeros(8 * 30 * 64), ch, ch[:199], torch.zeros(200), torch.zeros(100 * 64))
-    with pytest.raises(ValueError, match="dw holds"):
-        b.moe_combine_bwd(lay, x, torch.zeros(8 * 30 * 64), ch, ch, src, torch.zeros(200), torch.zeros(8 * 30 * 64),
-                          torch.zeros(199))
-    with pytest.raises(ValueError, match="dx holds"):
-        b.moe_dispatch_bwd(lay, torch.zeros(8 * 30 * 64), ch, ch, torch.zeros(100 * 64 - 64))
-    p = b.gate_params(100, 64, 8, 2, 30, b.MOE_GATE_TOPK)
-    with pytest.raises(ValueError, match="slot_src holds"):
-        b.moe_gate(p, x, torch.zeros(64 * 8), None, None, None, None, None, ch, ch, torch.zeros(200),
-                   torch.zeros(8, dtype=i32), None, src[:-1], None)
-    pb = b.gate_bwd_params(100, 64, 8, 2, b.MOE_GATE_TOPK)
-    with pytest.raises(ValueError, match="logits holds"):
-        b.moe_gate_bwd(pb, None, None, torch.zeros(799), ch, torch.zeros(200), None, None, None, None, None, None)
-    pbase = b.base_params(96, 64, 8, 12)
-    with pytest.raises(ValueError, match="prices holds"):
-        b.moe_base_gate(pbase, torch.zeros(96 * 64), torch.zeros(64 * 8), None, None, torch.zeros(96, dtype=i32),
-                        torch.zeros(96, dtype=i32), torch.zeros(96), torch.zeros(8, dtype=i32),
-                        torch.zeros(96, dtype=i32), torch.zeros(7, dtype=torch.float64), None)
+    names, sizes = _SIZES[call]
+    fn = getattr(b, call)
+    for pos, (name, n) in enumerate(zip(names, sizes)):
+        if n == 0:
+            continue
+        args = [None] * len(names)
+        args[pos] = torch.zeros(n - 1)
+        with pytest.raises(ValueError, match=f"^{name} holds {n - 1} elements"):
+            fn(_params(call), *args)
+        args[pos] = torch.zeros(n)
+        with pytest.raises(ValueError, match=f"^{name} must be on the GPU"):
+            fn(_params(call), *args)

@@ -155,10 +155,15 @@ def test_split_projection_shapes(dtype, E, k, kind, normalize, d, bias, S):
     (80, 3, 0, 1, 256, False, 300), (96, 8, 0, 0, 128, True, 300), (112, 2, 0, 0, 384, False, 300),
     (128, 8, 1, 0, 256, True, 300), (128, 2, 0, 1, 384, False, 300), (48, 3, 1, 0, 256, False, 300),
     (64, 8, 1, 0, 256, True, 300), (128, 4, 1, 0, 384, False, 300), (80, 5, 1, 0, 256, False, 300),
-    # W held in registers (8 lanes per token select)
+    # W held in registers: eight waves up to d * E = 64 K (8 lanes per token select)
     (32, 2, 0, 1, 512, True, 300), (64, 4, 1, 0, 1024, True, 300), (128, 8, 0, 1, 512, False, 300),
     (16, 2, 0, 0, 2048, False, 300), (32, 8, 1, 0, 1024, True, 300), (64, 1, 0, 0, 512, False, 300),
     (64, 2, 0, 1, 512, True, 20000),
+    # ... four waves up to 128 K (4 lanes per token select); S = 20000 and 40000
+    # give blocks two and three wave blocks
+    (32, 2, 0, 1, 2048, True, 20000), (32, 8, 1, 0, 2048, False, 300), (64, 8, 0, 1, 2048, True, 300),
+    (64, 4, 1, 0, 2048, False, 40000), (64, 1, 0, 0, 2048, True, 77), (128, 3, 0, 0, 1024, True, 700),
+    (128, 8, 1, 0, 1024, False, 20000),
     # W^T staged per K phase (persistent, one block per CU); S = 40000 gives some
     # blocks three wave blocks, one of them without a partner
     (64, 2, 0, 1, 1536, True, 40000), (128, 1, 1, 0, 1024, False, 3000), (16, 4, 0, 1, 4096, True, 300),

@@ -515,14 +515,14 @@ def main():
         kh = min(k, E // G, 8)
         gp = hm.gate_params(S, d, E, kh, C, hm.MOE_GATE_HTOPK, w["normalize"], 0, dcode, 0, groups=G)
         ms = time_gate(gp, x=x, wg=wg, bias=bias)
-        b = ab["gate"] - S * k * 12 + S * kh * 12 + 2 * S * E * 4  # + logits written and read once
+        b = ab["gate"] - S * k * 12 + S * kh * 12  # the same bytes as the top-k gate, for kh choices
         gates["htopk"] = {"ms": round(ms, 5), "groups": G, "k": kh, "alg_bytes": b,
                           "GB/s": round(b / (ms * 1e-3) / 1e9, 1)}
         noise = torch.from_numpy(
             (-np.log(-np.log(np.random.default_rng(3).random((S, E))))).astype(np.float32)).to(dev)
         gp = hm.gate_params(S, d, E, k, C, w["kind"], w["normalize"], 0, dcode, 0, temperature=0.5)
         ms = time_gate(gp, x=x, wg=wg, bias=bias, noise=noise)
-        b = ab["gate"] + 3 * S * E * 4  # + noise read, logits written and read once
+        b = ab["gate"] + S * E * 4  # + the noise read
         gates["dense_to_sparse"] = {"ms": round(ms, 5), "temperature": 0.5, "alg_bytes": b,
                                     "GB/s": round(b / (ms * 1e-3) / 1e9, 1)}
         del noise

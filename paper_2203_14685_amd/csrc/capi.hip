@@ -408,7 +408,18 @@ moe_status moe_gate(const moe_gate_params* p, const void* x, const void* wg, con
   int32_t* hist = static_cast<int32_t*>(workspace);
   hipError_t err;
 
-  if (gate_extended(p)) {
+  RouteArgs fused{};
+  fused.S = p->S; fused.d = p->d; fused.E = p->E; fused.k = p->k; fused.nb = nb;
+  fused.kind = p->kind; fused.normalize = p->normalize; fused.logits_in = 0; fused.dtype = p->dtype;
+  fused.x = x; fused.wg = wg; fused.bias = bias; fused.logits = logits;
+  fused.ids = ids; fused.weights = weights; fused.hist = hist;
+  fused.groups = p->groups; fused.temperature = p->temperature; fused.noise = noise;
+  if (gate_extended(p) && !p->logits_in && route_fuses_extended(fused)) {
+    // projection, noise, temperature and selection in one kernel: the final
+    // logits never leave it unless the caller asks for them
+    err = launch_route(fused, stream);
+    if (err != hipSuccess) return hip_fail(err, "moe_gate: route kernel launch");
+  } else if (gate_extended(p)) {
     // raw logits (projected into the workspace, or given), then noise,
     // temperature and selection in a kernel of their own
     float* wsl = reinterpret_cast<float*>(static_cast<char*>(workspace) +

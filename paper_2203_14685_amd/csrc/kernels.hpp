@@ -20,6 +20,12 @@ struct RouteArgs {
   int32_t* ids;             // [S, k]
   float* weights;           // [S, k]
   int32_t* hist;            // [k, E, nb] workspace (nb = 64-token wave blocks)
+  // the extended gates, for a route kernel that selects on final logits itself
+  // (route_fuses_extended): kind 3 is the hierarchical top-k over `groups`
+  // groups; temperature > 0 selects on (logits + noise) / temperature
+  int groups;
+  float temperature;
+  const float* noise;       // [S, E] or null
 };
 
 struct ScanArgs {
@@ -77,6 +83,10 @@ bool route_uses_mfma_ph(const RouteArgs& a);
 // Compute units of the current device (queried once per device).
 int device_cu_count();
 bool route_uses_mfma_rs(const RouteArgs& a);
+// True when the register-resident route kernel takes this projection: it then
+// also applies the noise and temperature and the hierarchical top-k itself, so
+// the extended gates need no logits round trip.
+bool route_fuses_extended(const RouteArgs& a);
 hipError_t launch_scan(const ScanArgs& a, hipStream_t st);
 hipError_t launch_assign(const AssignArgs& a, hipStream_t st);
 // Scan and assign, in one launch when the histogram is small (the offsets then

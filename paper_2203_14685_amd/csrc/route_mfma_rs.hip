@@ -20,7 +20,9 @@
 // products wait for every load in flight.  After four tiles (one 64-token wave
 // block) the block selects with WAVES lanes per token (each lane streams
 // E/WAVES experts, then a butterfly merge) and writes the wave block's
-// (rank, expert) histogram.
+// (rank, expert) histogram.  The extended gates select here too: Dense-To-Sparse
+// first turns the wave block's logits into (logits + noise) / temperature in
+// LDS, and the hierarchical top-k (MODE 3) runs its two-level selection.
 #include "select.hpp"
 
 namespace hetumoe {
@@ -51,7 +53,8 @@ __device__ __forceinline__ void load_wrow(const uint16_t* p, uint16_t (&out)[NT]
   }
 }
 
-template <int WAVES, int NT, int KSL, int KMAX, bool KTOP1>
+// MODE: 0 top-k, 1 kTop1, 3 hierarchical top-k
+template <int WAVES, int NT, int KSL, int KMAX, int MODE>
 __global__ __launch_bounds__(WAVES * 64) void route_mfma_rs_kernel(RouteArgs a) {
   constexpr int kThreads = WAVES * kWave;
   constexpr int E = NT * 16;
@@ -139,6 +142,18 @@ __global__ __launch_bounds__(WAVES * 64) void route_mfma_rs_kernel(RouteArgs a) 
     if (t != 3) return;
 
     // ------------------------------------------------ wave block complete
+    if (a.temperature > 0.f) {
+      // final logits of Dense-To-Sparse, in fp32 as the selection sees them
+      for (int o = tid; o < kGroupTokens * E; o += kThreads) {
+        const int r = o / E, e = o % E;
+        if (tok0 + r < a.S) {
+          float v = lg[r * (E + 1) + e];
+          if (a.noise) v += a.noise[(tok0 + r) * E + e];
+          lg[r * (E + 1) + e] = v / a.temperature;
+        }
+      }
+      __syncthreads();
+    }
     if (a.logits) {
       for (int o = tid; o < kGroupTokens * E; o += kThreads) {
         const int r = o / E, e = o % E;
@@ -148,8 +163,12 @@ __global__ __launch_bounds__(WAVES * 64) void route_mfma_rs_kernel(RouteArgs a) 
     const int tt = tid / P, j = tid % P;  // token of the wave block, lane within its P
     const int64_t s = tok0 + tt;
     const bool valid = s < a.S;
-    select_token<P, KMAX, KTOP1>(&lg[tt * (E + 1)], E, a.k, a.normalize, j, valid, a.ids + s * a.k,
-                                 a.weights + s * a.k, hist_lds);
+    if constexpr (MODE == 3)
+      select_token_htopk<P, KMAX>(&lg[tt * (E + 1)], E, a.k, E / a.groups, a.normalize, j, valid, a.ids + s * a.k,
+                                  a.weights + s * a.k, hist_lds);
+    else
+      select_token<P, KMAX, MODE == 1>(&lg[tt * (E + 1)], E, a.k, a.normalize, j, valid, a.ids + s * a.k,
+                                       a.weights + s * a.k, hist_lds);
     __syncthreads();
     for (int i = tid; i < a.k * E; i += kThreads) {
       const int r = i / E, e = i % E;
@@ -171,18 +190,26 @@ __global__ __launch_bounds__(WAVES * 64) void route_mfma_rs_kernel(RouteArgs a) 
 }
 
 // ---------------------------------------------------------------- launch
-template <int WAVES, int NT, int KSL, int KMAX, bool KTOP1>
+template <int WAVES, int NT, int KSL, int KMAX, int MODE>
 static hipError_t launch_rs_t(const RouteArgs& a, int grid, hipStream_t st) {
-  route_mfma_rs_kernel<WAVES, NT, KSL, KMAX, KTOP1><<<dim3(grid), dim3(WAVES * kWave), 0, st>>>(a);
+  route_mfma_rs_kernel<WAVES, NT, KSL, KMAX, MODE><<<dim3(grid), dim3(WAVES * kWave), 0, st>>>(a);
   return hipGetLastError();
 }
 
 template <int WAVES, int NT, int KSL>
 static hipError_t launch_rs_nt(const RouteArgs& a, int grid, hipStream_t st) {
-  if (a.kind == 1) return launch_rs_t<WAVES, NT, KSL, 1, true>(a, grid, st);
-  if (a.k == 1) return launch_rs_t<WAVES, NT, KSL, 1, false>(a, grid, st);
-  if (a.k == 2) return launch_rs_t<WAVES, NT, KSL, 2, false>(a, grid, st);
-  return launch_rs_t<WAVES, NT, KSL, 8, false>(a, grid, st);
+  if (a.kind == 1) return launch_rs_t<WAVES, NT, KSL, 1, 1>(a, grid, st);
+  // sorted lists no longer than k needs: each logit's insertion walks all of them
+  if (a.kind == 3) {
+    if (a.k == 1) return launch_rs_t<WAVES, NT, KSL, 1, 3>(a, grid, st);
+    if (a.k == 2) return launch_rs_t<WAVES, NT, KSL, 2, 3>(a, grid, st);
+    if (a.k <= 4) return launch_rs_t<WAVES, NT, KSL, 4, 3>(a, grid, st);
+    return launch_rs_t<WAVES, NT, KSL, 8, 3>(a, grid, st);
+  }
+  if (a.k == 1) return launch_rs_t<WAVES, NT, KSL, 1, 0>(a, grid, st);
+  if (a.k == 2) return launch_rs_t<WAVES, NT, KSL, 2, 0>(a, grid, st);
+  if (a.k <= 4) return launch_rs_t<WAVES, NT, KSL, 4, 0>(a, grid, st);
+  return launch_rs_t<WAVES, NT, KSL, 8, 0>(a, grid, st);
 }
 
 // Shapes served: bf16, E in {16, 32, 64, 128}, d in {512, 1024, 2048}, with
@@ -194,6 +221,8 @@ bool route_uses_mfma_rs(const RouteArgs& a) {
   if (static_cast<int64_t>(a.d) * a.E > 131072) return false;
   return (reinterpret_cast<uintptr_t>(a.x) % 16) == 0 && (reinterpret_cast<uintptr_t>(a.wg) % 16) == 0;
 }
+
+bool route_fuses_extended(const RouteArgs& a) { return route_uses_mfma_rs(a); }
 
 hipError_t launch_route_mfma_rs(const RouteArgs& a, int cus, hipStream_t st) {
   const int grid = a.nb < cus ? a.nb : cus;

@@ -40,6 +40,9 @@ def gumbel(shape, seed):
     ("bf16", 1000, 2048, 64, 4, 2, 1, True), ("bf16", 700, 1024, 64, 8, 4, 0, False),
     ("f32", 517, 256, 16, 2, 3, 1, False), ("bf16", 300, 512, 48, 3, 8, 0, True),
     ("f32", 130, 132, 6, 3, 2, 1, False), ("bf16", 65, 256, 128, 16, 8, 1, False), ("f32", 64, 64, 12, 1, 4, 0, False),
+    # selection inside the register-resident projection (four waves)
+    ("bf16", 3000, 2048, 64, 4, 1, 0, True), ("bf16", 20000, 1024, 128, 8, 4, 1, False),
+    ("bf16", 333, 2048, 32, 2, 8, 0, True),
 ])
 def test_htopk_projection(dtype, S, d, E, groups, k, normalize, bias):
     announce(f"htopk dtype={dtype} S={S} d={d} E={E} groups={groups} k={k} normalize={normalize}")
@@ -81,6 +84,23 @@ def test_dense_to_sparse_projection(kind, k, normalize, groups, tau, dtype, E):
     g = gpu_gate(w, inp, E, k, C, kind, normalize, groups=groups, noise=noise, temperature=tau)
     _, st = check_gate(w, inp, g, E, k, C, kind, normalize, groups=groups, noise=noise, temperature=tau)
     print(f"[stats] dense-to-sparse kind={kind}: {st}", flush=True)
+
+
+@pytest.mark.parametrize("kind,k,normalize,groups,tau,E,d,S", [
+    (1, 4, 0, 0, 0.5, 64, 2048, 5000), (0, 1, 0, 0, 0.5, 64, 2048, 20000), (3, 2, 1, 4, 0.3, 128, 1024, 700),
+    (0, 8, 1, 0, 1.5, 32, 2048, 257),
+])
+def test_dense_to_sparse_register_kernel(kind, k, normalize, groups, tau, E, d, S):
+    """Shapes whose projection keeps W in registers (four waves): noise,
+    temperature and selection run in the projection kernel's epilogue."""
+    announce(f"dense-to-sparse in the projection kind={kind} k={k} tau={tau} E={E} d={d} S={S}")
+    w = dict(kind=kind, k=k, normalize=normalize, dtype="bf16", S=S, d=d, E=E, cf=1.25)
+    inp = wl.make_inputs(w, seed=5 + k + E)
+    noise = gumbel((S, E), 31 + k)
+    C = cap(1.25, k, S, E)
+    g = gpu_gate(w, inp, E, k, C, kind, normalize, groups=groups, noise=noise, temperature=tau)
+    _, st = check_gate(w, inp, g, E, k, C, kind, normalize, groups=groups, noise=noise, temperature=tau)
+    print(f"[stats] dense-to-sparse in the projection kind={kind} E={E}: {st}", flush=True)
 
 
 @pytest.mark.parametrize("kind,k,groups", [(0, 2, 0), (3, 3, 2), (1, 2, 0)])

@@ -19,7 +19,10 @@
 // Every output row is written with non-temporal stores: the buffers are far
 // larger than the 256 MB Infinity Cache, and plain stores leave dirty lines there
 // whose write-back then slows whichever kernel runs next (measured: dispatch
-// after a plain-store producer ~25% slower than after a streaming one).
+// after a plain-store producer ~25% slower than after a streaming one).  The
+// wave, short-row and token-major forms also read their source rows with
+// non-temporal loads (each row is read once; 2-7 % faster), the flat forms with
+// plain loads (1-2 % faster there).
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -118,8 +121,8 @@ __global__ __launch_bounds__(kCombineWaves * kWave) void combine_kernel(RowArgs 
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u) {
         const int i = base + u * kWave + lane;
-        // each expert row is read once: streaming loads (1-2 % faster than
-        // cached ones for 8 KiB rows; the flat forms measured slower with them)
+        // each source row is read once: streaming loads, as in the short and
+        // token-major forms (the flat forms measured slower with them)
         if (i < nch) v[u] = __builtin_nontemporal_load(&srow[i]);
       }
 #pragma unroll
@@ -178,7 +181,7 @@ __global__ __launch_bounds__(kCombineWaves * kWave) void combine_short_kernel(Ro
     }
     u32x4 v[8];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) v[u] = ye[rowoff[u / CPR] + (u % CPR) * kWave + lane];
+    for (int u = 0; u < 8; ++u) v[u] = __builtin_nontemporal_load(&ye[rowoff[u / CPR] + (u % CPR) * kWave + lane]);
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       if (ok[u / CPR]) {
@@ -437,7 +440,7 @@ __global__ __launch_bounds__(kWideWaves * kWave) void dispatch_scatter_kernel(Ro
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       const int i = base + u * kWave + lane;
-      if (i < nch) v[u] = srow[i];
+      if (i < nch) v[u] = __builtin_nontemporal_load(&srow[i]);
     }
     for (int r = 0; r < k; ++r) {
       const int slot = a.slots[s * k + r];
@@ -481,7 +484,7 @@ __global__ __launch_bounds__(kWideWaves * kWave) void combine_bwd_scatter_kernel
 #pragma unroll
     for (int u = 0; u < kU; ++u) {
       const int i = base + u * kWave + lane;
-      if (i < nch) v[u] = dyrow[i];
+      if (i < nch) v[u] = __builtin_nontemporal_load(&dyrow[i]);
     }
 #pragma unroll
     for (int r0 = 0; r0 < 8; r0 += kRG) {
@@ -501,7 +504,7 @@ __global__ __launch_bounds__(kWideWaves * kWave) void combine_bwd_scatter_kernel
 #pragma unroll
           for (int u = 0; u < kU; ++u) {
             const int i = base + u * kWave + lane;
-            if (kept[j] && i < nch) ve[j][u] = yerow[i];
+            if (kept[j] && i < nch) ve[j][u] = __builtin_nontemporal_load(&yerow[i]);
           }
         }
       }

@@ -24,6 +24,8 @@
 //   assign  one wave per wave block: the rank of each token among the block's
 //           tokens with the same expert comes from ballots on the bits of the
 //           expert id (ordered, no atomics) -> slots, slot_src.
+#include <atomic>
+
 #include "select.hpp"
 
 namespace hetumoe {
@@ -328,15 +330,17 @@ __global__ __launch_bounds__(kBlock) void scan_assign_kernel(ScanArgs sa, Assign
 
 // ---------------------------------------------------------------- launchers
 int device_cu_count() {
-  static int cached[64] = {0};
+  // calls may come from several host threads: the cache is atomic (every
+  // thread that fills an entry writes the same value)
+  static std::atomic<int> cached[64];
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  if (cached[dev] == 0) {
-    int n = 0;
+  int n = cached[dev].load(std::memory_order_relaxed);
+  if (n == 0) {
     if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
-    cached[dev] = n;
+    cached[dev].store(n, std::memory_order_relaxed);
   }
-  return cached[dev];
+  return n;
 }
 
 hipError_t launch_route(const RouteArgs& a, hipStream_t st) {

@@ -15,7 +15,7 @@
 // more writes in flight than long row walks (a 1 GiB fill: 6.8 TB/s with one
 // store per thread against 5.7 TB/s with eight), which is why the writers of
 // [E,C,d] use the flat form; the wave form stays where it measured faster
-// (8 KiB token rows, k >= 3, and the token-major scatters).
+// (token rows longer than 2 KiB, k >= 3, and the token-major scatters).
 // Every output row is written with non-temporal stores: the buffers are far
 // larger than the 256 MB Infinity Cache, and plain stores leave dirty lines there
 // whose write-back then slows whichever kernel runs next (measured: dispatch
@@ -205,7 +205,13 @@ __global__ __launch_bounds__(kCombineWaves * kWave) void combine_short_kernel(Ro
 }
 
 // Flat form of the two above for k <= KMAX <= 2: each thread combines one
-// 16-byte chunk of a token row per step, the choices' loads issued together.
+// 16-byte chunk of a token row per step.  Every load of both steps is issued
+// before the first store: vector loads and stores retire in order on one
+// counter, so a store between two loads makes the second wait for it
+// (measured at 2 KiB rows, k = 2: 14.1 -> 13.3 us).  At 4 and 8 KiB rows
+// with k = 1 this form, run alone, beat the wave forms (31.0 against 39.4 us,
+// 157 against 160 us), but was slower in the pass, right after the dispatch's
+// streaming stores (51.7 against 43.6 us, 176.9 against 164.6 us).
 template <typename T, bool POW2, bool WEIGHTED, int KMAX>
 __global__ __launch_bounds__(kFlatThreads) void combine_flat_kernel(RowArgs a, int lg, int64_t total) {
   constexpr int kEl = Chunk<T>::kElems;
@@ -215,40 +221,45 @@ __global__ __launch_bounds__(kFlatThreads) void combine_flat_kernel(RowArgs a, i
   const int col_b = POW2 ? 0 : static_cast<int>(gb - row_b * nch);
   const u32x4* ye = reinterpret_cast<const u32x4*>(a.src);
   u32x4* out = reinterpret_cast<u32x4*>(a.dst);
+  u32x4 v[kFlatPer][KMAX];
+  float w[kFlatPer][KMAX];
+  bool ok[kFlatPer][KMAX];
+#pragma unroll
+  for (int u = 0; u < kFlatPer; ++u) {
+    const int off = u * kFlatThreads + static_cast<int>(threadIdx.x);
+    const bool in = gb + off < total;
+    int64_t s;
+    int col;
+    flat_pos<POW2>(gb, row_b, col_b, off, nch, lg, s, col);
+#pragma unroll
+    for (int r = 0; r < KMAX; ++r) {
+      ok[u][r] = false;
+      w[u][r] = 1.f;
+      v[u][r] = u32x4{0u, 0u, 0u, 0u};
+      if (in && r < k) {
+        const int slot = a.slots[s * k + r];
+        const int e = a.ids[s * k + r];
+        // dropped choices (slot -1) and out-of-contract entries contribute nothing
+        ok[u][r] = slot >= 0 && slot < a.C && e >= 0 && e < a.E;
+        if (WEIGHTED) w[u][r] = a.weights[s * k + r];
+        if (ok[u][r]) v[u][r] = ye[(static_cast<int64_t>(e) * a.C + slot) * nch + col];
+      }
+    }
+  }
 #pragma unroll
   for (int u = 0; u < kFlatPer; ++u) {
     const int off = u * kFlatThreads + static_cast<int>(threadIdx.x);
     if (gb + off >= total) continue;
-    int64_t s;
-    int col;
-    flat_pos<POW2>(gb, row_b, col_b, off, nch, lg, s, col);
-    u32x4 v[KMAX];
-    float w[KMAX];
-    bool ok[KMAX];
-#pragma unroll
-    for (int r = 0; r < KMAX; ++r) {
-      ok[r] = false;
-      w[r] = 1.f;
-      v[r] = u32x4{0u, 0u, 0u, 0u};
-      if (r < k) {
-        const int slot = a.slots[s * k + r];
-        const int e = a.ids[s * k + r];
-        // dropped choices (slot -1) and out-of-contract entries contribute nothing
-        ok[r] = slot >= 0 && slot < a.C && e >= 0 && e < a.E;
-        if (WEIGHTED) w[r] = a.weights[s * k + r];
-        if (ok[r]) v[r] = ye[(static_cast<int64_t>(e) * a.C + slot) * nch + col];
-      }
-    }
     float acc[kEl];
 #pragma unroll
     for (int q = 0; q < kEl; ++q) acc[q] = 0.f;
 #pragma unroll
     for (int r = 0; r < KMAX; ++r) {
-      if (!ok[r]) continue;
+      if (!ok[u][r]) continue;
       float f[kEl];
-      Chunk<T>::unpack(v[r], f);
+      Chunk<T>::unpack(v[u][r], f);
 #pragma unroll
-      for (int q = 0; q < kEl; ++q) acc[q] = WEIGHTED ? fmaf(w[r], f[q], acc[q]) : acc[q] + f[q];
+      for (int q = 0; q < kEl; ++q) acc[q] = WEIGHTED ? fmaf(w[u][r], f[q], acc[q]) : acc[q] + f[q];
     }
     store_nt(out + gb + off, Chunk<T>::pack(acc));
   }
@@ -619,8 +630,8 @@ static void launch_combine_flat(const RowArgs& a, bool weighted, hipStream_t st)
 hipError_t launch_combine(const RowArgs& a, bool weighted, hipStream_t st) {
   if (a.rows == 0 || a.nch == 0) return hipSuccess;
   // k <= 2 over rows of up to 2 KiB: flat form (measured 7-15 % faster than
-  // the wave forms at 1 and 2 KiB rows; 15 % slower at 4 KiB rows, and slower
-  // at 8 KiB rows and at k = 4)
+  // the wave forms at 1 and 2 KiB rows; slower in the pass at 4 and 8 KiB rows,
+  // and slower at k = 4)
   if (a.k <= 2 && a.nch <= 128) {
     if (a.dtype == 1) launch_combine_flat<bf16_t>(a, weighted, st);
     else launch_combine_flat<float>(a, weighted, st);

@@ -243,10 +243,12 @@ def test_layout_ops_many_choices_and_drops(dtype, k, C):
 @pytest.mark.parametrize("dtype,d,k,S,C", [
     ("bf16", 512, 1, 517, 40), ("bf16", 1024, 2, 519, 70), ("bf16", 2048, 3, 1, 1), ("f32", 256, 1, 1023, 90),
     ("f32", 512, 2, 3, 1), ("f32", 1024, 3, 261, 50), ("bf16", 2048, 1, 2, 0),
+    ("bf16", 512, 4, 301, 60), ("f32", 512, 3, 130, 30), ("bf16", 2048, 2, 97, 20),
 ])
 def test_layout_ops_short_rows(dtype, d, k, S, C):
-    """Rows of 1, 2 and 4 KiB, where a wave combines several tokens at once: token
-    counts that leave the last wave partly empty, drops, and C = 0."""
+    """Rows of 1, 2 and 4 KiB: a wave combines several tokens at once (k >= 3, and
+    every k at 4 KiB), the flat form takes k <= 2 up to 2 KiB; token counts that
+    leave the last wave partly empty, drops, and C = 0."""
     E = 16
     announce(f"layout ops short rows dtype={dtype} d={d} k={k} S={S} C={C}")
     rng = np.random.default_rng(d + k + S)

@@ -41,11 +41,12 @@ def dispatch(x, slot_src, k):
     return xe
 
 
-def combine(ye, ids, slots, weights, dtype):
+def combine(ye, ids, slots, weights, dtype, with_exact=False):
     """y[s] = sum_{r: slots[s,r] >= 0} weights[s,r] * ye[ids[s,r], slots[s,r]].
 
     A token with no kept choice gets a zero row (reading R5).  Returns
-    (y in storage dtype, magnitude sum_r |w * ye| as float64).
+    (y in storage dtype, magnitude sum_r |w * ye| as float64), and with
+    `with_exact` also the fp64 sum before its one rounding.
     """
     ye64 = decode(ye, dtype)
     ids = np.asarray(ids)
@@ -60,11 +61,14 @@ def combine(ye, ids, slots, weights, dtype):
         term = w[kept, r, None] * ye64[ids[kept, r], slots[kept, r]]
         y[kept] += term
         mag[kept] += np.abs(term)
+    if with_exact:
+        return encode(y, dtype), mag, y
     return encode(y, dtype), mag
 
 
-def dispatch_bwd(dxe, ids, slots, dtype):
-    """dx[s] = sum_{r kept} dxe[ids[s,r], slots[s,r]]; (dx, magnitude)."""
+def dispatch_bwd(dxe, ids, slots, dtype, with_exact=False):
+    """dx[s] = sum_{r kept} dxe[ids[s,r], slots[s,r]]; (dx, magnitude), and with
+    `with_exact` also the fp64 sum before its one rounding."""
     dxe64 = decode(dxe, dtype)
     ids = np.asarray(ids)
     slots = np.asarray(slots)
@@ -77,16 +81,19 @@ def dispatch_bwd(dxe, ids, slots, dtype):
         term = dxe64[ids[kept, r], slots[kept, r]]
         dx[kept] += term
         mag[kept] += np.abs(term)
+    if with_exact:
+        return encode(dx, dtype), mag, dx
     return encode(dx, dtype), mag
 
 
-def combine_bwd(dy, ye, slot_src, weights, k, dtype, want_dw=True):
+def combine_bwd(dy, ye, slot_src, weights, k, dtype, want_dw=True, with_exact=False):
     """Gradients of combine.
 
     dye[e, c] = weights[s, r] * dy[s] for (s, r) held in slot (e, c), 0 if the
     slot is empty.  dw[s, r] = <dy[s], ye[e, c]> for the slot (e, c) holding
     (s, r); 0 for dropped choices.  Returns (dye in storage dtype, dye
-    magnitude, dw float64 or None, dw magnitude or None).
+    magnitude, dw float64 or None, dw magnitude or None), and with
+    `with_exact` also the fp64 dye before its one rounding.
     """
     dy64 = decode(dy, dtype)
     slot_src = np.asarray(slot_src)
@@ -101,11 +108,13 @@ def combine_bwd(dy, ye, slot_src, weights, k, dtype, want_dw=True):
     dye = encode(dye64, dtype)
     dye_mag = np.abs(dye64)
     if not want_dw:
-        return dye, dye_mag, None, None
+        return (dye, dye_mag, None, None, dye64) if with_exact else (dye, dye_mag, None, None)
     ye64 = decode(ye, dtype)
     dw = np.zeros((S, k), dtype=np.float64)
     dw_mag = np.zeros((S, k), dtype=np.float64)
     rows = ye64[full]                                   # [n_kept, d]
     dw[s_of, r_of] = np.einsum("nd,nd->n", dy64[s_of], rows)
     dw_mag[s_of, r_of] = np.einsum("nd,nd->n", np.abs(dy64[s_of]), np.abs(rows))
+    if with_exact:
+        return dye, dye_mag, dw, dw_mag, dye64
     return dye, dye_mag, dw, dw_mag

@@ -17,6 +17,8 @@ from paper_2203_14685_amd import workloads as wl
 
 RTOL = {"f32": 1e-5, "bf16": 2e-2}
 DEV = "cuda"
+U32 = 2.0 ** -24   # unit roundoff of fp32
+U64 = 2.0 ** -50   # slack for the oracle's own fp64 sums (a few units of 2^-53)
 
 
 def announce(msg):
@@ -40,6 +42,43 @@ def assert_close(gpu, ref, mag, rtol, what):
     nz = mag > 0
     worst = float((err[nz] / mag[nz]).max()) if nz.any() else 0.0
     return worst
+
+
+def check_rounded_once(gpu, exact, mag, nterms, what, rounded=None):
+    """bf16 outputs are formed in fp32 and rounded once (RNE): each GPU value must
+    equal the correctly rounded bf16 value of the exact result, except where the
+    fp32 accumulation's error bound, nterms * 2^-24 * M (plus the oracle's own
+    fp64 error), straddles a bf16 rounding boundary; there the value on either
+    side of the boundary is accepted.  `nterms` broadcasts against `gpu` (terms
+    summed into each element); `rounded`, when given, is the oracle's bf16
+    rounding of `exact`.  Returns the number of accepted straddles.  Zeros
+    compare by value (+0 == -0)."""
+    gpu = np.asarray(gpu, dtype=np.uint16)
+    want = oracle.encode(exact, "bf16") if rounded is None else np.asarray(rounded, dtype=np.uint16)
+    g64, w64 = decode(gpu, "bf16"), decode(want, "bf16")
+    off = g64 != w64
+    if not off.any():
+        return 0
+    idx = np.nonzero(off)
+    ex = np.asarray(exact, dtype=np.float64)[idx]
+    bound = (np.broadcast_to(np.asarray(nterms, dtype=np.float64), gpu.shape)[idx] * U32 + U64) * \
+        np.asarray(mag, dtype=np.float64)[idx]
+    lo = decode(oracle.encode(ex - bound, "bf16"), "bf16")
+    hi = decode(oracle.encode(ex + bound, "bf16"), "bf16")
+    g = g64[idx]
+    ok = (lo != hi) & ((g == lo) | (g == hi))
+    if not ok.all():
+        bad = np.nonzero(~ok)[0][:5]
+        first = [tuple(int(i[b]) for i in idx) for b in bad]
+        raise AssertionError(f"{what}: {int((~ok).sum())} of {gpu.size} values not the once-rounded bf16 of the "
+                             f"exact result; first {first}: gpu {g[bad]} rounded exact {w64[idx][bad]} "
+                             f"exact {ex[bad]} fp32 bound {bound[bad]}")
+    return int(ok.sum())
+
+
+def kept_terms(slots):
+    """Terms summed into each token row by combine / dispatch backward: its kept choices."""
+    return (np.asarray(slots) >= 0).sum(axis=1)[:, None]
 
 
 def assert_equal(gpu, ref, what):
@@ -119,20 +158,31 @@ def check_layout_ops(w, x_host, ids, slots, weights, slot_src, E, C, k, seed=0):
     # combine on random expert outputs
     ye = wl.make_rows((E, C, d), dt, seed + 3)
     y = wl.to_host(hm.combine(wl.to_device(ye, dt), d_ids, d_slots, d_w))
-    y_ref, y_mag = oracle.combine(ye, ids, slots, weights.astype(np.float32).astype(np.float64), dt)
+    y_ref, y_mag, y_ex = oracle.combine(ye, ids, slots, weights.astype(np.float32).astype(np.float64), dt,
+                                        with_exact=True)
     stats["combine_err"] = assert_close(decode(y, dt), decode(y_ref, dt), y_mag, rt, "combine y")
+    nt = kept_terms(slots)
+    if dt == "bf16":
+        stats["combine_straddles"] = check_rounded_once(y, y_ex, y_mag, nt, "combine y", y_ref)
     # dispatch backward
     dxe = wl.make_rows((E, C, d), dt, seed + 4)
     dx = wl.to_host(hm.dispatch_bwd(wl.to_device(dxe, dt), d_ids, d_slots))
-    dx_ref, dx_mag = oracle.dispatch_bwd(dxe, ids, slots, dt)
+    dx_ref, dx_mag, dx_ex = oracle.dispatch_bwd(dxe, ids, slots, dt, with_exact=True)
     stats["dispatch_bwd_err"] = assert_close(decode(dx, dt), decode(dx_ref, dt), dx_mag, rt, "dispatch_bwd dx")
+    one = (nt[:, 0] == 1)
+    assert_equal(dx[one], dx_ref[one], "dispatch_bwd dx of tokens with one kept choice (a copy)")
+    if dt == "bf16":
+        stats["dispatch_bwd_straddles"] = check_rounded_once(dx, dx_ex, dx_mag, nt, "dispatch_bwd dx", dx_ref)
     # combine backward, with and without dw
     dy = wl.make_rows((S, d), dt, seed + 2)
     d_dy, d_ye = wl.to_device(dy, dt), wl.to_device(ye, dt)
     dye, dw = hm.combine_bwd(d_dy, d_ids, d_slots, d_src, d_w, ye=d_ye, want_dw=True)
     dye, dw = wl.to_host(dye), wl.to_host(dw)
-    dye_ref, dye_mag, dw_ref, dw_mag = oracle.combine_bwd(dy, ye, slot_src, weights.astype(np.float32), k, dt)
+    dye_ref, dye_mag, dw_ref, dw_mag, dye_ex = oracle.combine_bwd(dy, ye, slot_src, weights.astype(np.float32), k, dt,
+                                                                  with_exact=True)
     stats["combine_bwd_dye_err"] = assert_close(decode(dye, dt), decode(dye_ref, dt), dye_mag, rt, "combine_bwd dye")
+    if dt == "bf16":
+        stats["combine_bwd_dye_straddles"] = check_rounded_once(dye, dye_ex, dye_mag, 1, "combine_bwd dye", dye_ref)
     stats["combine_bwd_dw_err"] = assert_close(dw, dw_ref, dw_mag, RTOL["f32"], "combine_bwd dw")
     dye2, dw2 = hm.combine_bwd(d_dy, d_ids, d_slots, d_src, d_w, want_dw=False)
     assert dw2 is None

@@ -13,6 +13,7 @@ import oracle
 import paper_2203_14685_amd as hm
 from paper_2203_14685_amd import workloads as wl
 
+from _fullsize import check_layout_full
 from _parity import (RTOL, announce, assert_close, assert_equal, check_gate, check_layout_ops, decode,
                      gpu_gate)
 
@@ -315,20 +316,13 @@ def test_determinism_and_guard_bands():
     assert_equal(wl.to_host(xe), oracle.dispatch(inp["x"], a["slot_src"], k), "dispatch into a view")
 
 
-# ------------------------------------------------------------------ full sizes, sampled
-
-def _compact_combine(ye, ids, slots, w):
-    """Sub-problem holding only the expert rows the given tokens reference."""
-    n, k = ids.shape
-    d = ye.shape[2]
-    sub = np.zeros((n * k, 1, d), dtype=ye.dtype)
-    kept = slots >= 0
-    sub[kept.reshape(-1), 0] = ye[ids[kept], slots[kept]]
-    return sub, np.arange(n * k, dtype=np.int32).reshape(n, k), np.where(kept, 0, -1).astype(np.int32), w
-
+# ------------------------------------------------------------------ full sizes, every element
 
 @pytest.mark.parametrize("wid", [1, 2, 3, 4, 5])
 def test_full_size_parity(wid):
+    """Every routing integer and every element of xe, y, dx, dye and dw at the
+    workload's full size, against the oracle run in chunks (the checks are in
+    tests/_fullsize.py, which needs no GPU)."""
     w = W[wid]
     S, d, E, k, C, dt = w["S"], w["d"], w["E"], w["k"], w["C"], w["dtype"]
     assert C == oracle.capacity(w["cf"], k, S, E)
@@ -336,54 +330,23 @@ def test_full_size_parity(wid):
     inp = wl.make_inputs(w, seed=0)
     g = gpu_gate(w, inp, E, k, C, w["kind"], w["normalize"])
     ref, st = check_gate(w, inp, g, E, k, C, w["kind"], w["normalize"])
-    rng = np.random.default_rng(100 + wid)
+    del ref
     x = wl.to_device(inp["x"], dt)
     d_src = wl.to_device(g["slot_src"], "i32")
     d_ids, d_slots = wl.to_device(g["ids"], "i32"), wl.to_device(g["slots"], "i32")
     d_w = wl.to_device(g["weights"], "f32")
-    # dispatch: sampled rows bit-exact, plus every empty row zero
-    xe = hm.dispatch(x, d_ids, d_slots, d_src)
-    rows = rng.choice(E * C, size=min(E * C, 2048), replace=False)
-    rows = np.concatenate([rows, np.arange(C)])               # all of expert 0
-    got = wl.to_host(xe.view(E * C, d)[torch.from_numpy(rows).cuda()])
-    want = oracle.dispatch(inp["x"], g["slot_src"].reshape(-1)[rows][None, :], k)[0]
-    assert_equal(got, want, "dispatch sampled rows")
-    empty = torch.from_numpy(g["slot_src"].reshape(-1) < 0).cuda()
-    if empty.any():
-        assert (xe.view(E * C, d)[empty] == 0).all()
-    # combine with identity experts (ye = xe) on sampled tokens
-    ye_host = oracle.dispatch(inp["x"], g["slot_src"], k)
-    ye = wl.to_device(ye_host, dt)
-    y = hm.combine(ye, d_ids, d_slots, d_w)
-    toks = rng.choice(S, size=min(S, 1024), replace=False)
-    sub = _compact_combine(ye_host, g["ids"][toks], g["slots"][toks], g["weights"][toks].astype(np.float64))
-    y_ref, y_mag = oracle.combine(*sub, dt)
-    st["combine_err"] = assert_close(decode(wl.to_host(y[torch.from_numpy(toks).cuda()]), dt), decode(y_ref, dt),
-                                     y_mag, RTOL[dt], "combine sampled tokens")
-    # backward of dispatch and combine on sampled outputs
-    dx = hm.dispatch_bwd(ye, d_ids, d_slots)
-    sub = _compact_combine(ye_host, g["ids"][toks], g["slots"][toks], None)
-    dx_ref, dx_mag = oracle.dispatch_bwd(sub[0], sub[1], sub[2], dt)
-    st["dispatch_bwd_err"] = assert_close(decode(wl.to_host(dx[torch.from_numpy(toks).cuda()]), dt),
-                                          decode(dx_ref, dt), dx_mag, RTOL[dt], "dispatch_bwd sampled tokens")
     dy_host = wl.make_rows((S, d), dt, 2)
+    ye_host = wl.make_rows((E, C, d), dt, 3)  # random expert outputs (also the dispatch-backward input)
+    ye = wl.to_device(ye_host, dt)
+    xe = hm.dispatch(x, d_ids, d_slots, d_src)
+    y = hm.combine(ye, d_ids, d_slots, d_w)
+    dx = hm.dispatch_bwd(ye, d_ids, d_slots)
     dye, dw = hm.combine_bwd(wl.to_device(dy_host, dt), d_ids, d_slots, d_src, d_w, ye=ye, want_dw=True)
-    src = g["slot_src"].reshape(-1)[rows]
-    full = src >= 0
-    s_of = np.where(full, src // k, 0)
-    dy_sub = dy_host[s_of]
-    src_sub = np.where(full, np.arange(len(rows)) * k + src % k, -1)[None, :]
-    w_sub = np.zeros((len(rows), k), dtype=np.float32)
-    w_sub[np.arange(len(rows)), np.where(full, src % k, 0)] = g["weights"].reshape(-1)[np.where(full, src, 0)]
-    ye_sub = ye_host.reshape(E * C, d)[rows][None]
-    dye_ref, dye_mag, dw_ref, dw_mag = oracle.combine_bwd(dy_sub, ye_sub, src_sub, w_sub, k, dt)
-    got_dye = wl.to_host(dye.view(E * C, d)[torch.from_numpy(rows).cuda()])
-    st["combine_bwd_dye_err"] = assert_close(decode(got_dye, dt), decode(dye_ref[0], dt), dye_mag[0], RTOL[dt],
-                                             "combine_bwd sampled dye rows")
-    dw_h = wl.to_host(dw)
-    r_of = np.where(full, src % k, 0)
-    st["combine_bwd_dw_err"] = assert_close(dw_h[s_of[full], r_of[full]], dw_ref[np.arange(len(rows))[full], r_of[full]],
-                                            dw_mag[np.arange(len(rows))[full], r_of[full]], RTOL["f32"], "dw sampled")
-    assert (dw_h[g["slots"] < 0] == 0).all()
     torch.cuda.synchronize()
+    outs = {"xe": wl.to_host(xe), "y": wl.to_host(y), "dx": wl.to_host(dx), "dye": wl.to_host(dye),
+            "dw": wl.to_host(dw)}
+    del x, xe, ye, y, dx, dye, dw
+    torch.cuda.empty_cache()
+    st.update(check_layout_full(dt, inp["x"], ye_host, dy_host, g["ids"], g["slots"], g["weights"], g["slot_src"], k,
+                                outs))
     print(f"[stats] full workload {wid}: {st}", flush=True)

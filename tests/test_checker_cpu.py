@@ -123,3 +123,16 @@ def test_rounded_once_straddle_is_accepted_both_ways():
     assert check_rounded_once(np.array([down[0], up[1]]), ex, mag, 1, "t") == 1
     with pytest.raises(AssertionError):
         check_rounded_once(np.array([up[0], np.uint16(up[1] + 1)]), ex, mag, 1, "t")
+
+
+def test_rounded_once_cancellation_widens_the_accepted_range():
+    # a result of 1.5e-6 from terms of magnitude 0.75: the fp32 bound
+    # (2^-24 * 0.75 per term) spans about a dozen bf16 ulps of the result
+    ex = np.array([1.495e-6])
+    mag = np.array([0.76])
+    want = oracle.encode(ex, "bf16")
+    two_below = np.array([np.uint16(want[0] - 2)])
+    assert check_rounded_once(two_below, ex, mag, 2, "t") == 1
+    far = np.array([np.uint16(want[0] - 40)])
+    with pytest.raises(AssertionError):
+        check_rounded_once(far, ex, mag, 2, "t")

@@ -15,7 +15,8 @@
  * Memory     Every buffer argument is DEVICE memory owned by the caller.  Only
  *            the parameter structs are host memory, read during the call.  The
  *            library allocates nothing and keeps no state between calls; it is
- *            reentrant.
+ *            reentrant (moe_gate_noalloc alone uses a fixed device array of the
+ *            library's, see there).
  * Layout     Row-major, densely packed.  x, y, dy, dx: [S, d].  Expert buffers
  *            xe, ye, dxe, dye: [E, C, d].  Per-choice arrays ids, slots,
  *            weights, dw: [S, k].  logits: [S, E] fp32.  slot_src: [E, C].
@@ -55,7 +56,7 @@
 extern "C" {
 #endif
 
-#define MOE_ABI_VERSION 6
+#define MOE_ABI_VERSION 7
 
 /* Symbols of the C ABI are the only ones the shared library exports. */
 #define MOE_API __attribute__((visibility("default")))
@@ -157,6 +158,37 @@ MOE_API moe_status moe_gate(const moe_gate_params* p, const void* x, const void*
                     const int32_t* hash_table, float* logits, int32_t* ids, int32_t* slots,
                     float* weights, int32_t* counts, int32_t* demand, int32_t* slot_src,
                     void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Largest workspace moe_gate_noalloc serves from its fixed scratch (4 MiB). */
+#define MOE_GATE_NOALLOC_MAX_BYTES (4u << 20)
+
+/*
+ * moe_gate_noalloc -- moe_gate for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, hosts that forbid
+ * allocation): the same computation, arguments and outputs as moe_gate, without
+ * the workspace arguments.  Its scratch is a fixed device array of
+ * MOE_GATE_NOALLOC_MAX_BYTES inside the library, one per GPU, held from the
+ * first call on that GPU until the process ends; the call itself allocates
+ * nothing (no hipMalloc, no allocating library routine).
+ *
+ * Limit    the workspace moe_gate_workspace_size() reports for `p` must be at
+ *          most MOE_GATE_NOALLOC_MAX_BYTES (the histogram, 4 * k * E * ceil(S/64)
+ *          bytes, plus S * E * 4 bytes of logits for the Dense-To-Sparse and
+ *          hierarchical gates that select in a kernel of their own); larger
+ *          requests return MOE_ERR_UNSUPPORTED before any HIP call.
+ * Scratch  every call on one GPU uses that GPU's one array: calls that overlap
+ *          on one GPU (several streams or host threads at once) race and give
+ *          undefined results.  Calls in order on one stream are safe; no
+ *          contents carry over between calls (each call overwrites all the
+ *          scratch it reads).
+ * Errors   as moe_gate; the first call on a GPU may also return MOE_ERR_HIP if
+ *          the scratch's device address cannot be looked up.
+ */
+MOE_API moe_status moe_gate_noalloc(const moe_gate_params* p, const void* x, const void* wg,
+                            const float* bias, const int32_t* token_ids, const float* noise,
+                            const int32_t* hash_table, float* logits, int32_t* ids, int32_t* slots,
+                            float* weights, int32_t* counts, int32_t* demand, int32_t* slot_src,
+                            hipStream_t stream);
 
 /*
  * moe_hash_balanced_table -- the balanced assignment of the Hash Layer gate

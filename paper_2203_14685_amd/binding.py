@@ -22,7 +22,7 @@ MOE_F32, MOE_BF16 = 0, 1
 MOE_GATE_TOPK, MOE_GATE_KTOP1, MOE_GATE_HASH, MOE_GATE_HTOPK = 0, 1, 2, 3
 
 EXPORTED = (
-    "moe_gate_workspace_size", "moe_gate", "moe_dispatch", "moe_combine",
+    "moe_gate_workspace_size", "moe_gate", "moe_gate_noalloc", "moe_dispatch", "moe_combine",
     "moe_dispatch_bwd", "moe_combine_bwd", "moe_gate_bwd_workspace_size", "moe_gate_bwd",
     "moe_hash_balanced_table", "moe_base_gate_workspace_size", "moe_base_gate",
     "moe_status_string", "moe_last_error", "moe_abi_version",
@@ -87,6 +87,8 @@ def load():
     lib.moe_gate_workspace_size.argtypes = [ctypes.POINTER(GateParams), ctypes.POINTER(ctypes.c_size_t)]
     lib.moe_gate.argtypes = [ctypes.POINTER(GateParams), vp, vp, f32p, i32p, f32p, i32p, f32p, i32p, i32p,
                              f32p, i32p, i32p, i32p, vp, ctypes.c_size_t, vp]
+    lib.moe_gate_noalloc.argtypes = [ctypes.POINTER(GateParams), vp, vp, f32p, i32p, f32p, i32p, f32p, i32p, i32p,
+                                     f32p, i32p, i32p, i32p, vp]
     lib.moe_hash_balanced_table.argtypes = [vp, ctypes.c_int32, ctypes.c_int32, vp]
     lib.moe_dispatch.argtypes = [ctypes.POINTER(Layout), vp, i32p, i32p, i32p, vp, vp]
     lib.moe_combine.argtypes = [ctypes.POINTER(Layout), vp, i32p, i32p, f32p, vp, vp]
@@ -186,6 +188,22 @@ def moe_gate(params, x, wg, bias, token_ids, noise, hash_table, logits, ids, slo
         _ptr(ids, i32, "ids", S * k), _ptr(slots, i32, "slots", S * k), _ptr(weights, f32, "weights", S * k),
         _ptr(counts, i32, "counts", E), _ptr(demand, i32, "demand", E), _ptr(slot_src, i32, "slot_src", E * C),
         _ptr(workspace, None, "workspace"), ws_bytes, _stream(stream)))
+
+
+def moe_gate_noalloc(params, x, wg, bias, token_ids, noise, hash_table, logits, ids, slots, weights, counts, demand,
+                     slot_src, stream=None):
+    """moe_gate without a workspace: the library's fixed scratch serves it."""
+    lib = load()
+    f32, i32 = torch.float32, torch.int32
+    xdt = torch.bfloat16 if params.dtype == MOE_BF16 else torch.float32
+    S, d, E, k, C = params.S, params.d, params.E, params.k, params.capacity
+    _check(lib.moe_gate_noalloc(
+        ctypes.byref(params), _ptr(x, xdt, "x", S * d), _ptr(wg, xdt, "wg", d * E), _ptr(bias, f32, "bias", E),
+        _ptr(token_ids, i32, "token_ids", S), _ptr(noise, f32, "noise", S * E),
+        _ptr(hash_table, i32, "hash_table", params.hash_vocab), _ptr(logits, f32, "logits", S * E),
+        _ptr(ids, i32, "ids", S * k), _ptr(slots, i32, "slots", S * k), _ptr(weights, f32, "weights", S * k),
+        _ptr(counts, i32, "counts", E), _ptr(demand, i32, "demand", E), _ptr(slot_src, i32, "slot_src", E * C),
+        _stream(stream)))
 
 
 def _layout(S, d, E, k, capacity, dtype):

@@ -5,6 +5,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <vector>
 
@@ -365,11 +366,43 @@ moe_status moe_gate_workspace_size(const moe_gate_params* p, size_t* bytes) {
   return ok();
 }
 
-moe_status moe_gate(const moe_gate_params* p, const void* x, const void* wg, const float* bias,
-                    const int32_t* token_ids, const float* noise, const int32_t* hash_table, float* logits,
-                    int32_t* ids, int32_t* slots, float* weights, int32_t* counts, int32_t* demand,
-                    int32_t* slot_src, void* workspace, size_t workspace_bytes, hipStream_t stream) {
-  static const char* who = "moe_gate";
+}  // extern "C"
+
+namespace {
+
+// Scratch of moe_gate_noalloc: the gate's workspace in device memory the library
+// owns, one copy per GPU, held until the process ends.  Host code uses only the
+// address hipGetSymbolAddress returns for the current device, never the name.
+constexpr size_t kGateScratchBytes = MOE_GATE_NOALLOC_MAX_BYTES;
+__device__ __align__(256) unsigned char scratch[kGateScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::atomic<void*> g_scratch_ptr[kMaxDevices];
+
+// Device address of the current device's scratch (looked up once per device;
+// every thread that looks it up stores the same address).
+moe_status scratch_address(const char* who, void** out) {
+  int dev = -1;
+  hipError_t err = hipGetDevice(&dev);
+  if (err != hipSuccess) return hip_fail(err, "moe_gate_noalloc: hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(MOE_ERR_UNSUPPORTED, "%s: device %d beyond the %d served", who, dev, kMaxDevices);
+  void* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (!p) {
+    err = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (err != hipSuccess) return hip_fail(err, "moe_gate_noalloc: hipGetSymbolAddress(scratch)");
+    if (!p) return fail(MOE_ERR_HIP, "%s: hipGetSymbolAddress(scratch) gave NULL", who);
+    g_scratch_ptr[dev].store(p, std::memory_order_release);
+  }
+  *out = p;
+  return MOE_OK;
+}
+
+// moe_gate and moe_gate_noalloc: with `noalloc` the workspace arguments are
+// ignored and the gate runs in the library's scratch.
+moe_status gate_call(const char* who, bool noalloc, const moe_gate_params* p, const void* x, const void* wg,
+                     const float* bias, const int32_t* token_ids, const float* noise, const int32_t* hash_table,
+                     float* logits, int32_t* ids, int32_t* slots, float* weights, int32_t* counts, int32_t* demand,
+                     int32_t* slot_src, void* workspace, size_t workspace_bytes, hipStream_t stream) {
   CHECK(check_gate_params(p));
   const int64_t S = p->S, E = p->E, k = p->k, C = p->capacity;
   const size_t elt = elt_size(p->dtype);
@@ -400,9 +433,17 @@ moe_status moe_gate(const moe_gate_params* p, const void* x, const void* wg, con
   CHECK(need(demand, 0, 4, who, "demand"));
   CHECK(need(slot_src, E * C, 4, who, "slot_src"));
   const size_t ws = gate_workspace_bytes(p);
-  if (workspace_bytes < ws) return fail(MOE_ERR_WORKSPACE, "%s: workspace of %zu bytes, %zu needed", who, workspace_bytes, ws);
-  if (ws > 0 && !workspace) return fail(MOE_ERR_WORKSPACE, "%s: workspace is NULL", who);
-  if (workspace && !aligned(workspace, 16)) return fail(MOE_ERR_WORKSPACE, "%s: workspace is not 16-byte aligned", who);
+  if (noalloc) {
+    if (ws > kGateScratchBytes)
+      return fail(MOE_ERR_UNSUPPORTED, "%s: this gate needs %zu bytes of scratch; the fixed scratch holds %zu "
+                  "(use moe_gate with a workspace)", who, ws, kGateScratchBytes);
+    CHECK(scratch_address(who, &workspace));
+    workspace_bytes = kGateScratchBytes;
+  } else {
+    if (workspace_bytes < ws) return fail(MOE_ERR_WORKSPACE, "%s: workspace of %zu bytes, %zu needed", who, workspace_bytes, ws);
+    if (ws > 0 && !workspace) return fail(MOE_ERR_WORKSPACE, "%s: workspace is NULL", who);
+    if (workspace && !aligned(workspace, 16)) return fail(MOE_ERR_WORKSPACE, "%s: workspace is not 16-byte aligned", who);
+  }
 
   const int nb = static_cast<int>(hist_blocks(S));
   int32_t* hist = static_cast<int32_t*>(workspace);
@@ -466,6 +507,26 @@ moe_status moe_gate(const moe_gate_params* p, const void* x, const void* wg, con
   err = launch_scan_assign(sa, aa, stream);
   if (err != hipSuccess) return hip_fail(err, "moe_gate: scan / assign kernel launch");
   return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+moe_status moe_gate(const moe_gate_params* p, const void* x, const void* wg, const float* bias,
+                    const int32_t* token_ids, const float* noise, const int32_t* hash_table, float* logits,
+                    int32_t* ids, int32_t* slots, float* weights, int32_t* counts, int32_t* demand,
+                    int32_t* slot_src, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  return gate_call("moe_gate", false, p, x, wg, bias, token_ids, noise, hash_table, logits, ids, slots, weights,
+                   counts, demand, slot_src, workspace, workspace_bytes, stream);
+}
+
+moe_status moe_gate_noalloc(const moe_gate_params* p, const void* x, const void* wg, const float* bias,
+                            const int32_t* token_ids, const float* noise, const int32_t* hash_table, float* logits,
+                            int32_t* ids, int32_t* slots, float* weights, int32_t* counts, int32_t* demand,
+                            int32_t* slot_src, hipStream_t stream) {
+  return gate_call("moe_gate_noalloc", true, p, x, wg, bias, token_ids, noise, hash_table, logits, ids, slots,
+                   weights, counts, demand, slot_src, nullptr, 0, stream);
 }
 
 moe_status moe_hash_balanced_table(const double* freq, int32_t vocab, int32_t E, int32_t* table) {

@@ -38,7 +38,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_abi_version_and_struct_layout(lib):
-    assert lib.moe_abi_version() == 6
+    assert lib.moe_abi_version() == 7
     assert ctypes.sizeof(b.GateParams) == 56
     assert b.GateParams.hash_seed.offset == 40
     assert b.GateParams.temperature.offset == 48 and b.GateParams.hash_vocab.offset == 52
@@ -93,6 +93,21 @@ def test_null_params_and_extended_workspace(lib):
     for params in (hm.gate_params(1000, 256, 16, 2, 20, 3, groups=4), hm.gate_params(1000, 256, 16, 2, 20, 0, temperature=0.5)):
         hist = 2 * ((1000 + 63) // 64) * 16 * 4
         assert _ws(params) == (0, (hist + 255) // 256 * 256 + 1000 * 16 * 4)
+
+
+def test_noalloc_validates_before_any_hip_call(lib):
+    assert lib.moe_gate_noalloc(None, *([None] * 13), None) == b.MOE_ERR_INVALID_ARG
+    bad = hm.gate_params(100, 256, 0, 1, 20, 0)
+    assert lib.moe_gate_noalloc(ctypes.byref(bad), *([None] * 13), None) == b.MOE_ERR_INVALID_ARG
+    # a histogram of 8 * 1024 * 256 int32 (8 MiB) exceeds the 4 MiB scratch:
+    # refused after the pointer checks, before the scratch is looked up; the
+    # stand-in addresses are never dereferenced
+    p = hm.gate_params(16384, 0, 1024, 8, 4, 0, 0, 1, 0)
+    fake = ctypes.c_void_p(1 << 20)
+    st = lib.moe_gate_noalloc(ctypes.byref(p), None, None, None, None, None, None, fake, fake, fake, fake, fake, None,
+                              fake, None)
+    assert st == b.MOE_ERR_UNSUPPORTED, lib.moe_last_error()
+    assert b"scratch" in lib.moe_last_error()
 
 
 def test_balanced_hash_table_matches_the_oracle(lib):

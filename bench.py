@@ -35,37 +35,29 @@ OPS_KERNELS = ("dispatch", "combine", "combine_bwd", "dispatch_bwd", "gate")
 def kernel_of_op(op, w):
     """(kernel symbol fragment in traces, sources that kernel is compiled from) of
     the one kernel an op launches for workload dict `w`, following the launch
-    rules of the layout library: with several choices per token dispatch and
-    combine backward scatter token-major; with one, both run the flat
-    one-chunk-per-thread form (combine backward with dw only on rows of 64 to
-    1024 chunks, a power of two); combine and dispatch backward run the flat form
-    for k <= 2 on rows of up to 128 chunks, several tokens per wave on rows of
-    64, 128 or 256 chunks otherwise, one token per wave beyond."""
+    rules of the layout library: with one choice per token, dispatch and combine
+    backward run the slot-row kernel (combine backward with dw there only on
+    rows of 64 to 512 chunks, a power of two, else one wave per row); with
+    several, the token-major forms; combine and dispatch backward always run the
+    token-row kernel, its choice list sized 1, 2, 4 or 8."""
     elt = "hetumoe::bf16_t" if w["dtype"] == "bf16" else "float"
     k = w["k"]
     nch = w["d"] * (2 if w["dtype"] == "bf16" else 4) // 16
     pow2 = nch > 0 and (nch & (nch - 1)) == 0
     p2 = "true" if pow2 else "false"
     dw = w["kind"] != 2  # learned gates have weights to differentiate (hash: none)
+    kmax = 1 if k == 1 else 2 if k == 2 else 4 if k <= 4 else 8
     if k > 1:
-        cbwd = "combine_bwd_scatter_kernel"
-    elif dw and not (pow2 and 64 <= nch <= 1024):
-        cbwd = f"combine_bwd_kernel<{elt}, true>"
+        cbwd = f"combine_bwd_scatter_kernel<{elt}, {'true' if dw else 'false'}>"
+    elif dw and not (pow2 and 64 <= nch <= 512):
+        cbwd = f"combine_bwd_wave_kernel<{elt}>"
     else:
-        cbwd = f"combine_bwd_flat_kernel<{elt}, {'true' if dw else p2}, {'true' if dw else 'false'}>"
-
-    def comb(weighted):
-        t = "true" if weighted else "false"
-        if k <= 2 and nch <= 128:
-            return f"combine_flat_kernel<{elt}, {p2}, {t}, {k}>"
-        if nch in (64, 128, 256) and w["E"] * w["C"] > 0:
-            return f"combine_short_kernel<{elt}, {t}, "
-        return f"combine_kernel<{elt}, {t}>"
-
-    return {"dispatch": ("dispatch_scatter_kernel" if k > 1 else f"dispatch_flat_kernel<{p2}>", _LAYOUT_SRC),
-            "combine": (comb(True), _LAYOUT_SRC),
+        cbwd = f"slot_rows_kernel<{elt}, true, {'true' if dw else 'false'}, {p2}>"
+    return {"dispatch": ("dispatch_scatter_kernel" if k > 1 else f"slot_rows_kernel<float, false, false, {p2}>",
+                         _LAYOUT_SRC),
+            "combine": (f"token_rows_kernel<{elt}, true, {kmax}>", _LAYOUT_SRC),
             "combine_bwd": (cbwd, _LAYOUT_SRC),
-            "dispatch_bwd": (comb(False), _LAYOUT_SRC),
+            "dispatch_bwd": (f"token_rows_kernel<{elt}, false, {kmax}>", _LAYOUT_SRC),
             "gate": ("route_", _GATE_SRC)}[op]
 
 
@@ -113,7 +105,7 @@ def summarize_pmc(args):
             f.write(f"# HBM traffic per launch of {frag} ({op}), workload {w['name']}\n")
             f.write("# from two rocprofv3 counter runs (TMPDIR=/tmp, from /tmp, repo at $R):\n")
             f.write(f"#   rocprofv3 --pmc FETCH_SIZE --output-format csv -d <dir> -- python3 $R/bench.py --workload "
-                    f"{args.workload} --steps 3 --warmup 1 --no-cpu-baseline --no-base --cold-iters 0 "
+                    f"{args.workload} --steps 3 --warmup 1 --no-cpu-baseline --no-base --no-workloads --cold-iters 0 "
                     f"--calib-copy-mib {args.calib_copy_mib}\n")
             f.write("#   (the same with --pmc WRITE_SIZE)\n")
             f.write(f"# calibration: one {args.calib_copy_mib} MiB device copy read FETCH {fc:.0f} KiB, WRITE {wc:.0f} KiB\n")
@@ -148,7 +140,8 @@ def summarize_mfma(args):
     lines = [f"# matrix-core use per launch, workload {w['name']}",
              "# from one rocprofv3 counter run (TMPDIR=/tmp, from /tmp, repo at $R):",
              f"#   rocprofv3 --pmc MfmaUtil MfmaFlopsBF16 GRBM_GUI_ACTIVE --output-format csv -d <dir> -- python3 "
-             f"$R/bench.py --workload {args.workload} --steps 3 --warmup 1 --no-cpu-baseline --no-base --cold-iters 0",
+             f"$R/bench.py --workload {args.workload} --steps 3 --warmup 1 --no-cpu-baseline --no-base --no-workloads "
+             "--cold-iters 0",
              "# MfmaUtil = matrix-unit busy cycles summed over SIMDs / (GPU active cycles x SIMDs) x 100;",
              "# MfmaFlopsBF16 = bf16 MFMA operations x 512 (flops counted by the hardware)",
              f"# algorithmic flops of one projection 2*S*d*E = {alg}",
@@ -196,6 +189,9 @@ def parse():
     ap.add_argument("--cold-iters", type=int, default=10,
                     help="per-op timings from a cold cache: launches of each op, each after reading a 1 GiB "
                          "buffer (0 = skip)")
+    ap.add_argument("--no-workloads", action="store_true",
+                    help="skip the compact figures of the other four workloads (for counter and trace runs of one "
+                         "workload)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="before the timed region, run one device copy of this many MiB (counter calibration)")
     return ap.parse_args()
@@ -257,11 +253,14 @@ def measured_traffic(workload_name, op, sha):
         return None
 
 
-def cpu_baseline(w, target_s=12.0):
+def cpu_baseline(w, target_s=8.0):
     """The oracle, untuned, on a bounded sample of the same workload (its first
     S_s tokens, capacity scaled the same way), timed on this host, stage by
-    stage; for learned gates the fp64 projection (a numpy BLAS product) is also
-    timed with the BLAS pool limited to one thread."""
+    stage; the sample doubles until a pass takes about target_s / 2, then the
+    pass runs three times and each stage reports its median (one run when a
+    pass exceeds 30 s).  For learned gates the fp64 projection (a numpy BLAS
+    product) is also timed with the whole BLAS pool and with one thread, median
+    of three."""
     import math
 
     import oracle
@@ -275,10 +274,9 @@ def cpu_baseline(w, target_s=12.0):
     k, E, d, dt = w["k"], w["E"], w["d"], w["dtype"]
     learned = w["kind"] != 2
 
-    def run(S_s):
+    def run(S_s, data=None):
         C_s = int(math.ceil(w["cf"] * k * S_s / E))
-        inp = wl.make_inputs(w, S=S_s, seed=0)
-        dy = wl.make_rows((S_s, d), dt, 2)
+        inp, dy = data if data is not None else (wl.make_inputs(w, S=S_s, seed=0), wl.make_rows((S_s, d), dt, 2))
         t0 = time.perf_counter()
         g = oracle.gate(w["kind"], k, E, C_s, normalize=w["normalize"], dtype=dt, x=inp["x"], wg=inp["wg"],
                         bias=inp["bias"], token_ids=inp["token_ids"], hash_seed=0)
@@ -292,31 +290,44 @@ def cpu_baseline(w, target_s=12.0):
         oracle.dispatch_bwd(dye, g["ids"], g["slots"], dt)
         t5 = time.perf_counter()
         st = {"gate": t1 - t0, "dispatch": t2 - t1, "combine": t3 - t2, "combine_bwd": t4 - t3, "dispatch_bwd": t5 - t4}
-        return t5 - t0, st, inp
+        return t5 - t0, st, (inp, dy)
 
     S_s = 512
-    t, st, inp = run(S_s)
+    t, st, data = run(S_s)
     while t < target_s / 2 and S_s * 2 <= w["S"]:
         S_s *= 2
-        t, st, inp = run(S_s)
+        t, st, data = run(S_s)
+    runs = [(t, st)]
+    if t <= 30.0:
+        runs += [run(S_s, data)[:2] for _ in range(2)]
+
+    def med(v):
+        return sorted(v)[len(v) // 2]
+    t = med([r[0] for r in runs])
+    stage = {key: med([r[1][key] for r in runs]) for key in runs[0][1]}
     out = {"value": round(S_s / t, 1), "unit": "tokens/s", "cores": int(blas_threads if learned else 1),
            "kind": "oracle",
            "sample": f"first {S_s} of {w['S']} tokens of the same workload (capacity scaled alike), "
-                     f"full pass gate+dispatch+combine+combine_bwd+dispatch_bwd in {t:.2f} s, fp64 numpy",
-           "stage_s": {key: round(v, 3) for key, v in st.items()}}
+                     f"full pass gate+dispatch+combine+combine_bwd+dispatch_bwd, median of {len(runs)} "
+                     f"passes {t:.2f} s, fp64 numpy",
+           "stage_s": {key: round(v, 3) for key, v in stage.items()}, "passes": len(runs)}
     if learned:
         # the projection alone (numpy BLAS, fp64) with the whole pool and with one thread
+        inp = data[0]
         pt = {}
         for n in sorted({blas_threads, 1}, reverse=True):
             if threadpool_limits is None and n != blas_threads:
                 continue
-            t0 = time.perf_counter()
-            if threadpool_limits is not None:
-                with threadpool_limits(limits=n, user_api="blas"):
+            ts = []
+            for _ in range(3):
+                t0 = time.perf_counter()
+                if threadpool_limits is not None:
+                    with threadpool_limits(limits=n, user_api="blas"):
+                        oracle.logits(inp["x"], inp["wg"], dt, inp["bias"])
+                else:
                     oracle.logits(inp["x"], inp["wg"], dt, inp["bias"])
-            else:
-                oracle.logits(inp["x"], inp["wg"], dt, inp["bias"])
-            pt[str(n)] = round(time.perf_counter() - t0, 3)
+                ts.append(time.perf_counter() - t0)
+            pt[str(n)] = round(med(ts), 3)
         out["projection_s_by_threads"] = pt
     try:
         out["host"] = {"cpus_allowed": len(os.sched_getaffinity(0)),
@@ -325,6 +336,119 @@ def cpu_baseline(w, target_s=12.0):
     except OSError:
         pass
     return out
+
+
+def build_pass(w, dev):
+    """Device inputs, outputs and the five op calls of one step of workload `w`
+    (identity experts: ye = xe, dxe = dye)."""
+    import types
+
+    import torch
+    import paper_2203_14685_amd as hm
+    from paper_2203_14685_amd import workloads as wl
+    S, d, E, k, C, dt = w["S"], w["d"], w["E"], w["k"], w["C"], w["dtype"]
+    tdt = torch.bfloat16 if dt == "bf16" else torch.float32
+    dcode = hm.MOE_BF16 if dt == "bf16" else hm.MOE_F32
+    learned = w["kind"] != 2
+    P = types.SimpleNamespace()
+    P.inp = inp = wl.make_inputs(w, seed=0)
+    P.x = x = wl.to_device(inp["x"], dt)
+    P.wg = wg = wl.to_device(inp["wg"], dt)
+    P.bias = bias = wl.to_device(inp["bias"], "f32")
+    P.tok = tok = wl.to_device(inp["token_ids"], "i32")
+    P.dy = dy = wl.to_device(wl.make_rows((S, d), dt, 2), dt)
+    P.params = params = hm.gate_params(S, d if learned else 0, E, k, C, w["kind"], w["normalize"], 0, dcode, 0)
+    i32, f32 = torch.int32, torch.float32
+    P.ids = ids = torch.empty((S, k), dtype=i32, device=dev)
+    P.slots = slots = torch.empty((S, k), dtype=i32, device=dev)
+    P.weights = weights = torch.empty((S, k), dtype=f32, device=dev)
+    P.counts = counts = torch.empty((E,), dtype=i32, device=dev)
+    P.demand = demand = torch.empty((E,), dtype=i32, device=dev)
+    P.slot_src = slot_src = torch.empty((E, C), dtype=i32, device=dev)
+    P.ws = ws = torch.empty((hm.moe_gate_workspace_size(params),), dtype=torch.uint8, device=dev)
+    P.xe = xe = torch.empty((E, C, d), dtype=tdt, device=dev)
+    P.y = y = torch.empty((S, d), dtype=tdt, device=dev)
+    P.dye = dye = torch.empty((E, C, d), dtype=tdt, device=dev)
+    P.dw = dw = torch.empty((S, k), dtype=f32, device=dev) if learned else None
+    P.dx = dx = torch.empty((S, d), dtype=tdt, device=dev)
+    lay = hm.Layout(S, d, E, k, C, dcode)
+    P.op_calls = {
+        "gate": lambda st: hm.moe_gate(params, x if learned else None, wg, bias, tok if not learned else None, None,
+                                       None, None, ids, slots, weights, counts, demand, slot_src, ws, st),
+        "dispatch": lambda st: hm.moe_dispatch(lay, x, ids, slots, slot_src, xe, st),
+        "combine": lambda st: hm.moe_combine(lay, xe, ids, slots, weights, y, st),
+        "combine_bwd": lambda st: hm.moe_combine_bwd(lay, dy, xe if learned else None, ids, slots, slot_src, weights,
+                                                     dye, dw, st),
+        "dispatch_bwd": lambda st: hm.moe_dispatch_bwd(lay, dye, ids, slots, dx, st),
+    }
+    return P
+
+
+def workload_summary(wid, steps, warmup):
+    """Compact figures of one workload, measured in the same run as the headline:
+    step time eager (per-op HIP events on the library's stream) and as a HIP
+    graph replay, tokens/s, the step's and each op's share of the HBM peak, the
+    dominant op's kernel, and the gate's time."""
+    import torch
+    from paper_2203_14685_amd import workloads as wl
+    w = wl.WORKLOADS[wid]
+    dev = torch.device("cuda:0")
+    S, d, E, k, C = w["S"], w["d"], w["E"], w["k"], w["C"]
+    elt = 2 if w["dtype"] == "bf16" else 4
+    P = build_pass(w, dev)
+    stream = torch.cuda.current_stream()
+
+    def step(evs=None, st=None):
+        st = stream if st is None else st
+        for i, op in enumerate(OPS):
+            if evs is not None:
+                evs[i].record(st)
+            P.op_calls[op](st)
+        if evs is not None:
+            evs[len(OPS)].record(st)
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(OPS) + 1)] for _ in range(steps)]
+    t0 = time.perf_counter()
+    for i in range(steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    eager_ms = (time.perf_counter() - t0) * 1e3 / steps
+    op_ms = {op: sum(e[j].elapsed_time(e[j + 1]) for e in evs) / steps for j, op in enumerate(OPS)}
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step(None, torch.cuda.current_stream())  # the capture stream
+    torch.cuda.synchronize()
+    for _ in range(warmup):
+        graph.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        graph.replay()
+    torch.cuda.synchronize()
+    graph_ms = (time.perf_counter() - t0) * 1e3 / steps
+    sl = P.slots.cpu().numpy()
+    n_kept = int((sl >= 0).sum())
+    tok_kept = int((sl >= 0).any(axis=1).sum())
+    ab = alg_bytes(w, S, d, E, k, C, elt, n_kept, tok_kept, w["kind"] != 2)
+    step_bytes = sum(ab.values())
+    fwd_ms = op_ms["gate"] + op_ms["dispatch"] + op_ms["combine"]
+    fwd_bytes = ab["gate"] + ab["dispatch"] + ab["combine"]
+    dom = max(OPS, key=lambda o: op_ms[o])
+
+    def frac(b, ms):
+        return round(b / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)
+    del graph, P
+    torch.cuda.empty_cache()
+    return {"step_ms": {"eager": round(eager_ms, 4), "graph": round(graph_ms, 4)},
+            "tokens/s": {"eager": round(S / (eager_ms * 1e-3), 1), "graph": round(S / (graph_ms * 1e-3), 1)},
+            "step_frac": {"eager": frac(step_bytes, eager_ms), "graph": frac(step_bytes, graph_ms)},
+            "fwd": {"ms": round(fwd_ms, 5), "frac": frac(fwd_bytes, fwd_ms)},
+            "ops_frac": {op: frac(ab[op], op_ms[op]) for op in OPS},
+            "ops_us": {op: round(op_ms[op] * 1e3, 2) for op in OPS},
+            "dominant": {"op": dom, "kernel": kernel_of_op(dom, w)[0].split("<")[0], "frac": frac(ab[dom], op_ms[dom])},
+            "gate_us": round(op_ms["gate"] * 1e3, 2)}
 
 
 def main():
@@ -359,39 +483,13 @@ def main():
     learned = w["kind"] != 2
     want_dw = learned
 
-    inp = wl.make_inputs(w, seed=0)
-    x = wl.to_device(inp["x"], dt)
-    wg = wl.to_device(inp["wg"], dt)
-    bias = wl.to_device(inp["bias"], "f32")
-    tok = wl.to_device(inp["token_ids"], "i32")
-    dy = wl.to_device(wl.make_rows((S, d), dt, 2), dt)
-
-    params = hm.gate_params(S, d if learned else 0, E, k, C, w["kind"], w["normalize"], 0, dcode, 0)
-    i32, f32 = torch.int32, torch.float32
-    ids = torch.empty((S, k), dtype=i32, device=dev)
-    slots = torch.empty((S, k), dtype=i32, device=dev)
-    weights = torch.empty((S, k), dtype=f32, device=dev)
-    counts = torch.empty((E,), dtype=i32, device=dev)
-    demand = torch.empty((E,), dtype=i32, device=dev)
-    slot_src = torch.empty((E, C), dtype=i32, device=dev)
-    ws = torch.empty((hm.moe_gate_workspace_size(params),), dtype=torch.uint8, device=dev)
-    xe = torch.empty((E, C, d), dtype=tdt, device=dev)
-    y = torch.empty((S, d), dtype=tdt, device=dev)
-    dye = torch.empty((E, C, d), dtype=tdt, device=dev)
-    dw = torch.empty((S, k), dtype=f32, device=dev) if want_dw else None
-    dx = torch.empty((S, d), dtype=tdt, device=dev)
-    lay = hm.Layout(S, d, E, k, C, dcode)
+    P = build_pass(w, dev)
+    x, wg, bias, tok, dy, inp = P.x, P.wg, P.bias, P.tok, P.dy, P.inp
+    params, ids, slots, weights, counts, demand, slot_src, ws = (P.params, P.ids, P.slots, P.weights, P.counts,
+                                                                 P.demand, P.slot_src, P.ws)
+    xe, dw, dx = P.xe, P.dw, P.dx
     stream = torch.cuda.current_stream()
-
-    op_calls = {
-        "gate": lambda st: hm.moe_gate(params, x if learned else None, wg, bias, tok if not learned else None, None,
-                                       None, None, ids, slots, weights, counts, demand, slot_src, ws, st),
-        "dispatch": lambda st: hm.moe_dispatch(lay, x, ids, slots, slot_src, xe, st),
-        "combine": lambda st: hm.moe_combine(lay, xe, ids, slots, weights, y, st),
-        "combine_bwd": lambda st: hm.moe_combine_bwd(lay, dy, xe if want_dw else None, ids, slots, slot_src, weights,
-                                                     dye, dw, st),
-        "dispatch_bwd": lambda st: hm.moe_dispatch_bwd(lay, dye, ids, slots, dx, st),
-    }
+    op_calls = P.op_calls
 
     def step(evs=None, st=None):
         st = stream if st is None else st
@@ -647,6 +745,15 @@ def main():
     out["fwd"] = {"ms": round(fwd_ms, 5), "tokens/s": round(S / (fwd_ms * 1e-3), 1),
                   "frac": round((ab["gate"] + ab["dispatch"] + ab["combine"]) / (fwd_ms * 1e-3) / 1e9
                                 / HBM_PEAK_GBS, 4)}
+    if not args.no_workloads:
+        # the other workloads, compact, in the same run (no CPU baseline, no BASE)
+        out["workloads"] = {}
+        for wid in sorted(wl.WORKLOADS):
+            if wid == args.workload:
+                continue
+            print(f"[bench] workload {wid} {wl.WORKLOADS[wid]['name']}: compact figures", file=sys.stderr, flush=True)
+            out["workloads"][wl.WORKLOADS[wid]["name"]] = workload_summary(wid, min(args.steps, 20),
+                                                                           max(1, min(args.warmup, 5)))
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(w)

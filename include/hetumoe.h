@@ -2,7 +2,7 @@
  * hetumoe.h -- C ABI of the single-GPU MoE gate / layout-transform hot path
  * (HetuMoE, arXiv 2203.14685), built for AMD Instinct MI355X (gfx950).
  *
- * The calls follow Algorithm 1 ("General MoE Training Process") of the paper:
+ * The calls follow Algorithm 1 of the paper (one training step of an MoE layer):
  *   step 1  W, id = Gate(x)                      -> moe_gate
  *   step 2  x' = Layout_Transform(x, id)         -> moe_dispatch
  *   step 6  y = Reverse_Layout_Transform(y', id) -> moe_combine (gate-weighted)

@@ -10,13 +10,13 @@ Arithmetic is fp64 on exactly decoded inputs.  bf16 tensors are held as uint16
 bit patterns (see :mod:`oracle.bf16`).  Every function cites the passage of the
 paper it follows:
 
-* Algorithm 1 ("General MoE Training Process"), steps 1, 2 and 6, and the
+* Algorithm 1 (one training step of an MoE layer), steps 1, 2 and 6, and the
   numbered list of Sec. 2 that describes them;
 * Eq. 1 (Sec. 3.1, Top1/Top2/Topk gate) and the capacity-factor sentence next
   to it;
 * Sec. 3.1 kTop1 (expert prototyping) and Hash Layer paragraphs;
-* Sec. 3.2 "Gate Optimization" (top-k over a (num_tokens, num_experts) input)
-  and "Layout Transform Optimization" (tokens of one expert made contiguous);
+* Sec. 3.2, on the gate (top-k over a (num_tokens, num_experts) input) and
+  on the layout transform (tokens of one expert made contiguous);
 * the gradient of Eq. 1 that end-to-end training of the layer (Sec. 2) needs,
   and a load-balancing loss (reading R16) for the gates of Sec. 3.1;
 * the BASE layer's balanced assignment (Sec. 3.1, the equation of the BASE

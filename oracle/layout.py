@@ -2,8 +2,8 @@
 
 TEST INFRASTRUCTURE ONLY (see the package docstring).
 
-* dispatch     -- Layout_Transform (Algorithm 1, step 2; Sec. 3.2 "Layout
-                  Transform Optimization"): every token is copied into the
+* dispatch     -- Layout_Transform (Algorithm 1, step 2; Sec. 3.2, layout
+                  transform): every token is copied into the
                   contiguous buffer of each expert it was kept for, here a fixed
                   [E, C, d] buffer whose empty rows are zero (reading R6).
 * combine      -- Reverse_Layout_Transform (step 6) together with the

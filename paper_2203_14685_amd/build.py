@@ -39,6 +39,25 @@ def _run(cmd):
     return res.returncode, res.stdout + res.stderr
 
 
+def prune_stale_objects(objdir, sources=SOURCES):
+    """Delete the objects in `objdir` that no source of `sources` produces.  Such
+    objects (left by a source since removed or renamed) could otherwise be linked
+    in and their weak kernel symbols win over the current ones."""
+    current = {src.replace(".hip", ".o") for src in sources}
+    removed = []
+    for name in sorted(os.listdir(objdir)):
+        if name.endswith(".o") and name not in current:
+            os.remove(os.path.join(objdir, name))
+            removed.append(name)
+    return removed
+
+
+def link_command(cc, objdir, out, sources=SOURCES):
+    """The link line: exactly the objects of `sources`, never a glob of `objdir`."""
+    objs = [os.path.join(objdir, src.replace(".hip", ".o")) for src in sources]
+    return [cc, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", out]
+
+
 def build(verbose=True):
     """Compile every HIP source (in parallel) and link paper_2203_14685_amd/libhetumoe.so."""
     from concurrent.futures import ThreadPoolExecutor
@@ -46,12 +65,7 @@ def build(verbose=True):
     t0 = time.time()
     objdir = os.path.join(PKG, "_build")
     os.makedirs(objdir, exist_ok=True)
-    # objects of sources no longer built would otherwise sit beside the current
-    # ones, and a link that globs the folder could pick up their kernels
-    current = {src.replace(".hip", ".o") for src in SOURCES}
-    for name in os.listdir(objdir):
-        if name.endswith(".o") and name not in current:
-            os.remove(os.path.join(objdir, name))
+    prune_stale_objects(objdir)
     jobs = []
     for src in SOURCES:
         obj = os.path.join(objdir, src.replace(".hip", ".o"))
@@ -69,7 +83,7 @@ def build(verbose=True):
             raise RuntimeError(f"hipcc failed on {cmd[-3]} with exit code {rc}")
         logs.append(out)
     tmp = LIB + ".tmp"
-    rc, out = _run([cc, "--offload-arch=gfx950", "-shared", "-fPIC", *[o for o, _ in jobs], "-o", tmp])
+    rc, out = _run(link_command(cc, objdir, tmp))
     if rc != 0:
         sys.stderr.write(out)
         raise RuntimeError(f"link failed with exit code {rc}")

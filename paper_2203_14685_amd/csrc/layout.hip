@@ -3,53 +3,54 @@
 // and results are bitwise reproducible.  Outputs indexed by token (combine,
 // dispatch backward) are gathers; outputs indexed by expert slot (dispatch,
 // combine backward) are gathers over slots for k = 1 and token-major scatters
-// for k > 1, so that each token row is read once.
+// for k > 1, so that each token row is read once from memory.
 //
-// Two row forms.  The flat form (the [E,C,d] gathers for k = 1, and the
-// token-order gathers for k <= 2 over rows of up to 2 KiB) gives every thread
-// one 16-byte chunk of the flattened output per step, two steps per thread, so
-// a block of 512 threads writes 16 KiB and lives briefly.  The wave form gives
-// one wavefront one output row, walked in 16-byte chunks (64 lanes x 16 B =
-// 1 KiB per instruction) with up to kUnroll loads per lane in flight before
-// the first store.  On MI355X many short-lived waves with few stores each kept
-// more writes in flight than long row walks (a 1 GiB fill: 6.8 TB/s with one
-// store per thread against 5.7 TB/s with eight), which is why the writers of
-// [E,C,d] use the flat form; the wave form stays where it measured faster
-// (token rows longer than 2 KiB, k >= 3, and the token-major scatters).
-// Every output row is written with non-temporal stores: the buffers are far
-// larger than the 256 MB Infinity Cache, and plain stores leave dirty lines there
-// whose write-back then slows whichever kernel runs next (measured: dispatch
-// after a plain-store producer ~25% slower than after a streaming one).  The
-// wave, short-row and token-major forms also read their source rows with
-// non-temporal loads (each row is read once; 2-7 % faster), the flat forms with
-// plain loads (1-2 % faster there).
+// The kernels are bound by HBM bandwidth, and on MI355X how a kernel writes
+// matters as much as how it reads (measured at the hash workload's shape,
+// 8 KiB rows, 1 GiB expert buffers, in pass order):
+// * Writers of [E,C,d] buffers larger than the Infinity Cache run in two
+//   phases of one launch: the first blocks write the empty slots' zero rows,
+//   the later blocks the copied rows.  Two pure streams (a fill, then a copy)
+//   beat one interleaved stream (dispatch 256 -> 236 us).
+// * Writers of token rows (combine, dispatch backward) give a row to a block
+//   of threads, one 16-byte chunk each, and store through buffer instructions
+//   with an explicit cache policy: rows with data non-temporal at every scope
+//   (sc0 sc1 nt), zero rows of tokens with nothing kept sc1 only, which lets
+//   those writes merge in the caches (combine 165 -> 156 us).  Plain stores of
+//   whole [E,C,d] buffers instead leave dirty lines behind that slow the next
+//   kernel, so those writers keep non-temporal stores.
+// * Row indices are made wave-uniform (readfirstlane) wherever a wave lies
+//   inside one row, so that routing comes through scalar loads and buffer
+//   resources sit in scalar registers; a per-lane resource would make the
+//   compiler loop over the lanes' distinct values.
+// Source rows are read with non-temporal loads: each is read once.
 #include "common.hpp"
 #include "kernels.hpp"
 
 namespace hetumoe {
 
 constexpr int kUnroll = 8;
-// Waves per block, one row per wave.  Large blocks measured faster on MI355X for
-// these gathers (16 waves for the [E,C,d] writers); the combine kernels keep 4
-// so that their fp32 accumulators fit the register budget without spilling.
-constexpr int kWideWaves = 16;
-constexpr int kCombineWaves = 4;
+constexpr int kWideWaves = 16;  // token-major dispatch: one token per wave, 16 waves per block
 // The token-major combine backward with dw holds ~126 VGPRs, four waves per
 // SIMD: 16-wave blocks would run one at a time per CU.  Blocks of 8 balance
 // small batches better (workload of 8192 tokens, k = 2: 20.5 -> 18.5 us).
 constexpr int kBwdScatterWaves = 8;
 
-__device__ __forceinline__ void store_nt(u32x4* p, const u32x4& v) { __builtin_nontemporal_store(v, p); }
+// Row kernels: kRowThreads threads, one 16-byte chunk each per step.
+constexpr int kRowThreads = 512;
+constexpr int kRowWaves = kRowThreads / kWave;
 
-// ---------------------------------------------------------------- flat form
-constexpr int kFlatThreads = 512;
-constexpr int kFlatPer = 2;                          // chunks per thread
-constexpr int kFlatChunks = kFlatThreads * kFlatPer;  // chunks per block
-constexpr int kFlatWaves = kFlatThreads / kWave;
+// Cache-policy bits of gfx950's buffer instructions (sc0 = 1, nt = 2, sc1 = 16)
+// and word 3 of a raw buffer resource of 32-bit elements (gfx9 family).
+constexpr int kPolDataRow = 1 | 2 | 16;
+constexpr int kPolZeroRow = 16;
+constexpr int kRsrcWord3 = 0x00020000;
+
+__device__ __forceinline__ void store_nt(u32x4* p, const u32x4& v) { __builtin_nontemporal_store(v, p); }
+__device__ __forceinline__ u32x4 load_nt(const u32x4* p) { return __builtin_nontemporal_load(p); }
 
 // Row and column of chunk gb + off of a flattened [rows, nch] output, where gb
-// is the block's first chunk (row_b, col_b precomputed) and off < kFlatChunks.
-// POW2: nch = 1 << lg.
+// is the block's first chunk (row_b, col_b precomputed).  POW2: nch = 1 << lg.
 template <bool POW2>
 __device__ __forceinline__ void flat_pos(int64_t gb, int64_t row_b, int col_b, int off, int nch, int lg, int64_t& row,
                                          int& col) {
@@ -65,218 +66,123 @@ __device__ __forceinline__ void flat_pos(int64_t gb, int64_t row_b, int col_b, i
   }
 }
 
-// ---------------------------------------------------------------- dispatch
-// xe[row] = x[slot_src[row] / k], or zeros for an empty slot.  Flat form for
-// k = 1 (k > 1 uses the token-major scatter further down).
-template <bool POW2>
-__global__ __launch_bounds__(kFlatThreads) void dispatch_flat_kernel(RowArgs a, int lg, int64_t total) {
-  const int nch = a.nch;
-  const int64_t gb = static_cast<int64_t>(blockIdx.x) * kFlatChunks;
+// Buffer-resource helpers.  A resource must sit in scalar registers, so every
+// base passed here is uniform over the wave (the block's first chunk, or a
+// row index made uniform with readfirstlane where a wave lies inside one row).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* p, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), 0, bytes, kRsrcWord3);
+}
+__device__ __forceinline__ u32x4 buf_load_nt(__amdgpu_buffer_rsrc_t r, int off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 2);
+}
+__device__ __forceinline__ void buf_store_nt(const u32x4& v, __amdgpu_buffer_rsrc_t r, int off) {
+  __builtin_amdgcn_raw_buffer_store_b128(v, r, off, 0, 2);
+}
+
+// ---------------------------------------------------------------- [E,C,d] writers, k = 1
+// xe[row] = x[slot_src[row]] (dispatch) or dye[row] = w[src] * dy[src] with,
+// under DW, dw[src] = <dy[src], ye[row]> (combine backward); zeros for an empty
+// slot.  TWO (buffers larger than the 256 MB Infinity Cache): blocks [0, nb)
+// take the zero rows of their 512 chunks, blocks [nb, 2 nb) the copied rows of
+// the same chunks; otherwise each block takes both kinds of its chunks (a
+// buffer the cache holds measured faster written in one pass: workload of
+// 32768 tokens at 4 KiB rows, dispatch 38.9 -> 33.3 us).  Blocks past the row
+// blocks clear dw of dropped choices.  WR (rows a multiple of 64 chunks): every wave lies inside
+// one row, whose index, source and branches are then wave-uniform (scalar
+// loads of slot_src, buffer resources per row).  With DW a row is a power of
+// two of 64 to 512 chunks, so every row lies inside one block: each wave sums
+// its part of the dot product, one thread per row adds its waves' parts in
+// order.
+template <typename T, bool SCALE, bool DW, bool POW2, bool WR, bool TWO>
+__global__ __launch_bounds__(kRowThreads) void slot_rows_kernel(RowArgs a, int lg, int64_t total, int64_t nb) {
+  constexpr int kEl = Chunk<T>::kElems;
+  const int nch = a.nch, S = a.S;
+  const int32_t* slot_src = a.slot_src;
+  const u32x4* srcp = reinterpret_cast<const u32x4*>(a.src);
+  u32x4* dstp = reinterpret_cast<u32x4*>(a.dst);
+  const float* wts = a.weights;
+  const int64_t bid = blockIdx.x;
+  const int64_t row_grid = TWO ? 2 * nb : nb;
+  if (bid >= row_grid) {
+    if constexpr (DW) {
+      const int64_t i = (bid - row_grid) * kRowThreads + threadIdx.x;
+      if (i < a.S && a.slots[i] < 0) a.dw[i] = 0.f;
+    }
+    return;
+  }
+  const bool full_phase = !TWO || bid >= nb;
+  const int64_t gb = (TWO && full_phase ? bid - nb : bid) * kRowThreads;
   const int64_t row_b = POW2 ? 0 : gb / nch;
   const int col_b = POW2 ? 0 : static_cast<int>(gb - row_b * nch);
-  const u32x4* x = reinterpret_cast<const u32x4*>(a.src);
-  u32x4* xe = reinterpret_cast<u32x4*>(a.dst);
-  u32x4 v[kFlatPer];
-#pragma unroll
-  for (int u = 0; u < kFlatPer; ++u) {
-    const int off = u * kFlatThreads + static_cast<int>(threadIdx.x);
-    int64_t row;
-    int col;
-    flat_pos<POW2>(gb, row_b, col_b, off, nch, lg, row, col);
-    // entries outside [0, S) are out of contract and treated as empty slots
-    const int src = gb + off < total ? a.slot_src[row] : -1;
-    v[u] = u32x4{0u, 0u, 0u, 0u};
-    if (src >= 0 && src < a.S) v[u] = x[static_cast<int64_t>(src) * nch + col];
-  }
-#pragma unroll
-  for (int u = 0; u < kFlatPer; ++u) {
-    const int64_t g = gb + u * kFlatThreads + static_cast<int>(threadIdx.x);
-    if (g < total) store_nt(xe + g, v[u]);
-  }
-}
-
-// ---------------------------------------------------------------- combine
-// y[s] = sum_{r kept} w[s,r] * ye[ids[s,r], slots[s,r]]  (WEIGHTED)
-// dx[s] = sum_{r kept} dxe[ids[s,r], slots[s,r]]        (!WEIGHTED)
-// fp32 accumulation in r order, one rounding to T.
-template <typename T, bool WEIGHTED>
-__global__ __launch_bounds__(kCombineWaves * kWave) void combine_kernel(RowArgs a) {
-  constexpr int kEl = Chunk<T>::kElems;
-  const int64_t s = static_cast<int64_t>(blockIdx.x) * kCombineWaves + threadIdx.x / kWave;
-  if (s >= a.rows) return;
-  const int lane = lane_id();
-  const int nch = a.nch, k = a.k;
-  const u32x4* ye = reinterpret_cast<const u32x4*>(a.src);
-  u32x4* out = reinterpret_cast<u32x4*>(a.dst) + s * nch;
-  for (int base = 0; base < nch; base += kWave * kUnroll) {
-    float acc[kUnroll][kEl];
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u)
-#pragma unroll
-      for (int q = 0; q < kEl; ++q) acc[u][q] = 0.f;
-    for (int r = 0; r < k; ++r) {
-      const int slot = a.slots[s * k + r];
-      const int e = a.ids[s * k + r];
-      // dropped choices (slot -1) and out-of-contract entries contribute nothing
-      if (slot < 0 || slot >= a.C || e < 0 || e >= a.E) continue;
-      const float w = WEIGHTED ? a.weights[s * k + r] : 1.f;
-      const u32x4* srow = ye + (static_cast<int64_t>(e) * a.C + slot) * nch;
-      u32x4 v[kUnroll];
-#pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        const int i = base + u * kWave + lane;
-        // each source row is read once: streaming loads, as in the short and
-        // token-major forms (the flat forms measured slower with them)
-        if (i < nch) v[u] = __builtin_nontemporal_load(&srow[i]);
-      }
-#pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        const int i = base + u * kWave + lane;
-        if (i < nch) {
-          float f[kEl];
-          Chunk<T>::unpack(v[u], f);
-#pragma unroll
-          for (int q = 0; q < kEl; ++q) acc[u][q] = WEIGHTED ? fmaf(w, f[q], acc[u][q]) : acc[u][q] + f[q];
-        }
-      }
+  int64_t row;
+  int col;
+  flat_pos<POW2>(gb, row_b, col_b, static_cast<int>(threadIdx.x), nch, lg, row, col);
+  if constexpr (WR) row = __builtin_amdgcn_readfirstlane(static_cast<int>(row));  // rows < 2^31
+  const int64_t g = gb + threadIdx.x;
+  const bool in = g < total;  // wave-uniform under WR (total is a multiple of 64)
+  // entries outside [0, S) are out of contract and treated as empty slots
+  const int src = in ? slot_src[row] : -1;
+  const bool full = (src >= 0) & (src < S);
+  float dot = 0.f;
+  if (in && (!TWO || full == full_phase)) {
+    u32x4 v = u32x4{0u, 0u, 0u, 0u};
+    float w = 0.f;
+    if (full) {
+      const u32x4* srow = srcp + static_cast<int64_t>(src) * nch;
+      if constexpr (WR) v = buf_load_nt(buf_rsrc(srow, nch * 16), col * 16);
+      else v = load_nt(srow + col);
+      if constexpr (SCALE) w = wts[src];
     }
-#pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const int i = base + u * kWave + lane;
-      if (i < nch) store_nt(out + i, Chunk<T>::pack(acc[u]));
-    }
-  }
-}
-
-// Short rows (CPR x 64 chunks per row, CPR in {1, 2, 4}): one wave takes
-// RPW = 8 / CPR tokens so that every lane still has 8 loads in flight.  All of
-// a rank's slot, id and weight reads come first; the row loads are then issued
-// unconditionally (a dropped choice reads row 0 of the expert buffer, which
-// needs E * C > 0, and its value is discarded), so no load waits behind a
-// branch on another load's result.
-template <typename T, bool WEIGHTED, int CPR>
-__global__ __launch_bounds__(kCombineWaves * kWave) void combine_short_kernel(RowArgs a) {
-  constexpr int kEl = Chunk<T>::kElems;
-  constexpr int RPW = 8 / CPR;
-  constexpr int nch = CPR * kWave;
-  const int64_t s0 = (static_cast<int64_t>(blockIdx.x) * kCombineWaves + threadIdx.x / kWave) * RPW;
-  if (s0 >= a.rows) return;
-  const int lane = lane_id();
-  const int k = a.k;
-  const u32x4* ye = reinterpret_cast<const u32x4*>(a.src);
-  u32x4* out = reinterpret_cast<u32x4*>(a.dst);
-  float acc[8][kEl];
-#pragma unroll
-  for (int u = 0; u < 8; ++u)
-#pragma unroll
-    for (int q = 0; q < kEl; ++q) acc[u][q] = 0.f;
-  for (int r = 0; r < k; ++r) {
-    int64_t rowoff[RPW];
-    float w[RPW];
-    bool ok[RPW];
-#pragma unroll
-    for (int t = 0; t < RPW; ++t) {
-      const int64_t s = min(s0 + t, a.rows - 1);
-      const int slot = a.slots[s * k + r];
-      const int e = a.ids[s * k + r];
-      w[t] = WEIGHTED ? a.weights[s * k + r] : 1.f;
-      ok[t] = (s0 + t < a.rows) && slot >= 0 && slot < a.C && e >= 0 && e < a.E;
-      rowoff[t] = ok[t] ? (static_cast<int64_t>(e) * a.C + slot) * nch : 0;
-    }
-    u32x4 v[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) v[u] = __builtin_nontemporal_load(&ye[rowoff[u / CPR] + (u % CPR) * kWave + lane]);
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      if (ok[u / CPR]) {
+    if constexpr (SCALE) {
+      if (full) {
         float f[kEl];
-        Chunk<T>::unpack(v[u], f);
+        Chunk<T>::unpack(v, f);
+        if constexpr (DW) {
+          float gq[kEl];
+          const u32x4* yb = reinterpret_cast<const u32x4*>(a.aux) + gb;
+          Chunk<T>::unpack(WR ? buf_load_nt(buf_rsrc(yb, kRowThreads * 16), threadIdx.x * 16) : load_nt(yb + threadIdx.x), gq);
 #pragma unroll
-        for (int q = 0; q < kEl; ++q)
-          acc[u][q] = WEIGHTED ? fmaf(w[u / CPR], f[q], acc[u][q]) : acc[u][q] + f[q];
+          for (int q = 0; q < kEl; ++q) dot = fmaf(f[q], gq[q], dot);
+        }
+#pragma unroll
+        for (int q = 0; q < kEl; ++q) f[q] *= w;
+        v = Chunk<T>::pack(f);
+      }
+    }
+    u32x4* db = dstp + gb;
+    if constexpr (WR) buf_store_nt(v, buf_rsrc(db, kRowThreads * 16), threadIdx.x * 16);
+    else store_nt(db + threadIdx.x, v);
+  }
+  if constexpr (DW) {
+    if (!full_phase) return;  // uniform over the block
+    __shared__ float part[kRowWaves];
+    const float t = wave_sum(dot);
+    if (lane_id() == 0) part[threadIdx.x / kWave] = t;
+    __syncthreads();
+    const int rows_here = kRowThreads >> lg;
+    const int parts = nch / kWave;
+    if (static_cast<int>(threadIdx.x) < rows_here) {
+      const int64_t r = (gb >> lg) + threadIdx.x;
+      if (r < a.rows) {
+        float sum = 0.f;
+        for (int j = 0; j < parts; ++j) sum += part[threadIdx.x * parts + j];
+        const int s2 = a.slot_src[r];
+        if (s2 >= 0 && s2 < a.S) a.dw[s2] = sum;
       }
     }
   }
-#pragma unroll
-  for (int u = 0; u < 8; ++u) {
-    const int64_t s = s0 + u / CPR;
-    if (s < a.rows) store_nt(out + s * nch + (u % CPR) * kWave + lane, Chunk<T>::pack(acc[u]));
-  }
 }
 
-// Flat form of the two above for k <= KMAX <= 2: each thread combines one
-// 16-byte chunk of a token row per step.  Every load of both steps is issued
-// before the first store: vector loads and stores retire in order on one
-// counter, so a store between two loads makes the second wait for it
-// (measured at 2 KiB rows, k = 2: 14.1 -> 13.3 us).  At 4 and 8 KiB rows
-// with k = 1 this form, run alone, beat the wave forms (31.0 against 39.4 us,
-// 157 against 160 us), but was slower in the pass, right after the dispatch's
-// streaming stores (51.7 against 43.6 us, 176.9 against 164.6 us).
-template <typename T, bool POW2, bool WEIGHTED, int KMAX>
-__global__ __launch_bounds__(kFlatThreads) void combine_flat_kernel(RowArgs a, int lg, int64_t total) {
-  constexpr int kEl = Chunk<T>::kElems;
-  const int nch = a.nch, k = a.k;
-  const int64_t gb = static_cast<int64_t>(blockIdx.x) * kFlatChunks;
-  const int64_t row_b = POW2 ? 0 : gb / nch;
-  const int col_b = POW2 ? 0 : static_cast<int>(gb - row_b * nch);
-  const u32x4* ye = reinterpret_cast<const u32x4*>(a.src);
-  u32x4* out = reinterpret_cast<u32x4*>(a.dst);
-  u32x4 v[kFlatPer][KMAX];
-  float w[kFlatPer][KMAX];
-  bool ok[kFlatPer][KMAX];
-#pragma unroll
-  for (int u = 0; u < kFlatPer; ++u) {
-    const int off = u * kFlatThreads + static_cast<int>(threadIdx.x);
-    const bool in = gb + off < total;
-    int64_t s;
-    int col;
-    flat_pos<POW2>(gb, row_b, col_b, off, nch, lg, s, col);
-#pragma unroll
-    for (int r = 0; r < KMAX; ++r) {
-      ok[u][r] = false;
-      w[u][r] = 1.f;
-      v[u][r] = u32x4{0u, 0u, 0u, 0u};
-      if (in && r < k) {
-        const int slot = a.slots[s * k + r];
-        const int e = a.ids[s * k + r];
-        // dropped choices (slot -1) and out-of-contract entries contribute nothing
-        ok[u][r] = slot >= 0 && slot < a.C && e >= 0 && e < a.E;
-        if (WEIGHTED) w[u][r] = a.weights[s * k + r];
-        if (ok[u][r]) v[u][r] = ye[(static_cast<int64_t>(e) * a.C + slot) * nch + col];
-      }
-    }
-  }
-#pragma unroll
-  for (int u = 0; u < kFlatPer; ++u) {
-    const int off = u * kFlatThreads + static_cast<int>(threadIdx.x);
-    if (gb + off >= total) continue;
-    float acc[kEl];
-#pragma unroll
-    for (int q = 0; q < kEl; ++q) acc[q] = 0.f;
-#pragma unroll
-    for (int r = 0; r < KMAX; ++r) {
-      if (!ok[u][r]) continue;
-      float f[kEl];
-      Chunk<T>::unpack(v[u][r], f);
-#pragma unroll
-      for (int q = 0; q < kEl; ++q) acc[q] = WEIGHTED ? fmaf(w[u][r], f[q], acc[q]) : acc[q] + f[q];
-    }
-    store_nt(out + gb + off, Chunk<T>::pack(acc));
-  }
-}
-
-// ---------------------------------------------------------------- combine backward
-// Rows [0, rows): dye[row] = w[src] * dy[src / k] (zeros for an empty slot) and,
-// with DW, dw[src] = <dy[src / k], ye[row]>.  Blocks past the row blocks clear
-// dw of dropped choices.
-template <typename T, bool DW>
-__global__ __launch_bounds__(kWideWaves * kWave) void combine_bwd_kernel(RowArgs a, int64_t row_blocks) {
+// Combine backward with dw for k = 1 on rows slot_rows_kernel does not take
+// (not a power of two, or longer than 512 chunks): one wave per row, kUnroll
+// chunks per lane in flight.  Blocks past the row blocks clear dw of dropped
+// choices.
+template <typename T>
+__global__ __launch_bounds__(kWideWaves * kWave) void combine_bwd_wave_kernel(RowArgs a, int64_t row_blocks) {
   constexpr int kEl = Chunk<T>::kElems;
   if (static_cast<int64_t>(blockIdx.x) >= row_blocks) {
-    if constexpr (DW) {
-      const int64_t i = (static_cast<int64_t>(blockIdx.x) - row_blocks) * (kWideWaves * kWave) + threadIdx.x;
-      if (i < static_cast<int64_t>(a.S) * a.k && a.slots[i] < 0) a.dw[i] = 0.f;
-    }
+    const int64_t i = (static_cast<int64_t>(blockIdx.x) - row_blocks) * (kWideWaves * kWave) + threadIdx.x;
+    if (i < static_cast<int64_t>(a.S) * a.k && a.slots[i] < 0) a.dw[i] = 0.f;
     return;
   }
   const int64_t row = static_cast<int64_t>(blockIdx.x) * kWideWaves + threadIdx.x / kWave;
@@ -286,8 +192,7 @@ __global__ __launch_bounds__(kWideWaves * kWave) void combine_bwd_kernel(RowArgs
   const int src = a.slot_src[row];
   u32x4* dst = reinterpret_cast<u32x4*>(a.dst) + row * nch;
   if (src < 0 || src >= a.S * a.k) {  // empty (or out-of-contract) slot
-    const u32x4 z = {0u, 0u, 0u, 0u};
-    for (int i = lane; i < nch; i += kWave) store_nt(dst + i, z);
+    for (int i = lane; i < nch; i += kWave) store_nt(dst + i, u32x4{0u, 0u, 0u, 0u});
     return;
   }
   const float w = a.weights[src];
@@ -295,125 +200,111 @@ __global__ __launch_bounds__(kWideWaves * kWave) void combine_bwd_kernel(RowArgs
   const u32x4* yerow = reinterpret_cast<const u32x4*>(a.aux) + row * nch;
   float dot = 0.f;
   for (int base = 0; base < nch; base += kWave * kUnroll) {
-    u32x4 v[kUnroll];
-    u32x4 ve[DW ? kUnroll : 1];
+    u32x4 v[kUnroll], ve[kUnroll];
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       const int i = base + u * kWave + lane;
       if (i < nch) {
-        v[u] = dyrow[i];
-        if constexpr (DW) ve[u] = yerow[i];
+        v[u] = load_nt(dyrow + i);
+        ve[u] = load_nt(yerow + i);
       }
     }
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       const int i = base + u * kWave + lane;
       if (i < nch) {
-        float f[kEl];
+        float f[kEl], g[kEl];
         Chunk<T>::unpack(v[u], f);
-        if constexpr (DW) {
-          float g[kEl];
-          Chunk<T>::unpack(ve[u], g);
+        Chunk<T>::unpack(ve[u], g);
 #pragma unroll
-          for (int q = 0; q < kEl; ++q) dot = fmaf(f[q], g[q], dot);
-        }
+        for (int q = 0; q < kEl; ++q) dot = fmaf(f[q], g[q], dot);
 #pragma unroll
         for (int q = 0; q < kEl; ++q) f[q] *= w;
         store_nt(dst + i, Chunk<T>::pack(f));
       }
     }
   }
-  if constexpr (DW) {
-    dot = wave_sum(dot);
-    if (lane == 0) a.dw[src] = dot;
-  }
+  dot = wave_sum(dot);
+  if (lane == 0) a.dw[src] = dot;
 }
 
-// Flat form of the kernel above for k = 1.  With DW the row length must be a
-// power of two between 64 chunks (one wave) and kFlatChunks, so that every
-// wave lies inside one row and every row inside one block: each wave sums its
-// part of <dy, ye>, and one thread per row adds the parts of its waves in
-// order.  Blocks past the row blocks clear dw of dropped choices.
-template <typename T, bool POW2, bool DW>
-__global__ __launch_bounds__(kFlatThreads) void combine_bwd_flat_kernel(RowArgs a, int lg, int64_t total,
-                                                                        int64_t row_blocks) {
+// ---------------------------------------------------------------- token rows: combine, dispatch backward
+// y[s] = sum_{r kept} w[s,r] * ye[ids[s,r], slots[s,r]]  (WEIGHTED)
+// dx[s] = sum_{r kept} dxe[ids[s,r], slots[s,r]]        (!WEIGHTED)
+// fp32 accumulation in r order, one rounding to T.  A block takes rpb rows of
+// tpr threads (tpr = nch for rows of up to 512 chunks, else 512 threads
+// walking the row); a thread loads the chunk of every kept choice before it
+// sums them (CPT chunks each, tpr * CPT chunks per row and step: with several
+// choices, more loads in flight).  WR (tpr a multiple of 64): the token of a wave is uniform, its
+// routing comes through scalar loads, and the row is stored through a buffer
+// resource with the cache policy of its kind: kPolDataRow, or kPolZeroRow for
+// a token with nothing kept.
+template <typename T, bool WEIGHTED, int KMAX, bool WR, int CPT>
+__global__ __launch_bounds__(kRowThreads) void token_rows_kernel(RowArgs a, int tpr, int rpb) {
   constexpr int kEl = Chunk<T>::kElems;
-  if (static_cast<int64_t>(blockIdx.x) >= row_blocks) {
-    if constexpr (DW) {
-      const int64_t i = (static_cast<int64_t>(blockIdx.x) - row_blocks) * kFlatThreads + threadIdx.x;
-      if (i < a.S && a.slots[i] < 0) a.dw[i] = 0.f;
-    }
-    return;
-  }
+  const int rl = static_cast<int>(threadIdx.x) / tpr;
+  int64_t s = static_cast<int64_t>(blockIdx.x) * rpb + rl;
+  if constexpr (WR) s = __builtin_amdgcn_readfirstlane(static_cast<int>(s));  // rows < 2^31
+  if (rl >= rpb || s >= a.rows) return;
   const int nch = a.nch;
-  const int64_t gb = static_cast<int64_t>(blockIdx.x) * kFlatChunks;
-  const int64_t row_b = POW2 ? 0 : gb / nch;
-  const int col_b = POW2 ? 0 : static_cast<int>(gb - row_b * nch);
-  const u32x4* dy = reinterpret_cast<const u32x4*>(a.src);
-  const u32x4* ye = reinterpret_cast<const u32x4*>(a.aux);
-  u32x4* dye = reinterpret_cast<u32x4*>(a.dst);
-  u32x4 v[kFlatPer];
-  u32x4 ve[DW ? kFlatPer : 1];
-  float w[kFlatPer];
-  bool ok[kFlatPer];
+  const int k = KMAX <= 2 ? KMAX : a.k;  // the launcher picks KMAX = k for k <= 2
+  const u32x4* src = reinterpret_cast<const u32x4*>(a.src);
+  // every routing value is loaded before any is tested, so that the loads
+  // overlap (a short-circuit test would make each wait for the one before)
+  int slot[KMAX], e[KMAX];
+  float w[KMAX];
 #pragma unroll
-  for (int u = 0; u < kFlatPer; ++u) {
-    const int off = u * kFlatThreads + static_cast<int>(threadIdx.x);
-    int64_t row;
-    int col;
-    flat_pos<POW2>(gb, row_b, col_b, off, nch, lg, row, col);
-    // entries outside [0, S) are out of contract and treated as empty slots
-    const int src = gb + off < total ? a.slot_src[row] : -1;
-    ok[u] = src >= 0 && src < a.S;
-    v[u] = u32x4{0u, 0u, 0u, 0u};
-    w[u] = 0.f;
-    if constexpr (DW) ve[u] = u32x4{0u, 0u, 0u, 0u};
-    if (ok[u]) {
-      v[u] = dy[static_cast<int64_t>(src) * nch + col];
-      w[u] = a.weights[src];
-      if constexpr (DW) ve[u] = ye[gb + off];
-    }
+  for (int r = 0; r < KMAX; ++r) {
+    const bool have = r < k;
+    slot[r] = have ? a.slots[s * k + r] : -1;
+    e[r] = have ? a.ids[s * k + r] : 0;
+    w[r] = (WEIGHTED && have) ? a.weights[s * k + r] : 1.f;
   }
-  float dot[kFlatPer];
+  int64_t off[KMAX];
+  bool ok[KMAX];
+  bool any = false;
 #pragma unroll
-  for (int u = 0; u < kFlatPer; ++u) {
-    const int64_t g = gb + u * kFlatThreads + static_cast<int>(threadIdx.x);
-    dot[u] = 0.f;
-    if (g >= total) continue;
-    if (!ok[u]) {  // empty slot: zeros, no arithmetic
-      store_nt(dye + g, u32x4{0u, 0u, 0u, 0u});
-      continue;
-    }
-    float f[kEl];
-    Chunk<T>::unpack(v[u], f);
-    if constexpr (DW) {
-      float gq[kEl];
-      Chunk<T>::unpack(ve[u], gq);
-#pragma unroll
-      for (int q = 0; q < kEl; ++q) dot[u] = fmaf(f[q], gq[q], dot[u]);
-    }
-#pragma unroll
-    for (int q = 0; q < kEl; ++q) f[q] *= w[u];
-    store_nt(dye + g, Chunk<T>::pack(f));
+  for (int r = 0; r < KMAX; ++r) {
+    // dropped choices (slot -1) and out-of-contract entries contribute nothing
+    ok[r] = (slot[r] >= 0) & (slot[r] < a.C) & (e[r] >= 0) & (e[r] < a.E);
+    off[r] = ok[r] ? (static_cast<int64_t>(e[r]) * a.C + slot[r]) * nch : 0;
+    any = any | ok[r];
   }
-  if constexpr (DW) {
-    __shared__ float part[kFlatPer * kFlatWaves];  // [u][wave]: chunk offset / 64
-    const int wave = threadIdx.x / kWave;
+  u32x4* orow = reinterpret_cast<u32x4*>(a.dst) + s * nch;
+  const __amdgpu_buffer_rsrc_t out = buf_rsrc(orow, nch * 16);
+  for (int c0 = static_cast<int>(threadIdx.x) - rl * tpr; c0 < nch; c0 += tpr * CPT) {
+    u32x4 v[CPT][KMAX];
 #pragma unroll
-    for (int u = 0; u < kFlatPer; ++u) {
-      const float t = wave_sum(dot[u]);
-      if (lane_id() == 0) part[u * kFlatWaves + wave] = t;
+    for (int u = 0; u < CPT; ++u) {
+      const int c = c0 + u * tpr;
+#pragma unroll
+      for (int r = 0; r < KMAX; ++r) {
+        if (!ok[r] || c >= nch) continue;
+        if constexpr (WR) v[u][r] = buf_load_nt(buf_rsrc(src + off[r], nch * 16), c * 16);
+        else v[u][r] = load_nt(src + off[r] + c);
+      }
     }
-    __syncthreads();
-    const int rows_here = kFlatChunks >> lg;
-    const int parts = nch / kWave;
-    if (static_cast<int>(threadIdx.x) < rows_here) {
-      const int64_t row = (gb >> lg) + threadIdx.x;
-      if (row < a.rows) {
-        float t = 0.f;
-        for (int j = 0; j < parts; ++j) t += part[threadIdx.x * parts + j];
-        const int src = a.slot_src[row];
-        if (src >= 0 && src < a.S) a.dw[src] = t;
+#pragma unroll
+    for (int u = 0; u < CPT; ++u) {
+      const int c = c0 + u * tpr;
+      if (c >= nch) continue;
+      float acc[kEl];
+#pragma unroll
+      for (int q = 0; q < kEl; ++q) acc[q] = 0.f;
+#pragma unroll
+      for (int r = 0; r < KMAX; ++r) {
+        if (!ok[r]) continue;
+        float f[kEl];
+        Chunk<T>::unpack(v[u][r], f);
+#pragma unroll
+        for (int q = 0; q < kEl; ++q) acc[q] = WEIGHTED ? fmaf(w[r], f[q], acc[q]) : acc[q] + f[q];
+      }
+      const u32x4 o = Chunk<T>::pack(acc);
+      if constexpr (WR) {
+        if (any) __builtin_amdgcn_raw_buffer_store_b128(o, out, c * 16, 0, kPolDataRow);
+        else __builtin_amdgcn_raw_buffer_store_b128(o, out, c * 16, 0, kPolZeroRow);
+      } else {
+        store_nt(orow + c, o);
       }
     }
   }
@@ -455,7 +346,7 @@ __global__ __launch_bounds__(kWideWaves * kWave) void dispatch_scatter_kernel(Ro
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       const int i = base + u * kWave + lane;
-      if (i < nch) v[u] = __builtin_nontemporal_load(&srow[i]);
+      if (i < nch) v[u] = load_nt(srow + i);
     }
     for (int r = 0; r < k; ++r) {
       const int slot = a.slots[s * k + r];
@@ -499,7 +390,7 @@ __global__ __launch_bounds__(kBwdScatterWaves * kWave) void combine_bwd_scatter_
 #pragma unroll
     for (int u = 0; u < kU; ++u) {
       const int i = base + u * kWave + lane;
-      if (i < nch) v[u] = __builtin_nontemporal_load(&dyrow[i]);
+      if (i < nch) v[u] = load_nt(dyrow + i);
     }
 #pragma unroll
     for (int r0 = 0; r0 < 8; r0 += kRG) {
@@ -519,7 +410,7 @@ __global__ __launch_bounds__(kBwdScatterWaves * kWave) void combine_bwd_scatter_
 #pragma unroll
           for (int u = 0; u < kU; ++u) {
             const int i = base + u * kWave + lane;
-            if (kept[j] && i < nch) ve[j][u] = __builtin_nontemporal_load(&yerow[i]);
+            if (kept[j] && i < nch) ve[j][u] = load_nt(yerow + i);
           }
         }
       }
@@ -559,16 +450,6 @@ __global__ __launch_bounds__(kBwdScatterWaves * kWave) void combine_bwd_scatter_
 }
 
 // ---------------------------------------------------------------- launchers
-static inline unsigned blocks_for_rows(int64_t rows, int waves) {
-  return static_cast<unsigned>((rows + waves - 1) / waves);
-}
-
-static unsigned zero_blocks(int64_t rows, int waves = kWideWaves) {
-  const int64_t b = (rows + waves - 1) / waves;
-  const int64_t cap = static_cast<int64_t>(kZeroBlocks) * kWideWaves / waves;
-  return static_cast<unsigned>(b < cap ? b : cap);
-}
-
 // log2(n) for a power of two, else -1
 static inline int pow2_log(int n) {
   if (n <= 0 || (n & (n - 1)) != 0) return -1;
@@ -577,136 +458,124 @@ static inline int pow2_log(int n) {
   return lg;
 }
 
-static inline unsigned flat_blocks(int64_t total) {
-  return static_cast<unsigned>((total + kFlatChunks - 1) / kFlatChunks);
+static inline int64_t row_blocks(int64_t total) { return (total + kRowThreads - 1) / kRowThreads; }
+
+// Output size above which the [E,C,d] writers run in two phases (the Infinity
+// Cache of MI355X holds 256 MB).
+constexpr int64_t kTwoPhaseBytes = int64_t(256) << 20;
+
+template <typename T, bool SCALE, bool DW, bool TWO>
+static void launch_slot_rows_t(const RowArgs& a, int64_t total, int64_t nb, hipStream_t st) {
+  const int64_t dwb = DW ? (static_cast<int64_t>(a.S) + kRowThreads - 1) / kRowThreads : 0;
+  const unsigned grid = static_cast<unsigned>((TWO ? 2 * nb : nb) + dwb);
+  if (grid == 0) return;
+  const int lg = pow2_log(a.nch);
+  const dim3 g(grid), block(kRowThreads);
+  if (a.nch % kWave == 0) {
+    if (lg >= 0) slot_rows_kernel<T, SCALE, DW, true, true, TWO><<<g, block, 0, st>>>(a, lg, total, nb);
+    else slot_rows_kernel<T, SCALE, DW, false, true, TWO><<<g, block, 0, st>>>(a, lg, total, nb);
+  } else {
+    if (lg >= 0) slot_rows_kernel<T, SCALE, DW, true, false, TWO><<<g, block, 0, st>>>(a, lg, total, nb);
+    else slot_rows_kernel<T, SCALE, DW, false, false, TWO><<<g, block, 0, st>>>(a, lg, total, nb);
+  }
+}
+
+template <typename T, bool SCALE, bool DW>
+static void launch_slot_rows(const RowArgs& a, hipStream_t st) {
+  const int64_t total = a.rows * a.nch;
+  const int64_t nb = row_blocks(total);
+  if (total * 16 > kTwoPhaseBytes) launch_slot_rows_t<T, SCALE, DW, true>(a, total, nb, st);
+  else launch_slot_rows_t<T, SCALE, DW, false>(a, total, nb, st);
+}
+
+static unsigned zero_blocks(int64_t rows, int waves) {
+  const int64_t b = (rows + waves - 1) / waves;
+  const int64_t cap = static_cast<int64_t>(kZeroBlocks) * kWideWaves / waves;
+  return static_cast<unsigned>(b < cap ? b : cap);
 }
 
 hipError_t launch_dispatch(const RowArgs& a, hipStream_t st) {
   if (a.k > 1) {
     const int64_t tok_blocks = (static_cast<int64_t>(a.S) + kWideWaves - 1) / kWideWaves;
-    const unsigned grid = static_cast<unsigned>(tok_blocks) + zero_blocks(a.rows);
+    const unsigned grid = static_cast<unsigned>(tok_blocks) + zero_blocks(a.rows, kWideWaves);
     if (grid == 0) return hipSuccess;
     dispatch_scatter_kernel<<<dim3(grid), dim3(kWideWaves * kWave), 0, st>>>(a, tok_blocks);
     return hipGetLastError();
   }
-  const int64_t total = a.rows * a.nch;
-  if (total == 0) return hipSuccess;
-  const int lg = pow2_log(a.nch);
-  const dim3 grid(flat_blocks(total)), block(kFlatThreads);
-  if (lg >= 0) dispatch_flat_kernel<true><<<grid, block, 0, st>>>(a, lg, total);
-  else dispatch_flat_kernel<false><<<grid, block, 0, st>>>(a, lg, total);
+  // the element type is irrelevant to a bit copy
+  launch_slot_rows<float, false, false>(a, st);
   return hipGetLastError();
 }
 
+template <typename T, bool WEIGHTED, bool WR, int CPT>
+static void launch_token_rows_w(const RowArgs& a, int tpr, int rpb, hipStream_t st) {
+  const dim3 grid(static_cast<unsigned>((a.rows + rpb - 1) / rpb)), block(kRowThreads);
+  if (a.k == 1) token_rows_kernel<T, WEIGHTED, 1, WR, CPT><<<grid, block, 0, st>>>(a, tpr, rpb);
+  else if (a.k == 2) token_rows_kernel<T, WEIGHTED, 2, WR, CPT><<<grid, block, 0, st>>>(a, tpr, rpb);
+  else if (a.k <= 4) token_rows_kernel<T, WEIGHTED, 4, WR, CPT><<<grid, block, 0, st>>>(a, tpr, rpb);
+  else token_rows_kernel<T, WEIGHTED, 8, WR, CPT><<<grid, block, 0, st>>>(a, tpr, rpb);
+}
+
 template <typename T, bool WEIGHTED>
-static void launch_combine_short(const RowArgs& a, hipStream_t st) {
-  const int cpr = a.nch / kWave, rpw = 8 / cpr;
-  const dim3 grid(blocks_for_rows((a.rows + rpw - 1) / rpw, kCombineWaves)), block(kCombineWaves * kWave);
-  if (cpr == 1) combine_short_kernel<T, WEIGHTED, 1><<<grid, block, 0, st>>>(a);
-  else if (cpr == 2) combine_short_kernel<T, WEIGHTED, 2><<<grid, block, 0, st>>>(a);
-  else combine_short_kernel<T, WEIGHTED, 4><<<grid, block, 0, st>>>(a);
-}
-
-template <typename T, bool POW2, bool WEIGHTED>
-static void launch_combine_flat_t(const RowArgs& a, int lg, int64_t total, hipStream_t st) {
-  const dim3 grid(flat_blocks(total)), block(kFlatThreads);
-  if (a.k == 1) combine_flat_kernel<T, POW2, WEIGHTED, 1><<<grid, block, 0, st>>>(a, lg, total);
-  else combine_flat_kernel<T, POW2, WEIGHTED, 2><<<grid, block, 0, st>>>(a, lg, total);
-}
-
-template <typename T>
-static void launch_combine_flat(const RowArgs& a, bool weighted, hipStream_t st) {
-  const int64_t total = a.rows * a.nch;
-  const int lg = pow2_log(a.nch);
-  if (lg >= 0) {
-    if (weighted) launch_combine_flat_t<T, true, true>(a, lg, total, st);
-    else launch_combine_flat_t<T, true, false>(a, lg, total, st);
-  } else {
-    if (weighted) launch_combine_flat_t<T, false, true>(a, lg, total, st);
-    else launch_combine_flat_t<T, false, false>(a, lg, total, st);
-  }
+static void launch_token_rows_t(const RowArgs& a, hipStream_t st) {
+  // with three or more choices, two chunks per thread where rows split evenly
+  // into waves; otherwise one
+  const int cpt = (a.k >= 3 && a.nch % (2 * kWave) == 0) ? 2 : 1;
+  const int rt = a.nch / cpt;  // threads a row would take
+  const int tpr = rt <= kRowThreads ? rt : kRowThreads;
+  const int rpb = rt <= kRowThreads ? kRowThreads / rt : 1;
+  if (cpt == 2) launch_token_rows_w<T, WEIGHTED, true, 2>(a, tpr, rpb, st);
+  else if (tpr % kWave == 0) launch_token_rows_w<T, WEIGHTED, true, 1>(a, tpr, rpb, st);
+  else launch_token_rows_w<T, WEIGHTED, false, 1>(a, tpr, rpb, st);
 }
 
 hipError_t launch_combine(const RowArgs& a, bool weighted, hipStream_t st) {
   if (a.rows == 0 || a.nch == 0) return hipSuccess;
-  // k <= 2 over rows of up to 2 KiB: flat form (measured 7-15 % faster than
-  // the wave forms at 1 and 2 KiB rows; slower in the pass at 4 and 8 KiB rows,
-  // and slower at k = 4)
-  if (a.k <= 2 && a.nch <= 128) {
-    if (a.dtype == 1) launch_combine_flat<bf16_t>(a, weighted, st);
-    else launch_combine_flat<float>(a, weighted, st);
-    return hipGetLastError();
-  }
-  // short rows: several tokens per wave (measured 9-11 % faster at 2 and 4 KiB
-  // rows); longer rows: one token per wave
-  if ((a.nch == 64 || a.nch == 128 || a.nch == 256) && static_cast<int64_t>(a.E) * a.C > 0) {
-    if (a.dtype == 1) {
-      if (weighted) launch_combine_short<bf16_t, true>(a, st);
-      else launch_combine_short<bf16_t, false>(a, st);
-    } else {
-      if (weighted) launch_combine_short<float, true>(a, st);
-      else launch_combine_short<float, false>(a, st);
-    }
-    return hipGetLastError();
-  }
-  const dim3 grid(blocks_for_rows(a.rows, kCombineWaves)), block(kCombineWaves * kWave);
   if (a.dtype == 1) {
-    if (weighted) combine_kernel<bf16_t, true><<<grid, block, 0, st>>>(a);
-    else combine_kernel<bf16_t, false><<<grid, block, 0, st>>>(a);
+    if (weighted) launch_token_rows_t<bf16_t, true>(a, st);
+    else launch_token_rows_t<bf16_t, false>(a, st);
   } else {
-    if (weighted) combine_kernel<float, true><<<grid, block, 0, st>>>(a);
-    else combine_kernel<float, false><<<grid, block, 0, st>>>(a);
+    if (weighted) launch_token_rows_t<float, true>(a, st);
+    else launch_token_rows_t<float, false>(a, st);
   }
   return hipGetLastError();
 }
 
 hipError_t launch_combine_bwd(const RowArgs& a, hipStream_t st) {
-  constexpr int kThreads = kWideWaves * kWave;
   if (a.k > 1) {
     const int64_t tok_blocks = (static_cast<int64_t>(a.S) + kBwdScatterWaves - 1) / kBwdScatterWaves;
     const unsigned grid = static_cast<unsigned>(tok_blocks) + zero_blocks(a.rows, kBwdScatterWaves);
     if (grid == 0) return hipSuccess;
-    const dim3 block(kBwdScatterWaves * kWave);
+    const dim3 g(grid), block(kBwdScatterWaves * kWave);
     if (a.dtype == 1) {
-      if (a.dw) combine_bwd_scatter_kernel<bf16_t, true><<<dim3(grid), block, 0, st>>>(a, tok_blocks);
-      else combine_bwd_scatter_kernel<bf16_t, false><<<dim3(grid), block, 0, st>>>(a, tok_blocks);
+      if (a.dw) combine_bwd_scatter_kernel<bf16_t, true><<<g, block, 0, st>>>(a, tok_blocks);
+      else combine_bwd_scatter_kernel<bf16_t, false><<<g, block, 0, st>>>(a, tok_blocks);
     } else {
-      if (a.dw) combine_bwd_scatter_kernel<float, true><<<dim3(grid), block, 0, st>>>(a, tok_blocks);
-      else combine_bwd_scatter_kernel<float, false><<<dim3(grid), block, 0, st>>>(a, tok_blocks);
+      if (a.dw) combine_bwd_scatter_kernel<float, true><<<g, block, 0, st>>>(a, tok_blocks);
+      else combine_bwd_scatter_kernel<float, false><<<g, block, 0, st>>>(a, tok_blocks);
     }
     return hipGetLastError();
   }
-  // k = 1: flat form, with dw where a row is a power of two of 64 to
-  // kFlatChunks chunks (else the wave form below)
+  // k = 1: two-phase slot rows, with dw where a row is a power of two of 64 to
+  // 512 chunks (else one wave per row)
   const int lg = pow2_log(a.nch);
-  if (!a.dw || (lg >= 6 && a.nch <= kFlatChunks)) {
-    const int64_t total = a.rows * a.nch;
-    const int64_t row_blocks = flat_blocks(total);
-    const int64_t dw_blocks = a.dw ? (static_cast<int64_t>(a.S) + kFlatThreads - 1) / kFlatThreads : 0;
-    if (row_blocks + dw_blocks == 0) return hipSuccess;
-    const dim3 grid(static_cast<unsigned>(row_blocks + dw_blocks)), block(kFlatThreads);
-    if (a.dtype == 1) {
-      if (a.dw) combine_bwd_flat_kernel<bf16_t, true, true><<<grid, block, 0, st>>>(a, lg, total, row_blocks);
-      else if (lg >= 0) combine_bwd_flat_kernel<bf16_t, true, false><<<grid, block, 0, st>>>(a, lg, total, row_blocks);
-      else combine_bwd_flat_kernel<bf16_t, false, false><<<grid, block, 0, st>>>(a, lg, total, row_blocks);
-    } else {
-      if (a.dw) combine_bwd_flat_kernel<float, true, true><<<grid, block, 0, st>>>(a, lg, total, row_blocks);
-      else if (lg >= 0) combine_bwd_flat_kernel<float, true, false><<<grid, block, 0, st>>>(a, lg, total, row_blocks);
-      else combine_bwd_flat_kernel<float, false, false><<<grid, block, 0, st>>>(a, lg, total, row_blocks);
-    }
+  if (!a.dw) {
+    if (a.dtype == 1) launch_slot_rows<bf16_t, true, false>(a, st);
+    else launch_slot_rows<float, true, false>(a, st);
     return hipGetLastError();
   }
-  const int64_t row_blocks = blocks_for_rows(a.rows, kWideWaves);
-  const int64_t dw_blocks = (static_cast<int64_t>(a.S) * a.k + kThreads - 1) / kThreads;
-  if (row_blocks + dw_blocks == 0) return hipSuccess;
-  const dim3 grid(static_cast<unsigned>(row_blocks + dw_blocks)), block(kThreads);
-  if (a.dtype == 1) {
-    if (a.dw) combine_bwd_kernel<bf16_t, true><<<grid, block, 0, st>>>(a, row_blocks);
-    else combine_bwd_kernel<bf16_t, false><<<grid, block, 0, st>>>(a, row_blocks);
-  } else {
-    if (a.dw) combine_bwd_kernel<float, true><<<grid, block, 0, st>>>(a, row_blocks);
-    else combine_bwd_kernel<float, false><<<grid, block, 0, st>>>(a, row_blocks);
+  if (lg >= 6 && a.nch <= kRowThreads) {
+    if (a.dtype == 1) launch_slot_rows<bf16_t, true, true>(a, st);
+    else launch_slot_rows<float, true, true>(a, st);
+    return hipGetLastError();
   }
+  constexpr int kThreads = kWideWaves * kWave;
+  const int64_t rb = (a.rows + kWideWaves - 1) / kWideWaves;
+  const int64_t dwb = (static_cast<int64_t>(a.S) * a.k + kThreads - 1) / kThreads;
+  if (rb + dwb == 0) return hipSuccess;
+  const dim3 grid(static_cast<unsigned>(rb + dwb)), block(kThreads);
+  if (a.dtype == 1) combine_bwd_wave_kernel<bf16_t><<<grid, block, 0, st>>>(a, rb);
+  else combine_bwd_wave_kernel<float><<<grid, block, 0, st>>>(a, rb);
   return hipGetLastError();
 }
 

@@ -169,6 +169,51 @@ def summarize_mfma(args):
     print("\n".join(lines))
 
 
+def summarize_route(args):
+    """profiles/route_choice_<workload>.txt from two rocprofv3 --kernel-trace
+    --stats runs of this benchmark on one workload: the library as built (matrix
+    cores where the shape allows) and a build with HETUMOE_ROUTE_VALU_ONLY (the
+    vector-ALU projection).  Lists the gate's kernels of each run, average
+    duration per launch and calls."""
+    import csv
+    import glob
+    from paper_2203_14685_amd import workloads as wl
+    w = wl.WORKLOADS[args.workload]
+
+    def gate_rows(d):
+        rows = []
+        for f in glob.glob(os.path.join(d, "**", "*kernel_stats.csv"), recursive=True):
+            with open(f) as fh:
+                rows += list(csv.DictReader(fh))
+        out = []
+        for r in rows:
+            name = r["Name"].replace("void ", "").replace("hetumoe::", "").split("(")[0]
+            if name.startswith(("route_", "scan_", "assign_", "scan_assign", "select_ext")):
+                out.append((name, int(r["Calls"]), float(r["AverageNs"])))
+        if not out:
+            raise SystemExit(f"no gate kernels in {d}")
+        return out
+    runs = {"matrix cores (as built)": gate_rows(args.summarize_route[0]),
+            "vector ALUs (HETUMOE_ROUTE_VALU_ONLY)": gate_rows(args.summarize_route[1])}
+    alg = w["S"] * w["d"] * (2 if w["dtype"] == "bf16" else 4) + w["d"] * w["E"] * 2
+    lines = [f"# gate projection route, matrix cores against vector ALUs, workload {w['name']}",
+             "# two rocprofv3 kernel traces (TMPDIR=/tmp, from /tmp, repo at $R):",
+             f"#   rocprofv3 --kernel-trace --stats --output-format csv -d <dir> -- python3 $R/bench.py --workload "
+             f"{args.workload} --steps 20 --warmup 5 --no-cpu-baseline --no-base --no-workloads --cold-iters 0",
+             "#   the same with HETUMOE_LIBRARY=<lib> after `python -m paper_2203_14685_amd.build --out <lib> "
+             "-D HETUMOE_ROUTE_VALU_ONLY`",
+             f"# x + W bytes the projection must read: {alg}",
+             "%-40s %-60s %7s %10s %9s" % ("build", "kernel", "calls", "avg_us", "GB/s")]
+    for label, rows in runs.items():
+        for name, calls, ns in sorted(rows, key=lambda r: -r[2]):
+            gbs = alg / ns if name.startswith("route_") else float("nan")
+            lines.append("%-40s %-60s %7d %10.2f %9.1f" % (label, name[:60], calls, ns / 1e3, gbs))
+    path = os.path.join(ROOT, "profiles", f"route_choice_{w['name']}.txt")
+    with open(path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -184,6 +229,9 @@ def parse():
     ap.add_argument("--summarize-mfma", metavar="DIR",
                     help="write profiles/mfma_<workload>.txt from a rocprofv3 --pmc MfmaUtil MfmaFlopsBF16 "
                          "GRBM_GUI_ACTIVE output folder and exit")
+    ap.add_argument("--summarize-route", nargs=2, metavar=("MFMA_DIR", "VALU_DIR"),
+                    help="write profiles/route_choice_<workload>.txt from two rocprofv3 --kernel-trace --stats "
+                         "folders (library as built, and built with HETUMOE_ROUTE_VALU_ONLY) and exit")
     ap.add_argument("--no-base", action="store_true",
                     help="skip the BASE-layer timing (thousands of small launches; for counter runs)")
     ap.add_argument("--cold-iters", type=int, default=10,
@@ -458,6 +506,9 @@ def main():
         return
     if args.summarize_mfma:
         summarize_mfma(args)
+        return
+    if args.summarize_route:
+        summarize_route(args)
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:

@@ -15,7 +15,10 @@ import os
 import torch
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "libhetumoe.so")
+# HETUMOE_LIBRARY names another build of the library (for instance one made with
+# `python -m paper_2203_14685_amd.build --out ... -D HETUMOE_ROUTE_VALU_ONLY` to
+# time the vector-ALU projection); by default the in-tree build is loaded.
+LIB_PATH = os.environ.get("HETUMOE_LIBRARY") or os.path.join(_PKG, "libhetumoe.so")
 
 MOE_OK, MOE_ERR_INVALID_ARG, MOE_ERR_UNSUPPORTED, MOE_ERR_WORKSPACE, MOE_ERR_HIP, MOE_ERR_NOT_CONVERGED = range(6)
 MOE_F32, MOE_BF16 = 0, 1

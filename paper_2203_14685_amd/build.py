@@ -58,18 +58,22 @@ def link_command(cc, objdir, out, sources=SOURCES):
     return [cc, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", out]
 
 
-def build(verbose=True):
-    """Compile every HIP source (in parallel) and link paper_2203_14685_amd/libhetumoe.so."""
+def build(verbose=True, out=None, defines=()):
+    """Compile every HIP source (in parallel) and link paper_2203_14685_amd/libhetumoe.so
+    (or `out`, from objects in a folder of its own, with the macros `defines`:
+    HETUMOE_ROUTE_VALU_ONLY builds a library whose gate projects on the vector
+    ALUs only, to time those routes against the matrix-core ones)."""
     from concurrent.futures import ThreadPoolExecutor
     cc = hipcc()
     t0 = time.time()
-    objdir = os.path.join(PKG, "_build")
+    lib = LIB if out is None else os.path.abspath(out)
+    objdir = os.path.join(PKG, "_build") if out is None else lib + ".objs"
     os.makedirs(objdir, exist_ok=True)
     prune_stale_objects(objdir)
     jobs = []
     for src in SOURCES:
         obj = os.path.join(objdir, src.replace(".hip", ".o"))
-        flags = [f for f in HIPCC_FLAGS if f != "-shared"]
+        flags = [f for f in HIPCC_FLAGS if f != "-shared"] + [f"-D{d}" for d in defines]
         jobs.append((obj, [cc, *flags, "-I", INCLUDE, "-I", CSRC, "-c", os.path.join(CSRC, src), "-o", obj]))
     if verbose:
         print(f"[build] {cc} {' '.join(HIPCC_FLAGS)} ... ({len(jobs)} sources)", flush=True)
@@ -82,19 +86,24 @@ def build(verbose=True):
             sys.stderr.write(" ".join(cmd) + "\n" + out)
             raise RuntimeError(f"hipcc failed on {cmd[-3]} with exit code {rc}")
         logs.append(out)
-    tmp = LIB + ".tmp"
-    rc, out = _run(link_command(cc, objdir, tmp))
+    tmp = lib + ".tmp"
+    rc, log = _run(link_command(cc, objdir, tmp))
     if rc != 0:
-        sys.stderr.write(out)
+        sys.stderr.write(log)
         raise RuntimeError(f"link failed with exit code {rc}")
-    os.replace(tmp, LIB)
+    os.replace(tmp, lib)
     if verbose:
         warn = [ln for out in logs for ln in out.splitlines() if "packed-fp32-ops" not in ln and ln.strip()]
         if warn:
             sys.stderr.write("\n".join(warn) + "\n")
-        print(f"[build] {LIB} in {time.time() - t0:.1f}s", flush=True)
-    return LIB
+        print(f"[build] {lib} in {time.time() - t0:.1f}s", flush=True)
+    return lib
 
 
 if __name__ == "__main__":
-    build()
+    import argparse
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--out", help="write the library here instead of the package")
+    ap.add_argument("-D", dest="defines", action="append", default=[], help="macro for every source")
+    args = ap.parse_args()
+    build(out=args.out, defines=args.defines)

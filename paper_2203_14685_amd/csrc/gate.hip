@@ -350,9 +350,13 @@ hipError_t launch_route(const RouteArgs& a, hipStream_t st) {
     route_hash_kernel<<<dim3(blocks), dim3(kBlock), static_cast<size_t>(kWavesPerBlock) * a.E * sizeof(int), st>>>(a);
     return hipGetLastError();
   }
+#ifndef HETUMOE_ROUTE_VALU_ONLY
+  // matrix-core projections (a build with HETUMOE_ROUTE_VALU_ONLY defined, used
+  // only to time the vector-ALU routes against them, skips these)
   if (route_uses_mfma_rs(a)) return launch_route_mfma_rs(a, device_cu_count(), st);
   if (route_uses_mfma_ph(a)) return launch_route_mfma_ph(a, device_cu_count(), st);
   if (route_uses_mfma(a)) return launch_route_mfma(a, st);
+#endif
   // with logits given, the element type of x and wg is irrelevant
   if (a.dtype == 1 && !a.logits_in) return launch_route_valu_bf16(a, st);
   return launch_route_valu_f32(a, st);

@@ -222,7 +222,11 @@ bool route_uses_mfma_rs(const RouteArgs& a) {
   return (reinterpret_cast<uintptr_t>(a.x) % 16) == 0 && (reinterpret_cast<uintptr_t>(a.wg) % 16) == 0;
 }
 
+#ifndef HETUMOE_ROUTE_VALU_ONLY
 bool route_fuses_extended(const RouteArgs& a) { return route_uses_mfma_rs(a); }
+#else
+bool route_fuses_extended(const RouteArgs&) { return false; }
+#endif
 
 hipError_t launch_route_mfma_rs(const RouteArgs& a, int cus, hipStream_t st) {
   const int grid = a.nb < cus ? a.nb : cus;

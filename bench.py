@@ -36,8 +36,9 @@ def kernel_of_op(op, w):
     """(kernel symbol fragment in traces, sources that kernel is compiled from) of
     the one kernel an op launches for workload dict `w`, following the launch
     rules of the layout library: with one choice per token, dispatch and combine
-    backward run the slot-row kernel (combine backward with dw there only on
-    rows of 64 to 512 chunks, a power of two, else one wave per row); with
+    backward run the slot-row kernel (its compile-time form on rows of 64 to 512
+    chunks, a power of two; combine backward with dw only there, else one wave
+    per row); with
     several, the token-major forms; combine and dispatch backward always run the
     token-row kernel, its choice list sized 1, 2, 4 or 8."""
     elt = "hetumoe::bf16_t" if w["dtype"] == "bf16" else "float"
@@ -47,14 +48,17 @@ def kernel_of_op(op, w):
     p2 = "true" if pow2 else "false"
     dw = w["kind"] != 2  # learned gates have weights to differentiate (hash: none)
     kmax = 1 if k == 1 else 2 if k == 2 else 4 if k <= 4 else 8
+    lg = nch.bit_length() - 1
+    fast = pow2 and 64 <= nch <= 512 and w["E"] * w["C"] > 0  # the compile-time row length form
+    slot = (lambda t, sc, d: f"slot_rows_pow2_kernel<{t}, {sc}, {d}, {lg}") if fast else \
+        (lambda t, sc, d: f"slot_rows_kernel<{t}, {sc}, {d}, {p2}")
     if k > 1:
         cbwd = f"combine_bwd_scatter_kernel<{elt}, {'true' if dw else 'false'}>"
     elif dw and not (pow2 and 64 <= nch <= 512):
         cbwd = f"combine_bwd_wave_kernel<{elt}>"
     else:
-        cbwd = f"slot_rows_kernel<{elt}, true, {'true' if dw else 'false'}, {p2}>"
-    return {"dispatch": ("dispatch_scatter_kernel" if k > 1 else f"slot_rows_kernel<float, false, false, {p2}>",
-                         _LAYOUT_SRC),
+        cbwd = slot(elt, "true", "true" if dw else "false")
+    return {"dispatch": ("dispatch_scatter_kernel" if k > 1 else slot("float", "false", "false"), _LAYOUT_SRC),
             "combine": (f"token_rows_kernel<{elt}, true, {kmax}>", _LAYOUT_SRC),
             "combine_bwd": (cbwd, _LAYOUT_SRC),
             "dispatch_bwd": (f"token_rows_kernel<{elt}, false, {kmax}>", _LAYOUT_SRC),

@@ -173,6 +173,81 @@ __global__ __launch_bounds__(kRowThreads) void slot_rows_kernel(RowArgs a, int l
   }
 }
 
+// The same for rows of NCH = 2^LG chunks, 64 to 512 (one to eight waves, so
+// every row lies inside one block), with nothing but the block and phase
+// indices on the path to the first load: blockIdx.y is the phase (TWO: 0 zero
+// rows, 1 copied rows; else 0 both), chunks past the buffer are clamped onto
+// its last one and their stores skipped, and an empty slot or a chunk of the
+// other phase skips its load by a branch uniform over the wave.  The first
+// phase's blocks below ceil(S / 512) also clear dw of dropped choices.
+template <typename T, bool SCALE, bool DW, int LG, bool TWO>
+__global__ __launch_bounds__(kRowThreads) void slot_rows_pow2_kernel(RowArgs a, int64_t total) {
+  constexpr int kEl = Chunk<T>::kElems;
+  constexpr int NCH = 1 << LG;
+  const bool copy_phase = !TWO || blockIdx.y == 1;
+  const int64_t gb = static_cast<int64_t>(blockIdx.x) * kRowThreads;
+  const int64_t g = gb + threadIdx.x;
+  const bool live = g < total;
+  const int64_t gc = live ? g : total - 1;  // total > 0
+  const int row = __builtin_amdgcn_readfirstlane(static_cast<int>(gc >> LG));
+  const int col = static_cast<int>(gc & (NCH - 1));
+  // entries outside [0, S) are out of contract and treated as empty slots
+  const int src = a.slot_src[row];
+  const bool full = (src >= 0) & (src < a.S);
+  // uniform over the wave: its chunks lie in one row, and total is a multiple of 64
+  const bool act = __builtin_amdgcn_readfirstlane(static_cast<int>(live & (!TWO || full == copy_phase))) != 0;
+  u32x4 v = u32x4{0u, 0u, 0u, 0u};
+  float dot = 0.f;
+  if (copy_phase && act && full) {
+    const u32x4* srow = reinterpret_cast<const u32x4*>(a.src) + static_cast<int64_t>(src) * NCH;
+    v = buf_load_nt(buf_rsrc(srow, NCH * 16), col * 16);
+    if constexpr (SCALE) {
+      const float w = a.weights[src];
+      u32x4 ve = u32x4{0u, 0u, 0u, 0u};
+      if constexpr (DW)
+        ve = buf_load_nt(buf_rsrc(reinterpret_cast<const u32x4*>(a.aux) + gb, kRowThreads * 16),
+                         static_cast<int>(threadIdx.x) * 16);
+      {
+        float f[kEl];
+        Chunk<T>::unpack(v, f);
+        if constexpr (DW) {
+          float gq[kEl];
+          Chunk<T>::unpack(ve, gq);
+#pragma unroll
+          for (int q = 0; q < kEl; ++q) dot = fmaf(f[q], gq[q], dot);
+        }
+#pragma unroll
+        for (int q = 0; q < kEl; ++q) f[q] *= w;
+        v = Chunk<T>::pack(f);
+      }
+    }
+  }
+  if (act) buf_store_nt(v, buf_rsrc(reinterpret_cast<u32x4*>(a.dst) + gb, kRowThreads * 16), threadIdx.x * 16);
+  if constexpr (DW) {
+    if (blockIdx.y == 0) {
+      const int64_t i = gb + threadIdx.x;
+      if (i < a.S && a.slots[i] < 0) a.dw[i] = 0.f;
+    }
+    if (!copy_phase) return;  // uniform over the block
+    __shared__ float part[kRowWaves];
+    const float t = wave_sum(dot);
+    if (lane_id() == 0) part[threadIdx.x / kWave] = t;
+    __syncthreads();
+    constexpr int kRowsHere = kRowThreads / NCH;
+    constexpr int kParts = NCH / kWave;
+    if (static_cast<int>(threadIdx.x) < kRowsHere) {
+      const int64_t r = (gb >> LG) + threadIdx.x;
+      if (r < a.rows) {
+        float sum = 0.f;
+#pragma unroll
+        for (int j = 0; j < kParts; ++j) sum += part[threadIdx.x * kParts + j];
+        const int s2 = a.slot_src[r];
+        if (s2 >= 0 && s2 < a.S) a.dw[s2] = sum;
+      }
+    }
+  }
+}
+
 // Combine backward with dw for k = 1 on rows slot_rows_kernel does not take
 // (not a power of two, or longer than 512 chunks): one wave per row, kUnroll
 // chunks per lane in flight.  Blocks past the row blocks clear dw of dropped
@@ -239,13 +314,25 @@ __global__ __launch_bounds__(kWideWaves * kWave) void combine_bwd_wave_kernel(Ro
 // routing comes through scalar loads, and the row is stored through a buffer
 // resource with the cache policy of its kind: kPolDataRow, or kPolZeroRow for
 // a token with nothing kept.
-template <typename T, bool WEIGHTED, int KMAX, bool WR, int CPT>
-__global__ __launch_bounds__(kRowThreads) void token_rows_kernel(RowArgs a, int tpr, int rpb) {
+template <typename T, bool WEIGHTED, int KMAX, bool WR, int CPT, int TPR>
+__global__ __launch_bounds__(kRowThreads) void token_rows_kernel(RowArgs a, int tpr_arg, int rpb_arg) {
   constexpr int kEl = Chunk<T>::kElems;
+  // TPR > 0 (then also WR): threads per row known when compiled, a row is
+  // exactly TPR * CPT chunks, and every thread of the block has a row.  That
+  // path has no branch before its loads: rows past the batch are clamped onto
+  // the last one (their stores are skipped), and a dropped choice loads from an
+  // offset past its buffer resource, which returns zeros without a memory access.
+  const int tpr = TPR > 0 ? TPR : tpr_arg;
+  const int rpb = TPR > 0 ? kRowThreads / TPR : rpb_arg;
   const int rl = static_cast<int>(threadIdx.x) / tpr;
   int64_t s = static_cast<int64_t>(blockIdx.x) * rpb + rl;
+  const bool live = TPR > 0 ? s < a.rows : (rl < rpb && s < a.rows);
+  if constexpr (TPR > 0) {
+    if (s >= a.rows) s = a.rows - 1;
+  } else if (!live) {
+    return;
+  }
   if constexpr (WR) s = __builtin_amdgcn_readfirstlane(static_cast<int>(s));  // rows < 2^31
-  if (rl >= rpb || s >= a.rows) return;
   const int nch = a.nch;
   const int k = KMAX <= 2 ? KMAX : a.k;  // the launcher picks KMAX = k for k <= 2
   const u32x4* src = reinterpret_cast<const u32x4*>(a.src);
@@ -271,7 +358,36 @@ __global__ __launch_bounds__(kRowThreads) void token_rows_kernel(RowArgs a, int 
     any = any | ok[r];
   }
   u32x4* orow = reinterpret_cast<u32x4*>(a.dst) + s * nch;
-  const __amdgpu_buffer_rsrc_t out = buf_rsrc(orow, nch * 16);
+  if constexpr (TPR > 0) {
+    const __amdgpu_buffer_rsrc_t out = buf_rsrc(orow, nch * 16);
+    const int c0 = static_cast<int>(threadIdx.x) - rl * tpr;
+    u32x4 v[CPT][KMAX];
+#pragma unroll
+    for (int u = 0; u < CPT; ++u)
+#pragma unroll
+      for (int r = 0; r < KMAX; ++r)
+        v[u][r] = buf_load_nt(buf_rsrc(src + off[r], nch * 16), ok[r] ? (c0 + u * tpr) * 16 : 0x7ffffff0);
+#pragma unroll
+    for (int u = 0; u < CPT; ++u) {
+      float acc[kEl];
+#pragma unroll
+      for (int q = 0; q < kEl; ++q) acc[q] = 0.f;
+#pragma unroll
+      for (int r = 0; r < KMAX; ++r) {
+        if (!ok[r]) continue;
+        float f[kEl];
+        Chunk<T>::unpack(v[u][r], f);
+#pragma unroll
+        for (int q = 0; q < kEl; ++q) acc[q] = WEIGHTED ? fmaf(w[r], f[q], acc[q]) : acc[q] + f[q];
+      }
+      const u32x4 o = Chunk<T>::pack(acc);
+      if (live) {
+        if (any) __builtin_amdgcn_raw_buffer_store_b128(o, out, (c0 + u * tpr) * 16, 0, kPolDataRow);
+        else __builtin_amdgcn_raw_buffer_store_b128(o, out, (c0 + u * tpr) * 16, 0, kPolZeroRow);
+      }
+    }
+    return;
+  }
   for (int c0 = static_cast<int>(threadIdx.x) - rl * tpr; c0 < nch; c0 += tpr * CPT) {
     u32x4 v[CPT][KMAX];
 #pragma unroll
@@ -301,6 +417,7 @@ __global__ __launch_bounds__(kRowThreads) void token_rows_kernel(RowArgs a, int 
       }
       const u32x4 o = Chunk<T>::pack(acc);
       if constexpr (WR) {
+        const __amdgpu_buffer_rsrc_t out = buf_rsrc(orow, nch * 16);
         if (any) __builtin_amdgcn_raw_buffer_store_b128(o, out, c * 16, 0, kPolDataRow);
         else __builtin_amdgcn_raw_buffer_store_b128(o, out, c * 16, 0, kPolZeroRow);
       } else {
@@ -480,9 +597,31 @@ static void launch_slot_rows_t(const RowArgs& a, int64_t total, int64_t nb, hipS
   }
 }
 
+template <typename T, bool SCALE, bool DW, int LG>
+static void launch_slot_rows_pow2(const RowArgs& a, int64_t total, hipStream_t st) {
+  const int64_t nb = row_blocks(total);
+  const int64_t dwb = DW ? (static_cast<int64_t>(a.S) + kRowThreads - 1) / kRowThreads : 0;
+  const dim3 block(kRowThreads);
+  if (total * 16 > kTwoPhaseBytes) {
+    slot_rows_pow2_kernel<T, SCALE, DW, LG, true>
+        <<<dim3(static_cast<unsigned>(nb > dwb ? nb : dwb), 2), block, 0, st>>>(a, total);
+  } else {
+    slot_rows_pow2_kernel<T, SCALE, DW, LG, false>
+        <<<dim3(static_cast<unsigned>(nb > dwb ? nb : dwb), 1), block, 0, st>>>(a, total);
+  }
+}
+
 template <typename T, bool SCALE, bool DW>
 static void launch_slot_rows(const RowArgs& a, hipStream_t st) {
   const int64_t total = a.rows * a.nch;
+  const int lg = pow2_log(a.nch);
+  if (total > 0 && lg >= 6 && lg <= 9) {
+    if (lg == 9) launch_slot_rows_pow2<T, SCALE, DW, 9>(a, total, st);
+    else if (lg == 8) launch_slot_rows_pow2<T, SCALE, DW, 8>(a, total, st);
+    else if (lg == 7) launch_slot_rows_pow2<T, SCALE, DW, 7>(a, total, st);
+    else launch_slot_rows_pow2<T, SCALE, DW, 6>(a, total, st);
+    return;
+  }
   const int64_t nb = row_blocks(total);
   if (total * 16 > kTwoPhaseBytes) launch_slot_rows_t<T, SCALE, DW, true>(a, total, nb, st);
   else launch_slot_rows_t<T, SCALE, DW, false>(a, total, nb, st);
@@ -507,13 +646,24 @@ hipError_t launch_dispatch(const RowArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
+template <typename T, bool WEIGHTED, bool WR, int CPT, int TPR>
+static void launch_token_rows_k(const RowArgs& a, int tpr, int rpb, hipStream_t st) {
+  const dim3 grid(static_cast<unsigned>((a.rows + rpb - 1) / rpb)), block(kRowThreads);
+  if (a.k == 1) token_rows_kernel<T, WEIGHTED, 1, WR, CPT, TPR><<<grid, block, 0, st>>>(a, tpr, rpb);
+  else if (a.k == 2) token_rows_kernel<T, WEIGHTED, 2, WR, CPT, TPR><<<grid, block, 0, st>>>(a, tpr, rpb);
+  else if (a.k <= 4) token_rows_kernel<T, WEIGHTED, 4, WR, CPT, TPR><<<grid, block, 0, st>>>(a, tpr, rpb);
+  else token_rows_kernel<T, WEIGHTED, 8, WR, CPT, TPR><<<grid, block, 0, st>>>(a, tpr, rpb);
+}
+
 template <typename T, bool WEIGHTED, bool WR, int CPT>
 static void launch_token_rows_w(const RowArgs& a, int tpr, int rpb, hipStream_t st) {
-  const dim3 grid(static_cast<unsigned>((a.rows + rpb - 1) / rpb)), block(kRowThreads);
-  if (a.k == 1) token_rows_kernel<T, WEIGHTED, 1, WR, CPT><<<grid, block, 0, st>>>(a, tpr, rpb);
-  else if (a.k == 2) token_rows_kernel<T, WEIGHTED, 2, WR, CPT><<<grid, block, 0, st>>>(a, tpr, rpb);
-  else if (a.k <= 4) token_rows_kernel<T, WEIGHTED, 4, WR, CPT><<<grid, block, 0, st>>>(a, tpr, rpb);
-  else token_rows_kernel<T, WEIGHTED, 8, WR, CPT><<<grid, block, 0, st>>>(a, tpr, rpb);
+  // rows of exactly tpr * CPT chunks with tpr dividing the block: the
+  // compile-time path
+  const bool exact = WR && a.nch == tpr * CPT;
+  if (exact && tpr == 512) launch_token_rows_k<T, WEIGHTED, WR, CPT, 512>(a, tpr, rpb, st);
+  else if (exact && tpr == 256) launch_token_rows_k<T, WEIGHTED, WR, CPT, 256>(a, tpr, rpb, st);
+  else if (exact && tpr == 128) launch_token_rows_k<T, WEIGHTED, WR, CPT, 128>(a, tpr, rpb, st);
+  else launch_token_rows_k<T, WEIGHTED, WR, CPT, 0>(a, tpr, rpb, st);
 }
 
 template <typename T, bool WEIGHTED>

@@ -218,6 +218,37 @@ def summarize_route(args):
     print("\n".join(lines))
 
 
+def summarize_trace(args):
+    """profiles/kernels_<workload>.txt from one rocprofv3 --kernel-trace --stats
+    run of this benchmark on one workload (its kernel_stats.csv)."""
+    import csv
+    import glob
+    from paper_2203_14685_amd import workloads as wl
+    w = wl.WORKLOADS[args.workload]
+    rows = []
+    for f in glob.glob(os.path.join(args.summarize_trace, "**", "*kernel_stats.csv"), recursive=True):
+        with open(f) as fh:
+            rows += list(csv.DictReader(fh))
+    if not rows:
+        raise SystemExit(f"no kernel_stats.csv under {args.summarize_trace}")
+    lines = [f"# rocprofv3 kernel trace: workload {w['name']}, one fwd+bwd step per call",
+             "# command (from /tmp, TMPDIR=/tmp; repo at $R):",
+             f"#   rocprofv3 --kernel-trace --stats --output-format csv -d <dir> -- python3 $R/bench.py --workload "
+             f"{args.workload} --steps 20 --warmup 5 --no-cpu-baseline --no-workloads",
+             "# kernel_stats.csv of that run, MI355X (gfx950).  The step's kernels run warmup + steps + cold-cache",
+             "# launches; the timings after the timed step (gate backward, further gates, BASE layer, copy",
+             "# ceiling) add their own launches, hence the other call counts.",
+             "%-74s %6s %12s %12s %12s %7s" % ("kernel", "calls", "avg_ns", "min_ns", "max_ns", "pct")]
+    for r in sorted(rows, key=lambda r: -float(r["TotalDurationNs"])):
+        name = r["Name"].replace("void ", "").replace("hetumoe::", "").split("(")[0]
+        lines.append("%-74s %6d %12.0f %12d %12d %7.2f" % (name[:74], int(r["Calls"]), float(r["AverageNs"]),
+                                                           int(r["MinNs"]), int(r["MaxNs"]), float(r["Percentage"])))
+    path = os.path.join(ROOT, "profiles", f"kernels_{w['name']}.txt")
+    with open(path, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines[:20]))
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -233,6 +264,8 @@ def parse():
     ap.add_argument("--summarize-mfma", metavar="DIR",
                     help="write profiles/mfma_<workload>.txt from a rocprofv3 --pmc MfmaUtil MfmaFlopsBF16 "
                          "GRBM_GUI_ACTIVE output folder and exit")
+    ap.add_argument("--summarize-trace", metavar="DIR",
+                    help="write profiles/kernels_<workload>.txt from a rocprofv3 --kernel-trace --stats folder and exit")
     ap.add_argument("--summarize-route", nargs=2, metavar=("MFMA_DIR", "VALU_DIR"),
                     help="write profiles/route_choice_<workload>.txt from two rocprofv3 --kernel-trace --stats "
                          "folders (library as built, and built with HETUMOE_ROUTE_VALU_ONLY) and exit")
@@ -513,6 +546,9 @@ def main():
         return
     if args.summarize_route:
         summarize_route(args)
+        return
+    if args.summarize_trace:
+        summarize_trace(args)
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:

@@ -435,13 +435,15 @@ __global__ __launch_bounds__(kRowThreads) void token_rows_kernel(RowArgs a, int 
 // ones.  Each output row still has exactly one writer.
 constexpr int kZeroBlocks = 1024;
 
-__device__ __forceinline__ void zero_empty_rows(const RowArgs& a, int64_t first_wave, int64_t nwaves, int lane) {
+// first_wave is uniform over the wave (made so by the callers), so the rows,
+// their slot_src entries and the buffer resources are too.
+__device__ __forceinline__ void zero_empty_rows(const RowArgs& a, int first_wave, int64_t nwaves, int lane) {
   const u32x4 z = {0u, 0u, 0u, 0u};
   for (int64_t row = first_wave; row < a.rows; row += nwaves) {
     const int src = a.slot_src[row];
     if (src >= 0 && src < a.S * a.k) continue;
-    u32x4* dst = reinterpret_cast<u32x4*>(a.dst) + row * a.nch;
-    for (int i = lane; i < a.nch; i += kWave) store_nt(dst + i, z);
+    const __amdgpu_buffer_rsrc_t dst = buf_rsrc(reinterpret_cast<u32x4*>(a.dst) + row * a.nch, a.nch * 16);
+    for (int i = lane; i < a.nch; i += kWave) buf_store_nt(z, dst, i * 16);
   }
 }
 
@@ -450,31 +452,30 @@ __global__ __launch_bounds__(kWideWaves * kWave) void dispatch_scatter_kernel(Ro
   const int lane = lane_id();
   const int wave = threadIdx.x / kWave;
   if (static_cast<int64_t>(blockIdx.x) >= tok_blocks) {
-    zero_empty_rows(a, (static_cast<int64_t>(blockIdx.x) - tok_blocks) * kWideWaves + wave,
+    zero_empty_rows(a, __builtin_amdgcn_readfirstlane(
+                           static_cast<int>((static_cast<int64_t>(blockIdx.x) - tok_blocks) * kWideWaves + wave)),
                     static_cast<int64_t>(gridDim.x - tok_blocks) * kWideWaves, lane);
     return;
   }
-  const int64_t s = static_cast<int64_t>(blockIdx.x) * kWideWaves + wave;
+  // the token is uniform over the wave: scalar routing loads, row resources in
+  // scalar registers; chunks past the row fall outside its resource (loads give
+  // zeros, stores are dropped), so the row walk needs no bounds test
+  const int64_t s = __builtin_amdgcn_readfirstlane(static_cast<int>(static_cast<int64_t>(blockIdx.x) * kWideWaves + wave));
   if (s >= a.S) return;
   const int nch = a.nch, k = a.k;
-  const u32x4* srow = reinterpret_cast<const u32x4*>(a.src) + s * nch;
+  const __amdgpu_buffer_rsrc_t srow = buf_rsrc(reinterpret_cast<const u32x4*>(a.src) + s * nch, nch * 16);
   for (int base = 0; base < nch; base += kWave * kUnroll) {
     u32x4 v[kUnroll];
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      const int i = base + u * kWave + lane;
-      if (i < nch) v[u] = load_nt(srow + i);
-    }
+    for (int u = 0; u < kUnroll; ++u) v[u] = buf_load_nt(srow, (base + u * kWave + lane) * 16);
     for (int r = 0; r < k; ++r) {
       const int slot = a.slots[s * k + r];
       const int e = a.ids[s * k + r];
       if (slot < 0 || slot >= a.C || e < 0 || e >= a.E) continue;
-      u32x4* dst = reinterpret_cast<u32x4*>(a.dst) + (static_cast<int64_t>(e) * a.C + slot) * nch;
+      const __amdgpu_buffer_rsrc_t dst =
+          buf_rsrc(reinterpret_cast<u32x4*>(a.dst) + (static_cast<int64_t>(e) * a.C + slot) * nch, nch * 16);
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        const int i = base + u * kWave + lane;
-        if (i < nch) store_nt(dst + i, v[u]);
-      }
+      for (int u = 0; u < kUnroll; ++u) buf_store_nt(v[u], dst, (base + u * kWave + lane) * 16);
     }
   }
 }
@@ -491,24 +492,25 @@ __global__ __launch_bounds__(kBwdScatterWaves * kWave) void combine_bwd_scatter_
   const int lane = lane_id();
   const int wave = threadIdx.x / kWave;
   if (static_cast<int64_t>(blockIdx.x) >= tok_blocks) {
-    zero_empty_rows(a, (static_cast<int64_t>(blockIdx.x) - tok_blocks) * kBwdScatterWaves + wave,
+    zero_empty_rows(a, __builtin_amdgcn_readfirstlane(
+                           static_cast<int>((static_cast<int64_t>(blockIdx.x) - tok_blocks) * kBwdScatterWaves + wave)),
                     static_cast<int64_t>(gridDim.x - tok_blocks) * kBwdScatterWaves, lane);
     return;
   }
-  const int64_t s = static_cast<int64_t>(blockIdx.x) * kBwdScatterWaves + wave;
+  // the token is uniform over the wave (scalar routing, row resources in scalar
+  // registers); chunks past a row fall outside its resource: loads give zeros,
+  // stores are dropped, so the row walk needs no bounds test
+  const int64_t s = __builtin_amdgcn_readfirstlane(static_cast<int>(static_cast<int64_t>(blockIdx.x) * kBwdScatterWaves + wave));
   if (s >= a.S) return;
   const int nch = a.nch, k = a.k;
-  const u32x4* dyrow = reinterpret_cast<const u32x4*>(a.src) + s * nch;
+  const __amdgpu_buffer_rsrc_t dyrow = buf_rsrc(reinterpret_cast<const u32x4*>(a.src) + s * nch, nch * 16);
   float dot[8];
 #pragma unroll
   for (int r = 0; r < 8; ++r) dot[r] = 0.f;
   for (int base = 0; base < nch; base += kWave * kU) {
     u32x4 v[kU];
 #pragma unroll
-    for (int u = 0; u < kU; ++u) {
-      const int i = base + u * kWave + lane;
-      if (i < nch) v[u] = load_nt(dyrow + i);
-    }
+    for (int u = 0; u < kU; ++u) v[u] = buf_load_nt(dyrow, (base + u * kWave + lane) * 16);
 #pragma unroll
     for (int r0 = 0; r0 < 8; r0 += kRG) {
       if (r0 >= k) break;
@@ -520,38 +522,34 @@ __global__ __launch_bounds__(kBwdScatterWaves * kWave) void combine_bwd_scatter_
         const int r = r0 + j;
         const int slot = (r < k) ? a.slots[s * k + r] : -1;
         const int e = (r < k) ? a.ids[s * k + r] : -1;
-        kept[j] = slot >= 0 && slot < a.C && e >= 0 && e < a.E;
+        kept[j] = (slot >= 0) & (slot < a.C) & (e >= 0) & (e < a.E);
         row[j] = kept[j] ? static_cast<int64_t>(e) * a.C + slot : 0;
         if constexpr (DW) {
-          const u32x4* yerow = reinterpret_cast<const u32x4*>(a.aux) + row[j] * nch;
+          const __amdgpu_buffer_rsrc_t yerow =
+              buf_rsrc(reinterpret_cast<const u32x4*>(a.aux) + row[j] * nch, kept[j] ? nch * 16 : 0);
 #pragma unroll
-          for (int u = 0; u < kU; ++u) {
-            const int i = base + u * kWave + lane;
-            if (kept[j] && i < nch) ve[j][u] = load_nt(yerow + i);
-          }
+          for (int u = 0; u < kU; ++u) ve[j][u] = buf_load_nt(yerow, (base + u * kWave + lane) * 16);
         }
       }
 #pragma unroll
       for (int j = 0; j < kRG; ++j) {
         if (!kept[j]) continue;
         const float w = a.weights[s * k + r0 + j];
-        u32x4* dst = reinterpret_cast<u32x4*>(a.dst) + row[j] * nch;
+        const __amdgpu_buffer_rsrc_t dst = buf_rsrc(reinterpret_cast<u32x4*>(a.dst) + row[j] * nch, nch * 16);
 #pragma unroll
         for (int u = 0; u < kU; ++u) {
           const int i = base + u * kWave + lane;
-          if (i < nch) {
-            float f[kEl];
-            Chunk<T>::unpack(v[u], f);
-            if constexpr (DW) {
-              float gq[kEl];
-              Chunk<T>::unpack(ve[j][u], gq);
+          float f[kEl];
+          Chunk<T>::unpack(v[u], f);
+          if constexpr (DW) {
+            float gq[kEl];
+            Chunk<T>::unpack(ve[j][u], gq);
 #pragma unroll
-              for (int q = 0; q < kEl; ++q) dot[r0 + j] = fmaf(f[q], gq[q], dot[r0 + j]);
-            }
-#pragma unroll
-            for (int q = 0; q < kEl; ++q) f[q] *= w;
-            store_nt(dst + i, Chunk<T>::pack(f));
+            for (int q = 0; q < kEl; ++q) dot[r0 + j] = fmaf(f[q], gq[q], dot[r0 + j]);
           }
+#pragma unroll
+          for (int q = 0; q < kEl; ++q) f[q] *= w;
+          buf_store_nt(Chunk<T>::pack(f), dst, i * 16);
         }
       }
     }

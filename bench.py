@@ -59,9 +59,9 @@ def kernel_of_op(op, w):
     else:
         cbwd = slot(elt, "true", "true" if dw else "false")
     return {"dispatch": ("dispatch_scatter_kernel" if k > 1 else slot("float", "false", "false"), _LAYOUT_SRC),
-            "combine": (f"token_rows_kernel<{elt}, true, {kmax}>", _LAYOUT_SRC),
+            "combine": (f"token_rows_kernel<{elt}, true, {kmax},", _LAYOUT_SRC),
             "combine_bwd": (cbwd, _LAYOUT_SRC),
-            "dispatch_bwd": (f"token_rows_kernel<{elt}, false, {kmax}>", _LAYOUT_SRC),
+            "dispatch_bwd": (f"token_rows_kernel<{elt}, false, {kmax},", _LAYOUT_SRC),
             "gate": ("route_", _GATE_SRC)}[op]
 
 

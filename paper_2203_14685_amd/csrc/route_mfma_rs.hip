@@ -2,24 +2,27 @@
 // of Eq. 1 with softmax and expert selection (Sec. 3.1 top-k / kTop1), for
 // shapes whose W fits in the register file of one CU.
 //
-// Persistent blocks of WAVES waves, one block per CU.  Wave w owns the K slice
-// [w*KSL, (w+1)*KSL) of d = WAVES*KSL and keeps the B fragments of W^T for
-// that slice (all E = 16*NT experts) in registers for the whole kernel, so W
-// is read once per CU.  Eight waves (two per SIMD) serve W up to 64 K
-// elements; four waves (one per SIMD, up to 512 registers each) serve up to
-// 128 K.  Column n of N tile nt holds expert n*NT + nt, so a lane's NT experts
-// are adjacent in a row of W and each K row of its fragments is one load.
+// Persistent blocks of WAVES waves, one block per CU.  Each wave owns one K
+// slice [sl*KSL, (sl+1)*KSL) of d = WAVES*KSL and keeps the B fragments of W^T
+// for that slice (all E = 16*NT experts) in registers for the whole kernel, so
+// W is read once per CU.  Eight waves (two per SIMD, up to 256 registers each)
+// serve W up to 128 K elements.  The slices are dealt to the waves rotated by
+// the block index, so that the blocks do not all read the same rows of W at
+// the same moment; the partial sums are stored and added in slice order, so
+// the result does not depend on the rotation.  Column n of N tile nt holds
+// expert n*NT + nt, so a lane's NT experts are adjacent in a row of W and each
+// K row of its fragments is one load.
 // The block then streams 16-token tiles of x: each wave loads the tile's
 // columns of its slice into one of two buffers while the other is multiplied
 // (KSL/32 x NT v_mfma_f32_16x16x32_bf16), and the partial 16 x E tiles are
-// summed in a fixed order through LDS.  K step ks of wave w covers the columns
-// [w*KSL + 32ks, +32) and lane group g = lane/16 the 8 at w*KSL + 32ks + 8g,
+// summed in a fixed order through LDS.  K step ks of slice sl covers the columns
+// [sl*KSL + 32ks, +32) and lane group g = lane/16 the 8 at sl*KSL + 32ks + 8g,
 // so the 4 lanes of a row load 64 contiguous bytes per instruction.  The loads
 // are unconditional (rows past the batch read its last row, results unused):
 // a branch around them, or a register copy of a loaded value, would make the
 // products wait for every load in flight.  After four tiles (one 64-token wave
-// block) the block selects with WAVES lanes per token (each lane streams
-// E/WAVES experts, then a butterfly merge) and writes the wave block's
+// block) the block selects with WAVES lanes per token (each lane takes its
+// E/WAVES logits from LDS at once, then a butterfly merge) and writes the wave block's
 // (rank, expert) histogram.  The extended gates select here too: Dense-To-Sparse
 // first turns the wave block's logits into (logits + noise) / temperature in
 // LDS, and the hierarchical top-k (MODE 3) runs its two-level selection.
@@ -60,9 +63,12 @@ __global__ __launch_bounds__(WAVES * 64) void route_mfma_rs_kernel(RouteArgs a) 
   constexpr int E = NT * 16;
   constexpr int KSTEPS = KSL / 32;  // MFMA K steps per tile per wave
   constexpr int P = kThreads / kGroupTokens;  // selection lanes per token
-  static_assert(KSTEPS * NT <= (WAVES == 8 ? 16 : 64), "W^T fragments must fit the register budget");
-  __shared__ float part[WAVES * kTileTokens * E];      // per-wave partial logits of one tile
-  __shared__ float lg[kGroupTokens * (E + 1)];         // logits (+ bias) of the current wave block
+  constexpr int SL = E / P;                   // logits per selection lane
+  constexpr int LGS = E + 4;                  // row stride of lg: every lane's slice 16-byte aligned
+  static_assert(KSTEPS * NT <= (WAVES == 8 ? 32 : 64), "W^T fragments must fit the register budget");
+  static_assert(SL >= 2 && SL * P == E, "selection slices");
+  __shared__ float part[WAVES * kTileTokens * E];      // per-slice partial logits of one tile
+  __shared__ __align__(16) float lg[kGroupTokens * LGS];  // logits (+ bias) of the current wave block
   __shared__ int hist_lds[8 * E];                      // [k][E], k <= 8
 
   const int tid = threadIdx.x;
@@ -70,7 +76,8 @@ __global__ __launch_bounds__(WAVES * 64) void route_mfma_rs_kernel(RouteArgs a) 
   const int lane = lane_id();
   const int g = lane / 16, m = lane % 16;
   const int d = a.d;
-  const int kbase = w * KSL + 8 * g;  // + 32 ks per K step
+  const int sl = (w + static_cast<int>(blockIdx.x)) % WAVES;  // K slice of this wave
+  const int kbase = sl * KSL + 8 * g;  // + 32 ks per K step
   const uint16_t* wg = reinterpret_cast<const uint16_t*>(a.wg);
   const uint16_t* x = reinterpret_cast<const uint16_t*>(a.x);
 
@@ -125,18 +132,18 @@ __global__ __launch_bounds__(WAVES * 64) void route_mfma_rs_kernel(RouteArgs a) 
       for (int nt = 0; nt < NT; ++nt)
         acc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, __builtin_bit_cast(bf16x8, bfr[ks][nt]), acc[nt], 0, 0, 0);
     }
-    // partial tile of this wave: lane holds rows 4g+i, experts m*NT + nt
+    // partial tile of this wave's slice: lane holds rows 4g+i, experts m*NT + nt
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) part[(w * kTileTokens + 4 * g + i) * E + m * NT + nt] = acc[nt][i];
+      for (int i = 0; i < 4; ++i) part[(sl * kTileTokens + 4 * g + i) * E + m * NT + nt] = acc[nt][i];
     __syncthreads();
     for (int o = tid; o < kTileTokens * E; o += kThreads) {
       const int r = o / E, e = o % E;
       float sum = bias_e;
 #pragma unroll
       for (int v = 0; v < WAVES; ++v) sum += part[(v * kTileTokens + r) * E + e];
-      lg[(t * kTileTokens + r) * (E + 1) + e] = sum;
+      lg[(t * kTileTokens + r) * LGS + e] = sum;
     }
     __syncthreads();
     if (t != 3) return;
@@ -147,9 +154,9 @@ __global__ __launch_bounds__(WAVES * 64) void route_mfma_rs_kernel(RouteArgs a) 
       for (int o = tid; o < kGroupTokens * E; o += kThreads) {
         const int r = o / E, e = o % E;
         if (tok0 + r < a.S) {
-          float v = lg[r * (E + 1) + e];
+          float v = lg[r * LGS + e];
           if (a.noise) v += a.noise[(tok0 + r) * E + e];
-          lg[r * (E + 1) + e] = v / a.temperature;
+          lg[r * LGS + e] = v / a.temperature;
         }
       }
       __syncthreads();
@@ -157,18 +164,18 @@ __global__ __launch_bounds__(WAVES * 64) void route_mfma_rs_kernel(RouteArgs a) 
     if (a.logits) {
       for (int o = tid; o < kGroupTokens * E; o += kThreads) {
         const int r = o / E, e = o % E;
-        if (tok0 + r < a.S) a.logits[(tok0 + r) * E + e] = lg[r * (E + 1) + e];
+        if (tok0 + r < a.S) a.logits[(tok0 + r) * E + e] = lg[r * LGS + e];
       }
     }
     const int tt = tid / P, j = tid % P;  // token of the wave block, lane within its P
     const int64_t s = tok0 + tt;
     const bool valid = s < a.S;
     if constexpr (MODE == 3)
-      select_token_htopk<P, KMAX>(&lg[tt * (E + 1)], E, a.k, E / a.groups, a.normalize, j, valid, a.ids + s * a.k,
-                                  a.weights + s * a.k, hist_lds);
+      select_token_htopk_c<P, KMAX, SL>(&lg[tt * LGS], a.k, E / a.groups, a.normalize, j, valid, a.ids + s * a.k,
+                                        a.weights + s * a.k, hist_lds);
     else
-      select_token<P, KMAX, MODE == 1>(&lg[tt * (E + 1)], E, a.k, a.normalize, j, valid, a.ids + s * a.k,
-                                       a.weights + s * a.k, hist_lds);
+      select_token_c<P, KMAX, MODE == 1, SL>(&lg[tt * LGS], a.k, a.normalize, j, valid, a.ids + s * a.k,
+                                             a.weights + s * a.k, hist_lds);
     __syncthreads();
     for (int i = tid; i < a.k * E; i += kThreads) {
       const int r = i / E, e = i % E;
@@ -213,7 +220,7 @@ static hipError_t launch_rs_nt(const RouteArgs& a, int grid, hipStream_t st) {
 }
 
 // Shapes served: bf16, E in {16, 32, 64, 128}, d in {512, 1024, 2048}, with
-// d * E <= 131072 (eight waves up to 65536, four beyond).
+// d * E <= 131072, all with eight waves.
 bool route_uses_mfma_rs(const RouteArgs& a) {
   if (a.kind == 2 || a.logits_in || a.dtype != 1) return false;
   if (a.E != 16 && a.E != 32 && a.E != 64 && a.E != 128) return false;
@@ -237,12 +244,12 @@ hipError_t launch_route_mfma_rs(const RouteArgs& a, int cus, hipStream_t st) {
     case 16 * 10000 + 2048: return launch_rs_nt<8, 1, 256>(a, grid, st);
     case 32 * 10000 + 512: return launch_rs_nt<8, 2, 64>(a, grid, st);
     case 32 * 10000 + 1024: return launch_rs_nt<8, 2, 128>(a, grid, st);
-    case 32 * 10000 + 2048: return launch_rs_nt<4, 2, 512>(a, grid, st);
+    case 32 * 10000 + 2048: return launch_rs_nt<8, 2, 256>(a, grid, st);
     case 64 * 10000 + 512: return launch_rs_nt<8, 4, 64>(a, grid, st);
     case 64 * 10000 + 1024: return launch_rs_nt<8, 4, 128>(a, grid, st);
-    case 64 * 10000 + 2048: return launch_rs_nt<4, 4, 512>(a, grid, st);
+    case 64 * 10000 + 2048: return launch_rs_nt<8, 4, 256>(a, grid, st);
     case 128 * 10000 + 512: return launch_rs_nt<8, 8, 64>(a, grid, st);
-    case 128 * 10000 + 1024: return launch_rs_nt<4, 8, 256>(a, grid, st);
+    case 128 * 10000 + 1024: return launch_rs_nt<8, 8, 128>(a, grid, st);
     default: return hipErrorInvalidValue;
   }
 }

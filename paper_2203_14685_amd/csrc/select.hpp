@@ -218,6 +218,102 @@ __device__ __forceinline__ void select_token(const float* lrow, int E, int k, in
   }
 }
 
+// ---------------------------------------------------------------- selection on a compile-time slice
+// The same selections for kernels that know E at compile time: lane j's SL =
+// E / P logits are read from LDS at once (`lslice` points at them; 8-byte
+// aligned for SL = 2, 16-byte aligned from SL = 4 on) and held in registers;
+// the maximum comes first and the softmax sum of the slice relative to it
+// second, so no step waits on the one before it.
+template <int SL>
+__device__ __forceinline__ void load_slice(const float* lslice, float (&v)[SL]) {
+  if constexpr (SL % 4 == 0) {
+#pragma unroll
+    for (int i = 0; i < SL; i += 4) {
+      const float4 q = *reinterpret_cast<const float4*>(lslice + i);
+      v[i] = q.x; v[i + 1] = q.y; v[i + 2] = q.z; v[i + 3] = q.w;
+    }
+  } else if constexpr (SL == 2) {
+    const float2 q = *reinterpret_cast<const float2*>(lslice);
+    v[0] = q.x; v[1] = q.y;
+  } else {
+#pragma unroll
+    for (int i = 0; i < SL; ++i) v[i] = lslice[i];
+  }
+}
+
+template <int SL>
+__device__ __forceinline__ float slice_max(const float (&v)[SL]) {
+  float mx = v[0];
+#pragma unroll
+  for (int i = 1; i < SL; ++i) mx = fmaxf(mx, v[i]);
+  return mx;
+}
+
+template <int SL>
+__device__ __forceinline__ float slice_expsum(const float (&v)[SL], float mx) {
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < SL; ++i) s += __expf(v[i] - mx);
+  return s;
+}
+
+// Top-k state of a slice: sorted insertion in expert order (an equal logit
+// never displaces a lower expert), with the slice's softmax sum.
+template <int KMAX, int SL>
+__device__ __forceinline__ void topk_of_slice(const float (&v)[SL], int e0, TopkState<KMAX>& tk) {
+  tk.init();
+  tk.m = slice_max(v);
+  tk.ssum = slice_expsum(v, tk.m);
+#pragma unroll
+  for (int i = 0; i < SL; ++i) tk.insert(v[i], e0 + i);
+}
+
+// P lanes per token, each with SL = E / P logits of its row at lrow + j * SL.
+template <int P, int KMAX, bool KTOP1, int SL>
+__device__ __forceinline__ void select_token_c(const float* lrow, int k, int normalize, int j, bool valid,
+                                               int32_t* ids, float* weights, int* hist_lds) {
+  constexpr int E = P * SL;
+  const int e0 = j * SL;
+  if constexpr (!KTOP1) {
+    float v[SL];
+    load_slice<SL>(lrow + e0, v);
+    TopkState<KMAX> tk;
+    topk_of_slice<KMAX, SL>(v, e0, tk);
+#pragma unroll
+    for (int msk = 1; msk < P; msk <<= 1) tk.merge_xor(msk);
+    if (valid && j == 0) {
+      tk.finish(k, normalize, ids, weights);
+#pragma unroll
+      for (int r = 0; r < KMAX; ++r)
+        if (r < k) atomicAdd(&hist_lds[r * E + tk.ti[r]], 1);
+    }
+  } else if (P % k == 0) {
+    // L = P / k lanes per group; lane j's experts lie in group j / L
+    const int L = P / k;
+    float v[SL];
+    load_slice<SL>(lrow + e0, v);
+    GroupBest gb;
+    gb.bv = v[0];
+    gb.bi = e0;
+#pragma unroll
+    for (int i = 1; i < SL; ++i) {
+      const bool up = v[i] > gb.bv;  // strict: the lower expert keeps a tie
+      gb.bv = up ? v[i] : gb.bv;
+      gb.bi = up ? e0 + i : gb.bi;
+    }
+    gb.gsum = slice_expsum(v, gb.bv);
+    for (int msk = 1; msk < L; msk <<= 1) gb.merge_xor(msk);
+    if (valid && j % L == 0) {
+      const int grp = j / L;
+      ids[grp] = gb.bi;
+      weights[grp] = 1.f / gb.gsum;
+      atomicAdd(&hist_lds[grp * E + gb.bi], 1);
+    }
+  } else {
+    select_token<P, KMAX, true>(lrow, E, k, normalize, j, valid, ids, weights, hist_lds);
+  }
+}
+
 // ---------------------------------------------------------------- wave-block histogram
 // hist[r][e][wb] = number of tokens of wave block wb whose rank-r choice is e.
 // Every wave of the block calls this (it synchronises the block); `active` waves
@@ -244,6 +340,43 @@ __device__ __forceinline__ void select_token_htopk(const float* lrow, int E, int
   for (int e = 0; e < slice; ++e) {
     const int ee = e0 + e;
     if (ee >= lo && ee < hi) tk.insert(lrow[ee], ee);
+  }
+#pragma unroll
+  for (int msk = 1; msk < P; msk <<= 1) tk.merge_xor(msk);
+  // the group holds the overall best: the full softmax sum relative to it
+  tk.m = t1.m;
+  tk.ssum = t1.ssum;
+  if (valid && j == 0) {
+    tk.finish(k, normalize, ids, weights);
+#pragma unroll
+    for (int r = 0; r < KMAX; ++r)
+      if (r < k) atomicAdd(&hist_lds[r * E + tk.ti[r]], 1);
+  }
+}
+
+// Hierarchical top-k on a compile-time slice (see select_token_c).
+template <int P, int KMAX, int SL>
+__device__ __forceinline__ void select_token_htopk_c(const float* lrow, int k, int Gs, int normalize, int j,
+                                                     bool valid, int32_t* ids, float* weights, int* hist_lds) {
+  constexpr int E = P * SL;
+  const int e0 = j * SL;
+  float v[SL];
+  load_slice<SL>(lrow + e0, v);
+  TopkState<1> t1;
+  topk_of_slice<1, SL>(v, e0, t1);
+#pragma unroll
+  for (int msk = 1; msk < P; msk <<= 1) t1.merge_xor(msk);
+  const int best = t1.ti[0] == kEmpty ? 0 : t1.ti[0];
+  const int lo = (best / Gs) * Gs, hi = lo + Gs;
+  TopkState<KMAX> tk;
+  tk.init();
+  // experts outside the group go in as empty entries, which never displace
+  // anything (no branch per logit)
+#pragma unroll
+  for (int i = 0; i < SL; ++i) {
+    const int ee = e0 + i;
+    const bool in = ee >= lo && ee < hi;
+    tk.insert(in ? v[i] : -INFINITY, in ? ee : kEmpty);
   }
 #pragma unroll
   for (int msk = 1; msk < P; msk <<= 1) tk.merge_xor(msk);

@@ -81,6 +81,23 @@ def test_dense_ties_logits_in(E, k, kind, normalize):
         _logits_case(S, E, k, kind, normalize, C, L)
 
 
+@pytest.mark.parametrize("S,E,k,kind,normalize", [
+    # histograms (k E rows of one count per 64-token wave block) past the
+    # one-launch scan-and-assign limit, so that the scan and the assignment run
+    # as two kernels: ragged wave-block counts (313, 516, 625), kTop1, top-8
+    # and E = 1024
+    (20000, 64, 2, 0, 1), (33000, 64, 1, 0, 0), (32768, 64, 4, 1, 0), (40000, 16, 8, 0, 1),
+    (9000, 1024, 2, 0, 0),
+])
+def test_scan_assign_histogram_sizes(S, E, k, kind, normalize):
+    announce(f"scan/assign S={S} E={E} k={k} kind={kind}")
+    rng = np.random.default_rng(S + E + k)
+    L = rng.integers(0, 3, size=(S, E)).astype(np.float32)
+    L[:, : max(1, E // 16)] += 1.0  # favoured experts overflow their capacity
+    for C in (1, cap(1.0, k, S, E) // 2, cap(1.25, k, S, E), S * k):
+        _logits_case(S, E, k, kind, normalize, C, L)
+
+
 def test_all_equal_logits_and_zero_signs():
     S, E = 300, 8
     announce("all-equal logits")

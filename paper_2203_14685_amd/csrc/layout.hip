@@ -31,9 +31,7 @@ namespace hetumoe {
 
 constexpr int kUnroll = 8;
 constexpr int kWideWaves = 16;  // token-major dispatch: one token per wave, 16 waves per block
-// The token-major combine backward with dw holds ~126 VGPRs, four waves per
-// SIMD: 16-wave blocks would run one at a time per CU.  Blocks of 8 balance
-// small batches better (workload of 8192 tokens, k = 2: 20.5 -> 18.5 us).
+// Waves per block of the choice-major combine backward (k > 1).
 constexpr int kBwdScatterWaves = 8;
 
 // Row kernels: kRowThreads threads, one 16-byte chunk each per step.
@@ -429,10 +427,12 @@ __global__ __launch_bounds__(kRowThreads) void token_rows_kernel(RowArgs a, int 
 
 // ---------------------------------------------------------------- token-major forms (k > 1)
 // With several choices per token, the slot-major gathers above read each token
-// row once per kept choice.  These forms read it once: blocks [0, tok_blocks)
-// take one token per wave and write (or, backward, scale and dot) its kept
-// rows; the remaining blocks stride over the expert slots and zero the empty
-// ones.  Each output row still has exactly one writer.
+// row once per kept choice, at times far apart.  These forms walk the choices
+// in token order instead: the dispatch takes one token per wave and writes its
+// kept rows; the combine backward takes one choice per wave, the choices of a
+// token side by side, so that the token row comes from memory once.  The
+// remaining blocks stride over the expert slots and zero the empty ones.  Each
+// output row still has exactly one writer.
 constexpr int kZeroBlocks = 1024;
 
 // first_wave is uniform over the wave (made so by the callers), so the rows,
@@ -482,85 +482,71 @@ __global__ __launch_bounds__(kWideWaves * kWave) void dispatch_scatter_kernel(Ro
 
 // For every kept (s, r): dye[ids, slots] = w[s,r] * dy[s] and, with DW,
 // dw[s,r] = <dy[s], ye[ids, slots]>; dropped choices get dw = 0; empty slots
-// of dye are zero.  One wave per token walks the row in steps of 4 chunks per
-// lane and issues the loads of up to 4 choices' ye rows together.
+// of dye are zero.  One wave per choice (s, r), the k waves of a token next to
+// each other in a block: dy[s] comes from memory for the first of them and
+// from the L2 for the others (cached loads), each ye row is read once
+// (non-temporal).  A wave per token carrying all k dot products held ~126
+// VGPRs; a wave per choice holds ~72 (workload of 32768 tokens, k = 4, 4 KiB
+// rows: 235 -> 207 us).
 template <typename T, bool DW>
-__global__ __launch_bounds__(kBwdScatterWaves * kWave) void combine_bwd_scatter_kernel(RowArgs a, int64_t tok_blocks) {
+__global__ __launch_bounds__(kBwdScatterWaves * kWave) void combine_bwd_scatter_kernel(RowArgs a, int64_t pair_blocks) {
   constexpr int kEl = Chunk<T>::kElems;
-  constexpr int kU = 4;   // chunks per lane per step
-  constexpr int kRG = 4;  // choices whose rows are loaded together
+  constexpr int kU = 4;  // chunks per lane per step
   const int lane = lane_id();
   const int wave = threadIdx.x / kWave;
-  if (static_cast<int64_t>(blockIdx.x) >= tok_blocks) {
+  if (static_cast<int64_t>(blockIdx.x) >= pair_blocks) {
     zero_empty_rows(a, __builtin_amdgcn_readfirstlane(
-                           static_cast<int>((static_cast<int64_t>(blockIdx.x) - tok_blocks) * kBwdScatterWaves + wave)),
-                    static_cast<int64_t>(gridDim.x - tok_blocks) * kBwdScatterWaves, lane);
+                           static_cast<int>((static_cast<int64_t>(blockIdx.x) - pair_blocks) * kBwdScatterWaves + wave)),
+                    static_cast<int64_t>(gridDim.x - pair_blocks) * kBwdScatterWaves, lane);
     return;
   }
-  // the token is uniform over the wave (scalar routing, row resources in scalar
-  // registers); chunks past a row fall outside its resource: loads give zeros,
-  // stores are dropped, so the row walk needs no bounds test
-  const int64_t s = __builtin_amdgcn_readfirstlane(static_cast<int>(static_cast<int64_t>(blockIdx.x) * kBwdScatterWaves + wave));
-  if (s >= a.S) return;
-  const int nch = a.nch, k = a.k;
+  // the choice is uniform over the wave (scalar routing, row resources in
+  // scalar registers); chunks past a row fall outside its resource: loads give
+  // zeros, stores are dropped, so the row walk needs no bounds test
+  const int64_t pr = __builtin_amdgcn_readfirstlane(static_cast<int>(static_cast<int64_t>(blockIdx.x) * kBwdScatterWaves + wave));
+  if (pr >= static_cast<int64_t>(a.S) * a.k) return;
+  const int slot = a.slots[pr];
+  const int e = a.ids[pr];
+  if (!((slot >= 0) & (slot < a.C) & (e >= 0) & (e < a.E))) {
+    if constexpr (DW)
+      if (lane == 0) a.dw[pr] = 0.f;
+    return;
+  }
+  const int nch = a.nch;
+  const int64_t s = pr / a.k;
+  const int64_t row = static_cast<int64_t>(e) * a.C + slot;
+  const float w = a.weights[pr];
   const __amdgpu_buffer_rsrc_t dyrow = buf_rsrc(reinterpret_cast<const u32x4*>(a.src) + s * nch, nch * 16);
-  float dot[8];
-#pragma unroll
-  for (int r = 0; r < 8; ++r) dot[r] = 0.f;
+  const __amdgpu_buffer_rsrc_t dst = buf_rsrc(reinterpret_cast<u32x4*>(a.dst) + row * nch, nch * 16);
+  float dot = 0.f;
   for (int base = 0; base < nch; base += kWave * kU) {
     u32x4 v[kU];
 #pragma unroll
-    for (int u = 0; u < kU; ++u) v[u] = buf_load_nt(dyrow, (base + u * kWave + lane) * 16);
+    for (int u = 0; u < kU; ++u) v[u] = __builtin_amdgcn_raw_buffer_load_b128(dyrow, (base + u * kWave + lane) * 16, 0, 0);
+    u32x4 g[DW ? kU : 1];
+    if constexpr (DW) {
+      const __amdgpu_buffer_rsrc_t yerow = buf_rsrc(reinterpret_cast<const u32x4*>(a.aux) + row * nch, nch * 16);
 #pragma unroll
-    for (int r0 = 0; r0 < 8; r0 += kRG) {
-      if (r0 >= k) break;
-      int64_t row[kRG];
-      bool kept[kRG];
-      u32x4 ve[DW ? kRG : 1][kU];
+      for (int u = 0; u < kU; ++u) g[u] = buf_load_nt(yerow, (base + u * kWave + lane) * 16);
+    }
 #pragma unroll
-      for (int j = 0; j < kRG; ++j) {
-        const int r = r0 + j;
-        const int slot = (r < k) ? a.slots[s * k + r] : -1;
-        const int e = (r < k) ? a.ids[s * k + r] : -1;
-        kept[j] = (slot >= 0) & (slot < a.C) & (e >= 0) & (e < a.E);
-        row[j] = kept[j] ? static_cast<int64_t>(e) * a.C + slot : 0;
-        if constexpr (DW) {
-          const __amdgpu_buffer_rsrc_t yerow =
-              buf_rsrc(reinterpret_cast<const u32x4*>(a.aux) + row[j] * nch, kept[j] ? nch * 16 : 0);
+    for (int u = 0; u < kU; ++u) {
+      float f[kEl];
+      Chunk<T>::unpack(v[u], f);
+      if constexpr (DW) {
+        float gq[kEl];
+        Chunk<T>::unpack(g[u], gq);
 #pragma unroll
-          for (int u = 0; u < kU; ++u) ve[j][u] = buf_load_nt(yerow, (base + u * kWave + lane) * 16);
-        }
+        for (int q = 0; q < kEl; ++q) dot = fmaf(f[q], gq[q], dot);
       }
 #pragma unroll
-      for (int j = 0; j < kRG; ++j) {
-        if (!kept[j]) continue;
-        const float w = a.weights[s * k + r0 + j];
-        const __amdgpu_buffer_rsrc_t dst = buf_rsrc(reinterpret_cast<u32x4*>(a.dst) + row[j] * nch, nch * 16);
-#pragma unroll
-        for (int u = 0; u < kU; ++u) {
-          const int i = base + u * kWave + lane;
-          float f[kEl];
-          Chunk<T>::unpack(v[u], f);
-          if constexpr (DW) {
-            float gq[kEl];
-            Chunk<T>::unpack(ve[j][u], gq);
-#pragma unroll
-            for (int q = 0; q < kEl; ++q) dot[r0 + j] = fmaf(f[q], gq[q], dot[r0 + j]);
-          }
-#pragma unroll
-          for (int q = 0; q < kEl; ++q) f[q] *= w;
-          buf_store_nt(Chunk<T>::pack(f), dst, i * 16);
-        }
-      }
+      for (int q = 0; q < kEl; ++q) f[q] *= w;
+      buf_store_nt(Chunk<T>::pack(f), dst, (base + u * kWave + lane) * 16);
     }
   }
   if constexpr (DW) {
-#pragma unroll
-    for (int r = 0; r < 8; ++r) {
-      if (r >= k) break;
-      const float t = wave_sum(dot[r]);
-      if (lane == 0) a.dw[s * k + r] = (a.slots[s * k + r] >= 0) ? t : 0.f;
-    }
+    const float t = wave_sum(dot);
+    if (lane == 0) a.dw[pr] = t;
   }
 }
 
@@ -691,16 +677,16 @@ hipError_t launch_combine(const RowArgs& a, bool weighted, hipStream_t st) {
 
 hipError_t launch_combine_bwd(const RowArgs& a, hipStream_t st) {
   if (a.k > 1) {
-    const int64_t tok_blocks = (static_cast<int64_t>(a.S) + kBwdScatterWaves - 1) / kBwdScatterWaves;
-    const unsigned grid = static_cast<unsigned>(tok_blocks) + zero_blocks(a.rows, kBwdScatterWaves);
+    const int64_t pair_blocks = (static_cast<int64_t>(a.S) * a.k + kBwdScatterWaves - 1) / kBwdScatterWaves;
+    const unsigned grid = static_cast<unsigned>(pair_blocks) + zero_blocks(a.rows, kBwdScatterWaves);
     if (grid == 0) return hipSuccess;
     const dim3 g(grid), block(kBwdScatterWaves * kWave);
     if (a.dtype == 1) {
-      if (a.dw) combine_bwd_scatter_kernel<bf16_t, true><<<g, block, 0, st>>>(a, tok_blocks);
-      else combine_bwd_scatter_kernel<bf16_t, false><<<g, block, 0, st>>>(a, tok_blocks);
+      if (a.dw) combine_bwd_scatter_kernel<bf16_t, true><<<g, block, 0, st>>>(a, pair_blocks);
+      else combine_bwd_scatter_kernel<bf16_t, false><<<g, block, 0, st>>>(a, pair_blocks);
     } else {
-      if (a.dw) combine_bwd_scatter_kernel<float, true><<<g, block, 0, st>>>(a, tok_blocks);
-      else combine_bwd_scatter_kernel<float, false><<<g, block, 0, st>>>(a, tok_blocks);
+      if (a.dw) combine_bwd_scatter_kernel<float, true><<<g, block, 0, st>>>(a, pair_blocks);
+      else combine_bwd_scatter_kernel<float, false><<<g, block, 0, st>>>(a, pair_blocks);
     }
     return hipGetLastError();
   }

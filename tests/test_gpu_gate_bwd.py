@@ -96,6 +96,10 @@ CASES = [
     (130, 448, 48, 1, 0, 0, "bf16", 0.01, False),       # 3 tiles, fewer than 4 chunks per range
     (900, 64, 80, 3, 0, 1, "bf16", 0.0, True),          # d = 64: one live wave per block
     (1500, 192, 128, 2, 0, 1, "bf16", 0.0, False),      # E = 128, one wave per SIMD
+    # first-choice counts past one block's batch (several count blocks), and a
+    # balance loss over more experts than one block of column sums holds
+    (70000, 64, 16, 1, 0, 0, "bf16", 0.02, False),
+    (66000, 128, 96, 2, 0, 1, "bf16", 0.03, True),
 ]
 
 

@@ -499,7 +499,7 @@ __global__ __launch_bounds__(kBwdThreads) __attribute__((amdgpu_waves_per_eu(NT 
 // Block: 64 tokens (wave w: 16) x 256 columns (4 passes of 64); blocks are
 // numbered column block first.  A[s][e] = dL
 // in three bf16 parts, kept in registers; B[e][j] = W[j][e] from the block's W
-// rows staged in LDS.  The 16 x 64 fp32 results go through LDS column-major
+// rows staged in LDS, two passes' rows in turn (one barrier per pass).  The 16 x 64 fp32 results go through LDS column-major
 // (each lane's 4 tokens of one column are contiguous: one 16-byte store; a
 // row-major tile written element by element was miscompiled, two of its LDS
 // stores merged with a wrong offset), then each lane adds the incoming dx to
@@ -578,12 +578,14 @@ __device__ __forceinline__ void dx_mfma_body(const GateBwdArgs& a, uint16_t* wl,
   for (int cb = 0; cb < 4; ++cb) {
     const int j0 = jb + cb * kWave;
     if (j0 >= a.d) break;  // the same for the whole block
-    __syncthreads();  // previous pass's W rows consumed
+    // W rows double buffered: pass cb - 2 last read this buffer, before the
+    // barrier of pass cb - 1, so one barrier per pass suffices
+    uint16_t* wb = wl + (cb & 1) * kWave * LDW;
 #pragma unroll
     for (int u = 0; u < WPT; ++u) {  // clamped like the loads: a repeated piece rewrites its own value
       const int q = min(threadIdx.x + u * kBwdThreads, kWave * (E / 8) - 1);
       const int r = q / (E / 8), p8 = q % (E / 8);
-      *reinterpret_cast<u32x4*>(&wl[r * LDW + 8 * p8]) = wreg[u];
+      *reinterpret_cast<u32x4*>(&wb[r * LDW + 8 * p8]) = wreg[u];
     }
     __syncthreads();
     load_w(j0 + kWave);
@@ -598,7 +600,7 @@ __device__ __forceinline__ void dx_mfma_body(const GateBwdArgs& a, uint16_t* wl,
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
         const int e0 = 32 * ks + 8 * g;
-        const u32x4 b = e0 < E ? *reinterpret_cast<const u32x4*>(&wl[(16 * nt + m) * LDW + e0]) : zero;
+        const u32x4 b = e0 < E ? *reinterpret_cast<const u32x4*>(&wb[(16 * nt + m) * LDW + e0]) : zero;
         acc[nt] = mfma_bf16(ah[ks], b, acc[nt]);
         acc[nt] = mfma_bf16(am[ks], b, acc[nt]);
         acc[nt] = mfma_bf16(al[ks], b, acc[nt]);
@@ -641,7 +643,7 @@ __device__ __forceinline__ void dx_mfma_body(const GateBwdArgs& a, uint16_t* wl,
 
 template <int NT, bool ACC>
 __global__ __launch_bounds__(kBwdThreads) void dx_mfma_kernel(GateBwdArgs a) {
-  __shared__ __align__(16) uint16_t wl[kWave * DxShape<NT>::LDW];
+  __shared__ __align__(16) uint16_t wl[2 * kWave * DxShape<NT>::LDW];
   __shared__ __align__(16) float ot[kBwdWaves * kWave * DxShape<NT>::LDT];
   const int ncb = (a.d + 4 * kWave - 1) / (4 * kWave);
   if ((static_cast<int64_t>(blockIdx.x / ncb) + 1) * kWave <= a.S) dx_mfma_body<NT, ACC, true>(a, wl, ot);

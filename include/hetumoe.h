@@ -245,8 +245,10 @@ MOE_API moe_status moe_base_gate_workspace_size(const moe_base_params* p, size_t
  * every token is within eps of its best L[s,e] - p[e].  info (host memory, may
  * be NULL) receives the auction's statistics.
  *
- * Unlike the other calls this one SYNCHRONIZES `stream`: the host reads the
- * number of unassigned tokens after every 8 rounds.  It returns
+ * Unlike the other calls this one SYNCHRONIZES `stream`: the host enqueues the
+ * auction's launches in batches (64, then 128 at a time; a launch that finds
+ * the auction finished returns at once) and reads its done flag after each
+ * batch.  It returns
  * MOE_ERR_NOT_CONVERGED when a phase reaches max_rounds, and
  * MOE_ERR_INVALID_ARG when a score is infinite or NaN (found on the device
  * after the projection); outputs are then undefined.

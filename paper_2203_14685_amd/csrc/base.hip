@@ -439,9 +439,9 @@ __device__ __forceinline__ void base_wave_bid(const BaseArgs& a, const double* p
   }
 #pragma unroll
   for (int off = 1; off < kWave; off <<= 1) {
-    const double ov1 = __shfl_xor(v1, off, kWave), ov2 = __shfl_xor(v2, off, kWave);
-    const double ol1 = __shfl_xor(l1, off, kWave);
-    const int oe1 = __shfl_xor(e1, off, kWave);
+    const double ov1 = xor_partner(v1, off), ov2 = xor_partner(v2, off);
+    const double ol1 = xor_partner(l1, off);
+    const int oe1 = xor_partner(e1, off);
     if (ov1 > v1 || (ov1 == v1 && oe1 < e1)) {
       v2 = fmax(ov2, v1);
       v1 = ov1;
@@ -492,11 +492,8 @@ __device__ __forceinline__ int base_wave_place(const BaseArgs& a, double* pr, in
       if (i == c - 2) vlast = hv[q];
     }
   }
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    p += __shfl_xor(p, off, kWave);
-    ev = max(ev, __shfl_xor(ev, off, kWave));
-  }
+  p = group_reduce<kWave>(p, OpAdd());
+  ev = group_reduce<kWave>(ev, OpMaxI());
   vlast = __shfl(vlast, (c - 2) & (kWave - 1), kWave);
   bad = p >= c;
   if (bad) return -1;
@@ -563,8 +560,7 @@ __device__ __forceinline__ void base_wave_merge(const BaseArgs& a, double* pr, i
         ahead[q] += b_first;
         cnt += !b_first;
       }
-#pragma unroll
-      for (int off = 32; off >= 1; off >>= 1) cnt += __shfl_xor(cnt, off, kWave);
+      cnt = group_reduce<kWave>(cnt, OpAdd());
       if (lane == b) ahead_b += cnt;
     }
 #pragma unroll

@@ -103,10 +103,106 @@ __device__ __forceinline__ int popc_below(uint64_t mask) {
                                    __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u));
 }
 
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, kWave);
+// Value of lane (lane ^ M) for M = 1, 2, 4, 8, 16 or 32, bit for bit what a
+// shuffle gives, without a trip through the LDS crossbar: M = 1 and 2
+// are DPP quad permutations, M = 8 the DPP rotation of each 16-lane row by 8,
+// M = 4 two DPP row shifts, each writing half of the lanes, M = 16 and 32 the
+// gfx950 permlane swaps (each lane gets back its own value and its partner's:
+// the one that differs from its own is the partner's, and if neither differs
+// the two are equal).
+template <int M>
+__device__ __forceinline__ int xor_partner_i(int iv) {
+  if constexpr (M == 1 || M == 2 || M == 8) {
+    constexpr int ctrl = M == 1 ? 0xB1 : M == 2 ? 0x4E : 0x128;
+    return __builtin_amdgcn_update_dpp(iv, iv, ctrl, 0xF, 0xF, false);
+  } else if constexpr (M == 4) {
+    // lanes 0-3 and 8-11 of each row (DPP banks 0 and 2) read 4 lanes up
+    // (row_shl:4), lanes 4-7 and 12-15 (banks 1 and 3) 4 lanes down (row_shr:4);
+    // the banks a move does not write keep the other move's value
+    const int up = __builtin_amdgcn_update_dpp(iv, iv, 0x104, 0xF, 0x5, false);
+    return __builtin_amdgcn_update_dpp(up, iv, 0x114, 0xF, 0xA, false);
+  } else if constexpr (M == 16) {
+    const auto r = __builtin_amdgcn_permlane16_swap(iv, iv, false, false);
+    return static_cast<int>(r[0]) == iv ? static_cast<int>(r[1]) : static_cast<int>(r[0]);
+  } else {
+    static_assert(M == 32, "M is a power of two up to 32");
+    const auto r = __builtin_amdgcn_permlane32_swap(iv, iv, false, false);
+    return static_cast<int>(r[0]) == iv ? static_cast<int>(r[1]) : static_cast<int>(r[0]);
+  }
+}
+
+template <int M, class T>
+__device__ __forceinline__ T xor_partner(T v) {
+  if constexpr (sizeof(T) == 4) {
+    return __builtin_bit_cast(T, xor_partner_i<M>(__builtin_bit_cast(int, v)));
+  } else {
+    static_assert(sizeof(T) == 8, "32- or 64-bit values");
+    const uint64_t u = __builtin_bit_cast(uint64_t, v);
+    const uint32_t lo = static_cast<uint32_t>(xor_partner_i<M>(static_cast<int>(u)));
+    const uint32_t hi = static_cast<uint32_t>(xor_partner_i<M>(static_cast<int>(u >> 32)));
+    return __builtin_bit_cast(T, (static_cast<uint64_t>(hi) << 32) | lo);
+  }
+}
+
+// The same for a mask (1, 2, 4, 8, 16 or 32) known only at run time and equal on
+// all lanes; a constant mask folds to its case.
+template <class T>
+__device__ __forceinline__ T xor_partner(T v, int mask) {
+  switch (mask) {
+    case 1: return xor_partner<1>(v);
+    case 2: return xor_partner<2>(v);
+    case 4: return xor_partner<4>(v);
+    case 8: return xor_partner<8>(v);
+    case 16: return xor_partner<16>(v);
+    default: return xor_partner<32>(v);
+  }
+}
+
+// op(v, value of lane ^ M) for a commutative `op`.
+template <int M, class T, class Op>
+__device__ __forceinline__ T xor_step(T v, Op op) {
+  if constexpr (M == 16 || M == 32) {
+    // the swap's two results are the lane's own value and its partner's
+    static_assert(sizeof(T) == 4, "32-bit values");
+    const int iv = __builtin_bit_cast(int, v);
+    const auto r = M == 16 ? __builtin_amdgcn_permlane16_swap(iv, iv, false, false)
+                           : __builtin_amdgcn_permlane32_swap(iv, iv, false, false);
+    return op(__builtin_bit_cast(T, static_cast<int>(r[0])), __builtin_bit_cast(T, static_cast<int>(r[1])));
+  } else {
+    return op(v, xor_partner<M>(v));
+  }
+}
+
+// All-reduce over aligned groups of G lanes (G a power of two up to 64): the
+// butterfly steps M = 1 .. G / 2 in increasing order.  Step 4 pairs lane i with
+// lane 7 - i of its 8 (the DPP half-row mirror) instead of i ^ 4: after steps 1
+// and 2 every aligned group of 4 lanes holds one value, so both partners hold
+// the same and the result is the shuffle butterfly's bit for bit.
+template <int G, class T, class Op>
+__device__ __forceinline__ T group_reduce(T v, Op op) {
+  if constexpr (G >= 2) v = xor_step<1>(v, op);
+  if constexpr (G >= 4) v = xor_step<2>(v, op);
+  if constexpr (G >= 8) {
+    const int iv = __builtin_bit_cast(int, v);
+    v = op(v, __builtin_bit_cast(T, __builtin_amdgcn_update_dpp(iv, iv, 0x141, 0xF, 0xF, false)));
+  }
+  if constexpr (G >= 16) v = xor_step<8>(v, op);
+  if constexpr (G >= 32) v = xor_step<16>(v, op);
+  if constexpr (G >= 64) v = xor_step<32>(v, op);
   return v;
 }
+
+struct OpAdd {
+  template <class T>
+  __device__ __forceinline__ T operator()(T a, T b) const { return a + b; }
+};
+struct OpMaxI {
+  __device__ __forceinline__ int operator()(int a, int b) const { return a > b ? a : b; }
+};
+struct OpMaxF {
+  __device__ __forceinline__ float operator()(float a, float b) const { return fmaxf(a, b); }
+};
+
+__device__ __forceinline__ float wave_sum(float v) { return group_reduce<kWave>(v, OpAdd()); }
 
 }  // namespace hetumoe

@@ -22,15 +22,24 @@ constexpr int kBwdThreads = kBwdWaves * kWave;
 
 template <int P>
 __device__ __forceinline__ float group_max(float v) {
-#pragma unroll
-  for (int m = 1; m < P; m <<= 1) v = fmaxf(v, __shfl_xor(v, m));
-  return v;
+  return group_reduce<P>(v, OpMaxF());
 }
 
 template <int P>
 __device__ __forceinline__ float group_sum(float v) {
-#pragma unroll
-  for (int m = 1; m < P; m <<= 1) v += __shfl_xor(v, m);
+  return group_reduce<P>(v, OpAdd());
+}
+
+// Sum over the lanes that hold the same position within their group of P, i.e.
+// over lanes l, l + P, l + 2P, ... (the butterfly steps M = P .. 32).
+template <int P>
+__device__ __forceinline__ float across_groups_sum(float v) {
+  if constexpr (P <= 1) v = xor_step<1>(v, OpAdd());
+  if constexpr (P <= 2) v = xor_step<2>(v, OpAdd());
+  if constexpr (P <= 4) v = xor_step<4>(v, OpAdd());
+  if constexpr (P <= 8) v = xor_step<8>(v, OpAdd());
+  if constexpr (P <= 16) v = xor_step<16>(v, OpAdd());
+  if constexpr (P <= 32) v = xor_step<32>(v, OpAdd());
   return v;
 }
 
@@ -286,11 +295,10 @@ __global__ __launch_bounds__(WAVES * kWave) void gate_dl_kernel(GateBwdArgs a) {
   }
   // sums over the token lanes of each wave
 #pragma unroll
-  for (int i = 0; i < EPL; ++i)
-    for (int msk = P; msk < kWave; msk <<= 1) {
-      bsum[i] += __shfl_xor(bsum[i], msk);
-      psum[i] += __shfl_xor(psum[i], msk);
-    }
+  for (int i = 0; i < EPL; ++i) {
+    bsum[i] = across_groups_sum<P>(bsum[i]);
+    psum[i] = across_groups_sum<P>(psum[i]);
+  }
   __syncthreads();  // dL tile complete
   if (a.dlt) {
     const int64_t plane = static_cast<int64_t>(E) * a.s_pad;

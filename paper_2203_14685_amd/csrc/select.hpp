@@ -62,8 +62,8 @@ struct TopkState {
     int ci[KMAX];
 #pragma unroll
     for (int i = 0; i < KMAX; ++i) {
-      const float pv = __shfl_xor(tv[KMAX - 1 - i], mask, kWave);
-      const int pi = __shfl_xor(ti[KMAX - 1 - i], mask, kWave);
+      const float pv = xor_partner(tv[KMAX - 1 - i], mask);
+      const int pi = xor_partner(ti[KMAX - 1 - i], mask);
       const bool mine = better(tv[i], ti[i], pv, pi);
       cv[i] = mine ? tv[i] : pv;
       ci[i] = mine ? ti[i] : pi;
@@ -85,8 +85,8 @@ struct TopkState {
     }
 #pragma unroll
     for (int i = 0; i < KMAX; ++i) { tv[i] = cv[i]; ti[i] = ci[i]; }
-    const float pm = __shfl_xor(m, mask, kWave);
-    const float ps = __shfl_xor(ssum, mask, kWave);
+    const float pm = xor_partner(m, mask);
+    const float ps = xor_partner(ssum, mask);
     const float nm = fmaxf(m, pm);
     // a side that has seen nothing has m = -inf and ssum = 0: contributes 0
     const float a = (ssum > 0.f) ? ssum * __expf(m - nm) : 0.f;
@@ -130,9 +130,9 @@ struct GroupBest {
     else { gsum += __expf(v - bv); }
   }
   __device__ __forceinline__ void merge_xor(int mask) {
-    const float pv = __shfl_xor(bv, mask, kWave);
-    const int pi = __shfl_xor(bi, mask, kWave);
-    const float ps = __shfl_xor(gsum, mask, kWave);
+    const float pv = xor_partner(bv, mask);
+    const int pi = xor_partner(bi, mask);
+    const float ps = xor_partner(gsum, mask);
     if (pi == kEmpty) return;
     if (bi == kEmpty) { bv = pv; bi = pi; gsum = ps; return; }
     const bool partner_wins = pv > bv || (pv == bv && pi < bi);

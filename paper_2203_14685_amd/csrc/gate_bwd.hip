@@ -517,40 +517,52 @@ struct DxShape {
   static constexpr int E = 16 * NT;
   static constexpr int KS = (E + 31) / 32;  // K steps of 32 experts (a half step when E % 32 == 16)
   static constexpr int LDW = E + 8;         // padded W row in LDS (bf16)
-  static constexpr int LDT = 16 + 4;        // padded column of the output tile (fp32, 16 tokens)
 };
 
 // FULL: all 64 tokens of the block exist (every block but a ragged last one),
 // so no token test splits the code: a branch around a load or a store makes
 // the compiler wait for every outstanding memory operation (stores and loads
 // share one in-order counter).
+//
+// The product is taken transposed, dx^T = W dL^T: W rows are the A operand and
+// the wave's 16 tokens of dL the B operand, so lane (g, m) of a 16 x 16 tile
+// ends up with 4 consecutive columns of token m.  A swap of rows between the
+// accumulators of tiles 0 and 1 (and of 2 and 3) gives every lane 8
+// consecutive columns of its token, and a rotation by 8 lanes within each row
+// regroups them so that one store covers 8 tokens x 128 bytes: whole 128-byte
+// lines, which is what keeps the store stream fast while the memory is also
+// writing back what earlier kernels left dirty.  No LDS transpose.
 template <int NT, bool ACC, bool FULL>
-__device__ __forceinline__ void dx_mfma_body(const GateBwdArgs& a, uint16_t* wl, float* ot) {
-  constexpr int E = DxShape<NT>::E, KS = DxShape<NT>::KS, LDW = DxShape<NT>::LDW, LDT = DxShape<NT>::LDT;
+__device__ __forceinline__ void dx_mfma_body(const GateBwdArgs& a, uint16_t* wl) {
+  constexpr int E = DxShape<NT>::E, KS = DxShape<NT>::KS, LDW = DxShape<NT>::LDW;
   const int w = threadIdx.x / kWave, lane = lane_id();
   const int g = lane / 16, m = lane % 16;
   const int ncb = (a.d + 4 * kWave - 1) / (4 * kWave);  // column blocks of 256
   const int64_t tb = blockIdx.x / ncb;                   // 64-token block
-  const int64_t s0 = tb * kWave + 16 * w;
+  const int64_t s0 = tb * kWave + 16 * w;               // the wave's first token
+  const int64_t sm = s0 + m;                             // this lane's token in the product
+  const bool tok_ok = FULL || sm < a.S;
   const uint16_t* wg = reinterpret_cast<const uint16_t*>(a.wg);
-  uint16_t* dxp = reinterpret_cast<uint16_t*>(a.dx);
+  // tokens of this lane's two pieces of dx: 8 h + (m & 7)
+  const int64_t sp0 = s0 + (m & 7), sp1 = s0 + 8 + (m & 7);
+  const bool ok0 = FULL || sp0 < a.S, ok1 = FULL || sp1 < a.S;
+  uint16_t* dxr0 = reinterpret_cast<uint16_t*>(a.dx) + (ok0 ? sp0 : 0) * a.d;
+  uint16_t* dxr1 = reinterpret_cast<uint16_t*>(a.dx) + (ok1 ? sp1 : 0) * a.d;
   const u32x4 zero = {0u, 0u, 0u, 0u};
 
   u32x4 ah[KS], am[KS], al[KS];
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) {
     const int e0 = 32 * ks + 8 * g;
-    const int64_t s = s0 + m;
     float vv[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    if ((FULL || s < a.S) && e0 < E) {
-      const float4 p0 = *reinterpret_cast<const float4*>(a.dl + s * E + e0);
-      const float4 p1 = *reinterpret_cast<const float4*>(a.dl + s * E + e0 + 4);
+    if (tok_ok && e0 < E) {
+      const float4 p0 = *reinterpret_cast<const float4*>(a.dl + sm * E + e0);
+      const float4 p1 = *reinterpret_cast<const float4*>(a.dl + sm * E + e0 + 4);
       vv[0] = p0.x; vv[1] = p0.y; vv[2] = p0.z; vv[3] = p0.w;
       vv[4] = p1.x; vv[5] = p1.y; vv[6] = p1.z; vv[7] = p1.w;
     }
     split8(vv, ah[ks], am[ks], al[ks]);
   }
-  float* out = ot + w * kWave * LDT;
   const int jb = static_cast<int>(blockIdx.x % ncb) * 4 * kWave;
   // Loads are unconditional (clamped addresses; a value past the end is never
   // used), so that no branch hides one from the wait counts, and they are
@@ -568,16 +580,16 @@ __device__ __forceinline__ void dx_mfma_body(const GateBwdArgs& a, uint16_t* wl,
       wreg[u] = *reinterpret_cast<const u32x4*>(wg + static_cast<int64_t>(row) * E + 8 * p8);
     }
   };
-  // lane -> two chunks of 8 columns of one token (chunk id = lane + 64 h)
+  // lane (g, m): piece h of a pass is token 8 h + (m & 7), 8 columns at
+  // 32 (m >> 3) + cofs
+  const int cofs = 16 * (g & 1) + 8 * (g >> 1), pcol = 32 * (m >> 3) + cofs;
   auto dx_at = [&](int h, int j0) {
-    const int id = lane + kWave * h, t = id / 8, c8 = id % 8;
-    const int64_t s = s0 + t;
-    return reinterpret_cast<u32x4*>(dxp + ((FULL || s < a.S) ? s : 0) * a.d + min(j0, a.d - kWave) + 8 * c8);
+    return reinterpret_cast<u32x4*>((h ? dxr1 : dxr0) + min(j0, a.d - kWave) + pcol);
   };
   u32x4 din[2] = {zero, zero}, dnx[2] = {zero, zero};
   if constexpr (ACC) {
 #pragma unroll
-    for (int h = 0; h < 2; ++h) din[h] = *dx_at(h, jb);
+    for (int p = 0; p < 2; ++p) din[p] = *dx_at(p, jb);
   }
   load_w(jb);
   // unrolled, so that handing the prefetched dx to the next pass is a renaming,
@@ -599,36 +611,68 @@ __device__ __forceinline__ void dx_mfma_body(const GateBwdArgs& a, uint16_t* wl,
     load_w(j0 + kWave);
     if constexpr (ACC) {
 #pragma unroll
-      for (int h = 0; h < 2; ++h) dnx[h] = *dx_at(h, j0 + kWave);
+      for (int p = 0; p < 2; ++p) dnx[p] = *dx_at(p, j0 + kWave);
     }
     f32x4 acc[4];
+    // the W fragments of two tiles read from LDS together, then their products
 #pragma unroll
-    for (int nt = 0; nt < 4; ++nt) {
-      acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int hh = 0; hh < 2; ++hh) {
+      u32x4 bw[2][KS];
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const int e0 = 32 * ks + 8 * g;
-        const u32x4 b = e0 < E ? *reinterpret_cast<const u32x4*>(&wb[(16 * nt + m) * LDW + e0]) : zero;
-        acc[nt] = mfma_bf16(ah[ks], b, acc[nt]);
-        acc[nt] = mfma_bf16(am[ks], b, acc[nt]);
-        acc[nt] = mfma_bf16(al[ks], b, acc[nt]);
+      for (int q = 0; q < 2; ++q)
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          const int e0 = 32 * ks + 8 * g;
+          bw[q][ks] = e0 < E ? *reinterpret_cast<const u32x4*>(&wb[(16 * (2 * hh + q) + m) * LDW + e0]) : zero;
+        }
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        const int nt = 2 * hh + q;
+        acc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          acc[nt] = mfma_bf16(bw[q][ks], ah[ks], acc[nt]);
+          acc[nt] = mfma_bf16(bw[q][ks], am[ks], acc[nt]);
+          acc[nt] = mfma_bf16(bw[q][ks], al[ks], acc[nt]);
+        }
       }
     }
-    // lane (g, m) holds tokens 4 g + i of column 16 nt + m; the tile is the
-    // wave's own, so wave-level fences order it
+    // lane (g, m) holds columns 16 nt + 4 g + i of token m.  The permlane16
+    // swap exchanges odd rows of its first operand with even rows of its
+    // second: lanes of even g keep tile 2p's columns 4 g.. and get tile 2p's
+    // 4 (g + 1).. from lane g + 1; lanes of odd g get tile 2p + 1's 4 (g - 1)..
+    // and keep their own 4 g.. of it: X (p = 0) and Y (p = 1) hold 8 columns
+    // at 32 p + cofs of token m.  (The vector components are copied to scalars
+    // first: a bit cast taken straight from a component of an ext-vector reads
+    // component 0.)
+    float xv[8], yv[8];
 #pragma unroll
-    for (int nt = 0; nt < 4; ++nt)
-      *reinterpret_cast<float4*>(&out[(16 * nt + m) * LDT + 4 * g]) =
-          make_float4(acc[nt][0], acc[nt][1], acc[nt][2], acc[nt][3]);
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    for (int i = 0; i < 4; ++i) {
+      const float f0 = acc[0][i], f1 = acc[1][i], f2 = acc[2][i], f3 = acc[3][i];
+      const auto r = __builtin_amdgcn_permlane16_swap(__builtin_bit_cast(int, f0), __builtin_bit_cast(int, f1),
+                                                      false, false);
+      const auto q = __builtin_amdgcn_permlane16_swap(__builtin_bit_cast(int, f2), __builtin_bit_cast(int, f3),
+                                                      false, false);
+      xv[i] = __builtin_bit_cast(float, static_cast<int>(r[0]));
+      xv[4 + i] = __builtin_bit_cast(float, static_cast<int>(r[1]));
+      yv[i] = __builtin_bit_cast(float, static_cast<int>(q[0]));
+      yv[4 + i] = __builtin_bit_cast(float, static_cast<int>(q[1]));
+    }
+    // piece 0 (tokens 0-7): lanes m < 8 their own X, lanes m >= 8 the Y of lane
+    // m - 8; piece 1 (tokens 8-15): lanes m < 8 the X of lane m + 8, lanes
+    // m >= 8 their own Y.  Lane m meets lane m +- 8 by a DPP rotation of its
+    // 16-lane row by 8.
+    const bool lo = m < 8;
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      const int id = lane + kWave * h, t = id / 8, c8 = id % 8;
       float o[8];
 #pragma unroll
-      for (int q = 0; q < 8; ++q) o[q] = out[(8 * c8 + q) * LDT + t];
+      for (int i = 0; i < 8; ++i) {
+        const float keep = h == 0 ? xv[i] : yv[i];
+        const float moved = __builtin_bit_cast(
+            float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, h == 0 ? yv[i] : xv[i]), 0x128, 0xF, 0xF, false));
+        o[i] = (h == 0) == lo ? keep : moved;
+      }
       if constexpr (ACC) {
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
@@ -636,26 +680,25 @@ __device__ __forceinline__ void dx_mfma_body(const GateBwdArgs& a, uint16_t* wl,
           o[2 * q + 1] += bf16_hi(din[h][q]);
         }
       }
-      if (FULL || s0 + t < a.S)
+      if (h == 0 ? ok0 : ok1)
         __builtin_nontemporal_store(u32x4{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]),
                                           pack_bf16x2(o[4], o[5]), pack_bf16x2(o[6], o[7])},
                                     dx_at(h, j0));
     }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 #pragma unroll
-    for (int h = 0; h < 2; ++h) din[h] = dnx[h];
+    for (int p = 0; p < 2; ++p) din[p] = dnx[p];
   }
 }
 
+// Up to 64 experts the kernel fits four waves per SIMD (at most 128 registers);
+// more experts need more registers for the dL planes and take fewer waves.
 template <int NT, bool ACC>
-__global__ __launch_bounds__(kBwdThreads) void dx_mfma_kernel(GateBwdArgs a) {
+__global__ __launch_bounds__(kBwdThreads) __attribute__((amdgpu_waves_per_eu(NT <= 4 ? 4 : 1, NT <= 4 ? 4 : 8)))
+void dx_mfma_kernel(GateBwdArgs a) {
   __shared__ __align__(16) uint16_t wl[2 * kWave * DxShape<NT>::LDW];
-  __shared__ __align__(16) float ot[kBwdWaves * kWave * DxShape<NT>::LDT];
   const int ncb = (a.d + 4 * kWave - 1) / (4 * kWave);
-  if ((static_cast<int64_t>(blockIdx.x / ncb) + 1) * kWave <= a.S) dx_mfma_body<NT, ACC, true>(a, wl, ot);
-  else dx_mfma_body<NT, ACC, false>(a, wl, ot);
+  if ((static_cast<int64_t>(blockIdx.x / ncb) + 1) * kWave <= a.S) dx_mfma_body<NT, ACC, true>(a, wl);
+  else dx_mfma_body<NT, ACC, false>(a, wl);
 }
 
 // ---------------------------------------------------------------- dW, dx on the vector ALUs

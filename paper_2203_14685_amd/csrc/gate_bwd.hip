@@ -505,13 +505,10 @@ __global__ __launch_bounds__(kBwdThreads) __attribute__((amdgpu_waves_per_eu(NT 
 
 // ---------------------------------------------------------------- dx on matrix cores
 // Block: 64 tokens (wave w: 16) x 256 columns (4 passes of 64); blocks are
-// numbered column block first.  A[s][e] = dL
-// in three bf16 parts, kept in registers; B[e][j] = W[j][e] from the block's W
-// rows staged in LDS, two passes' rows in turn (one barrier per pass).  The 16 x 64 fp32 results go through LDS column-major
-// (each lane's 4 tokens of one column are contiguous: one 16-byte store; a
-// row-major tile written element by element was miscompiled, two of its LDS
-// stores merged with a wrong offset), then each lane adds the incoming dx to
-// two 8-column pieces of a token row and stores them, 16 bytes each.
+// numbered column block first.  dL of the wave's tokens is kept in registers
+// in three bf16 parts; the W rows of a pass are staged in LDS, two passes' rows
+// in turn (one barrier per pass).  Each lane adds the incoming dx to its two
+// 16-byte pieces of the result and stores them.
 template <int NT>
 struct DxShape {
   static constexpr int E = 16 * NT;

@@ -233,6 +233,22 @@ __global__ __launch_bounds__(WAVES * kWave) void gate_dl_kernel(GateBwdArgs a) {
       }
 #pragma unroll
       for (int i = 0; i < EPL; ++i) dl[i] -= p[i] * gsum;
+    } else if (EPL <= 8 && E == P * EPL && k == EPL) {
+      // kTop1 with groups of exactly P experts: element i of every lane is
+      // expert j + P i, which lies in group i, so the k groups' maxima and
+      // sums reduce side by side (the same arithmetic as the loop below)
+      float mg[EPL], sg[EPL];
+#pragma unroll
+      for (int i = 0; i < EPL; ++i) mg[i] = group_max<P>(v[i]);
+#pragma unroll
+      for (int i = 0; i < EPL; ++i) sg[i] = group_sum<P>(expf(v[i] - mg[i]));
+#pragma unroll
+      for (int i = 0; i < (EPL <= 8 ? EPL : 8); ++i) {
+        const int lo = i * P, id = idr[i];
+        if (id < lo || id >= lo + P) continue;
+        const float scale = dwr[i] * (expf(lr[i] - mg[i]) / sg[i]);
+        dl[i] += scale * ((j + P * i == id ? 1.f : 0.f) - expf(v[i] - mg[i]) / sg[i]);
+      }
     } else {
       // kTop1: softmax within each contiguous group of G experts
       const int G = E / k;

@@ -89,6 +89,8 @@ CASES = [
     (200, 64, 1024, 8, 0, 0, "f32", 0.05, False),       # 16 experts per lane
     (333, 128, 200, 2, 0, 1, "bf16", 0.0, True),        # E not a power of two
     (77, 512, 24, 3, 1, 0, "bf16", 0.0, False),         # kTop1 3 x 8
+    (500, 256, 16, 4, 1, 0, "f32", 0.0, False),         # kTop1 4 x 4: groups of one lane set (P = 4)
+    (600, 128, 32, 4, 1, 0, "bf16", 0.0, True),         # kTop1 4 x 8: groups of one lane set (P = 8)
     (1, 256, 8, 2, 0, 1, "f32", 0.0, True),
     (4100, 512, 32, 1, 0, 0, "f32", 0.1, False),        # several token ranges for dW
     # matrix-core dW: blocks of 256 columns with waves past d, 2..8 expert tiles

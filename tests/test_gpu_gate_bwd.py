@@ -102,6 +102,10 @@ CASES = [
     # balance loss over more experts than one block of column sums holds
     (70000, 64, 16, 1, 0, 0, "bf16", 0.02, False),
     (66000, 128, 96, 2, 0, 1, "bf16", 0.03, True),
+    # matrix-core dW over 47 token ranges with a ragged batch, and over 64
+    # ranges at E = 32
+    (12000, 1024, 16, 2, 0, 1, "bf16", 0.0, True),
+    (16400, 512, 32, 1, 0, 0, "bf16", 0.01, True),
 ]
 
 

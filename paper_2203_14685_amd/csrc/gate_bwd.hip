@@ -164,21 +164,35 @@ __global__ __launch_bounds__(WAVES * kWave) void gate_dl_kernel(GateBwdArgs a) {
       dl[i] = 0.f;
       p[i] = 0.f;
     }
-    // chosen experts, their gradients and logits (out-of-range ids are ignored)
+    // chosen experts and their gradients, loaded together (out-of-range ids
+    // are ignored); the chosen logits come from the token's own lanes: expert
+    // e is element e / P of lane e % P of the token
     int idr[8];
     float dwr[8], lr[8];
 #pragma unroll
     for (int r = 0; r < 8; ++r) {
-      idr[r] = -1;
-      dwr[r] = 0.f;
+      int e = -1;
+      float g = 0.f;
+      if (r < k) {
+        const int64_t q = (valid ? s : 0) * k + r;
+        e = a.ids[q];
+        g = a.dw[q];
+      }
+      const bool ok = valid && e >= 0 && e < E;
+      idr[r] = ok ? e : -1;
+      dwr[r] = ok ? g : 0.f;
+    }
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
       lr[r] = -INFINITY;
-      if (r < k && valid) {
-        const int e = a.ids[s * k + r];
-        if (e >= 0 && e < E) {
-          idr[r] = e;
-          dwr[r] = a.dw[s * k + r];
-          lr[r] = lrow[e];
-        }
+      if (r < k) {
+        const int e = idr[r] >= 0 ? idr[r] : 0;
+        float cand = v[0];
+#pragma unroll
+        for (int i = 1; i < EPL; ++i)
+          if (e / P == i) cand = v[i];
+        const float got = __shfl(cand, (lane & ~(P - 1)) | (e % P), kWave);
+        lr[r] = idr[r] >= 0 ? got : -INFINITY;
       }
     }
     float m = 0.f, se = 1.f;

@@ -71,14 +71,16 @@ __device__ __forceinline__ f32x4 mfma_bf16(const u32x4& a, const u32x4& b, const
 // ---------------------------------------------------------------- column sums
 // out[e] = sum over rows b of part[b][e]: 16 threads per column take rows
 // q, q + 16, ... in order, then their 16 sums are added in order.
+// Column sums of part [rows, E] for the 64 columns of column block cb, 16
+// threads per column (1024 threads): 8 rows' loads in flight, added in row
+// order, then the 16 partial sums in order.  Returns the total on the threads
+// of the first wave (q == 0) and writes it to out[e].
 template <typename T>
-__global__ __launch_bounds__(1024) void colsum_kernel(const T* part, int64_t rows, int E, T* out) {
-  __shared__ T red[16][kWave];
+__device__ __forceinline__ T colsum_cols(const T* part, int64_t rows, int E, T* out, int cb, T (*red)[kWave]) {
   const int q = threadIdx.x / kWave, c = threadIdx.x % kWave;
-  const int e = blockIdx.x * kWave + c;
+  const int e = cb * kWave + c;
   T v = 0;
   if (e < E) {
-    // 8 rows' loads in flight, then added in row order
     for (int64_t b0 = q; b0 < rows; b0 += 16 * 8) {
       T t[8];
 #pragma unroll
@@ -92,11 +94,18 @@ __global__ __launch_bounds__(1024) void colsum_kernel(const T* part, int64_t row
   }
   red[q][c] = v;
   __syncthreads();
+  T t = 0;
   if (q == 0 && e < E) {
-    T t = 0;
     for (int i = 0; i < 16; ++i) t += red[i][c];
     out[e] = t;
   }
+  return t;
+}
+
+template <typename T>
+__global__ __launch_bounds__(1024) void colsum_kernel(const T* part, int64_t rows, int E, T* out) {
+  __shared__ T red[16][kWave];
+  colsum_cols(part, rows, E, out, blockIdx.x, red);
 }
 
 // ---------------------------------------------------------------- first choices
@@ -382,6 +391,28 @@ __global__ __launch_bounds__(1024) void aux_loss_kernel(GateBwdArgs a) {
     __syncthreads();
   }
   if (t == 0) a.aux_loss[0] = a.aux_coef * static_cast<float>(a.E) * red[0];
+}
+
+// db and the balance loss side by side in one launch (E <= 64): with dbias,
+// block 0 sums the per-wave-block dL sums into it; the last block sums the
+// softmax sums into pe and then forms the loss from them (first-choice counts
+// cnt), so no block waits for another.
+__global__ __launch_bounds__(1024) void dl_sums_loss_kernel(GateBwdArgs a) {
+  __shared__ float red[16][kWave];
+  if (a.dbias && blockIdx.x == 0) {
+    colsum_cols(a.bpart, a.nb, a.E, a.dbias, 0, red);
+    return;
+  }
+  const float pe = colsum_cols(a.ppart, a.nb, a.E, a.pe, 0, red);
+  if (threadIdx.x >= kWave) return;  // the loss is the first wave's (a whole wave)
+  const int e = threadIdx.x;
+  float term = 0.f;
+  if (e < a.E && a.S > 0) {
+    const float inv_s = 1.f / static_cast<float>(a.S);
+    term = (static_cast<float>(a.cnt[e]) * inv_s) * (pe * inv_s);
+  }
+  term = wave_sum(term);
+  if (e == 0) a.aux_loss[0] = a.aux_coef * static_cast<float>(a.E) * term;
 }
 
 // ---------------------------------------------------------------- dW on matrix cores
@@ -895,6 +926,11 @@ hipError_t launch_gate_bwd_dl(const GateBwdArgs& a, hipStream_t st) {
     else if (E <= 256) launch_dl_t<64, 4>(a, st);
     else if (E <= 512) launch_dl_t<64, 8>(a, st);
     else launch_dl_t<64, 16>(a, st);
+  }
+  if (aux && a.aux_loss && a.E <= kWave) {
+    // db and the loss in one launch (block 0: db, block 1: softmax sums, loss)
+    dl_sums_loss_kernel<<<dim3(a.dbias ? 2 : 1), dim3(1024), 0, st>>>(a);
+    return hipGetLastError();
   }
   if (a.dbias) launch_colsum_f(a.bpart, a.nb, a.E, a.dbias, st);
   if (aux && a.aux_loss) {

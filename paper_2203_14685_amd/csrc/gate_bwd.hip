@@ -127,6 +127,23 @@ __global__ __launch_bounds__(1024) void aux_counts_kernel(GateBwdArgs a, int32_t
   for (int e = threadIdx.x; e < a.E; e += blockDim.x) cpart[static_cast<int64_t>(blockIdx.x) * a.E + e] = h[e];
 }
 
+// With at most kCountRowsInline rows of partial counts there is no column-sum
+// launch: the dL blocks stage the rows in LDS and add them up themselves, as
+// do the loss kernels (integer sums: exact in any order).
+constexpr int kCountRowsInline = 16;
+
+__host__ __device__ inline int count_rows(int S) { return (S + kCountTokens - 1) / kCountTokens; }
+
+// First-choice count of expert e for the loss kernels.
+__device__ __forceinline__ int first_count(const GateBwdArgs& a, int e) {
+  const int rows = count_rows(a.S);
+  if (rows > kCountRowsInline) return a.cnt[e];
+  const int32_t* cpart = a.cnt + a.E;
+  int c = 0;
+  for (int r = 0; r < rows; ++r) c += cpart[static_cast<int64_t>(r) * a.E + e];
+  return c;
+}
+
 // ---------------------------------------------------------------- dL
 // One block per 64-token wave block of WAVES waves, each taking 64 / WAVES
 // tokens.  P lanes per token (a power of two, 4 <= P <= 64), EPL experts per
@@ -140,7 +157,8 @@ __global__ __launch_bounds__(WAVES * kWave) void gate_dl_kernel(GateBwdArgs a) {
   constexpr int TW = kWave / WAVES;              // tokens per wave
   constexpr int PASSES = TW / TP;
   static_assert(TW % TP == 0, "whole passes");
-  extern __shared__ float sh[];  // [64][E + 1] dL tile (dlt only), then [2][WAVES][E] sums
+  extern __shared__ float sh[];  // [64][E + 1] dL tile (dlt only), then [2][WAVES][E] sums;
+                                 // the partial counts after the larger of the two
   const int lane = lane_id();
   const int w = threadIdx.x / kWave;
   const int j = lane % P, sub = lane / P;
@@ -151,11 +169,13 @@ __global__ __launch_bounds__(WAVES * kWave) void gate_dl_kernel(GateBwdArgs a) {
   const bool full_softmax = topk && (a.normalize == 0 || aux);
   const float inv_s = a.S > 0 ? 1.f / static_cast<float>(a.S) : 0.f;
   const float c_aux = a.aux_coef * static_cast<float>(E) * inv_s;
+  // first-choice counts: cnt, or the partial rows added up here (below)
+  const int crows = aux && count_rows(a.S) <= kCountRowsInline ? count_rows(a.S) : 0;
   float f[EPL], psum[EPL], bsum[EPL];
 #pragma unroll
   for (int i = 0; i < EPL; ++i) {
     const int e = j + P * i;
-    f[i] = (aux && e < E) ? static_cast<float>(a.cnt[e]) * inv_s : 0.f;
+    f[i] = (aux && crows == 0 && e < E) ? static_cast<float>(a.cnt[e]) * inv_s : 0.f;
     psum[i] = 0.f;
     bsum[i] = 0.f;
   }
@@ -190,6 +210,23 @@ __global__ __launch_bounds__(WAVES * kWave) void gate_dl_kernel(GateBwdArgs a) {
       const bool ok = valid && e >= 0 && e < E;
       idr[r] = ok ? e : -1;
       dwr[r] = ok ? g : 0.f;
+    }
+    if (pass == 0 && crows > 0) {
+      // the partial counts, one load per thread, issued after this pass's
+      // logits so that the two latencies overlap; staged past the tile and
+      // the sums, so nothing overwrites them
+      int* cs = reinterpret_cast<int*>(sh + max(a.dlt ? kWave * (E + 1) : 0, 2 * WAVES * E));
+      const int32_t* cpart = a.cnt + E;
+      for (int q = threadIdx.x; q < crows * E; q += WAVES * kWave) cs[q] = cpart[q];
+      __syncthreads();
+#pragma unroll
+      for (int i = 0; i < EPL; ++i) {
+        const int e = j + P * i;
+        if (e >= E) continue;
+        int c = 0;
+        for (int r = 0; r < crows; ++r) c += cs[r * E + e];
+        f[i] = static_cast<float>(c) * inv_s;
+      }
     }
 #pragma unroll
     for (int r = 0; r < 8; ++r) {
@@ -382,7 +419,7 @@ __global__ __launch_bounds__(1024) void aux_loss_kernel(GateBwdArgs a) {
   float term = 0.f;
   if (t < a.E && a.S > 0) {
     const float inv_s = 1.f / static_cast<float>(a.S);
-    term = (static_cast<float>(a.cnt[t]) * inv_s) * (a.pe[t] * inv_s);
+    term = (static_cast<float>(first_count(a, t)) * inv_s) * (a.pe[t] * inv_s);
   }
   red[t] = term;
   __syncthreads();
@@ -409,7 +446,7 @@ __global__ __launch_bounds__(1024) void dl_sums_loss_kernel(GateBwdArgs a) {
   float term = 0.f;
   if (e < a.E && a.S > 0) {
     const float inv_s = 1.f / static_cast<float>(a.S);
-    term = (static_cast<float>(a.cnt[e]) * inv_s) * (pe * inv_s);
+    term = (static_cast<float>(first_count(a, e)) * inv_s) * (pe * inv_s);
   }
   term = wave_sum(term);
   if (e == 0) a.aux_loss[0] = a.aux_coef * static_cast<float>(a.E) * term;
@@ -896,8 +933,10 @@ static void launch_dl_t(const GateBwdArgs& a, hipStream_t st) {
   constexpr int WAVES = P <= 32 ? (kWave / TP < 16 ? kWave / TP : 16) : 4;
   const size_t tile = a.dlt ? static_cast<size_t>(kWave) * (a.E + 1) * sizeof(float) : 0;
   const size_t sums = static_cast<size_t>(2 * WAVES) * a.E * sizeof(float);
+  const int rows = count_rows(a.S);
+  const size_t counts = (a.aux_coef != 0.f && rows <= kCountRowsInline) ? static_cast<size_t>(rows) * a.E * sizeof(int) : 0;
   gate_dl_kernel<P, EPL, WAVES>
-      <<<dim3(static_cast<unsigned>(a.nb)), dim3(WAVES * kWave), tile > sums ? tile : sums, st>>>(a);
+      <<<dim3(static_cast<unsigned>(a.nb)), dim3(WAVES * kWave), (tile > sums ? tile : sums) + counts, st>>>(a);
 }
 
 static void launch_colsum_f(const float* part, int64_t rows, int E, float* out, hipStream_t st) {
@@ -913,7 +952,8 @@ hipError_t launch_gate_bwd_dl(const GateBwdArgs& a, hipStream_t st) {
     if (cblocks > 0)
       aux_counts_kernel<<<dim3(static_cast<unsigned>(cblocks)), dim3(1024), static_cast<size_t>(a.E) * sizeof(int),
                           st>>>(a, cpart);
-    colsum_kernel<int32_t><<<dim3((a.E + kWave - 1) / kWave), dim3(1024), 0, st>>>(cpart, cblocks, a.E, a.cnt);
+    if (cblocks > kCountRowsInline)
+      colsum_kernel<int32_t><<<dim3((a.E + kWave - 1) / kWave), dim3(1024), 0, st>>>(cpart, cblocks, a.E, a.cnt);
   }
   if (a.nb > 0) {
     const int E = a.E;

@@ -323,6 +323,8 @@ moe_status moe_gate_bwd(const moe_gate_bwd_params* p, const void* x, const void*
   // the matrix-core dx reads W rows and dL with 16-byte loads
   a.mfma_dx = (g.mfma && dx && aligned(wg, 16) && (!dlogits || aligned(dlogits, 16))) ? 1 : 0;
   a.s_pad = g.s_pad;
+  // with dW wanted, its reduction launch also takes db and the balance loss
+  a.sums_in_reduce = (dwg && p->E <= 64) ? 1 : 0;
   a.x = x; a.wg = wg; a.logits = logits; a.ids = ids; a.dw = dw;
   a.dl = dlogits ? dlogits : reinterpret_cast<float*>(ws + g.off_dl);
   a.dlt = a.mfma_dw ? reinterpret_cast<uint16_t*>(ws + g.off_dlt) : nullptr;

@@ -430,13 +430,12 @@ __global__ __launch_bounds__(1024) void aux_loss_kernel(GateBwdArgs a) {
   if (t == 0) a.aux_loss[0] = a.aux_coef * static_cast<float>(a.E) * red[0];
 }
 
-// db and the balance loss side by side in one launch (E <= 64): with dbias,
-// block 0 sums the per-wave-block dL sums into it; the last block sums the
-// softmax sums into pe and then forms the loss from them (first-choice counts
-// cnt), so no block waits for another.
-__global__ __launch_bounds__(1024) void dl_sums_loss_kernel(GateBwdArgs a) {
-  __shared__ float red[16][kWave];
-  if (a.dbias && blockIdx.x == 0) {
+// db and the balance loss side by side (E <= 64), block sb of 1024 threads:
+// with dbias, block 0 sums the per-wave-block dL sums into it; the other sums
+// the softmax sums into pe and then forms the loss from them (first-choice
+// counts), so no block waits for another.
+__device__ __forceinline__ void dl_sums_block(const GateBwdArgs& a, int sb, float (*red)[kWave]) {
+  if (a.dbias && sb == 0) {
     colsum_cols(a.bpart, a.nb, a.E, a.dbias, 0, red);
     return;
   }
@@ -450,6 +449,16 @@ __global__ __launch_bounds__(1024) void dl_sums_loss_kernel(GateBwdArgs a) {
   }
   term = wave_sum(term);
   if (e == 0) a.aux_loss[0] = a.aux_coef * static_cast<float>(a.E) * term;
+}
+
+// Blocks of the sums above: db if wanted, the loss if wanted.
+inline int dl_sums_blocks(const GateBwdArgs& a) {
+  return (a.dbias ? 1 : 0) + (a.aux_coef != 0.f && a.aux_loss ? 1 : 0);
+}
+
+__global__ __launch_bounds__(1024) void dl_sums_loss_kernel(GateBwdArgs a) {
+  __shared__ float red[16][kWave];
+  dl_sums_block(a, blockIdx.x, red);
 }
 
 // ---------------------------------------------------------------- dW on matrix cores
@@ -851,10 +860,19 @@ __global__ __launch_bounds__(kBwdThreads) void dwg_partial_kernel(GateBwdArgs a)
   }
 }
 
-// dwg[j][e] = sum over the token ranges, in order.
-__global__ __launch_bounds__(kBwdThreads) void dwg_reduce_kernel(GateBwdArgs a) {
+// dwg[j][e] = sum over the token ranges, in order; blocks past the sums run
+// the db / balance-loss sums (sums_in_reduce).
+constexpr int kReduceThreads = 1024;
+
+__global__ __launch_bounds__(kReduceThreads) void dwg_reduce_kernel(GateBwdArgs a) {
   const int64_t n = static_cast<int64_t>(a.E) * a.d;
-  const int64_t idx = static_cast<int64_t>(blockIdx.x) * kBwdThreads + threadIdx.x;
+  const int64_t nr = (n + kReduceThreads - 1) / kReduceThreads;
+  if (static_cast<int64_t>(blockIdx.x) >= nr) {
+    __shared__ float red[16][kWave];
+    dl_sums_block(a, static_cast<int>(blockIdx.x - nr), red);
+    return;
+  }
+  const int64_t idx = static_cast<int64_t>(blockIdx.x) * kReduceThreads + threadIdx.x;
   if (idx >= n) return;
   const int e = static_cast<int>(idx / a.d), jx = static_cast<int>(idx % a.d);
   // eight ranges' loads in flight at a time; the additions stay in range order
@@ -967,9 +985,10 @@ hipError_t launch_gate_bwd_dl(const GateBwdArgs& a, hipStream_t st) {
     else if (E <= 512) launch_dl_t<64, 8>(a, st);
     else launch_dl_t<64, 16>(a, st);
   }
-  if (aux && a.aux_loss && a.E <= kWave) {
-    // db and the loss in one launch (block 0: db, block 1: softmax sums, loss)
-    dl_sums_loss_kernel<<<dim3(a.dbias ? 2 : 1), dim3(1024), 0, st>>>(a);
+  if (a.sums_in_reduce) return hipGetLastError();  // the dW reduction launch takes them
+  if (a.E <= kWave && dl_sums_blocks(a) > 0) {
+    // db and the loss in one launch
+    dl_sums_loss_kernel<<<dim3(dl_sums_blocks(a)), dim3(1024), 0, st>>>(a);
     return hipGetLastError();
   }
   if (a.dbias) launch_colsum_f(a.bpart, a.nb, a.E, a.dbias, st);
@@ -1010,7 +1029,9 @@ hipError_t launch_gate_bwd_dwg(const GateBwdArgs& a, hipStream_t st) {
     }
   }
   const int64_t n = static_cast<int64_t>(a.E) * a.d;
-  dwg_reduce_kernel<<<dim3(static_cast<unsigned>((n + kBwdThreads - 1) / kBwdThreads)), dim3(kBwdThreads), 0, st>>>(a);
+  const int64_t nr = (n + kReduceThreads - 1) / kReduceThreads;
+  const int64_t extra = a.sums_in_reduce ? dl_sums_blocks(a) : 0;
+  dwg_reduce_kernel<<<dim3(static_cast<unsigned>(nr + extra)), dim3(kReduceThreads), 0, st>>>(a);
   return hipGetLastError();
 }
 

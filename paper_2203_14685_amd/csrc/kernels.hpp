@@ -105,6 +105,7 @@ struct GateBwdArgs {
   float temperature;        // > 0: the logits are (L + noise) / temperature; gradients w.r.t. L
   int nsplit, split_tokens; // dW is summed over tokens in nsplit ranges of split_tokens (a multiple of 64)
   int mfma_dw, mfma_dx;     // matrix-core paths (bf16, E a multiple of 16 up to 128, d a multiple of 64)
+  int sums_in_reduce;       // db, the softmax sums and the loss run as extra blocks of the dW reduction
   int64_t s_pad;            // row length of dlt: S rounded up to 64
   const void* x;            // [S, d]
   const void* wg;           // [d, E]

@@ -186,6 +186,23 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(ScanArgs a) {
   __shared__ int wave_tot[kScanWaves];
   const int e = blockIdx.x;
   int carry = 0;
+  if (a.nb <= kScanThreads && a.k <= 8) {
+    // every rank's row in one pass: all the loads first, then the scans in
+    // rank order
+    const int b = threadIdx.x;
+    int v[8];
+#pragma unroll
+    for (int r = 0; r < 8; ++r)
+      v[r] = (r < a.k && b < a.nb) ? a.hist[(static_cast<int64_t>(r) * a.E + e) * a.nb + b] : 0;
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      if (r >= a.k) break;
+      int total;
+      const int incl = block_inclusive_scan(v[r], wave_tot, total);
+      if (b < a.nb) a.hist[(static_cast<int64_t>(r) * a.E + e) * a.nb + b] = carry + incl - v[r];
+      carry += total;
+    }
+  } else
   for (int r = 0; r < a.k; ++r) {
     int32_t* row = a.hist + (static_cast<int64_t>(r) * a.E + e) * a.nb;
     for (int b0 = 0; b0 < a.nb; b0 += kScanThreads) {
@@ -214,16 +231,24 @@ __global__ __launch_bounds__(kBlock) void assign_kernel(AssignArgs a) {
   const int k = a.k;
   // ids are in [0, E); invalid lanes use E, so bits of 0..E are compared
   const int nbits = 32 - __clz(a.E);
+  const int lane = lane_id();
   for (int r = 0; r < k; ++r) {
     const int e = valid ? a.ids[s * k + r] : a.E;
+    // up to 64 experts: lane x loads expert x's offset for this wave block
+    // beside the ids, and each lane takes its expert's by a shuffle (no load
+    // that waits on the id)
+    int off_lane = 0;
+    if (a.E <= kWave) off_lane = a.offs[(static_cast<int64_t>(r) * a.E + min(lane, a.E - 1)) * a.nb + wb];
     uint64_t same = ~0ull;
     for (int bit = 0; bit < nbits; ++bit) {
       const bool on = (e >> bit) & 1;
       const uint64_t bal = __ballot(on);
       same &= on ? bal : ~bal;
     }
+    const int off_e = a.E <= kWave ? __shfl(off_lane, min(e, a.E - 1), kWave) : 0;
     if (valid) {
-      const int pos = a.offs[(static_cast<int64_t>(r) * a.E + e) * a.nb + wb] + popc_below(same);
+      const int base = a.E <= kWave ? off_e : a.offs[(static_cast<int64_t>(r) * a.E + e) * a.nb + wb];
+      const int pos = base + popc_below(same);
       const bool kept = pos < a.C;
       a.slots[s * k + r] = kept ? pos : -1;
       if (kept) a.slot_src[static_cast<int64_t>(e) * a.C + pos] = static_cast<int>(s * k + r);

@@ -611,11 +611,16 @@ __global__ __launch_bounds__(kBwdThreads) __attribute__((amdgpu_waves_per_eu(NT 
 }
 
 // ---------------------------------------------------------------- dx on matrix cores
-// Block: 64 tokens (wave w: 16) x 256 columns (4 passes of 64); blocks are
-// numbered column block first.  dL of the wave's tokens is kept in registers
+// Block: 16 tokens per wave (8 or 4 waves) x 256 columns (4 passes of 64);
+// blocks are numbered column block first.  dL of the wave's tokens is kept in registers
 // in three bf16 parts; the W rows of a pass are staged in LDS, two passes' rows
 // in turn (one barrier per pass).  Each lane adds the incoming dx to its two
 // 16-byte pieces of the result and stores them.
+// Waves per dx block (16 tokens each): up to 64 experts (at most 128
+// registers, four waves per SIMD) eight, so that a block's W rows are staged
+// in LDS for 128 tokens; more experts take more registers and keep four.
+constexpr int dx_waves(int NT) { return NT <= 4 ? 8 : 4; }
+
 template <int NT>
 struct DxShape {
   static constexpr int E = 16 * NT;
@@ -636,14 +641,15 @@ struct DxShape {
 // regroups them so that one store covers 8 tokens x 128 bytes: whole 128-byte
 // lines, which is what keeps the store stream fast while the memory is also
 // writing back what earlier kernels left dirty.  No LDS transpose.
-template <int NT, bool ACC, bool FULL>
+template <int NT, bool ACC, bool FULL, int DW>
 __device__ __forceinline__ void dx_mfma_body(const GateBwdArgs& a, uint16_t* wl) {
   constexpr int E = DxShape<NT>::E, KS = DxShape<NT>::KS, LDW = DxShape<NT>::LDW;
+  constexpr int kThreads = DW * kWave;
   const int w = threadIdx.x / kWave, lane = lane_id();
   const int g = lane / 16, m = lane % 16;
   const int ncb = (a.d + 4 * kWave - 1) / (4 * kWave);  // column blocks of 256
-  const int64_t tb = blockIdx.x / ncb;                   // 64-token block
-  const int64_t s0 = tb * kWave + 16 * w;               // the wave's first token
+  const int64_t tb = blockIdx.x / ncb;                   // block of 16 * DW tokens
+  const int64_t s0 = tb * (16 * DW) + 16 * w;           // the wave's first token
   const int64_t sm = s0 + m;                             // this lane's token in the product
   const bool tok_ok = FULL || sm < a.S;
   const uint16_t* wg = reinterpret_cast<const uint16_t*>(a.wg);
@@ -673,12 +679,12 @@ __device__ __forceinline__ void dx_mfma_body(const GateBwdArgs& a, uint16_t* wl)
   // issued a pass ahead: W rows and the incoming dx of pass cb + 1 while pass
   // cb runs.  Vector-memory loads complete in issue order, so the waits for
   // one pass's values leave the next pass's loads in flight.
-  constexpr int WPT = (kWave * (E / 8) + kBwdThreads - 1) / kBwdThreads;  // 16-byte pieces per thread
+  constexpr int WPT = (kWave * (E / 8) + kThreads - 1) / kThreads;  // 16-byte pieces per thread
   u32x4 wreg[WPT];
   auto load_w = [&](int j0) {
 #pragma unroll
     for (int u = 0; u < WPT; ++u) {
-      const int q = min(threadIdx.x + u * kBwdThreads, kWave * (E / 8) - 1);
+      const int q = min(static_cast<int>(threadIdx.x) + u * kThreads, kWave * (E / 8) - 1);
       const int r = q / (E / 8), p8 = q % (E / 8);
       const int row = min(j0 + r, a.d - 1);
       wreg[u] = *reinterpret_cast<const u32x4*>(wg + static_cast<int64_t>(row) * E + 8 * p8);
@@ -707,7 +713,7 @@ __device__ __forceinline__ void dx_mfma_body(const GateBwdArgs& a, uint16_t* wl)
     uint16_t* wb = wl + (cb & 1) * kWave * LDW;
 #pragma unroll
     for (int u = 0; u < WPT; ++u) {  // clamped like the loads: a repeated piece rewrites its own value
-      const int q = min(threadIdx.x + u * kBwdThreads, kWave * (E / 8) - 1);
+      const int q = min(static_cast<int>(threadIdx.x) + u * kThreads, kWave * (E / 8) - 1);
       const int r = q / (E / 8), p8 = q % (E / 8);
       *reinterpret_cast<u32x4*>(&wb[r * LDW + 8 * p8]) = wreg[u];
     }
@@ -796,13 +802,13 @@ __device__ __forceinline__ void dx_mfma_body(const GateBwdArgs& a, uint16_t* wl)
 
 // Up to 64 experts the kernel fits four waves per SIMD (at most 128 registers);
 // more experts need more registers for the dL planes and take fewer waves.
-template <int NT, bool ACC>
-__global__ __launch_bounds__(kBwdThreads) __attribute__((amdgpu_waves_per_eu(NT <= 4 ? 4 : 1, NT <= 4 ? 4 : 8)))
+template <int NT, bool ACC, int DW>
+__global__ __launch_bounds__(DW * kWave) __attribute__((amdgpu_waves_per_eu(NT <= 4 ? 4 : 1, NT <= 4 ? 4 : 8)))
 void dx_mfma_kernel(GateBwdArgs a) {
   __shared__ __align__(16) uint16_t wl[2 * kWave * DxShape<NT>::LDW];
   const int ncb = (a.d + 4 * kWave - 1) / (4 * kWave);
-  if ((static_cast<int64_t>(blockIdx.x / ncb) + 1) * kWave <= a.S) dx_mfma_body<NT, ACC, true>(a, wl);
-  else dx_mfma_body<NT, ACC, false>(a, wl);
+  if ((static_cast<int64_t>(blockIdx.x / ncb) + 1) * (16 * DW) <= a.S) dx_mfma_body<NT, ACC, true, DW>(a, wl);
+  else dx_mfma_body<NT, ACC, false, DW>(a, wl);
 }
 
 // ---------------------------------------------------------------- dW, dx on the vector ALUs
@@ -1039,9 +1045,11 @@ template <int NT>
 static void launch_dx_mfma_t(const GateBwdArgs& a, hipStream_t st) {
   // 1-D grid, the column blocks of one 64-token block consecutive, so that
   // they run side by side and whole rows of dx stream together
-  const dim3 grid(static_cast<unsigned>(static_cast<int64_t>((a.d + 4 * kWave - 1) / (4 * kWave)) * a.nb));
-  if (a.accumulate) dx_mfma_kernel<NT, true><<<grid, dim3(kBwdThreads), 0, st>>>(a);
-  else dx_mfma_kernel<NT, false><<<grid, dim3(kBwdThreads), 0, st>>>(a);
+  constexpr int DW = dx_waves(NT);
+  const int64_t tblocks = (static_cast<int64_t>(a.S) + 16 * DW - 1) / (16 * DW);
+  const dim3 grid(static_cast<unsigned>(static_cast<int64_t>((a.d + 4 * kWave - 1) / (4 * kWave)) * tblocks));
+  if (a.accumulate) dx_mfma_kernel<NT, true, DW><<<grid, dim3(DW * kWave), 0, st>>>(a);
+  else dx_mfma_kernel<NT, false, DW><<<grid, dim3(DW * kWave), 0, st>>>(a);
 }
 
 hipError_t launch_gate_bwd_dx(const GateBwdArgs& a, hipStream_t st) {

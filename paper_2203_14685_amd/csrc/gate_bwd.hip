@@ -377,15 +377,20 @@ __global__ __launch_bounds__(WAVES * kWave) void gate_dl_kernel(GateBwdArgs a) {
   }
   __syncthreads();  // dL tile complete
   if (a.dlt) {
+    // 8 consecutive tokens of one expert per thread: one 16-byte store per
+    // plane (s_pad is a multiple of 64, so the pieces are 16-byte aligned)
     const int64_t plane = static_cast<int64_t>(E) * a.s_pad;
-    for (int q = threadIdx.x; q < E * kWave; q += WAVES * kWave) {
-      const int e = q / kWave, tok = q % kWave;
-      uint32_t hb, mb, lb;
-      split3(sh[tok * (E + 1) + e], hb, mb, lb);
-      const int64_t o = static_cast<int64_t>(e) * a.s_pad + wb * kWave + tok;
-      a.dlt[o] = static_cast<uint16_t>(hb);
-      a.dlt[plane + o] = static_cast<uint16_t>(mb);
-      a.dlt[2 * plane + o] = static_cast<uint16_t>(lb);
+    for (int q = threadIdx.x; q < E * (kWave / 8); q += WAVES * kWave) {
+      const int e = q / (kWave / 8), t0 = (q % (kWave / 8)) * 8;
+      float v8[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v8[u] = sh[(t0 + u) * (E + 1) + e];
+      u32x4 hi, mi, lo;
+      split8(v8, hi, mi, lo);
+      const int64_t o = static_cast<int64_t>(e) * a.s_pad + wb * kWave + t0;
+      *reinterpret_cast<u32x4*>(a.dlt + o) = hi;
+      *reinterpret_cast<u32x4*>(a.dlt + plane + o) = mi;
+      *reinterpret_cast<u32x4*>(a.dlt + 2 * plane + o) = lo;
     }
   }
   __syncthreads();  // tile consumed before its space holds the sums

@@ -140,7 +140,7 @@ hipError_t launch_gate_bwd_dx(const GateBwdArgs& a, hipStream_t st);
 // are carved out by the C ABI.
 constexpr int kBaseCand = 2048;          // bidders an expert considers per round
 constexpr int kBaseMaxCap = 2048;        // largest S / E
-constexpr double kBaseEpsStep = 8.0;     // eps divisor between phases
+constexpr double kBaseEpsStep = 32.0;    // eps divisor between phases
 constexpr double kBaseEpsEnd = 0x1p-30;  // final eps, relative to the score range
 constexpr int kBaseRangeBlocks = 256;    // blocks of the score-range reduction
 constexpr int kBaseTail = 64;            // rounds with at most this many bidders run in one workgroup

@@ -886,7 +886,7 @@ hipError_t run_base_auction(const BaseArgs& a, hipStream_t st, BaseStats* stats)
   base_reset_kernel<<<tok_blocks, kBlock, 0, st>>>(a);
   if ((err = hipGetLastError()) != hipSuccess) return err;
   // the device ends the auction within (max_rounds + 1) rounds per phase; the
-  // phases are at most 2 + log_32(2^30 / 4) < 8, so 12 per phase is a safe bound
+  // phases are at most 2 + log_32(2^30 / 4) < 8, so a bound of 12 phases is safe
   const int64_t limit = static_cast<int64_t>(a.max_rounds + 1) * 12 + 1;
   int r = 0;
   int batch = 64;

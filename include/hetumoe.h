@@ -56,7 +56,7 @@
 extern "C" {
 #endif
 
-#define MOE_ABI_VERSION 7
+#define MOE_ABI_VERSION 8
 
 /* Symbols of the C ABI are the only ones the shared library exports. */
 #define MOE_API __attribute__((visibility("default")))
@@ -260,6 +260,53 @@ MOE_API moe_status moe_base_gate(const moe_base_params* p, const void* x, const 
                                  float* weights, int32_t* counts, int32_t* slot_src, double* prices,
                                  void* workspace, size_t workspace_bytes, moe_base_info* info,
                                  hipStream_t stream);
+
+/* What the auction of moe_base_gate_async did (DEVICE memory, written by its
+ * last kernel; 24 bytes, 8-byte aligned). */
+typedef struct {
+  int32_t phases;     /* eps phases run (0 when S == 0) */
+  int32_t rounds;     /* bidding rounds, summed over phases */
+  double eps;         /* eps of the last phase run */
+  int32_t status;     /* 0 balanced assignment found; 1 not found within the rounds
+                         enqueued or max_rounds; 2 a score is infinite or NaN */
+  int32_t pad;
+} moe_base_status;
+
+/* Largest launch_rounds moe_base_gate_async accepts. */
+#define MOE_BASE_MAX_LAUNCH_ROUNDS 16384
+
+/*
+ * moe_base_gate_async -- moe_base_gate without host synchronization, for
+ * callers that capture their work in a HIP graph or cannot wait on the host.
+ * The same kernels run with the same arguments and inputs, so when status->
+ * status ends 0 every output is bitwise that of moe_base_gate, and the same
+ * optimality bound holds with status->eps.
+ *
+ * Instead of reading the auction's done flag between batches, the call
+ * enqueues exactly launch_rounds rounds (in [1, MOE_BASE_MAX_LAUNCH_ROUNDS];
+ * one round is a bid, a resolve and a tail kernel, the tail kernel finishing
+ * the rounds with few bidders in one workgroup; a round enqueued after the
+ * auction has ended returns at once, in a few microseconds).  Rounds that
+ * suffice are workload-dependent: moe_base_gate's info->rounds bounds them
+ * from above, and the synchronous call's first batch is 64.  The outcome is
+ * written to `status` (device memory, required) by the call's last auction
+ * kernel; no host read, memset or allocation is made.
+ *
+ * Outputs are always written and always in range: when status->status is 1
+ * or 2, ids holds each token's expert as the unfinished auction left it (or
+ * s mod E for a token holding none), so counts may exceed S / E and tokens
+ * past the capacity get slot -1 as in moe_gate; weights may be NaN when
+ * status->status is 2.  Argument errors are those of moe_base_gate, plus
+ * MOE_ERR_INVALID_ARG for launch_rounds outside its range or a NULL or
+ * misaligned status; no device-side failure is reported by the return value.
+ * Workspace as for moe_base_gate; calls that overlap on one workspace race.
+ */
+MOE_API moe_status moe_base_gate_async(const moe_base_params* p, const void* x, const void* wg,
+                                       const float* bias, float* logits, int32_t* ids, int32_t* slots,
+                                       float* weights, int32_t* counts, int32_t* slot_src,
+                                       double* prices, void* workspace, size_t workspace_bytes,
+                                       int32_t launch_rounds, moe_base_status* status,
+                                       hipStream_t stream);
 
 /*
  * moe_dispatch -- step 2 of Algorithm 1 (Layout_Transform; Sec. 3.2, layout

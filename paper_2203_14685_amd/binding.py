@@ -28,7 +28,7 @@ EXPORTED = (
     "moe_gate_workspace_size", "moe_gate", "moe_gate_noalloc", "moe_dispatch", "moe_combine",
     "moe_dispatch_bwd", "moe_combine_bwd", "moe_gate_bwd_workspace_size", "moe_gate_bwd",
     "moe_hash_balanced_table", "moe_base_gate_workspace_size", "moe_base_gate",
-    "moe_status_string", "moe_last_error", "moe_abi_version",
+    "moe_base_gate_async", "moe_status_string", "moe_last_error", "moe_abi_version",
 )
 
 
@@ -75,6 +75,12 @@ class BaseInfo(ctypes.Structure):
     _fields_ = [("phases", ctypes.c_int32), ("rounds", ctypes.c_int32), ("eps", ctypes.c_double)]
 
 
+# moe_base_status, which moe_base_gate_async writes to device memory: 24 bytes,
+# read back as int32 [6] (phases, rounds, eps as two words, status, pad)
+BASE_STATUS_BYTES = 24
+MOE_BASE_MAX_LAUNCH_ROUNDS = 16384
+
+
 _lib = None
 
 
@@ -103,9 +109,12 @@ def load():
     lib.moe_base_gate_workspace_size.argtypes = [ctypes.POINTER(BaseParams), ctypes.POINTER(ctypes.c_size_t)]
     lib.moe_base_gate.argtypes = [ctypes.POINTER(BaseParams), vp, vp, f32p, f32p, i32p, i32p, f32p, i32p, i32p,
                                   vp, vp, ctypes.c_size_t, ctypes.POINTER(BaseInfo), vp]
+    lib.moe_base_gate_async.argtypes = [ctypes.POINTER(BaseParams), vp, vp, f32p, f32p, i32p, i32p, f32p, i32p,
+                                        i32p, vp, vp, ctypes.c_size_t, ctypes.c_int32, vp, vp]
     for name in ("moe_gate_workspace_size", "moe_gate", "moe_dispatch", "moe_combine",
                  "moe_dispatch_bwd", "moe_combine_bwd", "moe_gate_bwd_workspace_size", "moe_gate_bwd",
-                 "moe_hash_balanced_table", "moe_base_gate_workspace_size", "moe_base_gate"):
+                 "moe_hash_balanced_table", "moe_base_gate_workspace_size", "moe_base_gate",
+                 "moe_base_gate_async"):
         getattr(lib, name).restype = ctypes.c_int
     lib.moe_status_string.argtypes = [ctypes.c_int]
     lib.moe_status_string.restype = ctypes.c_char_p
@@ -333,11 +342,41 @@ def moe_base_gate(params, x, wg, bias, logits, ids, slots, weights, counts, slot
         _stream(stream)))
 
 
+def moe_base_gate_async(params, x, wg, bias, logits, ids, slots, weights, counts, slot_src, prices, workspace,
+                        launch_rounds, status, stream=None):
+    """moe_base_gate with `launch_rounds` auction rounds enqueued and no host
+    synchronization; `status`: a device tensor of at least 24 bytes, 8-byte
+    aligned, that receives the moe_base_status (see base_status)."""
+    lib = load()
+    f32, i32 = torch.float32, torch.int32
+    xdt = torch.bfloat16 if params.dtype == MOE_BF16 else torch.float32
+    S, d, E, C = params.S, params.d, params.E, params.capacity
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    if status is not None and status.numel() * status.element_size() < BASE_STATUS_BYTES:
+        raise ValueError("status must hold at least 24 bytes")
+    _check(lib.moe_base_gate_async(
+        ctypes.byref(params), _ptr(x, xdt, "x", S * d), _ptr(wg, xdt, "wg", d * E), _ptr(bias, f32, "bias", E),
+        _ptr(logits, f32, "logits", S * E), _ptr(ids, i32, "ids", S), _ptr(slots, i32, "slots", S),
+        _ptr(weights, f32, "weights", S), _ptr(counts, i32, "counts", E), _ptr(slot_src, i32, "slot_src", E * C),
+        _ptr(prices, torch.float64, "prices", E), _ptr(workspace, None, "workspace"), ws_bytes,
+        int(launch_rounds), _ptr(status, None, "status"), _stream(stream)))
+
+
+def base_status(status):
+    """Decode a moe_base_status tensor (device or host) into a dict."""
+    import numpy as np
+    raw = status.detach().reshape(-1).view(torch.uint8)[:BASE_STATUS_BYTES].cpu().numpy()
+    w = raw.view(np.int32)
+    return dict(phases=int(w[0]), rounds=int(w[1]), eps=float(raw[8:16].view(np.float64)[0]), status=int(w[4]))
+
+
 def base_gate(E, capacity=None, *, x=None, wg=None, bias=None, logits=None, logits_in=False, want_logits=False,
-              max_rounds=0, stream=None):
+              max_rounds=0, launch_rounds=None, stream=None):
     """Allocate the outputs and run moe_base_gate; returns a dict of device
     tensors (ids, slots, weights as [S, 1], the shape the layout calls take;
-    prices [E] float64) plus "info" (phases, rounds, eps of the auction)."""
+    prices [E] float64) plus "info" (phases, rounds, eps of the auction).
+    With launch_rounds, moe_base_gate_async runs instead and "status" is the
+    device moe_base_status (int64 [3]; decode it with base_status)."""
     if logits_in:
         S, d, dcode = int(logits.shape[0]), 0, MOE_F32
         dev = logits.device
@@ -358,6 +397,11 @@ def base_gate(E, capacity=None, *, x=None, wg=None, bias=None, logits=None, logi
         logits = torch.empty((S, E), dtype=torch.float32, device=dev) if want_logits else None
     out["logits"] = logits
     ws = torch.empty((moe_base_gate_workspace_size(params),), dtype=torch.uint8, device=dev)
+    if launch_rounds is not None:
+        out["status"] = torch.empty((3,), dtype=torch.int64, device=dev)
+        moe_base_gate_async(params, x, wg, bias, logits, out["ids"], out["slots"], out["weights"], out["counts"],
+                            out["slot_src"], out["prices"], ws, launch_rounds, out["status"], stream)
+        return out
     info = BaseInfo()
     moe_base_gate(params, x, wg, bias, logits, out["ids"], out["slots"], out["weights"], out["counts"],
                   out["slot_src"], out["prices"], ws, info, stream)

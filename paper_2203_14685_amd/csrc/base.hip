@@ -843,18 +843,26 @@ __global__ __launch_bounds__(kBaseThreads) void base_tail_kernel(BaseArgs a, int
 // ---------------------------------------------------------------- outputs
 // ids, weights (sigmoid of the score) and the wave-block histogram [E, nb]
 // that the scan and assign kernels turn into slots
-__global__ __launch_bounds__(kBlock) void base_finish_kernel(BaseArgs a, int r) {
+// With `status` (the asynchronous form) the outputs are written whatever the
+// outcome, every token with a valid expert (its current one, else s mod E, so
+// that the slot kernels that follow stay in bounds), and the outcome goes to
+// status; without it (the host reads the state) only a finished auction writes.
+__global__ __launch_bounds__(kBlock) void base_finish_kernel(BaseArgs a, int r, BaseDevStatus* status) {
   const BaseState st = a.state[r & 1];
-  if (!st.done || st.failed) return;
+  const bool ok = st.done && !st.failed;
+  if (!ok && status == nullptr) return;
   extern __shared__ int hist_lds[];  // [kWavesPerBlock, E]
   const int tid = threadIdx.x;
   const int w = tid / kWave;
   const int lane = lane_id();
   const int64_t s = static_cast<int64_t>(blockIdx.x) * kBlock + tid;
   const bool valid = s < a.S;
+  if (status && blockIdx.x == 0 && tid == 0)
+    *status = BaseDevStatus{st.phase + 1, st.rounds_total, st.eps, ok ? 0 : (st.failed == 2 ? 2 : 1), 0};
   int e = 0;
   if (valid) {
     e = a.assign[s];
+    if (e < 0 || e >= a.E) e = static_cast<int>(s % a.E);
     a.ids[s] = e;
     a.weights[s] = 1.f / (1.f + expf(-a.logits[s * a.E + e]));
   }
@@ -869,6 +877,9 @@ __global__ __launch_bounds__(kBlock) void base_finish_kernel(BaseArgs a, int r) 
   if (a.prices_out && blockIdx.x == 0)
     for (int i = tid; i < a.E; i += kBlock) a.prices_out[i] = a.price[i];
 }
+
+// The outcome of an empty batch: nothing to assign.
+__global__ void base_empty_status_kernel(BaseDevStatus* status) { *status = BaseDevStatus{0, 0, 0.0, 0, 0}; }
 
 // ---------------------------------------------------------------- driver
 size_t base_resolve_lds(int cap) { return static_cast<size_t>(cap + kBaseCand) * (sizeof(double) + sizeof(int)); }
@@ -915,7 +926,30 @@ hipError_t run_base_auction(const BaseArgs& a, hipStream_t st, BaseStats* stats)
   stats->not_converged = host.failed == 1;
   stats->bad_scores = host.failed == 2;
   if (host.failed) return hipSuccess;
-  base_finish_kernel<<<tok_blocks, kBlock, static_cast<size_t>(kWavesPerBlock) * a.E * sizeof(int), st>>>(a, r);
+  base_finish_kernel<<<tok_blocks, kBlock, static_cast<size_t>(kWavesPerBlock) * a.E * sizeof(int), st>>>(a, r, nullptr);
+  return hipGetLastError();
+}
+
+hipError_t run_base_auction_async(const BaseArgs& a, int launch_rounds, BaseDevStatus* status, hipStream_t st) {
+  if (a.S == 0) {
+    base_empty_status_kernel<<<1, 1, 0, st>>>(status);
+    return hipGetLastError();
+  }
+  const unsigned tok_blocks = static_cast<unsigned>((a.S + kBlock - 1) / kBlock);
+  const size_t bid_lds = static_cast<size_t>(a.E) * (sizeof(double) + sizeof(int));
+  const size_t tail_lds = static_cast<size_t>(a.E + a.cap) * (sizeof(double) + sizeof(int));
+  const bool vec = a.E % 4 == 0 && reinterpret_cast<uintptr_t>(a.logits) % 16 == 0;
+  base_range_kernel<<<kBaseRangeBlocks, kBaseThreads, 0, st>>>(a);
+  base_init_kernel<<<1, kBaseRangeBlocks, 0, st>>>(a);
+  base_reset_kernel<<<tok_blocks, kBlock, 0, st>>>(a);
+  for (int r = 0; r < launch_rounds; ++r) {
+    if (vec) base_bid_kernel<true><<<tok_blocks, kBlock, bid_lds, st>>>(a, r);
+    else base_bid_kernel<false><<<tok_blocks, kBlock, bid_lds, st>>>(a, r);
+    base_resolve_kernel<<<static_cast<unsigned>(a.E), kBaseThreads, base_resolve_lds(a.cap), st>>>(a, r);
+    base_tail_kernel<<<1, kBaseThreads, tail_lds, st>>>(a, r);
+  }
+  base_finish_kernel<<<tok_blocks, kBlock, static_cast<size_t>(kWavesPerBlock) * a.E * sizeof(int), st>>>(
+      a, launch_rounds, status);
   return hipGetLastError();
 }
 

@@ -1,6 +1,7 @@
 // C ABI of the library: argument validation (before any HIP call), workspace
 // sizing and kernel launches.  See include/hetumoe.h for the contract.
 #include <stdarg.h>
+#include <stddef.h>
 #include <stdio.h>
 #include <string.h>
 
@@ -14,6 +15,12 @@
 #include "kernels.hpp"
 
 using namespace hetumoe;
+
+// the asynchronous BASE call hands its caller's struct to the finish kernel
+static_assert(sizeof(moe_base_status) == sizeof(BaseDevStatus) && sizeof(moe_base_status) == 24, "status layout");
+static_assert(offsetof(moe_base_status, eps) == offsetof(BaseDevStatus, eps) &&
+                  offsetof(moe_base_status, status) == offsetof(BaseDevStatus, status),
+              "status layout");
 
 namespace {
 
@@ -635,11 +642,18 @@ moe_status moe_base_gate_workspace_size(const moe_base_params* p, size_t* bytes)
   return ok();
 }
 
-moe_status moe_base_gate(const moe_base_params* p, const void* x, const void* wg, const float* bias, float* logits,
-                         int32_t* ids, int32_t* slots, float* weights, int32_t* counts, int32_t* slot_src,
-                         double* prices, void* workspace, size_t workspace_bytes, moe_base_info* info,
-                         hipStream_t stream) {
-  static const char* who = "moe_base_gate";
+}  // extern "C"
+
+namespace {
+
+// moe_base_gate and moe_base_gate_async: with launch_rounds == 0 the host reads
+// the auction's state between batches of rounds (synchronous, info filled);
+// otherwise exactly launch_rounds rounds are enqueued, nothing is read back,
+// and the outcome goes to the device struct dstatus.
+moe_status base_gate_run(const char* who, const moe_base_params* p, const void* x, const void* wg, const float* bias,
+                         float* logits, int32_t* ids, int32_t* slots, float* weights, int32_t* counts,
+                         int32_t* slot_src, double* prices, void* workspace, size_t workspace_bytes,
+                         moe_base_info* info, int launch_rounds, moe_base_status* dstatus, hipStream_t stream) {
   CHECK(check_base_params(p));
   const int64_t S = p->S, E = p->E, C = p->capacity;
   const size_t elt = elt_size(p->dtype);
@@ -701,13 +715,18 @@ moe_status moe_base_gate(const moe_base_params* p, const void* x, const void* wg
   a.state = reinterpret_cast<BaseState*>(ws + b.off_state);
   a.range_part = reinterpret_cast<float*>(ws + b.off_range);
   a.ids = ids; a.weights = weights; a.hist = hist; a.prices_out = prices;
-  BaseStats stats{};
-  err = run_base_auction(a, stream, &stats);
-  if (err != hipSuccess) return hip_fail(err, "moe_base_gate: auction");
-  if (info) *info = moe_base_info{stats.phases, stats.rounds, stats.eps};
-  if (stats.bad_scores) return fail(MOE_ERR_INVALID_ARG, "%s: a score is infinite or NaN", who);
-  if (stats.not_converged)
-    return fail(MOE_ERR_NOT_CONVERGED, "%s: no balanced assignment after %d rounds of a phase", who, a.max_rounds);
+  if (launch_rounds > 0) {
+    err = run_base_auction_async(a, launch_rounds, reinterpret_cast<BaseDevStatus*>(dstatus), stream);
+    if (err != hipSuccess) return hip_fail(err, "moe_base_gate_async: auction launch");
+  } else {
+    BaseStats stats{};
+    err = run_base_auction(a, stream, &stats);
+    if (err != hipSuccess) return hip_fail(err, "moe_base_gate: auction");
+    if (info) *info = moe_base_info{stats.phases, stats.rounds, stats.eps};
+    if (stats.bad_scores) return fail(MOE_ERR_INVALID_ARG, "%s: a score is infinite or NaN", who);
+    if (stats.not_converged)
+      return fail(MOE_ERR_NOT_CONVERGED, "%s: no balanced assignment after %d rounds of a phase", who, a.max_rounds);
+  }
 
   ScanArgs sa{};
   sa.E = p->E; sa.k = 1; sa.nb = nb; sa.C = p->capacity;
@@ -718,6 +737,33 @@ moe_status moe_base_gate(const moe_base_params* p, const void* x, const void* wg
   err = launch_scan_assign(sa, aa, stream);
   if (err != hipSuccess) return hip_fail(err, "moe_base_gate: scan / assign kernel launch");
   return ok();
+}
+
+
+}  // namespace
+
+extern "C" {
+
+moe_status moe_base_gate(const moe_base_params* p, const void* x, const void* wg, const float* bias, float* logits,
+                         int32_t* ids, int32_t* slots, float* weights, int32_t* counts, int32_t* slot_src,
+                         double* prices, void* workspace, size_t workspace_bytes, moe_base_info* info,
+                         hipStream_t stream) {
+  return base_gate_run("moe_base_gate", p, x, wg, bias, logits, ids, slots, weights, counts, slot_src, prices,
+                       workspace, workspace_bytes, info, 0, nullptr, stream);
+}
+
+moe_status moe_base_gate_async(const moe_base_params* p, const void* x, const void* wg, const float* bias,
+                               float* logits, int32_t* ids, int32_t* slots, float* weights, int32_t* counts,
+                               int32_t* slot_src, double* prices, void* workspace, size_t workspace_bytes,
+                               int32_t launch_rounds, moe_base_status* status, hipStream_t stream) {
+  static const char* who = "moe_base_gate_async";
+  if (launch_rounds < 1 || launch_rounds > MOE_BASE_MAX_LAUNCH_ROUNDS)
+    return fail(MOE_ERR_INVALID_ARG, "%s: launch_rounds = %d outside [1, %d]", who, launch_rounds,
+                MOE_BASE_MAX_LAUNCH_ROUNDS);
+  if (!status) return fail(MOE_ERR_INVALID_ARG, "%s: status is NULL", who);
+  if (!aligned(status, 8)) return fail(MOE_ERR_INVALID_ARG, "%s: status is not 8-byte aligned", who);
+  return base_gate_run(who, p, x, wg, bias, logits, ids, slots, weights, counts, slot_src, prices, workspace,
+                       workspace_bytes, nullptr, launch_rounds, status, stream);
 }
 
 }  // extern "C"

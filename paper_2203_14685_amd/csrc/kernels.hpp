@@ -182,8 +182,22 @@ struct BaseStats {
   int bad_scores;          // a score is infinite or NaN
 };
 
+// What the auction did, written to device memory by the asynchronous form
+// (the layout of moe_base_status).
+struct BaseDevStatus {
+  int32_t phases, rounds;  // phases run, rounds summed over phases
+  double eps;              // eps of the last phase
+  int32_t status;          // 0 converged, 1 not converged within the rounds enqueued or allowed, 2 bad scores
+  int32_t pad;
+};
+
 size_t base_resolve_lds(int cap);
 // Runs the auction and writes ids, weights and hist.  Synchronizes `st`.
 hipError_t run_base_auction(const BaseArgs& a, hipStream_t st, BaseStats* stats);
+// The same auction with `launch_rounds` rounds enqueued and no host
+// synchronization (rounds after the end return at once); the outcome goes to
+// `status` in device memory, and every token gets a valid expert even when the
+// auction did not finish (its current one, else s mod E).
+hipError_t run_base_auction_async(const BaseArgs& a, int launch_rounds, BaseDevStatus* status, hipStream_t st);
 
 }  // namespace hetumoe

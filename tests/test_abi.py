@@ -38,7 +38,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_abi_version_and_struct_layout(lib):
-    assert lib.moe_abi_version() == 7
+    assert lib.moe_abi_version() == 8
     assert ctypes.sizeof(b.GateParams) == 56
     assert b.GateParams.hash_seed.offset == 40
     assert b.GateParams.temperature.offset == 48 and b.GateParams.hash_vocab.offset == 52
@@ -344,6 +344,30 @@ def test_base_pointer_checks(lib):
     pl = hm.base_params(128, 0, 8, 16, 1, b.MOE_F32)
     assert call(pl, x=None, wg=None) == b.MOE_ERR_INVALID_ARG          # logits_in needs logits
     assert call(pl, logits=A16) == b.MOE_ERR_INVALID_ARG               # ... and no x / wg
+
+
+def test_base_async_argument_checks(lib):
+    """moe_base_gate_async: launch_rounds within [1, MOE_BASE_MAX_LAUNCH_ROUNDS]
+    and an 8-byte aligned status are required; everything else is checked as
+    for moe_base_gate.  All refused before any HIP call."""
+    p = hm.base_params(128, 256, 8, 16, 0, b.MOE_F32)
+    call = lambda prm=p, **kw: lib.moe_base_gate_async(
+        ctypes.byref(prm), kw.get("x", A16), kw.get("wg", A16), None, None, A16, A16, A16, A16, A16, None,
+        kw.get("ws", A16), kw.get("wsb", 1 << 30), kw.get("rounds", 64), kw.get("status", A16), None)
+    for r in (0, -1, b.MOE_BASE_MAX_LAUNCH_ROUNDS + 1):
+        assert call(rounds=r) == b.MOE_ERR_INVALID_ARG, r
+        assert b"launch_rounds" in lib.moe_last_error()
+    assert call(status=None) == b.MOE_ERR_INVALID_ARG
+    assert call(status=A16 + 4) == b.MOE_ERR_INVALID_ARG
+    assert call(x=None) == b.MOE_ERR_INVALID_ARG
+    assert call(x=A16 + 4) == b.MOE_ERR_UNSUPPORTED
+    assert call(ws=None) == b.MOE_ERR_WORKSPACE
+    assert call(wsb=64) == b.MOE_ERR_WORKSPACE
+    assert call(hm.base_params(100, 256, 8, 16, 0, b.MOE_F32)) == b.MOE_ERR_INVALID_ARG  # S not a multiple of E
+    assert lib.moe_base_gate_async(None, *([None] * 10), None, 0, 64, A16, None) == b.MOE_ERR_INVALID_ARG
+    # the header's limit is the binding's
+    text = open(HEADER).read()
+    assert f"#define MOE_BASE_MAX_LAUNCH_ROUNDS {b.MOE_BASE_MAX_LAUNCH_ROUNDS}" in text
 
 
 # (call, argument names after the params struct, elements each needs) at

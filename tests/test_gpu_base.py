@@ -290,3 +290,117 @@ def test_base_errors_found_on_the_device():
     with pytest.raises(hm.MoeError) as ex:
         run_base(L=L, E=E)
     assert ex.value.status == 1
+
+
+def _base_async(E, C, launch_rounds, L=None, x=None, wg=None, bias=None, dtype="f32", max_rounds=0):
+    if L is not None:
+        out = hm.base_gate(E, C, logits=wl.to_device(L, "f32"), logits_in=True, max_rounds=max_rounds,
+                           launch_rounds=launch_rounds)
+    else:
+        out = hm.base_gate(E, C, x=wl.to_device(x, dtype), wg=wl.to_device(wg, dtype),
+                           bias=wl.to_device(bias, "f32"), want_logits=True, max_rounds=max_rounds,
+                           launch_rounds=launch_rounds)
+    torch.cuda.synchronize()
+    status = hm.base_status(out.pop("status"))
+    h = {k: wl.to_host(v) for k, v in out.items()}
+    return h, status
+
+
+_BASE_KEYS = ("ids", "slots", "weights", "counts", "slot_src", "prices")
+
+
+@pytest.mark.parametrize("S,E,seed,proj", [(2048, 64, 0, False), (6000, 12, 6, False), (4096, 64, 1, True)])
+def test_base_async_matches_sync(S, E, seed, proj):
+    """moe_base_gate_async with enough rounds enqueued: status 0 with the
+    synchronous call's phases, rounds and eps, and bitwise its outputs."""
+    announce(f"base async S={S} E={E} proj={proj}")
+    if proj:
+        w = dict(kind=0, k=1, normalize=0, dtype="bf16", S=S, d=1024, E=E, cf=1.0, hot_experts=4, hot_bias=0.5)
+        inp = wl.make_inputs(w, seed=seed)
+        kw = dict(x=inp["x"], wg=inp["wg"], bias=inp["bias"], dtype="bf16")
+    else:
+        kw = dict(L=np.random.default_rng(seed).standard_normal((S, E)).astype(np.float32))
+    g = run_base(E=E, **kw)
+    info = g["info"]
+    ga, st = _base_async(E, S // E, 256, **kw)
+    assert st == dict(phases=info["phases"], rounds=info["rounds"], eps=info["eps"], status=0), (st, info)
+    for key in _BASE_KEYS + (("logits",) if proj else ()):
+        assert_equal(ga[key], g[key], f"async {key}")
+
+
+def test_base_async_round_budget_too_small():
+    """One round enqueued cannot finish the auction: status 1, and the outputs
+    are still a valid routing (ids in range, slots by their definition).  A NaN
+    score gives status 2; a phase that reaches max_rounds, status 1."""
+    announce("base async, one round")
+    S, E = 2048, 64
+    L = np.random.default_rng(3).standard_normal((S, E)).astype(np.float32)
+    g, st = _base_async(E, S // E, 1, L=L)
+    assert st["status"] == 1, st
+    ids = g["ids"][:, 0]
+    assert ((ids >= 0) & (ids < E)).all()
+    slots_by_property(ids, g["slots"], g["counts"], g["slot_src"], E, S // E)
+    L[17, 5] = np.nan
+    _, st = _base_async(E, S // E, 64, L=L)
+    assert st["status"] == 2, st
+    L[17, 5] = 0.5
+    g, st = _base_async(E, S // E, 256, L=L, max_rounds=1)
+    assert st["status"] == 1, st
+    assert ((g["ids"] >= 0) & (g["ids"] < E)).all()
+
+
+def test_base_async_empty():
+    announce("base async S=0")
+    out = hm.base_gate(8, 4, logits=torch.empty((0, 8), dtype=torch.float32, device="cuda"), logits_in=True,
+                       launch_rounds=4)
+    torch.cuda.synchronize()
+    assert hm.base_status(out["status"]) == dict(phases=0, rounds=0, eps=0.0, status=0)
+    assert (wl.to_host(out["counts"]) == 0).all()
+    assert (wl.to_host(out["slot_src"]) == -1).all()
+
+
+def test_base_async_graph_replays():
+    """The asynchronous call captured in a HIP graph: each replay, on new scores
+    copied into the captured input between replays, gives bitwise the eager
+    synchronous call's outputs on those scores."""
+    announce("base async graph capture")
+    S, E = 2048, 32
+    C = S // E
+    dev = "cuda"
+    p = hm.base_params(S, 0, E, C, 1, hm.MOE_F32)
+    Lbuf = torch.empty((S, E), dtype=torch.float32, device=dev)
+    out = {
+        "ids": torch.empty((S, 1), dtype=torch.int32, device=dev),
+        "slots": torch.empty((S, 1), dtype=torch.int32, device=dev),
+        "weights": torch.empty((S, 1), dtype=torch.float32, device=dev),
+        "counts": torch.empty((E,), dtype=torch.int32, device=dev),
+        "slot_src": torch.empty((E, C), dtype=torch.int32, device=dev),
+        "prices": torch.empty((E,), dtype=torch.float64, device=dev),
+    }
+    status = torch.empty((3,), dtype=torch.int64, device=dev)
+    ws = torch.empty((hm.moe_base_gate_workspace_size(p),), dtype=torch.uint8, device=dev)
+    args = lambda: (p, None, None, None, Lbuf, out["ids"], out["slots"], out["weights"], out["counts"],
+                    out["slot_src"], out["prices"], ws, 128, status)
+    Lbuf.copy_(wl.to_device(np.random.default_rng(40).standard_normal((S, E)).astype(np.float32), "f32"))
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        hm.moe_base_gate_async(*args(), stream=s)  # warm-up outside the graph
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        hm.moe_base_gate_async(*args(), stream=torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    for rep in range(4):
+        L = np.random.default_rng(41 + rep).standard_normal((S, E)).astype(np.float32) * (1 + rep)
+        Lbuf.copy_(wl.to_device(L, "f32"))
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        st = hm.base_status(status)
+        got = {k: wl.to_host(v) for k, v in out.items()}
+        ref = run_base(L=L, E=E)
+        assert st["status"] == 0 and st["rounds"] == ref["info"]["rounds"], (rep, st, ref["info"])
+        for key in _BASE_KEYS:
+            assert_equal(got[key], ref[key], f"replay {rep} {key}")

@@ -248,7 +248,8 @@ MOE_API moe_status moe_base_gate_workspace_size(const moe_base_params* p, size_t
  * Unlike the other calls this one SYNCHRONIZES `stream`: the host enqueues the
  * auction's launches in batches (64, then 128 at a time; a launch that finds
  * the auction finished returns at once) and reads its done flag after each
- * batch.  It returns
+ * batch (moe_base_gate_async below enqueues a fixed number of launches
+ * instead and reads nothing back).  It returns
  * MOE_ERR_NOT_CONVERGED when a phase reaches max_rounds, and
  * MOE_ERR_INVALID_ARG when a score is infinite or NaN (found on the device
  * after the projection); outputs are then undefined.

@@ -456,6 +456,57 @@ __device__ __forceinline__ void base_wave_bid(const BaseArgs& a, const double* p
   bid_out = l1 - v2 + eps;
 }
 
+// The same bid with G lanes over experts (an aligned group of G lanes per
+// token, G <= 16 so that the butterflies stay in a row of the wave): every
+// lane of the group returns the same expert and bid.
+template <int G>
+__device__ __forceinline__ void base_group_bid(const BaseArgs& a, const double* pr, double eps, int t, int sub,
+                                               int& e_out, double& bid_out) {
+  static_assert(G >= 1 && G <= 16 && (G & (G - 1)) == 0, "G a power of two up to 16");
+  const float* row = a.logits + static_cast<int64_t>(t) * a.E;
+  double v1 = -INFINITY, v2 = -INFINITY, l1 = 0.0;
+  int e1 = 0x7fffffff;
+  for (int e0 = 0; e0 < a.E; e0 += 8 * G) {
+    float lv[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {  // loads issued together (clamped: past E reads expert 0, skipped)
+      const int e = e0 + q * G + sub;
+      lv[q] = row[e < a.E ? e : 0];
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int e = e0 + q * G + sub;
+      if (e >= a.E) continue;
+      const double v = static_cast<double>(lv[q]) - pr[e];
+      if (v > v1) {
+        v2 = v1;
+        v1 = v;
+        e1 = e;
+        l1 = static_cast<double>(lv[q]);
+      } else if (v > v2) {
+        v2 = v;
+      }
+    }
+  }
+#pragma unroll
+  for (int off = 1; off < G; off <<= 1) {
+    const double ov1 = xor_partner(v1, off), ov2 = xor_partner(v2, off);
+    const double ol1 = xor_partner(l1, off);
+    const int oe1 = xor_partner(e1, off);
+    if (ov1 > v1 || (ov1 == v1 && oe1 < e1)) {
+      v2 = fmax(ov2, v1);
+      v1 = ov1;
+      e1 = oe1;
+      l1 = ol1;
+    } else {
+      v2 = fmax(v2, ov1);
+    }
+  }
+  if (a.E == 1) v2 = v1;
+  e_out = e1;
+  bid_out = l1 - v2 + eps;
+}
+
 // Expert e takes the only bid for it this round, (bid, t): the holders ahead
 // of it are counted by the lanes while staged in `hvs`/`hts` (LDS of c
 // entries), then the holders behind it move up one place from there, the last
@@ -749,59 +800,47 @@ __global__ __launch_bounds__(kBaseThreads) void base_tail_kernel(BaseArgs a, int
       }
       have_bids = true;
     }
-    // bids, as in base_bid_kernel
-    if (!have_bids && tid < n) {
-      const int t = U[tid];
-      const float* row = a.logits + static_cast<int64_t>(t) * E;
-      double v1 = -INFINITY, v2 = -INFINITY;
-      int e1 = 0;
-      for (int e0 = 0; e0 < E; e0 += 32) {  // 32 loads issued together
-        float lv[32];
-#pragma unroll
-        for (int q = 0; q < 32; ++q) lv[q] = row[e0 + q < E ? e0 + q : 0];
-#pragma unroll
-        for (int q = 0; q < 32; ++q) {
-          if (e0 + q >= E) break;
-          const double v = static_cast<double>(lv[q]) - pr[e0 + q];
-          if (v > v1) {
-            v2 = v1;
-            v1 = v;
-            e1 = e0 + q;
-          } else if (v > v2) {
-            v2 = v;
-          }
+    // bids of more than 16 bidders: 16 lanes each (up to 64 bidders)
+    if (!have_bids) {
+      const int g = tid / 16;
+      if (g < n) {  // uniform in each group of 16 lanes
+        int e1;
+        double bid;
+        base_group_bid<16>(a, pr, eps, U[g], tid % 16, e1, bid);
+        if (tid % 16 == 0) {
+          bex[g] = e1;
+          bvv[g] = bid;
         }
       }
-      if (E == 1) v2 = v1;
-      bex[tid] = e1;
-      bvv[tid] = static_cast<double>(row[e1]) - v2 + eps;
     }
     if (tid == 0) nU2 = 0;
     __syncthreads();
-    // wave 0, a lane per bidder: kr = bidders of the same expert ahead of it,
-    // nbe = bidders of its expert (the others' values by readlane); the best
-    // bidder of each expert (kr == 0) leads it
-    if (w == 0) {
-      const bool live = lane < n;
-      const int e = live ? bex[lane] : -1;
-      const double v = live ? bvv[lane] : 0.0;
-      const int t = live ? U[lane] : 0;
-      const uint2 vb = __builtin_bit_cast(uint2, v);
+    // 16 lanes per bidder: kr = bidders of the same expert ahead of it, nbe =
+    // bidders of its expert; then wave 0 lists the best bidder of each expert
+    // (kr == 0), which leads it
+    {
+      const int g = tid / 16, sub = tid % 16;
       int k = 0, m = 0;
-      for (int q = 0; q < n; ++q) {
-        const int eq = __builtin_amdgcn_readlane(e, q);
-        const uint2 qb = {static_cast<unsigned>(__builtin_amdgcn_readlane(static_cast<int>(vb.x), q)),
-                          static_cast<unsigned>(__builtin_amdgcn_readlane(static_cast<int>(vb.y), q))};
-        const int tq = __builtin_amdgcn_readlane(t, q);
-        const bool same = eq == e;
-        m += same;
-        k += same && base_before(__builtin_bit_cast(double, qb), tq, v, t);
+      if (g < n) {
+        const int e = bex[g];
+        const double v = bvv[g];
+        const int t = U[g];
+        for (int j = sub; j < n; j += 16) {
+          const bool same = bex[j] == e;
+          m += same;
+          k += same && base_before(bvv[j], U[j], v, t);
+        }
       }
-      if (live) {
-        kr[lane] = k;
-        nbe[lane] = m;
+      k = group_reduce<16>(k, OpAdd());
+      m = group_reduce<16>(m, OpAdd());
+      if (g < n && sub == 0) {
+        kr[g] = k;
+        nbe[g] = m;
       }
-      const bool lead = live && k == 0;
+    }
+    __syncthreads();
+    if (w == 0) {
+      const bool lead = lane < n && kr[lane] == 0;
       const uint64_t lm = __ballot(lead);
       if (lead) ldr[popc_below(lm)] = lane;
       if (lane == 0) nL = __popcll(lm);

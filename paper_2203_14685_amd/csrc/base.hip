@@ -92,8 +92,7 @@ __global__ __launch_bounds__(kBaseRangeBlocks) void base_init_kernel(BaseArgs a)
     st.done = bad ? 1 : 0;
     a.state[0] = st;
     a.state[1] = st;
-    a.counts[0] = 0;
-    a.counts[1] = 0;
+    for (int i = 0; i < 4; ++i) a.counts[i] = 0;
   }
 }
 
@@ -118,7 +117,10 @@ __global__ __launch_bounds__(kBlock) void base_bid_kernel(BaseArgs a, int r) {
   extern __shared__ double price[];  // [E], then int ecnt[E]
   int* ecnt = reinterpret_cast<int*>(price + a.E);
   __shared__ int nblk;
-  if (blockIdx.x == 0 && threadIdx.x == 0) a.counts[(r + 1) & 1] = 0;  // for the next round
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    a.counts[(r + 1) & 1] = 0;  // for the next round
+    a.counts[2 + (r & 1)] = 0;  // slots this round's resolve step fills
+  }
   for (int e = threadIdx.x; e < a.E; e += kBlock) {
     price[e] = a.price[e];
     ecnt[e] = 0;
@@ -364,7 +366,10 @@ __global__ __launch_bounds__(kBaseThreads) void base_resolve_kernel(BaseArgs a, 
         if (r_ == c - 1) a.price[e] = v;
       }
     }
-    if (tid == 0) a.hold_n[e] = min(c, nh + nb);
+    if (tid == 0) {
+      a.hold_n[e] = min(c, nh + nb);
+      atomicAdd(&a.counts[2 + (r & 1)], min(c, nh + nb) - nh);
+    }
     return;
   }
   // few bidders: ranks in the union of holders (sorted) and bidders (unsorted) by counting
@@ -400,7 +405,10 @@ __global__ __launch_bounds__(kBaseThreads) void base_resolve_kernel(BaseArgs a, 
       if (r_ == c - 1) a.price[e] = v;
     }
   }
-  if (tid == 0) a.hold_n[e] = min(c, nh + nb);
+  if (tid == 0) {
+    a.hold_n[e] = min(c, nh + nb);
+    atomicAdd(&a.counts[2 + (r & 1)], min(c, nh + nb) - nh);
+  }
 }
 
 // ---------------------------------------------------------------- one wave per bidder
@@ -662,6 +670,11 @@ __device__ __forceinline__ void base_wave_merge(const BaseArgs& a, double* pr, i
 __global__ __launch_bounds__(kBaseThreads) void base_tail_kernel(BaseArgs a, int r) {
   BaseState* sp = a.state + ((r + 1) & 1);
   if (sp->done) return;
+  // unassigned after this round: those at its start less the slots its resolve
+  // step filled (a round that began with none changes phase and unassigns all:
+  // the scan below counts them)
+  const int un0 = a.counts[r & 1];
+  if (un0 > 0 && un0 - a.counts[2 + (r & 1)] > kBaseTail) return;  // uniform: more than the tail takes
   const double eps = sp->eps;
   int rounds_phase = sp->rounds_phase, rounds_total = sp->rounds_total, failed = 0;
   extern __shared__ double tail_lds[];

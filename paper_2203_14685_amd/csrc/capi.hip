@@ -258,7 +258,7 @@ BasePlan plan_base(const moe_base_params* p, bool own_logits) {
   b.off_bid_e = off;   off += align256(S * 4);
   b.off_bid_v = off;   off += align256(S * 8);
   b.off_bid_cnt = off; off += align256(E * 4);
-  b.off_counts = off;  off += align256(2 * 4);
+  b.off_counts = off;  off += align256(4 * 4);
   b.off_state = off;   off += align256(2 * sizeof(BaseState));
   b.off_range = off;   off += align256(3 * kBaseRangeBlocks * sizeof(float));
   b.total = off;

@@ -416,19 +416,37 @@ __global__ __launch_bounds__(kBaseThreads) void base_resolve_kernel(BaseArgs a, 
 // on ties) and the best other value by butterflies over (value, expert); max
 // is exact, so this equals the sequential scan of base_bid_kernel.  Every lane
 // returns the same expert and bid.
-__device__ __forceinline__ void base_wave_bid(const BaseArgs& a, const double* pr, double eps, int t, int lane,
-                                              int& e_out, double& bid_out) {
+// Token t's scores for experts q * 64 + lane, q < 4, loaded together (clamped:
+// a lane past E reads expert 0).
+__device__ __forceinline__ void base_row_load(const BaseArgs& a, int t, int lane, float (&lv)[4]) {
+  const float* row = a.logits + static_cast<int64_t>(t) * a.E;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int e = q * kWave + lane;
+    lv[q] = row[e < a.E ? e : 0];
+  }
+}
+
+// base_wave_bid with the scores of the first 256 experts already loaded (lv0,
+// from base_row_load).
+__device__ __forceinline__ void base_wave_bid_from(const BaseArgs& a, const double* pr, double eps, int t, int lane,
+                                                   const float (&lv0)[4], int& e_out, double& bid_out) {
   const float* row = a.logits + static_cast<int64_t>(t) * a.E;
   double v1 = -INFINITY, v2 = -INFINITY, l1 = 0.0;
   int e1 = 0x7fffffff;
-  // four experts per lane per batch, loaded together (clamped: a lane past E
-  // reads expert 0 and skips it)
+  // four experts per lane per batch, loaded together past the first 256
+  // (clamped: a lane past E reads expert 0 and skips it)
   for (int e0 = 0; e0 < a.E; e0 += 4 * kWave) {
     float lv[4];
+    if (e0 == 0) {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int e = e0 + q * kWave + lane;
-      lv[q] = row[e < a.E ? e : 0];
+      for (int q = 0; q < 4; ++q) lv[q] = lv0[q];
+    } else {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int e = e0 + q * kWave + lane;
+        lv[q] = row[e < a.E ? e : 0];
+      }
     }
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
@@ -462,6 +480,13 @@ __device__ __forceinline__ void base_wave_bid(const BaseArgs& a, const double* p
   if (a.E == 1) v2 = v1;
   e_out = e1;
   bid_out = l1 - v2 + eps;
+}
+
+__device__ __forceinline__ void base_wave_bid(const BaseArgs& a, const double* pr, double eps, int t, int lane,
+                                              int& e_out, double& bid_out) {
+  float lv[4];
+  base_row_load(a, t, lane, lv);
+  base_wave_bid_from(a, pr, eps, t, lane, lv, e_out, bid_out);
 }
 
 // The same bid with G lanes over experts (an aligned group of G lanes per
@@ -518,11 +543,12 @@ __device__ __forceinline__ void base_group_bid(const BaseArgs& a, const double* 
 // Expert e takes the only bid for it this round, (bid, t): the holders ahead
 // of it are counted by the lanes while staged in `hvs`/`hts` (LDS of c
 // entries), then the holders behind it move up one place from there, the last
-// one dropping out when the list is full.  Returns the evicted token or -1;
-// `bad` is set if the bid does not rank below c (it always does: a bid
-// exceeds its expert's price, the c-th best bid).
+// one dropping out when the list is full.  Returns the evicted token or -1
+// (and its scores in `next`, from base_row_load); `bad` is set if the bid does
+// not rank below c (it always does: a bid exceeds its expert's price, the c-th
+// best bid).
 __device__ __forceinline__ int base_wave_place(const BaseArgs& a, double* pr, int* hn, int e, double bid, int t,
-                                               int lane, double* hvs, int* hts, bool& bad) {
+                                               int lane, double* hvs, int* hts, bool& bad, float (&next)[4]) {
   const int c = a.cap;
   const int nh = hn[e];
   const int64_t base = static_cast<int64_t>(e) * c;
@@ -553,6 +579,10 @@ __device__ __forceinline__ int base_wave_place(const BaseArgs& a, double* pr, in
   }
   p = group_reduce<kWave>(p, OpAdd());
   ev = group_reduce<kWave>(ev, OpMaxI());
+  // the evictee bids next: its scores are requested now, so that their latency
+  // overlaps the holder shift and the wait for its stores (unconditional: no
+  // branch around loads)
+  base_row_load(a, ev >= 0 ? ev : t, lane, next);
   vlast = __shfl(vlast, (c - 2) & (kWave - 1), kWave);
   bad = p >= c;
   if (bad) return -1;
@@ -729,6 +759,8 @@ __global__ __launch_bounds__(kBaseThreads) void base_tail_kernel(BaseArgs a, int
       if (w == 0) {
         int t = U[0];
         int k = 0, fl = 0;
+        float lv[4];
+        base_row_load(a, t, lane, lv);
         for (;;) {
           if (rounds_phase + k >= a.max_rounds) {
             fl = 1;
@@ -736,9 +768,9 @@ __global__ __launch_bounds__(kBaseThreads) void base_tail_kernel(BaseArgs a, int
           }
           int e1;
           double bid;
-          base_wave_bid(a, pr, eps, t, lane, e1, bid);
+          base_wave_bid_from(a, pr, eps, t, lane, lv, e1, bid);
           bool bad;
-          const int evicted = base_wave_place(a, pr, hn, e1, bid, t, lane, hvs, hts, bad);
+          const int evicted = base_wave_place(a, pr, hn, e1, bid, t, lane, hvs, hts, bad, lv);
           if (bad) {  // cannot happen (see base_wave_place); stop rather than loop
             fl = 1;
             break;

@@ -246,10 +246,13 @@ MOE_API moe_status moe_base_gate_workspace_size(const moe_base_params* p, size_t
  * be NULL) receives the auction's statistics.
  *
  * Unlike the other calls this one SYNCHRONIZES `stream`: the host enqueues the
- * auction's launches in batches (64, then 128 at a time; a launch that finds
- * the auction finished returns at once) and reads its done flag after each
- * batch (moe_base_gate_async below enqueues a fixed number of launches
- * instead and reads nothing back).  It returns
+ * auction's launches a few rounds ahead of the device, which reports its
+ * progress and its end in a small pinned host buffer (one per host thread,
+ * allocated on first use and kept until the process ends; without it, the
+ * host enqueues batches of 64, then 128 rounds and reads the done flag after
+ * each); a launch that finds the auction finished returns at once.
+ * moe_base_gate_async below enqueues a fixed number of launches instead and
+ * reads nothing back.  It returns
  * MOE_ERR_NOT_CONVERGED when a phase reaches max_rounds, and
  * MOE_ERR_INVALID_ARG when a score is infinite or NaN (found on the device
  * after the projection); outputs are then undefined.

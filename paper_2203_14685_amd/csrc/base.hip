@@ -18,6 +18,8 @@
 // state[r & 1] and the resolve kernel's block 0 writes state[(r + 1) & 1], so
 // the host only enqueues rounds and checks the done flag now and then.  Rounds
 // enqueued after the auction has finished return at once.
+#include <chrono>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -245,6 +247,10 @@ __global__ __launch_bounds__(kBaseThreads) void base_resolve_kernel(BaseArgs a, 
       }
     }
     a.state[(r + 1) & 1] = nx;
+    if (a.host_flag) {  // pacing for the host (synchronous form only)
+      __hip_atomic_store(&a.host_flag->done, nx.done, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+      __hip_atomic_store(&a.host_flag->round, r, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+    }
   }
   if (st.done || fail) return;
   if (n_un == 0) {
@@ -968,10 +974,41 @@ __global__ void base_empty_status_kernel(BaseDevStatus* status) { *status = Base
 // ---------------------------------------------------------------- driver
 size_t base_resolve_lds(int cap) { return static_cast<size_t>(cap + kBaseCand) * (sizeof(double) + sizeof(int)); }
 
-hipError_t run_base_auction(const BaseArgs& a, hipStream_t st, BaseStats* stats) {
+// A pinned, device-mapped progress word per host thread (a synchronous call
+// blocks its thread, so one suffices), allocated on first use and kept until
+// the process ends; null if it cannot be had.
+BaseHostFlag* base_host_flag() {
+  thread_local BaseHostFlag* flag = nullptr;
+  thread_local bool tried = false;
+  if (!tried) {
+    tried = true;
+    void* p = nullptr;
+    if (hipHostMalloc(&p, sizeof(BaseHostFlag), hipHostMallocMapped | hipHostMallocPortable) == hipSuccess)
+      flag = static_cast<BaseHostFlag*>(p);
+    else
+      (void)hipGetLastError();  // clear the failure; pacing falls back to host reads
+  }
+  return flag;
+}
+
+hipError_t run_base_auction(const BaseArgs& a_in, hipStream_t st, BaseStats* stats) {
   hipError_t err;
   *stats = BaseStats{};
-  if (a.S == 0) return hipSuccess;
+  if (a_in.S == 0) return hipSuccess;
+  BaseArgs a = a_in;
+  BaseHostFlag* hf = base_host_flag();
+  a.host_flag = nullptr;
+  if (hf) {
+    void* dp = nullptr;
+    if (hipHostGetDevicePointer(&dp, hf, 0) == hipSuccess) {
+      a.host_flag = static_cast<BaseHostFlag*>(dp);
+      __atomic_store_n(&hf->done, 0, __ATOMIC_RELAXED);
+      __atomic_store_n(&hf->round, -1, __ATOMIC_RELEASE);
+    } else {
+      (void)hipGetLastError();
+      hf = nullptr;
+    }
+  }
   const unsigned tok_blocks = static_cast<unsigned>((a.S + kBlock - 1) / kBlock);
   const size_t bid_lds = static_cast<size_t>(a.E) * (sizeof(double) + sizeof(int));
   const size_t tail_lds = static_cast<size_t>(a.E + a.cap) * (sizeof(double) + sizeof(int));
@@ -980,29 +1017,59 @@ hipError_t run_base_auction(const BaseArgs& a, hipStream_t st, BaseStats* stats)
   base_init_kernel<<<1, kBaseRangeBlocks, 0, st>>>(a);
   base_reset_kernel<<<tok_blocks, kBlock, 0, st>>>(a);
   if ((err = hipGetLastError()) != hipSuccess) return err;
+  auto round = [&](int r) {
+    if (vec) base_bid_kernel<true><<<tok_blocks, kBlock, bid_lds, st>>>(a, r);
+    else base_bid_kernel<false><<<tok_blocks, kBlock, bid_lds, st>>>(a, r);
+    base_resolve_kernel<<<static_cast<unsigned>(a.E), kBaseThreads, base_resolve_lds(a.cap), st>>>(a, r);
+    base_tail_kernel<<<1, kBaseThreads, tail_lds, st>>>(a, r);
+  };
   // the device ends the auction within (max_rounds + 1) rounds per phase; the
   // phases are at most 2 + log_32(2^30 / 4) < 8, so a bound of 12 phases is safe
   const int64_t limit = static_cast<int64_t>(a.max_rounds + 1) * 12 + 1;
   int r = 0;
-  int batch = 64;
   BaseState host{};
-  for (;;) {
-    for (int i = 0; i < batch; ++i, ++r) {
-      if (vec) base_bid_kernel<true><<<tok_blocks, kBlock, bid_lds, st>>>(a, r);
-      else base_bid_kernel<false><<<tok_blocks, kBlock, bid_lds, st>>>(a, r);
-      base_resolve_kernel<<<static_cast<unsigned>(a.E), kBaseThreads, base_resolve_lds(a.cap), st>>>(a, r);
-      base_tail_kernel<<<1, kBaseThreads, tail_lds, st>>>(a, r);
+  if (hf) {
+    // Paced: the host keeps kAhead rounds queued beyond the last one the device
+    // has reached, and stops once the device reports the end.  A wait without
+    // progress for a long time falls back to synchronizing the stream.
+    constexpr int kAhead = 6;
+    bool ended = false;
+    for (; r < limit && !ended; ++r) {
+      round(r);
+      if ((err = hipGetLastError()) != hipSuccess) return err;
+      if (r < kAhead) continue;
+      const auto t0 = std::chrono::steady_clock::now();
+      for (int spins = 0;; ++spins) {
+        if (__atomic_load_n(&hf->done, __ATOMIC_ACQUIRE)) {
+          ended = true;
+          break;
+        }
+        if (__atomic_load_n(&hf->round, __ATOMIC_ACQUIRE) >= r - kAhead) break;
+        if ((spins & 1023) == 1023 && std::chrono::steady_clock::now() - t0 > std::chrono::seconds(20)) {
+          if ((err = hipStreamSynchronize(st)) != hipSuccess) return err;
+          break;
+        }
+      }
     }
-    if ((err = hipGetLastError()) != hipSuccess) return err;
     if ((err = hipMemcpyAsync(&host, a.state + (r & 1), sizeof(host), hipMemcpyDeviceToHost, st)) != hipSuccess)
       return err;
     if ((err = hipStreamSynchronize(st)) != hipSuccess) return err;
-    if (host.done) break;
-    if (r >= limit) {
-      host.failed = 1;
-      break;
+    if (!host.done) host.failed = 1;  // the round limit: only a failing device gets here
+  } else {
+    int batch = 64;
+    for (;;) {
+      for (int i = 0; i < batch; ++i, ++r) round(r);
+      if ((err = hipGetLastError()) != hipSuccess) return err;
+      if ((err = hipMemcpyAsync(&host, a.state + (r & 1), sizeof(host), hipMemcpyDeviceToHost, st)) != hipSuccess)
+        return err;
+      if ((err = hipStreamSynchronize(st)) != hipSuccess) return err;
+      if (host.done) break;
+      if (r >= limit) {
+        host.failed = 1;
+        break;
+      }
+      batch = 128;
     }
-    batch = 128;
   }
   stats->phases = host.phase + 1;
   stats->rounds = host.rounds_total;

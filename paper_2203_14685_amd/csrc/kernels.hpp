@@ -174,6 +174,14 @@ struct BaseArgs {
   float* weights;          // [S]
   int32_t* hist;           // [E, nb]
   double* prices_out;      // [E] or null: final prices
+  struct BaseHostFlag* host_flag;  // or null: progress written to host memory for the host's pacing
+};
+
+// Progress of the synchronous auction, written by the device to pinned host
+// memory (system scope) and polled by the host that enqueues the rounds.
+struct BaseHostFlag {
+  int32_t round;           // last round whose resolve step has started
+  int32_t done;            // the auction has ended (converged or failed)
 };
 
 struct BaseStats {

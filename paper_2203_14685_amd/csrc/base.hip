@@ -16,8 +16,9 @@
 //
 // The auction's control lives on the device: round r reads the state block
 // state[r & 1] and the resolve kernel's block 0 writes state[(r + 1) & 1], so
-// the host only enqueues rounds and checks the done flag now and then.  Rounds
-// enqueued after the auction has finished return at once.
+// the host only enqueues rounds (paced by a progress word the device writes to
+// pinned host memory, or a fixed number of them in the asynchronous form).
+// Rounds enqueued after the auction has finished return at once.
 #include <chrono>
 
 #include "common.hpp"

@@ -110,6 +110,59 @@ __global__ __launch_bounds__(kBlock) void base_reset_kernel(BaseArgs a) {
   }
 }
 
+// The bid of token t with G lanes over experts (an aligned group of G lanes
+// per token, G <= 16 so that the butterflies stay in a row of the wave): the
+// best value (lower expert on ties) and the best other value by butterflies
+// over (value, expert); max is exact, so this equals the sequential scan of
+// base_bid_kernel.  Every lane of the group returns the same expert and bid.
+template <int G>
+__device__ __forceinline__ void base_group_bid(const BaseArgs& a, const double* pr, double eps, int t, int sub,
+                                               int& e_out, double& bid_out) {
+  static_assert(G >= 1 && G <= 16 && (G & (G - 1)) == 0, "G a power of two up to 16");
+  const float* row = a.logits + static_cast<int64_t>(t) * a.E;
+  double v1 = -INFINITY, v2 = -INFINITY, l1 = 0.0;
+  int e1 = 0x7fffffff;
+  for (int e0 = 0; e0 < a.E; e0 += 8 * G) {
+    float lv[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {  // loads issued together (clamped: past E reads expert 0, skipped)
+      const int e = e0 + q * G + sub;
+      lv[q] = row[e < a.E ? e : 0];
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int e = e0 + q * G + sub;
+      if (e >= a.E) continue;
+      const double v = static_cast<double>(lv[q]) - pr[e];
+      if (v > v1) {
+        v2 = v1;
+        v1 = v;
+        e1 = e;
+        l1 = static_cast<double>(lv[q]);
+      } else if (v > v2) {
+        v2 = v;
+      }
+    }
+  }
+#pragma unroll
+  for (int off = 1; off < G; off <<= 1) {
+    const double ov1 = xor_partner(v1, off), ov2 = xor_partner(v2, off);
+    const double ol1 = xor_partner(l1, off);
+    const int oe1 = xor_partner(e1, off);
+    if (ov1 > v1 || (ov1 == v1 && oe1 < e1)) {
+      v2 = fmax(ov2, v1);
+      v1 = ov1;
+      e1 = oe1;
+      l1 = ol1;
+    } else {
+      v2 = fmax(v2, ov1);
+    }
+  }
+  if (a.E == 1) v2 = v1;
+  e_out = e1;
+  bid_out = l1 - v2 + eps;
+}
+
 // ---------------------------------------------------------------- bids
 // One thread per token.  counts[r & 1] receives the number of tokens unassigned
 // at the round's start, bid_cnt[e] the bidders of expert e.
@@ -128,12 +181,34 @@ __global__ __launch_bounds__(kBlock) void base_bid_kernel(BaseArgs a, int r) {
     price[e] = a.price[e];
     ecnt[e] = 0;
   }
-  if (threadIdx.x == 0) nblk = 0;
+  __shared__ int lst[16], nlst;
+  if (threadIdx.x == 0) {
+    nblk = 0;
+    nlst = 0;
+  }
   const int64_t s = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
   const bool bidder = s < a.S && a.assign[s] < 0;
   if (s < a.S && !bidder) a.bid_e[s] = -1;
-  if (__syncthreads_or(bidder) == 0) return;  // no bidder in this block
-  if (bidder) {
+  const int nbb = __syncthreads_count(bidder);
+  if (nbb == 0) return;  // no bidder in this block
+  if (nbb <= 16) {
+    // few bidders (the later rounds of a phase): 16 lanes over the experts each
+    if (bidder) lst[atomicAdd(&nlst, 1)] = threadIdx.x;
+    __syncthreads();
+    const int g = threadIdx.x / 16;
+    if (g < nbb) {  // uniform in each group of 16 lanes
+      const int64_t t = static_cast<int64_t>(blockIdx.x) * kBlock + lst[g];
+      int e1;
+      double bid;
+      base_group_bid<16>(a, price, st.eps, static_cast<int>(t), threadIdx.x % 16, e1, bid);
+      if (threadIdx.x % 16 == 0) {
+        a.bid_e[t] = e1;
+        a.bid_v[t] = bid;
+        atomicAdd(&ecnt[e1], 1);
+        atomicAdd(&nblk, 1);
+      }
+    }
+  } else if (bidder) {
     const float* row = a.logits + s * a.E;
     double v1 = -INFINITY, v2 = -INFINITY;
     int e1 = 0;
@@ -494,57 +569,6 @@ __device__ __forceinline__ void base_wave_bid(const BaseArgs& a, const double* p
   float lv[4];
   base_row_load(a, t, lane, lv);
   base_wave_bid_from(a, pr, eps, t, lane, lv, e_out, bid_out);
-}
-
-// The same bid with G lanes over experts (an aligned group of G lanes per
-// token, G <= 16 so that the butterflies stay in a row of the wave): every
-// lane of the group returns the same expert and bid.
-template <int G>
-__device__ __forceinline__ void base_group_bid(const BaseArgs& a, const double* pr, double eps, int t, int sub,
-                                               int& e_out, double& bid_out) {
-  static_assert(G >= 1 && G <= 16 && (G & (G - 1)) == 0, "G a power of two up to 16");
-  const float* row = a.logits + static_cast<int64_t>(t) * a.E;
-  double v1 = -INFINITY, v2 = -INFINITY, l1 = 0.0;
-  int e1 = 0x7fffffff;
-  for (int e0 = 0; e0 < a.E; e0 += 8 * G) {
-    float lv[8];
-#pragma unroll
-    for (int q = 0; q < 8; ++q) {  // loads issued together (clamped: past E reads expert 0, skipped)
-      const int e = e0 + q * G + sub;
-      lv[q] = row[e < a.E ? e : 0];
-    }
-#pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const int e = e0 + q * G + sub;
-      if (e >= a.E) continue;
-      const double v = static_cast<double>(lv[q]) - pr[e];
-      if (v > v1) {
-        v2 = v1;
-        v1 = v;
-        e1 = e;
-        l1 = static_cast<double>(lv[q]);
-      } else if (v > v2) {
-        v2 = v;
-      }
-    }
-  }
-#pragma unroll
-  for (int off = 1; off < G; off <<= 1) {
-    const double ov1 = xor_partner(v1, off), ov2 = xor_partner(v2, off);
-    const double ol1 = xor_partner(l1, off);
-    const int oe1 = xor_partner(e1, off);
-    if (ov1 > v1 || (ov1 == v1 && oe1 < e1)) {
-      v2 = fmax(ov2, v1);
-      v1 = ov1;
-      e1 = oe1;
-      l1 = ol1;
-    } else {
-      v2 = fmax(v2, ov1);
-    }
-  }
-  if (a.E == 1) v2 = v1;
-  e_out = e1;
-  bid_out = l1 - v2 + eps;
 }
 
 // Expert e takes the only bid for it this round, (bid, t): the holders ahead

@@ -181,11 +181,13 @@ __global__ __launch_bounds__(kBlock) void base_bid_kernel(BaseArgs a, int r) {
     price[e] = a.price[e];
     ecnt[e] = 0;
   }
-  __shared__ int lst[16], nlst;
+  __shared__ int lst[16], nlst, boff;
   if (threadIdx.x == 0) {
     nblk = 0;
     nlst = 0;
   }
+  int myrank = -1;  // this thread's bidder's place in the block's share of the round's list
+  int mytok = 0;
   const int64_t s = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
   const bool bidder = s < a.S && a.assign[s] < 0;
   if (s < a.S && !bidder) a.bid_e[s] = -1;
@@ -205,7 +207,8 @@ __global__ __launch_bounds__(kBlock) void base_bid_kernel(BaseArgs a, int r) {
         a.bid_e[t] = e1;
         a.bid_v[t] = bid;
         atomicAdd(&ecnt[e1], 1);
-        atomicAdd(&nblk, 1);
+        myrank = atomicAdd(&nblk, 1);
+        mytok = static_cast<int>(t);
       }
     }
   } else if (bidder) {
@@ -245,12 +248,16 @@ __global__ __launch_bounds__(kBlock) void base_bid_kernel(BaseArgs a, int r) {
     a.bid_e[s] = e1;
     a.bid_v[s] = static_cast<double>(row[e1]) - v2 + st.eps;
     atomicAdd(&ecnt[e1], 1);
-    atomicAdd(&nblk, 1);
+    myrank = atomicAdd(&nblk, 1);
+    mytok = static_cast<int>(s);
   }
   __syncthreads();
   for (int e = threadIdx.x; e < a.E; e += kBlock)
     if (ecnt[e] > 0) atomicAdd(&a.bid_cnt[e], ecnt[e]);
-  if (threadIdx.x == 0) atomicAdd(&a.counts[r & 1], nblk);
+  // the block's places in the round's bidder list
+  if (threadIdx.x == 0) boff = atomicAdd(&a.counts[r & 1], nblk);
+  __syncthreads();
+  if (myrank >= 0) a.blist[boff + myrank] = mytok;
 }
 
 // ---------------------------------------------------------------- resolve
@@ -358,8 +365,33 @@ __global__ __launch_bounds__(kBaseThreads) void base_resolve_kernel(BaseArgs a, 
     ht[i] = a.hold_t[base + i];
   }
   // bidders in token order: per pass kBaseIters tiles of kBaseThreads tokens;
-  // a ballot mask per (tile, wave), an exclusive scan of their counts
+  // a ballot mask per (tile, wave), an exclusive scan of their counts.  When
+  // the expert takes all its bidders (at most kBaseCand) and the round has few,
+  // they are found in the round's bidder list instead (in any order: the ranks
+  // below use the total order alone, so the set decides the outcome).
   int have = 0;
+  if (nbid <= kBaseCand && static_cast<int64_t>(n_un) * 8 <= a.S) {
+    if (tid == 0) pass_total = 0;
+    __syncthreads();
+    for (int i0 = 0; i0 < n_un; i0 += 4 * kBaseThreads) {
+      int t[4], be[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {  // unconditional loads (clamped), issued together
+        const int i = i0 + q * kBaseThreads + tid;
+        t[q] = a.blist[i < n_un ? i : 0];
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) be[q] = a.bid_e[t[q]];
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (i0 + q * kBaseThreads + tid < n_un && be[q] == e) {
+          const int pos = atomicAdd(&pass_total, 1);  // < nbid <= kBaseCand
+          if (pos < kBaseCand) bt[pos] = t[q];
+        }
+    }
+    __syncthreads();
+    have = min(pass_total, kBaseCand);  // == nbid
+  } else
   for (int64_t p0 = 0; p0 < a.S && have < kBaseCand; p0 += static_cast<int64_t>(kBaseIters) * kBaseThreads) {
     int be[kBaseIters];
 #pragma unroll

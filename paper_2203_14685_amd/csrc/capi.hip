@@ -241,7 +241,7 @@ moe_status check_base_params(const moe_base_params* p) {
 // counts int32 [2]; the auction state [2]; range partials fp32 [3, 256].
 struct BasePlan {
   size_t off_hist, off_logits, off_price, off_hold_v, off_hold_t, off_hold_n, off_assign, off_bid_e, off_bid_v,
-      off_bid_cnt, off_counts, off_state, off_range, total;
+      off_bid_cnt, off_blist, off_counts, off_state, off_range, total;
 };
 
 BasePlan plan_base(const moe_base_params* p, bool own_logits) {
@@ -258,6 +258,7 @@ BasePlan plan_base(const moe_base_params* p, bool own_logits) {
   b.off_bid_e = off;   off += align256(S * 4);
   b.off_bid_v = off;   off += align256(S * 8);
   b.off_bid_cnt = off; off += align256(E * 4);
+  b.off_blist = off;   off += align256(S * 4);
   b.off_counts = off;  off += align256(4 * 4);
   b.off_state = off;   off += align256(2 * sizeof(BaseState));
   b.off_range = off;   off += align256(3 * kBaseRangeBlocks * sizeof(float));
@@ -711,6 +712,7 @@ moe_status base_gate_run(const char* who, const moe_base_params* p, const void* 
   a.bid_e = reinterpret_cast<int32_t*>(ws + b.off_bid_e);
   a.bid_v = reinterpret_cast<double*>(ws + b.off_bid_v);
   a.bid_cnt = reinterpret_cast<int32_t*>(ws + b.off_bid_cnt);
+  a.blist = reinterpret_cast<int32_t*>(ws + b.off_blist);
   a.counts = reinterpret_cast<int32_t*>(ws + b.off_counts);
   a.state = reinterpret_cast<BaseState*>(ws + b.off_state);
   a.range_part = reinterpret_cast<float*>(ws + b.off_range);

@@ -166,6 +166,7 @@ struct BaseArgs {
   int32_t* bid_e;          // [S] expert bid for this round, -1 = none
   double* bid_v;           // [S]
   int32_t* bid_cnt;        // [E] bidders of each expert this round
+  int32_t* blist;          // [S] this round's bidders, in any order (counts[r & 1] of them)
   int32_t* counts;         // [4] unassigned tokens at the start of a round, by round parity;
                            //     then slots its resolve step filled (kept bidders less evicted holders)
   BaseState* state;        // [2]

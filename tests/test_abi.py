@@ -289,7 +289,8 @@ def _base_ws(params):
 def _base_ws_formula(S, E, logits_in):
     nb = (S + 63) // 64
     return (_a256(nb * E * 4) + (0 if logits_in else _a256(S * E * 4)) + _a256(E * 8) + _a256(S * 8)
-            + _a256(S * 4) + _a256(E * 4) + 2 * _a256(S * 4) + _a256(S * 8) + _a256(E * 4) + 256 + 256 + 3072)
+            + _a256(S * 4) + _a256(E * 4) + 2 * _a256(S * 4) + _a256(S * 8) + _a256(E * 4) + _a256(S * 4)
+            + 256 + 256 + 3072)
 
 
 def test_base_struct_and_workspace(lib):

@@ -250,7 +250,8 @@ MOE_API moe_status moe_base_gate_workspace_size(const moe_base_params* p, size_t
  * progress and its end in a small pinned host buffer (one per host thread,
  * allocated on first use and kept until the process ends; without it, the
  * host enqueues batches of 64, then 128 rounds and reads the done flag after
- * each); a launch that finds the auction finished returns at once.
+ * each, as it also does when the environment sets HETUMOE_BASE_BATCHES=1); a
+ * launch that finds the auction finished returns at once.
  * moe_base_gate_async below enqueues a fixed number of launches instead and
  * reads nothing back.  It returns
  * MOE_ERR_NOT_CONVERGED when a phase reaches max_rounds, and

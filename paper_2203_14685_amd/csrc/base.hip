@@ -20,6 +20,7 @@
 // pinned host memory, or a fixed number of them in the asynchronous form).
 // Rounds enqueued after the auction has finished return at once.
 #include <chrono>
+#include <cstdlib>
 
 #include "common.hpp"
 #include "kernels.hpp"
@@ -1053,7 +1054,10 @@ hipError_t run_base_auction(const BaseArgs& a_in, hipStream_t st, BaseStats* sta
   *stats = BaseStats{};
   if (a_in.S == 0) return hipSuccess;
   BaseArgs a = a_in;
-  BaseHostFlag* hf = base_host_flag();
+  // HETUMOE_BASE_BATCHES=1 selects the batches (the path taken without pinned
+  // memory), so that tests can compare the two
+  const char* batches = getenv("HETUMOE_BASE_BATCHES");
+  BaseHostFlag* hf = (batches && batches[0] == '1') ? nullptr : base_host_flag();
   a.host_flag = nullptr;
   if (hf) {
     void* dp = nullptr;

@@ -404,3 +404,19 @@ def test_base_async_graph_replays():
         assert st["status"] == 0 and st["rounds"] == ref["info"]["rounds"], (rep, st, ref["info"])
         for key in _BASE_KEYS:
             assert_equal(got[key], ref[key], f"replay {rep} {key}")
+
+
+def test_base_batches_equal_paced(monkeypatch):
+    """The synchronous call's two ways of enqueueing rounds (paced by the
+    device's progress word, and the batches it falls back to without pinned
+    memory) give bitwise the same outputs and statistics."""
+    announce("base paced vs batches")
+    S, E = 4096, 64
+    L = np.random.default_rng(31).standard_normal((S, E)).astype(np.float32)
+    L[:, :8] += np.float32(0.5)
+    paced = run_base(L=L, E=E)
+    monkeypatch.setenv("HETUMOE_BASE_BATCHES", "1")
+    batched = run_base(L=L, E=E)
+    assert paced["info"] == batched["info"]
+    for key in _BASE_KEYS:
+        assert_equal(batched[key], paced[key], f"batches {key}")

@@ -293,7 +293,8 @@ typedef struct {
  * the rounds with few bidders in one workgroup; a round enqueued after the
  * auction has ended returns at once, in a few microseconds).  Rounds that
  * suffice are workload-dependent: moe_base_gate's info->rounds bounds them
- * from above, and the synchronous call's first batch is 64.  The outcome is
+ * from above (the workloads of 32768 tokens over 64 experts end within 64).  The
+ * outcome is
  * written to `status` (device memory, required) by the call's last auction
  * kernel; no host read, memset or allocation is made.
  *

@@ -765,10 +765,11 @@ __global__ __launch_bounds__(kBaseThreads) void base_tail_kernel(BaseArgs a, int
   BaseState* sp = a.state + ((r + 1) & 1);
   if (sp->done) return;
   // unassigned after this round: those at its start less the slots its resolve
-  // step filled (a round that began with none changes phase and unassigns all:
-  // the scan below counts them)
+  // step filled; a round that began with none (and did not end the auction)
+  // changed phase and unassigned all S
   const int un0 = a.counts[r & 1];
-  if (un0 > 0 && un0 - a.counts[2 + (r & 1)] > kBaseTail) return;  // uniform: more than the tail takes
+  const int64_t left = un0 > 0 ? un0 - a.counts[2 + (r & 1)] : static_cast<int64_t>(a.S);
+  if (left > kBaseTail) return;  // uniform: more than the tail takes
   const double eps = sp->eps;
   int rounds_phase = sp->rounds_phase, rounds_total = sp->rounds_total, failed = 0;
   extern __shared__ double tail_lds[];

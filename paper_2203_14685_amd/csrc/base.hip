@@ -751,6 +751,19 @@ __device__ __forceinline__ void base_wave_merge(const BaseArgs& a, double* pr, i
   if (lane == 0) hn[e] = min(c, nh + nbid);
 }
 
+// The tail's unassigned lists: this round's and the next (filled by the
+// merges) trade places; every thread swaps its own pointers after the barrier
+// that completes the next list, and the count of the list that becomes the next
+// one is cleared before its first append in the following round.
+__device__ __forceinline__ void swap_lists(int*& U, int*& U2, int*& nU, int*& nU2) {
+  int* t = U;
+  U = U2;
+  U2 = t;
+  int* c = nU;
+  nU = nU2;
+  nU2 = c;
+}
+
 // ---------------------------------------------------------------- tail
 // Most rounds of a phase have a handful of bidders.  Once at most kBaseTail
 // tokens are unassigned after a round, one workgroup runs the following rounds
@@ -778,12 +791,16 @@ __global__ __launch_bounds__(kBaseThreads) void base_tail_kernel(BaseArgs a, int
   double* hvs = pr + E;                               // one expert's holder bids [c] (one-bidder rounds)
   int* hn = reinterpret_cast<int*>(hvs + c);          // holder counts [E]
   int* hts = hn + E;                                  // the holders' tokens [c]
-  __shared__ int U[kBaseTail], U2[kBaseTail];
+  __shared__ int Ubuf[2][kBaseTail];  // unassigned tokens of this round and the next, swapped
   __shared__ int bex[kBaseTail], kr[kBaseTail], nbe[kBaseTail], ldr[kBaseTail];
   __shared__ double bvv[kBaseTail];
-  __shared__ int nU, nU2, nL, fast_rounds, fast_fail;
+  __shared__ int nUbuf[2], nL, fast_rounds, fast_fail;
   const int tid = threadIdx.x, lane = lane_id(), w = tid / kWave;
-  if (tid == 0) nU = 0;
+  int* U = Ubuf[0];
+  int* U2 = Ubuf[1];
+  int* nU = &nUbuf[0];
+  int* nU2 = &nUbuf[1];
+  if (tid == 0) *nU = 0;
   __syncthreads();
   // unassigned tokens (any order)
   for (int64_t s0 = 0; s0 < a.S; s0 += 8 * kBaseThreads) {
@@ -796,19 +813,19 @@ __global__ __launch_bounds__(kBaseThreads) void base_tail_kernel(BaseArgs a, int
 #pragma unroll
     for (int q = 0; q < 8; ++q)
       if (v[q] < 0 && s0 + q * kBaseThreads + tid < a.S) {
-        const int p = atomicAdd(&nU, 1);
+        const int p = atomicAdd(nU, 1);
         if (p < kBaseTail) U[p] = static_cast<int>(s0 + q * kBaseThreads + tid);
       }
   }
   __syncthreads();
-  if (nU == 0 || nU > kBaseTail) return;  // uniform
+  if (*nU == 0 || *nU > kBaseTail) return;  // uniform
   for (int e = tid; e < E; e += kBaseThreads) {
     pr[e] = a.price[e];
     hn[e] = a.hold_n[e];
   }
   __syncthreads();
   for (;;) {
-    const int n = nU;  // uniform (read after a barrier)
+    const int n = *nU;  // uniform (read after a barrier)
     if (n == 0 || n > kBaseTail) break;
     if (rounds_phase >= a.max_rounds) {
       failed = 1;
@@ -853,7 +870,7 @@ __global__ __launch_bounds__(kBaseThreads) void base_tail_kernel(BaseArgs a, int
         }
         if (lane == 0) {
           U[0] = t;
-          nU = t >= 0 ? 1 : 0;
+          *nU = t >= 0 ? 1 : 0;
           fast_rounds = k;
           fast_fail = fl;
         }
@@ -883,7 +900,7 @@ __global__ __launch_bounds__(kBaseThreads) void base_tail_kernel(BaseArgs a, int
         }
       }
       if (tid == 0) {
-        nU2 = 0;
+        *nU2 = 0;
         fast_fail = 0;
       }
       __syncthreads();
@@ -898,14 +915,11 @@ __global__ __launch_bounds__(kBaseThreads) void base_tail_kernel(BaseArgs a, int
         distinct = __ballot(clash) == 0;
       }
       if (distinct) {  // uniform: every wave read the same bids
-        if (w < n) base_wave_merge(a, pr, hn, bex[w], 1ull << w, 1, n, bvv, U, nullptr, lane, U2, &nU2);
-        __syncthreads();
-        const int n2 = nU2;
-        if (tid < min(n2, kBaseTail)) U[tid] = U2[tid];
-        if (tid == 0) nU = n2;
+        if (w < n) base_wave_merge(a, pr, hn, bex[w], 1ull << w, 1, n, bvv, U, nullptr, lane, U2, nU2);
+        __syncthreads();  // the next list and its count are complete
+        swap_lists(U, U2, nU, nU2);
         rounds_phase += 1;
         rounds_total += 1;
-        __syncthreads();
         continue;
       }
       have_bids = true;
@@ -923,7 +937,7 @@ __global__ __launch_bounds__(kBaseThreads) void base_tail_kernel(BaseArgs a, int
         }
       }
     }
-    if (tid == 0) nU2 = 0;
+    if (tid == 0) *nU2 = 0;
     __syncthreads();
     // 16 lanes per bidder: kr = bidders of the same expert ahead of it, nbe =
     // bidders of its expert; then wave 0 lists the best bidder of each expert
@@ -965,15 +979,12 @@ __global__ __launch_bounds__(kBaseThreads) void base_tail_kernel(BaseArgs a, int
     for (int li = w; li < nL; li += kBaseWaves) {
       const int e = bex[ldr[li]];
       const uint64_t bm = __ballot(lane < n && bex[lane] == e);
-      base_wave_merge(a, pr, hn, e, bm, nbe[ldr[li]], n, bvv, U, kr, lane, U2, &nU2);
+      base_wave_merge(a, pr, hn, e, bm, nbe[ldr[li]], n, bvv, U, kr, lane, U2, nU2);
     }
-    __syncthreads();
-    const int n2 = nU2;
-    if (tid < min(n2, kBaseTail)) U[tid] = U2[tid];
-    if (tid == 0) nU = n2;
+    __syncthreads();  // the next list and its count are complete
+    swap_lists(U, U2, nU, nU2);
     rounds_phase += 1;
     rounds_total += 1;
-    __syncthreads();
   }
   for (int e = tid; e < E; e += kBaseThreads) {
     a.price[e] = pr[e];

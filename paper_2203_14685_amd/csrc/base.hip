@@ -776,12 +776,14 @@ __device__ __forceinline__ void swap_lists(int*& U, int*& U2, int*& nU, int*& nU
 // ranking uses a total order.
 __global__ __launch_bounds__(kBaseThreads) void base_tail_kernel(BaseArgs a, int r) {
   BaseState* sp = a.state + ((r + 1) & 1);
-  if (sp->done) return;
   // unassigned after this round: those at its start less the slots its resolve
   // step filled; a round that began with none (and did not end the auction)
-  // changed phase and unassigned all S
-  const int un0 = a.counts[r & 1];
-  const int64_t left = un0 > 0 ? un0 - a.counts[2 + (r & 1)] : static_cast<int64_t>(a.S);
+  // changed phase and unassigned all S.  The three words are read together,
+  // before the first decision, so that a launch that has nothing to do waits
+  // for one memory round trip.
+  const int done = sp->done, un0 = a.counts[r & 1], filled = a.counts[2 + (r & 1)];
+  if (done) return;
+  const int64_t left = un0 > 0 ? un0 - filled : static_cast<int64_t>(a.S);
   if (left > kBaseTail) return;  // uniform: more than the tail takes
   const double eps = sp->eps;
   int rounds_phase = sp->rounds_phase, rounds_total = sp->rounds_total, failed = 0;

@@ -169,6 +169,11 @@ __device__ __forceinline__ void base_group_bid(const BaseArgs& a, const double* 
 // at the round's start, bid_cnt[e] the bidders of expert e.
 template <bool VEC>
 __global__ __launch_bounds__(kBlock) void base_bid_kernel(BaseArgs a, int r) {
+  // the token's assignment and the first kBlock prices are read with the
+  // state: a launch waits for one memory round trip before its first decision
+  const int64_t s = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+  const int asg = a.assign[s < a.S ? s : 0];
+  const double p0 = a.price[threadIdx.x < a.E ? threadIdx.x : 0];
   const BaseState st = a.state[r & 1];
   if (st.done) return;
   extern __shared__ double price[];  // [E], then int ecnt[E]
@@ -179,7 +184,7 @@ __global__ __launch_bounds__(kBlock) void base_bid_kernel(BaseArgs a, int r) {
     a.counts[2 + (r & 1)] = 0;  // slots this round's resolve step fills
   }
   for (int e = threadIdx.x; e < a.E; e += kBlock) {
-    price[e] = a.price[e];
+    price[e] = e < kBlock ? p0 : a.price[e];
     ecnt[e] = 0;
   }
   __shared__ int lst[16], nlst, boff;
@@ -189,8 +194,7 @@ __global__ __launch_bounds__(kBlock) void base_bid_kernel(BaseArgs a, int r) {
   }
   int myrank = -1;  // this thread's bidder's place in the block's share of the round's list
   int mytok = 0;
-  const int64_t s = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
-  const bool bidder = s < a.S && a.assign[s] < 0;
+  const bool bidder = s < a.S && asg < 0;
   if (s < a.S && !bidder) a.bid_e[s] = -1;
   const int nbb = __syncthreads_count(bidder);
   if (nbb == 0) return;  // no bidder in this block
@@ -306,10 +310,12 @@ __device__ __forceinline__ int base_rank_in(const double* v, const int* t, int n
 // ranks them and its holders in the order (bid desc, token asc) by counting;
 // ranks below c are kept, holders ranked c or beyond are evicted.
 __global__ __launch_bounds__(kBaseThreads) void base_resolve_kernel(BaseArgs a, int r) {
-  const BaseState st = a.state[r & 1];
   const int e = blockIdx.x;
   const int tid = threadIdx.x;
-  const int n_un = st.done ? 0 : a.counts[r & 1];
+  // every word the first decisions need, read together (one round trip)
+  const int cnt = a.counts[r & 1], nbid = a.bid_cnt[e], nh = a.hold_n[e];
+  const BaseState st = a.state[r & 1];
+  const int n_un = st.done ? 0 : cnt;
   const bool fail = !st.done && n_un > 0 && st.rounds_phase >= a.max_rounds;
   if (e == 0 && tid == 0) {
     BaseState nx = st;
@@ -346,7 +352,6 @@ __global__ __launch_bounds__(kBaseThreads) void base_resolve_kernel(BaseArgs a, 
     }
     return;
   }
-  const int nbid = a.bid_cnt[e];
   if (nbid == 0) return;
 
   extern __shared__ double base_lds[];
@@ -360,7 +365,6 @@ __global__ __launch_bounds__(kBaseThreads) void base_resolve_kernel(BaseArgs a, 
   __shared__ int pass_total;
   const int lane = lane_id(), w = tid / kWave;
   const int64_t base = static_cast<int64_t>(e) * c;
-  const int nh = a.hold_n[e];
   for (int i = tid; i < nh; i += kBaseThreads) {
     hv[i] = a.hold_v[base + i];
     ht[i] = a.hold_t[base + i];
